@@ -1,0 +1,350 @@
+"""Plain fp64 CPU oracle of the Spectral-LSH hot path.
+
+TEST INFRASTRUCTURE (CPU oracle); see oracle/__init__.py for who may import it.
+
+Each function follows one step of the paper (arXiv 2607.19368, "Spectral-LSH:
+Sub-Quadratic Prompt Compression via Krylov-Projected Locality-Sensitive
+Hashing") in its order and notation.  Notation used here: N tokens, embedding
+width D (the paper's d), m random features (the paper's D), n_it Lanczos steps
+(the paper's r in Algorithm 2), r kept Ritz vectors (the paper's k), b hash bits.
+Library primitives serve as steps (BLAS matmul, LAPACK eigh); there is no
+blocking, fusion or reordering beyond what the paper states.
+
+Readings of the paper that this file takes (where it is silent or ambiguous):
+  R1 (Eq. 2-3) The random-feature map is sqrt(2/m) cos(x W + psi) times the
+     per-token factor s(x) = exp(||x||^2 / (2 sqrt(D))). Without s the map
+     estimates the Gaussian kernel exp(-||x-y||^2 / (2 sqrt(D))); with it the
+     estimate is unbiased for the unnormalised kernel exp(x.y / sqrt(D)) that
+     Eq. 2 names, since that kernel equals s(x) s(y) times the Gaussian one.
+     kernel="gauss" gives the map exactly as Eq. 3 prints it.
+  R2 The feature map consumes X rounded to bf16; the merge uses X as given.
+  R3 (Algorithm 2) "Full re-orthogonalization" is classical Gram-Schmidt applied
+     twice against q_1..q_j after the three-term subtraction; alpha_j is taken
+     before the subtraction and beta_j after the re-orthogonalization; the
+     corrections are not folded into T.
+  R4 (Algorithm 2) Breakdown: stop when beta_j <= 1e-10 * max_{i<=j} |alpha_i|.
+  R5 (Algorithm 1) Ritz columns are the top-r eigenvectors of T in ascending
+     eigenvalue order (the slice V[:, n-r:n]); each eigenvector's sign makes its
+     first nonzero component positive; Z is not rescaled.  If Lanczos stopped
+     after n_eff < r steps, Z gets r - n_eff leading zero columns (and the
+     corresponding Ritz values are reported as 0).
+  R6 (Eq. 5) Hash bit l is 1 iff r_l . z_i > 0 (a tie gives 0); the code is
+     sum_l bit_l 2^l.
+  R7 (Eq. 7, section 3.4, section 3.6) Positions are 0-based token indices; a
+     bucket's position is the max of its members' positions; macro-tokens are
+     ordered by that position; a bucket whose mean is the zero vector yields the
+     zero vector.
+  R8 (Eq. 8) The centroid is the normalised sum of the raw rows; zero rows
+     contribute 0 to the score.
+  R9 (section 3.6) tau(rho) is piecewise linear in log2(rho) through (2, 0.70),
+     (8, 0.60), (16, 0.55), 0.70 below 2; rho >= 16 routes every window to the
+     spectral path.
+  R10 (section 3.5) Chunk size k = max(1, round(rho)) with round-half-to-even;
+     the last chunk may be partial; chunks are renormalised like Eq. 7 and take
+     the max position of their members.
+"""
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+
+# --------------------------------------------------------------------------
+# bf16 rounding of the feature-map input (reading R2)
+# --------------------------------------------------------------------------
+def bf16_round(a):
+    """Round to bfloat16 (nearest-even) after rounding to float32; fp64 out."""
+    f = np.ascontiguousarray(a, dtype=np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    r = ((u + np.uint64(0x7FFF) + ((u >> np.uint64(16)) & np.uint64(1))) >> np.uint64(16)) << np.uint64(16)
+    return r.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+# --------------------------------------------------------------------------
+# Step 1: random-feature map (section 3.2, Eq. 2-3; Algorithm 1 first step)
+# --------------------------------------------------------------------------
+def unnormalised_kernel(X, Y=None):
+    """kappa(x, y) = exp(x.y / sqrt(D)) (section 3.2), explicit, for checks."""
+    Y = X if Y is None else Y
+    D = X.shape[1]
+    return np.exp((X @ Y.T) / math.sqrt(D))
+
+
+def feature_map(X, W, psi, kernel="softmax"):
+    """Phi[i, j] = s_i sqrt(2/m) cos(x_i . W[:, j] + psi_j)   (Eq. 3, reading R1).
+
+    X: N x D (any float type; rounded to bf16 first, reading R2).
+    W: D x m, psi: m.  Returns N x m fp64.
+    """
+    Xh = bf16_round(X)
+    D = Xh.shape[1]
+    m = W.shape[1]
+    Phi = math.sqrt(2.0 / m) * np.cos(Xh @ W + psi[None, :])
+    if kernel == "softmax":
+        s = np.exp(np.sum(Xh * Xh, axis=1) / (2.0 * math.sqrt(D)))
+        Phi *= s[:, None]
+    elif kernel != "gauss":
+        raise ValueError(kernel)
+    return Phi
+
+
+# --------------------------------------------------------------------------
+# Step 2: implicit Lanczos (Eq. 4, Algorithm 2)
+# --------------------------------------------------------------------------
+@dataclass
+class LanczosResult:
+    alpha: np.ndarray          # n_eff diagonal entries of T
+    beta: np.ndarray           # n_eff entries: beta[:n_eff-1] off-diagonal, beta[-1] the residual norm
+    Q: np.ndarray              # N x n_eff orthonormal basis
+    q_next: np.ndarray         # q_{n_eff+1} (zeros if the run broke down)
+    n_eff: int
+    broke_down: bool
+
+
+def implicit_matvec(Phi, v):
+    """A v ~ Phi (Phi^T v), never forming the N x N kernel (Eq. 4)."""
+    return Phi @ (Phi.T @ v)
+
+
+def lanczos(Phi, q1, n_it, breakdown_rel=1e-10, matvec=None):
+    """Algorithm 2 with full re-orthogonalization (readings R3, R4)."""
+    mv = (lambda v: implicit_matvec(Phi, v)) if matvec is None else matvec
+    N = q1.shape[0]
+    Q = np.zeros((N, n_it + 1))
+    alpha = np.zeros(n_it)
+    beta = np.zeros(n_it)
+    Q[:, 0] = q1 / np.linalg.norm(q1)
+    amax = 0.0
+    n_eff = n_it
+    broke = False
+    for j in range(n_it):
+        z = mv(Q[:, j])
+        alpha[j] = Q[:, j] @ z
+        z = z - alpha[j] * Q[:, j]
+        if j > 0:
+            z = z - beta[j - 1] * Q[:, j - 1]
+        for _ in range(2):                       # full re-orthogonalization
+            h = Q[:, :j + 1].T @ z
+            z = z - Q[:, :j + 1] @ h
+        beta[j] = np.linalg.norm(z)
+        amax = max(amax, abs(alpha[j]))
+        if beta[j] <= breakdown_rel * amax:
+            n_eff = j + 1
+            broke = True
+            break
+        Q[:, j + 1] = z / beta[j]
+    q_next = np.zeros(N) if broke else Q[:, n_eff].copy()
+    return LanczosResult(alpha[:n_eff].copy(), beta[:n_eff].copy(),
+                         Q[:, :n_eff].copy(), q_next, n_eff, broke)
+
+
+def tridiagonal(alpha, beta_off):
+    """T = tridiag(beta; alpha; beta) (Algorithm 2, last step)."""
+    n = len(alpha)
+    T = np.diag(np.asarray(alpha, dtype=np.float64))
+    if n > 1:
+        T += np.diag(beta_off[:n - 1], 1) + np.diag(beta_off[:n - 1], -1)
+    return T
+
+
+# --------------------------------------------------------------------------
+# Step 3: Eigh(T) and Ritz coordinates (Algorithm 1, reading R5)
+# --------------------------------------------------------------------------
+def eigh_tridiagonal(alpha, beta_off):
+    """Eigenpairs of T, ascending, with each vector's first nonzero entry > 0."""
+    theta, S = np.linalg.eigh(tridiagonal(alpha, beta_off))
+    for c in range(S.shape[1]):
+        nz = np.flatnonzero(S[:, c] != 0.0)
+        if nz.size and S[nz[0], c] < 0:
+            S[:, c] = -S[:, c]
+    return theta, S
+
+
+def ritz(lz, r):
+    """Top-r Ritz values (ascending) and coordinates Z = Q S[:, n-r:]."""
+    n = lz.n_eff
+    theta, S = eigh_tridiagonal(lz.alpha, lz.beta)
+    r_eff = min(r, n)
+    N = lz.Q.shape[0]
+    Z = np.zeros((N, r))
+    Z[:, r - r_eff:] = lz.Q @ S[:, n - r_eff:]
+    vals = np.zeros(r)
+    vals[r - r_eff:] = theta[n - r_eff:]
+    return vals, Z, theta, S
+
+
+# --------------------------------------------------------------------------
+# Step 4: SimHash in the spectral subspace (Eq. 5, reading R6)
+# --------------------------------------------------------------------------
+def projections(Z, R):
+    return Z @ R
+
+
+def simhash(Z, R):
+    """codes[i] = sum_l [r_l . z_i > 0] 2^l  (Eq. 5)."""
+    P = projections(Z, R)
+    bits = (P > 0.0).astype(np.int64)
+    return (bits << np.arange(R.shape[1], dtype=np.int64)[None, :]).sum(axis=1)
+
+
+# --------------------------------------------------------------------------
+# Step 5: macro-tokens (Eq. 7, section 3.4 max positions, section 3.6 order)
+# --------------------------------------------------------------------------
+@dataclass
+class MergeResult:
+    E: np.ndarray              # M x D macro-token embeddings (fp64)
+    P: np.ndarray              # M positions (int64), ascending
+    tok2macro: np.ndarray      # N macro index per token
+    members: list = field(default_factory=list)   # member token indices per macro (ascending)
+    codes_of_macro: np.ndarray = None
+
+
+def renormalised_mean(rows):
+    """Eq. 7: mean of the rows rescaled to the mean row norm (zero stays zero)."""
+    rows = np.asarray(rows, dtype=np.float64)
+    mean = rows.mean(axis=0)
+    eta = np.linalg.norm(rows, axis=1).mean()
+    nrm = np.linalg.norm(mean)
+    if nrm == 0.0:
+        return np.zeros_like(mean)
+    return mean * (eta / nrm)
+
+
+def merge(X, codes, positions=None, compact=False):
+    """Group tokens by code; one renormalised mean per group; max position;
+    groups ordered by that position (reading R7)."""
+    X = np.asarray(X)
+    N = len(codes)
+    pos = np.arange(N, dtype=np.int64) if positions is None else np.asarray(positions, np.int64)
+    groups = {}
+    for i in range(N):
+        groups.setdefault(int(codes[i]), []).append(i)
+    entries = sorted(((max(pos[idx]), c, idx) for c, idx in groups.items()), key=lambda e: e[0])
+    M = len(entries)
+    E = np.zeros((M, X.shape[1]))
+    P = np.zeros(M, dtype=np.int64)
+    t2m = np.zeros(N, dtype=np.int64)
+    members = []
+    cm = np.zeros(M, dtype=np.int64)
+    for k, (p, c, idx) in enumerate(entries):
+        E[k] = renormalised_mean(X[idx].astype(np.float64))
+        P[k] = p
+        t2m[idx] = k
+        members.append(np.asarray(idx, dtype=np.int64))
+        cm[k] = c
+    if compact:
+        P = np.arange(M, dtype=np.int64)
+    return MergeResult(E, P, t2m, members, cm)
+
+
+# --------------------------------------------------------------------------
+# Adaptive backend pieces (section 3.5 chunk, section 3.6 Eq. 8 and routing)
+# --------------------------------------------------------------------------
+def redundancy_score(Xw):
+    """Eq. 8: mean cosine of each row to the normalised centroid (reading R8)."""
+    Xw = np.asarray(Xw, dtype=np.float64)
+    S = Xw.sum(axis=0)
+    sn = np.linalg.norm(S)
+    if sn == 0.0:
+        return 0.0
+    xbar = S / sn
+    norms = np.linalg.norm(Xw, axis=1)
+    dots = Xw @ xbar
+    cos = np.where(norms > 0, dots / np.where(norms > 0, norms, 1.0), 0.0)
+    return float(cos.mean())
+
+
+def tau_of_rho(rho):
+    """Routing threshold schedule (section 3.6, reading R9)."""
+    if rho <= 2.0:
+        return 0.70
+    if rho <= 8.0:
+        return 0.70 + (0.60 - 0.70) * (math.log2(rho) - 1.0) / 2.0
+    if rho < 16.0:
+        return 0.60 + (0.55 - 0.60) * (math.log2(rho) - 3.0)
+    return 0.55
+
+
+def route_window(L, score, rho, tau=None):
+    """True = spectral path, False = chunk (section 3.6)."""
+    if rho >= 16.0:
+        return True
+    if L <= 4:
+        return False
+    t = tau_of_rho(rho) if tau is None else tau
+    return score >= t
+
+
+def chunk_size(rho):
+    return max(1, int(round(rho)))          # Python round: half to even (reading R10)
+
+
+def chunk_pool(Xw, k, pos0=0):
+    """Section 3.5: consecutive groups of k rows, renormalised mean, max position."""
+    L = Xw.shape[0]
+    starts = list(range(0, L, k))
+    E = np.stack([renormalised_mean(Xw[s:min(s + k, L)]) for s in starts])
+    P = np.array([pos0 + min(s + k, L) - 1 for s in starts], dtype=np.int64)
+    return E, P
+
+
+# --------------------------------------------------------------------------
+# End to end (Algorithm 1)
+# --------------------------------------------------------------------------
+@dataclass
+class CompressResult:
+    Phi: np.ndarray
+    lz: LanczosResult
+    ritz_values: np.ndarray
+    Z: np.ndarray
+    proj: np.ndarray
+    codes: np.ndarray
+    merge: MergeResult
+
+
+def compress(X, W, psi, q1, R, n_it, r, kernel="softmax", positions=None, keep_phi=True):
+    """One global Spectral-LSH pass over X (Algorithm 1)."""
+    Phi = feature_map(X, W, psi, kernel)
+    lz = lanczos(Phi, q1, n_it)
+    vals, Z, _, _ = ritz(lz, r)
+    proj = projections(Z, R)
+    codes = simhash(Z, R)
+    mg = merge(X, codes, positions)
+    return CompressResult(Phi if keep_phi else None, lz, vals, Z, proj, codes, mg)
+
+
+@dataclass
+class WindowResult:
+    window: int
+    score: float
+    spectral: bool
+    E: np.ndarray
+    P: np.ndarray
+    tok2macro: np.ndarray      # window-local macro index per token
+    detail: CompressResult = None
+
+
+def compress_adaptive(X, L, rho, W, psi, q1_of_window, R, n_it, r, tau=None,
+                      kernel="softmax", keep_detail=False):
+    """Adaptive backend over consecutive windows of L tokens (section 3.6):
+    score each window (Eq. 8), route it, run chunk pooling (section 3.5) or
+    Spectral-LSH (Algorithm 1) on it with global positions, and return the
+    macro-tokens of all windows in ascending position order."""
+    N = X.shape[0]
+    if N % L:
+        raise ValueError("N must be a multiple of the window length")
+    out = []
+    for w in range(N // L):
+        Xw = X[w * L:(w + 1) * L]
+        score = redundancy_score(Xw)
+        spectral = route_window(L, score, rho, tau)
+        if spectral:
+            res = compress(Xw, W, psi, q1_of_window(w), R, n_it, r, kernel,
+                           positions=w * L + np.arange(L), keep_phi=False)
+            out.append(WindowResult(w, score, True, res.merge.E, res.merge.P,
+                                    res.merge.tok2macro, res if keep_detail else None))
+        else:
+            k = chunk_size(rho)
+            E, P = chunk_pool(Xw, k, pos0=w * L)
+            out.append(WindowResult(w, score, False, E, P, np.arange(L) // k))
+    return out

@@ -1,0 +1,142 @@
+"""Seeded synthetic inputs shaped like the paper's workloads.
+
+This module only produces input data (token ids and embedding rows); it holds
+none of the method's arithmetic and is shared by the tests, the benchmark and
+the oracle checks.  The paper evaluates on packed C4 / Wikitext-103 sequences of
+2048-16384 tokens embedded by Mistral-7B and Qwen2.5 models (section 5.1); those
+data and weights are not available, so these generators stand in for them with
+the same shapes:
+
+  tiny          N=512, D=256 fp32 rows from a 32-component Gaussian mixture
+                (unit-norm centres, within-cluster std 0.1).
+  mistral7b     N=4096 ids ~ Zipf(1.1) over 32768 rows, D=4096 bf16 table N(0, 0.02).
+  qwen7b        N=8192 ids ~ Zipf(1.1) over 152064 rows, D=3584 bf16 table N(0, 0.02).
+  qwen14b_long  N=32768 ids ~ Zipf(1.1) over 152064 rows, D=5120 bf16 table N(0, 0.02).
+  adaptive64    64 windows of 2048 ids, D=4096 bf16 table over 32768 rows; even
+                windows repeat a Zipf template of period U{16..64} with 10% of
+                positions replaced by fresh Zipf draws (JSON/code/table-like
+                redundancy), odd windows are i.i.d. Zipf(1.1).
+
+Table rows are generated per id on demand (row id -> its own seeded stream), so
+the 152064-row tables are never materialised.
+"""
+from dataclasses import dataclass
+
+import numpy as np
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    N: int            # tokens (all windows together)
+    D: int            # embedding width
+    m: int            # random features
+    n_it: int         # Lanczos steps
+    r: int            # kept Ritz vectors
+    bits: int         # SimHash bits
+    rho: float        # target compression
+    vocab: int = 0
+    window: int = 0   # window length (0 = one global window)
+    x_dtype: str = "bf16"
+
+
+WORKLOADS = {
+    "tiny": Workload("tiny", 512, 256, 256, 32, 8, 6, 4.0, 0, 0, "f32"),
+    "mistral7b": Workload("mistral7b", 4096, 4096, 1024, 64, 32, 10, 8.0, 32768),
+    "qwen7b": Workload("qwen7b", 8192, 3584, 2048, 96, 64, 12, 16.0, 152064),
+    "qwen14b_long": Workload("qwen14b_long", 32768, 5120, 2048, 128, 64, 14, 16.0, 152064),
+    "adaptive64": Workload("adaptive64", 64 * 2048, 4096, 1024, 48, 32, 10, 8.0, 32768, 2048),
+}
+
+
+def f32_to_bf16_bits(a):
+    """float32 -> bf16 bit patterns (uint16), round to nearest even."""
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    r = (u + np.uint64(0x7FFF) + ((u >> np.uint64(16)) & np.uint64(1))) >> np.uint64(16)
+    return r.astype(np.uint16)
+
+
+def bf16_bits_to_f32(b):
+    return (np.ascontiguousarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def zipf_ids(rng, vocab, n, s=1.1):
+    """n ids in [0, vocab) with P(id = k-1) proportional to k^-s."""
+    k = np.arange(1, vocab + 1, dtype=np.float64)
+    cdf = np.cumsum(k ** -s)
+    cdf /= cdf[-1]
+    u = rng.random(n)
+    return np.minimum(np.searchsorted(cdf, u, side="right"), vocab - 1).astype(np.int64)
+
+
+def table_rows(seed, ids, D, std=0.02):
+    """bf16 bits of embedding-table rows for the given ids (each id its own stream)."""
+    out = np.empty((len(ids), D), dtype=np.uint16)
+    for j, i in enumerate(ids):
+        g = np.random.default_rng(np.random.SeedSequence([int(seed), 0x7AB1E, int(i)]))
+        out[j] = f32_to_bf16_bits((std * g.standard_normal(D)).astype(np.float32))
+    return out
+
+
+def embed(seed, ids, D):
+    """Gather rows of the seeded N(0, 0.02) bf16 table: N x D uint16 bits."""
+    uniq, inv = np.unique(ids, return_inverse=True)
+    rows = table_rows(seed, uniq, D)
+    return rows[inv.reshape(-1)]
+
+
+def mixture(seed, N, D, comps=32, sigma=0.1):
+    rng = np.random.default_rng(np.random.SeedSequence([int(seed), 0xC1]))
+    C = rng.standard_normal((comps, D))
+    C /= np.linalg.norm(C, axis=1, keepdims=True)
+    lab = rng.integers(0, comps, N)
+    return (C[lab] + sigma * rng.standard_normal((N, D))).astype(np.float32), lab
+
+
+def periodic_ids(rng, vocab, L, pmin=16, pmax=64, sub=0.10):
+    P = int(rng.integers(pmin, pmax + 1))
+    tmpl = zipf_ids(rng, vocab, P)
+    ids = tmpl[np.arange(L) % P].copy()
+    mask = rng.random(L) < sub
+    ids[mask] = zipf_ids(rng, vocab, int(mask.sum()))
+    return ids, P
+
+
+@dataclass
+class Inputs:
+    workload: Workload
+    X: np.ndarray          # N x D: uint16 bf16 bits, or float32 for the tiny mixture
+    ids: np.ndarray        # token ids (or mixture labels)
+    periods: np.ndarray = None   # adaptive64: template period per window (0 = i.i.d.)
+
+    def x_float(self, rows=slice(None)):
+        """Values of X as float64 (exact)."""
+        Xs = self.X[rows]
+        if self.workload.x_dtype == "bf16":
+            return bf16_bits_to_f32(Xs).astype(np.float64)
+        return Xs.astype(np.float64)
+
+
+def make_inputs(name, seed=0, N=None):
+    """Seeded synthetic X for a named workload.  N overrides the token count
+    (same distributions, used for reduced-size parity cases)."""
+    wl = WORKLOADS[name]
+    if N is not None and N != wl.N:
+        wl = Workload(wl.name, N, wl.D, wl.m, wl.n_it, wl.r, wl.bits, wl.rho, wl.vocab, wl.window, wl.x_dtype)
+    if wl.x_dtype == "f32":
+        X, lab = mixture(seed, wl.N, wl.D)
+        return Inputs(wl, X, lab)
+    rng = np.random.default_rng(np.random.SeedSequence([int(seed), 0x1D5]))
+    if wl.window:
+        n_win = wl.N // wl.window
+        ids = np.empty(wl.N, dtype=np.int64)
+        periods = np.zeros(n_win, dtype=np.int64)
+        for w in range(n_win):
+            seg = slice(w * wl.window, (w + 1) * wl.window)
+            if w % 2 == 0:
+                ids[seg], periods[w] = periodic_ids(rng, wl.vocab, wl.window)
+            else:
+                ids[seg] = zipf_ids(rng, wl.vocab, wl.window)
+        return Inputs(wl, embed(seed, ids, wl.D), ids, periods)
+    ids = zipf_ids(rng, wl.vocab, wl.N)
+    return Inputs(wl, embed(seed, ids, wl.D), ids)
