@@ -1,0 +1,187 @@
+"""Throughput of the Spectral-LSH hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload qwen7b] [--no-cpu-baseline]
+
+A step is one pass of the whole path over one prompt already resident in HBM:
+feature map -> Lanczos (all steps) -> eigensolve + Ritz -> SimHash -> merge
+(plus routing for the windowed adaptive workload).  Prints one JSON line.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "compressed prompt tokens/sec at N=8192,D=3584,ρ=16; Lanczos matvec HBM GB/s"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="qwen7b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--timing", type=int, default=1, help="record per-stage HIP events")
+    return ap.parse_args()
+
+
+def cpu_baseline(inp, min_seconds=10.0, max_reps=40):
+    """The oracle, untouched, on the same prompt: feature map .. merge (parameter
+    drawing excluded, as on the GPU side where it happens in slh_create), repeated
+    until about min_seconds of CPU work have been timed."""
+    import numpy as np
+    from oracle import params as OP
+    from oracle import spectral_lsh as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max((d.get("num_threads", 1) for d in threadpool_info()), default=1)
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    wl = inp.workload
+    L = wl.window or wl.N
+    W = OP.projection(0, wl.D, wl.m)
+    psi = OP.phases(0, wl.m)
+    R = OP.hyperplanes(0, wl.r, wl.bits)
+    q1 = [OP.start_vector(0, L, w) for w in range(wl.N // L)]
+    times = []
+    while len(times) < 2 or (sum(times) < min_seconds and len(times) < max_reps):
+        t0 = time.perf_counter()
+        for w in range(wl.N // L):
+            Xw = inp.x_float(slice(w * L, (w + 1) * L))
+            Phi = O.feature_map(Xw, W, psi)
+            lz = O.lanczos(Phi, q1[w], wl.n_it)
+            _, Z, _, _ = O.ritz(lz, wl.r)
+            codes = O.simhash(Z, R)
+            O.merge(Xw, codes, positions=w * L + np.arange(L))
+        times.append(time.perf_counter() - t0)
+    t = sum(times) / len(times)
+    return {"value": wl.N / t, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"the full {wl.name} prompt ({wl.N} tokens), feature map through merge, "
+                      f"{len(times)} runs in {sum(times):.1f} s ({t:.2f} s each)",
+            "seconds": t}
+
+
+def main():
+    a = parse()
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: this build runs on one GPU only (the path is single-GPU; see the "
+              "sharding notes in DESIGN.md); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+    import paper_2607_19368_amd as P
+    from paper_2607_19368_amd import slh as B
+    from workloads import make_inputs
+
+    P.load()                                   # fails loudly if libslh.so is missing
+    torch.cuda.set_device(0)
+    inp = make_inputs(a.workload)
+    wl = inp.workload
+    L = wl.window or wl.N
+    X = torch.from_numpy(inp.X.view(np.int16).copy()).view(torch.bfloat16).cuda() \
+        if wl.x_dtype == "bf16" else torch.from_numpy(inp.X).cuda()
+
+    ctx = P.slh_create(wl.N, wl.D, wl.m, wl.r, wl.bits, 0)
+    if wl.window:
+        P.slh_set_option(ctx, B.SLH_OPT_WINDOW_LEN, wl.window)
+    tau = -1.0
+    if wl.window:
+        # routing threshold: midpoint of the 32nd and 33rd largest window scores
+        _, sc = P.slh_route(ctx, X, wl.rho, -1.0)
+        s = np.sort(sc)[::-1]
+        tau = 0.5 * (s[31] + s[32])
+    cap = P.slh_merge_capacity(ctx) if not wl.window else wl.N
+    E = torch.empty((cap, wl.D), dtype=torch.float32, device="cuda")
+    Pp = torch.empty(cap, dtype=torch.int32, device="cuda")
+    T2M = torch.empty(wl.N, dtype=torch.int32, device="cuda")
+
+    def step():
+        if wl.window:
+            P.slh_route(ctx, X, wl.rho, tau)
+        P.slh_feature_map(ctx, X)
+        P.slh_lanczos(ctx, wl.n_it, want=False)
+        P.slh_simhash(ctx)
+        return P.slh_merge(ctx, X, E, Pp, T2M)[3]
+
+    # timed region 1: the production path (Lanczos loop replayed as one HIP graph)
+    for _ in range(a.warmup):
+        M = step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(a.steps):
+        M = step()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ms_per_step = 1e3 * dt / a.steps
+    value = wl.N * a.steps / dt
+
+    # timed region 2: the same steps with HIP events around every stage and every
+    # pass over Phi (launched without the graph so that each pass can be bracketed)
+    stage_sum = {k: 0.0 for k in B.STAGE_NAMES}
+    ms2 = None
+    if a.timing:
+        P.slh_set_option(ctx, B.SLH_OPT_TIMING, 1)
+        for _ in range(2):
+            step()
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for _ in range(a.steps):
+            step()
+            st = P.slh_stage_times(ctx)
+            for k in stage_sum:
+                stage_sum[k] += st[k]
+        torch.cuda.synchronize()
+        ms2 = 1e3 * (time.perf_counter() - t1) / a.steps
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": a.steps,
+        "warmup": a.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f64",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name}: N={wl.N} D={wl.D} m={wl.m} n_it={wl.n_it} r={wl.r} "
+                        f"bits={wl.bits} rho={wl.rho:g}" + (f" window={wl.window}" if wl.window else ""),
+            "inputs": "Zipf(1.1) token ids over a seeded N(0,0.02) bf16 embedding table"
+                      if wl.x_dtype == "bf16" else "seeded Gaussian mixture, fp32",
+            "precision": "bf16 MFMA feature map with fp32 accumulation, fp32 Phi, fp64 Lanczos/"
+                         "eigensolve/Ritz/SimHash, fp32 merge sums",
+            "M": int(M), "rho_achieved": wl.N / max(1, int(M)),
+        },
+    }
+    if a.timing and stage_sum["phi_pass_count"] > 0:
+        K = a.steps
+        n_win = ctx.n_spectral
+        pass_ms = stage_sum["phi_pass_ms_sum"] / stage_sum["phi_pass_count"]
+        # algorithmic bytes per pass over Phi (either half of the implicit matvec,
+        # Eq. 4): Phi once (4 B/elt) + the L-vector (q in, or u out) + the m-vector
+        # (t out, or t in), fp64, per window
+        alg = n_win * (4.0 * L * wl.m + 8.0 * (L + wl.m))
+        ach = alg / (pass_ms * 1e-3) / 1e9
+        out["roofline"] = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                           "frac": ach / HBM_PEAK_GBS, "traffic": None,
+                           "kernel": "k_lz_phit + k_lz_phiu (t = Phi^T q and u = Phi t)",
+                           "bytes_per_launch": alg, "avg_launch_ms": pass_ms}
+        fm_ms = stage_sum["featmap_ms"] / K
+        flops = 2.0 * n_win * L * wl.D * wl.m
+        out["featmap_mfma"] = {"bound": "mfma", "achieved": flops / (fm_ms * 1e-3) / 1e12,
+                               "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                               "frac": flops / (fm_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
+                               "avg_launch_ms": fm_ms}
+        out["stages_ms"] = {k: v / K for k, v in stage_sum.items() if k != "phi_pass_count"}
+        out["stages_ms"]["phi_pass_avg_ms"] = pass_ms
+        out["stages_ms"]["ms_per_step_with_events"] = ms2
+    if not a.no_cpu_baseline:
+        cb = cpu_baseline(inp)
+        out["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,224 @@
+/*
+ * slh.h - C ABI of the Spectral-LSH hot path on AMD MI355X (gfx950).
+ *
+ * Spectral-LSH (arXiv 2607.19368) compresses N token embeddings X (N x D)
+ * into M macro-tokens: a random-feature map Phi of the unnormalised softmax
+ * kernel (section 3.2, Eq. 2-3), Lanczos with full re-orthogonalization on the
+ * implicit operator Phi (Phi^T v) (Eq. 4, Algorithm 2), an eigensolve of the
+ * Lanczos tridiagonal T and the top-r Ritz coordinates Z (Algorithm 1),
+ * SimHash of Z (Eq. 5) and a merge of each hash bucket into one renormalised
+ * mean with the bucket's max position (Eq. 7, section 3.4), ordered by that
+ * position (section 3.6).  The adaptive backend (section 3.6, Eq. 8) routes
+ * windows of the prompt either to that path or to chunk pooling (section 3.5).
+ *
+ * Notation: N tokens, D embedding width (the paper's d), m random features
+ * (the paper's D), n_it Lanczos steps (the paper's r in Algorithm 2), r kept
+ * Ritz vectors (the paper's k), bits SimHash bits (the paper's b).
+ *
+ * Conventions for every call:
+ *  - Return value: SLH_OK (0) or a negative SLH_E* code.  On error no output
+ *    is written and slh_last_error() describes the cause.
+ *  - "device" pointers are HIP device memory of the current device, owned by
+ *    the caller; "host" pointers are ordinary host memory owned by the caller.
+ *    The context owns every workspace (parameters, Phi, Lanczos basis, codes,
+ *    merge scratch) and frees it in slh_destroy.
+ *  - All GPU work is enqueued on the stream given to slh_set_stream (default:
+ *    the null stream).  Calls return without waiting for it, except where a
+ *    host output is produced (noted per call).
+ *  - A context is not thread-safe; separate contexts are independent.
+ *  - Calls must follow the path order: [slh_route] -> slh_feature_map ->
+ *    slh_lanczos -> slh_simhash -> slh_merge; calling a step before its
+ *    predecessor returns SLH_ESTATE.
+ */
+#ifndef SLH_H
+#define SLH_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct slh_ctx slh_ctx;
+
+/* status codes */
+#define SLH_OK      0
+#define SLH_EINVAL (-1)   /* bad argument, size or alignment                      */
+#define SLH_ENOMEM (-2)   /* device or host allocation failed                     */
+#define SLH_EHIP   (-3)   /* a HIP runtime call failed (message has the details)  */
+#define SLH_ESTATE (-4)   /* step called out of order                             */
+
+/* element types of X */
+#define SLH_BF16 0        /* bfloat16, raw 16-bit patterns                          */
+#define SLH_F32  1        /* float32                                                */
+
+/* options for slh_set_option (set before slh_feature_map) */
+#define SLH_OPT_KERNEL        1  /* 0: unbiased for exp(x.y/sqrt(D)) (default): the
+                                    Eq. 3 map times s(x) = exp(|x|^2/(2 sqrt(D)));
+                                    1: the Eq. 3 map as printed (Gaussian kernel)      */
+#define SLH_OPT_WINDOW_LEN    2  /* window length L (N must be a multiple of L);
+                                    0 (default) = one window of N tokens.  Every step
+                                    then runs independently per window (section 3.5
+                                    local backend, section 3.6 adaptive backend)       */
+#define SLH_OPT_POS_MODE      3  /* 0: representative positions (default), 1: compact
+                                    0..M-1 (section 5.6, compressed position mode)     */
+#define SLH_OPT_BREAKDOWN_TOL 4  /* Lanczos stops when beta_j <= tol * max_i alpha_i
+                                    (Algorithm 2 break); default 1e-10                 */
+#define SLH_OPT_TIMING        5  /* 1: record HIP events around each stage and around
+                                    every pass over Phi (see slh_stage_times)          */
+
+/*
+ * Random parameters of the method, drawn from `seed` with Philox4x32-10
+ * (Salmon et al., SC'11): key = (seed lo, seed hi), counter = (block lo,
+ * block hi, stream, window); block n gives the uniform
+ * u = ((w0 >> 5) * 2^26 + (w1 >> 6)) / 2^53 and, with w2/w3 likewise, the
+ * Box-Muller pair (sqrt(-2 ln(1-u_a)) cos(2 pi u_b), ... sin(...)) as elements
+ * 2n, 2n+1.  Streams: 1 = W, 2 = psi, 3 = q1, 4 = R.
+ *   W[k][j]  = bf16_rne(float(n_{k*m+j} / sqrt(sqrt(D))))    (section 3.2: variance 1/sqrt(d))
+ *   psi[j]   = float(2 pi u_j)                                 (section 3.2: Uniform(0, 2 pi))
+ *   R[c][l]  = n_{c*bits+l}                                    (Eq. 5: r_l ~ N(0, I))
+ *   q1 (window w) = first n normals of stream 3, window w, scaled to unit norm
+ *                                                              (Algorithm 2 start)
+ * These two calls run on the host only and touch no GPU.
+ */
+/* W_out: host, D*m uint16 bf16 patterns, row-major [D][m] (may be NULL);
+   psi_out: host, m floats (may be NULL); R_out: host, r*bits doubles,
+   row-major [r][bits] (may be NULL). */
+int slh_gen_params(uint64_t seed, int64_t D, int64_t m, int32_t r, int32_t bits,
+                   uint16_t *W_out, float *psi_out, double *R_out);
+/* q_out: host, n doubles. */
+int slh_gen_start(uint64_t seed, int64_t window, int64_t n, double *q_out);
+
+/*
+ * Create a context for prompts of N tokens of width D with m random features,
+ * r kept Ritz vectors and `bits` SimHash bits (Algorithm 1 inputs).  Draws the
+ * parameters (above) on the host and uploads them to the current device.
+ * Limits: N >= 2; D >= 8 and D % 8 == 0; m % 256 == 0 and 256 <= m <= 2048;
+ * 1 <= r <= 128; 1 <= bits <= 16.  *out receives the context (NULL on error).
+ */
+int slh_create(slh_ctx **out, int64_t N, int64_t D, int64_t m, int32_t r,
+               int32_t bits, uint64_t seed);
+void slh_destroy(slh_ctx *ctx);
+const char *slh_last_error(const slh_ctx *ctx);
+
+int slh_set_option(slh_ctx *ctx, int32_t key, double value);
+/* stream: a hipStream_t (NULL = null stream). */
+int slh_set_stream(slh_ctx *ctx, void *stream);
+
+/*
+ * Adaptive routing (section 3.6): per window, the redundancy score of Eq. 8
+ * (mean cosine of each row to the normalised sum of the rows), then
+ *   spectral if rho >= 16, else chunk if L <= 4, else spectral iff score >= tau;
+ * tau < 0 selects the schedule tau(rho): 0.70 at rho <= 2, linear in log2(rho)
+ * through 0.60 at 8 and 0.55 at 16.  Chunk windows are pooled in groups of
+ * k = max(1, round-half-even(rho)) consecutive tokens (section 3.5).
+ * Without this call every window takes the spectral path.
+ * X: device, N rows of width D, row stride ldx elements (ldx >= D, ldx % 8 == 0,
+ * 16-byte aligned).  route_out: host, n_windows bytes (1 = spectral), may be
+ * NULL; scores_out: host, n_windows doubles, may be NULL.  Synchronises the
+ * stream (the routing decision is made on the host from the device scores).
+ */
+int slh_route(slh_ctx *ctx, const void *X, int32_t x_dtype, int64_t ldx,
+              double rho, double tau, uint8_t *route_out, double *scores_out);
+
+/*
+ * Step 1 (Eq. 3, Algorithm 1 first line): Phi = s(x) sqrt(2/m) cos(bf16(X) W + psi)
+ * for the tokens of every spectral window, stored fp32 in the context.
+ * X as for slh_route.  Asynchronous.
+ */
+int slh_feature_map(slh_ctx *ctx, const void *X, int32_t x_dtype, int64_t ldx);
+
+/*
+ * Steps 2-3 (Algorithm 2, then Eigh(T) and the top-r Ritz coordinates of
+ * Algorithm 1): n_it Lanczos steps on Phi (Phi^T v) with full
+ * re-orthogonalization, in fp64, from the seeded start vector of each window;
+ * then the top-r eigenpairs of T (ascending; each eigenvector's first nonzero
+ * entry positive) and Z = Q S[:, n-r:n] (N x r, fp64, kept in the context).
+ * Requires r <= n_it <= min(L, 256).  A window whose beta_j falls below the
+ * breakdown tolerance stops after n_eff = j steps (not an error): its Z then has
+ * r - min(r, n_eff) leading zero columns and zero Ritz values.
+ * ritz_out: host, n_spectral * r doubles (ascending per window) or NULL;
+ * iters_out: host, n_spectral int32 (n_eff per window) or NULL.  If either is
+ * non-NULL the call synchronises the stream; with both NULL it is asynchronous.
+ */
+int slh_lanczos(slh_ctx *ctx, int32_t n_it, double *ritz_out, int32_t *iters_out);
+
+/*
+ * Step 4 (Eq. 5): code_i = sum_l [R[:, l] . z_i > 0] 2^l for tokens of spectral
+ * windows.  codes_out: device, N uint32 (tokens of chunk windows get
+ * 0xFFFFFFFF), or NULL (codes stay in the context).  Asynchronous.
+ */
+int slh_simhash(slh_ctx *ctx, uint32_t *codes_out);
+
+/*
+ * Step 5 (Eq. 7; section 3.4 max positions; section 3.6 ordering): one
+ * macro-token per (window, code) bucket, and per chunk group of chunk windows:
+ * E = mean of the member rows of X (as given) rescaled to the mean member norm
+ * (zero if the mean is zero), position = max member token index (global, 0-based;
+ * or 0..M-1 in compact mode), macro-tokens in ascending position order.
+ * X: the same tokens passed to slh_feature_map.
+ * emb_out: device, cap x D floats (row-major); pos_out: device, cap int32;
+ * tok2macro_out: device, N int32 (macro index of each token), may be NULL;
+ * cap >= the bound n_spectral_windows * min(L, 2^bits) + chunk groups.
+ * *M_out (host) receives M.  Synchronises the stream.
+ */
+int slh_merge(slh_ctx *ctx, const void *X, int32_t x_dtype, int64_t ldx,
+              float *emb_out, int32_t *pos_out, int32_t *tok2macro_out,
+              int64_t cap, int64_t *M_out);
+
+/* Capacity slh_merge needs for the current routing. */
+int64_t slh_merge_capacity(const slh_ctx *ctx);
+
+/*
+ * Copy an intermediate result to host memory (parity checks and diagnostics).
+ * Synchronises the stream.  `bytes` must equal the size listed:
+ *   SLH_OUT_PHI    n_act*L*m floats      Phi rows of the spectral windows in order
+ *   SLH_OUT_ALPHA  n_act*n_it doubles    diagonal of T per window (zero past n_eff)
+ *   SLH_OUT_BETA   n_act*n_it doubles    beta_1..beta_{n_it} per window
+ *   SLH_OUT_Z      n_act*L*r doubles     Ritz coordinates, row-major per window
+ *   SLH_OUT_PROJ   n_act*L*bits doubles  SimHash projections R^T z_i
+ *   SLH_OUT_CODES  N uint32              codes (0xFFFFFFFF for chunk windows)
+ *   SLH_OUT_THETA  n_act*r doubles       kept Ritz values (ascending)
+ *   SLH_OUT_Q      n_act*(n_it+1)*L doubles  Lanczos basis, vector-major
+ *   SLH_OUT_WINDOWS n_act int32          window index of each spectral window
+ * (n_act = number of spectral windows.)
+ */
+#define SLH_OUT_PHI     1
+#define SLH_OUT_ALPHA   2
+#define SLH_OUT_BETA    3
+#define SLH_OUT_Z       4
+#define SLH_OUT_PROJ    5
+#define SLH_OUT_CODES   6
+#define SLH_OUT_THETA   7
+#define SLH_OUT_Q       8
+#define SLH_OUT_WINDOWS 9
+int slh_copy_out(slh_ctx *ctx, int32_t which, void *dst_host, int64_t bytes);
+
+/*
+ * Replace a stage's result with caller data so a later stage can be checked on
+ * its own (step-wise parity).  src: device memory, `bytes` exactly:
+ *   SLH_OUT_PHI    n_act*L*m floats  -> Phi; the next call may be slh_lanczos
+ *   SLH_OUT_CODES  N uint32          -> codes; the next call may be slh_merge
+ * Asynchronous (device-to-device copy on the context stream).
+ */
+int slh_load(slh_ctx *ctx, int32_t which, const void *src, int64_t bytes);
+
+/*
+ * Stage timings of the most recent calls, from HIP events on the context
+ * stream (requires SLH_OPT_TIMING = 1 before those calls).  Fills up to n of:
+ *   [0] feature map ms        [1] Lanczos loop ms (all steps, all windows)
+ *   [2] sum of Phi-pass ms     [3] number of Phi passes timed (2 per step)
+ *   [4] eigensolve + Ritz ms  [5] SimHash ms   [6] merge ms
+ * Synchronises the stream.
+ */
+int slh_stage_times(slh_ctx *ctx, double *ms_out, int32_t n);
+
+/* Number of windows and of spectral windows of the current routing. */
+int64_t slh_num_windows(const slh_ctx *ctx);
+int64_t slh_num_spectral(const slh_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SLH_H */

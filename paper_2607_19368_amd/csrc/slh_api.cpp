@@ -1,0 +1,834 @@
+// Host side of the C ABI declared in include/slh.h: argument checks, the
+// method's seeded parameters, workspace ownership, and the launch sequence of
+// each step.  All arithmetic of the path runs in the HIP kernels.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "slh.h"
+#include "slh_internal.h"
+
+using namespace slh;
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11) and the derived streams.
+// ---------------------------------------------------------------------------
+namespace {
+
+inline void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c[0];
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c[2];
+    const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+    const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+    const uint32_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
+    c[0] = n0;
+    c[1] = lo1;
+    c[2] = n2;
+    c[3] = lo0;
+  }
+}
+
+inline void philox_block(uint64_t seed, uint32_t stream, uint32_t window, uint64_t n,
+                         uint32_t out[4]) {
+  out[0] = (uint32_t)n;
+  out[1] = (uint32_t)(n >> 32);
+  out[2] = stream;
+  out[3] = window;
+  philox4x32_10(out, (uint32_t)seed, (uint32_t)(seed >> 32));
+}
+
+inline double u53(uint32_t a, uint32_t b) {
+  return ((double)(a >> 5) * 67108864.0 + (double)(b >> 6)) / 9007199254740992.0;
+}
+
+enum { STREAM_W = 1, STREAM_PSI = 2, STREAM_Q1 = 3, STREAM_R = 4 };
+
+void gen_normals(uint64_t seed, uint32_t stream, uint32_t window, int64_t count, double* out) {
+  const int64_t nb = (count + 1) / 2;
+  for (int64_t n = 0; n < nb; ++n) {
+    uint32_t w[4];
+    philox_block(seed, stream, window, (uint64_t)n, w);
+    const double ua = u53(w[0], w[1]), ub = u53(w[2], w[3]);
+    const double rad = std::sqrt(-2.0 * std::log(1.0 - ua));
+    const double ang = (2.0 * M_PI) * ub;
+    out[2 * n] = rad * std::cos(ang);
+    if (2 * n + 1 < count) out[2 * n + 1] = rad * std::sin(ang);
+  }
+}
+
+inline uint16_t bf16_rne(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// context
+// ---------------------------------------------------------------------------
+struct DevBuf {
+  void* p = nullptr;
+  size_t bytes = 0;
+};
+
+struct slh_ctx {
+  int64_t N = 0, D = 0, m = 0;
+  int r = 0, bits = 0;
+  uint64_t seed = 0;
+  int gauss = 0, compact = 0;
+  int64_t L = 0, n_win = 1;
+  double tol = 1e-10;
+  hipStream_t stream = nullptr;
+  hipStream_t cap_stream = nullptr;
+  int device = 0, n_cu = 256;
+  std::string err;
+
+  // routing
+  std::vector<uint8_t> route_h;
+  std::vector<int> winlist_h;
+  int n_act = 0, chunk_k = 1;
+  bool routed = false;
+  bool routing_on_device = false;
+
+  // stage: 0 ready, 1 feature map done, 2 Lanczos done, 3 SimHash done
+  int stage = 0;
+  int n_it = 0;
+  const void* norms_of = nullptr;   // X for which the row norms are current
+  int64_t q1_L = -1;                // window length q1all was drawn for
+
+  std::vector<DevBuf*> all;
+  DevBuf Wt, psi, R, q1all, q1act, winlist, route;
+  DevBuf nrm2_fm, nrm_x, rowscale, Xb, Phi;
+  DevBuf Q, T, U, Z1, Spart, H1part, H1, H2part, H2, alpha, beta, neff, stop, amax;
+  DevBuf theta, Seig, Z, proj, codes;
+  DevBuf keyA, keyB, valA, valB, tmpi, segid, segk, sval, sloc, mw, wbase, sseg, Mtot;
+  DevBuf part, part_seg, part_cnt, part_nsum, part_end;
+  DevBuf rpart, scores;
+
+  hipGraphExec_t lz_exec = nullptr;
+  std::string lz_key;
+
+  // timing (SLH_OPT_TIMING)
+  int timing = 0;
+  std::vector<hipEvent_t> ev_fb, ev_fa;    // around each fused pass
+  hipEvent_t ev[12] = {};                   // stage brackets: fm, lz, eig, sh, mg
+  bool ev_made = false;
+  int fused_timed = 0;
+};
+
+namespace {
+
+int fail(slh_ctx* c, int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (c) c->err = buf;
+  return code;
+}
+
+#define HIP_TRY(c, expr)                                                                   \
+  do {                                                                                     \
+    hipError_t e_ = (expr);                                                                \
+    if (e_ != hipSuccess)                                                                  \
+      return fail((c), SLH_EHIP, "%s failed: %s", #expr, hipGetErrorString(e_));           \
+  } while (0)
+
+// grow-only device buffer
+int ensure(slh_ctx* c, DevBuf& b, size_t bytes) {
+  if (bytes == 0) bytes = 16;
+  if (b.bytes >= bytes) return SLH_OK;
+  if (b.p) {
+    hipError_t e = hipFree(b.p);
+    if (e != hipSuccess) return fail(c, SLH_EHIP, "hipFree: %s", hipGetErrorString(e));
+    b.p = nullptr;
+    b.bytes = 0;
+  }
+  hipError_t e = hipMalloc(&b.p, bytes);
+  if (e != hipSuccess) {
+    b.p = nullptr;
+    return fail(c, SLH_ENOMEM, "hipMalloc(%zu): %s", bytes, hipGetErrorString(e));
+  }
+  b.bytes = bytes;
+  return SLH_OK;
+}
+
+#define ENSURE(c, b, bytes)                   \
+  do {                                        \
+    int rc_ = ensure((c), (b), (bytes));      \
+    if (rc_ != SLH_OK) return rc_;            \
+  } while (0)
+
+template <class T>
+T* P(DevBuf& b) {
+  return (T*)b.p;
+}
+
+int make_events(slh_ctx* c, int n_fused) {
+  if (!c->ev_made) {
+    for (auto& e : c->ev)
+      HIP_TRY(c, hipEventCreate(&e));
+    c->ev_made = true;
+  }
+  while ((int)c->ev_fb.size() < n_fused) {
+    hipEvent_t a, b;
+    HIP_TRY(c, hipEventCreate(&a));
+    HIP_TRY(c, hipEventCreate(&b));
+    c->ev_fb.push_back(a);
+    c->ev_fa.push_back(b);
+  }
+  return SLH_OK;
+}
+
+void drop_graph(slh_ctx* c) {
+  if (c->lz_exec) {
+    (void)hipGraphExecDestroy(c->lz_exec);
+    c->lz_exec = nullptr;
+  }
+  c->lz_key.clear();
+}
+
+int64_t window_len(const slh_ctx* c) { return c->L > 0 ? c->L : c->N; }
+
+int check_x(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx) {
+  if (!X) return fail(c, SLH_EINVAL, "X is NULL");
+  if (dtype != SLH_BF16 && dtype != SLH_F32) return fail(c, SLH_EINVAL, "unknown x_dtype %d", dtype);
+  if (ldx < c->D || ldx % 8 != 0)
+    return fail(c, SLH_EINVAL, "ldx must be >= D and a multiple of 8 (got %lld)", (long long)ldx);
+  if (((uintptr_t)X) % 16 != 0) return fail(c, SLH_EINVAL, "X must be 16-byte aligned");
+  return SLH_OK;
+}
+
+// row norms (and the bf16 copy of fp32 X) for the given X
+int prep_norms(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx) {
+  ENSURE(c, c->nrm2_fm, c->N * sizeof(double));
+  ENSURE(c, c->nrm_x, c->N * sizeof(double));
+  ENSURE(c, c->rowscale, c->N * sizeof(float));
+  uint16_t* xb = nullptr;
+  if (dtype == SLH_F32) {
+    ENSURE(c, c->Xb, (size_t)c->N * c->D * sizeof(uint16_t));
+    xb = P<uint16_t>(c->Xb);
+  }
+  HIP_TRY(c, launch_rownorm(X, dtype == SLH_BF16 ? 0 : 1, ldx, c->N, (int)c->D, (int)c->m,
+                            c->gauss, P<double>(c->nrm2_fm), P<double>(c->nrm_x),
+                            P<float>(c->rowscale), xb, c->stream));
+  c->norms_of = X;
+  return SLH_OK;
+}
+
+int upload_routing(slh_ctx* c) {
+  ENSURE(c, c->winlist, std::max<size_t>(1, c->winlist_h.size()) * sizeof(int));
+  ENSURE(c, c->route, std::max<size_t>(1, c->route_h.size()));
+  if (!c->winlist_h.empty())
+    HIP_TRY(c, hipMemcpyAsync(c->winlist.p, c->winlist_h.data(), c->winlist_h.size() * sizeof(int),
+                              hipMemcpyHostToDevice, c->stream));
+  HIP_TRY(c, hipMemcpyAsync(c->route.p, c->route_h.data(), c->route_h.size(),
+                            hipMemcpyHostToDevice, c->stream));
+  // the host vectors must stay alive until the copies complete
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  c->routing_on_device = true;
+  return SLH_OK;
+}
+
+int ensure_routing(slh_ctx* c) {
+  return c->routing_on_device ? SLH_OK : upload_routing(c);
+}
+
+void route_all_spectral(slh_ctx* c) {
+  c->route_h.assign((size_t)c->n_win, 1);
+  c->winlist_h.resize((size_t)c->n_win);
+  for (int64_t w = 0; w < c->n_win; ++w) c->winlist_h[(size_t)w] = (int)w;
+  c->n_act = (int)c->n_win;
+  c->chunk_k = 1;
+  c->routing_on_device = false;
+}
+
+int64_t capacity(const slh_ctx* c) {
+  const int64_t L = window_len(c);
+  const int64_t per_spec = std::min<int64_t>(L, (int64_t)1 << c->bits);
+  int64_t cap = 0;
+  for (int64_t w = 0; w < c->n_win; ++w)
+    cap += c->route_h[(size_t)w] ? per_spec : (L + c->chunk_k - 1) / c->chunk_k;
+  return cap;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// ABI
+// ---------------------------------------------------------------------------
+extern "C" {
+
+int slh_gen_params(uint64_t seed, int64_t D, int64_t m, int32_t r, int32_t bits,
+                   uint16_t* W_out, float* psi_out, double* R_out) {
+  if (D <= 0 || m <= 0 || r <= 0 || bits <= 0) return SLH_EINVAL;
+  if (W_out) {
+    const double std_w = 1.0 / std::sqrt(std::sqrt((double)D));
+    const int64_t total = D * m;
+    std::vector<double> nrm((size_t)std::min<int64_t>(total, 1 << 20) + 1);
+    // stream W in chunks of whole Philox blocks
+    for (int64_t e0 = 0; e0 < total; e0 += (1 << 20)) {
+      const int64_t cnt = std::min<int64_t>(1 << 20, total - e0);
+      const int64_t nb0 = e0 / 2, nb = (cnt + 1) / 2;
+      for (int64_t b = 0; b < nb; ++b) {
+        uint32_t w[4];
+        philox_block(seed, STREAM_W, 0, (uint64_t)(nb0 + b), w);
+        const double ua = u53(w[0], w[1]), ub = u53(w[2], w[3]);
+        const double rad = std::sqrt(-2.0 * std::log(1.0 - ua));
+        const double ang = (2.0 * M_PI) * ub;
+        nrm[(size_t)(2 * b)] = rad * std::cos(ang);
+        nrm[(size_t)(2 * b + 1)] = rad * std::sin(ang);
+      }
+      for (int64_t e = 0; e < cnt; ++e) W_out[e0 + e] = bf16_rne((float)(nrm[(size_t)e] * std_w));
+    }
+  }
+  if (psi_out) {
+    for (int64_t j = 0; j < m; ++j) {
+      uint32_t w[4];
+      philox_block(seed, STREAM_PSI, 0, (uint64_t)j, w);
+      psi_out[j] = (float)((2.0 * M_PI) * u53(w[0], w[1]));
+    }
+  }
+  if (R_out) gen_normals(seed, STREAM_R, 0, (int64_t)r * bits, R_out);
+  return SLH_OK;
+}
+
+int slh_gen_start(uint64_t seed, int64_t window, int64_t n, double* q_out) {
+  if (n <= 0 || !q_out || window < 0) return SLH_EINVAL;
+  gen_normals(seed, STREAM_Q1, (uint32_t)window, n, q_out);
+  double s = 0.0;
+  for (int64_t i = 0; i < n; ++i) s += q_out[i] * q_out[i];
+  const double nrm = std::sqrt(s);
+  for (int64_t i = 0; i < n; ++i) q_out[i] /= nrm;
+  return SLH_OK;
+}
+
+const char* slh_last_error(const slh_ctx* c) { return c ? c->err.c_str() : "no context"; }
+
+int slh_create(slh_ctx** out, int64_t N, int64_t D, int64_t m, int32_t r, int32_t bits,
+               uint64_t seed) {
+  if (!out) return SLH_EINVAL;
+  *out = nullptr;
+  if (N < 2 || N > (int64_t)1 << 30) return SLH_EINVAL;
+  if (D < 8 || D % 8 != 0 || D > 65536) return SLH_EINVAL;
+  if (m < 256 || m > 2048 || m % 256 != 0) return SLH_EINVAL;
+  if (r < 1 || r > 128) return SLH_EINVAL;
+  if (bits < 1 || bits > 16) return SLH_EINVAL;
+  slh_ctx* c = new (std::nothrow) slh_ctx();
+  if (!c) return SLH_ENOMEM;
+  c->N = N;
+  c->D = D;
+  c->m = m;
+  c->r = r;
+  c->bits = bits;
+  c->seed = seed;
+  c->n_win = 1;
+  if (hipGetDevice(&c->device) != hipSuccess) {
+    delete c;
+    return SLH_EHIP;
+  }
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, c->device) == hipSuccess) c->n_cu = prop.multiProcessorCount;
+  route_all_spectral(c);
+  // parameters: W transposed to [m][D] for K-contiguous MFMA operands
+  std::vector<uint16_t> W((size_t)(D * m)), Wt((size_t)(D * m));
+  std::vector<float> psi((size_t)m);
+  std::vector<double> R((size_t)r * bits);
+  slh_gen_params(seed, D, m, r, bits, W.data(), psi.data(), R.data());
+  for (int64_t k = 0; k < D; ++k)
+    for (int64_t j = 0; j < m; ++j) Wt[(size_t)(j * D + k)] = W[(size_t)(k * m + j)];
+  int rc = SLH_OK;
+  if ((rc = ensure(c, c->Wt, Wt.size() * 2)) || (rc = ensure(c, c->psi, psi.size() * 4)) ||
+      (rc = ensure(c, c->R, R.size() * 8))) {
+    slh_destroy(c);
+    return rc;
+  }
+  if (hipMemcpy(c->Wt.p, Wt.data(), Wt.size() * 2, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(c->psi.p, psi.data(), psi.size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(c->R.p, R.data(), R.size() * 8, hipMemcpyHostToDevice) != hipSuccess) {
+    slh_destroy(c);
+    return SLH_EHIP;
+  }
+  if (hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking) != hipSuccess) {
+    slh_destroy(c);
+    return SLH_EHIP;
+  }
+  *out = c;
+  return SLH_OK;
+}
+
+void slh_destroy(slh_ctx* c) {
+  if (!c) return;
+  drop_graph(c);
+  DevBuf* bufs[] = {&c->Wt, &c->psi, &c->R, &c->q1all, &c->q1act, &c->winlist, &c->route,
+                    &c->nrm2_fm, &c->nrm_x, &c->rowscale, &c->Xb, &c->Phi, &c->Q, &c->T,
+                    &c->U, &c->Z1, &c->Spart, &c->H1part, &c->H1, &c->H2part, &c->H2,
+                    &c->alpha, &c->beta, &c->neff, &c->stop, &c->amax, &c->theta, &c->Seig, &c->Z,
+                    &c->proj, &c->codes, &c->keyA, &c->keyB, &c->valA, &c->valB, &c->tmpi,
+                    &c->segid, &c->segk, &c->sval, &c->sloc, &c->mw, &c->wbase, &c->sseg,
+                    &c->Mtot, &c->part, &c->part_seg, &c->part_cnt, &c->part_nsum,
+                    &c->part_end, &c->rpart, &c->scores};
+  for (DevBuf* b : bufs)
+    if (b->p) (void)hipFree(b->p);
+  if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
+  if (c->ev_made)
+    for (auto& e : c->ev) (void)hipEventDestroy(e);
+  for (auto& e : c->ev_fb) (void)hipEventDestroy(e);
+  for (auto& e : c->ev_fa) (void)hipEventDestroy(e);
+  delete c;
+}
+
+int slh_set_option(slh_ctx* c, int32_t key, double v) {
+  if (!c) return SLH_EINVAL;
+  switch (key) {
+    case SLH_OPT_KERNEL:
+      if (v != 0.0 && v != 1.0) return fail(c, SLH_EINVAL, "KERNEL must be 0 or 1");
+      c->gauss = (int)v;
+      c->norms_of = nullptr;
+      break;
+    case SLH_OPT_WINDOW_LEN: {
+      const int64_t L = (int64_t)v;
+      if ((double)L != v || L < 0) return fail(c, SLH_EINVAL, "WINDOW_LEN must be a non-negative integer");
+      const int64_t Le = L ? L : c->N;
+      if (Le < 2 || c->N % Le != 0) return fail(c, SLH_EINVAL, "N must be a multiple of WINDOW_LEN >= 2");
+      c->L = L;
+      c->n_win = c->N / Le;
+      route_all_spectral(c);
+      c->routed = false;
+      drop_graph(c);
+      break;
+    }
+    case SLH_OPT_POS_MODE:
+      if (v != 0.0 && v != 1.0) return fail(c, SLH_EINVAL, "POS_MODE must be 0 or 1");
+      c->compact = (int)v;
+      break;
+    case SLH_OPT_BREAKDOWN_TOL:
+      if (!(v >= 0.0)) return fail(c, SLH_EINVAL, "BREAKDOWN_TOL must be >= 0");
+      c->tol = v;
+      drop_graph(c);
+      break;
+    case SLH_OPT_TIMING:
+      if (v != 0.0 && v != 1.0) return fail(c, SLH_EINVAL, "TIMING must be 0 or 1");
+      c->timing = (int)v;
+      drop_graph(c);
+      if (c->timing && make_events(c, 0)) return SLH_EHIP;
+      break;
+    default:
+      return fail(c, SLH_EINVAL, "unknown option %d", key);
+  }
+  c->stage = 0;
+  return SLH_OK;
+}
+
+int slh_set_stream(slh_ctx* c, void* s) {
+  if (!c) return SLH_EINVAL;
+  c->stream = (hipStream_t)s;
+  return SLH_OK;
+}
+
+int64_t slh_num_windows(const slh_ctx* c) { return c ? c->n_win : 0; }
+int64_t slh_num_spectral(const slh_ctx* c) { return c ? c->n_act : 0; }
+int64_t slh_merge_capacity(const slh_ctx* c) { return c ? capacity(c) : 0; }
+
+int slh_route(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, double rho, double tau,
+              uint8_t* route_out, double* scores_out) {
+  if (!c) return SLH_EINVAL;
+  int rc = check_x(c, X, dtype, ldx);
+  if (rc) return rc;
+  if (!(rho > 0.0)) return fail(c, SLH_EINVAL, "rho must be > 0");
+  const int64_t L = window_len(c);
+  if ((rc = prep_norms(c, X, dtype, ldx))) return rc;
+  ENSURE(c, c->rpart, (size_t)c->n_win * ((c->D + 1023) / 1024) * 2 * sizeof(double));
+  ENSURE(c, c->scores, (size_t)c->n_win * sizeof(double));
+  HIP_TRY(c, launch_route_scores(X, dtype == SLH_BF16 ? 0 : 1, ldx, P<double>(c->nrm_x),
+                                 (int)c->n_win, (int)L, (int)c->D, P<double>(c->rpart),
+                                 P<double>(c->scores), c->stream));
+  std::vector<double> sc((size_t)c->n_win);
+  HIP_TRY(c, hipMemcpyAsync(sc.data(), c->scores.p, sc.size() * sizeof(double),
+                            hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  // tau(rho): 0.70 at rho <= 2, linear in log2(rho) through 0.60 at 8 and 0.55 at 16
+  double t = tau;
+  if (!(tau >= 0.0)) {
+    const double l2 = std::log2(rho);
+    if (rho <= 2.0) t = 0.70;
+    else if (rho <= 8.0) t = 0.70 - 0.05 * (l2 - 1.0);
+    else if (rho < 16.0) t = 0.60 - 0.05 * (l2 - 3.0);
+    else t = 0.55;
+  }
+  c->route_h.assign((size_t)c->n_win, 0);
+  c->winlist_h.clear();
+  for (int64_t w = 0; w < c->n_win; ++w) {
+    bool spectral;
+    if (rho >= 16.0) spectral = true;
+    else if (L <= 4) spectral = false;
+    else spectral = sc[(size_t)w] >= t;
+    c->route_h[(size_t)w] = spectral ? 1 : 0;
+    if (spectral) c->winlist_h.push_back((int)w);
+  }
+  c->n_act = (int)c->winlist_h.size();
+  c->chunk_k = std::max(1, (int)std::nearbyint(rho));   // round half to even
+  c->routed = true;
+  c->routing_on_device = false;
+  drop_graph(c);
+  if ((rc = upload_routing(c))) return rc;
+  if (route_out) std::memcpy(route_out, c->route_h.data(), c->route_h.size());
+  if (scores_out) std::memcpy(scores_out, sc.data(), sc.size() * sizeof(double));
+  c->stage = 0;
+  return SLH_OK;
+}
+
+int slh_feature_map(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx) {
+  if (!c) return SLH_EINVAL;
+  int rc = check_x(c, X, dtype, ldx);
+  if (rc) return rc;
+  if ((rc = ensure_routing(c))) return rc;
+  if (c->norms_of != X || dtype == SLH_F32)
+    if ((rc = prep_norms(c, X, dtype, ldx))) return rc;
+  const int64_t L = window_len(c);
+  const int64_t rows = (int64_t)c->n_act * L;
+  ENSURE(c, c->Phi, (size_t)std::max<int64_t>(rows, 1) * c->m * sizeof(float));
+  FeatmapArgs a;
+  a.X = dtype == SLH_F32 ? P<uint16_t>(c->Xb) : (const uint16_t*)X;
+  a.ldx = dtype == SLH_F32 ? c->D : ldx;
+  a.Wt = P<uint16_t>(c->Wt);
+  a.psi = P<float>(c->psi);
+  a.rowscale = P<float>(c->rowscale);
+  a.Phi = P<float>(c->Phi);
+  a.winlist = (c->n_act == c->n_win) ? nullptr : P<int>(c->winlist);
+  a.n_rows = rows;
+  a.L = L;
+  a.D = (int)c->D;
+  a.m = (int)c->m;
+  if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[0], c->stream));
+  HIP_TRY(c, launch_featmap(a, c->stream));
+  if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[1], c->stream));
+  c->stage = 1;
+  return SLH_OK;
+}
+
+int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) {
+  if (!c) return SLH_EINVAL;
+  if (c->stage < 1) return fail(c, SLH_ESTATE, "slh_lanczos before slh_feature_map");
+  const int64_t L = window_len(c);
+  if (n_it < c->r || n_it > std::min<int64_t>(L, 256))
+    return fail(c, SLH_EINVAL, "need r <= n_it <= min(L, 256) (n_it=%d, r=%d, L=%lld)", n_it,
+                c->r, (long long)L);
+  const int na = c->n_act;
+  c->n_it = n_it;
+  if (na > 0) {
+    // start vectors of the spectral windows
+    if (c->q1_L != L) {
+      ENSURE(c, c->q1all, (size_t)c->N * sizeof(double));
+      std::vector<double> q((size_t)c->N);
+      for (int64_t w = 0; w < c->n_win; ++w) slh_gen_start(c->seed, w, L, q.data() + w * L);
+      HIP_TRY(c, hipMemcpy(c->q1all.p, q.data(), q.size() * sizeof(double), hipMemcpyHostToDevice));
+      c->q1_L = L;
+    }
+    const double* q1act = P<double>(c->q1all);
+    if (na != c->n_win) {
+      ENSURE(c, c->q1act, (size_t)na * L * sizeof(double));
+      for (int a = 0; a < na; ++a)
+        HIP_TRY(c, hipMemcpyAsync(P<double>(c->q1act) + (int64_t)a * L,
+                                  P<double>(c->q1all) + (int64_t)c->winlist_h[(size_t)a] * L,
+                                  L * sizeof(double), hipMemcpyDeviceToDevice, c->stream));
+      q1act = P<double>(c->q1act);
+    }
+    LanczosWS w;
+    w.n_act = na;
+    w.L = (int)L;
+    w.m = (int)c->m;
+    w.n_it = n_it;
+    w.ldq = n_it + 1;
+    w.tol = c->tol;
+    {
+      // rows per thread (8..32, a multiple of 8): aim for about two blocks per CU over all
+      // windows; fewer rows per block only multiply the partial sums of Phi^T v
+      const int rp = 512 / lanczos_m4((int)c->m);
+      const int64_t per_win = std::max<int64_t>(1, (int64_t)2 * c->n_cu / na);
+      int64_t rpt = (L + rp * per_win - 1) / (rp * per_win);
+      rpt = ((rpt + 7) / 8) * 8;
+      rpt = std::max<int64_t>(8, std::min<int64_t>(rpt, 32));
+      w.RPT = (int)rpt;
+      w.RB1 = rp * w.RPT;
+      w.G1 = (int)((L + w.RB1 - 1) / w.RB1);
+    }
+    w.G3 = (int)std::max<int64_t>(1, std::min<int64_t>(64, (L + 127) / 128));
+    w.RB3 = (int)((L + w.G3 - 1) / w.G3);
+    const size_t hs = (size_t)w.ldq + 1;
+    ENSURE(c, c->Q, (size_t)na * w.ldq * L * 8);
+    ENSURE(c, c->T, (size_t)na * w.ldq * c->m * 8);
+    ENSURE(c, c->U, (size_t)na * L * 8);
+    ENSURE(c, c->Z1, (size_t)na * L * 8);
+    ENSURE(c, c->Spart, (size_t)na * w.G1 * c->m * 8);
+    ENSURE(c, c->H1part, (size_t)na * w.G1 * hs * 8);
+    ENSURE(c, c->H1, (size_t)na * hs * 8);
+    ENSURE(c, c->H2part, (size_t)na * w.G3 * hs * 8);
+    ENSURE(c, c->H2, (size_t)na * hs * 8);
+    ENSURE(c, c->alpha, (size_t)na * n_it * 8);
+    ENSURE(c, c->beta, (size_t)na * n_it * 8);
+    ENSURE(c, c->neff, (size_t)na * 4);
+    ENSURE(c, c->stop, (size_t)na * 4);
+    ENSURE(c, c->amax, (size_t)na * 8);
+    ENSURE(c, c->theta, (size_t)na * c->r * 8);
+    ENSURE(c, c->Seig, (size_t)na * n_it * c->r * 8);
+    ENSURE(c, c->Z, (size_t)na * L * c->r * 8);
+    w.Phi = P<float>(c->Phi);
+    w.Q = P<double>(c->Q);
+    w.T = P<double>(c->T);
+    w.U = P<double>(c->U);
+    w.Z1 = P<double>(c->Z1);
+    w.Spart = P<double>(c->Spart);
+    w.H1part = P<double>(c->H1part);
+    w.H1 = P<double>(c->H1);
+    w.H2part = P<double>(c->H2part);
+    w.H2 = P<double>(c->H2);
+    w.alpha = P<double>(c->alpha);
+    w.beta = P<double>(c->beta);
+    w.neff = P<int>(c->neff);
+    w.stop = P<int>(c->stop);
+    w.amax = P<double>(c->amax);
+    if (c->timing) {
+      // timing: launch the step sequence directly so that every pass over Phi
+      // can be bracketed by events (events inside a captured graph cannot be timed)
+      int rc_ev = make_events(c, 2 * n_it);
+      if (rc_ev) return rc_ev;
+      HIP_TRY(c, hipEventRecord(c->ev[2], c->stream));
+      HIP_TRY(c, launch_lanczos(w, q1act, c->stream, c->ev_fb.data(), c->ev_fa.data()));
+    } else {
+      // the step sequence is captured once per configuration and replayed as a graph
+      std::string key((const char*)&w, sizeof w);
+      key.append((const char*)&q1act, sizeof q1act);
+      if (!c->lz_exec || c->lz_key != key) {
+        drop_graph(c);
+        hipGraph_t g = nullptr;
+        HIP_TRY(c, hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal));
+        hipError_t le = launch_lanczos(w, q1act, c->cap_stream);
+        hipError_t ee = hipStreamEndCapture(c->cap_stream, &g);
+        if (le != hipSuccess || ee != hipSuccess) {
+          if (g) (void)hipGraphDestroy(g);
+          return fail(c, SLH_EHIP, "Lanczos graph capture: %s / %s", hipGetErrorString(le),
+                      hipGetErrorString(ee));
+        }
+        hipError_t ie = hipGraphInstantiate(&c->lz_exec, g, nullptr, nullptr, 0);
+        (void)hipGraphDestroy(g);
+        if (ie != hipSuccess) {
+          c->lz_exec = nullptr;
+          return fail(c, SLH_EHIP, "hipGraphInstantiate: %s", hipGetErrorString(ie));
+        }
+        c->lz_key = key;
+      }
+      HIP_TRY(c, hipGraphLaunch(c->lz_exec, c->stream));
+    }
+    if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[3], c->stream));
+    c->fused_timed = c->timing ? 2 * n_it : 0;
+    HIP_TRY(c, launch_tridiag_eig(w.alpha, w.beta, w.neff, na, n_it, c->r, P<double>(c->theta),
+                                  P<double>(c->Seig), c->stream));
+    HIP_TRY(c, launch_ritz(w.Q, P<double>(c->Seig), w.neff, na, (int)L, w.ldq, n_it, c->r,
+                           P<double>(c->Z), c->stream));
+    if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[4], c->stream));
+  }
+  if ((ritz_out || iters_out) && na > 0) {
+    if (ritz_out)
+      HIP_TRY(c, hipMemcpyAsync(ritz_out, c->theta.p, (size_t)na * c->r * 8, hipMemcpyDeviceToHost,
+                                c->stream));
+    if (iters_out)
+      HIP_TRY(c, hipMemcpyAsync(iters_out, c->neff.p, (size_t)na * 4, hipMemcpyDeviceToHost,
+                                c->stream));
+    HIP_TRY(c, hipStreamSynchronize(c->stream));
+  }
+  c->stage = 2;
+  return SLH_OK;
+}
+
+int slh_simhash(slh_ctx* c, uint32_t* codes_out) {
+  if (!c) return SLH_EINVAL;
+  if (c->stage < 2) return fail(c, SLH_ESTATE, "slh_simhash before slh_lanczos");
+  const int64_t L = window_len(c);
+  const int na = c->n_act;
+  ENSURE(c, c->codes, (size_t)c->N * 4);
+  ENSURE(c, c->proj, (size_t)std::max(na, 1) * L * c->bits * 8);
+  if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[5], c->stream));
+  if (na != c->n_win) HIP_TRY(c, launch_fill_u32(P<uint32_t>(c->codes), c->N, 0xFFFFFFFFu, c->stream));
+  if (na > 0)
+    HIP_TRY(c, launch_simhash(P<double>(c->Z), P<double>(c->R),
+                              na == c->n_win ? nullptr : P<int>(c->winlist), na, (int)L, c->r,
+                              c->bits, P<uint32_t>(c->codes), P<double>(c->proj), c->stream));
+  if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[6], c->stream));
+  if (codes_out)
+    HIP_TRY(c, hipMemcpyAsync(codes_out, c->codes.p, (size_t)c->N * 4, hipMemcpyDeviceToDevice,
+                              c->stream));
+  c->stage = 3;
+  return SLH_OK;
+}
+
+int slh_merge(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, float* emb_out,
+              int32_t* pos_out, int32_t* tok2macro_out, int64_t cap, int64_t* M_out) {
+  if (!c) return SLH_EINVAL;
+  if (c->stage < 3) return fail(c, SLH_ESTATE, "slh_merge before slh_simhash");
+  int rc = check_x(c, X, dtype, ldx);
+  if (rc) return rc;
+  if (!emb_out || !pos_out || !M_out) return fail(c, SLH_EINVAL, "NULL output");
+  const int64_t need = capacity(c);
+  if (cap < need) return fail(c, SLH_EINVAL, "cap %lld < required %lld", (long long)cap, (long long)need);
+  if (c->norms_of != X)
+    if ((rc = prep_norms(c, X, dtype, ldx))) return rc;
+  const int64_t L = window_len(c);
+  const int64_t N = c->N;
+  const int CH = 32;
+  const int nch = merge_nchunks(N, CH);
+  ENSURE(c, c->keyA, N * 4);
+  ENSURE(c, c->keyB, N * 4);
+  ENSURE(c, c->valA, N * 4);
+  ENSURE(c, c->valB, N * 4);
+  ENSURE(c, c->tmpi, N * 4);
+  ENSURE(c, c->segid, N * 4);
+  ENSURE(c, c->segk, N * 4);
+  ENSURE(c, c->sval, N * 4);
+  ENSURE(c, c->sloc, N * 4);
+  ENSURE(c, c->sseg, N * 4);
+  ENSURE(c, c->mw, c->n_win * 4);
+  ENSURE(c, c->wbase, (c->n_win + 1) * 4);
+  ENSURE(c, c->Mtot, 4);
+  ENSURE(c, c->part, (size_t)2 * nch * c->D * 4);
+  ENSURE(c, c->part_seg, (size_t)2 * nch * 4);
+  ENSURE(c, c->part_cnt, (size_t)2 * nch * 4);
+  ENSURE(c, c->part_nsum, (size_t)2 * nch * 8);
+  ENSURE(c, c->part_end, (size_t)2 * nch * 4);
+  ENSURE(c, c->codes, (size_t)N * 4);
+  if ((rc = ensure_routing(c))) return rc;
+  MergeWS w;
+  w.n_win = (int)c->n_win;
+  w.L = (int)L;
+  w.bits = c->bits;
+  w.chunk_k = c->chunk_k;
+  w.compact = c->compact;
+  w.D = (int)c->D;
+  w.N = N;
+  w.route = P<uint8_t>(c->route);
+  w.codes = P<uint32_t>(c->codes);
+  w.nrm_x = P<double>(c->nrm_x);
+  w.keyA = P<uint32_t>(c->keyA);
+  w.keyB = P<uint32_t>(c->keyB);
+  w.valA = P<int>(c->valA);
+  w.valB = P<int>(c->valB);
+  w.tmpi = P<int>(c->tmpi);
+  w.segid = P<int>(c->segid);
+  w.segk = P<int>(c->segk);
+  w.sval = P<int>(c->sval);
+  w.sloc = P<int>(c->sloc);
+  w.mw = P<int>(c->mw);
+  w.wbase = P<int>(c->wbase);
+  w.sseg = P<int>(c->sseg);
+  w.Mtot = P<int>(c->Mtot);
+  w.part = P<float>(c->part);
+  w.part_seg = P<int>(c->part_seg);
+  w.part_cnt = P<int>(c->part_cnt);
+  w.part_nsum = P<double>(c->part_nsum);
+  w.part_end = P<int>(c->part_end);
+  w.CH = CH;
+  if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[7], c->stream));
+  HIP_TRY(c, launch_merge(w, X, dtype == SLH_BF16 ? 0 : 1, ldx, emb_out, pos_out, tok2macro_out,
+                          c->stream));
+  if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[8], c->stream));
+  int M = 0;
+  HIP_TRY(c, hipMemcpyAsync(&M, c->Mtot.p, 4, hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  *M_out = M;
+  return SLH_OK;
+}
+
+int slh_stage_times(slh_ctx* c, double* out, int32_t n) {
+  if (!c || !out || n < 0) return SLH_EINVAL;
+  if (!c->timing || !c->ev_made) return fail(c, SLH_ESTATE, "SLH_OPT_TIMING is off");
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  double v[7] = {0, 0, 0, 0, 0, 0, 0};
+  float ms = 0.f;
+  auto el = [&](hipEvent_t a, hipEvent_t b) -> double {
+    float t = 0.f;
+    return hipEventElapsedTime(&t, a, b) == hipSuccess ? (double)t : -1.0;
+  };
+  v[0] = el(c->ev[0], c->ev[1]);
+  v[1] = el(c->ev[2], c->ev[3]);
+  for (int j = 0; j < c->fused_timed; ++j) {
+    ms = (float)el(c->ev_fb[(size_t)j], c->ev_fa[(size_t)j]);
+    v[2] += ms;
+  }
+  v[3] = c->fused_timed;
+  v[4] = el(c->ev[3], c->ev[4]);
+  v[5] = el(c->ev[5], c->ev[6]);
+  v[6] = el(c->ev[7], c->ev[8]);
+  for (int i = 0; i < n && i < 7; ++i) out[i] = v[i];
+  (void)hipGetLastError();   // a stage that did not run leaves unrecorded events
+  return SLH_OK;
+}
+
+int slh_load(slh_ctx* c, int32_t which, const void* src, int64_t bytes) {
+  if (!c || !src) return SLH_EINVAL;
+  const int64_t L = window_len(c);
+  const int64_t na = c->n_act;
+  int rc = ensure_routing(c);
+  if (rc) return rc;
+  if (which == SLH_OUT_PHI) {
+    const int64_t want = na * L * c->m * 4;
+    if (bytes != want) return fail(c, SLH_EINVAL, "bytes must be %lld", (long long)want);
+    ENSURE(c, c->Phi, (size_t)std::max<int64_t>(want, 4));
+    if (want) HIP_TRY(c, hipMemcpyAsync(c->Phi.p, src, (size_t)want, hipMemcpyDeviceToDevice, c->stream));
+    c->stage = 1;
+    return SLH_OK;
+  }
+  if (which == SLH_OUT_CODES) {
+    const int64_t want = c->N * 4;
+    if (bytes != want) return fail(c, SLH_EINVAL, "bytes must be %lld", (long long)want);
+    ENSURE(c, c->codes, (size_t)want);
+    HIP_TRY(c, hipMemcpyAsync(c->codes.p, src, (size_t)want, hipMemcpyDeviceToDevice, c->stream));
+    c->stage = 3;
+    return SLH_OK;
+  }
+  return fail(c, SLH_EINVAL, "slh_load supports SLH_OUT_PHI and SLH_OUT_CODES");
+}
+
+int slh_copy_out(slh_ctx* c, int32_t which, void* dst, int64_t bytes) {
+  if (!c || !dst) return SLH_EINVAL;
+  const int64_t L = window_len(c);
+  const int64_t na = c->n_act;
+  const DevBuf* b = nullptr;
+  int64_t want = 0;
+  switch (which) {
+    case SLH_OUT_PHI: b = &c->Phi; want = na * L * c->m * 4; break;
+    case SLH_OUT_ALPHA: b = &c->alpha; want = na * c->n_it * 8; break;
+    case SLH_OUT_BETA: b = &c->beta; want = na * c->n_it * 8; break;
+    case SLH_OUT_Z: b = &c->Z; want = na * L * c->r * 8; break;
+    case SLH_OUT_PROJ: b = &c->proj; want = na * L * c->bits * 8; break;
+    case SLH_OUT_CODES: b = &c->codes; want = c->N * 4; break;
+    case SLH_OUT_THETA: b = &c->theta; want = na * c->r * 8; break;
+    case SLH_OUT_Q: b = &c->Q; want = na * (c->n_it + 1) * L * 8; break;
+    case SLH_OUT_WINDOWS:
+      if (bytes != na * 4) return fail(c, SLH_EINVAL, "bytes must be %lld", (long long)(na * 4));
+      if (na) std::memcpy(dst, c->winlist_h.data(), (size_t)na * 4);
+      return SLH_OK;
+    default: return fail(c, SLH_EINVAL, "unknown output %d", which);
+  }
+  if (bytes != want) return fail(c, SLH_EINVAL, "bytes must be %lld", (long long)want);
+  if (want == 0) return SLH_OK;
+  if (!b->p || (int64_t)b->bytes < want) return fail(c, SLH_ESTATE, "output %d not computed", which);
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  HIP_TRY(c, hipMemcpy(dst, b->p, (size_t)want, hipMemcpyDeviceToHost));
+  return SLH_OK;
+}
+
+}  // extern "C"

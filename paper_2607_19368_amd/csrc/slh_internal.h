@@ -1,0 +1,107 @@
+// Internal launcher declarations shared by the host library and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace slh {
+
+// ---- preparation (k_prep.hip) ----
+// Row norms of X: nrm2_fm[i] = |bf16(x_i)|^2 and nrm_x[i] = |x_i| (X as given),
+// both accumulated in fp64, and rowscale[i] = fp32(s_i * sqrt(2/m)) with
+// s_i = exp(nrm2_fm[i] / (2 sqrt(D))) (or 1 for the Gaussian map).
+// For fp32 X it also writes the bf16 copy Xb (row stride D).
+hipError_t launch_rownorm(const void* X, int dtype, int64_t ldx, int64_t N, int D, int m,
+                          int gauss, double* nrm2_fm, double* nrm_x, float* rowscale,
+                          uint16_t* Xb, hipStream_t s);
+
+// ---- feature map (k_featmap.hip) ----
+struct FeatmapArgs {
+  const uint16_t* X;      // bf16 rows, global token index, row stride ldx
+  int64_t ldx;
+  const uint16_t* Wt;     // [m][D] bf16 (transposed projection)
+  const float* psi;       // [m]
+  const float* rowscale;  // [N] global token index
+  float* Phi;             // [n_rows][m]
+  const int* winlist;     // active window -> window index (n_rows / L entries)
+  int64_t n_rows;         // n_act * L
+  int64_t L;
+  int D, m;
+};
+hipError_t launch_featmap(const FeatmapArgs& a, hipStream_t s);
+
+// ---- Lanczos (k_lanczos.hip) ----
+struct LanczosWS {
+  int n_act, L, m, n_it, ldq;   // ldq = n_it + 1 vectors per window
+  const float* Phi;             // [n_act][L][m]
+  double* Q;                    // [n_act][ldq][L]  Lanczos basis, vector-major
+  double* T;                    // [n_act][ldq][m]  t_k = Phi^T q_k
+  double* U;                    // [n_act][L]       u = Phi t_j
+  double* Z1;                   // [n_act][L]       after the first Gram-Schmidt pass
+  double* Spart;                // [n_act][G1][m]   partials of t_j
+  double* H1part;               // [n_act][G1][ldq+1]
+  double* H1;                   // [n_act][ldq+1]   Q_j^T u
+  double* H2part;               // [n_act][G3][ldq+1] (slot ldq: |z1|^2)
+  double* H2;                   // [n_act][ldq+1]   Q_j^T z1 and |z1|^2
+  double* alpha;                // [n_act][n_it]
+  double* beta;                 // [n_act][n_it]
+  int* neff;                    // [n_act]  steps done
+  int* stop;                    // [n_act]  1 after breakdown
+  double* amax;                 // [n_act]  max |alpha| so far (breakdown scale)
+  double tol;
+  int G1, RB1, RPT;             // Phi-pass row blocks: RB1 = (512 / M4) * RPT rows, RPT in {8,16,24,32}
+  int G3, RB3;                  // orthogonalisation row blocks
+};
+int lanczos_m4(int m);   // threads per Phi row in the passes (power of two >= m / 4)
+// ev_before/ev_after (may be NULL): 2 * n_it events each, recorded around the
+// two Phi passes of every step (index 2j: Phi^T q_j, 2j + 1: Phi t_j).
+hipError_t launch_lanczos(const LanczosWS& w, const double* q1_act, hipStream_t s,
+                          const hipEvent_t* ev_before = nullptr,
+                          const hipEvent_t* ev_after = nullptr);
+
+// ---- eigensolve + Ritz + SimHash (k_eig.hip, k_hash.hip) ----
+hipError_t launch_tridiag_eig(const double* alpha, const double* beta, const int* neff,
+                              int n_act, int n_it, int r, double* theta, double* Seig,
+                              hipStream_t s);
+hipError_t launch_ritz(const double* Q, const double* Seig, const int* neff, int n_act,
+                       int L, int ldq, int n_it, int r, double* Z, hipStream_t s);
+hipError_t launch_simhash(const double* Z, const double* R, const int* winlist, int n_act,
+                          int L, int r, int bits, uint32_t* codes, double* proj,
+                          hipStream_t s);
+
+hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
+
+// ---- merge (k_merge.hip) ----
+struct MergeWS {
+  int n_win, L, bits, chunk_k, compact, D;
+  int64_t N;
+  const uint8_t* route;         // [n_win] 1 = spectral (device)
+  const uint32_t* codes;        // [N]
+  const double* nrm_x;          // [N]
+  uint32_t* keyA; uint32_t* keyB;  // [N] radix-sort keys
+  int* valA; int* valB;            // [N] radix-sort values (token index)
+  int* tmpi;                    // [N] representative flags / ranks (token order)
+  int* segid;                   // [N] bucket ordinal per sorted position
+  int* segk;                    // [N] bucket ordinal -> window-local macro rank
+  int* sval;                    // [N] member token per sorted position
+  int* sloc;                    // [N] window-local macro rank per sorted position
+  int* mw;                      // [n_win] macro count per window
+  int* wbase;                   // [n_win + 1] first global macro index per window
+  int* sseg;                    // [N] global macro index per sorted position
+  int* Mtot;                    // [1]
+  float* part;                  // [2 * nchunks][D] partial sums of cut buckets
+  int* part_seg;                // [2 * nchunks] macro of the slot, -1 if unused
+  int* part_cnt;                // [2 * nchunks]
+  double* part_nsum;            // [2 * nchunks] sum of member norms
+  int* part_end;                // [2 * nchunks] 1 if the bucket ends in this slot
+  int CH;                       // sorted positions per reduction chunk (<= 64)
+};
+int merge_nchunks(int64_t N, int CH);
+hipError_t launch_merge(const MergeWS& w, const void* X, int dtype, int64_t ldx,
+                        float* E, int* P, int* tok2macro, hipStream_t s);
+
+// ---- adaptive routing (k_route.hip) ----
+hipError_t launch_route_scores(const void* X, int dtype, int64_t ldx, const double* nrm_x,
+                               int n_win, int L, int D, double* part, double* scores,
+                               hipStream_t s);
+
+}  // namespace slh

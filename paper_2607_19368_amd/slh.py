@@ -1,0 +1,271 @@
+"""Python binding of libslh.so (include/slh.h): argument marshalling only.
+
+Every function keeps the C name and takes torch tensors for device buffers
+(PyTorch supplies device memory and the stream); all computation runs in the
+library's HIP kernels.  There is no fallback: if the library is not built or
+cannot be loaded, every call raises.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libslh.so")
+
+SLH_OK, SLH_EINVAL, SLH_ENOMEM, SLH_EHIP, SLH_ESTATE = 0, -1, -2, -3, -4
+SLH_BF16, SLH_F32 = 0, 1
+SLH_OPT_KERNEL, SLH_OPT_WINDOW_LEN, SLH_OPT_POS_MODE, SLH_OPT_BREAKDOWN_TOL, SLH_OPT_TIMING = 1, 2, 3, 4, 5
+SLH_OUT_PHI, SLH_OUT_ALPHA, SLH_OUT_BETA, SLH_OUT_Z = 1, 2, 3, 4
+SLH_OUT_PROJ, SLH_OUT_CODES, SLH_OUT_THETA, SLH_OUT_Q, SLH_OUT_WINDOWS = 5, 6, 7, 8, 9
+
+EXPORTS = [
+    "slh_gen_params", "slh_gen_start", "slh_create", "slh_destroy", "slh_last_error",
+    "slh_set_option", "slh_set_stream", "slh_route", "slh_feature_map", "slh_lanczos",
+    "slh_simhash", "slh_merge", "slh_merge_capacity", "slh_copy_out", "slh_num_windows",
+    "slh_num_spectral", "slh_load", "slh_stage_times",
+]
+
+_lib = None
+
+
+class SLHError(RuntimeError):
+    pass
+
+
+def load():
+    """Load libslh.so (raises if it is missing)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise SLHError(f"{LIB_PATH} is not built; run `python -m paper_2607_19368_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, u64, dp = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_void_p
+    sig = {
+        "slh_gen_params": (i32, [u64, i64, i64, i32, i32, vp, vp, vp]),
+        "slh_gen_start": (i32, [u64, i64, i64, vp]),
+        "slh_create": (i32, [ctypes.POINTER(vp), i64, i64, i64, i32, i32, u64]),
+        "slh_destroy": (None, [vp]),
+        "slh_last_error": (ctypes.c_char_p, [vp]),
+        "slh_set_option": (i32, [vp, i32, ctypes.c_double]),
+        "slh_set_stream": (i32, [vp, vp]),
+        "slh_route": (i32, [vp, vp, i32, i64, ctypes.c_double, ctypes.c_double, vp, vp]),
+        "slh_feature_map": (i32, [vp, vp, i32, i64]),
+        "slh_lanczos": (i32, [vp, i32, vp, vp]),
+        "slh_simhash": (i32, [vp, vp]),
+        "slh_merge": (i32, [vp, vp, i32, i64, vp, vp, vp, i64, vp]),
+        "slh_merge_capacity": (i64, [vp]),
+        "slh_copy_out": (i32, [vp, i32, vp, i64]),
+        "slh_num_windows": (i64, [vp]),
+        "slh_num_spectral": (i64, [vp]),
+        "slh_load": (i32, [vp, i32, vp, i64]),
+        "slh_stage_times": (i32, [vp, vp, i32]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = L
+    return L
+
+
+def _check(ctx, rc, what):
+    if rc != SLH_OK:
+        msg = load().slh_last_error(ctx.handle if ctx is not None else None)
+        raise SLHError(f"{what} failed ({rc}): {msg.decode() if msg else ''}")
+
+
+def _ptr(a):
+    return ctypes.c_void_p(a.ctypes.data) if isinstance(a, np.ndarray) else ctypes.c_void_p(a)
+
+
+def _xinfo(X):
+    import torch
+    if X.dim() != 2 or X.stride(1) != 1:
+        raise SLHError("X must be a 2-D tensor with unit column stride")
+    if X.dtype == torch.bfloat16:
+        dt = SLH_BF16
+    elif X.dtype == torch.float32:
+        dt = SLH_F32
+    else:
+        raise SLHError(f"unsupported X dtype {X.dtype}")
+    if not X.is_cuda:
+        raise SLHError("X must be a device tensor")
+    return ctypes.c_void_p(X.data_ptr()), dt, X.stride(0)
+
+
+class Ctx:
+    """Owns one slh_ctx handle."""
+
+    def __init__(self, handle, N, D, m, r, bits):
+        self.handle = handle
+        self.N, self.D, self.m, self.r, self.bits = N, D, m, r, bits
+        self.n_it = 0
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib is not None:
+            _lib.slh_destroy(self.handle)
+            self.handle = None
+
+    @property
+    def n_windows(self):
+        return int(load().slh_num_windows(self.handle))
+
+    @property
+    def n_spectral(self):
+        return int(load().slh_num_spectral(self.handle))
+
+    @property
+    def window_len(self):
+        return self.N // self.n_windows
+
+
+# ---------------------------------------------------------------- host-only calls
+def slh_gen_params(seed, D, m, r, bits):
+    """(W bf16 bits [D, m] uint16, psi [m] float32, R [r, bits] float64)."""
+    W = np.empty((D, m), np.uint16)
+    psi = np.empty(m, np.float32)
+    R = np.empty((r, bits), np.float64)
+    rc = load().slh_gen_params(seed, D, m, r, bits, _ptr(W), _ptr(psi), _ptr(R))
+    if rc != SLH_OK:
+        raise SLHError(f"slh_gen_params failed ({rc})")
+    return W, psi, R
+
+
+def slh_gen_start(seed, window, n):
+    q = np.empty(n, np.float64)
+    rc = load().slh_gen_start(seed, window, n, _ptr(q))
+    if rc != SLH_OK:
+        raise SLHError(f"slh_gen_start failed ({rc})")
+    return q
+
+
+# ---------------------------------------------------------------- context calls
+def slh_create(N, D, m, r, bits, seed=0):
+    h = ctypes.c_void_p()
+    rc = load().slh_create(ctypes.byref(h), N, D, m, r, bits, seed)
+    if rc != SLH_OK:
+        raise SLHError(f"slh_create(N={N}, D={D}, m={m}, r={r}, bits={bits}) failed ({rc})")
+    ctx = Ctx(h, N, D, m, r, bits)
+    slh_set_stream(ctx)
+    return ctx
+
+
+def slh_set_option(ctx, key, value):
+    _check(ctx, load().slh_set_option(ctx.handle, key, float(value)), "slh_set_option")
+
+
+def slh_set_stream(ctx, stream=None):
+    """Use `stream` (a torch.cuda.Stream; default: torch's current stream)."""
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    _check(ctx, load().slh_set_stream(ctx.handle, ctypes.c_void_p(stream.cuda_stream)), "slh_set_stream")
+
+
+def slh_route(ctx, X, rho, tau=-1.0):
+    p, dt, ld = _xinfo(X)
+    nw = ctx.n_windows
+    route = np.empty(nw, np.uint8)
+    scores = np.empty(nw, np.float64)
+    _check(ctx, load().slh_route(ctx.handle, p, dt, ld, float(rho), float(tau), _ptr(route), _ptr(scores)),
+           "slh_route")
+    return route, scores
+
+
+def slh_feature_map(ctx, X):
+    p, dt, ld = _xinfo(X)
+    _check(ctx, load().slh_feature_map(ctx.handle, p, dt, ld), "slh_feature_map")
+
+
+def slh_lanczos(ctx, n_it, want=True):
+    """Runs n_it steps; returns (ritz [n_spectral, r], iters [n_spectral]) or None."""
+    ctx.n_it = n_it
+    na = ctx.n_spectral
+    if want:
+        ritz = np.zeros((na, ctx.r), np.float64)
+        iters = np.zeros(na, np.int32)
+        _check(ctx, load().slh_lanczos(ctx.handle, n_it, _ptr(ritz), _ptr(iters)), "slh_lanczos")
+        return ritz, iters
+    _check(ctx, load().slh_lanczos(ctx.handle, n_it, None, None), "slh_lanczos")
+    return None
+
+
+def slh_simhash(ctx, codes_out=None):
+    p = ctypes.c_void_p(codes_out.data_ptr()) if codes_out is not None else None
+    _check(ctx, load().slh_simhash(ctx.handle, p), "slh_simhash")
+    return codes_out
+
+
+def slh_merge_capacity(ctx):
+    return int(load().slh_merge_capacity(ctx.handle))
+
+
+def slh_merge(ctx, X, emb_out=None, pos_out=None, tok2macro_out=None):
+    """Returns (E [M, D] float32, P [M] int32, tok2macro [N] int32, M) as device tensors
+    (views of the given or newly allocated outputs)."""
+    import torch
+    p, dt, ld = _xinfo(X)
+    cap = slh_merge_capacity(ctx)
+    if emb_out is None:
+        emb_out = torch.empty((cap, ctx.D), dtype=torch.float32, device=X.device)
+    if pos_out is None:
+        pos_out = torch.empty(cap, dtype=torch.int32, device=X.device)
+    if tok2macro_out is None:
+        tok2macro_out = torch.empty(ctx.N, dtype=torch.int32, device=X.device)
+    M = ctypes.c_int64(0)
+    _check(ctx, load().slh_merge(ctx.handle, p, dt, ld, ctypes.c_void_p(emb_out.data_ptr()),
+                                 ctypes.c_void_p(pos_out.data_ptr()),
+                                 ctypes.c_void_p(tok2macro_out.data_ptr()), emb_out.shape[0],
+                                 ctypes.byref(M)), "slh_merge")
+    m = int(M.value)
+    return emb_out[:m], pos_out[:m], tok2macro_out, m
+
+
+_OUT = {
+    SLH_OUT_PHI: (np.float32, lambda c: (c.n_spectral, c.window_len, c.m)),
+    SLH_OUT_ALPHA: (np.float64, lambda c: (c.n_spectral, c.n_it)),
+    SLH_OUT_BETA: (np.float64, lambda c: (c.n_spectral, c.n_it)),
+    SLH_OUT_Z: (np.float64, lambda c: (c.n_spectral, c.window_len, c.r)),
+    SLH_OUT_PROJ: (np.float64, lambda c: (c.n_spectral, c.window_len, c.bits)),
+    SLH_OUT_CODES: (np.uint32, lambda c: (c.N,)),
+    SLH_OUT_THETA: (np.float64, lambda c: (c.n_spectral, c.r)),
+    SLH_OUT_Q: (np.float64, lambda c: (c.n_spectral, c.n_it + 1, c.window_len)),
+    SLH_OUT_WINDOWS: (np.int32, lambda c: (c.n_spectral,)),
+}
+
+
+STAGE_NAMES = ["featmap_ms", "lanczos_ms", "phi_pass_ms_sum", "phi_pass_count", "eig_ritz_ms",
+               "simhash_ms", "merge_ms"]
+
+
+def slh_stage_times(ctx):
+    """Dict of the stage timings recorded with SLH_OPT_TIMING = 1."""
+    out = np.zeros(len(STAGE_NAMES), np.float64)
+    _check(ctx, load().slh_stage_times(ctx.handle, _ptr(out), len(out)), "slh_stage_times")
+    return dict(zip(STAGE_NAMES, out.tolist()))
+
+
+def slh_load(ctx, which, src):
+    """Replace the Phi (SLH_OUT_PHI) or codes (SLH_OUT_CODES) stage result with a device tensor."""
+    nbytes = src.numel() * src.element_size()
+    _check(ctx, load().slh_load(ctx.handle, which, ctypes.c_void_p(src.data_ptr()), nbytes), "slh_load")
+
+
+def slh_copy_out(ctx, which):
+    dt, shape = _OUT[which]
+    a = np.empty(shape(ctx), dt)
+    _check(ctx, load().slh_copy_out(ctx.handle, which, _ptr(a), a.nbytes), "slh_copy_out")
+    return a
+
+
+def compress(ctx, X, n_it, rho=None, tau=-1.0, want_ritz=False):
+    """The whole path on one prompt: [route] -> feature map -> Lanczos -> SimHash -> merge."""
+    if rho is not None:
+        slh_route(ctx, X, rho, tau)
+    slh_feature_map(ctx, X)
+    lz = slh_lanczos(ctx, n_it, want=want_ritz)
+    slh_simhash(ctx)
+    E, P, t2m, M = slh_merge(ctx, X)
+    return E, P, t2m, M, lz

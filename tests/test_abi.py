@@ -1,0 +1,86 @@
+"""CPU checks of the C ABI: the library loads, exports every declared symbol,
+draws the method's parameters bit-identically to the oracle's independent
+generator, and rejects bad arguments before touching a GPU."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import params as OP
+import paper_2607_19368_amd.slh as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "slh.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(slh_\w+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    lib = B.load()
+    names = header_functions()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(B.EXPORTS)
+
+
+def test_missing_library_fails_loudly(monkeypatch):
+    monkeypatch.setattr(B, "_lib", None)
+    monkeypatch.setattr(B, "LIB_PATH", "/nonexistent/libslh.so")
+    with pytest.raises(B.SLHError):
+        B.load()
+
+
+@pytest.mark.parametrize("seed,D,m,r,bits", [(0, 256, 256, 8, 6), (5, 64, 512, 3, 16), (2**40 + 7, 24, 256, 1, 1)])
+def test_parameters_match_oracle_generator(seed, D, m, r, bits):
+    W, psi, R = B.slh_gen_params(seed, D, m, r, bits)
+    Wv = (W.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    assert np.array_equal(Wv, OP.projection(seed, D, m))
+    assert np.array_equal(psi.astype(np.float64), OP.phases(seed, m))
+    Ro = OP.hyperplanes(seed, r, bits)
+    # both sides evaluate Box-Muller with their own libm; allow 2 ulp
+    assert np.all(np.abs(R - Ro) <= 4.5e-16 * np.maximum(np.abs(Ro), 1e-300))
+
+
+@pytest.mark.parametrize("window,n", [(0, 512), (7, 2048), (3, 33)])
+def test_start_vector_matches_oracle(window, n):
+    q = B.slh_gen_start(11, window, n)
+    qo = OP.start_vector(11, n, window)
+    assert np.max(np.abs(q - qo)) < 1e-15
+    assert abs(np.linalg.norm(q) - 1.0) < 1e-14
+
+
+@pytest.mark.parametrize("args", [
+    (1, 256, 256, 8, 6),        # N < 2
+    (0, 256, 256, 8, 6),
+    (512, 250, 256, 8, 6),      # D % 8
+    (512, 0, 256, 8, 6),
+    (512, 256, 300, 8, 6),      # m % 256
+    (512, 256, 4096, 8, 6),     # m > 2048
+    (512, 256, 256, 0, 6),      # r
+    (512, 256, 256, 129, 6),
+    (512, 256, 256, 8, 0),      # bits
+    (512, 256, 256, 8, 17),
+])
+def test_create_rejects_bad_sizes_without_gpu(args):
+    lib = B.load()
+    h = ctypes.c_void_p(1234)
+    rc = lib.slh_create(ctypes.byref(h), *args, 0)
+    assert rc == B.SLH_EINVAL
+    assert not h.value
+
+
+def test_host_calls_reject_bad_arguments():
+    lib = B.load()
+    assert lib.slh_gen_params(0, 0, 256, 1, 1, None, None, None) == B.SLH_EINVAL
+    assert lib.slh_gen_start(0, 0, 0, None) == B.SLH_EINVAL
+    assert lib.slh_set_option(None, B.SLH_OPT_KERNEL, 0.0) == B.SLH_EINVAL
+    assert lib.slh_feature_map(None, None, 0, 0) == B.SLH_EINVAL
+    assert lib.slh_lanczos(None, 4, None, None) == B.SLH_EINVAL
+    assert lib.slh_copy_out(None, B.SLH_OUT_PHI, None, 0) == B.SLH_EINVAL
+    assert lib.slh_merge_capacity(None) == 0
