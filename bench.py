@@ -71,8 +71,8 @@ def cpu_baseline(inp, min_seconds=10.0, max_reps=40):
 def main():
     a = parse()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py: this build runs on one GPU only (the path is single-GPU; see the "
-              "sharding notes in DESIGN.md); use --gpus 1", file=sys.stderr)
+        print("bench.py: the hot path runs on one GPU; multi-GPU sharding is not "
+              "implemented, use --gpus 1", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
@@ -122,8 +122,9 @@ def main():
     ms_per_step = 1e3 * dt / a.steps
     value = wl.N * a.steps / dt
 
-    # timed region 2: the same steps with HIP events around every stage and every
-    # pass over Phi (launched without the graph so that each pass can be bracketed)
+    # timed region 2: the same steps with HIP events around every stage; the passes
+    # over Phi are launched without the graph, each receiving its own kernel start /
+    # end timestamps
     stage_sum = {k: 0.0 for k in B.STAGE_NAMES}
     ms2 = None
     if a.timing:

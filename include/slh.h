@@ -93,7 +93,7 @@ int slh_gen_start(uint64_t seed, int64_t window, int64_t n, double *q_out);
  * Create a context for prompts of N tokens of width D with m random features,
  * r kept Ritz vectors and `bits` SimHash bits (Algorithm 1 inputs).  Draws the
  * parameters (above) on the host and uploads them to the current device.
- * Limits: N >= 2; D >= 8 and D % 8 == 0; m % 256 == 0 and 256 <= m <= 2048;
+ * Limits: N >= 2; 8 <= D <= 32768 and D % 8 == 0; m % 256 == 0 and 256 <= m <= 2048;
  * 1 <= r <= 128; 1 <= bits <= 16.  *out receives the context (NULL on error).
  */
 int slh_create(slh_ctx **out, int64_t N, int64_t D, int64_t m, int32_t r,

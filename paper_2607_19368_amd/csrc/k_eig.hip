@@ -99,10 +99,11 @@ __global__ __launch_bounds__(64) void k_tridiag_eig(const double* __restrict__ a
   }
   const double th = 0.5 * (lo + hi);
 
-  // inverse iteration on lane 0 (tridiagonal LU with partial pivoting)
+  // inverse iteration: LU of T - th I with partial pivoting on lane 0; the
+  // triangular solves carry the running entries in registers
   if (lane == 0) {
     const double eps_piv = DBL_EPSILON * fmax(tnorm, DBL_MIN);
-    // factor T - th I = P L U; U has diagonal fd, superdiagonals fu1, fu2
+    // T - th I = P L U; U has diagonal fd (stored inverted), superdiagonals fu1, fu2
     double dcur = al[0] - th, ucur = (n > 1) ? b1[0] : 0.0;
     for (int k = 0; k < n - 1; ++k) {
       const double sub = b1[k];                   // entry (k+1, k)
@@ -112,7 +113,7 @@ __global__ __launch_bounds__(64) void k_tridiag_eig(const double* __restrict__ a
         // no interchange
         if (fabs(dcur) < eps_piv) dcur = (dcur < 0.0 ? -eps_piv : eps_piv);
         const double l = sub / dcur;
-        fd[k] = dcur;
+        fd[k] = 1.0 / dcur;
         fu1[k] = ucur;
         fu2[k] = 0.0;
         fl[k] = l;
@@ -122,7 +123,7 @@ __global__ __launch_bounds__(64) void k_tridiag_eig(const double* __restrict__ a
       } else {
         // swap rows k and k+1
         const double l = dcur / sub;
-        fd[k] = sub;
+        fd[k] = 1.0 / sub;
         fu1[k] = dnext;
         fu2[k] = unext;
         fl[k] = l;
@@ -132,51 +133,64 @@ __global__ __launch_bounds__(64) void k_tridiag_eig(const double* __restrict__ a
       }
     }
     if (fabs(dcur) < eps_piv) dcur = (dcur < 0.0 ? -eps_piv : eps_piv);
-    fd[n - 1] = dcur;
+    fd[n - 1] = 1.0 / dcur;
     fu1[n - 1] = 0.0;
     fu2[n - 1] = 0.0;
-    // start vector: fixed pseudo-random entries in [-1, 1)
-    for (int k = 0; k < n; ++k) {
-      unsigned h = (unsigned)(k + 1) * 2654435761u;
-      h ^= h >> 15;
-      h *= 2246822519u;
-      h ^= h >> 13;
-      y[k] = (double)(h >> 8) * (2.0 / 16777216.0) - 1.0;
-    }
-    for (int itr = 0; itr < 2; ++itr) {
-      // forward: apply L^{-1} P
-      for (int k = 0; k < n - 1; ++k) {
-        if (piv[k]) {
-          const double t = y[k];
-          y[k] = y[k + 1];
-          y[k + 1] = t - fl[k] * y[k];
-        } else {
-          y[k + 1] -= fl[k] * y[k];
-        }
-      }
-      // backward: U x = y
-      for (int k = n - 1; k >= 0; --k) {
-        double v = y[k];
-        if (k + 1 < n) v -= fu1[k] * y[k + 1];
-        if (k + 2 < n) v -= fu2[k] * y[k + 2];
-        y[k] = v / fd[k];
-      }
-      double mx = 0.0;
-      for (int k = 0; k < n; ++k) mx = fmax(mx, fabs(y[k]));
-      const double inv = mx > 0.0 ? 1.0 / mx : 1.0;
-      for (int k = 0; k < n; ++k) y[k] *= inv;
-    }
-    double nr = 0.0;
-    for (int k = 0; k < n; ++k) nr = fma(y[k], y[k], nr);
-    double sc = 1.0 / sqrt(nr);
-    int first = 0;
-    while (first < n - 1 && y[first] == 0.0) ++first;
-    if (y[first] < 0.0) sc = -sc;
-    for (int k = 0; k < n; ++k) y[k] *= sc;
-    theta[(int64_t)a * r + c] = th;
+  }
+  // start vector: fixed pseudo-random entries in [-1, 1)
+  for (int k = lane; k < n; k += 64) {
+    unsigned h = (unsigned)(k + 1) * 2654435761u;
+    h ^= h >> 15;
+    h *= 2246822519u;
+    h ^= h >> 13;
+    y[k] = (double)(h >> 8) * (2.0 / 16777216.0) - 1.0;
   }
   __syncthreads();
-  for (int k = lane; k < n_it; k += 64) Sa[(int64_t)k * r + c] = (k < n) ? y[k] : 0.0;
+  for (int itr = 0; itr < 2; ++itr) {
+    if (lane == 0) {
+      // forward: apply L^{-1} P (cur = running entry k)
+      double cur = y[0];
+      for (int k = 0; k < n - 1; ++k) {
+        const double nxt = y[k + 1];
+        if (piv[k]) {
+          y[k] = nxt;
+          cur = cur - fl[k] * nxt;
+        } else {
+          y[k] = cur;
+          cur = nxt - fl[k] * cur;
+        }
+      }
+      y[n - 1] = cur;
+      // backward: U x = y (x1 = x[k+1], x2 = x[k+2])
+      double x1 = 0.0, x2 = 0.0;
+      for (int k = n - 1; k >= 0; --k) {
+        const double xk = ((y[k] - fu1[k] * x1) - fu2[k] * x2) * fd[k];
+        y[k] = xk;
+        x2 = x1;
+        x1 = xk;
+      }
+    }
+    __syncthreads();
+    double mx = 0.0;
+    for (int k = lane; k < n; k += 64) mx = fmax(mx, fabs(y[k]));
+    for (int o = 32; o >= 1; o >>= 1) mx = fmax(mx, __shfl_xor(mx, o, 64));
+    const double inv = mx > 0.0 ? 1.0 / mx : 1.0;
+    for (int k = lane; k < n; k += 64) y[k] *= inv;
+    __syncthreads();
+  }
+  // unit norm; sign such that the first nonzero entry is positive
+  double nr = 0.0;
+  int first = n - 1;
+  for (int k = lane; k < n; k += 64) {
+    nr = fma(y[k], y[k], nr);
+    if (y[k] != 0.0 && k < first) first = k;
+  }
+  nr = wave_sum_f64(nr);
+  for (int o = 32; o >= 1; o >>= 1) first = min(first, __shfl_xor(first, o, 64));
+  double sc = 1.0 / sqrt(nr);
+  if (y[first] < 0.0) sc = -sc;
+  if (lane == 0) theta[(int64_t)a * r + c] = th;
+  for (int k = lane; k < n_it; k += 64) Sa[(int64_t)k * r + c] = (k < n) ? y[k] * sc : 0.0;
 }
 
 hipError_t launch_tridiag_eig(const double* alpha, const double* beta, const int* neff,
@@ -189,50 +203,60 @@ hipError_t launch_tridiag_eig(const double* alpha, const double* beta, const int
 }
 
 // Z[a][i][c] = sum_{k < n_eff} Q[a][k][i] Seig[a][k][c]   (fp64).
-// Thread = (row, group of 16 columns); S is staged through LDS 32 rows at a time.
+// Thread = (row, group of 8 columns); S is staged through LDS 32 rows at a time
+// (rows past n_eff zero-filled) and Q is read 8 rows of k at a time.
 __global__ __launch_bounds__(256) void k_ritz(const double* __restrict__ Q,
                                               const double* __restrict__ Seig,
                                               const int* __restrict__ neff, int L, int ldq,
                                               int n_it, int r, double* __restrict__ Z) {
   const int a = blockIdx.y, tid = threadIdx.x;
   const int n = neff[a];
-  const int cgroups = (r + 15) / 16;
+  const int cgroups = (r + 7) / 8;
   const int rpb = 256 / cgroups;
   const int cg = tid % cgroups;
   const int i = blockIdx.x * rpb + tid / cgroups;
   const bool active = (tid / cgroups) < rpb && i < L;
+  const int ic = min(i, L - 1);
   const double* Qa = Q + (int64_t)a * ldq * L;
   const double* Sa = Seig + (int64_t)a * n_it * r;
   __shared__ double sS[32 * 128];
-  double acc[16];
+  double acc[8];
 #pragma unroll
-  for (int c = 0; c < 16; ++c) acc[c] = 0.0;
+  for (int c = 0; c < 8; ++c) acc[c] = 0.0;
   for (int k0 = 0; k0 < n; k0 += 32) {
     const int nk = min(32, n - k0);
-    for (int e = tid; e < nk * r; e += 256) sS[(e / r) * 128 + (e % r)] = Sa[(int64_t)(k0 + e / r) * r + (e % r)];
+    for (int e = tid; e < 32 * 128; e += 256) {
+      const int kr = e >> 7, c = e & 127;
+      sS[e] = (kr < nk && c < r) ? Sa[(int64_t)(k0 + kr) * r + c] : 0.0;
+    }
     __syncthreads();
     if (active) {
-      for (int kk = 0; kk < nk; ++kk) {
-        const double q = Qa[(int64_t)(k0 + kk) * L + i];
-        const double* srow = sS + kk * 128 + cg * 16;
+      for (int kk = 0; kk < nk; kk += 8) {
+        double q[8];
 #pragma unroll
-        for (int c = 0; c < 16; ++c) acc[c] = fma(q, srow[c], acc[c]);
+        for (int e = 0; e < 8; ++e) q[e] = Qa[(int64_t)min(k0 + kk + e, n - 1) * L + ic];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const double* srow = sS + (kk + e) * 128 + cg * 8;   // zero rows past nk
+#pragma unroll
+          for (int c = 0; c < 8; ++c) acc[c] = fma(q[e], srow[c], acc[c]);
+        }
       }
     }
     __syncthreads();
   }
   if (active) {
-    double* zr = Z + ((int64_t)a * L + i) * r + cg * 16;
+    double* zr = Z + ((int64_t)a * L + i) * r + cg * 8;
 #pragma unroll
-    for (int c = 0; c < 16; ++c)
-      if (cg * 16 + c < r) zr[c] = acc[c];
+    for (int c = 0; c < 8; ++c)
+      if (cg * 8 + c < r) zr[c] = acc[c];
   }
 }
 
 hipError_t launch_ritz(const double* Q, const double* Seig, const int* neff, int n_act, int L,
                        int ldq, int n_it, int r, double* Z, hipStream_t s) {
   (void)hipGetLastError();
-  const int cgroups = (r + 15) / 16;
+  const int cgroups = (r + 7) / 8;
   const int rpb = 256 / cgroups;
   hipLaunchKernelGGL(k_ritz, dim3((unsigned)((L + rpb - 1) / rpb), n_act), dim3(256), 0, s, Q,
                      Seig, neff, L, ldq, n_it, r, Z);

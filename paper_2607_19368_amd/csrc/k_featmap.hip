@@ -18,6 +18,8 @@
 #include "slh_device.h"
 #include "slh_internal.h"
 
+#include <hip/hip_ext.h>
+
 namespace slh {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -206,16 +208,20 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_featmap(FeatmapArgs a) {
   }
 }
 
-hipError_t launch_featmap(const FeatmapArgs& a, hipStream_t s) {
+hipError_t launch_featmap(const FeatmapArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   (void)hipGetLastError();
   if (a.n_rows <= 0) return hipSuccess;
   // 256 x 256 tiles when that still gives at least one tile per CU, else 128 x 128
   int64_t t256 = ((a.n_rows + 255) / 256) * (a.m / 256);
   if (a.m % 256 == 0 && t256 >= 256) {
-    hipLaunchKernelGGL((k_featmap<256, 256, 2, 4>), dim3((unsigned)t256), dim3(512), 0, s, a);
+    auto k = k_featmap<256, 256, 2, 4>;
+    if (e0) hipExtLaunchKernelGGL(k, dim3((unsigned)t256), dim3(512), 0, s, e0, e1, 0, a);
+    else hipLaunchKernelGGL(k, dim3((unsigned)t256), dim3(512), 0, s, a);
   } else {
     int64_t t128 = ((a.n_rows + 127) / 128) * (a.m / 128);
-    hipLaunchKernelGGL((k_featmap<128, 128, 2, 2>), dim3((unsigned)t128), dim3(256), 0, s, a);
+    auto k = k_featmap<128, 128, 2, 2>;
+    if (e0) hipExtLaunchKernelGGL(k, dim3((unsigned)t128), dim3(256), 0, s, e0, e1, 0, a);
+    else hipLaunchKernelGGL(k, dim3((unsigned)t128), dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }

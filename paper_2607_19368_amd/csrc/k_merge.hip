@@ -206,43 +206,68 @@ __global__ __launch_bounds__(256) void k_mg_finalize(MergeWS w, int* __restrict_
   if (end) P[g] = w.compact ? g : tok;
 }
 
-template <int DT, int PPT>
-__device__ __forceinline__ void mg_load(const void* X, int64_t ldx, int tok, int D,
-                                        float (&x)[2 * PPT]) {
-  const int tid = threadIdx.x;
+// Member rows are read 8 columns per thread (one 16-byte load for bf16, two
+// for fp32) by 512 threads, PPT passes of 4096 columns; D % 8 == 0.
+template <int DT> struct MgRaw;
+template <> struct MgRaw<0> { uint4 v; };
+template <> struct MgRaw<1> { float4 lo, hi; };
+
+template <int DT>
+__device__ __forceinline__ MgRaw<DT> mg_load(const void* X, int64_t ldx, int tok, int col) {
+  MgRaw<DT> r;
+  if constexpr (DT == 0) {
+    r.v = *(const uint4*)((const uint16_t*)X + (int64_t)tok * ldx + col);
+  } else {
+    const float4* p = (const float4*)((const float*)X + (int64_t)tok * ldx + col);
+    r.lo = p[0];
+    r.hi = p[1];
+  }
+  return r;
+}
+
+template <int DT>
+__device__ __forceinline__ void mg_add(float* acc, const MgRaw<DT>& r) {
+  if constexpr (DT == 0) {
+    const uint32_t u[4] = {r.v.x, r.v.y, r.v.z, r.v.w};
 #pragma unroll
-  for (int q = 0; q < PPT; ++q) {
-    const int p = tid + 256 * q;
-    if (2 * p < D) {
-      if (DT == 0) {
-        const uint32_t v = *((const uint32_t*)((const uint16_t*)X + (int64_t)tok * ldx) + p);
-        x[2 * q] = __uint_as_float(v << 16);
-        x[2 * q + 1] = __uint_as_float(v & 0xFFFF0000u);
-      } else {
-        const float2 v = *((const float2*)((const float*)X + (int64_t)tok * ldx) + p);
-        x[2 * q] = v.x;
-        x[2 * q + 1] = v.y;
-      }
-    } else {
-      x[2 * q] = 0.0f;
-      x[2 * q + 1] = 0.0f;
+    for (int e = 0; e < 4; ++e) {
+      acc[2 * e] += __uint_as_float(u[e] << 16);
+      acc[2 * e + 1] += __uint_as_float(u[e] & 0xFFFF0000u);
     }
+  } else {
+    acc[0] += r.lo.x; acc[1] += r.lo.y; acc[2] += r.lo.z; acc[3] += r.lo.w;
+    acc[4] += r.hi.x; acc[5] += r.hi.y; acc[6] += r.hi.z; acc[7] += r.hi.w;
   }
 }
 
+__device__ __forceinline__ void mg_store8(float* dst, const float* v, float scale) {
+  ((float4*)dst)[0] = make_float4(v[0] * scale, v[1] * scale, v[2] * scale, v[3] * scale);
+  ((float4*)dst)[1] = make_float4(v[4] * scale, v[5] * scale, v[6] * scale, v[7] * scale);
+}
+
+// Sum over the 512 threads of one float per thread (fixed order); `red` holds
+// 8 floats; all threads get the result.  Contains one barrier.
+__device__ __forceinline__ float mg_block_sum(float v, float* red) {
+  v = wave_sum_f32(v);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return ((red[0] + red[1]) + (red[2] + red[3])) + ((red[4] + red[5]) + (red[6] + red[7]));
+}
+
+// One workgroup per chunk of CH sorted positions; member rows stream DEPTH at
+// a time with the next DEPTH in flight (DEPTH sized to keep the row buffers at
+// 64 registers).
 template <int DT, int PPT>
-__global__ __launch_bounds__(256) void k_mg_reduce(MergeWS w, const void* __restrict__ X,
+__global__ __launch_bounds__(512) void k_mg_reduce(MergeWS w, const void* __restrict__ X,
                                                    int64_t ldx, float* __restrict__ E) {
-  const int c = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c = blockIdx.x, tid = threadIdx.x;
   const int D = w.D;
   const int64_t s0 = (int64_t)c * w.CH;
   const int n = (int)min((int64_t)w.CH, w.N - s0);
   __shared__ int ssv[MG_CHMAX], ssg[MG_CHMAX];
   __shared__ double snrm[MG_CHMAX];
   __shared__ int prev_g, next_g;
-  __shared__ float runsq[MG_CHMAX][4];
-  __shared__ int run_g[MG_CHMAX], run_len[MG_CHMAX], run_kind[MG_CHMAX];
-  __shared__ double run_nsum[MG_CHMAX];
+  __shared__ float red[2][8];
   if (tid < n) {
     const int tok = w.sval[s0 + tid];
     ssv[tid] = tok;
@@ -254,155 +279,221 @@ __global__ __launch_bounds__(256) void k_mg_reduce(MergeWS w, const void* __rest
     next_g = (s0 + n < w.N) ? w.sseg[s0 + n] : -1;
   }
   __syncthreads();
-  float acc[2 * PPT], x[2 * PPT];
+  int col[PPT];
+  bool cin[PPT];
 #pragma unroll
-  for (int e = 0; e < 2 * PPT; ++e) acc[e] = 0.0f;
+  for (int q = 0; q < PPT; ++q) {
+    const int c8 = 8 * (tid + 512 * q);
+    cin[q] = c8 < D;
+    col[q] = min(c8, D - 8);
+  }
+  float acc[PPT][8];
+#pragma unroll
+  for (int q = 0; q < PPT; ++q)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[q][e] = 0.0f;
+  constexpr int DEPTH = (8 / (PPT * (DT + 1))) > 0 ? 8 / (PPT * (DT + 1)) : 1;
+  MgRaw<DT> rc[DEPTH][PPT], rn[DEPTH][PPT];
+  auto load_batch = [&](MgRaw<DT> (&dst)[DEPTH][PPT], int b) {
+#pragma unroll
+    for (int e = 0; e < DEPTH; ++e) {
+      const int tok = ssv[min(DEPTH * b + e, n - 1)];
+#pragma unroll
+      for (int q = 0; q < PPT; ++q) dst[e][q] = mg_load<DT>(X, ldx, tok, col[q]);
+    }
+  };
   double nsum = 0.0;
-  int rs = 0, nrun = 0;
-  mg_load<DT, PPT>(X, ldx, ssv[0], D, x);
-  for (int s = 0; s < n; ++s) {
-    float cur[2 * PPT];
+  int rs = 0, par = 0;
+  bool had_head = false, had_tail = false;
+  const int nbat = (n + DEPTH - 1) / DEPTH;
+  load_batch(rc, 0);
+  for (int b = 0; b < nbat; ++b) {
+    if (b + 1 < nbat) load_batch(rn, b + 1);
 #pragma unroll
-    for (int e = 0; e < 2 * PPT; ++e) cur[e] = x[e];
-    if (s + 1 < n) mg_load<DT, PPT>(X, ldx, ssv[s + 1], D, x);
+    for (int e = 0; e < DEPTH; ++e) {
+      const int s = DEPTH * b + e;
+      if (s < n) {
 #pragma unroll
-    for (int e = 0; e < 2 * PPT; ++e) acc[e] += cur[e];
-    nsum += snrm[s];
-    const int g = ssg[s];
-    if (s == n - 1 || ssg[s + 1] != g) {
-      const bool starts = (rs > 0) || (prev_g != g);
-      const bool ends = (s < n - 1) || (next_g != g);
-      // kind 0: whole bucket -> E; 1: head partial (slot 2c); 2: tail partial (slot 2c+1)
-      const int kind = (starts && ends) ? 0 : (!starts ? 1 : 2);
-      float* dst = (kind == 0) ? (E + (int64_t)g * D)
-                               : (w.part + (int64_t)(2 * c + (kind == 2)) * D);
-      float sq = 0.0f;
+        for (int q = 0; q < PPT; ++q)
+          if (cin[q]) mg_add<DT>(acc[q], rc[e][q]);
+        nsum += snrm[s];
+        const int g = ssg[s];
+        if (s == n - 1 || ssg[s + 1] != g) {
+          const bool starts = (rs > 0) || (prev_g != g);
+          const bool ends = (s < n - 1) || (next_g != g);
+          // kind 0: whole bucket -> E (Eq. 7 renormalisation: sum * mean member norm / |sum|);
+          // 1: head partial (slot 2c); 2: tail partial (slot 2c+1)
+          const int kind = (starts && ends) ? 0 : (!starts ? 1 : 2);
+          if (kind == 0) {
+            float sq = 0.0f;
 #pragma unroll
-      for (int q = 0; q < PPT; ++q) {
-        const int p = tid + 256 * q;
-        if (2 * p < D) {
-          *(float2*)(dst + 2 * p) = make_float2(acc[2 * q], acc[2 * q + 1]);
-          sq += acc[2 * q] * acc[2 * q] + acc[2 * q + 1] * acc[2 * q + 1];
+            for (int q = 0; q < PPT; ++q)
+              if (cin[q])
+#pragma unroll
+                for (int k = 0; k < 8; ++k) sq += acc[q][k] * acc[q][k];
+            const float tsq = mg_block_sum(sq, red[par]);
+            par ^= 1;
+            const double nrm = sqrt((double)tsq);
+            const float scale = nrm > 0.0 ? (float)(nsum / ((double)(s - rs + 1) * nrm)) : 0.0f;
+            float* dst = E + (int64_t)g * D;
+#pragma unroll
+            for (int q = 0; q < PPT; ++q)
+              if (cin[q]) mg_store8(dst + col[q], acc[q], scale);
+          } else {
+            const int slot = 2 * c + (kind == 2);
+            float* dst = w.part + (int64_t)slot * D;
+#pragma unroll
+            for (int q = 0; q < PPT; ++q)
+              if (cin[q]) mg_store8(dst + col[q], acc[q], 1.0f);
+            if (tid == 0) {
+              w.part_seg[slot] = g;
+              w.part_cnt[slot] = s - rs + 1;
+              w.part_nsum[slot] = nsum;
+              w.part_end[slot] = ends;
+            }
+            had_head |= kind == 1;
+            had_tail |= kind == 2;
+          }
+#pragma unroll
+          for (int q = 0; q < PPT; ++q)
+#pragma unroll
+            for (int k = 0; k < 8; ++k) acc[q][k] = 0.0f;
+          nsum = 0.0;
+          rs = s + 1;
         }
       }
-      sq = wave_sum_f32(sq);
-      if (lane == 0) runsq[nrun][wave] = sq;
-      if (tid == 0) {
-        run_g[nrun] = g;
-        run_len[nrun] = s - rs + 1;
-        run_kind[nrun] = kind;
-        run_nsum[nrun] = nsum;
-        if (kind != 0) {
-          const int slot = 2 * c + (kind == 2);
-          w.part_seg[slot] = g;
-          w.part_cnt[slot] = s - rs + 1;
-          w.part_nsum[slot] = nsum;
-          w.part_end[slot] = ends;
-        }
-      }
-#pragma unroll
-      for (int e = 0; e < 2 * PPT; ++e) acc[e] = 0.0f;
-      nsum = 0.0;
-      rs = s + 1;
-      ++nrun;
     }
+#pragma unroll
+    for (int e = 0; e < DEPTH; ++e)
+#pragma unroll
+      for (int q = 0; q < PPT; ++q) rc[e][q] = rn[e][q];
   }
-  __syncthreads();
   if (tid == 0) {
-    bool head = false, tail = false;
-    for (int k = 0; k < nrun; ++k) {
-      head |= run_kind[k] == 1;
-      tail |= run_kind[k] == 2;
-    }
-    if (!head) w.part_seg[2 * c] = -1;
-    if (!tail) w.part_seg[2 * c + 1] = -1;
-  }
-  // renormalise whole buckets: E = sum * (mean member norm) / |sum|  (Eq. 7)
-  for (int k = 0; k < nrun; ++k) {
-    if (run_kind[k] != 0) continue;
-    const float sq = (runsq[k][0] + runsq[k][1]) + (runsq[k][2] + runsq[k][3]);
-    const double nrm = sqrt((double)sq);
-    const float scale = nrm > 0.0 ? (float)(run_nsum[k] / ((double)run_len[k] * nrm)) : 0.0f;
-    float* dst = E + (int64_t)run_g[k] * D;
-#pragma unroll
-    for (int q = 0; q < PPT; ++q) {
-      const int p = tid + 256 * q;
-      if (2 * p < D) {
-        float2 v = *(float2*)(dst + 2 * p);
-        *(float2*)(dst + 2 * p) = make_float2(v.x * scale, v.y * scale);
-      }
-    }
+    if (!had_head) w.part_seg[2 * c] = -1;
+    if (!had_tail) w.part_seg[2 * c + 1] = -1;
   }
 }
 
+// A bucket cut by chunk edges: its tail partial in chunk c plus the head
+// partials of chunks c+1 .. last, summed in chunk order (8 / PPT rows in flight),
+// then renormalised.
 template <int PPT>
-__global__ __launch_bounds__(256) void k_mg_combine(MergeWS w, float* __restrict__ E,
+__global__ __launch_bounds__(512) void k_mg_combine(MergeWS w, float* __restrict__ E,
                                                     int nchunks) {
   const int c = blockIdx.x, tid = threadIdx.x;
   const int D = w.D;
   const int g = w.part_seg[2 * c + 1];
   if (g < 0) return;
-  __shared__ float red[4];
-  float acc[2 * PPT];
+  __shared__ int s_last;
+  __shared__ float red[8];
+  __shared__ double dred[8];
+  __shared__ int ired[8];
+  // last chunk of the chain: the first cc > c whose head slot belongs to another
+  // macro (then cc - 1) or ends the bucket (then cc)
+  int last = nchunks - 1;
+  for (int base = c + 1; base < nchunks; base += 512) {
+    const int cc = base + tid;
+    int x = nchunks - 1;
+    if (cc < nchunks) {
+      if (w.part_seg[2 * cc] != g) x = cc - 1;
+      else if (w.part_end[2 * cc]) x = cc;
+    }
+    for (int o = 32; o >= 1; o >>= 1) x = min(x, __shfl_xor(x, o, 64));
+    if ((tid & 63) == 0) ired[tid >> 6] = x;
+    __syncthreads();
+    if (tid == 0) {
+      int m = ired[0];
+      for (int k = 1; k < 8; ++k) m = min(m, ired[k]);
+      s_last = m;
+    }
+    __syncthreads();
+    last = s_last;
+    if (last < base + 511) break;
+    __syncthreads();
+  }
+  int col[PPT];
+  bool cin[PPT];
 #pragma unroll
   for (int q = 0; q < PPT; ++q) {
-    const int p = tid + 256 * q;
-    float2 v = (2 * p < D) ? *(const float2*)(w.part + (int64_t)(2 * c + 1) * D + 2 * p)
-                           : make_float2(0.f, 0.f);
-    acc[2 * q] = v.x;
-    acc[2 * q + 1] = v.y;
+    const int c8 = 8 * (tid + 512 * q);
+    cin[q] = c8 < D;
+    col[q] = min(c8, D - 8);
   }
-  int cnt = w.part_cnt[2 * c + 1];
-  double nsum = w.part_nsum[2 * c + 1];
-  for (int cc = c + 1; cc < nchunks; ++cc) {
-    const int slot = 2 * cc;
-    if (w.part_seg[slot] != g) break;
+  float acc[PPT][8];
+  {
+    const float* src = w.part + (int64_t)(2 * c + 1) * D;
 #pragma unroll
     for (int q = 0; q < PPT; ++q) {
-      const int p = tid + 256 * q;
-      if (2 * p < D) {
-        float2 v = *(const float2*)(w.part + (int64_t)slot * D + 2 * p);
-        acc[2 * q] += v.x;
-        acc[2 * q + 1] += v.y;
-      }
+      const MgRaw<1> r = mg_load<1>(src, 0, 0, col[q]);
+      acc[q][0] = r.lo.x; acc[q][1] = r.lo.y; acc[q][2] = r.lo.z; acc[q][3] = r.lo.w;
+      acc[q][4] = r.hi.x; acc[q][5] = r.hi.y; acc[q][6] = r.hi.z; acc[q][7] = r.hi.w;
     }
-    cnt += w.part_cnt[slot];
-    nsum += w.part_nsum[slot];
-    if (w.part_end[slot]) break;
+  }
+  // head partials of chunks c+1 .. last, DEPTH at a time
+  constexpr int DEPTH = (8 / PPT) > 0 ? 8 / PPT : 1;
+  for (int cc0 = c + 1; cc0 <= last; cc0 += DEPTH) {
+    MgRaw<1> r[DEPTH][PPT];
+#pragma unroll
+    for (int e = 0; e < DEPTH; ++e) {
+      const float* src = w.part + (int64_t)(2 * min(cc0 + e, last)) * D;
+#pragma unroll
+      for (int q = 0; q < PPT; ++q) r[e][q] = mg_load<1>(src, 0, 0, col[q]);
+    }
+#pragma unroll
+    for (int e = 0; e < DEPTH; ++e)
+      if (cc0 + e <= last)
+#pragma unroll
+        for (int q = 0; q < PPT; ++q) mg_add<1>(acc[q], r[e][q]);
+  }
+  // member count and norm sum over the same slots (fixed order)
+  int cnt = 0;
+  double nsum = 0.0;
+  for (int cc = c + 1 + tid; cc <= last; cc += 512) {
+    cnt += w.part_cnt[2 * cc];
+    nsum += w.part_nsum[2 * cc];
+  }
+  cnt = wave_sum_i32(cnt);
+  nsum = wave_sum_f64(nsum);
+  if ((tid & 63) == 0) {
+    ired[tid >> 6] = cnt;
+    dred[tid >> 6] = nsum;
   }
   float sq = 0.0f;
 #pragma unroll
-  for (int e = 0; e < 2 * PPT; ++e) sq += acc[e] * acc[e];
-  sq = wave_sum_f32(sq);
-  if ((tid & 63) == 0) red[tid >> 6] = sq;
-  __syncthreads();
-  const float tsq = (red[0] + red[1]) + (red[2] + red[3]);
+  for (int q = 0; q < PPT; ++q)
+    if (cin[q])
+#pragma unroll
+      for (int k = 0; k < 8; ++k) sq += acc[q][k] * acc[q][k];
+  const float tsq = mg_block_sum(sq, red);       // its barrier also publishes ired / dred
+  int tcnt = w.part_cnt[2 * c + 1];
+  double tns = w.part_nsum[2 * c + 1];
+  for (int k = 0; k < 8; ++k) {
+    tcnt += ired[k];
+    tns += dred[k];
+  }
   const double nrm = sqrt((double)tsq);
-  const float scale = nrm > 0.0 ? (float)(nsum / ((double)cnt * nrm)) : 0.0f;
+  const float scale = nrm > 0.0 ? (float)(tns / ((double)tcnt * nrm)) : 0.0f;
   float* dst = E + (int64_t)g * D;
 #pragma unroll
-  for (int q = 0; q < PPT; ++q) {
-    const int p = tid + 256 * q;
-    if (2 * p < D) *(float2*)(dst + 2 * p) = make_float2(acc[2 * q] * scale, acc[2 * q + 1] * scale);
-  }
+  for (int q = 0; q < PPT; ++q)
+    if (cin[q]) mg_store8(dst + col[q], acc[q], scale);
 }
 
 template <int DT, int PPT>
 static void launch_reduce_combine(const MergeWS& w, const void* X, int64_t ldx, float* E,
                                   int nchunks, hipStream_t s) {
-  hipLaunchKernelGGL((k_mg_reduce<DT, PPT>), dim3(nchunks), dim3(256), 0, s, w, X, ldx, E);
-  hipLaunchKernelGGL((k_mg_combine<PPT>), dim3(nchunks), dim3(256), 0, s, w, E, nchunks);
+  hipLaunchKernelGGL((k_mg_reduce<DT, PPT>), dim3(nchunks), dim3(512), 0, s, w, X, ldx, E);
+  hipLaunchKernelGGL((k_mg_combine<PPT>), dim3(nchunks), dim3(512), 0, s, w, E, nchunks);
 }
 
 template <int DT>
 static void dispatch_ppt(const MergeWS& w, const void* X, int64_t ldx, float* E, int nchunks,
                          hipStream_t s) {
-  const int ppt = (w.D / 2 + 255) / 256;
+  const int ppt = (w.D + 4095) / 4096;
   if (ppt <= 1) launch_reduce_combine<DT, 1>(w, X, ldx, E, nchunks, s);
   else if (ppt <= 2) launch_reduce_combine<DT, 2>(w, X, ldx, E, nchunks, s);
   else if (ppt <= 4) launch_reduce_combine<DT, 4>(w, X, ldx, E, nchunks, s);
-  else if (ppt <= 8) launch_reduce_combine<DT, 8>(w, X, ldx, E, nchunks, s);
-  else launch_reduce_combine<DT, 16>(w, X, ldx, E, nchunks, s);
+  else launch_reduce_combine<DT, 8>(w, X, ldx, E, nchunks, s);      // D <= 32768
 }
 
 int merge_nchunks(int64_t N, int CH) { return (int)((N + CH - 1) / CH); }

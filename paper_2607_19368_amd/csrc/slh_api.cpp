@@ -112,7 +112,7 @@ struct slh_ctx {
   std::vector<DevBuf*> all;
   DevBuf Wt, psi, R, q1all, q1act, winlist, route;
   DevBuf nrm2_fm, nrm_x, rowscale, Xb, Phi;
-  DevBuf Q, T, U, Z1, Spart, H1part, H1, H2part, H2, alpha, beta, neff, stop, amax;
+  DevBuf Q, T, U, Z1, Spart, H1, H2part, H2, alpha, beta, neff, stop, amax;
   DevBuf theta, Seig, Z, proj, codes;
   DevBuf keyA, keyB, valA, valB, tmpi, segid, segk, sval, sloc, mw, wbase, sseg, Mtot;
   DevBuf part, part_seg, part_cnt, part_nsum, part_end;
@@ -324,7 +324,7 @@ int slh_create(slh_ctx** out, int64_t N, int64_t D, int64_t m, int32_t r, int32_
   if (!out) return SLH_EINVAL;
   *out = nullptr;
   if (N < 2 || N > (int64_t)1 << 30) return SLH_EINVAL;
-  if (D < 8 || D % 8 != 0 || D > 65536) return SLH_EINVAL;
+  if (D < 8 || D % 8 != 0 || D > 32768) return SLH_EINVAL;
   if (m < 256 || m > 2048 || m % 256 != 0) return SLH_EINVAL;
   if (r < 1 || r > 128) return SLH_EINVAL;
   if (bits < 1 || bits > 16) return SLH_EINVAL;
@@ -376,7 +376,7 @@ void slh_destroy(slh_ctx* c) {
   drop_graph(c);
   DevBuf* bufs[] = {&c->Wt, &c->psi, &c->R, &c->q1all, &c->q1act, &c->winlist, &c->route,
                     &c->nrm2_fm, &c->nrm_x, &c->rowscale, &c->Xb, &c->Phi, &c->Q, &c->T,
-                    &c->U, &c->Z1, &c->Spart, &c->H1part, &c->H1, &c->H2part, &c->H2,
+                    &c->U, &c->Z1, &c->Spart, &c->H1, &c->H2part, &c->H2,
                     &c->alpha, &c->beta, &c->neff, &c->stop, &c->amax, &c->theta, &c->Seig, &c->Z,
                     &c->proj, &c->codes, &c->keyA, &c->keyB, &c->valA, &c->valB, &c->tmpi,
                     &c->segid, &c->segk, &c->sval, &c->sloc, &c->mw, &c->wbase, &c->sseg,
@@ -514,9 +514,8 @@ int slh_feature_map(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx) {
   a.L = L;
   a.D = (int)c->D;
   a.m = (int)c->m;
-  if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[0], c->stream));
-  HIP_TRY(c, launch_featmap(a, c->stream));
-  if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[1], c->stream));
+  HIP_TRY(c, launch_featmap(a, c->stream, c->timing ? c->ev[0] : nullptr,
+                            c->timing ? c->ev[1] : nullptr));
   c->stage = 1;
   return SLH_OK;
 }
@@ -556,26 +555,30 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
     w.ldq = n_it + 1;
     w.tol = c->tol;
     {
-      // rows per thread (8..32, a multiple of 8): aim for about two blocks per CU over all
-      // windows; fewer rows per block only multiply the partial sums of Phi^T v
+      // about four blocks per CU over all windows in each pass over Phi
+      const int64_t target = (int64_t)4 * c->n_cu;
+      auto rows8 = [](int64_t rows) {          // multiple of 8 in [8, 32]
+        rows = ((rows + 7) / 8) * 8;
+        return (int)std::max<int64_t>(8, std::min<int64_t>(rows, 32));
+      };
+      const int ns = (int)(c->m / 256);
+      const int64_t ga = std::max<int64_t>(1, target / ((int64_t)na * ns));
+      w.RWA = rows8((L + 8 * ga - 1) / (8 * ga));
+      w.RBA = 8 * w.RWA;
+      w.GA = (int)((L + w.RBA - 1) / w.RBA);
       const int rp = 512 / lanczos_m4((int)c->m);
-      const int64_t per_win = std::max<int64_t>(1, (int64_t)2 * c->n_cu / na);
-      int64_t rpt = (L + rp * per_win - 1) / (rp * per_win);
-      rpt = ((rpt + 7) / 8) * 8;
-      rpt = std::max<int64_t>(8, std::min<int64_t>(rpt, 32));
-      w.RPT = (int)rpt;
-      w.RB1 = rp * w.RPT;
-      w.G1 = (int)((L + w.RB1 - 1) / w.RB1);
+      const int64_t gb = std::max<int64_t>(1, target / na);
+      w.RPT = rows8((L + rp * gb - 1) / (rp * gb));
+      w.RBB = rp * w.RPT;
+      w.GB = (int)((L + w.RBB - 1) / w.RBB);
+      w.G3 = (int)((L + 31) / 32);
     }
-    w.G3 = (int)std::max<int64_t>(1, std::min<int64_t>(64, (L + 127) / 128));
-    w.RB3 = (int)((L + w.G3 - 1) / w.G3);
     const size_t hs = (size_t)w.ldq + 1;
     ENSURE(c, c->Q, (size_t)na * w.ldq * L * 8);
     ENSURE(c, c->T, (size_t)na * w.ldq * c->m * 8);
     ENSURE(c, c->U, (size_t)na * L * 8);
     ENSURE(c, c->Z1, (size_t)na * L * 8);
-    ENSURE(c, c->Spart, (size_t)na * w.G1 * c->m * 8);
-    ENSURE(c, c->H1part, (size_t)na * w.G1 * hs * 8);
+    ENSURE(c, c->Spart, (size_t)na * w.GA * c->m * 8);
     ENSURE(c, c->H1, (size_t)na * hs * 8);
     ENSURE(c, c->H2part, (size_t)na * w.G3 * hs * 8);
     ENSURE(c, c->H2, (size_t)na * hs * 8);
@@ -593,7 +596,6 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
     w.U = P<double>(c->U);
     w.Z1 = P<double>(c->Z1);
     w.Spart = P<double>(c->Spart);
-    w.H1part = P<double>(c->H1part);
     w.H1 = P<double>(c->H1);
     w.H2part = P<double>(c->H2part);
     w.H2 = P<double>(c->H2);
@@ -689,7 +691,7 @@ int slh_merge(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, float* emb_
     if ((rc = prep_norms(c, X, dtype, ldx))) return rc;
   const int64_t L = window_len(c);
   const int64_t N = c->N;
-  const int CH = 32;
+  const int CH = 16;
   const int nch = merge_nchunks(N, CH);
   ENSURE(c, c->keyA, N * 4);
   ENSURE(c, c->keyB, N * 4);

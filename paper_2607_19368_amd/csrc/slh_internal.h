@@ -27,7 +27,9 @@ struct FeatmapArgs {
   int64_t L;
   int D, m;
 };
-hipError_t launch_featmap(const FeatmapArgs& a, hipStream_t s);
+// e0/e1 (may be NULL): receive the kernel's own start / end timestamps.
+hipError_t launch_featmap(const FeatmapArgs& a, hipStream_t s, hipEvent_t e0 = nullptr,
+                          hipEvent_t e1 = nullptr);
 
 // ---- Lanczos (k_lanczos.hip) ----
 struct LanczosWS {
@@ -37,23 +39,24 @@ struct LanczosWS {
   double* T;                    // [n_act][ldq][m]  t_k = Phi^T q_k
   double* U;                    // [n_act][L]       u = Phi t_j
   double* Z1;                   // [n_act][L]       after the first Gram-Schmidt pass
-  double* Spart;                // [n_act][G1][m]   partials of t_j
-  double* H1part;               // [n_act][G1][ldq+1]
+  double* Spart;                // [n_act][GA][m]   partials of Phi^T z1 per row group
   double* H1;                   // [n_act][ldq+1]   Q_j^T u
   double* H2part;               // [n_act][G3][ldq+1] (slot ldq: |z1|^2)
-  double* H2;                   // [n_act][ldq+1]   Q_j^T z1 and |z1|^2
+  double* H2;                   // [n_act][ldq+1]   Q^T z1 and |z1|^2
   double* alpha;                // [n_act][n_it]
   double* beta;                 // [n_act][n_it]
   int* neff;                    // [n_act]  steps done
   int* stop;                    // [n_act]  1 after breakdown
   double* amax;                 // [n_act]  max |alpha| so far (breakdown scale)
   double tol;
-  int G1, RB1, RPT;             // Phi-pass row blocks: RB1 = (512 / M4) * RPT rows, RPT in {8,16,24,32}
-  int G3, RB3;                  // orthogonalisation row blocks
+  int GA, RBA, RWA;             // Phi^T v: row groups of RBA = 8 * RWA rows (RWA in {8,16,24,32})
+  int GB, RBB, RPT;             // Phi t: row blocks of RBB = (512 / M4) * RPT rows (RPT in {8,..,32})
+  int G3;                       // orthogonalisation blocks of 32 rows
 };
 int lanczos_m4(int m);   // threads per Phi row in the passes (power of two >= m / 4)
-// ev_before/ev_after (may be NULL): 2 * n_it events each, recorded around the
-// two Phi passes of every step (index 2j: Phi^T q_j, 2j + 1: Phi t_j).
+// ev_before/ev_after (may be NULL): 2 * n_it events each, receiving the start
+// and end timestamps of the two Phi passes of every step (index 2j: Phi^T v,
+// 2j + 1: Phi t_j).
 hipError_t launch_lanczos(const LanczosWS& w, const double* q1_act, hipStream_t s,
                           const hipEvent_t* ev_before = nullptr,
                           const hipEvent_t* ev_after = nullptr);
