@@ -14,11 +14,12 @@
 //           the breakdown test, and t_j = (Phi^T z1 - sum_k h2_k t_k) / beta
 //           (the second Gram-Schmidt pass applied in feature space; its
 //           coefficients h2 are at rounding level).
-//   phiu    u = Phi t_j (= A q_j) over row blocks; the first blocks of the
-//           launch form h1 = Q_j^T u as t_k^T t_j (k <= j), the same inner
-//           products taken in feature space, so no pass over Q is needed.
-//   orth    per 32 rows: q_j = (z1 - Q_{j-1} h2) / beta (second pass in row
-//           space, stored as Q[j]); alpha_j = h1_j = q_j^T A q_j;
+//   phiu    u = Phi t_j (= A q_j): the same (row group, column slice) blocks
+//           write per-slice partial row dots; the first blocks of the launch
+//           form h1 = Q_j^T u as t_k^T t_j (k <= j), the same inner products
+//           taken in feature space, so no pass over Q is needed.
+//   orth    per 32 rows: u from its slice partials; q_j = (z1 - Q_{j-1} h2) /
+//           beta (second pass in row space, stored as Q[j]); alpha_j = h1_j;
 //           z1 = u - Q_j h1 (first classical Gram-Schmidt pass of step j);
 //           partials of h2 = Q_j^T z1 and |z1|^2.  One read of Q_j feeds both
 //           the q_j update and z1.
@@ -92,6 +93,14 @@ __device__ __forceinline__ double half_sum8_f64(const double (&v)[8]) {
   return y;
 }
 
+// Value of v in lane l (l uniform), through the scalar unit.
+__device__ __forceinline__ double readlane_f64(double v, int l) {
+  const unsigned long long x = (unsigned long long)__double_as_longlong(v);
+  const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)x, l);
+  const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(x >> 32), l);
+  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+
 // Sum of src[g * ld] over g < G with 8 loads in flight (fixed order).
 __device__ __forceinline__ double sum_strided(const double* __restrict__ src, int64_t ld, int G) {
   double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
@@ -140,12 +149,12 @@ __device__ __forceinline__ double block_colsum(const double* __restrict__ src, i
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(512) void k_lz_phit(LanczosWS w, int j) {
   const int a = blockIdx.y;
-  if (w.stop[a]) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = w.L, m = w.m, hs = w.ldq + 1;
   const int nx = (j > 0) ? (j + 15) / 16 + 1 : 0;
   int g = blockIdx.x;
   if (g < nx) {
+    if (w.stop[a]) return;
     const double* hp = w.H2part + (int64_t)a * w.G3 * hs;
     double* dst = w.H2 + (int64_t)a * hs;
     if (g == nx - 1) {                         // |z1|^2 (slot ldq)
@@ -167,29 +176,35 @@ __global__ __launch_bounds__(512) void k_lz_phit(LanczosWS w, int j) {
   const double* vsrc = (j == 0) ? (w.Q + (int64_t)a * w.ldq * L) : (w.Z1 + (int64_t)a * L);
   double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
   float4 vc[8], vn[8];
-  auto load8 = [&](float4 (&dst)[8], int b) {
+  double wc, wn;
+  // rows r0 + wave + 8 (8 b + e), e < 8, of batch b; lane e (mod 8) also loads the
+  // weight of row e (0 past the group), broadcast when the batch is consumed
+  auto load8 = [&](float4 (&dst)[8], double& wd, int b) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int i = min(r0 + wave + 8 * (8 * b + e), r1 - 1);
       dst[e] = *(const float4*)(base + (int64_t)i * m);
     }
+    const int iw = r0 + wave + 8 * (8 * b + (lane & 7));
+    const double v = vsrc[min(iw, r1 - 1)];
+    wd = (iw < r1) ? v : 0.0;
   };
   const int nb = w.RWA / 8;
-  load8(vc, 0);
+  load8(vc, wc, 0);                 // in flight while the stop flag is read
+  if (w.stop[a]) return;
   for (int b = 0; b < nb; ++b) {
-    if (b + 1 < nb) load8(vn, b + 1);
+    if (b + 1 < nb) load8(vn, wn, b + 1);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const int i = r0 + wave + 8 * (8 * b + e);
-      const double vi = vsrc[min(i, r1 - 1)];
-      const double qi = (i < r1) ? vi : 0.0;
-      s0 = fma((double)vc[e].x, qi, s0);
-      s1 = fma((double)vc[e].y, qi, s1);
-      s2 = fma((double)vc[e].z, qi, s2);
-      s3 = fma((double)vc[e].w, qi, s3);
+      const double q = readlane_f64(wc, e);
+      s0 = fma((double)vc[e].x, q, s0);
+      s1 = fma((double)vc[e].y, q, s1);
+      s2 = fma((double)vc[e].z, q, s2);
+      s3 = fma((double)vc[e].w, q, s3);
     }
 #pragma unroll
     for (int e = 0; e < 8; ++e) vc[e] = vn[e];
+    wc = wn;
   }
   __shared__ double cred[8][257];
   cred[wave][4 * lane + 0] = s0;
@@ -207,27 +222,56 @@ __global__ __launch_bounds__(512) void k_lz_phit(LanczosWS w, int j) {
 
 // ---------------------------------------------------------------------------
 // finish: beta_{j-1}, breakdown, and t_j on 16 columns per block (256 threads:
-// 16 columns x 16 partial lanes).
+// 16 columns x 16 partial lanes).  Every load is issued before the first
+// reduction.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_lz_finish(LanczosWS w, int j) {
   const int a = blockIdx.y, g = blockIdx.x, tid = threadIdx.x;
-  if (w.stop[a]) return;
   const int m = w.m, hs = w.ldq + 1;
-  __shared__ double h2[264];
-  __shared__ double sh;
+  const int cl = tid & 15, pl = tid >> 4;
+  const int c = g * 16 + cl;                   // m is a multiple of 16
+  const double* H2 = w.H2 + (int64_t)a * hs;
+  // partial of Phi^T z1 over row groups pl, pl + 16, ...
+  const double* Sp = w.Spart + (int64_t)a * w.GA * m + c;
+  const int cnt = (w.GA - pl + 15) / 16;
+  const double s = sum_strided(Sp + (int64_t)pl * m, (int64_t)16 * m, cnt > 0 ? cnt : 0);
+  // partial of sum_k h2_k t_k over k = pl, pl + 16, ... < j
+  double corr = 0.0;
+  {
+    const double* Ta = w.T + (int64_t)a * w.ldq * m + c;
+    double acc[4] = {0, 0, 0, 0};
+    int k = pl;
+    for (; k + 48 < j; k += 64) {
+      double tv[4], hv[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        tv[e] = Ta[(int64_t)(k + 16 * e) * m];
+        hv[e] = H2[k + 16 * e];
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[e] = fma(tv[e], hv[e], acc[e]);
+    }
+    for (; k < j; k += 16) acc[0] = fma(Ta[(int64_t)k * m], H2[k], acc[0]);
+    corr = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  }
+  // |h2|^2 partial
+  double hh = 0.0;
+  for (int k = tid; k < j; k += 256) {
+    const double v = H2[k];
+    hh = fma(v, v, hh);
+  }
+  const double z2 = (j > 0) ? H2[w.ldq] : 0.0;
+  if (w.stop[a]) return;
   __shared__ double red[4];
+  __shared__ double sh;
+  __shared__ double rs[16][17], rc[16][17];
+  rs[pl][cl] = s;
+  rc[pl][cl] = corr;
   double inv = 1.0;
   if (j > 0) {
-    const double* H2 = w.H2 + (int64_t)a * hs;
-    double hh = 0.0;
-    for (int k = tid; k < j; k += 256) {
-      const double v = H2[k];
-      h2[k] = v;
-      hh = fma(v, v, hh);
-    }
-    hh = block_sum_f64(hh, red);
+    hh = block_sum_f64(hh, red);               // (its barriers also publish rs / rc)
     if (tid == 0) {
-      const double b2 = H2[w.ldq] - hh;       // |z1 - Q h2|^2 for orthonormal Q
+      const double b2 = z2 - hh;               // |z1 - Q h2|^2 for orthonormal Q
       const double beta = b2 > 0.0 ? sqrt(b2) : 0.0;
       const bool brk = !(beta > w.tol * w.amax[a]);
       sh = brk ? 0.0 : beta;
@@ -239,30 +283,10 @@ __global__ __launch_bounds__(256) void k_lz_finish(LanczosWS w, int j) {
     __syncthreads();
     if (sh == 0.0) return;
     inv = 1.0 / sh;
+  } else {
+    __syncthreads();
   }
-  const int cl = tid & 15, pl = tid >> 4;
-  const int c = g * 16 + cl;
-  const int cc = min(c, m - 1);
-  const double* Sp = w.Spart + (int64_t)a * w.GA * m + cc;
-  const int cnt = (w.GA - pl + 15) / 16;
-  const double s = sum_strided(Sp + (int64_t)pl * m, (int64_t)16 * m, cnt > 0 ? cnt : 0);
-  double corr = 0.0;
-  if (j > 0) {
-    const double* Ta = w.T + (int64_t)a * w.ldq * m + cc;
-    double acc[4] = {0, 0, 0, 0};
-    int k = pl;
-    for (; k + 48 < j; k += 64) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) acc[e] = fma(Ta[(int64_t)(k + 16 * e) * m], h2[k + 16 * e], acc[e]);
-    }
-    for (; k < j; k += 16) acc[0] = fma(Ta[(int64_t)k * m], h2[k], acc[0]);
-    corr = (acc[0] + acc[1]) + (acc[2] + acc[3]);
-  }
-  __shared__ double rs[16][17], rc[16][17];
-  rs[pl][cl] = s;
-  rc[pl][cl] = corr;
-  __syncthreads();
-  if (tid < 16 && c < m) {
+  if (tid < 16) {
     double S = 0.0, C = 0.0;
     for (int p = 0; p < 16; ++p) {
       S += rs[p][cl];
@@ -274,17 +298,12 @@ __global__ __launch_bounds__(256) void k_lz_finish(LanczosWS w, int j) {
 
 // ---------------------------------------------------------------------------
 // phiu: blocks [0, nx) form h1_k = t_k^T t_j, k <= j (one wave per k); the
-// rest compute u = Phi t_j on RBB = RP * RPT rows each.  A row is covered by M4
-// threads (4 columns each); every thread keeps its partial dot of each row it
-// streams and one block-level reduction at the end gives u.
+// rest own (row group, 256-column slice) exactly as in phit and write the
+// slice's partial of u = Phi t_j for each row (Upart[slice][row]): lane = 4
+// columns, the 8 rows of a batch are summed over the wave in one butterfly.
 // ---------------------------------------------------------------------------
-template <int M4>
 __global__ __launch_bounds__(512) void k_lz_phiu(LanczosWS w, int j) {
-  constexpr int RP = 512 / M4;
-  constexpr int WPR = M4 >= 64 ? M4 / 64 : 1;     // waves per row group
-  constexpr int MAXR = 32;                        // rows per thread kept (RPT <= 32)
   const int a = blockIdx.y;
-  if (w.stop[a]) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = w.L, m = w.m;
   const double* Ta = w.T + (int64_t)a * w.ldq * m;
@@ -292,6 +311,7 @@ __global__ __launch_bounds__(512) void k_lz_phiu(LanczosWS w, int j) {
   const int nx = (j + 8) / 8;
   int g = blockIdx.x;
   if (g < nx) {
+    if (w.stop[a]) return;
     const int k = g * 8 + wave;
     if (k > j) return;
     const double* tk = Ta + (int64_t)k * m;
@@ -306,73 +326,52 @@ __global__ __launch_bounds__(512) void k_lz_phiu(LanczosWS w, int j) {
     return;
   }
   g -= nx;
-  const int r0 = g * w.RBB;
-  const int r1 = min(L, r0 + w.RBB);
-  const float* Phi = w.Phi + (int64_t)a * L * m;
-  __shared__ double ured[8][MAXR];
-  const int c4 = tid % M4, rs = tid / M4;
-  const bool cin = 4 * c4 < m;
-  const int cc = min(c4, m / 4 - 1);
-  double t0 = tj[4 * cc + 0], t1 = tj[4 * cc + 1], t2 = tj[4 * cc + 2], t3 = tj[4 * cc + 3];
-  if (!cin) t0 = t1 = t2 = t3 = 0.0;
-  const float* base = Phi + 4 * cc;
+  const int ns = m >> 8;
+  const int sl = g % ns, rg = g / ns;
+  const int r0 = rg * w.RBA;
+  const int r1 = min(L, r0 + w.RBA);
+  const float* base = w.Phi + (int64_t)a * L * m + sl * 256 + 4 * lane;
   float4 vc[8], vn[8];
   auto load8 = [&](float4 (&dst)[8], int b) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const int i = min(r0 + rs + RP * (8 * b + e), r1 - 1);
+      const int i = min(r0 + wave + 8 * (8 * b + e), r1 - 1);
       dst[e] = *(const float4*)(base + (int64_t)i * m);
     }
   };
-  double p[MAXR];
-  const int nb = w.RPT / 8;
-  load8(vc, 0);
+  const int nb = w.RWA / 8;
+  load8(vc, 0);                     // in flight while t_j and the stop flag are read
+  const double* tc = tj + sl * 256 + 4 * lane;
+  const double t0 = tc[0], t1 = tc[1], t2 = tc[2], t3 = tc[3];
+  if (w.stop[a]) return;
+  double* up = w.Upart + ((int64_t)a * ns + sl) * L;
+  const int idx = ((lane >> 5) & 1) * 4 + ((lane >> 4) & 1) * 2 + ((lane >> 3) & 1);
+  for (int b = 0; b < nb; ++b) {
+    if (b + 1 < nb) load8(vn, b + 1);
+    double p[8];
 #pragma unroll
-  for (int b = 0; b < MAXR / 8; ++b) {
-    if (b < nb) {
-      if (b + 1 < nb) load8(vn, b + 1);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        double d = (double)vc[e].x * t0;
-        d = fma((double)vc[e].y, t1, d);
-        d = fma((double)vc[e].z, t2, d);
-        p[8 * b + e] = fma((double)vc[e].w, t3, d);
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) vc[e] = vn[e];
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) p[8 * b + e] = 0.0;
+    for (int e = 0; e < 8; ++e) {
+      double d = (double)vc[e].x * t0;
+      d = fma((double)vc[e].y, t1, d);
+      d = fma((double)vc[e].z, t2, d);
+      p[e] = fma((double)vc[e].w, t3, d);
     }
-  }
-  // reduce p[q] over the wave (8 rows per butterfly), then over the WPR waves of a row group
+    const double tot = wave_sum8_f64(p);
+    const int i = r0 + wave + 8 * (8 * b + idx);
+    if ((lane & 7) == 0 && i < r1) up[i] = tot;
 #pragma unroll
-  for (int q0 = 0; q0 < MAXR; q0 += 8) {
-    if (q0 < w.RPT) {
-      double v8[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v8[e] = p[q0 + e];
-      const double tot = wave_sum8_f64(v8);
-      const int idx = ((lane >> 5) & 1) * 4 + ((lane >> 4) & 1) * 2 + ((lane >> 3) & 1);
-      if ((lane & 7) == 0) ured[wave][q0 + idx] = tot;
-    }
-  }
-  __syncthreads();
-  for (int x = tid; x < RP * w.RPT; x += 512) {
-    const int rsx = x / w.RPT, q = x % w.RPT;
-    double u = 0.0;
-    for (int ww = 0; ww < WPR; ++ww) u += ured[rsx * WPR + ww][q];
-    const int i = r0 + rsx + RP * q;
-    if (i < r1) w.U[(int64_t)a * L + i] = u;
+    for (int e = 0; e < 8; ++e) vc[e] = vn[e];
   }
 }
 
 // ---------------------------------------------------------------------------
-// orth on 32 rows per block (256 threads = 32 rows x 8 k-groups).
+// orth on 32 rows per block (256 threads = 32 rows x 8 k-groups).  Thread
+// (row, kg) loads Q[k][row] for k = kg + 8 t (k < j) once, into registers, and
+// uses them for the q_j update, for z1 = u - Q h1 and for the h2 partials.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_lz_orth(LanczosWS w, int j) {
+  constexpr int MAXT = 32;                     // n_it <= 256
   const int a = blockIdx.y, g = blockIdx.x;
-  if (w.stop[a]) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int L = w.L, hs = w.ldq + 1;
   const int rl = tid & 31, kg = tid >> 5;
@@ -380,38 +379,53 @@ __global__ __launch_bounds__(256) void k_lz_orth(LanczosWS w, int j) {
   const int i = r0 + rl;
   const int ic = min(i, L - 1);
   const double* Qa = w.Q + (int64_t)a * w.ldq * L;
+  const int nt = (j - kg + 7) / 8;             // k = kg + 8 t < j
+  double qv[MAXT];
+#pragma unroll
+  for (int t = 0; t < MAXT; ++t)
+    if (8 * t < j) qv[t] = Qa[(int64_t)min(kg + 8 * t, max(j - 1, 0)) * L + ic];
   __shared__ double h1[264], h2[264];
   __shared__ double rq[8][33], rz[8][33];
   __shared__ double sz[32], sq[32];
+  double ui = 0.0, zi = 0.0, q0 = 0.0, bet = 1.0;
+  if (tid < 32) {
+    const int ns = w.m >> 8;                   // <= 8 column slices
+    const double* up = w.Upart + (int64_t)a * ns * L + ic;
+    double us[8];
+#pragma unroll
+    for (int sl = 0; sl < 8; ++sl) us[sl] = up[(int64_t)min(sl, ns - 1) * L];
+#pragma unroll
+    for (int sl = 0; sl < 8; ++sl)
+      if (sl < ns) ui += us[sl];
+    if (j > 0) {
+      zi = w.Z1[(int64_t)a * L + ic];
+      bet = w.beta[(int64_t)a * w.n_it + j - 1];
+    } else {
+      q0 = Qa[ic];
+    }
+  }
   for (int k = tid; k <= j; k += 256) h1[k] = w.H1[(int64_t)a * hs + k];
   for (int k = tid; k < j; k += 256) h2[k] = w.H2[(int64_t)a * hs + k];
+  if (w.stop[a]) return;
   __syncthreads();
   if (g == 0 && tid == 0) {
     w.alpha[(int64_t)a * w.n_it + j] = h1[j];
     w.amax[a] = fmax(j ? w.amax[a] : 0.0, fabs(h1[j]));
     w.neff[a] = j + 1;
   }
-  // one pass over Q_{j-1} on this block's rows: Q h2 (q_j update) and Q h1 (z1)
+  // Q_{j-1} h2 (q_j update) and Q_{j-1} h1 (z1) over this thread's k
   {
-    double aq[4] = {0, 0, 0, 0}, az[4] = {0, 0, 0, 0};
-    int k = kg;
-    for (; k + 24 < j; k += 32) {
-      double qv[4];
+    double aq[2] = {0, 0}, az[2] = {0, 0};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) qv[e] = Qa[(int64_t)(k + 8 * e) * L + ic];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        aq[e] = fma(qv[e], h2[k + 8 * e], aq[e]);
-        az[e] = fma(qv[e], h1[k + 8 * e], az[e]);
+    for (int t = 0; t < MAXT; ++t) {
+      if (t < nt) {
+        const int k = kg + 8 * t;
+        aq[t & 1] = fma(qv[t], h2[k], aq[t & 1]);
+        az[t & 1] = fma(qv[t], h1[k], az[t & 1]);
       }
     }
-    for (; k < j; k += 8) {
-      const double qv = Qa[(int64_t)k * L + ic];
-      aq[0] = fma(qv, h2[k], aq[0]);
-      az[0] = fma(qv, h1[k], az[0]);
-    }
-    rq[kg][rl] = (aq[0] + aq[1]) + (aq[2] + aq[3]);
-    rz[kg][rl] = (az[0] + az[1]) + (az[2] + az[3]);
+    rq[kg][rl] = aq[0] + aq[1];
+    rz[kg][rl] = az[0] + az[1];
   }
   __syncthreads();
   if (tid < 32) {
@@ -420,40 +434,44 @@ __global__ __launch_bounds__(256) void k_lz_orth(LanczosWS w, int j) {
       if (j > 0) {
         double sub = 0.0;
         for (int p = 0; p < 8; ++p) sub += rq[p][rl];
-        q = (w.Z1[(int64_t)a * L + i] - sub) / w.beta[(int64_t)a * w.n_it + j - 1];
+        q = (zi - sub) / bet;
         w.Q[((int64_t)a * w.ldq + j) * L + i] = q;
       } else {
-        q = Qa[i];
+        q = q0;
       }
       double zs = 0.0;
       for (int p = 0; p < 8; ++p) zs += rz[p][rl];
-      z = w.U[(int64_t)a * L + i] - fma(q, h1[j], zs);
+      z = ui - fma(q, h1[j], zs);
       w.Z1[(int64_t)a * L + i] = z;
     }
     sz[rl] = z;
     sq[rl] = q;
   }
   __syncthreads();
-  // partials of h2_k = sum over these rows of Q[k] z1, k <= j: thread (row, k-group),
-  // k = kb + 8 kg + e; 8 products per thread, summed over the 32 rows of each half wave
+  // partials of h2_k = sum over these rows of Q[k] z1 for k < j (from the registers,
+  // summed over the 32 rows of each half wave, 8 values per butterfly) and k = j
   double* hp = w.H2part + ((int64_t)a * w.G3 + g) * hs;
   const double zl = sz[rl];
-  for (int kb = 0; kb <= j; kb += 64) {
-    double v8[8];
+  const int idx = ((lane >> 4) & 1) * 4 + ((lane >> 3) & 1) * 2 + ((lane >> 2) & 1);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int k = kb + 8 * kg + e;
-      const double qv = (k < j) ? Qa[(int64_t)max(0, min(k, j - 1)) * L + ic] : sq[rl];
-      v8[e] = (k <= j) ? qv * zl : 0.0;
+  for (int t0 = 0; t0 < MAXT; t0 += 8) {
+    if (8 * t0 < j) {                          // block-uniform
+      double v8[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v8[e] = (t0 + e < nt) ? qv[t0 + e] * zl : 0.0;
+      const double tot = half_sum8_f64(v8);
+      const int k = kg + 8 * (t0 + idx);
+      if ((lane & 3) == 0 && k < j) hp[k] = tot;
     }
-    const double tot = half_sum8_f64(v8);
-    const int k = kb + 8 * kg + ((lane >> 4) & 1) * 4 + ((lane >> 3) & 1) * 2 + ((lane >> 2) & 1);
-    if ((lane & 3) == 0 && k <= j) hp[k] = tot;
   }
-  if (tid == 0) {
-    double nz = 0.0;
-    for (int p = 0; p < 32; ++p) nz = fma(sz[p], sz[p], nz);
-    hp[w.ldq] = nz;
+  if (tid < 64) {
+    // k = j and |z1|^2 over the 32 rows: lanes 0-31 and 32-63 of wave 0
+    const double v = (tid < 32) ? sq[rl] * sz[rl] : sz[rl] * sz[rl];
+    double t = v;
+#pragma unroll
+    for (int o = 16; o >= 1; o >>= 1) t += __shfl_xor(t, o, 64);
+    if (tid == 0) hp[j] = t;
+    if (tid == 32) hp[w.ldq] = t;
   }
 }
 
@@ -503,20 +521,6 @@ static void launch_timed(K kernel, dim3 grid, dim3 block, hipStream_t s, hipEven
   else hipLaunchKernelGGL(kernel, grid, block, 0, s, w, j);
 }
 
-static void phiu_launch(const LanczosWS& w, int j, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-  const dim3 grid((j + 8) / 8 + w.GB, w.n_act);
-  const int m4 = w.m / 4;
-  if (m4 <= 64) launch_timed(k_lz_phiu<64>, grid, dim3(512), s, e0, e1, w, j);
-  else if (m4 <= 128) launch_timed(k_lz_phiu<128>, grid, dim3(512), s, e0, e1, w, j);
-  else if (m4 <= 256) launch_timed(k_lz_phiu<256>, grid, dim3(512), s, e0, e1, w, j);
-  else launch_timed(k_lz_phiu<512>, grid, dim3(512), s, e0, e1, w, j);
-}
-
-int lanczos_m4(int m) {
-  const int m4 = m / 4;
-  return m4 <= 64 ? 64 : m4 <= 128 ? 128 : m4 <= 256 ? 256 : 512;
-}
-
 hipError_t launch_lanczos(const LanczosWS& w, const double* q1_act, hipStream_t s,
                           const hipEvent_t* ev_before, const hipEvent_t* ev_after) {
   (void)hipGetLastError();
@@ -527,8 +531,9 @@ hipError_t launch_lanczos(const LanczosWS& w, const double* q1_act, hipStream_t 
     launch_timed(k_lz_phit, dim3(nx + ns * w.GA, w.n_act), dim3(512), s,
                  ev_before ? ev_before[2 * j] : nullptr, ev_after ? ev_after[2 * j] : nullptr, w, j);
     hipLaunchKernelGGL(k_lz_finish, dim3(w.m / 16, w.n_act), dim3(256), 0, s, w, j);
-    phiu_launch(w, j, s, ev_before ? ev_before[2 * j + 1] : nullptr,
-                ev_after ? ev_after[2 * j + 1] : nullptr);
+    launch_timed(k_lz_phiu, dim3((j + 8) / 8 + ns * w.GA, w.n_act), dim3(512), s,
+                 ev_before ? ev_before[2 * j + 1] : nullptr,
+                 ev_after ? ev_after[2 * j + 1] : nullptr, w, j);
     hipLaunchKernelGGL(k_lz_orth, dim3(w.G3, w.n_act), dim3(256), 0, s, w, j);
   }
   hipLaunchKernelGGL(k_lz_last_beta, dim3(w.n_act), dim3(256), 0, s, w);

@@ -555,7 +555,8 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
     w.ldq = n_it + 1;
     w.tol = c->tol;
     {
-      // about four blocks per CU over all windows in each pass over Phi
+      // about four blocks per CU over all windows in each pass over Phi (blocks of
+      // RBA rows x 256 columns)
       const int64_t target = (int64_t)4 * c->n_cu;
       auto rows8 = [](int64_t rows) {          // multiple of 8 in [8, 32]
         rows = ((rows + 7) / 8) * 8;
@@ -566,17 +567,12 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
       w.RWA = rows8((L + 8 * ga - 1) / (8 * ga));
       w.RBA = 8 * w.RWA;
       w.GA = (int)((L + w.RBA - 1) / w.RBA);
-      const int rp = 512 / lanczos_m4((int)c->m);
-      const int64_t gb = std::max<int64_t>(1, target / na);
-      w.RPT = rows8((L + rp * gb - 1) / (rp * gb));
-      w.RBB = rp * w.RPT;
-      w.GB = (int)((L + w.RBB - 1) / w.RBB);
       w.G3 = (int)((L + 31) / 32);
     }
     const size_t hs = (size_t)w.ldq + 1;
     ENSURE(c, c->Q, (size_t)na * w.ldq * L * 8);
     ENSURE(c, c->T, (size_t)na * w.ldq * c->m * 8);
-    ENSURE(c, c->U, (size_t)na * L * 8);
+    ENSURE(c, c->U, (size_t)na * (c->m / 256) * L * 8);
     ENSURE(c, c->Z1, (size_t)na * L * 8);
     ENSURE(c, c->Spart, (size_t)na * w.GA * c->m * 8);
     ENSURE(c, c->H1, (size_t)na * hs * 8);
@@ -593,7 +589,7 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
     w.Phi = P<float>(c->Phi);
     w.Q = P<double>(c->Q);
     w.T = P<double>(c->T);
-    w.U = P<double>(c->U);
+    w.Upart = P<double>(c->U);
     w.Z1 = P<double>(c->Z1);
     w.Spart = P<double>(c->Spart);
     w.H1 = P<double>(c->H1);

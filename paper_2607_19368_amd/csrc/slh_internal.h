@@ -37,7 +37,7 @@ struct LanczosWS {
   const float* Phi;             // [n_act][L][m]
   double* Q;                    // [n_act][ldq][L]  Lanczos basis, vector-major
   double* T;                    // [n_act][ldq][m]  t_k = Phi^T q_k
-  double* U;                    // [n_act][L]       u = Phi t_j
+  double* Upart;                // [n_act][m/256][L] partials of u = Phi t_j per column slice
   double* Z1;                   // [n_act][L]       after the first Gram-Schmidt pass
   double* Spart;                // [n_act][GA][m]   partials of Phi^T z1 per row group
   double* H1;                   // [n_act][ldq+1]   Q_j^T u
@@ -49,11 +49,9 @@ struct LanczosWS {
   int* stop;                    // [n_act]  1 after breakdown
   double* amax;                 // [n_act]  max |alpha| so far (breakdown scale)
   double tol;
-  int GA, RBA, RWA;             // Phi^T v: row groups of RBA = 8 * RWA rows (RWA in {8,16,24,32})
-  int GB, RBB, RPT;             // Phi t: row blocks of RBB = (512 / M4) * RPT rows (RPT in {8,..,32})
+  int GA, RBA, RWA;             // both passes: row groups of RBA = 8 * RWA rows (RWA in {8,16,24,32})
   int G3;                       // orthogonalisation blocks of 32 rows
 };
-int lanczos_m4(int m);   // threads per Phi row in the passes (power of two >= m / 4)
 // ev_before/ev_after (may be NULL): 2 * n_it events each, receiving the start
 // and end timestamps of the two Phi passes of every step (index 2j: Phi^T v,
 // 2j + 1: Phi t_j).
