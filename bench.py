@@ -21,6 +21,25 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 
 
+def measured_traffic(workload):
+    """HBM bytes per pass over Phi from the committed counter summary, if it was
+    taken on the current kernel source and this workload; else None."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "lanczos_passes_qwen7b_traffic.md")
+    src = os.path.join(ROOT, "paper_2607_19368_amd", "csrc", "k_lanczos.hip")
+    if workload != "qwen7b" or not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if ":" in line and not line.startswith(("|", "`", " ")):
+            k, _, v = line.partition(":")
+            fields[k.strip()] = v.strip()
+    cur = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if fields.get("k_lanczos.hip sha256") != cur or "traffic_bytes_per_pass" not in fields:
+        return None
+    return float(fields["traffic_bytes_per_pass"])
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -166,7 +185,9 @@ def main():
         alg = n_win * (4.0 * L * wl.m + 8.0 * (L + wl.m))
         ach = alg / (pass_ms * 1e-3) / 1e9
         out["roofline"] = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                           "frac": ach / HBM_PEAK_GBS, "traffic": None,
+                           "frac": ach / HBM_PEAK_GBS, "traffic": measured_traffic(wl.name),
+                           "traffic_unit": "HBM bytes per pass (FETCH_SIZE + WRITE_SIZE, "
+                                           "copy-calibrated; profiles/lanczos_passes_qwen7b_traffic.md)",
                            "kernel": "k_lz_phit + k_lz_phiu (t = Phi^T q and u = Phi t)",
                            "bytes_per_launch": alg, "avg_launch_ms": pass_ms}
         fm_ms = stage_sum["featmap_ms"] / K
