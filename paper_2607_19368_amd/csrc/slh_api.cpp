@@ -344,13 +344,15 @@ int slh_create(slh_ctx** out, int64_t N, int64_t D, int64_t m, int32_t r, int32_
   hipDeviceProp_t prop;
   if (hipGetDeviceProperties(&prop, c->device) == hipSuccess) c->n_cu = prop.multiProcessorCount;
   route_all_spectral(c);
-  // parameters: W transposed to [m][D] for K-contiguous MFMA operands
-  std::vector<uint16_t> W((size_t)(D * m)), Wt((size_t)(D * m));
+  // parameters: W transposed to [m][Dp] for K-contiguous MFMA operands, K padded
+  // with zeros to a multiple of 64 so the GEMM's K tail needs no masking
+  const int64_t Dp = ((D + 63) / 64) * 64;
+  std::vector<uint16_t> W((size_t)(D * m)), Wt((size_t)(Dp * m), 0);
   std::vector<float> psi((size_t)m);
   std::vector<double> R((size_t)r * bits);
   slh_gen_params(seed, D, m, r, bits, W.data(), psi.data(), R.data());
   for (int64_t k = 0; k < D; ++k)
-    for (int64_t j = 0; j < m; ++j) Wt[(size_t)(j * D + k)] = W[(size_t)(k * m + j)];
+    for (int64_t j = 0; j < m; ++j) Wt[(size_t)(j * Dp + k)] = W[(size_t)(k * m + j)];
   int rc = SLH_OK;
   if ((rc = ensure(c, c->Wt, Wt.size() * 2)) || (rc = ensure(c, c->psi, psi.size() * 4)) ||
       (rc = ensure(c, c->R, R.size() * 8))) {
@@ -513,6 +515,7 @@ int slh_feature_map(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx) {
   a.n_rows = rows;
   a.L = L;
   a.D = (int)c->D;
+  a.ldw = (int)(((c->D + 63) / 64) * 64);
   a.m = (int)c->m;
   HIP_TRY(c, launch_featmap(a, c->stream, c->timing ? c->ev[0] : nullptr,
                             c->timing ? c->ev[1] : nullptr));

@@ -18,7 +18,7 @@ hipError_t launch_rownorm(const void* X, int dtype, int64_t ldx, int64_t N, int 
 struct FeatmapArgs {
   const uint16_t* X;      // bf16 rows, global token index, row stride ldx
   int64_t ldx;
-  const uint16_t* Wt;     // [m][D] bf16 (transposed projection)
+  const uint16_t* Wt;     // [m][ldw] bf16 (transposed projection, zero for k >= D)
   const float* psi;       // [m]
   const float* rowscale;  // [N] global token index
   float* Phi;             // [n_rows][m]
@@ -26,6 +26,7 @@ struct FeatmapArgs {
   int64_t n_rows;         // n_act * L
   int64_t L;
   int D, m;
+  int ldw;                // D rounded up to a multiple of 64
 };
 // e0/e1 (may be NULL): receive the kernel's own start / end timestamps.
 hipError_t launch_featmap(const FeatmapArgs& a, hipStream_t s, hipEvent_t e0 = nullptr,
