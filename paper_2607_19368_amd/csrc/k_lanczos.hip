@@ -140,6 +140,23 @@ __device__ __forceinline__ double block_colsum(const double* __restrict__ src, i
   return t;
 }
 
+// Block g of nx = ceil(j / 16) + 1 (512 threads): H2[k] = sum over the orth
+// blocks of the h2 partials for k in [16 g, 16 g + 16) (k < j), or, for the
+// last block, |z1|^2 (slot ldq).
+__device__ __forceinline__ void h2_reduce_block(const LanczosWS& w, int a, int j, int g, int nx) {
+  const int hs = w.ldq + 1;
+  const double* hp = w.H2part + (int64_t)a * w.G3 * hs;
+  double* dst = w.H2 + (int64_t)a * hs;
+  if (g == nx - 1) {
+    const double v = block_colsum<1, 512>(hp + w.ldq, hs, w.G3, 0, 1);
+    if (threadIdx.x == 0) dst[w.ldq] = v;
+  } else {
+    const int c0 = g * 16;
+    const double v = block_colsum<16, 512>(hp, hs, w.G3, c0, j);
+    if (threadIdx.x < 16 && c0 + threadIdx.x < j) dst[c0 + threadIdx.x] = v;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // phit: blocks [0, nx) reduce h2 (k < j) and |z1|^2 of step j-1 over the orth
 // blocks; the rest own (row group rg, 256-column slice sl): each of the 8
@@ -155,16 +172,7 @@ __global__ __launch_bounds__(512) void k_lz_phit(LanczosWS w, int j) {
   int g = blockIdx.x;
   if (g < nx) {
     if (w.stop[a]) return;
-    const double* hp = w.H2part + (int64_t)a * w.G3 * hs;
-    double* dst = w.H2 + (int64_t)a * hs;
-    if (g == nx - 1) {                         // |z1|^2 (slot ldq)
-      const double v = block_colsum<1, 512>(hp + w.ldq, hs, w.G3, 0, 1);
-      if (tid == 0) dst[w.ldq] = v;
-    } else {
-      const int c0 = g * 16;
-      const double v = block_colsum<16, 512>(hp, hs, w.G3, c0, j);
-      if (tid < 16 && c0 + tid < j) dst[c0 + tid] = v;
-    }
+    h2_reduce_block(w, a, j, g, nx);
     return;
   }
   g -= nx;
@@ -475,23 +483,27 @@ __global__ __launch_bounds__(256) void k_lz_orth(LanczosWS w, int j) {
   }
 }
 
-// beta of the last step (reported; T does not use it): one block per window
-// reduces h2 and |z1|^2 of the last orthogonalisation.
+// beta of the last step (reported; T does not use it): h2 and |z1|^2 of the last
+// orthogonalisation are reduced as at the start of a step, then
+// beta = sqrt(|z1|^2 - |h2|^2).
+__global__ __launch_bounds__(512) void k_lz_h2sum(LanczosWS w) {
+  const int a = blockIdx.y;
+  if (w.stop[a]) return;
+  const int j = w.n_it, nx = (j + 15) / 16 + 1;
+  h2_reduce_block(w, a, j, blockIdx.x, nx);
+}
+
 __global__ __launch_bounds__(256) void k_lz_last_beta(LanczosWS w) {
   const int a = blockIdx.x, tid = threadIdx.x;
   if (w.stop[a]) return;
   const int j = w.n_it, hs = w.ldq + 1;
-  const double* hp = w.H2part + (int64_t)a * w.G3 * hs;
+  const double* H2 = w.H2 + (int64_t)a * hs;
   __shared__ double red[4];
   double hh = 0.0;
-  for (int c0 = 0; c0 < j; c0 += 16) {
-    const double v = block_colsum<16, 256>(hp, hs, w.G3, c0, j);
-    if (tid < 16) hh = fma(v, v, hh);
-  }
-  const double nz = block_colsum<1, 256>(hp + w.ldq, hs, w.G3, 0, 1);
+  for (int k = tid; k < j; k += 256) hh = fma(H2[k], H2[k], hh);
   hh = block_sum_f64(hh, red);
   if (tid == 0) {
-    const double b2 = nz - hh;
+    const double b2 = H2[w.ldq] - hh;
     w.beta[(int64_t)a * w.n_it + j - 1] = b2 > 0.0 ? sqrt(b2) : 0.0;
   }
 }
@@ -536,6 +548,7 @@ hipError_t launch_lanczos(const LanczosWS& w, const double* q1_act, hipStream_t 
                  ev_after ? ev_after[2 * j + 1] : nullptr, w, j);
     hipLaunchKernelGGL(k_lz_orth, dim3(w.G3, w.n_act), dim3(256), 0, s, w, j);
   }
+  hipLaunchKernelGGL(k_lz_h2sum, dim3((w.n_it + 15) / 16 + 1, w.n_act), dim3(512), 0, s, w);
   hipLaunchKernelGGL(k_lz_last_beta, dim3(w.n_act), dim3(256), 0, s, w);
   return hipGetLastError();
 }

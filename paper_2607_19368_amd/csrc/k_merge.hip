@@ -1,7 +1,9 @@
 // Macro-token construction (Eq. 7, section 3.4 max positions, section 3.6
 // ordering by representative position).
 //
-// book      one workgroup per window.  Spectral windows: stable LSD radix sort
+// book      one workgroup per window.  Windows of up to 16384 tokens are sorted
+//           in LDS (k_mg_book_lds: bitonic network on (code, token) keys);
+//           longer ones use global memory.  Spectral windows: stable LSD radix sort
 //           of (code, token) by code with 8-bit digits (histogram, scan and a
 //           stable scatter whose in-wave ranks come from ballot matching), so
 //           every bucket becomes a run of ascending token indices; a bucket's
@@ -172,6 +174,83 @@ __global__ __launch_bounds__(1024) void k_mg_book(MergeWS w) {
     w.sloc[base + s] = segk[segid[s]];
   }
   if (tid == 0) w.mw[win] = nseg;
+}
+
+// Book-keeping of a window held in LDS (L <= 16384): sort the keys
+// (code << tb) | local token (tb = log2 P, P = L rounded up to a power of two,
+// padded with all-ones keys) with a bitonic network, which orders each bucket's
+// members by token; flag each bucket's last token, an exclusive scan over
+// tokens gives the representatives' ranks, and each sorted position finds its
+// bucket's last member by binary search.  Same outputs as k_mg_book.
+// Dynamic LDS: P keys + L ranks.
+__global__ __launch_bounds__(1024) void k_mg_book_lds(MergeWS w, int P, int tb) {
+  extern __shared__ uint32_t mg_dyn[];
+  uint32_t* key = mg_dyn;                 // [P]
+  int* R = (int*)(mg_dyn + P);            // [L]
+  __shared__ int wsum[16];
+  const int win = blockIdx.x, tid = threadIdx.x;
+  const int L = w.L;
+  const int64_t base = (int64_t)win * L;
+  if (!w.route[win]) {
+    const int k = w.chunk_k;
+    for (int s = tid; s < L; s += 1024) {
+      w.sval[base + s] = (int)(base + s);
+      w.sloc[base + s] = s / k;
+    }
+    if (tid == 0) w.mw[win] = (L + k - 1) / k;
+    return;
+  }
+  const uint32_t tmask = (1u << tb) - 1u;
+  for (int i = tid; i < P; i += 1024)
+    key[i] = (i < L) ? ((w.codes[base + i] << tb) | (uint32_t)i) : 0xFFFFFFFFu;
+  for (int i = tid; i < L; i += 1024) R[i] = 0;
+  __syncthreads();
+  // bitonic sort, ascending
+  for (int k = 2; k <= P; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int t = tid; t < (P >> 1); t += 1024) {
+        const int i = 2 * t - (t & (j - 1));      // lower index of the pair, bit j clear
+        const int l = i + j;
+        const uint32_t ki = key[i], kl = key[l];
+        const bool up = (i & k) == 0;
+        if ((ki > kl) == up) {
+          key[i] = kl;
+          key[l] = ki;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // representatives: the last member of each bucket
+  for (int s = tid; s < L; s += 1024) {
+    const uint32_t c = key[s] >> tb;
+    if (s == L - 1 || (key[s + 1] >> tb) != c) R[key[s] & tmask] = 1;
+  }
+  __syncthreads();
+  // exclusive scan over tokens: R[t] = number of representatives before t
+  int carry = 0;
+  for (int b0 = 0; b0 < L; b0 += 1024) {
+    const int i = b0 + tid;
+    const int f = (i < L) ? R[i] : 0;
+    int tot;
+    const int inc = block_incl_scan_1024(f, wsum, tot);
+    if (i < L) R[i] = carry + inc - f;
+    carry += tot;
+    __syncthreads();
+  }
+  for (int s = tid; s < L; s += 1024) {
+    const uint32_t ks = key[s];
+    const uint32_t bound = ((ks >> tb) + 1u) << tb;  // first key of the next code
+    int lo = s, hi = L;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (key[mid] < bound) lo = mid + 1;
+      else hi = mid;
+    }
+    w.sval[base + s] = (int)(base + (ks & tmask));
+    w.sloc[base + s] = R[key[lo - 1] & tmask];
+  }
+  if (tid == 0) w.mw[win] = carry;
 }
 
 __global__ __launch_bounds__(1024) void k_mg_wbase(MergeWS w) {
@@ -501,7 +580,23 @@ int merge_nchunks(int64_t N, int CH) { return (int)((N + CH - 1) / CH); }
 hipError_t launch_merge(const MergeWS& w, const void* X, int dtype, int64_t ldx, float* E,
                         int* P, int* tok2macro, hipStream_t s) {
   (void)hipGetLastError();
-  hipLaunchKernelGGL(k_mg_book, dim3(w.n_win), dim3(1024), 0, s, w);
+  if (w.L <= 16384) {
+    int P = 1, tb = 0;
+    while (P < w.L) {
+      P <<= 1;
+      ++tb;
+    }
+    const size_t bytes = (size_t)P * 4 + (size_t)w.L * 4;
+    if (bytes > 65536) {
+      const hipError_t e = hipFuncSetAttribute((const void*)k_mg_book_lds,
+                                               hipFuncAttributeMaxDynamicSharedMemorySize,
+                                               (int)bytes);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(k_mg_book_lds, dim3(w.n_win), dim3(1024), bytes, s, w, P, tb);
+  } else {
+    hipLaunchKernelGGL(k_mg_book, dim3(w.n_win), dim3(1024), 0, s, w);
+  }
   hipLaunchKernelGGL(k_mg_wbase, dim3(1), dim3(1024), 0, s, w);
   hipLaunchKernelGGL(k_mg_finalize, dim3((unsigned)((w.N + 255) / 256)), dim3(256), 0, s, w, P,
                      tok2macro);
