@@ -178,16 +178,20 @@ T* P(DevBuf& b) {
   return (T*)b.p;
 }
 
+// Timing events only measure: no system-scope fence (cache writeback) when they
+// complete, which would otherwise slow the kernels that follow them; readers
+// synchronise the stream before reading them.
 int make_events(slh_ctx* c, int n_fused) {
+  const unsigned fl = hipEventDisableSystemFence;
   if (!c->ev_made) {
     for (auto& e : c->ev)
-      HIP_TRY(c, hipEventCreate(&e));
+      HIP_TRY(c, hipEventCreateWithFlags(&e, fl));
     c->ev_made = true;
   }
   while ((int)c->ev_fb.size() < n_fused) {
     hipEvent_t a, b;
-    HIP_TRY(c, hipEventCreate(&a));
-    HIP_TRY(c, hipEventCreate(&b));
+    HIP_TRY(c, hipEventCreateWithFlags(&a, fl));
+    HIP_TRY(c, hipEventCreateWithFlags(&b, fl));
     c->ev_fb.push_back(a);
     c->ev_fa.push_back(b);
   }
