@@ -45,6 +45,12 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 #ifndef FM_BIG_BN
 #define FM_BIG_BN 256            // N extent of the large tile (256 x FM_BIG_BN)
 #endif
+#ifndef FM_SROWS
+#define FM_SROWS 32              // epilogue rows staged per pass (16 or 32)
+#endif
+#ifndef FM_BIG_WGM
+#define FM_BIG_WGM 2             // waves along M in the large tile
+#endif
 #ifndef FM_BIG_WGN
 #define FM_BIG_WGN 4             // waves along N in the 256 x 256 tile (2 x FM_BIG_WGN waves)
 #endif
@@ -237,59 +243,62 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_featmap(FeatmapArgs a) {
   // cos(. + psi) * rowscale while streaming rows out with 16-byte stores.
   // Accumulator layout: lane holds column (lane & 31) of each 32x32 tile, rows
   // 8*(v/4) + 4*(lane/32) + (v%4).
-  constexpr int HM = 1;                              // MFMA row tiles staged per pass
   // pad 8 floats: rows 4 apart (the two half-waves of a store) start 32 banks apart
-  constexpr int SROWS = HM * 32, SCOLS = WN + 8;     // staged rows x (cols + pad)
+  constexpr int SROWS = FM_SROWS, SCOLS = WN + 8;    // staged rows x (cols + pad)
+  constexpr int NV = SROWS / 2;                      // accumulator values per lane per pass
+  static_assert(SROWS == 16 || SROWS == 32, "stage 16 or 32 rows at a time");
   static_assert(WGM * WGN * SROWS * SCOLS * 4 <= FM_NS * (STAGE_A + STAGE_B) * 2, "staging exceeds LDS");
   float* stage = (float*)smem + wave * (SROWS * SCOLS);
 #pragma unroll
-  for (int h = 0; h < TM / HM; ++h) {
+  for (int h = 0; h < TM; ++h) {
 #pragma unroll
-    for (int ii = 0; ii < HM; ++ii) {
+    for (int hf = 0; hf < 32 / SROWS; ++hf) {
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int r = 32 * ii + 8 * (v >> 2) + 4 * fk + (v & 3);
-          stage[r * SCOLS + 32 * j + fr] = acc[h * HM + ii][j][v];
+        for (int vv = 0; vv < NV; ++vv) {
+          const int v = hf * NV + vv;
+          const int r = 8 * (v >> 2) + 4 * fk + (v & 3) - hf * SROWS;
+          stage[r * SCOLS + 32 * j + fr] = acc[h][j][v];
         }
       }
-    }
 #if FM_EPI == 1
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #else
-    __syncthreads();
+      __syncthreads();
 #endif
-    // lane handles float4 column chunk (lane % (WN/4)) of rows lane / (WN/4) + k * (256/WN)
-    constexpr int CPR = WN / 4;                      // float4 chunks per row
-    constexpr int RPI = 64 / CPR;                    // rows per pass
-    const int cc = lane % CPR, rr = lane / CPR;
-    const int col = n0 + wn * WN + 4 * cc;
-    const float4 ps = *(const float4*)(a.psi + col);
-    for (int r = rr; r < SROWS; r += RPI) {
-      const int row = m0 + wm * WM + h * SROWS + r;
-      if (row < n_rows) {
-        const float sc = a.rowscale[fm_global_row(row, a.winlist, (int)a.L)];
-        const float4 v = *(const float4*)(&stage[r * SCOLS + 4 * cc]);
-        float4 o;
-        o.x = cosf(v.x + ps.x) * sc;
-        o.y = cosf(v.y + ps.y) * sc;
-        o.z = cosf(v.z + ps.z) * sc;
-        o.w = cosf(v.w + ps.w) * sc;
-        *(float4*)(a.Phi + (int64_t)row * a.m + col) = o;
+      // lane handles float4 column chunk (lane % (WN/4)) of rows lane / (WN/4) + k * (256/WN)
+      constexpr int CPR = WN / 4;                    // float4 chunks per row
+      constexpr int RPI = 64 / CPR;                  // rows per pass
+      const int cc = lane % CPR, rr = lane / CPR;
+      const int col = n0 + wn * WN + 4 * cc;
+      const float4 ps = *(const float4*)(a.psi + col);
+      for (int r = rr; r < SROWS; r += RPI) {
+        const int row = m0 + wm * WM + h * 32 + hf * SROWS + r;
+        if (row < n_rows) {
+          const float sc = a.rowscale[fm_global_row(row, a.winlist, (int)a.L)];
+          const float4 v = *(const float4*)(&stage[r * SCOLS + 4 * cc]);
+          float4 o;
+          o.x = cosf(v.x + ps.x) * sc;
+          o.y = cosf(v.y + ps.y) * sc;
+          o.z = cosf(v.z + ps.z) * sc;
+          o.w = cosf(v.w + ps.w) * sc;
+          *(float4*)(a.Phi + (int64_t)row * a.m + col) = o;
+        }
       }
-    }
 #if FM_EPI == 1
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #else
-    __syncthreads();
+      __syncthreads();
 #endif
+    }
   }
 }
+
 
 
 hipError_t launch_featmap(const FeatmapArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
@@ -298,8 +307,8 @@ hipError_t launch_featmap(const FeatmapArgs& a, hipStream_t s, hipEvent_t e0, hi
   // 256 x 256 tiles when that still gives at least one tile per CU, else 128 x 128
   int64_t t256 = ((a.n_rows + 255) / 256) * (a.m / FM_BIG_BN);
   if (a.m % FM_BIG_BN == 0 && t256 >= 256) {
-    auto k = k_featmap<256, FM_BIG_BN, 2, FM_BIG_WGN>;
-    const dim3 blk(64 * 2 * FM_BIG_WGN);
+    auto k = k_featmap<256, FM_BIG_BN, FM_BIG_WGM, FM_BIG_WGN>;
+    const dim3 blk(64 * FM_BIG_WGM * FM_BIG_WGN);
     if (e0) hipExtLaunchKernelGGL(k, dim3((unsigned)t256), blk, 0, s, e0, e1, 0, a);
     else hipLaunchKernelGGL(k, dim3((unsigned)t256), blk, 0, s, a);
   } else {

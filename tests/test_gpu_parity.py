@@ -281,3 +281,51 @@ def test_call_order_and_capacity_errors():
         P.slh_merge(ctx, Xd, emb_out=small)
     with pytest.raises(B.SLHError, match=r"\(-1\)"):
         P.slh_feature_map(ctx, Xd[:, 1:])     # misaligned rows
+
+
+def test_strided_rows():
+    """X given as a view with row stride D + 24 (padded rows): same results as the
+    contiguous layout, and parity with the oracle."""
+    import torch
+    inp = _custom("strided", 1024, 512, 256, 24, 8, 8)
+    wl = inp.workload
+    Xc = PR.to_device_x(inp)
+    pad = torch.zeros((wl.N, wl.D + 24), dtype=Xc.dtype, device=Xc.device)
+    pad[:, :wl.D] = Xc
+    Xs = pad[:, :wl.D]
+    assert Xs.stride(0) == wl.D + 24
+    gs = PR.run_gpu(inp, n_it=wl.n_it, X=Xs)
+    gc = PR.run_gpu(inp, n_it=wl.n_it, X=Xc)
+    assert np.array_equal(gs.E, gc.E) and np.array_equal(gs.t2m, gc.t2m)
+    o = PR.run_oracle(inp, n_it=wl.n_it)
+    rep = PR.compare(o, gs, wl.N)
+    _say(f"[strided] {rep}")
+
+
+def test_windows_with_and_without_breakdown():
+    """Four windows in one batch: windows 0 and 2 hold a single repeated row
+    (rank-one operator: Lanczos stops after two steps), windows 1 and 3 are
+    Zipf embeddings (no breakdown).  Each window must stop, hash and merge on
+    its own, as in the oracle."""
+    L = 256
+    base = _custom("mixwin", 4 * L, 256, 256, 20, 6, 6)
+    X = base.X.copy()
+    X[0:L] = X[0]
+    X[2 * L:3 * L] = X[2 * L + 5]
+    inp = Inputs(base.workload, X, base.ids)
+    g = PR.run_gpu(inp, n_it=20, window=L)
+    o = PR.run_oracle(inp, n_it=20, window=L)
+    iters_g = [w.iters for w in g.windows]
+    iters_o = [w.iters for w in o.windows]
+    _say(f"[mixed windows] iters gpu={iters_g} oracle={iters_o}")
+    assert iters_g == iters_o and iters_g[0] == iters_g[2] == 2 and iters_g[1] == iters_g[3] == 20
+    for w in (1, 3):
+        gw, ow = g.windows[w], o.windows[w]
+        rel = np.abs(gw.ritz - ow.ritz) / np.abs(ow.ritz)
+        assert rel.max() <= PR.RITZ_REL
+        assert PR.subspace_angle(ow.Z, gw.Z) < PR.ANGLE
+    for w in (0, 2):
+        gw, ow = g.windows[w], o.windows[w]
+        assert np.all(gw.Z[:, :4] == 0) and np.all(gw.ritz[:4] == 0)
+        assert abs(gw.ritz[-1] - ow.ritz[-1]) < 1e-5 * ow.ritz[-1]
+    PR.compare(o, g, L, check_spectral=False)
