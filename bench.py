@@ -111,7 +111,7 @@ def main():
     if wl.window:
         P.slh_set_option(ctx, B.SLH_OPT_WINDOW_LEN, wl.window)
     tau = -1.0
-    if wl.window:
+    if wl.adaptive:
         # routing threshold: midpoint of the 32nd and 33rd largest window scores
         _, sc = P.slh_route(ctx, X, wl.rho, -1.0)
         s = np.sort(sc)[::-1]
@@ -122,7 +122,7 @@ def main():
     T2M = torch.empty(wl.N, dtype=torch.int32, device="cuda")
 
     def step():
-        if wl.window:
+        if wl.adaptive:
             P.slh_route(ctx, X, wl.rho, tau)
         P.slh_feature_map(ctx, X)
         P.slh_lanczos(ctx, wl.n_it, want=False)

@@ -4,7 +4,8 @@ seeded inputs and compares them under the parity rules:
   * bucket codes, token->bucket maps and positions bit-exact, except rows where
     some oracle SimHash projection has |value| < 1e-5 (and every bucket that
     holds such a row, on either side);
-  * kept Ritz values within 1e-3 relative error;
+  * kept Ritz values within 1e-3 relative error (values that are zero up to
+    rounding, below 1e-12 of the largest, within that absolute floor);
   * largest principal angle between the GPU and oracle Ritz subspaces < 1e-2 rad;
   * macro-token embeddings within 1e-3 relative error (fp32 accumulation).
 """
@@ -55,6 +56,7 @@ class Run:
     Phi: np.ndarray = None
     scores: np.ndarray = None
     route: np.ndarray = None
+    R: np.ndarray = None             # SimHash hyperplanes (oracle runs)
 
 
 def run_gpu(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel=0, compact=False,
@@ -152,6 +154,7 @@ def run_oracle(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel="softmax"
         base += len(Pw)
     run.E = np.concatenate(Es)
     run.P = np.concatenate(Ps)
+    run.R = R
     if compact:
         run.P = np.arange(len(run.P))
     run.t2m = t2m
@@ -204,6 +207,7 @@ class Report:
     buckets_checked: int = 0
     buckets_excluded: int = 0
     undetermined_rows: int = 0
+    undecided_windows: int = 0
 
 
 def compare(o, g, L, check_spectral=True, ritz_rel=RITZ_REL, angle=ANGLE, emb_rel=EMB_REL,
@@ -225,17 +229,56 @@ def compare(o, g, L, check_spectral=True, ritz_rel=RITZ_REL, angle=ANGLE, emb_re
     excluded_tok = np.zeros(N, bool)
     for w, a in ow.items():
         b = gw[w]
-        assert a.iters == b.iters, (w, a.iters, b.iters)
+        floor_a = 1e-12 * float(np.abs(a.ritz).max(initial=0))
+        floor_b = 1e-12 * float(np.abs(b.ritz).max(initial=0))
+        undecided = False
+        if a.iters != b.iters:
+            # Only where the operator's rank ran out inside the Krylov space: the
+            # step that decides the breakdown then compares a rounding-noise beta
+            # with the threshold, and the extra steps add Ritz values that are
+            # zero up to rounding.  Both sides must show such values; the
+            # window's SimHash bits are not determined.
+            tiny_a = np.count_nonzero((a.ritz != 0) & (np.abs(a.ritz) <= floor_a))
+            tiny_b = np.count_nonzero((b.ritz != 0) & (np.abs(b.ritz) <= floor_b))
+            assert max(tiny_a, tiny_b) > 0 and abs(a.iters - b.iters) <= max(tiny_a, tiny_b), \
+                (w, a.iters, b.iters)
+            undecided = True
+            rep.undecided_windows += 1
         if check_spectral:
-            keep = a.ritz != 0
-            rel = np.abs(b.ritz[keep] - a.ritz[keep]) / np.abs(a.ritz[keep])
+            # Ritz values that are zero up to rounding (a rank-deficient operator
+            # inside the Krylov space) have no relative accuracy: they are checked
+            # against an absolute floor of 1e-12 of the largest one instead, and
+            # their Ritz vectors (directions of the null space that rounding
+            # picked) are left out of the subspace comparison.  Columns are in
+            # ascending order, so the determined ones align from the top.
+            ka = np.flatnonzero(np.abs(a.ritz) > floor_a)
+            kb = np.flatnonzero(np.abs(b.ritz) > floor_b)
+            assert len(ka) == len(kb), (w, len(ka), len(kb))
+            rel = np.abs(b.ritz[kb] - a.ritz[ka]) / np.abs(a.ritz[ka])
             rep.max_ritz_rel = max(rep.max_ritz_rel, float(rel.max(initial=0)))
             assert np.all(rel <= ritz_rel), (w, rel.max())
-            cols = np.flatnonzero(keep)
-            ang = subspace_angle(a.Z[:, cols], b.Z[:, cols])
+            if not undecided:
+                tiny = (a.ritz != 0) & (np.abs(a.ritz) <= floor_a)
+                assert np.all(np.abs(b.ritz[tiny] - a.ritz[tiny]) <= floor_a), (w, b.ritz[tiny], a.ritz[tiny])
+            ang = subspace_angle(a.Z[:, ka], b.Z[:, kb])
             rep.max_angle = max(rep.max_angle, ang)
             assert ang < angle, (w, ang)
+        if undecided:
+            rep.undetermined_rows += L
+            rep.excluded_rows += L
+            excluded_tok[w * L:(w + 1) * L] = True
+            continue
         ex = np.any(np.abs(a.proj) < EXCL, axis=1)
+        tiny = (a.ritz != 0) & (np.abs(a.ritz) <= floor_a)
+        if np.count_nonzero(tiny) >= 2 and o.R is not None:
+            # a null space of dimension >= 2 inside the Krylov space: any basis of
+            # it is a valid set of Ritz vectors, so a bit is determined only where
+            # no rotation of that basis can flip it (Cauchy-Schwarz bound)
+            zt = np.linalg.norm(a.Z[:, tiny], axis=1)[:, None]
+            rt = np.linalg.norm(o.R[tiny], axis=0)[None, :]
+            und = np.any(np.abs(a.proj) <= zt * rt, axis=1) & ~ex
+            rep.undetermined_rows += int(und.sum())
+            ex |= und
         if unc is not None and w in unc:
             thr = max(EXCL, 2.0 * unc[w])
             und = np.any(np.abs(a.proj) < thr, axis=1) & ~ex

@@ -329,3 +329,26 @@ def test_windows_with_and_without_breakdown():
         assert np.all(gw.Z[:, :4] == 0) and np.all(gw.ritz[:4] == 0)
         assert abs(gw.ritz[-1] - ow.ritz[-1]) < 1e-5 * ow.ritz[-1]
     PR.compare(o, g, L, check_spectral=False)
+
+
+def test_end_to_end_local16():
+    """Local backend at the paper's defaults: windows of 16 tokens, m = 256, a
+    full 16-step Krylov space per window (reduced to 64 windows here).  A window
+    holding repeated tokens has a rank-deficient operator; with r = 16 all of its
+    Ritz vectors are kept, including a basis of the null space inside the Krylov
+    space, which the method leaves arbitrary when it is 2-dimensional or more.
+    Such windows' SimHash bits are not determined, and the oracle's own
+    reversed-order evaluation (parity.oracle_uncertainty) marks them."""
+    inp = make_inputs("local16", N=1024)
+    wl = inp.workload
+    _say(f"[e2e] local16 N={wl.N} window={wl.window} n_it={wl.n_it} r={wl.r} bits={wl.bits}")
+    g = PR.run_gpu(inp, n_it=wl.n_it, window=wl.window)
+    o = PR.run_oracle(inp, n_it=wl.n_it, window=wl.window)
+    iters = sorted({w.iters for w in o.windows})
+    unc = {w.w: PR.oracle_uncertainty(inp, w.w, wl.window, wl.n_it) for w in o.windows}
+    determined = sum(u < PR.EXCL for u in unc.values())
+    _say(f"   oracle steps per window: {iters}; windows with determined bits: {determined}/{len(unc)}")
+    assert determined >= len(unc) // 2
+    rep = PR.compare(o, g, wl.window, unc=unc)
+    _say(f"   {rep}  M={len(g.P)}")
+    assert rep.undecided_windows <= len(unc) // 8

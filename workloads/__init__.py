@@ -16,6 +16,7 @@ the same shapes:
                 windows repeat a Zipf template of period U{16..64} with 10% of
                 positions replaced by fresh Zipf draws (JSON/code/table-like
                 redundancy), odd windows are i.i.d. Zipf(1.1).
+  local16       the qwen7b prompt cut into 512 windows of 16 tokens (local backend).
 
 Table rows are generated per id on demand (row id -> its own seeded stream), so
 the 152064-row tables are never materialised.
@@ -38,6 +39,7 @@ class Workload:
     vocab: int = 0
     window: int = 0   # window length (0 = one global window)
     x_dtype: str = "bf16"
+    adaptive: bool = False   # windows alternate periodic / i.i.d. streams and are routed
 
 
 WORKLOADS = {
@@ -45,7 +47,11 @@ WORKLOADS = {
     "mistral7b": Workload("mistral7b", 4096, 4096, 1024, 64, 32, 10, 8.0, 32768),
     "qwen7b": Workload("qwen7b", 8192, 3584, 2048, 96, 64, 12, 16.0, 152064),
     "qwen14b_long": Workload("qwen14b_long", 32768, 5120, 2048, 128, 64, 14, 16.0, 152064),
-    "adaptive64": Workload("adaptive64", 64 * 2048, 4096, 1024, 48, 32, 10, 8.0, 32768, 2048),
+    "adaptive64": Workload("adaptive64", 64 * 2048, 4096, 1024, 48, 32, 10, 8.0, 32768, 2048,
+                           "bf16", True),
+    # local backend at the paper's defaults (section 5.1): windows of 16 tokens,
+    # 256 random features, a full 16-step Krylov space, b = ceil(log2(16 / rho))
+    "local16": Workload("local16", 8192, 3584, 256, 16, 16, 2, 4.0, 152064, 16),
 }
 
 
@@ -122,12 +128,13 @@ def make_inputs(name, seed=0, N=None):
     (same distributions, used for reduced-size parity cases)."""
     wl = WORKLOADS[name]
     if N is not None and N != wl.N:
-        wl = Workload(wl.name, N, wl.D, wl.m, wl.n_it, wl.r, wl.bits, wl.rho, wl.vocab, wl.window, wl.x_dtype)
+        wl = Workload(wl.name, N, wl.D, wl.m, wl.n_it, wl.r, wl.bits, wl.rho, wl.vocab, wl.window,
+                      wl.x_dtype, wl.adaptive)
     if wl.x_dtype == "f32":
         X, lab = mixture(seed, wl.N, wl.D)
         return Inputs(wl, X, lab)
     rng = np.random.default_rng(np.random.SeedSequence([int(seed), 0x1D5]))
-    if wl.window:
+    if wl.adaptive:
         n_win = wl.N // wl.window
         ids = np.empty(wl.N, dtype=np.int64)
         periods = np.zeros(n_win, dtype=np.int64)
