@@ -175,30 +175,50 @@ def main():
             "M": int(M), "rho_achieved": wl.N / max(1, int(M)),
         },
     }
-    if a.timing and stage_sum["phi_pass_count"] > 0:
+    if a.timing:
         K = a.steps
         n_win = ctx.n_spectral
-        pass_ms = stage_sum["phi_pass_ms_sum"] / stage_sum["phi_pass_count"]
-        # algorithmic bytes per pass over Phi (either half of the implicit matvec,
-        # Eq. 4): Phi once (4 B/elt) + the L-vector (q in, or u out) + the m-vector
-        # (t out, or t in), fp64, per window
-        alg = n_win * (4.0 * L * wl.m + 8.0 * (L + wl.m))
-        ach = alg / (pass_ms * 1e-3) / 1e9
-        out["roofline"] = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                           "frac": ach / HBM_PEAK_GBS, "traffic": measured_traffic(wl.name),
-                           "traffic_unit": "HBM bytes per pass (FETCH_SIZE + WRITE_SIZE, "
-                                           "copy-calibrated; profiles/lanczos_passes_qwen7b_traffic.md)",
-                           "kernel": "k_lz_phit + k_lz_phiu (t = Phi^T q and u = Phi t)",
-                           "bytes_per_launch": alg, "avg_launch_ms": pass_ms}
         fm_ms = stage_sum["featmap_ms"] / K
         flops = 2.0 * n_win * L * wl.D * wl.m
-        out["featmap_mfma"] = {"bound": "mfma", "achieved": flops / (fm_ms * 1e-3) / 1e12,
-                               "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                               "frac": flops / (fm_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
+        fm_tf = flops / (fm_ms * 1e-3) / 1e12
+        out["featmap_mfma"] = {"bound": "mfma", "achieved": fm_tf, "peak": BF16_PEAK_TFLOPS,
+                               "unit": "TFLOP/s", "frac": fm_tf / BF16_PEAK_TFLOPS,
                                "avg_launch_ms": fm_ms}
         out["stages_ms"] = {k: v / K for k, v in stage_sum.items() if k != "phi_pass_count"}
-        out["stages_ms"]["phi_pass_avg_ms"] = pass_ms
         out["stages_ms"]["ms_per_step_with_events"] = ms2
+        if stage_sum["phi_pass_count"] > 0:
+            pass_ms = stage_sum["phi_pass_ms_sum"] / stage_sum["phi_pass_count"]
+            # algorithmic bytes per pass over Phi (either half of the implicit
+            # matvec, Eq. 4): Phi once (4 B/elt) + the L-vector (q in, or u out) +
+            # the m-vector (t out, or t in), fp64, per window
+            alg = n_win * (4.0 * L * wl.m + 8.0 * (L + wl.m))
+            ach = alg / (pass_ms * 1e-3) / 1e9
+            out["roofline"] = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                               "frac": ach / HBM_PEAK_GBS, "traffic": measured_traffic(wl.name),
+                               "traffic_unit": "HBM bytes per pass (FETCH_SIZE + WRITE_SIZE, "
+                                               "copy-calibrated; profiles/lanczos_passes_qwen7b_traffic.md)",
+                               "kernel": "k_lz_phit + k_lz_phiu (t = Phi^T q and u = Phi t)",
+                               "bytes_per_launch": alg, "avg_launch_ms": pass_ms}
+            out["stages_ms"]["phi_pass_avg_ms"] = pass_ms
+        else:
+            # short windows: one launch runs Lanczos, Eigh and Ritz of every window.
+            # Algorithmic bytes: Phi once, plus the basis, Ritz coordinates,
+            # alpha/beta/theta and the start vector, fp64, per window
+            lz_ms = stage_sum["lanczos_ms"] / K
+            alg = n_win * (4.0 * L * wl.m + 8.0 * ((wl.n_it + 1) * L + L * wl.r + L
+                                                   + 2 * wl.n_it + wl.r))
+            ach = alg / (lz_ms * 1e-3) / 1e9
+            loc = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                   "frac": ach / HBM_PEAK_GBS, "traffic": None,
+                   "kernel": "k_local (Lanczos + Eigh + Ritz, one wavefront per window; "
+                             "a serial chain of n_it dependent steps per window)",
+                   "bytes_per_launch": alg, "avg_launch_ms": lz_ms}
+            out["local_kernel"] = loc
+            if lz_ms >= fm_ms:
+                out["roofline"] = loc
+            else:
+                out["roofline"] = dict(out["featmap_mfma"], traffic=None,
+                                       kernel="k_featmap (bf16 MFMA GEMM + cos epilogue)")
     if not a.no_cpu_baseline:
         cb = cpu_baseline(inp)
         out["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}

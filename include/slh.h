@@ -66,6 +66,11 @@ typedef struct slh_ctx slh_ctx;
                                     (Algorithm 2 break); default 1e-10                 */
 #define SLH_OPT_TIMING        5  /* 1: record HIP events around each stage and around
                                     every pass over Phi (see slh_stage_times)          */
+#define SLH_OPT_SHORT_WINDOWS 6  /* 1 (default): windows of L <= 32 tokens run Lanczos,
+                                    Eigh and Ritz in one wavefront per window on the
+                                    explicit L x L operator Phi_w Phi_w^T (the same
+                                    operator and recurrence; section 3.5 local
+                                    backend); 0: the general path for every L          */
 
 /*
  * Random parameters of the method, drawn from `seed` with Philox4x32-10

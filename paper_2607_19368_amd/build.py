@@ -22,6 +22,7 @@ SOURCES = [
     "k_featmap.hip",
     "k_lanczos.hip",
     "k_eig.hip",
+    "k_local.hip",
     "k_hash.hip",
     "k_merge.hip",
     "k_route.hip",

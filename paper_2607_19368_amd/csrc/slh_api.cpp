@@ -121,6 +121,8 @@ struct slh_ctx {
   hipGraphExec_t lz_exec = nullptr;
   std::string lz_key;
 
+  int short_win = 1;                // SLH_OPT_SHORT_WINDOWS
+
   // timing (SLH_OPT_TIMING)
   int timing = 0;
   std::vector<hipEvent_t> ev_fb, ev_fa;    // around each fused pass
@@ -433,6 +435,10 @@ int slh_set_option(slh_ctx* c, int32_t key, double v) {
       drop_graph(c);
       if (c->timing && make_events(c, 0)) return SLH_EHIP;
       break;
+    case SLH_OPT_SHORT_WINDOWS:
+      if (v != 0.0 && v != 1.0) return fail(c, SLH_EINVAL, "SHORT_WINDOWS must be 0 or 1");
+      c->short_win = (int)v;
+      break;
     default:
       return fail(c, SLH_EINVAL, "unknown option %d", key);
   }
@@ -554,98 +560,117 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
                                   L * sizeof(double), hipMemcpyDeviceToDevice, c->stream));
       q1act = P<double>(c->q1act);
     }
-    LanczosWS w;
-    w.n_act = na;
-    w.L = (int)L;
-    w.m = (int)c->m;
-    w.n_it = n_it;
-    w.ldq = n_it + 1;
-    w.tol = c->tol;
-    {
-      // about four blocks per CU over all windows in each pass over Phi (blocks of
-      // RBA rows x 256 columns)
-      const int64_t target = (int64_t)4 * c->n_cu;
-      auto rows8 = [](int64_t rows) {          // multiple of 8 in [8, 32]
-        rows = ((rows + 7) / 8) * 8;
-        return (int)std::max<int64_t>(8, std::min<int64_t>(rows, 32));
-      };
-      const int ns = (int)(c->m / 256);
-      const int64_t ga = std::max<int64_t>(1, target / ((int64_t)na * ns));
-      w.RWA = rows8((L + 8 * ga - 1) / (8 * ga));
-      w.RBA = 8 * w.RWA;
-      w.GA = (int)((L + w.RBA - 1) / w.RBA);
-      w.G3 = (int)((L + 31) / 32);
-    }
-    const size_t hs = (size_t)w.ldq + 1;
-    ENSURE(c, c->Q, (size_t)na * w.ldq * L * 8);
-    ENSURE(c, c->T, (size_t)na * w.ldq * c->m * 8);
-    ENSURE(c, c->U, (size_t)na * (c->m / 256) * L * 8);
-    ENSURE(c, c->Z1, (size_t)na * L * 8);
-    ENSURE(c, c->Spart, (size_t)na * w.GA * c->m * 8);
-    ENSURE(c, c->H1, (size_t)na * hs * 8);
-    ENSURE(c, c->H2part, (size_t)na * w.G3 * hs * 8);
-    ENSURE(c, c->H2, (size_t)na * hs * 8);
-    ENSURE(c, c->alpha, (size_t)na * n_it * 8);
-    ENSURE(c, c->beta, (size_t)na * n_it * 8);
-    ENSURE(c, c->neff, (size_t)na * 4);
-    ENSURE(c, c->stop, (size_t)na * 4);
-    ENSURE(c, c->amax, (size_t)na * 8);
-    ENSURE(c, c->theta, (size_t)na * c->r * 8);
-    ENSURE(c, c->Seig, (size_t)na * n_it * c->r * 8);
-    ENSURE(c, c->Z, (size_t)na * L * c->r * 8);
-    w.Phi = P<float>(c->Phi);
-    w.Q = P<double>(c->Q);
-    w.T = P<double>(c->T);
-    w.Upart = P<double>(c->U);
-    w.Z1 = P<double>(c->Z1);
-    w.Spart = P<double>(c->Spart);
-    w.H1 = P<double>(c->H1);
-    w.H2part = P<double>(c->H2part);
-    w.H2 = P<double>(c->H2);
-    w.alpha = P<double>(c->alpha);
-    w.beta = P<double>(c->beta);
-    w.neff = P<int>(c->neff);
-    w.stop = P<int>(c->stop);
-    w.amax = P<double>(c->amax);
-    if (c->timing) {
-      // timing: launch the step sequence directly so that every pass over Phi
-      // can be bracketed by events (events inside a captured graph cannot be timed)
-      int rc_ev = make_events(c, 2 * n_it);
-      if (rc_ev) return rc_ev;
-      HIP_TRY(c, hipEventRecord(c->ev[2], c->stream));
-      HIP_TRY(c, launch_lanczos(w, q1act, c->stream, c->ev_fb.data(), c->ev_fa.data()));
-    } else {
-      // the step sequence is captured once per configuration and replayed as a graph
-      std::string key((const char*)&w, sizeof w);
-      key.append((const char*)&q1act, sizeof q1act);
-      if (!c->lz_exec || c->lz_key != key) {
-        drop_graph(c);
-        hipGraph_t g = nullptr;
-        HIP_TRY(c, hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal));
-        hipError_t le = launch_lanczos(w, q1act, c->cap_stream);
-        hipError_t ee = hipStreamEndCapture(c->cap_stream, &g);
-        if (le != hipSuccess || ee != hipSuccess) {
-          if (g) (void)hipGraphDestroy(g);
-          return fail(c, SLH_EHIP, "Lanczos graph capture: %s / %s", hipGetErrorString(le),
-                      hipGetErrorString(ee));
-        }
-        hipError_t ie = hipGraphInstantiate(&c->lz_exec, g, nullptr, nullptr, 0);
-        (void)hipGraphDestroy(g);
-        if (ie != hipSuccess) {
-          c->lz_exec = nullptr;
-          return fail(c, SLH_EHIP, "hipGraphInstantiate: %s", hipGetErrorString(ie));
-        }
-        c->lz_key = key;
+    if (c->short_win && local_supported((int)L, n_it, c->r)) {
+      // short windows: Lanczos, Eigh and Ritz of each window in one wavefront
+      ENSURE(c, c->Q, (size_t)na * (n_it + 1) * L * 8);
+      ENSURE(c, c->alpha, (size_t)na * n_it * 8);
+      ENSURE(c, c->beta, (size_t)na * n_it * 8);
+      ENSURE(c, c->neff, (size_t)na * 4);
+      ENSURE(c, c->theta, (size_t)na * c->r * 8);
+      ENSURE(c, c->Z, (size_t)na * L * c->r * 8);
+      if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[2], c->stream));
+      HIP_TRY(c, launch_local(P<float>(c->Phi), na, (int)c->m, (int)L, n_it, c->r, c->tol, q1act,
+                              P<double>(c->Q), P<double>(c->alpha), P<double>(c->beta),
+                              P<int>(c->neff), P<double>(c->theta), P<double>(c->Z), c->stream));
+      if (c->timing) {
+        HIP_TRY(c, hipEventRecord(c->ev[3], c->stream));
+        HIP_TRY(c, hipEventRecord(c->ev[4], c->stream));
       }
-      HIP_TRY(c, hipGraphLaunch(c->lz_exec, c->stream));
+      c->fused_timed = 0;
+    } else {
+      LanczosWS w;
+      w.n_act = na;
+      w.L = (int)L;
+      w.m = (int)c->m;
+      w.n_it = n_it;
+      w.ldq = n_it + 1;
+      w.tol = c->tol;
+      {
+        // about four blocks per CU over all windows in each pass over Phi (blocks of
+        // RBA rows x 256 columns)
+        const int64_t target = (int64_t)4 * c->n_cu;
+        auto rows8 = [](int64_t rows) {          // multiple of 8 in [8, 32]
+          rows = ((rows + 7) / 8) * 8;
+          return (int)std::max<int64_t>(8, std::min<int64_t>(rows, 32));
+        };
+        const int ns = (int)(c->m / 256);
+        const int64_t ga = std::max<int64_t>(1, target / ((int64_t)na * ns));
+        w.RWA = rows8((L + 8 * ga - 1) / (8 * ga));
+        w.RBA = 8 * w.RWA;
+        w.GA = (int)((L + w.RBA - 1) / w.RBA);
+        w.G3 = (int)((L + 31) / 32);
+      }
+      const size_t hs = (size_t)w.ldq + 1;
+      ENSURE(c, c->Q, (size_t)na * w.ldq * L * 8);
+      ENSURE(c, c->T, (size_t)na * w.ldq * c->m * 8);
+      ENSURE(c, c->U, (size_t)na * (c->m / 256) * L * 8);
+      ENSURE(c, c->Z1, (size_t)na * L * 8);
+      ENSURE(c, c->Spart, (size_t)na * w.GA * c->m * 8);
+      ENSURE(c, c->H1, (size_t)na * hs * 8);
+      ENSURE(c, c->H2part, (size_t)na * w.G3 * hs * 8);
+      ENSURE(c, c->H2, (size_t)na * hs * 8);
+      ENSURE(c, c->alpha, (size_t)na * n_it * 8);
+      ENSURE(c, c->beta, (size_t)na * n_it * 8);
+      ENSURE(c, c->neff, (size_t)na * 4);
+      ENSURE(c, c->stop, (size_t)na * 4);
+      ENSURE(c, c->amax, (size_t)na * 8);
+      ENSURE(c, c->theta, (size_t)na * c->r * 8);
+      ENSURE(c, c->Seig, (size_t)na * n_it * c->r * 8);
+      ENSURE(c, c->Z, (size_t)na * L * c->r * 8);
+      w.Phi = P<float>(c->Phi);
+      w.Q = P<double>(c->Q);
+      w.T = P<double>(c->T);
+      w.Upart = P<double>(c->U);
+      w.Z1 = P<double>(c->Z1);
+      w.Spart = P<double>(c->Spart);
+      w.H1 = P<double>(c->H1);
+      w.H2part = P<double>(c->H2part);
+      w.H2 = P<double>(c->H2);
+      w.alpha = P<double>(c->alpha);
+      w.beta = P<double>(c->beta);
+      w.neff = P<int>(c->neff);
+      w.stop = P<int>(c->stop);
+      w.amax = P<double>(c->amax);
+      if (c->timing) {
+        // timing: launch the step sequence directly so that every pass over Phi
+        // can be bracketed by events (events inside a captured graph cannot be timed)
+        int rc_ev = make_events(c, 2 * n_it);
+        if (rc_ev) return rc_ev;
+        HIP_TRY(c, hipEventRecord(c->ev[2], c->stream));
+        HIP_TRY(c, launch_lanczos(w, q1act, c->stream, c->ev_fb.data(), c->ev_fa.data()));
+      } else {
+        // the step sequence is captured once per configuration and replayed as a graph
+        std::string key((const char*)&w, sizeof w);
+        key.append((const char*)&q1act, sizeof q1act);
+        if (!c->lz_exec || c->lz_key != key) {
+          drop_graph(c);
+          hipGraph_t g = nullptr;
+          HIP_TRY(c, hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal));
+          hipError_t le = launch_lanczos(w, q1act, c->cap_stream);
+          hipError_t ee = hipStreamEndCapture(c->cap_stream, &g);
+          if (le != hipSuccess || ee != hipSuccess) {
+            if (g) (void)hipGraphDestroy(g);
+            return fail(c, SLH_EHIP, "Lanczos graph capture: %s / %s", hipGetErrorString(le),
+                        hipGetErrorString(ee));
+          }
+          hipError_t ie = hipGraphInstantiate(&c->lz_exec, g, nullptr, nullptr, 0);
+          (void)hipGraphDestroy(g);
+          if (ie != hipSuccess) {
+            c->lz_exec = nullptr;
+            return fail(c, SLH_EHIP, "hipGraphInstantiate: %s", hipGetErrorString(ie));
+          }
+          c->lz_key = key;
+        }
+        HIP_TRY(c, hipGraphLaunch(c->lz_exec, c->stream));
+      }
+      if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[3], c->stream));
+      c->fused_timed = c->timing ? 2 * n_it : 0;
+      HIP_TRY(c, launch_tridiag_eig(w.alpha, w.beta, w.neff, na, n_it, c->r, P<double>(c->theta),
+                                    P<double>(c->Seig), c->stream));
+      HIP_TRY(c, launch_ritz(w.Q, P<double>(c->Seig), w.neff, na, (int)L, w.ldq, n_it, c->r,
+                             P<double>(c->Z), c->stream));
+      if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[4], c->stream));
     }
-    if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[3], c->stream));
-    c->fused_timed = c->timing ? 2 * n_it : 0;
-    HIP_TRY(c, launch_tridiag_eig(w.alpha, w.beta, w.neff, na, n_it, c->r, P<double>(c->theta),
-                                  P<double>(c->Seig), c->stream));
-    HIP_TRY(c, launch_ritz(w.Q, P<double>(c->Seig), w.neff, na, (int)L, w.ldq, n_it, c->r,
-                           P<double>(c->Z), c->stream));
-    if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[4], c->stream));
   }
   if ((ritz_out || iters_out) && na > 0) {
     if (ritz_out)

@@ -70,6 +70,13 @@ hipError_t launch_simhash(const double* Z, const double* R, const int* winlist, 
                           int L, int r, int bits, uint32_t* codes, double* proj,
                           hipStream_t s);
 
+// ---- short windows (k_local.hip): Lanczos + Eigh + Ritz of each window in one
+// wavefront, on the window's explicit L x L operator (L <= 32, n_it <= L) ----
+bool local_supported(int L, int n_it, int r);
+hipError_t launch_local(const float* Phi, int n_act, int m, int L, int n_it, int r, double tol,
+                        const double* q1, double* Q, double* alpha, double* beta, int* neff,
+                        double* theta, double* Z, hipStream_t s);
+
 hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
 
 // ---- merge (k_merge.hip) ----

@@ -60,9 +60,10 @@ class Run:
 
 
 def run_gpu(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel=0, compact=False,
-            phi_from=None, codes_from=None, want_phi=False, X=None):
+            phi_from=None, codes_from=None, want_phi=False, X=None, short_windows=None):
     """phi_from: host float32 array (n_act*L, m) loaded instead of computing Phi;
-    codes_from: host uint32 (N,) loaded instead of computing codes."""
+    codes_from: host uint32 (N,) loaded instead of computing codes;
+    short_windows: value of SLH_OPT_SHORT_WINDOWS (None keeps the default)."""
     import torch
     import paper_2607_19368_amd as P
     from paper_2607_19368_amd import slh as B
@@ -74,6 +75,8 @@ def run_gpu(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel=0, compact=F
         P.slh_set_option(ctx, B.SLH_OPT_KERNEL, kernel)
     if compact:
         P.slh_set_option(ctx, B.SLH_OPT_POS_MODE, 1)
+    if short_windows is not None:
+        P.slh_set_option(ctx, B.SLH_OPT_SHORT_WINDOWS, short_windows)
     Xd = to_device_x(inp) if X is None else X
     run = Run()
     if rho is not None:
@@ -242,6 +245,13 @@ def compare(o, g, L, check_spectral=True, ritz_rel=RITZ_REL, angle=ANGLE, emb_re
             tiny_b = np.count_nonzero((b.ritz != 0) & (np.abs(b.ritz) <= floor_b))
             assert max(tiny_a, tiny_b) > 0 and abs(a.iters - b.iters) <= max(tiny_a, tiny_b), \
                 (w, a.iters, b.iters)
+            # the deciding beta (first step where one side stops) is at noise
+            # level on both sides: at most 1e-6 of that side's largest |alpha|
+            j0 = min(a.iters, b.iters) - 1
+            for s_ in (a, b):
+                if s_.beta is not None and s_.alpha is not None:
+                    am = float(np.abs(s_.alpha[:j0 + 1]).max())
+                    assert s_.beta[j0] <= 1e-6 * am, (w, j0, s_.beta[j0], am)
             undecided = True
             rep.undecided_windows += 1
         if check_spectral:

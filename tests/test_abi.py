@@ -84,3 +84,11 @@ def test_host_calls_reject_bad_arguments():
     assert lib.slh_lanczos(None, 4, None, None) == B.SLH_EINVAL
     assert lib.slh_copy_out(None, B.SLH_OUT_PHI, None, 0) == B.SLH_EINVAL
     assert lib.slh_merge_capacity(None) == 0
+
+
+def test_header_constants_match_binding():
+    src = open(os.path.join(ROOT, "include", "slh.h")).read()
+    defs = dict(re.findall(r"#define\s+(SLH_[A-Z0-9_]+)\s+\(?(-?\d+)\)?", src))
+    assert len(defs) >= 20
+    for name, val in defs.items():
+        assert getattr(B, name) == int(val), name
