@@ -102,16 +102,18 @@ __device__ __forceinline__ double readlane_f64(double v, int l) {
 }
 
 // Sum of src[g * ld] over g < G with 8 loads in flight (fixed order).
+// Every batch issues its 8 loads unconditionally (index clamped to G - 1, the
+// surplus values masked to zero afterwards), so a ragged tail costs one round
+// trip rather than one per element.
 __device__ __forceinline__ double sum_strided(const double* __restrict__ src, int64_t ld, int G) {
   double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  int g = 0;
-  for (; g + 8 <= G; g += 8) {
+  for (int g = 0; g < G; g += 8) {
+    double v[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] += src[(int64_t)(g + e) * ld];
+    for (int e = 0; e < 8; ++e) v[e] = src[(int64_t)min(g + e, G - 1) * ld];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] += (g + e < G) ? v[e] : 0.0;
   }
-#pragma unroll
-  for (int e = 0; e < 7; ++e)
-    if (g + e < G) acc[e] += src[(int64_t)(g + e) * ld];
   return ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
 }
 
@@ -239,37 +241,41 @@ __global__ __launch_bounds__(256) void k_lz_finish(LanczosWS w, int j) {
   const int cl = tid & 15, pl = tid >> 4;
   const int c = g * 16 + cl;                   // m is a multiple of 16
   const double* H2 = w.H2 + (int64_t)a * hs;
+  // The loads of t_k and h2_k (k = pl + 16 e < j <= 256), of the |h2|^2 terms
+  // (k = tid, tid + 256 < j), of |z1|^2 and of the step state are all issued
+  // before the first use, with clamped indices (surplus values are masked), so
+  // the kernel waits on memory once.
+  const int jm = max(j - 1, 0);
+  const double* Ta = w.T + (int64_t)a * w.ldq * m + c;
+  double tv[16], hv[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const int k = min(pl + 16 * e, jm);
+    tv[e] = Ta[(int64_t)k * m];
+    hv[e] = H2[k];
+  }
+  const double hq0 = H2[min(tid, jm)], hq1 = H2[min(tid + 256, jm)];
+  const double z2 = H2[w.ldq];
+  const int stopped = w.stop[a];
+  const double amax = w.amax[a];
   // partial of Phi^T z1 over row groups pl, pl + 16, ...
   const double* Sp = w.Spart + (int64_t)a * w.GA * m + c;
   const int cnt = (w.GA - pl + 15) / 16;
   const double s = sum_strided(Sp + (int64_t)pl * m, (int64_t)16 * m, cnt > 0 ? cnt : 0);
   // partial of sum_k h2_k t_k over k = pl, pl + 16, ... < j
-  double corr = 0.0;
+  double corr;
   {
-    const double* Ta = w.T + (int64_t)a * w.ldq * m + c;
     double acc[4] = {0, 0, 0, 0};
-    int k = pl;
-    for (; k + 48 < j; k += 64) {
-      double tv[4], hv[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        tv[e] = Ta[(int64_t)(k + 16 * e) * m];
-        hv[e] = H2[k + 16 * e];
-      }
-#pragma unroll
-      for (int e = 0; e < 4; ++e) acc[e] = fma(tv[e], hv[e], acc[e]);
-    }
-    for (; k < j; k += 16) acc[0] = fma(Ta[(int64_t)k * m], H2[k], acc[0]);
+    for (int e = 0; e < 16; ++e)
+      if (pl + 16 * e < j) acc[e & 3] = fma(tv[e], hv[e], acc[e & 3]);
     corr = (acc[0] + acc[1]) + (acc[2] + acc[3]);
   }
   // |h2|^2 partial
   double hh = 0.0;
-  for (int k = tid; k < j; k += 256) {
-    const double v = H2[k];
-    hh = fma(v, v, hh);
-  }
-  const double z2 = (j > 0) ? H2[w.ldq] : 0.0;
-  if (w.stop[a]) return;
+  if (tid < j) hh = fma(hq0, hq0, hh);
+  if (tid + 256 < j) hh = fma(hq1, hq1, hh);
+  if (stopped) return;
   __shared__ double red[4];
   __shared__ double sh;
   __shared__ double rs[16][17], rc[16][17];
@@ -281,7 +287,7 @@ __global__ __launch_bounds__(256) void k_lz_finish(LanczosWS w, int j) {
     if (tid == 0) {
       const double b2 = z2 - hh;               // |z1 - Q h2|^2 for orthonormal Q
       const double beta = b2 > 0.0 ? sqrt(b2) : 0.0;
-      const bool brk = !(beta > w.tol * w.amax[a]);
+      const bool brk = !(beta > w.tol * amax);
       sh = brk ? 0.0 : beta;
       if (g == 0) {
         w.beta[(int64_t)a * w.n_it + j - 1] = beta;
@@ -388,37 +394,43 @@ __global__ __launch_bounds__(256) void k_lz_orth(LanczosWS w, int j) {
   const int ic = min(i, L - 1);
   const double* Qa = w.Q + (int64_t)a * w.ldq * L;
   const int nt = (j - kg + 7) / 8;             // k = kg + 8 t < j
+  // every global load of the kernel is issued here, before the first use
+  // (indices clamped; values that are not needed are never used)
+  const int jm = max(j - 1, 0);
   double qv[MAXT];
 #pragma unroll
   for (int t = 0; t < MAXT; ++t)
-    if (8 * t < j) qv[t] = Qa[(int64_t)min(kg + 8 * t, max(j - 1, 0)) * L + ic];
+    if (8 * t < j) qv[t] = Qa[(int64_t)min(kg + 8 * t, jm) * L + ic];
+  const double* H1a = w.H1 + (int64_t)a * hs;
+  const double* H2a = w.H2 + (int64_t)a * hs;
+  const double h1v0 = H1a[min(tid, j)], h1v1 = H1a[min(tid + 256, j)];
+  const double h2v0 = H2a[min(tid, jm)], h2v1 = H2a[min(tid + 256, jm)];
+  const int ns = w.m >> 8;                     // <= 8 column slices
+  const double* up = w.Upart + (int64_t)a * ns * L + ic;
+  double us[8];
+#pragma unroll
+  for (int sl = 0; sl < 8; ++sl) us[sl] = up[(int64_t)min(sl, ns - 1) * L];
+  const double zi = w.Z1[(int64_t)a * L + ic];
+  const double bet = w.beta[(int64_t)a * w.n_it + jm];
+  const double q0 = Qa[ic];
+  const int stopped = w.stop[a];
+  const double amax0 = (j > 0) ? w.amax[a] : 0.0;
   __shared__ double h1[264], h2[264];
   __shared__ double rq[8][33], rz[8][33];
   __shared__ double sz[32], sq[32];
-  double ui = 0.0, zi = 0.0, q0 = 0.0, bet = 1.0;
-  if (tid < 32) {
-    const int ns = w.m >> 8;                   // <= 8 column slices
-    const double* up = w.Upart + (int64_t)a * ns * L + ic;
-    double us[8];
+  double ui = 0.0;
 #pragma unroll
-    for (int sl = 0; sl < 8; ++sl) us[sl] = up[(int64_t)min(sl, ns - 1) * L];
-#pragma unroll
-    for (int sl = 0; sl < 8; ++sl)
-      if (sl < ns) ui += us[sl];
-    if (j > 0) {
-      zi = w.Z1[(int64_t)a * L + ic];
-      bet = w.beta[(int64_t)a * w.n_it + j - 1];
-    } else {
-      q0 = Qa[ic];
-    }
-  }
-  for (int k = tid; k <= j; k += 256) h1[k] = w.H1[(int64_t)a * hs + k];
-  for (int k = tid; k < j; k += 256) h2[k] = w.H2[(int64_t)a * hs + k];
-  if (w.stop[a]) return;
+  for (int sl = 0; sl < 8; ++sl)
+    if (sl < ns) ui += us[sl];
+  if (tid <= j) h1[tid] = h1v0;
+  if (tid + 256 <= j) h1[tid + 256] = h1v1;
+  if (tid < j) h2[tid] = h2v0;
+  if (tid + 256 < j) h2[tid + 256] = h2v1;
+  if (stopped) return;
   __syncthreads();
   if (g == 0 && tid == 0) {
     w.alpha[(int64_t)a * w.n_it + j] = h1[j];
-    w.amax[a] = fmax(j ? w.amax[a] : 0.0, fabs(h1[j]));
+    w.amax[a] = fmax(amax0, fabs(h1[j]));
     w.neff[a] = j + 1;
   }
   // Q_{j-1} h2 (q_j update) and Q_{j-1} h1 (z1) over this thread's k
