@@ -42,6 +42,15 @@ Readings of the paper that this file takes (where it is silent or ambiguous):
   R10 (section 3.5) Chunk size k = max(1, round(rho)) with round-half-to-even;
      the last chunk may be partial; chunks are renormalised like Eq. 7 and take
      the max position of their members.
+  R16 (section 3.2 remark on row normalisation; appendix, softmax normalisation
+     gap) The normalised variant estimates the row sums s = Phi (Phi^T 1) and
+     uses diag(s)^-1 Phi Phi^T.  That operator is not symmetric; it is similar to
+     S = diag(s)^-1/2 Phi Phi^T diag(s)^-1/2 = Phi~ Phi~^T with Phi~ the rows of
+     Phi scaled by s_i^-1/2, so Lanczos runs unchanged on Phi~.  Its Ritz vectors
+     Z relate to those of the normalised operator by diag(s)^-1/2 Z, a positive
+     row scaling that leaves every SimHash bit unchanged; Z is reported.  A row
+     whose estimated sum is not positive gets weight 0 (it leaves the operator).
+     Row sums are per window.
 """
 import math
 from dataclasses import dataclass, field
@@ -86,6 +95,17 @@ def feature_map(X, W, psi, kernel="softmax"):
     elif kernel != "gauss":
         raise ValueError(kernel)
     return Phi
+
+
+def normalised_features(Phi):
+    """Phi~ = diag(w) Phi with w_i = s_i^-1/2, s = Phi (Phi^T 1) (reading R16).
+
+    Returns (Phi~, s).  w_i = 0 where s_i <= 0."""
+    s_hat = Phi @ (Phi.T @ np.ones(Phi.shape[0]))
+    w = np.zeros_like(s_hat)
+    pos = s_hat > 0
+    w[pos] = 1.0 / np.sqrt(s_hat[pos])
+    return Phi * w[:, None], s_hat
 
 
 # --------------------------------------------------------------------------
@@ -302,9 +322,13 @@ class CompressResult:
     merge: MergeResult
 
 
-def compress(X, W, psi, q1, R, n_it, r, kernel="softmax", positions=None, keep_phi=True):
-    """One global Spectral-LSH pass over X (Algorithm 1)."""
+def compress(X, W, psi, q1, R, n_it, r, kernel="softmax", positions=None, keep_phi=True,
+             normalise=False):
+    """One global Spectral-LSH pass over X (Algorithm 1); normalise=True runs
+    it on the normalised operator (reading R16)."""
     Phi = feature_map(X, W, psi, kernel)
+    if normalise:
+        Phi, _ = normalised_features(Phi)
     lz = lanczos(Phi, q1, n_it)
     vals, Z, _, _ = ritz(lz, r)
     proj = projections(Z, R)

@@ -193,6 +193,55 @@ def test_lanczos_identical_rows_rank_one():
     assert abs(vals[-1] - np.sum(Phi[0] ** 2) * 64) < 1e-9 * vals[-1]
 
 
+# ---------------------------------------------------------------- normalised operator
+def test_normalised_operator_closed_forms(tiny_run):
+    """Reading R16: the normalised matvec diag(s)^-1 Phi Phi^T with s = Phi Phi^T 1
+    maps 1 to 1 (rows sum to one), so S = Phi~ Phi~^T has sqrt(s) as an exact
+    eigenvector with eigenvalue 1; S and the non-symmetric normalised matrix
+    share their spectrum; the right eigenvectors of the latter are
+    diag(s)^-1/2 times those of S."""
+    wl, X, Phi, lz = tiny_run
+    Pn, s_hat = O.normalised_features(Phi)
+    A = Phi @ Phi.T
+    assert np.allclose(s_hat, A.sum(axis=1), rtol=1e-12, atol=0)
+    assert np.all(s_hat > 0)
+    P = A / s_hat[:, None]                        # the paper's normalised matrix
+    assert np.allclose(P.sum(axis=1), 1.0, rtol=0, atol=1e-12)
+    u = np.sqrt(s_hat)
+    assert np.allclose(Pn @ (Pn.T @ u), u, rtol=0, atol=1e-11 * np.abs(u).max())
+    S = Pn @ Pn.T
+    ev_S = np.sort(np.linalg.eigvalsh(S))
+    ev_P = np.sort(np.linalg.eigvals(P).real)
+    assert np.allclose(ev_S[-40:], ev_P[-40:], rtol=0, atol=1e-10)
+    # Lanczos on Phi~ (the unchanged algorithm): converged Ritz pairs of S give
+    # right eigenvectors diag(s)^-1/2 z of P
+    lzn = O.lanczos(Pn, OP.start_vector(0, wl.N), wl.n_it)
+    vals, Z, theta, Sv = O.ritz(lzn, wl.r)
+    resid = np.abs(lzn.beta[-1] * Sv[-1, :])
+    checked = 0
+    for c in range(wl.r):
+        k = lzn.n_eff - wl.r + c
+        if resid[k] < 1e-9 * theta[-1]:
+            v = Z[:, c] / np.sqrt(s_hat)
+            assert np.allclose(P @ v, vals[c] * v, rtol=0, atol=1e-7 * np.abs(v).max())
+            checked += 1
+    assert checked >= 3
+    assert abs(vals[-1] - 1.0) < 1e-9           # the top of the spectrum is 1 here
+    # SimHash of the right eigenvectors equals SimHash of Z (positive row scaling)
+    R = OP.hyperplanes(0, wl.r, wl.bits)
+    assert np.array_equal(O.simhash(Z, R), O.simhash(Z / np.sqrt(s_hat)[:, None], R))
+
+
+def test_normalised_operator_nonpositive_row_sum():
+    """Reading R16: a row whose estimated sum is not positive leaves the operator."""
+    Phi = np.array([[1.0, 0.0, 0.5], [-1.0, 0.2, 0.0], [0.0, 0.3, -0.5]])
+    Pn, s_hat = O.normalised_features(Phi)
+    c = Phi.sum(axis=0)                            # Phi^T 1 = [0, 0.5, 0]
+    assert np.allclose(s_hat, Phi @ c)             # [0, 0.1, 0.15]
+    assert s_hat[0] == 0.0 and np.all(Pn[0] == 0.0)
+    assert np.allclose(Pn[1:], Phi[1:] / np.sqrt(s_hat[1:, None]))
+
+
 def test_tridiagonal_eigensolve_toeplitz_closed_form():
     """tridiag(b; a; b) of order n: eigenvalues a + 2b cos(k pi/(n+1)),
     eigenvectors sin(j k pi/(n+1)) (first entry positive)."""
