@@ -51,7 +51,7 @@ def parse():
     return ap.parse_args()
 
 
-def cpu_baseline(inp, min_seconds=10.0, max_reps=40):
+def cpu_baseline(inp, min_seconds=10.0, max_reps=40, tau=None):
     """The oracle, untouched, on the same prompt: feature map .. merge (parameter
     drawing excluded, as on the GPU side where it happens in slh_create), repeated
     until about min_seconds of CPU work have been timed."""
@@ -74,7 +74,12 @@ def cpu_baseline(inp, min_seconds=10.0, max_reps=40):
         t0 = time.perf_counter()
         for w in range(wl.N // L):
             Xw = inp.x_float(slice(w * L, (w + 1) * L))
+            if wl.adaptive and not O.route_window(L, O.redundancy_score(Xw), wl.rho, tau):
+                O.chunk_pool(Xw, O.chunk_size(wl.rho), pos0=w * L)
+                continue
             Phi = O.feature_map(Xw, W, psi)
+            if wl.normalise:
+                Phi, _ = O.normalised_features(Phi)
             lz = O.lanczos(Phi, q1[w], wl.n_it)
             _, Z, _, _ = O.ritz(lz, wl.r)
             codes = O.simhash(Z, R)
@@ -110,6 +115,8 @@ def main():
     ctx = P.slh_create(wl.N, wl.D, wl.m, wl.r, wl.bits, 0)
     if wl.window:
         P.slh_set_option(ctx, B.SLH_OPT_WINDOW_LEN, wl.window)
+    if wl.normalise:
+        P.slh_set_option(ctx, B.SLH_OPT_NORMALIZE, 1)
     tau = -1.0
     if wl.adaptive:
         # routing threshold: midpoint of the 32nd and 33rd largest window scores
@@ -167,7 +174,8 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": f"{wl.name}: N={wl.N} D={wl.D} m={wl.m} n_it={wl.n_it} r={wl.r} "
-                        f"bits={wl.bits} rho={wl.rho:g}" + (f" window={wl.window}" if wl.window else ""),
+                        f"bits={wl.bits} rho={wl.rho:g}" + (f" window={wl.window}" if wl.window else "")
+                        + (" operator=row-normalised" if wl.normalise else ""),
             "inputs": "Zipf(1.1) token ids over a seeded N(0,0.02) bf16 embedding table"
                       if wl.x_dtype == "bf16" else "seeded Gaussian mixture, fp32",
             "precision": "bf16 MFMA feature map with fp32 accumulation, fp32 Phi, fp64 Lanczos/"
@@ -220,7 +228,7 @@ def main():
                 out["roofline"] = dict(out["featmap_mfma"], traffic=None,
                                        kernel="k_featmap (bf16 MFMA GEMM + cos epilogue)")
     if not a.no_cpu_baseline:
-        cb = cpu_baseline(inp)
+        cb = cpu_baseline(inp, tau=tau if wl.adaptive else None)
         out["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
     print(json.dumps(out), flush=True)
 

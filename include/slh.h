@@ -66,6 +66,17 @@ typedef struct slh_ctx slh_ctx;
                                     (Algorithm 2 break); default 1e-10                 */
 #define SLH_OPT_TIMING        5  /* 1: record HIP events around each stage and around
                                     every pass over Phi (see slh_stage_times)          */
+#define SLH_OPT_NORMALIZE     7  /* 1: the normalised operator (section 3.2 remark on
+                                    row normalisation; appendix on the softmax
+                                    normalisation gap): per window, row sums
+                                    s = Phi (Phi^T 1) are estimated and the rows of
+                                    Phi scaled by s_i^-1/2 (0 where s_i <= 0) inside
+                                    slh_feature_map, so Lanczos runs on
+                                    diag(s)^-1/2 Phi Phi^T diag(s)^-1/2, similar to
+                                    diag(s)^-1 Phi Phi^T.  Z holds that symmetric
+                                    operator's Ritz vectors (the normalised
+                                    operator's are diag(s)^-1/2 Z: the same SimHash
+                                    codes).  0 (default): Phi Phi^T as in Eq. 4     */
 #define SLH_OPT_SHORT_WINDOWS 6  /* 1 (default): windows of L <= 32 tokens run Lanczos,
                                     Eigh and Ritz in one wavefront per window on the
                                     explicit L x L operator Phi_w Phi_w^T (the same
@@ -186,6 +197,7 @@ int64_t slh_merge_capacity(const slh_ctx *ctx);
  *   SLH_OUT_THETA  n_act*r doubles       kept Ritz values (ascending)
  *   SLH_OUT_Q      n_act*(n_it+1)*L doubles  Lanczos basis, vector-major
  *   SLH_OUT_WINDOWS n_act int32          window index of each spectral window
+ *   SLH_OUT_ROWSUM n_act*L doubles       estimated row sums s (SLH_OPT_NORMALIZE = 1)
  * (n_act = number of spectral windows.)
  */
 #define SLH_OUT_PHI     1
@@ -197,6 +209,7 @@ int64_t slh_merge_capacity(const slh_ctx *ctx);
 #define SLH_OUT_THETA   7
 #define SLH_OUT_Q       8
 #define SLH_OUT_WINDOWS 9
+#define SLH_OUT_ROWSUM  10
 int slh_copy_out(slh_ctx *ctx, int32_t which, void *dst_host, int64_t bytes);
 
 /*
@@ -214,6 +227,7 @@ int slh_load(slh_ctx *ctx, int32_t which, const void *src, int64_t bytes);
  *   [0] feature map ms        [1] Lanczos loop ms (all steps, all windows)
  *   [2] sum of Phi-pass ms     [3] number of Phi passes timed (2 per step)
  *   [4] eigensolve + Ritz ms  [5] SimHash ms   [6] merge ms
+ *   [7] row normalisation ms (SLH_OPT_NORMALIZE = 1, else 0)
  * Synchronises the stream.
  */
 int slh_stage_times(slh_ctx *ctx, double *ms_out, int32_t n);

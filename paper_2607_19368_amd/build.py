@@ -23,6 +23,7 @@ SOURCES = [
     "k_lanczos.hip",
     "k_eig.hip",
     "k_local.hip",
+    "k_norm.hip",
     "k_hash.hip",
     "k_merge.hip",
     "k_route.hip",

@@ -122,6 +122,8 @@ struct slh_ctx {
   std::string lz_key;
 
   int short_win = 1;                // SLH_OPT_SHORT_WINDOWS
+  int normalize = 0;                // SLH_OPT_NORMALIZE
+  DevBuf nm_part, nm_csum, rowsum;
 
   // timing (SLH_OPT_TIMING)
   int timing = 0;
@@ -129,6 +131,7 @@ struct slh_ctx {
   hipEvent_t ev[12] = {};                   // stage brackets: fm, lz, eig, sh, mg
   bool ev_made = false;
   int fused_timed = 0;
+  int norm_timed = 0;
 };
 
 namespace {
@@ -435,6 +438,10 @@ int slh_set_option(slh_ctx* c, int32_t key, double v) {
       drop_graph(c);
       if (c->timing && make_events(c, 0)) return SLH_EHIP;
       break;
+    case SLH_OPT_NORMALIZE:
+      if (v != 0.0 && v != 1.0) return fail(c, SLH_EINVAL, "NORMALIZE must be 0 or 1");
+      c->normalize = (int)v;
+      break;
     case SLH_OPT_SHORT_WINDOWS:
       if (v != 0.0 && v != 1.0) return fail(c, SLH_EINVAL, "SHORT_WINDOWS must be 0 or 1");
       c->short_win = (int)v;
@@ -529,6 +536,18 @@ int slh_feature_map(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx) {
   a.m = (int)c->m;
   HIP_TRY(c, launch_featmap(a, c->stream, c->timing ? c->ev[0] : nullptr,
                             c->timing ? c->ev[1] : nullptr));
+  if (c->normalize && c->n_act > 0) {
+    const int G = normalise_groups(c->n_act, (int)L, (int)c->m, c->n_cu);
+    ENSURE(c, c->nm_part, (size_t)c->n_act * G * c->m * 8);
+    ENSURE(c, c->nm_csum, (size_t)c->n_act * c->m * 8);
+    ENSURE(c, c->rowsum, (size_t)rows * 8);
+    if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[9], c->stream));
+    HIP_TRY(c, launch_normalise(P<float>(c->Phi), c->n_act, (int)L, (int)c->m, G,
+                                P<double>(c->nm_part), P<double>(c->nm_csum),
+                                P<double>(c->rowsum), c->stream));
+    if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[10], c->stream));
+    c->norm_timed = c->timing;
+  }
   c->stage = 1;
   return SLH_OK;
 }
@@ -786,7 +805,7 @@ int slh_stage_times(slh_ctx* c, double* out, int32_t n) {
   if (!c || !out || n < 0) return SLH_EINVAL;
   if (!c->timing || !c->ev_made) return fail(c, SLH_ESTATE, "SLH_OPT_TIMING is off");
   HIP_TRY(c, hipStreamSynchronize(c->stream));
-  double v[7] = {0, 0, 0, 0, 0, 0, 0};
+  double v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   float ms = 0.f;
   auto el = [&](hipEvent_t a, hipEvent_t b) -> double {
     float t = 0.f;
@@ -802,7 +821,8 @@ int slh_stage_times(slh_ctx* c, double* out, int32_t n) {
   v[4] = el(c->ev[3], c->ev[4]);
   v[5] = el(c->ev[5], c->ev[6]);
   v[6] = el(c->ev[7], c->ev[8]);
-  for (int i = 0; i < n && i < 7; ++i) out[i] = v[i];
+  v[7] = c->norm_timed ? el(c->ev[9], c->ev[10]) : 0.0;
+  for (int i = 0; i < n && i < 8; ++i) out[i] = v[i];
   (void)hipGetLastError();   // a stage that did not run leaves unrecorded events
   return SLH_OK;
 }
@@ -847,6 +867,7 @@ int slh_copy_out(slh_ctx* c, int32_t which, void* dst, int64_t bytes) {
     case SLH_OUT_CODES: b = &c->codes; want = c->N * 4; break;
     case SLH_OUT_THETA: b = &c->theta; want = na * c->r * 8; break;
     case SLH_OUT_Q: b = &c->Q; want = na * (c->n_it + 1) * L * 8; break;
+    case SLH_OUT_ROWSUM: b = &c->rowsum; want = na * L * 8; break;
     case SLH_OUT_WINDOWS:
       if (bytes != na * 4) return fail(c, SLH_EINVAL, "bytes must be %lld", (long long)(na * 4));
       if (na) std::memcpy(dst, c->winlist_h.data(), (size_t)na * 4);

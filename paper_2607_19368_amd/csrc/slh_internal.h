@@ -77,6 +77,12 @@ hipError_t launch_local(const float* Phi, int n_act, int m, int L, int n_it, int
                         const double* q1, double* Q, double* alpha, double* beta, int* neff,
                         double* theta, double* Z, hipStream_t s);
 
+// ---- normalised operator (k_norm.hip): per window s = Phi (Phi^T 1), rows of
+// Phi scaled in place by s_i^-1/2 (0 where s_i <= 0); s kept in s_out ----
+int normalise_groups(int n_act, int L, int m, int n_cu);   // row groups G of the column sums
+hipError_t launch_normalise(float* Phi, int n_act, int L, int m, int G, double* part, double* csum,
+                            double* s_out, hipStream_t s);   // part: [n_act][G][m], csum: [n_act][m]
+
 hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
 
 // ---- merge (k_merge.hip) ----

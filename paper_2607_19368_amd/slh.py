@@ -16,9 +16,10 @@ LIB_PATH = os.path.join(_HERE, "libslh.so")
 SLH_OK, SLH_EINVAL, SLH_ENOMEM, SLH_EHIP, SLH_ESTATE = 0, -1, -2, -3, -4
 SLH_BF16, SLH_F32 = 0, 1
 SLH_OPT_KERNEL, SLH_OPT_WINDOW_LEN, SLH_OPT_POS_MODE, SLH_OPT_BREAKDOWN_TOL, SLH_OPT_TIMING = 1, 2, 3, 4, 5
-SLH_OPT_SHORT_WINDOWS = 6
+SLH_OPT_SHORT_WINDOWS, SLH_OPT_NORMALIZE = 6, 7
 SLH_OUT_PHI, SLH_OUT_ALPHA, SLH_OUT_BETA, SLH_OUT_Z = 1, 2, 3, 4
 SLH_OUT_PROJ, SLH_OUT_CODES, SLH_OUT_THETA, SLH_OUT_Q, SLH_OUT_WINDOWS = 5, 6, 7, 8, 9
+SLH_OUT_ROWSUM = 10
 
 EXPORTS = [
     "slh_gen_params", "slh_gen_start", "slh_create", "slh_destroy", "slh_last_error",
@@ -234,11 +235,12 @@ _OUT = {
     SLH_OUT_THETA: (np.float64, lambda c: (c.n_spectral, c.r)),
     SLH_OUT_Q: (np.float64, lambda c: (c.n_spectral, c.n_it + 1, c.window_len)),
     SLH_OUT_WINDOWS: (np.int32, lambda c: (c.n_spectral,)),
+    SLH_OUT_ROWSUM: (np.float64, lambda c: (c.n_spectral, c.window_len)),
 }
 
 
 STAGE_NAMES = ["featmap_ms", "lanczos_ms", "phi_pass_ms_sum", "phi_pass_count", "eig_ritz_ms",
-               "simhash_ms", "merge_ms"]
+               "simhash_ms", "merge_ms", "normalise_ms"]
 
 
 def slh_stage_times(ctx):

@@ -57,10 +57,12 @@ class Run:
     scores: np.ndarray = None
     route: np.ndarray = None
     R: np.ndarray = None             # SimHash hyperplanes (oracle runs)
+    rowsum: np.ndarray = None        # estimated row sums of the normalised operator
 
 
 def run_gpu(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel=0, compact=False,
-            phi_from=None, codes_from=None, want_phi=False, X=None, short_windows=None):
+            phi_from=None, codes_from=None, want_phi=False, X=None, short_windows=None,
+            normalise=False):
     """phi_from: host float32 array (n_act*L, m) loaded instead of computing Phi;
     codes_from: host uint32 (N,) loaded instead of computing codes;
     short_windows: value of SLH_OPT_SHORT_WINDOWS (None keeps the default)."""
@@ -77,6 +79,8 @@ def run_gpu(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel=0, compact=F
         P.slh_set_option(ctx, B.SLH_OPT_POS_MODE, 1)
     if short_windows is not None:
         P.slh_set_option(ctx, B.SLH_OPT_SHORT_WINDOWS, short_windows)
+    if normalise:
+        P.slh_set_option(ctx, B.SLH_OPT_NORMALIZE, 1)
     Xd = to_device_x(inp) if X is None else X
     run = Run()
     if rho is not None:
@@ -90,6 +94,8 @@ def run_gpu(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel=0, compact=F
             P.slh_load(ctx, B.SLH_OUT_PHI, torch.from_numpy(np.ascontiguousarray(phi_from, np.float32)).cuda())
         if want_phi and na:
             run.Phi = P.slh_copy_out(ctx, B.SLH_OUT_PHI).reshape(na * L, wl.m)
+        if normalise and na:
+            run.rowsum = P.slh_copy_out(ctx, B.SLH_OUT_ROWSUM).reshape(-1)
         ritz, iters = P.slh_lanczos(ctx, n_it, want=True)
         P.slh_simhash(ctx)
         wins = P.slh_copy_out(ctx, B.SLH_OUT_WINDOWS)
@@ -113,7 +119,7 @@ def run_gpu(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel=0, compact=F
 
 
 def run_oracle(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel="softmax", compact=False,
-               phi_rows=None):
+               phi_rows=None, normalise=False):
     wl = inp.workload
     N = wl.N
     L = window or N
@@ -125,6 +131,7 @@ def run_oracle(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel="softmax"
     t2m = np.zeros(N, np.int64)
     base = 0
     scores, route = [], []
+    rowsums = []
     for w in range(N // L):
         Xw = inp.x_float(slice(w * L, (w + 1) * L))
         if rho is not None:
@@ -136,6 +143,9 @@ def run_oracle(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel="softmax"
             spectral = True
         if spectral:
             Phi = O.feature_map(Xw, W, psi, kernel)
+            if normalise:
+                Phi, s_hat = O.normalised_features(Phi)
+                rowsums.append(s_hat)
             lz = O.lanczos(Phi, OP.start_vector(seed, L, w), n_it)
             vals, Z, _, _ = O.ritz(lz, wl.r)
             proj = O.projections(Z, R)
@@ -158,6 +168,8 @@ def run_oracle(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel="softmax"
     run.E = np.concatenate(Es)
     run.P = np.concatenate(Ps)
     run.R = R
+    if rowsums:
+        run.rowsum = np.concatenate(rowsums)
     if compact:
         run.P = np.arange(len(run.P))
     run.t2m = t2m
@@ -167,7 +179,7 @@ def run_oracle(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel="softmax"
     return run
 
 
-def oracle_uncertainty(inp, w, L, n_it, seed=0):
+def oracle_uncertainty(inp, w, L, n_it, seed=0, normalise=False):
     """How far two valid fp64 evaluations of the method disagree on window w.
 
     Reversing the token order leaves the method's result unchanged up to the
@@ -183,6 +195,8 @@ def oracle_uncertainty(inp, w, L, n_it, seed=0):
     q1 = OP.start_vector(seed, L, w)
     rv = np.arange(L)[::-1]
     Phi = O.feature_map(Xw, W, psi)
+    if normalise:
+        Phi, _ = O.normalised_features(Phi)
     _, Z, _, _ = O.ritz(O.lanczos(Phi, q1, n_it), wl.r)
     _, Zr, _, _ = O.ritz(O.lanczos(Phi[rv], q1[rv], n_it), wl.r)
     return float(np.max(np.abs(Zr[rv] @ R - Z @ R)))

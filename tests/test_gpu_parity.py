@@ -381,3 +381,33 @@ def test_short_windows(L, n_it, r, bits):
         rep = PR.compare(o, g, L, unc=unc)
         _say(f"   short={short}: {rep}  M={len(g.P)}")
         assert rep.undecided_windows <= len(unc) // 4
+
+
+@pytest.mark.parametrize("case", ["tiny", "mistral7b", "local16", "windows256"])
+def test_normalised_operator(case):
+    """SLH_OPT_NORMALIZE: per window, the rows of Phi are scaled by s_i^-1/2 with
+    s = Phi (Phi^T 1) before Lanczos (the symmetric form of the normalised
+    matvec).  The estimated row sums and the whole path must match the oracle;
+    the short-window kernel (local16) and the general windowed path
+    (windows256) both run on the scaled rows."""
+    if case == "local16":
+        inp, L = make_inputs("local16", N=1024), 16
+    elif case == "windows256":
+        inp, L = _custom("nwin", 4 * 256, 512, 256, 24, 8, 8), 256
+    else:
+        inp, L = make_inputs(case), 0
+    wl = inp.workload
+    n_it = wl.n_it
+    _say(f"[normalised] {case} N={wl.N} D={wl.D} m={wl.m} window={L} n_it={n_it}")
+    g = PR.run_gpu(inp, n_it=n_it, window=L, normalise=True)
+    o = PR.run_oracle(inp, n_it=n_it, window=L, normalise=True)
+    rel = np.abs(g.rowsum - o.rowsum) / np.abs(o.rowsum)
+    _say(f"   row sums: max rel {rel.max():.2e}")
+    assert rel.max() < 1e-5
+    unc = None
+    if L:
+        unc = {w.w: PR.oracle_uncertainty(inp, w.w, L, n_it, normalise=True) for w in o.windows}
+    rep = PR.compare(o, g, L or wl.N, unc=unc)
+    _say(f"   {rep}  M={len(g.P)}")
+    if unc is not None:
+        assert rep.undecided_windows <= len(unc) // 4

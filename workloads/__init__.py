@@ -17,10 +17,12 @@ the same shapes:
                 positions replaced by fresh Zipf draws (JSON/code/table-like
                 redundancy), odd windows are i.i.d. Zipf(1.1).
   local16       the qwen7b prompt cut into 512 windows of 16 tokens (local backend).
+  qwen7b_normalised  the qwen7b prompt, run on the row-normalised operator.
 
 Table rows are generated per id on demand (row id -> its own seeded stream), so
 the 152064-row tables are never materialised.
 """
+import dataclasses
 from dataclasses import dataclass
 
 import numpy as np
@@ -40,6 +42,7 @@ class Workload:
     window: int = 0   # window length (0 = one global window)
     x_dtype: str = "bf16"
     adaptive: bool = False   # windows alternate periodic / i.i.d. streams and are routed
+    normalise: bool = False  # run on the row-normalised operator
 
 
 WORKLOADS = {
@@ -52,6 +55,9 @@ WORKLOADS = {
     # local backend at the paper's defaults (section 5.1): windows of 16 tokens,
     # 256 random features, a full 16-step Krylov space, b = ceil(log2(16 / rho))
     "local16": Workload("local16", 8192, 3584, 256, 16, 16, 2, 4.0, 152064, 16),
+    # the qwen7b prompt on the row-normalised operator (section 3.2 remark)
+    "qwen7b_normalised": Workload("qwen7b_normalised", 8192, 3584, 2048, 96, 64, 12, 16.0, 152064,
+                                  normalise=True),
 }
 
 
@@ -128,8 +134,7 @@ def make_inputs(name, seed=0, N=None):
     (same distributions, used for reduced-size parity cases)."""
     wl = WORKLOADS[name]
     if N is not None and N != wl.N:
-        wl = Workload(wl.name, N, wl.D, wl.m, wl.n_it, wl.r, wl.bits, wl.rho, wl.vocab, wl.window,
-                      wl.x_dtype, wl.adaptive)
+        wl = dataclasses.replace(wl, N=N)
     if wl.x_dtype == "f32":
         X, lab = mixture(seed, wl.N, wl.D)
         return Inputs(wl, X, lab)
