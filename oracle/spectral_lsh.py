@@ -193,6 +193,15 @@ def ritz(lz, r):
     return vals, Z, theta, S
 
 
+def spectral_energy(ritz_values, Phi):
+    """Fraction of the operator's spectral energy captured by the kept Ritz
+    values: sum(theta) / tr(Phi Phi^T), with tr(Phi Phi^T) = ||Phi||_F^2 (the
+    quantity of the section 5 kill test on spectral energy and of the rank
+    ablation); 0 for an all-zero Phi."""
+    tr = float(np.sum(Phi * Phi))
+    return float(np.sum(ritz_values)) / tr if tr > 0 else 0.0
+
+
 # --------------------------------------------------------------------------
 # Step 4: SimHash in the spectral subspace (Eq. 5, reading R6)
 # --------------------------------------------------------------------------

@@ -193,6 +193,29 @@ def test_lanczos_identical_rows_rank_one():
     assert abs(vals[-1] - np.sum(Phi[0] ** 2) * 64) < 1e-9 * vals[-1]
 
 
+# ---------------------------------------------------------------- spectral energy
+def test_spectral_energy_exact_and_bounded(tiny_run):
+    """sum(theta)/||Phi||_F^2: 1 when the Krylov space holds the whole spectrum
+    (sum of all eigenvalues = trace = squared Frobenius norm); within (0, 1] and
+    non-decreasing in r otherwise (Ritz values of a PSD operator are >= 0 and,
+    by interlacing, the top r of them sum to at most the top r eigenvalues)."""
+    rng = np.random.default_rng(7)
+    N, m, rank = 200, 30, 9
+    Phi = rng.standard_normal((N, rank)) @ rng.standard_normal((rank, m))
+    lz = O.lanczos(Phi, rng.standard_normal(N), 20)
+    vals, _, _, _ = O.ritz(lz, rank)
+    assert abs(O.spectral_energy(vals, Phi) - 1.0) < 1e-12
+    wl, X, Phi, lz = tiny_run
+    lam = np.linalg.eigvalsh(Phi @ Phi.T)[::-1]
+    prev = 0.0
+    for r in (1, 2, 4, 8):
+        vals, _, _, _ = O.ritz(lz, r)
+        e = O.spectral_energy(vals, Phi)
+        assert prev <= e <= lam[:r].sum() / lam.sum() + 1e-12 and e <= 1.0
+        prev = e
+    assert O.spectral_energy(np.ones(3), np.zeros((4, 5))) == 0.0
+
+
 # ---------------------------------------------------------------- normalised operator
 def test_normalised_operator_closed_forms(tiny_run):
     """Reading R16: the normalised matvec diag(s)^-1 Phi Phi^T with s = Phi Phi^T 1
