@@ -42,6 +42,10 @@ Readings of the paper that this file takes (where it is silent or ambiguous):
   R10 (section 3.5) Chunk size k = max(1, round(rho)) with round-half-to-even;
      the last chunk may be partial; chunks are renormalised like Eq. 7 and take
      the max position of their members.
+  R17 (section 3.4 position schemes) Median is the lower median of the member
+     positions; mean is their average rounded half to even; macro-tokens are
+     ordered by the representative position, ties (possible only for the mean)
+     by the group's max position.  Chunk groups use the same scheme.
   R16 (section 3.2 remark on row normalisation; appendix, softmax normalisation
      gap) The normalised variant estimates the row sums s = Phi (Phi^T 1) and
      uses diag(s)^-1 Phi Phi^T.  That operator is not symmetric; it is similar to
@@ -239,16 +243,35 @@ def renormalised_mean(rows):
     return mean * (eta / nrm)
 
 
-def merge(X, codes, positions=None, compact=False):
-    """Group tokens by code; one renormalised mean per group; max position;
-    groups ordered by that position (reading R7)."""
+def group_position(p, scheme="max"):
+    """Representative position of a group with member positions p (section 3.4):
+    max (default), lower median, or mean rounded half to even (reading R17)."""
+    p = sorted(int(v) for v in p)
+    if scheme == "max":
+        return p[-1]
+    if scheme == "median":
+        return p[(len(p) - 1) // 2]
+    if scheme == "mean":
+        q, rem = divmod(sum(p), len(p))
+        if 2 * rem > len(p) or (2 * rem == len(p) and q % 2 == 1):
+            q += 1
+        return q
+    raise ValueError(scheme)
+
+
+def merge(X, codes, positions=None, compact=False, scheme="max"):
+    """Group tokens by code; one renormalised mean per group; the group's
+    representative position (max by default); groups ordered by that position,
+    ties (possible for the mean) by the max position (readings R7, R17)."""
     X = np.asarray(X)
     N = len(codes)
     pos = np.arange(N, dtype=np.int64) if positions is None else np.asarray(positions, np.int64)
     groups = {}
     for i in range(N):
         groups.setdefault(int(codes[i]), []).append(i)
-    entries = sorted(((max(pos[idx]), c, idx) for c, idx in groups.items()), key=lambda e: e[0])
+    entries = sorted(((group_position(pos[idx], scheme), max(pos[idx]), c, idx)
+                      for c, idx in groups.items()), key=lambda e: (e[0], e[1]))
+    entries = [(p, c, idx) for p, _, c, idx in entries]
     M = len(entries)
     E = np.zeros((M, X.shape[1]))
     P = np.zeros(M, dtype=np.int64)
@@ -308,12 +331,14 @@ def chunk_size(rho):
     return max(1, int(round(rho)))          # Python round: half to even (reading R10)
 
 
-def chunk_pool(Xw, k, pos0=0):
-    """Section 3.5: consecutive groups of k rows, renormalised mean, max position."""
+def chunk_pool(Xw, k, pos0=0, scheme="max"):
+    """Section 3.5: consecutive groups of k rows, renormalised mean, the group's
+    representative position (max by default, reading R17)."""
     L = Xw.shape[0]
     starts = list(range(0, L, k))
     E = np.stack([renormalised_mean(Xw[s:min(s + k, L)]) for s in starts])
-    P = np.array([pos0 + min(s + k, L) - 1 for s in starts], dtype=np.int64)
+    P = np.array([group_position(range(pos0 + s, pos0 + min(s + k, L)), scheme) for s in starts],
+                 dtype=np.int64)
     return E, P
 
 
@@ -332,7 +357,7 @@ class CompressResult:
 
 
 def compress(X, W, psi, q1, R, n_it, r, kernel="softmax", positions=None, keep_phi=True,
-             normalise=False):
+             normalise=False, scheme="max"):
     """One global Spectral-LSH pass over X (Algorithm 1); normalise=True runs
     it on the normalised operator (reading R16)."""
     Phi = feature_map(X, W, psi, kernel)
@@ -342,7 +367,7 @@ def compress(X, W, psi, q1, R, n_it, r, kernel="softmax", positions=None, keep_p
     vals, Z, _, _ = ritz(lz, r)
     proj = projections(Z, R)
     codes = simhash(Z, R)
-    mg = merge(X, codes, positions)
+    mg = merge(X, codes, positions, scheme=scheme)
     return CompressResult(Phi if keep_phi else None, lz, vals, Z, proj, codes, mg)
 
 
@@ -358,7 +383,7 @@ class WindowResult:
 
 
 def compress_adaptive(X, L, rho, W, psi, q1_of_window, R, n_it, r, tau=None,
-                      kernel="softmax", keep_detail=False):
+                      kernel="softmax", keep_detail=False, scheme="max"):
     """Adaptive backend over consecutive windows of L tokens (section 3.6):
     score each window (Eq. 8), route it, run chunk pooling (section 3.5) or
     Spectral-LSH (Algorithm 1) on it with global positions, and return the
@@ -373,11 +398,11 @@ def compress_adaptive(X, L, rho, W, psi, q1_of_window, R, n_it, r, tau=None,
         spectral = route_window(L, score, rho, tau)
         if spectral:
             res = compress(Xw, W, psi, q1_of_window(w), R, n_it, r, kernel,
-                           positions=w * L + np.arange(L), keep_phi=False)
+                           positions=w * L + np.arange(L), keep_phi=False, scheme=scheme)
             out.append(WindowResult(w, score, True, res.merge.E, res.merge.P,
                                     res.merge.tok2macro, res if keep_detail else None))
         else:
             k = chunk_size(rho)
-            E, P = chunk_pool(Xw, k, pos0=w * L)
+            E, P = chunk_pool(Xw, k, pos0=w * L, scheme=scheme)
             out.append(WindowResult(w, score, False, E, P, np.arange(L) // k))
     return out

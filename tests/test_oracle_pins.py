@@ -339,6 +339,47 @@ def test_merge_hand_example():
     assert np.all(z.E == 0) and list(z.P) == [1]
 
 
+def test_position_schemes_hand_example():
+    """Section 3.4 position schemes worked by hand (tests/golden/positions_hand.txt)."""
+    f = "positions_hand.txt"
+    X = np.arange(16, dtype=np.float64).reshape(8, 2) + 1.0
+    codes = _rows(f, "CODES")[0].astype(int)
+    for scheme, tag in (("max", "MAX"), ("median", "MEDIAN"), ("mean", "MEAN")):
+        mg = O.merge(X, codes, scheme=scheme)
+        assert list(mg.P) == list(_rows(f, tag + "_P")[0].astype(int)), scheme
+        assert list(mg.tok2macro) == list(_rows(f, tag + "_MAP")[0].astype(int)), scheme
+    tie = O.merge(X[:4], _rows(f, "TIE_CODES")[0].astype(int), scheme="mean")
+    assert list(tie.P) == list(_rows(f, "TIE_P")[0].astype(int))
+    assert list(tie.tok2macro) == list(_rows(f, "TIE_MAP")[0].astype(int))
+    for scheme, tag in (("max", "CHUNK_MAX"), ("median", "CHUNK_MEDIAN"), ("mean", "CHUNK_MEAN")):
+        _, P = O.chunk_pool(X, 3, scheme=scheme)
+        assert list(P) == list(_rows(f, tag)[0].astype(int)), scheme
+
+
+def test_position_schemes_invariants():
+    """Every scheme keeps the same groups and embeddings; median positions are
+    member positions; mean positions lie within [min, max]; max positions are
+    causal; positions are non-decreasing along the macro order."""
+    rng = np.random.default_rng(11)
+    N = 500
+    X = rng.standard_normal((N, 4))
+    codes = rng.integers(0, 40, N)
+    pos = 1000 + np.arange(N)
+    ref = O.merge(X, codes, positions=pos)
+    for scheme in ("max", "median", "mean"):
+        mg = O.merge(X, codes, positions=pos, scheme=scheme)
+        assert np.all(np.diff(mg.P) >= 0)
+        assert sorted(map(tuple, mg.members)) == sorted(map(tuple, ref.members))
+        for k, idx in enumerate(mg.members):
+            p = pos[idx]
+            if scheme == "median":
+                assert mg.P[k] in p
+            assert p.min() <= mg.P[k] <= p.max()
+            kr = ref.tok2macro[idx[0]]
+            assert np.array_equal(mg.E[k], ref.E[kr])
+        assert np.all(mg.tok2macro[np.arange(N)] >= 0)
+
+
 def test_merge_invariants():
     rng = np.random.default_rng(3)
     N, D = 700, 5
