@@ -77,6 +77,12 @@ typedef struct slh_ctx slh_ctx;
                                     operator's Ritz vectors (the normalised
                                     operator's are diag(s)^-1/2 Z: the same SimHash
                                     codes).  0 (default): Phi Phi^T as in Eq. 4     */
+#define SLH_OPT_POS_SCHEME    8  /* macro-token positions (section 3.4): 0 max of the
+                                    members' positions (default), 1 lower median,
+                                    2 mean rounded half to even; macro-tokens are
+                                    ordered by that position, ties (mean only) by
+                                    the max position.  Chunk groups of the adaptive
+                                    backend use the same scheme                     */
 #define SLH_OPT_SHORT_WINDOWS 6  /* 1 (default): windows of L <= 32 tokens run Lanczos,
                                     Eigh and Ritz in one wavefront per window on the
                                     explicit L x L operator Phi_w Phi_w^T (the same
@@ -231,6 +237,17 @@ int slh_load(slh_ctx *ctx, int32_t which, const void *src, int64_t bytes);
  * Synchronises the stream.
  */
 int slh_stage_times(slh_ctx *ctx, double *ms_out, int32_t n);
+
+/*
+ * Spectral-energy fraction (section 5 kill test on spectral energy; rank
+ * ablation): for each spectral window, sum of its r kept Ritz values divided by
+ * tr(Phi_w Phi_w^T) = ||Phi_w||_F^2, the squared Frobenius norm of the rows the
+ * Lanczos step used (after the row normalisation when SLH_OPT_NORMALIZE = 1);
+ * 0 for a window whose rows are all zero.  Call after slh_lanczos.
+ * energy_out: host, n_spectral doubles (window order of SLH_OUT_WINDOWS).
+ * Synchronises the stream.  SLH_ESTATE before slh_lanczos.
+ */
+int slh_spectral_energy(slh_ctx *ctx, double *energy_out);
 
 /* Number of windows and of spectral windows of the current routing. */
 int64_t slh_num_windows(const slh_ctx *ctx);

@@ -24,6 +24,7 @@ SOURCES = [
     "k_eig.hip",
     "k_local.hip",
     "k_norm.hip",
+    "k_diag.hip",
     "k_hash.hip",
     "k_merge.hip",
     "k_route.hip",

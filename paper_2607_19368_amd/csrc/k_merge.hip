@@ -21,6 +21,8 @@
 #include "slh_device.h"
 #include "slh_internal.h"
 
+#include <climits>
+
 namespace slh {
 
 #define MG_CHMAX 64
@@ -253,6 +255,166 @@ __global__ __launch_bounds__(1024) void k_mg_book_lds(MergeWS w, int P, int tb) 
   if (tid == 0) w.mw[win] = carry;
 }
 
+// inclusive max-scan of one int per thread over a 1024-thread block
+__device__ __forceinline__ int block_incl_max_1024(int v, int* wsum, int& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int t = __shfl_up(v, o, 64);
+    if (lane >= o) v = max(v, t);
+  }
+  __syncthreads();
+  if (lane == 63) wsum[wave] = v;
+  __syncthreads();
+  int pre = INT_MIN, tot = INT_MIN;
+  for (int k = 0; k < 16; ++k) {
+    int x = wsum[k];
+    if (k < wave) pre = max(pre, x);
+    tot = max(tot, x);
+  }
+  total = tot;
+  return max(v, pre);
+}
+
+// inclusive scan (sum) of one int64 per thread over a 1024-thread block
+__device__ __forceinline__ long long block_incl_scan_i64(long long v, long long* wsum,
+                                                         long long& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    long long t = __shfl_up(v, o, 64);
+    if (lane >= o) v += t;
+  }
+  __syncthreads();
+  if (lane == 63) wsum[wave] = v;
+  __syncthreads();
+  long long pre = 0, tot = 0;
+  for (int k = 0; k < 16; ++k) {
+    long long x = wsum[k];
+    if (k < wave) pre += x;
+    tot += x;
+  }
+  total = tot;
+  return v + pre;
+}
+
+__device__ __forceinline__ int mg_scheme_pos(int scheme, int first, int cnt, long long sum,
+                                             int median_pos, int max_pos) {
+  if (scheme == 1) return median_pos;
+  if (scheme == 2) {                             // mean, rounded half to even
+    long long q = sum / cnt, rem = sum - q * cnt;
+    if (2 * rem > cnt || (2 * rem == cnt && (q & 1))) ++q;
+    return (int)q;
+  }
+  (void)first;
+  return max_pos;
+}
+
+// Position schemes other than max (section 3.4): each bucket's representative
+// position is the lower median (scheme 1) or the mean rounded half to even
+// (scheme 2) of its member positions, and the buckets of a spectral window are
+// re-ranked by (that position, max position).  One 1024-thread block per window;
+// it reuses the book-keeping's sorted member order (sval: members of a bucket
+// are a run of ascending tokens) and runs (sloc).  Writes posv[s] = global
+// representative position at each run end s and rewrites sloc with the new
+// ranks.  Scratch (window slices of N-entry arrays): st run start per sorted
+// position, pre int64 prefix sums of member positions, tp per token the
+// representative of the bucket whose last member it is (-1 otherwise), cnt a
+// histogram of representative positions, hb its exclusive scan, rk the new rank
+// at each run start.  Ties (mean only) are counted directly: tied buckets scan
+// the window's tokens below their max position.
+__global__ __launch_bounds__(1024) void k_mg_rerank(MergeWS w, int scheme, int* __restrict__ posv,
+                                                    int* __restrict__ st, long long* __restrict__ pre,
+                                                    int* __restrict__ tp, int* __restrict__ cnt,
+                                                    int* __restrict__ hb, int* __restrict__ rk) {
+  const int win = blockIdx.x, tid = threadIdx.x;
+  const int L = w.L;
+  const int64_t base = (int64_t)win * L;
+  __shared__ int wsum[16];
+  __shared__ long long wsum64[16];
+  if (!w.route[win]) {
+    // chunk groups of k consecutive tokens (sorted order = token order)
+    const int k = w.chunk_k;
+    for (int g = tid; g < (L + k - 1) / k; g += 1024) {
+      const int s0 = g * k, s1 = min(s0 + k, L), n = s1 - s0;
+      const long long sum = (long long)n * (s0 + s1 - 1) / 2;
+      posv[base + s1 - 1] = (int)base + mg_scheme_pos(scheme, s0, n, sum, s0 + (n - 1) / 2, s1 - 1);
+    }
+    return;
+  }
+  // run starts (max-scan of start indices) and prefix sums of member positions
+  int carry = INT_MIN;
+  long long csum = 0;
+  for (int b0 = 0; b0 < L; b0 += 1024) {
+    const int s = b0 + tid;
+    int v = INT_MIN;
+    long long pv = 0;
+    if (s < L) {
+      v = (s == 0 || w.sloc[base + s] != w.sloc[base + s - 1]) ? s : INT_MIN;
+      pv = w.sval[base + s] - base;
+    }
+    int tot;
+    long long tot64;
+    const int inc = block_incl_max_1024(v, wsum, tot);
+    const long long pinc = block_incl_scan_i64(pv, wsum64, tot64);
+    if (s < L) {
+      st[base + s] = max(inc, carry);
+      pre[base + s] = csum + pinc;
+    }
+    carry = max(carry, tot);
+    csum += tot64;
+    __syncthreads();
+  }
+  for (int t = tid; t < L; t += 1024) {
+    tp[base + t] = -1;
+    cnt[base + t] = 0;
+  }
+  __threadfence();
+  __syncthreads();
+  // representative positions at run ends; histogram of them
+  for (int e = tid; e < L; e += 1024) {
+    if (e == L - 1 || w.sloc[base + e + 1] != w.sloc[base + e]) {
+      const int s0 = st[base + e], n = e - s0 + 1;
+      const long long sum = pre[base + e] - (s0 > 0 ? pre[base + s0 - 1] : 0);
+      const int mx = w.sval[base + e] - (int)base;
+      const int med = w.sval[base + s0 + (n - 1) / 2] - (int)base;
+      const int p = mg_scheme_pos(scheme, s0, n, sum, med, mx);
+      posv[base + e] = (int)base + p;
+      tp[base + mx] = p;
+      atomicAdd(&cnt[base + p], 1);
+    }
+  }
+  __threadfence();
+  __syncthreads();
+  // buckets with a smaller representative position: exclusive scan of cnt
+  int c2 = 0;
+  for (int b0 = 0; b0 < L; b0 += 1024) {
+    const int p = b0 + tid;
+    const int v = (p < L) ? cnt[base + p] : 0;
+    int tot;
+    const int inc = block_incl_scan_1024(v, wsum, tot);
+    if (p < L) hb[base + p] = c2 + inc - v;
+    c2 += tot;
+    __syncthreads();
+  }
+  __threadfence();
+  __syncthreads();
+  // rank = buckets with a smaller position + tied buckets with a smaller max
+  for (int e = tid; e < L; e += 1024) {
+    if (e == L - 1 || w.sloc[base + e + 1] != w.sloc[base + e]) {
+      const int p = posv[base + e] - (int)base;
+      const int mx = w.sval[base + e] - (int)base;
+      int r = hb[base + p];
+      if (cnt[base + p] > 1)
+        for (int t = 0; t < mx; ++t) r += (tp[base + t] == p);
+      rk[base + st[base + e]] = r;
+    }
+  }
+  __threadfence();
+  __syncthreads();
+  for (int s = tid; s < L; s += 1024) w.sloc[base + s] = rk[base + st[base + s]];
+}
+
 __global__ __launch_bounds__(1024) void k_mg_wbase(MergeWS w) {
   __shared__ int wsum[16];
   int carry = 0;
@@ -282,7 +444,7 @@ __global__ __launch_bounds__(256) void k_mg_finalize(MergeWS w, int* __restrict_
   const int tok = w.sval[s];
   if (tok2macro) tok2macro[tok] = g;
   const bool end = (s + 1 == w.N) || ((s + 1) % w.L == 0) || (w.sloc[s + 1] != loc);
-  if (end) P[g] = w.compact ? g : tok;
+  if (end) P[g] = w.compact ? g : (w.posv ? w.posv[s] : tok);
 }
 
 // Member rows are read 8 columns per thread (one 16-byte load for bf16, two
@@ -597,6 +759,9 @@ hipError_t launch_merge(const MergeWS& w, const void* X, int dtype, int64_t ldx,
   } else {
     hipLaunchKernelGGL(k_mg_book, dim3(w.n_win), dim3(1024), 0, s, w);
   }
+  if (w.scheme != 0)
+    hipLaunchKernelGGL(k_mg_rerank, dim3(w.n_win), dim3(1024), 0, s, w, w.scheme, w.posv, w.valA,
+                       w.pre, w.tmpi, w.segid, w.segk, w.valB);
   hipLaunchKernelGGL(k_mg_wbase, dim3(1), dim3(1024), 0, s, w);
   hipLaunchKernelGGL(k_mg_finalize, dim3((unsigned)((w.N + 255) / 256)), dim3(256), 0, s, w, P,
                      tok2macro);

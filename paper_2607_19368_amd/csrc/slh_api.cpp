@@ -123,7 +123,10 @@ struct slh_ctx {
 
   int short_win = 1;                // SLH_OPT_SHORT_WINDOWS
   int normalize = 0;                // SLH_OPT_NORMALIZE
+  int pos_scheme = 0;               // SLH_OPT_POS_SCHEME
+  DevBuf posv, mg_pre;
   DevBuf nm_part, nm_csum, rowsum;
+  DevBuf dg_rowsq, dg_energy;
 
   // timing (SLH_OPT_TIMING)
   int timing = 0;
@@ -437,6 +440,10 @@ int slh_set_option(slh_ctx* c, int32_t key, double v) {
       c->timing = (int)v;
       drop_graph(c);
       if (c->timing && make_events(c, 0)) return SLH_EHIP;
+      break;
+    case SLH_OPT_POS_SCHEME:
+      if (v != 0.0 && v != 1.0 && v != 2.0) return fail(c, SLH_EINVAL, "POS_SCHEME must be 0, 1 or 2");
+      c->pos_scheme = (int)v;
       break;
     case SLH_OPT_NORMALIZE:
       if (v != 0.0 && v != 1.0) return fail(c, SLH_EINVAL, "NORMALIZE must be 0 or 1");
@@ -790,6 +797,15 @@ int slh_merge(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, float* emb_
   w.part_nsum = P<double>(c->part_nsum);
   w.part_end = P<int>(c->part_end);
   w.CH = CH;
+  w.scheme = c->pos_scheme;
+  w.posv = nullptr;
+  w.pre = nullptr;
+  if (w.scheme) {
+    ENSURE(c, c->posv, (size_t)N * 4);
+    ENSURE(c, c->mg_pre, (size_t)N * 8);
+    w.posv = P<int>(c->posv);
+    w.pre = P<long long>(c->mg_pre);
+  }
   if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[7], c->stream));
   HIP_TRY(c, launch_merge(w, X, dtype == SLH_BF16 ? 0 : 1, ldx, emb_out, pos_out, tok2macro_out,
                           c->stream));
@@ -798,6 +814,21 @@ int slh_merge(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, float* emb_
   HIP_TRY(c, hipMemcpyAsync(&M, c->Mtot.p, 4, hipMemcpyDeviceToHost, c->stream));
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   *M_out = M;
+  return SLH_OK;
+}
+
+int slh_spectral_energy(slh_ctx* c, double* out) {
+  if (!c || !out) return SLH_EINVAL;
+  if (c->stage < 2) return fail(c, SLH_ESTATE, "slh_spectral_energy before slh_lanczos");
+  const int64_t L = window_len(c);
+  const int na = c->n_act;
+  if (na == 0) return SLH_OK;
+  ENSURE(c, c->dg_rowsq, (size_t)na * L * 8);
+  ENSURE(c, c->dg_energy, (size_t)na * 8);
+  HIP_TRY(c, launch_energy(P<float>(c->Phi), P<double>(c->theta), na, (int)L, (int)c->m, c->r,
+                           P<double>(c->dg_rowsq), P<double>(c->dg_energy), c->stream));
+  HIP_TRY(c, hipMemcpyAsync(out, c->dg_energy.p, (size_t)na * 8, hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
   return SLH_OK;
 }
 

@@ -83,6 +83,10 @@ int normalise_groups(int n_act, int L, int m, int n_cu);   // row groups G of th
 hipError_t launch_normalise(float* Phi, int n_act, int L, int m, int G, double* part, double* csum,
                             double* s_out, hipStream_t s);   // part: [n_act][G][m], csum: [n_act][m]
 
+// ---- diagnostics (k_diag.hip): per window sum(theta) / ||Phi_w||_F^2 ----
+hipError_t launch_energy(const float* Phi, const double* theta, int n_act, int L, int m, int r,
+                         double* rowsq, double* energy, hipStream_t s);   // rowsq: [n_act][L]
+
 hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
 
 // ---- merge (k_merge.hip) ----
@@ -109,6 +113,9 @@ struct MergeWS {
   double* part_nsum;            // [2 * nchunks] sum of member norms
   int* part_end;                // [2 * nchunks] 1 if the bucket ends in this slot
   int CH;                       // sorted positions per reduction chunk (<= 64)
+  int scheme;                   // position scheme: 0 max, 1 lower median, 2 mean (half to even)
+  int* posv;                    // [N] scheme != 0: representative position at each run end
+  long long* pre;               // [N] scheme != 0: prefix sums of member positions
 };
 int merge_nchunks(int64_t N, int CH);
 hipError_t launch_merge(const MergeWS& w, const void* X, int dtype, int64_t ldx,

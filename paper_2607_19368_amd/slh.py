@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(_HERE, "libslh.so")
 SLH_OK, SLH_EINVAL, SLH_ENOMEM, SLH_EHIP, SLH_ESTATE = 0, -1, -2, -3, -4
 SLH_BF16, SLH_F32 = 0, 1
 SLH_OPT_KERNEL, SLH_OPT_WINDOW_LEN, SLH_OPT_POS_MODE, SLH_OPT_BREAKDOWN_TOL, SLH_OPT_TIMING = 1, 2, 3, 4, 5
-SLH_OPT_SHORT_WINDOWS, SLH_OPT_NORMALIZE = 6, 7
+SLH_OPT_SHORT_WINDOWS, SLH_OPT_NORMALIZE, SLH_OPT_POS_SCHEME = 6, 7, 8
 SLH_OUT_PHI, SLH_OUT_ALPHA, SLH_OUT_BETA, SLH_OUT_Z = 1, 2, 3, 4
 SLH_OUT_PROJ, SLH_OUT_CODES, SLH_OUT_THETA, SLH_OUT_Q, SLH_OUT_WINDOWS = 5, 6, 7, 8, 9
 SLH_OUT_ROWSUM = 10
@@ -25,7 +25,7 @@ EXPORTS = [
     "slh_gen_params", "slh_gen_start", "slh_create", "slh_destroy", "slh_last_error",
     "slh_set_option", "slh_set_stream", "slh_route", "slh_feature_map", "slh_lanczos",
     "slh_simhash", "slh_merge", "slh_merge_capacity", "slh_copy_out", "slh_num_windows",
-    "slh_num_spectral", "slh_load", "slh_stage_times",
+    "slh_num_spectral", "slh_load", "slh_stage_times", "slh_spectral_energy",
 ]
 
 _lib = None
@@ -62,6 +62,7 @@ def load():
         "slh_num_windows": (i64, [vp]),
         "slh_num_spectral": (i64, [vp]),
         "slh_load": (i32, [vp, i32, vp, i64]),
+        "slh_spectral_energy": (i32, [vp, vp]),
         "slh_stage_times": (i32, [vp, vp, i32]),
     }
     for name, (res, args) in sig.items():
@@ -272,3 +273,10 @@ def compress(ctx, X, n_it, rho=None, tau=-1.0, want_ritz=False):
     slh_simhash(ctx)
     E, P, t2m, M = slh_merge(ctx, X)
     return E, P, t2m, M, lz
+
+
+def slh_spectral_energy(ctx):
+    """Per spectral window: sum of the kept Ritz values / ||Phi_w||_F^2."""
+    out = np.empty(ctx.n_spectral, np.float64)
+    _check(ctx, load().slh_spectral_energy(ctx.handle, _ptr(out)), "slh_spectral_energy")
+    return out

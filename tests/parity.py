@@ -62,7 +62,7 @@ class Run:
 
 def run_gpu(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel=0, compact=False,
             phi_from=None, codes_from=None, want_phi=False, X=None, short_windows=None,
-            normalise=False):
+            normalise=False, scheme=0):
     """phi_from: host float32 array (n_act*L, m) loaded instead of computing Phi;
     codes_from: host uint32 (N,) loaded instead of computing codes;
     short_windows: value of SLH_OPT_SHORT_WINDOWS (None keeps the default)."""
@@ -81,6 +81,8 @@ def run_gpu(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel=0, compact=F
         P.slh_set_option(ctx, B.SLH_OPT_SHORT_WINDOWS, short_windows)
     if normalise:
         P.slh_set_option(ctx, B.SLH_OPT_NORMALIZE, 1)
+    if scheme:
+        P.slh_set_option(ctx, B.SLH_OPT_POS_SCHEME, scheme)
     Xd = to_device_x(inp) if X is None else X
     run = Run()
     if rho is not None:
@@ -119,7 +121,7 @@ def run_gpu(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel=0, compact=F
 
 
 def run_oracle(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel="softmax", compact=False,
-               phi_rows=None, normalise=False):
+               phi_rows=None, normalise=False, scheme="max"):
     wl = inp.workload
     N = wl.N
     L = window or N
@@ -150,7 +152,7 @@ def run_oracle(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel="softmax"
             vals, Z, _, _ = O.ritz(lz, wl.r)
             proj = O.projections(Z, R)
             codes = O.simhash(Z, R)
-            mg = O.merge(Xw, codes, positions=w * L + np.arange(L))
+            mg = O.merge(Xw, codes, positions=w * L + np.arange(L), scheme=scheme)
             al = np.zeros(n_it); al[:lz.n_eff] = lz.alpha
             be = np.zeros(n_it); be[:lz.n_eff] = lz.beta
             run.windows.append(Window(w, True, codes, proj, vals, Z, lz.n_eff, al, be))
@@ -159,7 +161,7 @@ def run_oracle(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel="softmax"
             E, Pw, tm = mg.E, mg.P, mg.tok2macro
         else:
             k = O.chunk_size(rho)
-            E, Pw = O.chunk_pool(Xw, k, pos0=w * L)
+            E, Pw = O.chunk_pool(Xw, k, pos0=w * L, scheme=scheme)
             tm = np.arange(L) // k
         Es.append(E)
         Ps.append(Pw)
@@ -228,7 +230,7 @@ class Report:
 
 
 def compare(o, g, L, check_spectral=True, ritz_rel=RITZ_REL, angle=ANGLE, emb_rel=EMB_REL,
-            exact_codes=False, merge_only=False, unc=None):
+            exact_codes=False, merge_only=False, unc=None, scheme="max"):
     """Assert the parity rules; returns a Report.
 
     unc: optional {window: U} from oracle_uncertainty(); a SimHash bit whose
@@ -333,10 +335,22 @@ def compare(o, g, L, check_spectral=True, ritz_rel=RITZ_REL, angle=ANGLE, emb_re
     for i, k in enumerate(g.t2m):
         members_g[k].append(i)
     assert all(len(mm) > 0 for mm in members_g)
-    # GPU structural invariants: strictly increasing positions, causal, max rule
-    assert np.all(np.diff(g.P) > 0)
+    # GPU structural invariants of the position scheme (section 3.4): max and
+    # median positions are distinct members (strictly increasing), the max is
+    # causal; mean positions lie within the members' range (non-decreasing)
+    if scheme == "mean":
+        assert np.all(np.diff(g.P) >= 0)
+    else:
+        assert np.all(np.diff(g.P) > 0)
     for k, mm in enumerate(members_g):
-        assert g.P[k] == max(mm) or g.P[k] == k
+        if g.P[k] == k and not (min(mm) <= k <= max(mm)):
+            continue                                   # compact positions
+        if scheme == "max":
+            assert g.P[k] == max(mm)
+        elif scheme == "median":
+            assert g.P[k] in mm
+        else:
+            assert min(mm) <= g.P[k] <= max(mm)
     for k, mm in enumerate(members_o):
         if excluded_tok[mm].any():
             rep.buckets_excluded += 1

@@ -411,3 +411,108 @@ def test_normalised_operator(case):
     _say(f"   {rep}  M={len(g.P)}")
     if unc is not None:
         assert rep.undecided_windows <= len(unc) // 4
+
+
+@pytest.mark.parametrize("case", ["tiny", "windows256", "local16_normalised"])
+def test_spectral_energy(case):
+    """slh_spectral_energy: per spectral window, sum of the kept Ritz values over
+    ||Phi_w||_F^2, against the oracle's value on the same inputs (the GPU's fp32
+    Phi and fp64 sums: within 1e-6 relative)."""
+    import paper_2607_19368_amd as P
+    from paper_2607_19368_amd import slh as B
+    norm = False
+    if case == "tiny":
+        inp, L = make_inputs("tiny"), 0
+    elif case == "windows256":
+        inp, L = _custom("ewin", 4 * 256, 512, 256, 24, 8, 8), 256
+    else:
+        inp, L, norm = make_inputs("local16", N=512), 16, True
+    wl = inp.workload
+    ctx = P.slh_create(wl.N, wl.D, wl.m, wl.r, wl.bits, 0)
+    if L:
+        P.slh_set_option(ctx, B.SLH_OPT_WINDOW_LEN, L)
+    if norm:
+        P.slh_set_option(ctx, B.SLH_OPT_NORMALIZE, 1)
+    Xd = PR.to_device_x(inp)
+    P.slh_feature_map(ctx, Xd)
+    ritz, iters = P.slh_lanczos(ctx, wl.n_it, want=True)
+    e = P.slh_spectral_energy(ctx)
+    Lw = L or wl.N
+    W, psi = OP.projection(0, wl.D, wl.m), OP.phases(0, wl.m)
+    eo = []
+    for w in range(wl.N // Lw):
+        Phi = O.feature_map(inp.x_float(slice(w * Lw, (w + 1) * Lw)), W, psi)
+        if norm:
+            Phi, _ = O.normalised_features(Phi)
+        vals, _, _, _ = O.ritz(O.lanczos(Phi, OP.start_vector(0, Lw, w), wl.n_it), wl.r)
+        eo.append(O.spectral_energy(vals, Phi))
+    eo = np.array(eo)
+    rel = np.abs(e - eo) / eo
+    _say(f"[energy] {case}: gpu {e[:4]} oracle {eo[:4]} max rel {rel.max():.2e}")
+    assert np.all((e > 0) & (e <= 1.0 + 1e-12)) and rel.max() < 1e-6
+
+
+@pytest.mark.parametrize("scheme", ["median", "mean"])
+@pytest.mark.parametrize("case", ["tiny", "windows", "long"])
+def test_position_schemes(scheme, case):
+    """SLH_OPT_POS_SCHEME (section 3.4): the oracle's codes are loaded and the
+    GPU merge must give the same members, positions and order as the oracle's
+    merge under the median / mean scheme, bit for bit (embeddings 1e-5).
+    windows: 8 windows of 256 tokens, half routed to chunk pooling (whose groups
+    take the same scheme); long: one window of 20000 tokens (the global-memory
+    book-keeping path) with a Zipf-like code distribution."""
+    sid = {"median": 1, "mean": 2}[scheme]
+    rho = None
+    if case == "tiny":
+        inp, L = make_inputs("tiny"), 0
+        codes = np.random.default_rng(1).integers(0, 64, inp.workload.N)
+    elif case == "windows":
+        inp, L, rho = _custom("pwin", 8 * 256, 256, 256, 16, 8, 8), 256, 8.0
+        codes = np.random.default_rng(2).integers(0, 256, inp.workload.N)
+    else:
+        inp, L = _custom("plong", 20000, 64, 256, 8, 4, 12), 0
+        rng = np.random.default_rng(3)
+        codes = np.minimum(rng.zipf(1.3, inp.workload.N) - 1, 4095)
+    wl = inp.workload
+    Lw = L or wl.N
+    tau = -1.0
+    route = np.ones(wl.N // Lw, bool)
+    if rho is not None:
+        sc = np.array([O.redundancy_score(inp.x_float(slice(w * Lw, (w + 1) * Lw)))
+                       for w in range(wl.N // Lw)])
+        tau = float(np.median(sc))
+        route = np.array([O.route_window(Lw, v, rho, tau) for v in sc])
+    _say(f"[positions] {scheme} {case} N={wl.N} window={L} spectral windows={int(route.sum())}")
+    g = PR.run_gpu(inp, n_it=wl.r, window=L, rho=rho, tau=tau, codes_from=codes.astype(np.uint32),
+                   scheme=sid)
+    Es, Ps, t2m, base = [], [], np.zeros(wl.N, np.int64), 0
+    for w in range(wl.N // Lw):
+        Xw = inp.x_float(slice(w * Lw, (w + 1) * Lw))
+        if route[w]:
+            mg = O.merge(Xw, codes[w * Lw:(w + 1) * Lw], positions=w * Lw + np.arange(Lw),
+                         scheme=scheme)
+            E, P, tm = mg.E, mg.P, mg.tok2macro
+        else:
+            k = O.chunk_size(rho)
+            E, P = O.chunk_pool(Xw, k, pos0=w * Lw, scheme=scheme)
+            tm = np.arange(Lw) // k
+        Es.append(E)
+        Ps.append(P)
+        t2m[w * Lw:(w + 1) * Lw] = base + tm
+        base += len(P)
+    E, P = np.concatenate(Es), np.concatenate(Ps)
+    assert np.array_equal(g.P, P)
+    assert np.array_equal(g.t2m, t2m)
+    rel = np.linalg.norm(g.E - E, axis=1) / np.maximum(np.linalg.norm(E, axis=1), 1e-30)
+    _say(f"   M={len(P)} max emb rel {rel.max():.2e}; ties in P: {int(np.sum(np.diff(P) == 0))}")
+    assert rel.max() <= 1e-5
+
+
+def test_position_scheme_end_to_end():
+    """The whole path on the tiny mixture under the median scheme."""
+    inp = make_inputs("tiny")
+    wl = inp.workload
+    g = PR.run_gpu(inp, n_it=wl.n_it, scheme=1)
+    o = PR.run_oracle(inp, n_it=wl.n_it, scheme="median")
+    rep = PR.compare(o, g, wl.N, scheme="median")
+    _say(f"[positions e2e] {rep}")
