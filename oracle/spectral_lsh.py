@@ -46,6 +46,9 @@ Readings of the paper that this file takes (where it is silent or ambiguous):
      positions; mean is their average rounded half to even; macro-tokens are
      ordered by the representative position, ties (possible only for the mean)
      by the group's max position.  Chunk groups use the same scheme.
+  R18 (section 5 kill test on bucket purity) Purity counts token pairs i < j of
+     one bucket (one window) whose embeddings, as given, have cosine
+     similarity strictly above the threshold (0.7); a zero row has cosine 0.
   R16 (section 3.2 remark on row normalisation; appendix, softmax normalisation
      gap) The normalised variant estimates the row sums s = Phi (Phi^T 1) and
      uses diag(s)^-1 Phi Phi^T.  That operator is not symmetric; it is similar to
@@ -204,6 +207,34 @@ def spectral_energy(ritz_values, Phi):
     ablation); 0 for an all-zero Phi."""
     tr = float(np.sum(Phi * Phi))
     return float(np.sum(ritz_values)) / tr if tr > 0 else 0.0
+
+
+def bucket_purity(X, codes, thresh=0.7, L=None):
+    """Bucket purity (section 5 kill test on buckets): over token pairs i < j
+    that share a bucket (the same code, within the same window of L tokens when
+    L is given), the number whose embeddings have cosine similarity > thresh,
+    and the number of such pairs.  cos is taken as 0 when either row is zero
+    (reading R18).  Returns (similar_pairs, pairs)."""
+    X = np.asarray(X, dtype=np.float64)
+    N = len(codes)
+    L = L or N
+    nrm = np.linalg.norm(X, axis=1)
+    sim = tot = 0
+    for w in range(N // L):
+        groups = {}
+        for i in range(w * L, (w + 1) * L):
+            groups.setdefault(int(codes[i]), []).append(i)
+        for idx in groups.values():
+            n = len(idx)
+            if n < 2:
+                continue
+            G = X[idx] @ X[idx].T
+            den = np.outer(nrm[idx], nrm[idx])
+            C = np.divide(G, den, out=np.zeros_like(G), where=den > 0)
+            iu = np.triu_indices(n, 1)
+            sim += int(np.count_nonzero(C[iu] > thresh))
+            tot += n * (n - 1) // 2
+    return sim, tot
 
 
 # --------------------------------------------------------------------------

@@ -380,6 +380,32 @@ def test_position_schemes_invariants():
         assert np.all(mg.tok2macro[np.arange(N)] >= 0)
 
 
+def test_bucket_purity_hand_and_brute_force():
+    """Reading R18.  Hand example: rows (1,0), (1,0.1), (0,1), (-1,0), (0,0) with
+    codes 1 1 1 1 1 -> 10 pairs; cos > 0.7 only for rows 0-1 (0.995); the zero
+    row pairs count as cos 0.  Then a brute-force double loop on random data
+    with windows, and the closed forms for identical and orthogonal rows."""
+    X = np.array([[1.0, 0.0], [1.0, 0.1], [0.0, 1.0], [-1.0, 0.0], [0.0, 0.0]])
+    assert O.bucket_purity(X, np.ones(5, int)) == (1, 10)
+    assert O.bucket_purity(X, np.arange(5)) == (0, 0)
+    rng = np.random.default_rng(9)
+    N, L = 96, 32
+    Xr = rng.standard_normal((N, 3))
+    Xr[5] = 0.0
+    codes = rng.integers(0, 4, N)
+    sim = tot = 0
+    for i in range(N):
+        for j in range(i + 1, N):
+            if i // L == j // L and codes[i] == codes[j]:
+                tot += 1
+                ni, nj = np.linalg.norm(Xr[i]), np.linalg.norm(Xr[j])
+                c = Xr[i] @ Xr[j] / (ni * nj) if ni > 0 and nj > 0 else 0.0
+                sim += c > 0.7
+    assert O.bucket_purity(Xr, codes, L=L) == (sim, tot)
+    assert O.bucket_purity(np.tile(Xr[:1], (7, 1)), np.zeros(7, int)) == (21, 21)
+    assert O.bucket_purity(np.eye(6), np.zeros(6, int)) == (0, 15)
+
+
 def test_merge_invariants():
     rng = np.random.default_rng(3)
     N, D = 700, 5
