@@ -249,6 +249,18 @@ int slh_stage_times(slh_ctx *ctx, double *ms_out, int32_t n);
  */
 int slh_spectral_energy(slh_ctx *ctx, double *energy_out);
 
+/*
+ * Bucket purity (section 5 kill test on buckets): over token pairs i < j that
+ * share a bucket of a spectral window, counts_out[0] = pairs whose rows of X
+ * have cosine similarity > thresh (cosine 0 for a zero row), counts_out[1] =
+ * all such pairs; purity = counts_out[0] / counts_out[1].  X as passed to
+ * slh_merge (device, N x D, row stride ldx, x_dtype); thresh in [-1, 1] (the
+ * paper uses 0.7).  Call after slh_merge.  counts_out: host, 2 int64.
+ * Synchronises the stream.  SLH_ESTATE before slh_merge.
+ */
+int slh_bucket_purity(slh_ctx *ctx, const void *X, int32_t x_dtype, int64_t ldx, double thresh,
+                      int64_t *counts_out);
+
 /* Number of windows and of spectral windows of the current routing. */
 int64_t slh_num_windows(const slh_ctx *ctx);
 int64_t slh_num_spectral(const slh_ctx *ctx);

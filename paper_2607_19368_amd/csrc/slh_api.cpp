@@ -124,6 +124,8 @@ struct slh_ctx {
   int short_win = 1;                // SLH_OPT_SHORT_WINDOWS
   int normalize = 0;                // SLH_OPT_NORMALIZE
   int pos_scheme = 0;               // SLH_OPT_POS_SCHEME
+  int merged = 0;                   // slh_merge ran on the current codes
+  DevBuf dg_tiles, dg_counts;
   DevBuf posv, mg_pre;
   DevBuf nm_part, nm_csum, rowsum;
   DevBuf dg_rowsq, dg_energy;
@@ -457,6 +459,7 @@ int slh_set_option(slh_ctx* c, int32_t key, double v) {
       return fail(c, SLH_EINVAL, "unknown option %d", key);
   }
   c->stage = 0;
+  c->merged = 0;
   return SLH_OK;
 }
 
@@ -515,6 +518,7 @@ int slh_route(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, double rho,
   if (route_out) std::memcpy(route_out, c->route_h.data(), c->route_h.size());
   if (scores_out) std::memcpy(scores_out, sc.data(), sc.size() * sizeof(double));
   c->stage = 0;
+  c->merged = 0;
   return SLH_OK;
 }
 
@@ -556,6 +560,7 @@ int slh_feature_map(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx) {
     c->norm_timed = c->timing;
   }
   c->stage = 1;
+  c->merged = 0;
   return SLH_OK;
 }
 
@@ -708,6 +713,7 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
     HIP_TRY(c, hipStreamSynchronize(c->stream));
   }
   c->stage = 2;
+  c->merged = 0;
   return SLH_OK;
 }
 
@@ -729,6 +735,7 @@ int slh_simhash(slh_ctx* c, uint32_t* codes_out) {
     HIP_TRY(c, hipMemcpyAsync(codes_out, c->codes.p, (size_t)c->N * 4, hipMemcpyDeviceToDevice,
                               c->stream));
   c->stage = 3;
+  c->merged = 0;
   return SLH_OK;
 }
 
@@ -814,6 +821,7 @@ int slh_merge(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, float* emb_
   HIP_TRY(c, hipMemcpyAsync(&M, c->Mtot.p, 4, hipMemcpyDeviceToHost, c->stream));
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   *M_out = M;
+  c->merged = 1;
   return SLH_OK;
 }
 
@@ -829,6 +837,60 @@ int slh_spectral_energy(slh_ctx* c, double* out) {
                            P<double>(c->dg_rowsq), P<double>(c->dg_energy), c->stream));
   HIP_TRY(c, hipMemcpyAsync(out, c->dg_energy.p, (size_t)na * 8, hipMemcpyDeviceToHost, c->stream));
   HIP_TRY(c, hipStreamSynchronize(c->stream));
+  return SLH_OK;
+}
+
+int slh_bucket_purity(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, double thresh,
+                      int64_t* counts_out) {
+  if (!c || !counts_out) return SLH_EINVAL;
+  if (!c->merged) return fail(c, SLH_ESTATE, "slh_bucket_purity before slh_merge");
+  int rc = check_x(c, X, dtype, ldx);
+  if (rc) return rc;
+  if (!(thresh >= -1.0 && thresh <= 1.0)) return fail(c, SLH_EINVAL, "thresh must be in [-1, 1]");
+  if (c->norms_of != X)
+    if ((rc = prep_norms(c, X, dtype, ldx))) return rc;
+  const int64_t N = c->N, L = window_len(c);
+  // tiles of 64 x 64 sorted positions that hold same-bucket pairs (spectral windows)
+  std::vector<int> seg((size_t)N);
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  HIP_TRY(c, hipMemcpy(seg.data(), c->sseg.p, (size_t)N * 4, hipMemcpyDeviceToHost));
+  const int64_t nb = (N + 63) / 64;
+  std::vector<uint8_t> mark;
+  std::vector<int> tiles;
+  auto add = [&](int64_t A, int64_t B) {
+    const int64_t key = A * nb + B;
+    if (key >= (int64_t)mark.size() * 8) mark.resize((size_t)(key / 8 + 1 + nb), 0);
+    if (mark[(size_t)(key >> 3)] & (1u << (key & 7))) return;
+    mark[(size_t)(key >> 3)] |= (uint8_t)(1u << (key & 7));
+    tiles.push_back((int)A);
+    tiles.push_back((int)B);
+  };
+  for (int64_t s0 = 0; s0 < N;) {
+    int64_t s1 = s0 + 1;
+    while (s1 < N && seg[(size_t)s1] == seg[(size_t)s0]) ++s1;
+    if (s1 - s0 >= 2 && c->route_h[(size_t)(s0 / L)]) {
+      const int64_t fa = s0 / 64, fb = (s1 - 1) / 64;
+      for (int64_t A = fa; A <= fb; ++A)
+        for (int64_t B = A; B <= fb; ++B) add(A, B);
+    }
+    s0 = s1;
+  }
+  const int ntiles = (int)(tiles.size() / 2);
+  ENSURE(c, c->dg_counts, 16);
+  HIP_TRY(c, hipMemsetAsync(c->dg_counts.p, 0, 16, c->stream));
+  if (ntiles > 0) {
+    ENSURE(c, c->dg_tiles, tiles.size() * 4);
+    HIP_TRY(c, hipMemcpyAsync(c->dg_tiles.p, tiles.data(), tiles.size() * 4, hipMemcpyHostToDevice,
+                              c->stream));
+    HIP_TRY(c, launch_purity(X, dtype == SLH_BF16 ? 0 : 1, ldx, (int)c->D, P<int>(c->sval),
+                             P<int>(c->sseg), P<double>(c->nrm_x), N, P<int>(c->dg_tiles), ntiles,
+                             thresh, P<unsigned long long>(c->dg_counts), c->stream));
+  }
+  unsigned long long cnt[2] = {0, 0};
+  HIP_TRY(c, hipMemcpyAsync(cnt, c->dg_counts.p, 16, hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  counts_out[0] = (int64_t)cnt[0];
+  counts_out[1] = (int64_t)cnt[1];
   return SLH_OK;
 }
 
@@ -870,6 +932,7 @@ int slh_load(slh_ctx* c, int32_t which, const void* src, int64_t bytes) {
     ENSURE(c, c->Phi, (size_t)std::max<int64_t>(want, 4));
     if (want) HIP_TRY(c, hipMemcpyAsync(c->Phi.p, src, (size_t)want, hipMemcpyDeviceToDevice, c->stream));
     c->stage = 1;
+    c->merged = 0;
     return SLH_OK;
   }
   if (which == SLH_OUT_CODES) {
@@ -878,6 +941,7 @@ int slh_load(slh_ctx* c, int32_t which, const void* src, int64_t bytes) {
     ENSURE(c, c->codes, (size_t)want);
     HIP_TRY(c, hipMemcpyAsync(c->codes.p, src, (size_t)want, hipMemcpyDeviceToDevice, c->stream));
     c->stage = 3;
+    c->merged = 0;
     return SLH_OK;
   }
   return fail(c, SLH_EINVAL, "slh_load supports SLH_OUT_PHI and SLH_OUT_CODES");

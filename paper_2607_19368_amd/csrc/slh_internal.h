@@ -87,6 +87,12 @@ hipError_t launch_normalise(float* Phi, int n_act, int L, int m, int G, double* 
 hipError_t launch_energy(const float* Phi, const double* theta, int n_act, int L, int m, int r,
                          double* rowsq, double* energy, hipStream_t s);   // rowsq: [n_act][L]
 
+// bucket purity: tiles = ntiles (A, B) pairs of 64-position blocks of the sorted
+// member order; counts[0] += pairs with cos > thresh, counts[1] += pairs
+hipError_t launch_purity(const void* X, int dtype, int64_t ldx, int D, const int* sval,
+                         const int* sseg, const double* nrm, int64_t N, const int* tiles,
+                         int ntiles, double thresh, unsigned long long* counts, hipStream_t s);
+
 hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
 
 // ---- merge (k_merge.hip) ----

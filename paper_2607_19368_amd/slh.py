@@ -26,6 +26,7 @@ EXPORTS = [
     "slh_set_option", "slh_set_stream", "slh_route", "slh_feature_map", "slh_lanczos",
     "slh_simhash", "slh_merge", "slh_merge_capacity", "slh_copy_out", "slh_num_windows",
     "slh_num_spectral", "slh_load", "slh_stage_times", "slh_spectral_energy",
+    "slh_bucket_purity",
 ]
 
 _lib = None
@@ -63,6 +64,7 @@ def load():
         "slh_num_spectral": (i64, [vp]),
         "slh_load": (i32, [vp, i32, vp, i64]),
         "slh_spectral_energy": (i32, [vp, vp]),
+        "slh_bucket_purity": (i32, [vp, vp, i32, i64, ctypes.c_double, vp]),
         "slh_stage_times": (i32, [vp, vp, i32]),
     }
     for name, (res, args) in sig.items():
@@ -280,3 +282,13 @@ def slh_spectral_energy(ctx):
     out = np.empty(ctx.n_spectral, np.float64)
     _check(ctx, load().slh_spectral_energy(ctx.handle, _ptr(out)), "slh_spectral_energy")
     return out
+
+
+def slh_bucket_purity(ctx, X, thresh=0.7):
+    """(pairs with cosine > thresh, pairs) over same-bucket token pairs; X as
+    passed to slh_merge."""
+    p, dt, ld = _xinfo(X)
+    out = np.zeros(2, np.int64)
+    _check(ctx, load().slh_bucket_purity(ctx.handle, p, dt, ld, float(thresh), _ptr(out)),
+           "slh_bucket_purity")
+    return int(out[0]), int(out[1])

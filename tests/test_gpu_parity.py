@@ -516,3 +516,56 @@ def test_position_scheme_end_to_end():
     o = PR.run_oracle(inp, n_it=wl.n_it, scheme="median")
     rep = PR.compare(o, g, wl.N, scheme="median")
     _say(f"[positions e2e] {rep}")
+
+
+@pytest.mark.parametrize("case", ["tiny", "qwen7b", "windows"])
+def test_bucket_purity(case):
+    """slh_bucket_purity: same-bucket token pairs with cosine > 0.7 (bit-exact
+    counts against the oracle on the same codes; pairs whose fp64 cosine lies
+    within 1e-12 of the threshold may differ and are counted).  qwen7b: codes
+    = token id mod 4096 (identical tokens share buckets: the largest bucket
+    holds ~1100 pairs of identical rows); windows: 8 windows of 256, half
+    routed to chunk pooling (excluded: no LSH buckets)."""
+    import paper_2607_19368_amd as P
+    from paper_2607_19368_amd import slh as B
+    rho, L = None, 0
+    if case == "tiny":
+        inp = make_inputs("tiny")
+        codes = np.random.default_rng(1).integers(0, 16, inp.workload.N)
+    elif case == "qwen7b":
+        inp = make_inputs("qwen7b")
+        codes = inp.ids % 4096
+    else:
+        inp, L, rho = _custom("purw", 8 * 256, 256, 256, 16, 8, 8), 256, 8.0
+        codes = np.random.default_rng(2).integers(0, 8, inp.workload.N)
+    wl = inp.workload
+    Lw = L or wl.N
+    ctx = P.slh_create(wl.N, wl.D, wl.m, wl.r, wl.bits, 0)
+    if L:
+        P.slh_set_option(ctx, B.SLH_OPT_WINDOW_LEN, L)
+    Xd = PR.to_device_x(inp)
+    route = np.ones(wl.N // Lw, bool)
+    if rho is not None:
+        sc = np.array([O.redundancy_score(inp.x_float(slice(w * Lw, (w + 1) * Lw)))
+                       for w in range(wl.N // Lw)])
+        tau = float(np.median(sc))
+        r_gpu, _ = P.slh_route(ctx, Xd, rho, tau)
+        route = r_gpu.astype(bool)
+    import torch
+    P.slh_load(ctx, B.SLH_OUT_CODES, torch.from_numpy(codes.astype(np.int32)).cuda())
+    P.slh_merge(ctx, Xd)
+    sim, tot = P.slh_bucket_purity(ctx, Xd, 0.7)
+    X = inp.x_float()
+    osim = otot = near = 0
+    for w in range(wl.N // Lw):
+        if not route[w]:
+            continue
+        a, b = O.bucket_purity(X[w * Lw:(w + 1) * Lw], codes[w * Lw:(w + 1) * Lw])
+        osim += a
+        otot += b
+        # pairs within 1e-12 of the threshold (their bit may differ in fp64)
+        hi, _ = O.bucket_purity(X[w * Lw:(w + 1) * Lw], codes[w * Lw:(w + 1) * Lw], 0.7 + 1e-12)
+        lo, _ = O.bucket_purity(X[w * Lw:(w + 1) * Lw], codes[w * Lw:(w + 1) * Lw], 0.7 - 1e-12)
+        near += lo - hi
+    _say(f"[purity] {case}: gpu {sim}/{tot} oracle {osim}/{otot} near-threshold {near}")
+    assert tot == otot and abs(sim - osim) <= near
