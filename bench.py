@@ -227,6 +227,18 @@ def main():
             else:
                 out["roofline"] = dict(out["featmap_mfma"], traffic=None,
                                        kernel="k_featmap (bf16 MFMA GEMM + cos epilogue)")
+    # diagnostics of the last step (outside the timed regions): spectral-energy
+    # fraction of the kept Ritz values and bucket purity (section 5 kill tests)
+    if ctx.n_spectral:
+        t0 = time.perf_counter()
+        en = P.slh_spectral_energy(ctx)
+        t1 = time.perf_counter()
+        sim, tot = P.slh_bucket_purity(ctx, X, 0.7)
+        t2 = time.perf_counter()
+        out["diagnostics"] = {
+            "spectral_energy_mean": float(np.mean(en)), "spectral_energy_min": float(np.min(en)),
+            "bucket_purity": (sim / tot) if tot else None, "same_bucket_pairs": tot,
+            "energy_ms": 1e3 * (t1 - t0), "purity_ms": 1e3 * (t2 - t1)}
     if not a.no_cpu_baseline:
         cb = cpu_baseline(inp, tau=tau if wl.adaptive else None)
         out["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
