@@ -49,6 +49,9 @@ Readings of the paper that this file takes (where it is silent or ambiguous):
   R18 (section 5 kill test on bucket purity) Purity counts token pairs i < j of
      one bucket (one window) whose embeddings, as given, have cosine
      similarity strictly above the threshold (0.7); a zero row has cosine 0.
+  R19 (section 3.5, section 5.1) A preserved suffix of K tokens is not part of
+     any window or bucket: compression runs on the first N - K tokens and the
+     K tail tokens follow as singleton macro-tokens at their own positions.
   R16 (section 3.2 remark on row normalisation; appendix, softmax normalisation
      gap) The normalised variant estimates the row sums s = Phi (Phi^T 1) and
      uses diag(s)^-1 Phi Phi^T.  That operator is not symmetric; it is similar to
@@ -356,6 +359,24 @@ def route_window(L, score, rho, tau=None):
         return False
     t = tau_of_rho(rho) if tau is None else tau
     return score >= t
+
+
+def preserve_suffix(E, P, tok2macro, X_tail, pos0, compact=False):
+    """Section 3.5 (every backend can keep a fixed number of final tokens as
+    they are; section 5.1: the last 12 by default): each of the K tail rows
+    becomes a macro-token of its own (Eq. 7 on a single row gives the row) at its
+    own position pos0 + t, after the macro-tokens of the compressed tokens, whose
+    positions are all smaller (reading R19).  Returns (E, P, tok2macro) of the
+    whole prompt."""
+    X_tail = np.asarray(X_tail, dtype=np.float64)
+    K = X_tail.shape[0]
+    M = len(P)
+    E2 = np.concatenate([E, np.stack([renormalised_mean(X_tail[t:t + 1]) for t in range(K)])
+                         if K else np.zeros((0, E.shape[1]))])
+    P_tail = np.arange(M, M + K) if compact else pos0 + np.arange(K)
+    P2 = np.concatenate([np.asarray(P, np.int64), P_tail.astype(np.int64)])
+    t2m = np.concatenate([np.asarray(tok2macro, np.int64), np.arange(M, M + K, dtype=np.int64)])
+    return E2, P2, t2m
 
 
 def chunk_size(rho):

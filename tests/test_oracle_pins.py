@@ -406,6 +406,17 @@ def test_bucket_purity_hand_and_brute_force():
     assert O.bucket_purity(np.eye(6), np.zeros(6, int)) == (0, 15)
 
 
+def test_preserve_suffix_hand_example():
+    """Reading R19: two compressed macro-tokens then a kept tail of 2 rows."""
+    X = np.array([[3.0, 4.0], [1.0, 0.0], [0.0, 2.0], [-2.0, 0.0], [0.5, 0.5]])
+    mg = O.merge(X[:3], np.array([5, 3, 5]))          # {0, 2} at 2, {1} at 1 -> order {1}, {0, 2}
+    E, P, t2m = O.preserve_suffix(mg.E, mg.P, mg.tok2macro, X[3:], 3)
+    assert list(P) == [1, 2, 3, 4] and list(t2m) == [1, 0, 1, 2, 3]
+    assert np.array_equal(E[2:], X[3:]) and np.all(np.diff(P) > 0)
+    _, Pc, _ = O.preserve_suffix(mg.E, np.arange(2), mg.tok2macro, X[3:], 3, compact=True)
+    assert list(Pc) == [0, 1, 2, 3]
+
+
 def test_merge_invariants():
     rng = np.random.default_rng(3)
     N, D = 700, 5
