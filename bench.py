@@ -113,6 +113,8 @@ def main():
         if wl.x_dtype == "bf16" else torch.from_numpy(inp.X).cuda()
 
     ctx = P.slh_create(wl.N, wl.D, wl.m, wl.r, wl.bits, 0)
+    if wl.keep_last:
+        P.slh_set_option(ctx, B.SLH_OPT_KEEP_LAST, wl.keep_last)
     if wl.window:
         P.slh_set_option(ctx, B.SLH_OPT_WINDOW_LEN, wl.window)
     if wl.normalise:
@@ -175,7 +177,8 @@ def main():
         "config": {
             "workload": f"{wl.name}: N={wl.N} D={wl.D} m={wl.m} n_it={wl.n_it} r={wl.r} "
                         f"bits={wl.bits} rho={wl.rho:g}" + (f" window={wl.window}" if wl.window else "")
-                        + (" operator=row-normalised" if wl.normalise else ""),
+                        + (" operator=row-normalised" if wl.normalise else "")
+                        + (f" keep_last={wl.keep_last}" if wl.keep_last else ""),
             "inputs": "Zipf(1.1) token ids over a seeded N(0,0.02) bf16 embedding table"
                       if wl.x_dtype == "bf16" else "seeded Gaussian mixture, fp32",
             "precision": "bf16 MFMA feature map with fp32 accumulation, fp32 Phi, fp64 Lanczos/"

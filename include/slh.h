@@ -83,6 +83,17 @@ typedef struct slh_ctx slh_ctx;
                                     ordered by that position, ties (mean only) by
                                     the max position.  Chunk groups of the adaptive
                                     backend use the same scheme                     */
+#define SLH_OPT_KEEP_LAST     9  /* preserved suffix (section 3.5: every backend can
+                                    keep final tokens as they are; section 5.1: 12
+                                    by default): the last K tokens are not
+                                    compressed; each follows the compressed
+                                    macro-tokens as its own macro-token (its row,
+                                    its position).  Windows tile the first N - K
+                                    tokens (N - K must be a multiple of
+                                    WINDOW_LEN); routing, Phi and the Lanczos
+                                    outputs cover those tokens only; codes, the
+                                    token map and X keep N rows (tail codes are
+                                    0xFFFFFFFF).  0 (default) keeps none          */
 #define SLH_OPT_SHORT_WINDOWS 6  /* 1 (default): windows of L <= 32 tokens run Lanczos,
                                     Eigh and Ritz in one wavefront per window on the
                                     explicit L x L operator Phi_w Phi_w^T (the same

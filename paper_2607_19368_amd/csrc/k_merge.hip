@@ -737,6 +737,43 @@ static void dispatch_ppt(const MergeWS& w, const void* X, int64_t ldx, float* E,
   else launch_reduce_combine<DT, 8>(w, X, ldx, E, nchunks, s);      // D <= 32768
 }
 
+// Preserved suffix (section 3.5: every backend can keep a fixed number of final
+// tokens as they are; section 5.1: the last 12 by default): tail token N + t
+// becomes macro-token M + t with its own row (Eq. 7 on one row gives the row)
+// and position N + t (M + t in compact mode); M = the compressed part's count.
+template <int DT>
+__global__ __launch_bounds__(256) void k_mg_tail(const void* __restrict__ X, int64_t ldx, int D,
+                                                 int64_t N, const int* __restrict__ Mtot,
+                                                 int compact, float* __restrict__ E,
+                                                 int* __restrict__ P, int* __restrict__ tok2macro) {
+  const int t = blockIdx.x;
+  const int M = *Mtot;
+  const int64_t tok = N + t;
+  float* dst = E + (int64_t)(M + t) * D;
+  for (int c = threadIdx.x; c < D; c += 256) {
+    if constexpr (DT == 0) dst[c] = bf16_to_f32(((const uint16_t*)X)[tok * ldx + c]);
+    else dst[c] = ((const float*)X)[tok * ldx + c];
+  }
+  if (threadIdx.x == 0) {
+    P[M + t] = compact ? M + t : (int)tok;
+    if (tok2macro) tok2macro[tok] = M + t;
+  }
+}
+
+hipError_t launch_merge_tail(const void* X, int dtype, int64_t ldx, int D, int64_t N, int K,
+                             const int* Mtot, int compact, float* E, int* P, int* tok2macro,
+                             hipStream_t s) {
+  (void)hipGetLastError();
+  if (K <= 0) return hipSuccess;
+  if (dtype == 0)
+    hipLaunchKernelGGL(k_mg_tail<0>, dim3(K), dim3(256), 0, s, X, ldx, D, N, Mtot, compact, E, P,
+                       tok2macro);
+  else
+    hipLaunchKernelGGL(k_mg_tail<1>, dim3(K), dim3(256), 0, s, X, ldx, D, N, Mtot, compact, E, P,
+                       tok2macro);
+  return hipGetLastError();
+}
+
 int merge_nchunks(int64_t N, int CH) { return (int)((N + CH - 1) / CH); }
 
 hipError_t launch_merge(const MergeWS& w, const void* X, int dtype, int64_t ldx, float* E,

@@ -125,6 +125,8 @@ struct slh_ctx {
   int normalize = 0;                // SLH_OPT_NORMALIZE
   int pos_scheme = 0;               // SLH_OPT_POS_SCHEME
   int merged = 0;                   // slh_merge ran on the current codes
+  int64_t Ntot = 0;                 // prompt length; N = Ntot - keep_last tokens are compressed
+  int64_t keep_last = 0;            // SLH_OPT_KEEP_LAST
   DevBuf dg_tiles, dg_counts;
   DevBuf posv, mg_pre;
   DevBuf nm_part, nm_csum, rowsum;
@@ -277,7 +279,7 @@ int64_t capacity(const slh_ctx* c) {
   int64_t cap = 0;
   for (int64_t w = 0; w < c->n_win; ++w)
     cap += c->route_h[(size_t)w] ? per_spec : (L + c->chunk_k - 1) / c->chunk_k;
-  return cap;
+  return cap + c->keep_last;
 }
 
 }  // namespace
@@ -345,6 +347,7 @@ int slh_create(slh_ctx** out, int64_t N, int64_t D, int64_t m, int32_t r, int32_
   slh_ctx* c = new (std::nothrow) slh_ctx();
   if (!c) return SLH_ENOMEM;
   c->N = N;
+  c->Ntot = N;
   c->D = D;
   c->m = m;
   c->r = r;
@@ -443,6 +446,24 @@ int slh_set_option(slh_ctx* c, int32_t key, double v) {
       drop_graph(c);
       if (c->timing && make_events(c, 0)) return SLH_EHIP;
       break;
+    case SLH_OPT_KEEP_LAST: {
+      const int64_t K = (int64_t)v;
+      if ((double)K != v || K < 0 || c->Ntot - K < 2)
+        return fail(c, SLH_EINVAL, "KEEP_LAST must be an integer in [0, N - 2]");
+      const int64_t Nc = c->Ntot - K;
+      const int64_t Le = c->L ? c->L : Nc;
+      if (Nc % Le != 0)
+        return fail(c, SLH_EINVAL, "N - KEEP_LAST must be a multiple of WINDOW_LEN");
+      c->keep_last = K;
+      c->N = Nc;
+      c->n_win = Nc / Le;
+      c->norms_of = nullptr;
+      c->q1_L = -1;
+      route_all_spectral(c);
+      c->routed = false;
+      drop_graph(c);
+      break;
+    }
     case SLH_OPT_POS_SCHEME:
       if (v != 0.0 && v != 1.0 && v != 2.0) return fail(c, SLH_EINVAL, "POS_SCHEME must be 0, 1 or 2");
       c->pos_scheme = (int)v;
@@ -722,17 +743,18 @@ int slh_simhash(slh_ctx* c, uint32_t* codes_out) {
   if (c->stage < 2) return fail(c, SLH_ESTATE, "slh_simhash before slh_lanczos");
   const int64_t L = window_len(c);
   const int na = c->n_act;
-  ENSURE(c, c->codes, (size_t)c->N * 4);
+  ENSURE(c, c->codes, (size_t)c->Ntot * 4);
   ENSURE(c, c->proj, (size_t)std::max(na, 1) * L * c->bits * 8);
   if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[5], c->stream));
-  if (na != c->n_win) HIP_TRY(c, launch_fill_u32(P<uint32_t>(c->codes), c->N, 0xFFFFFFFFu, c->stream));
+  if (na != c->n_win || c->keep_last)
+    HIP_TRY(c, launch_fill_u32(P<uint32_t>(c->codes), c->Ntot, 0xFFFFFFFFu, c->stream));
   if (na > 0)
     HIP_TRY(c, launch_simhash(P<double>(c->Z), P<double>(c->R),
                               na == c->n_win ? nullptr : P<int>(c->winlist), na, (int)L, c->r,
                               c->bits, P<uint32_t>(c->codes), P<double>(c->proj), c->stream));
   if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[6], c->stream));
   if (codes_out)
-    HIP_TRY(c, hipMemcpyAsync(codes_out, c->codes.p, (size_t)c->N * 4, hipMemcpyDeviceToDevice,
+    HIP_TRY(c, hipMemcpyAsync(codes_out, c->codes.p, (size_t)c->Ntot * 4, hipMemcpyDeviceToDevice,
                               c->stream));
   c->stage = 3;
   c->merged = 0;
@@ -816,11 +838,14 @@ int slh_merge(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, float* emb_
   if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[7], c->stream));
   HIP_TRY(c, launch_merge(w, X, dtype == SLH_BF16 ? 0 : 1, ldx, emb_out, pos_out, tok2macro_out,
                           c->stream));
+  HIP_TRY(c, launch_merge_tail(X, dtype == SLH_BF16 ? 0 : 1, ldx, (int)c->D, N, (int)c->keep_last,
+                               P<int>(c->Mtot), c->compact, emb_out, pos_out, tok2macro_out,
+                               c->stream));
   if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[8], c->stream));
   int M = 0;
   HIP_TRY(c, hipMemcpyAsync(&M, c->Mtot.p, 4, hipMemcpyDeviceToHost, c->stream));
   HIP_TRY(c, hipStreamSynchronize(c->stream));
-  *M_out = M;
+  *M_out = M + c->keep_last;
   c->merged = 1;
   return SLH_OK;
 }
@@ -936,7 +961,7 @@ int slh_load(slh_ctx* c, int32_t which, const void* src, int64_t bytes) {
     return SLH_OK;
   }
   if (which == SLH_OUT_CODES) {
-    const int64_t want = c->N * 4;
+    const int64_t want = c->Ntot * 4;
     if (bytes != want) return fail(c, SLH_EINVAL, "bytes must be %lld", (long long)want);
     ENSURE(c, c->codes, (size_t)want);
     HIP_TRY(c, hipMemcpyAsync(c->codes.p, src, (size_t)want, hipMemcpyDeviceToDevice, c->stream));
@@ -959,7 +984,7 @@ int slh_copy_out(slh_ctx* c, int32_t which, void* dst, int64_t bytes) {
     case SLH_OUT_BETA: b = &c->beta; want = na * c->n_it * 8; break;
     case SLH_OUT_Z: b = &c->Z; want = na * L * c->r * 8; break;
     case SLH_OUT_PROJ: b = &c->proj; want = na * L * c->bits * 8; break;
-    case SLH_OUT_CODES: b = &c->codes; want = c->N * 4; break;
+    case SLH_OUT_CODES: b = &c->codes; want = c->Ntot * 4; break;
     case SLH_OUT_THETA: b = &c->theta; want = na * c->r * 8; break;
     case SLH_OUT_Q: b = &c->Q; want = na * (c->n_it + 1) * L * 8; break;
     case SLH_OUT_ROWSUM: b = &c->rowsum; want = na * L * 8; break;

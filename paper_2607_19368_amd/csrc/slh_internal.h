@@ -124,6 +124,10 @@ struct MergeWS {
   long long* pre;               // [N] scheme != 0: prefix sums of member positions
 };
 int merge_nchunks(int64_t N, int CH);
+// preserved suffix: tail tokens N .. N + K - 1 become macro-tokens *Mtot .. *Mtot + K - 1
+hipError_t launch_merge_tail(const void* X, int dtype, int64_t ldx, int D, int64_t N, int K,
+                             const int* Mtot, int compact, float* E, int* P, int* tok2macro,
+                             hipStream_t s);
 hipError_t launch_merge(const MergeWS& w, const void* X, int dtype, int64_t ldx,
                         float* E, int* P, int* tok2macro, hipStream_t s);
 

@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(_HERE, "libslh.so")
 SLH_OK, SLH_EINVAL, SLH_ENOMEM, SLH_EHIP, SLH_ESTATE = 0, -1, -2, -3, -4
 SLH_BF16, SLH_F32 = 0, 1
 SLH_OPT_KERNEL, SLH_OPT_WINDOW_LEN, SLH_OPT_POS_MODE, SLH_OPT_BREAKDOWN_TOL, SLH_OPT_TIMING = 1, 2, 3, 4, 5
-SLH_OPT_SHORT_WINDOWS, SLH_OPT_NORMALIZE, SLH_OPT_POS_SCHEME = 6, 7, 8
+SLH_OPT_SHORT_WINDOWS, SLH_OPT_NORMALIZE, SLH_OPT_POS_SCHEME, SLH_OPT_KEEP_LAST = 6, 7, 8, 9
 SLH_OUT_PHI, SLH_OUT_ALPHA, SLH_OUT_BETA, SLH_OUT_Z = 1, 2, 3, 4
 SLH_OUT_PROJ, SLH_OUT_CODES, SLH_OUT_THETA, SLH_OUT_Q, SLH_OUT_WINDOWS = 5, 6, 7, 8, 9
 SLH_OUT_ROWSUM = 10
@@ -107,6 +107,7 @@ class Ctx:
         self.handle = handle
         self.N, self.D, self.m, self.r, self.bits = N, D, m, r, bits
         self.n_it = 0
+        self.keep_last = 0          # preserved suffix (tokens N - keep_last .. N - 1)
 
     def __del__(self):
         if getattr(self, "handle", None) and _lib is not None:
@@ -123,7 +124,7 @@ class Ctx:
 
     @property
     def window_len(self):
-        return self.N // self.n_windows
+        return (self.N - self.keep_last) // self.n_windows
 
 
 # ---------------------------------------------------------------- host-only calls
@@ -159,6 +160,8 @@ def slh_create(N, D, m, r, bits, seed=0):
 
 def slh_set_option(ctx, key, value):
     _check(ctx, load().slh_set_option(ctx.handle, key, float(value)), "slh_set_option")
+    if key == SLH_OPT_KEEP_LAST:
+        ctx.keep_last = int(value)
 
 
 def slh_set_stream(ctx, stream=None):

@@ -62,7 +62,7 @@ class Run:
 
 def run_gpu(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel=0, compact=False,
             phi_from=None, codes_from=None, want_phi=False, X=None, short_windows=None,
-            normalise=False, scheme=0):
+            normalise=False, scheme=0, keep_last=None):
     """phi_from: host float32 array (n_act*L, m) loaded instead of computing Phi;
     codes_from: host uint32 (N,) loaded instead of computing codes;
     short_windows: value of SLH_OPT_SHORT_WINDOWS (None keeps the default)."""
@@ -71,6 +71,9 @@ def run_gpu(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel=0, compact=F
     from paper_2607_19368_amd import slh as B
     wl = inp.workload
     ctx = P.slh_create(wl.N, wl.D, wl.m, wl.r, wl.bits, seed)
+    K = wl.keep_last if keep_last is None else keep_last
+    if K:
+        P.slh_set_option(ctx, B.SLH_OPT_KEEP_LAST, K)
     if window:
         P.slh_set_option(ctx, B.SLH_OPT_WINDOW_LEN, window)
     if kernel:
@@ -121,9 +124,11 @@ def run_gpu(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel=0, compact=F
 
 
 def run_oracle(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel="softmax", compact=False,
-               phi_rows=None, normalise=False, scheme="max"):
+               phi_rows=None, normalise=False, scheme="max", keep_last=None):
     wl = inp.workload
-    N = wl.N
+    Ntot = wl.N
+    K = wl.keep_last if keep_last is None else keep_last
+    N = Ntot - K                     # compressed tokens; the last K are preserved
     L = window or N
     W = OP.projection(seed, wl.D, wl.m)
     psi = OP.phases(seed, wl.m)
@@ -175,6 +180,9 @@ def run_oracle(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel="softmax"
     if compact:
         run.P = np.arange(len(run.P))
     run.t2m = t2m
+    if K:
+        run.E, run.P, run.t2m = O.preserve_suffix(run.E, run.P, run.t2m,
+                                                  inp.x_float(slice(N, Ntot)), N, compact)
     if rho is not None:
         run.scores = np.array(scores)
         run.route = np.array(route, dtype=np.uint8)
@@ -343,8 +351,8 @@ def compare(o, g, L, check_spectral=True, ritz_rel=RITZ_REL, angle=ANGLE, emb_re
     else:
         assert np.all(np.diff(g.P) > 0)
     for k, mm in enumerate(members_g):
-        if g.P[k] == k and not (min(mm) <= k <= max(mm)):
-            continue                                   # compact positions
+        if g.P[k] == k:
+            continue                                   # compact positions (or coincidence)
         if scheme == "max":
             assert g.P[k] == max(mm)
         elif scheme == "median":

@@ -340,7 +340,7 @@ def test_end_to_end_local16():
     space, which the method leaves arbitrary when it is 2-dimensional or more.
     Such windows' SimHash bits are not determined, and the oracle's own
     reversed-order evaluation (parity.oracle_uncertainty) marks them."""
-    inp = make_inputs("local16", N=1024)
+    inp = make_inputs("local16", N=1036)
     wl = inp.workload
     _say(f"[e2e] local16 N={wl.N} window={wl.window} n_it={wl.n_it} r={wl.r} bits={wl.bits}")
     g = PR.run_gpu(inp, n_it=wl.n_it, window=wl.window)
@@ -391,7 +391,7 @@ def test_normalised_operator(case):
     the short-window kernel (local16) and the general windowed path
     (windows256) both run on the scaled rows."""
     if case == "local16":
-        inp, L = make_inputs("local16", N=1024), 16
+        inp, L = make_inputs("local16", N=1036), 16
     elif case == "windows256":
         inp, L = _custom("nwin", 4 * 256, 512, 256, 24, 8, 8), 256
     else:
@@ -426,9 +426,11 @@ def test_spectral_energy(case):
     elif case == "windows256":
         inp, L = _custom("ewin", 4 * 256, 512, 256, 24, 8, 8), 256
     else:
-        inp, L, norm = make_inputs("local16", N=512), 16, True
+        inp, L, norm = make_inputs("local16", N=524), 16, True
     wl = inp.workload
     ctx = P.slh_create(wl.N, wl.D, wl.m, wl.r, wl.bits, 0)
+    if wl.keep_last:
+        P.slh_set_option(ctx, B.SLH_OPT_KEEP_LAST, wl.keep_last)
     if L:
         P.slh_set_option(ctx, B.SLH_OPT_WINDOW_LEN, L)
     if norm:
@@ -440,7 +442,7 @@ def test_spectral_energy(case):
     Lw = L or wl.N
     W, psi = OP.projection(0, wl.D, wl.m), OP.phases(0, wl.m)
     eo = []
-    for w in range(wl.N // Lw):
+    for w in range((wl.N - wl.keep_last) // Lw):
         Phi = O.feature_map(inp.x_float(slice(w * Lw, (w + 1) * Lw)), W, psi)
         if norm:
             Phi, _ = O.normalised_features(Phi)
@@ -569,3 +571,31 @@ def test_bucket_purity(case):
         near += lo - hi
     _say(f"[purity] {case}: gpu {sim}/{tot} oracle {osim}/{otot} near-threshold {near}")
     assert tot == otot and abs(sim - osim) <= near
+
+
+@pytest.mark.parametrize("case", ["tiny_keep5", "local16_keep12", "compact_keep3"])
+def test_preserved_suffix(case):
+    """SLH_OPT_KEEP_LAST: the last K tokens are not compressed and follow the
+    compressed macro-tokens as their own rows at their own positions (reading
+    R19); compression runs on the first N - K tokens (windows tile them)."""
+    compact = False
+    if case == "tiny_keep5":
+        inp, L, K = make_inputs("tiny"), 0, 5
+        inp = Inputs(Workload("tk5", 517, 256, 256, 32, 8, 6, 4.0, 0, 0, "f32"),
+                     np.concatenate([inp.X, inp.X[:5] * 2.0]), np.zeros(517))
+    elif case == "local16_keep12":
+        inp, L, K = make_inputs("local16", N=1036), 16, 12
+    else:
+        inp, L, K, compact = _custom("ck3", 4 * 256 + 3, 256, 256, 16, 8, 8), 256, 3, True
+    wl = inp.workload
+    _say(f"[keep last] {case} N={wl.N} K={K} window={L}")
+    g = PR.run_gpu(inp, n_it=wl.n_it, window=L, keep_last=K, compact=compact)
+    o = PR.run_oracle(inp, n_it=wl.n_it, window=L, keep_last=K, compact=compact)
+    Nc = wl.N - K
+    M = len(o.P)
+    assert len(g.P) == M and np.array_equal(g.P[M - K:], o.P[M - K:])
+    assert np.array_equal(g.t2m[Nc:], o.t2m[Nc:])
+    assert np.array_equal(g.E[M - K:], o.E[M - K:].astype(np.float32))
+    unc = {w.w: PR.oracle_uncertainty(inp, w.w, L, wl.n_it) for w in o.windows} if L == 16 else None
+    rep = PR.compare(o, g, L or Nc, unc=unc)
+    _say(f"   {rep}  M={M}")

@@ -16,7 +16,8 @@ the same shapes:
                 windows repeat a Zipf template of period U{16..64} with 10% of
                 positions replaced by fresh Zipf draws (JSON/code/table-like
                 redundancy), odd windows are i.i.d. Zipf(1.1).
-  local16       the qwen7b prompt cut into 512 windows of 16 tokens (local backend).
+  local16       an 8204-token prompt (same recipe as qwen7b): 512 windows of 16 tokens
+                (local backend) and the last 12 tokens preserved.
   qwen7b_normalised  the qwen7b prompt, run on the row-normalised operator.
 
 Table rows are generated per id on demand (row id -> its own seeded stream), so
@@ -43,6 +44,7 @@ class Workload:
     x_dtype: str = "bf16"
     adaptive: bool = False   # windows alternate periodic / i.i.d. streams and are routed
     normalise: bool = False  # run on the row-normalised operator
+    keep_last: int = 0       # preserved suffix: the last keep_last tokens are not compressed
 
 
 WORKLOADS = {
@@ -53,8 +55,9 @@ WORKLOADS = {
     "adaptive64": Workload("adaptive64", 64 * 2048, 4096, 1024, 48, 32, 10, 8.0, 32768, 2048,
                            "bf16", True),
     # local backend at the paper's defaults (section 5.1): windows of 16 tokens,
-    # 256 random features, a full 16-step Krylov space, b = ceil(log2(16 / rho))
-    "local16": Workload("local16", 8192, 3584, 256, 16, 16, 2, 4.0, 152064, 16),
+    # 256 random features, a full 16-step Krylov space, b = ceil(log2(16 / rho)),
+    # the last 12 tokens preserved (a prompt of 8204 = 512 x 16 + 12 tokens)
+    "local16": Workload("local16", 8204, 3584, 256, 16, 16, 2, 4.0, 152064, 16, keep_last=12),
     # the qwen7b prompt on the row-normalised operator (section 3.2 remark)
     "qwen7b_normalised": Workload("qwen7b_normalised", 8192, 3584, 2048, 96, 64, 12, 16.0, 152064,
                                   normalise=True),
