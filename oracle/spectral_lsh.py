@@ -52,6 +52,11 @@ Readings of the paper that this file takes (where it is silent or ambiguous):
   R19 (section 3.5, section 5.1) A preserved suffix of K tokens is not part of
      any window or bucket: compression runs on the first N - K tokens and the
      K tail tokens follow as singleton macro-tokens at their own positions.
+  R20 (section 3.3 adjustment to the target length; no algorithm given, parity
+     unpinned) See adjust_to_target: per spectral window, budget
+     floor(B / n) (+1 for the first B mod n windows) of B target macro-tokens;
+     merges join runs of consecutive macro-tokens, splits cut groups into
+     contiguous member runs apportioned by size.
   R16 (section 3.2 remark on row normalisation; appendix, softmax normalisation
      gap) The normalised variant estimates the row sums s = Phi (Phi^T 1) and
      uses diag(s)^-1 Phi Phi^T.  That operator is not symmetric; it is similar to
@@ -359,6 +364,71 @@ def route_window(L, score, rho, tau=None):
         return False
     t = tau_of_rho(rho) if tau is None else tau
     return score >= t
+
+
+def adjust_to_target(groups, T):
+    """Exact target length (section 3.3: an adjustment step merges or splits
+    clusters until their number matches the target; the paper gives no
+    algorithm, reading R20, parity unpinned).  groups: member index arrays
+    (ascending) in macro order (ascending position).  Returns T groups in the
+    same form.
+
+    Merge (more groups than T): group k joins new group floor(k T / M), so runs
+    of consecutive groups in position order are merged into T near-equal runs.
+    Split (fewer): E = T - M extra pieces are apportioned to the groups in
+    proportion to s_k - 1 (the cuts a group of s_k members admits): floor of the
+    quota, then one more for the E - sum largest remainders (ties: earlier
+    group); a group of s members in n pieces is cut, in member order, into
+    pieces of ceil(s/n) (the first s mod n) and floor(s/n) members; pieces are
+    ordered by their last member."""
+    M = len(groups)
+    if T < 1 or T > sum(len(g) for g in groups):
+        raise ValueError("target out of range")
+    if M == T:
+        return [np.asarray(g) for g in groups]
+    if M > T:
+        out = [[] for _ in range(T)]
+        for k, g in enumerate(groups):
+            out[k * T // M].extend(int(v) for v in g)
+        return [np.array(sorted(g), dtype=np.int64) for g in out]
+    sizes = [len(g) for g in groups]
+    E, den = T - M, sum(sizes) - M
+    extra = [E * (s - 1) // den for s in sizes]
+    rem = [E * (s - 1) % den for s in sizes]
+    R = E - sum(extra)
+    order = sorted(range(M), key=lambda k: (-rem[k], k))
+    for k in order[:R]:
+        extra[k] += 1
+    pieces = []
+    for g, e in zip(groups, extra):
+        g = np.asarray(g, dtype=np.int64)
+        n, s_ = e + 1, len(g)
+        q, rr = divmod(s_, n)
+        cut = 0
+        for j in range(n):
+            sz = q + 1 if j < rr else q
+            pieces.append(g[cut:cut + sz])
+            cut += sz
+    pieces.sort(key=lambda p: int(p[-1]))
+    return pieces
+
+
+def merge_groups(X, groups, positions=None, compact=False):
+    """Eq. 7 and max positions for given member groups (in macro order)."""
+    X = np.asarray(X)
+    N = X.shape[0]
+    pos = np.arange(N, dtype=np.int64) if positions is None else np.asarray(positions, np.int64)
+    M = len(groups)
+    E = np.zeros((M, X.shape[1]))
+    P = np.zeros(M, dtype=np.int64)
+    t2m = np.full(N, -1, dtype=np.int64)
+    for k, g in enumerate(groups):
+        E[k] = renormalised_mean(X[g].astype(np.float64))
+        P[k] = int(pos[g].max())
+        t2m[g] = k
+    if compact:
+        P = np.arange(M, dtype=np.int64)
+    return E, P, t2m
 
 
 def preserve_suffix(E, P, tok2macro, X_tail, pos0, compact=False):

@@ -417,6 +417,46 @@ def test_preserve_suffix_hand_example():
     assert list(Pc) == [0, 1, 2, 3]
 
 
+def test_adjust_to_target_hand_and_invariants():
+    """Reading R20 (parity unpinned: the paper gives no algorithm).  Hand
+    examples of both directions, then invariants on random groupings: exactly
+    T groups, a partition of the members, ascending last members, merges join
+    runs of consecutive groups, splits are contiguous member runs."""
+    g = [np.array([0, 4]), np.array([1, 2, 5]), np.array([3, 6]), np.array([7])]
+    # merge 4 -> 2: groups 0,1 -> new 0; groups 2,3 -> new 1
+    m = O.adjust_to_target(g, 2)
+    assert [list(x) for x in m] == [[0, 1, 2, 4, 5], [3, 6, 7]]
+    # split 4 -> 6: E = 2, sizes 2 3 2 1, s-1 = 1 2 1 0, den = 8 - 4 = 4:
+    # quotas 2*1/4, 2*2/4 = 1, 2*1/4, 0 -> extra 0 1 0 0, remainders 2 0 2 0 ->
+    # R = 1 extra piece to group 0 (largest remainder, earliest)
+    sp = O.adjust_to_target(g, 6)
+    assert [list(x) for x in sp] == [[0], [1, 2], [4], [5], [3, 6], [7]]
+    assert [list(x) for x in O.adjust_to_target(g, 4)] == [list(x) for x in g]
+    rng = np.random.default_rng(13)
+    for trial in range(30):
+        N = int(rng.integers(20, 200))
+        codes = rng.integers(0, int(rng.integers(2, 40)), N)
+        mg = O.merge(np.zeros((N, 1)), codes)
+        M = len(mg.members)
+        for T in sorted({1, M, max(1, M // 3), min(N, 2 * M + 3), N}):
+            out = O.adjust_to_target(mg.members, T)
+            assert len(out) == T
+            assert np.array_equal(np.sort(np.concatenate(out)), np.arange(N))
+            last = [int(x[-1]) for x in out]
+            assert last == sorted(last)
+            if T < M:
+                for gg in out:   # a merged group is a union of consecutive groups
+                    ks = sorted({int(mg.tok2macro[v]) for v in gg})
+                    assert ks == list(range(ks[0], ks[-1] + 1))
+            if T > M:
+                for gg in out:   # a piece lies inside one group, as a contiguous run
+                    k = {int(mg.tok2macro[v]) for v in gg}
+                    assert len(k) == 1
+                    mem = list(mg.members[k.pop()])
+                    i0 = mem.index(int(gg[0]))
+                    assert mem[i0:i0 + len(gg)] == list(gg)
+
+
 def test_merge_invariants():
     rng = np.random.default_rng(3)
     N, D = 700, 5
