@@ -119,6 +119,8 @@ def main():
         P.slh_set_option(ctx, B.SLH_OPT_WINDOW_LEN, wl.window)
     if wl.normalise:
         P.slh_set_option(ctx, B.SLH_OPT_NORMALIZE, 1)
+    if wl.target:
+        P.slh_set_option(ctx, B.SLH_OPT_TARGET_LEN, wl.target)
     tau = -1.0
     if wl.adaptive:
         # routing threshold: midpoint of the 32nd and 33rd largest window scores
@@ -126,6 +128,9 @@ def main():
         s = np.sort(sc)[::-1]
         tau = 0.5 * (s[31] + s[32])
     cap = P.slh_merge_capacity(ctx) if not wl.window else wl.N
+    if wl.adaptive and wl.target:
+        P.slh_route(ctx, X, wl.rho, tau)           # budgets follow this routing
+        cap = max(cap, P.slh_merge_capacity(ctx))
     E = torch.empty((cap, wl.D), dtype=torch.float32, device="cuda")
     Pp = torch.empty(cap, dtype=torch.int32, device="cuda")
     T2M = torch.empty(wl.N, dtype=torch.int32, device="cuda")
@@ -178,7 +183,8 @@ def main():
             "workload": f"{wl.name}: N={wl.N} D={wl.D} m={wl.m} n_it={wl.n_it} r={wl.r} "
                         f"bits={wl.bits} rho={wl.rho:g}" + (f" window={wl.window}" if wl.window else "")
                         + (" operator=row-normalised" if wl.normalise else "")
-                        + (f" keep_last={wl.keep_last}" if wl.keep_last else ""),
+                        + (f" keep_last={wl.keep_last}" if wl.keep_last else "")
+                        + (f" target={wl.target}" if wl.target else ""),
             "inputs": "Zipf(1.1) token ids over a seeded N(0,0.02) bf16 embedding table"
                       if wl.x_dtype == "bf16" else "seeded Gaussian mixture, fp32",
             "precision": "bf16 MFMA feature map with fp32 accumulation, fp32 Phi, fp64 Lanczos/"

@@ -94,6 +94,19 @@ typedef struct slh_ctx slh_ctx;
                                     outputs cover those tokens only; codes, the
                                     token map and X keep N rows (tail codes are
                                     0xFFFFFFFF).  0 (default) keeps none          */
+#define SLH_OPT_TARGET_LEN    10 /* exact output length T (section 3.3: clusters are
+                                    merged or split until their number matches the
+                                    target; no algorithm is given, this library's
+                                    reading): the spectral windows share
+                                    B = T - chunk macro-tokens - KEEP_LAST as
+                                    floor(B/n) (+1 for the first B mod n); a window
+                                    with more buckets merges runs of consecutive
+                                    macro-tokens (macro k -> floor(k T_w / M_w)),
+                                    one with fewer cuts buckets into contiguous
+                                    member runs apportioned by size (largest
+                                    remainder).  Needs POS_SCHEME 0; slh_merge
+                                    fails with SLH_EINVAL when a budget leaves
+                                    [1, L].  0 (default): off                       */
 #define SLH_OPT_SHORT_WINDOWS 6  /* 1 (default): windows of L <= 32 tokens run Lanczos,
                                     Eigh and Ritz in one wavefront per window on the
                                     explicit L x L operator Phi_w Phi_w^T (the same

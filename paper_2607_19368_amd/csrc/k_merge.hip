@@ -415,6 +415,156 @@ __global__ __launch_bounds__(1024) void k_mg_rerank(MergeWS w, int scheme, int* 
   for (int s = tid; s < L; s += 1024) w.sloc[base + s] = rk[base + st[base + s]];
 }
 
+// Exact target length (section 3.3: clusters are merged or split until their
+// number matches the target; the paper gives no algorithm, so this follows one
+// fixed reading).  Window budget T = w.tw[win] (> 0 for spectral windows); one
+// block per window, after the book-keeping (sval: members by code, then token;
+// sloc: macro rank by max position; mw: count M).
+//   M > T: macro k joins new macro floor(k T / M) (runs of consecutive
+//          macro-tokens in position order); members are regrouped, buckets in
+//          rank order, so each new macro is a contiguous run ending with its
+//          max-position member.
+//   M < T: E = T - M extra pieces are apportioned in proportion to s_k - 1:
+//          floor(E (s_k - 1) / (L - M)) each, then one more for the largest
+//          remainders (ties: smaller k; ranked by direct counting); bucket k is
+//          cut into n_k contiguous pieces of its member run (the first s mod n
+//          of ceil(s / n) members), and pieces are ranked by their last member
+//          with a scan over the window's tokens.
+// Scratch (window slices of N-entry arrays): st run start per sorted position,
+// rsz / rof size and start of rank k's run, t0 / t1 / fl int work arrays, rem
+// int64 remainders.
+__global__ __launch_bounds__(1024) void k_mg_target(MergeWS w, int* __restrict__ st,
+                                                    int* __restrict__ rsz, int* __restrict__ rof,
+                                                    int* __restrict__ t0, int* __restrict__ t1,
+                                                    int* __restrict__ fl, long long* __restrict__ rem) {
+  const int win = blockIdx.x, tid = threadIdx.x;
+  const int L = w.L;
+  const int64_t base = (int64_t)win * L;
+  if (!w.route[win]) return;
+  const int T = w.tw[win], M = w.mw[win];
+  if (T <= 0 || T == M) return;
+  __shared__ int wsum[16];
+  __shared__ int sR;
+  // run starts: max-scan of the start indices in sorted order
+  int carry = INT_MIN;
+  for (int b0 = 0; b0 < L; b0 += 1024) {
+    const int s = b0 + tid;
+    int v = INT_MIN;
+    if (s < L) v = (s == 0 || w.sloc[base + s] != w.sloc[base + s - 1]) ? s : INT_MIN;
+    int tot;
+    const int inc = block_incl_max_1024(v, wsum, tot);
+    if (s < L) st[base + s] = max(inc, carry);
+    carry = max(carry, tot);
+    __syncthreads();
+  }
+  __threadfence();
+  __syncthreads();
+  for (int e = tid; e < L; e += 1024)
+    if (e == L - 1 || w.sloc[base + e + 1] != w.sloc[base + e]) {
+      const int k = w.sloc[base + e];
+      rsz[base + k] = e - st[base + e] + 1;
+      rof[base + k] = st[base + e];
+    }
+  __threadfence();
+  __syncthreads();
+  if (M > T) {
+    // exclusive prefix of the run sizes over ranks: new sorted position of each
+    // bucket's first member
+    int c2 = 0;
+    for (int b0 = 0; b0 < M; b0 += 1024) {
+      const int k = b0 + tid;
+      const int v = (k < M) ? rsz[base + k] : 0;
+      int tot;
+      const int inc = block_incl_scan_1024(v, wsum, tot);
+      if (k < M) t0[base + k] = c2 + inc - v;
+      c2 += tot;
+      __syncthreads();
+    }
+    __threadfence();
+    __syncthreads();
+    for (int s = tid; s < L; s += 1024) {
+      const int k = w.sloc[base + s];
+      const int dest = t0[base + k] + (s - st[base + s]);
+      t1[base + dest] = w.sval[base + s];
+      fl[base + dest] = (int)((long long)k * T / M);
+    }
+    __threadfence();
+    __syncthreads();
+    for (int s = tid; s < L; s += 1024) {
+      w.sval[base + s] = t1[base + s];
+      w.sloc[base + s] = fl[base + s];
+    }
+  } else {
+    const int E = T - M;
+    const long long den = (long long)L - M;      // > 0: a window with M = L has T <= L = M
+    int part = 0;
+    for (int k = tid; k < M; k += 1024) {
+      const long long num = (long long)E * (rsz[base + k] - 1);
+      t0[base + k] = (int)(num / den);
+      rem[base + k] = num % den;
+      part += (int)(num / den);
+    }
+    int tot;
+    (void)block_incl_scan_1024(part, wsum, tot);
+    if (tid == 0) sR = E - tot;
+    __threadfence();
+    __syncthreads();
+    const int R = sR;
+    // pieces per bucket: one more for the R largest remainders (ties: smaller k)
+    for (int k = tid; k < M; k += 1024) {
+      const long long rk = rem[base + k];
+      int ahead = 0;
+      if (R > 0)
+        for (int q = 0; q < M; ++q) {
+          const long long rq = rem[base + q];
+          ahead += (rq > rk) || (rq == rk && q < k);
+        }
+      // at most one piece per member (guaranteed by the apportionment; kept as a bound)
+      t1[base + k] = min(rsz[base + k], 1 + t0[base + k] + ((R > 0 && ahead < R) ? 1 : 0));
+    }
+    for (int t = tid; t < L; t += 1024) fl[base + t] = 0;
+    __threadfence();
+    __syncthreads();
+    // flag each piece's last member (by token)
+    for (int s = tid; s < L; s += 1024) {
+      const int k = w.sloc[base + s];
+      const int sz = rsz[base + k], n = t1[base + k];
+      const int q = sz / n, rr = sz % n, o = s - st[base + s];
+      const int j = (o < rr * (q + 1)) ? o / (q + 1) : rr + (o - rr * (q + 1)) / q;
+      const int last = (j < rr) ? (j + 1) * (q + 1) - 1 : rr * (q + 1) + (j - rr + 1) * q - 1;
+      if (o == last) fl[w.sval[base + s]] = 1;
+    }
+    __threadfence();
+    __syncthreads();
+    // rank of each piece = pieces whose last member precedes its own
+    int c3 = 0;
+    for (int b0 = 0; b0 < L; b0 += 1024) {
+      const int t = b0 + tid;
+      const int v = (t < L) ? fl[base + t] : 0;
+      int tt;
+      const int inc = block_incl_scan_1024(v, wsum, tt);
+      if (t < L) t0[base + t] = c3 + inc - v;
+      c3 += tt;
+      __syncthreads();
+    }
+    __threadfence();
+    __syncthreads();
+    for (int s = tid; s < L; s += 1024) {
+      const int k = w.sloc[base + s];
+      const int sz = rsz[base + k], n = t1[base + k];
+      const int q = sz / n, rr = sz % n, o = s - st[base + s];
+      const int j = (o < rr * (q + 1)) ? o / (q + 1) : rr + (o - rr * (q + 1)) / q;
+      const int last = (j < rr) ? (j + 1) * (q + 1) - 1 : rr * (q + 1) + (j - rr + 1) * q - 1;
+      const int ltok = w.sval[base + rof[base + k] + last];
+      fl[base + s] = t0[ltok];
+    }
+    __threadfence();
+    __syncthreads();
+    for (int s = tid; s < L; s += 1024) w.sloc[base + s] = fl[base + s];
+  }
+  if (tid == 0) w.mw[win] = T;
+}
+
 __global__ __launch_bounds__(1024) void k_mg_wbase(MergeWS w) {
   __shared__ int wsum[16];
   int carry = 0;
@@ -796,6 +946,9 @@ hipError_t launch_merge(const MergeWS& w, const void* X, int dtype, int64_t ldx,
   } else {
     hipLaunchKernelGGL(k_mg_book, dim3(w.n_win), dim3(1024), 0, s, w);
   }
+  if (w.tw)
+    hipLaunchKernelGGL(k_mg_target, dim3(w.n_win), dim3(1024), 0, s, w, w.valA, w.segid, w.segk,
+                       (int*)w.keyA, (int*)w.keyB, w.tg, w.pre);
   if (w.scheme != 0)
     hipLaunchKernelGGL(k_mg_rerank, dim3(w.n_win), dim3(1024), 0, s, w, w.scheme, w.posv, w.valA,
                        w.pre, w.tmpi, w.segid, w.segk, w.valB);

@@ -127,6 +127,9 @@ struct slh_ctx {
   int merged = 0;                   // slh_merge ran on the current codes
   int64_t Ntot = 0;                 // prompt length; N = Ntot - keep_last tokens are compressed
   int64_t keep_last = 0;            // SLH_OPT_KEEP_LAST
+  int64_t target_len = 0;           // SLH_OPT_TARGET_LEN (0 = off)
+  std::vector<int> tw_h;            // per-window budgets of the last merge
+  DevBuf tg_tw, tg_scr;
   DevBuf dg_tiles, dg_counts;
   DevBuf posv, mg_pre;
   DevBuf nm_part, nm_csum, rowsum;
@@ -273,12 +276,35 @@ void route_all_spectral(slh_ctx* c) {
   c->routing_on_device = false;
 }
 
+// Exact target length: the spectral windows share B = target - (chunk-window
+// macro-tokens) - (preserved tokens), floor(B / n) each and one more for the
+// first B mod n (window order).  Returns false if some budget would leave [1, L].
+bool target_budgets(const slh_ctx* c, std::vector<int>& tw) {
+  const int64_t L = window_len(c);
+  tw.assign((size_t)c->n_win, 0);
+  int64_t chunk = 0, ns = 0;
+  for (int64_t w = 0; w < c->n_win; ++w) {
+    if (c->route_h[(size_t)w]) ++ns;
+    else chunk += (L + c->chunk_k - 1) / c->chunk_k;
+  }
+  const int64_t B = c->target_len - chunk - c->keep_last;
+  if (ns == 0) return B == 0;
+  if (B < ns || B > ns * L) return false;
+  int64_t a = 0;
+  for (int64_t w = 0; w < c->n_win; ++w)
+    if (c->route_h[(size_t)w]) tw[(size_t)w] = (int)(B / ns + (a++ < B % ns ? 1 : 0));
+  return true;
+}
+
 int64_t capacity(const slh_ctx* c) {
   const int64_t L = window_len(c);
   const int64_t per_spec = std::min<int64_t>(L, (int64_t)1 << c->bits);
+  std::vector<int> tw;
+  const bool tg = c->target_len > 0 && target_budgets(c, tw);
   int64_t cap = 0;
   for (int64_t w = 0; w < c->n_win; ++w)
-    cap += c->route_h[(size_t)w] ? per_spec : (L + c->chunk_k - 1) / c->chunk_k;
+    cap += c->route_h[(size_t)w] ? std::max<int64_t>(per_spec, tg ? tw[(size_t)w] : 0)
+                                 : (L + c->chunk_k - 1) / c->chunk_k;
   return cap + c->keep_last;
 }
 
@@ -462,6 +488,13 @@ int slh_set_option(slh_ctx* c, int32_t key, double v) {
       route_all_spectral(c);
       c->routed = false;
       drop_graph(c);
+      break;
+    }
+    case SLH_OPT_TARGET_LEN: {
+      const int64_t T = (int64_t)v;
+      if ((double)T != v || T < 0 || T > c->Ntot)
+        return fail(c, SLH_EINVAL, "TARGET_LEN must be an integer in [0, N]");
+      c->target_len = T;
       break;
     }
     case SLH_OPT_POS_SCHEME:
@@ -829,6 +862,22 @@ int slh_merge(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, float* emb_
   w.scheme = c->pos_scheme;
   w.posv = nullptr;
   w.pre = nullptr;
+  w.tw = nullptr;
+  w.tg = nullptr;
+  if (c->target_len > 0) {
+    if (c->pos_scheme) return fail(c, SLH_EINVAL, "TARGET_LEN needs max positions (POS_SCHEME 0)");
+    if (!target_budgets(c, c->tw_h))
+      return fail(c, SLH_EINVAL, "TARGET_LEN %lld is not reachable with this routing",
+                  (long long)c->target_len);
+    ENSURE(c, c->tg_tw, (size_t)c->n_win * 4);
+    ENSURE(c, c->tg_scr, (size_t)N * 4);
+    ENSURE(c, c->mg_pre, (size_t)N * 8);
+    HIP_TRY(c, hipMemcpyAsync(c->tg_tw.p, c->tw_h.data(), (size_t)c->n_win * 4,
+                              hipMemcpyHostToDevice, c->stream));
+    w.tw = P<int>(c->tg_tw);
+    w.tg = P<int>(c->tg_scr);
+    w.pre = P<long long>(c->mg_pre);
+  }
   if (w.scheme) {
     ENSURE(c, c->posv, (size_t)N * 4);
     ENSURE(c, c->mg_pre, (size_t)N * 8);

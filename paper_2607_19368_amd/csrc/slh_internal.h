@@ -121,7 +121,9 @@ struct MergeWS {
   int CH;                       // sorted positions per reduction chunk (<= 64)
   int scheme;                   // position scheme: 0 max, 1 lower median, 2 mean (half to even)
   int* posv;                    // [N] scheme != 0: representative position at each run end
-  long long* pre;               // [N] scheme != 0: prefix sums of member positions
+  long long* pre;               // [N] scheme != 0 or target: prefix sums / remainders
+  const int* tw;                // [n_win] exact target length: budget per window (NULL = off)
+  int* tg;                      // [N] exact target length: scratch
 };
 int merge_nchunks(int64_t N, int CH);
 // preserved suffix: tail tokens N .. N + K - 1 become macro-tokens *Mtot .. *Mtot + K - 1

@@ -599,3 +599,92 @@ def test_preserved_suffix(case):
     unc = {w.w: PR.oracle_uncertainty(inp, w.w, L, wl.n_it) for w in o.windows} if L == 16 else None
     rep = PR.compare(o, g, L or Nc, unc=unc)
     _say(f"   {rep}  M={M}")
+
+
+@pytest.mark.parametrize("case,T", [("tiny", 30), ("tiny", 100), ("tiny", 1), ("tiny", 512),
+                                    ("windows", 200), ("windows", 700), ("long", 300),
+                                    ("keep", 90)])
+def test_exact_target_length(case, T):
+    """SLH_OPT_TARGET_LEN (reading R20; the paper gives no algorithm, so the
+    oracle follows the same reading and parity is unpinned): with the oracle's
+    codes loaded, the GPU merge must produce exactly the oracle's adjusted
+    groups (positions and token maps bit-exact, embeddings 1e-5).  tiny: one
+    window of 512 (merge to 30 / 1, split to 100 / 512); windows: 8 windows of
+    256, half routed to chunk pooling; long: one window of 20000 tokens;
+    keep: 512 + 12 preserved tokens."""
+    import torch
+    import paper_2607_19368_amd as P
+    from paper_2607_19368_amd import slh as B
+    rho, L, K = None, 0, 0
+    if case == "tiny":
+        inp = make_inputs("tiny")
+        codes = np.random.default_rng(1).integers(0, 64, inp.workload.N)
+    elif case == "windows":
+        inp, L, rho = _custom("twin", 8 * 256, 256, 256, 16, 8, 8), 256, 8.0
+        codes = np.random.default_rng(2).integers(0, 64, inp.workload.N)
+    elif case == "long":
+        inp = _custom("tlong", 20000, 64, 256, 8, 4, 12)
+        codes = np.minimum(np.random.default_rng(3).zipf(1.3, 20000) - 1, 4095)
+    else:
+        base = make_inputs("tiny")
+        inp = Inputs(Workload("tkeep", 524, 256, 256, 32, 8, 6, 4.0, 0, 0, "f32"),
+                     np.concatenate([base.X, base.X[:12] * 0.5]), np.zeros(524))
+        codes = np.random.default_rng(4).integers(0, 64, 524)
+        K = 12
+    wl = inp.workload
+    Nc = wl.N - K
+    Lw = L or Nc
+    ctx = P.slh_create(wl.N, wl.D, wl.m, wl.r, wl.bits, 0)
+    if K:
+        P.slh_set_option(ctx, B.SLH_OPT_KEEP_LAST, K)
+    if L:
+        P.slh_set_option(ctx, B.SLH_OPT_WINDOW_LEN, L)
+    P.slh_set_option(ctx, B.SLH_OPT_TARGET_LEN, T)
+    Xd = PR.to_device_x(inp)
+    route = np.ones(Nc // Lw, bool)
+    if rho is not None:
+        sc = np.array([O.redundancy_score(inp.x_float(slice(w * Lw, (w + 1) * Lw)))
+                       for w in range(Nc // Lw)])
+        r_gpu, _ = P.slh_route(ctx, Xd, rho, float(np.median(sc)))
+        route = r_gpu.astype(bool)
+    P.slh_load(ctx, B.SLH_OUT_CODES, torch.from_numpy(codes.astype(np.int32)).cuda())
+    E, Pp, t2m, M = P.slh_merge(ctx, Xd)
+    torch.cuda.synchronize()
+    gE, gP, gt = E[:M].cpu().numpy(), Pp[:M].cpu().numpy(), t2m.cpu().numpy()
+    # oracle: budgets, adjusted groups per spectral window, chunk windows, tail
+    n_s = int(route.sum())
+    chunk = sum((Lw + O.chunk_size(rho) - 1) // O.chunk_size(rho) for w in range(Nc // Lw)
+                if not route[w]) if rho else 0
+    Bud = T - chunk - K
+    budgets, a = [], 0
+    for w in range(Nc // Lw):
+        if route[w]:
+            budgets.append(Bud // n_s + (1 if a < Bud % n_s else 0))
+            a += 1
+        else:
+            budgets.append(0)
+    X = inp.x_float()
+    Es, Ps, tms = [], [], np.zeros(wl.N, np.int64)
+    base = 0
+    for w in range(Nc // Lw):
+        sl = slice(w * Lw, (w + 1) * Lw)
+        if route[w]:
+            groups = O.merge(X[sl], codes[sl]).members
+            groups = O.adjust_to_target(groups, budgets[w])
+            Ew, Pw, tw = O.merge_groups(X[sl], groups, positions=w * Lw + np.arange(Lw))
+        else:
+            k = O.chunk_size(rho)
+            Ew, Pw = O.chunk_pool(X[sl], k, pos0=w * Lw)
+            tw = np.arange(Lw) // k
+        Es.append(Ew)
+        Ps.append(Pw)
+        tms[sl] = base + tw
+        base += len(Pw)
+    oE, oP, ot = np.concatenate(Es), np.concatenate(Ps), tms[:Nc]
+    if K:
+        oE, oP, ot = O.preserve_suffix(oE, oP, ot, X[Nc:], Nc)
+    _say(f"[target] {case} T={T}: M gpu {M} oracle {len(oP)}")
+    assert M == T == len(oP)
+    assert np.array_equal(gP, oP) and np.array_equal(gt, ot)
+    rel = np.linalg.norm(gE - oE, axis=1) / np.maximum(np.linalg.norm(oE, axis=1), 1e-30)
+    assert rel.max() <= 1e-5

@@ -19,6 +19,7 @@ the same shapes:
   local16       an 8204-token prompt (same recipe as qwen7b): 512 windows of 16 tokens
                 (local backend) and the last 12 tokens preserved.
   qwen7b_normalised  the qwen7b prompt, run on the row-normalised operator.
+  qwen7b_exact, adaptive64_exact  the same prompts with an exact output length N / rho.
 
 Table rows are generated per id on demand (row id -> its own seeded stream), so
 the 152064-row tables are never materialised.
@@ -45,6 +46,7 @@ class Workload:
     adaptive: bool = False   # windows alternate periodic / i.i.d. streams and are routed
     normalise: bool = False  # run on the row-normalised operator
     keep_last: int = 0       # preserved suffix: the last keep_last tokens are not compressed
+    target: int = 0          # exact output length (0 = whatever the buckets give)
 
 
 WORKLOADS = {
@@ -61,6 +63,12 @@ WORKLOADS = {
     # the qwen7b prompt on the row-normalised operator (section 3.2 remark)
     "qwen7b_normalised": Workload("qwen7b_normalised", 8192, 3584, 2048, 96, 64, 12, 16.0, 152064,
                                   normalise=True),
+    # exact output length N / rho (section 3.3 adjustment): the qwen7b prompt to
+    # 512 macro-tokens; the adaptive batch to 16384 (a budget per window)
+    "qwen7b_exact": Workload("qwen7b_exact", 8192, 3584, 2048, 96, 64, 12, 16.0, 152064,
+                             target=512),
+    "adaptive64_exact": Workload("adaptive64_exact", 64 * 2048, 4096, 1024, 48, 32, 10, 8.0, 32768,
+                                 2048, "bf16", True, target=16384),
 }
 
 
