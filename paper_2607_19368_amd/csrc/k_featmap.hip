@@ -9,14 +9,15 @@
 // waits on memory; 128 x 128 with 2 x 2 waves for small problems); each wave
 // owns (BM/WGM) x (BN/WGN) as 32x32 MFMA tiles.  K advances FM_BK at a time
 // through FM_NS LDS stages filled by direct global-to-LDS loads issued
-// FM_NS - 1 stages ahead of the MFMAs that consume them (no register staging);
-// within a stage the operands of the next k16 step are read while the current
-// step's MFMAs run.  The 16-byte chunks of each LDS row are XOR-swizzled by the
-// row index so that the MFMA operand reads of 16 consecutive rows hit distinct
-// banks (see fm_swz).  Rows beyond n_rows re-read the last row and are not stored; K
-// beyond D is zero-filled in W (D % 8 == 0).  The epilogue stages the accumulators through LDS
-// so the cos/scale work runs on contiguous rows and Phi leaves in 16-byte
-// stores.
+// FM_NS - 1 stages ahead of the MFMAs that consume them (no register staging),
+// spread one behind each MFMA rather than in a burst; the operands of the next
+// k16 step are read while the current step's MFMAs run, and the last step of a
+// stage runs after the stage barrier.  The 16-byte chunks of each LDS row are
+// XOR-swizzled by the row index so that the MFMA operand reads of 16
+// consecutive rows hit distinct banks (see fm_swz).  Rows beyond n_rows re-read
+// the last row and are not stored; K beyond D is zero-filled in W (D % 8 == 0).
+// The epilogue stages the accumulators through LDS so the cos/scale work runs
+// on contiguous rows and Phi leaves in 16-byte streaming stores.
 #include "slh_device.h"
 #include "slh_internal.h"
 
@@ -33,11 +34,11 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 #ifndef FM_NS
 #define FM_NS 2                  // LDS stages (loads run FM_NS - 1 stages ahead)
 #endif
-#ifndef FM_DB
-#define FM_DB 1                  // read the next k16 step's operands during this step's MFMAs
+#ifndef FM_LSPREAD
+#define FM_LSPREAD 1             // k16 steps over which a stage's global->LDS loads are issued
 #endif
-#ifndef FM_IL
-#define FM_IL 1                  // pin an MFMA / LDS-read interleave (with FM_DB)
+#ifndef FM_NT
+#define FM_NT 1                  // stream Phi out with non-temporal stores
 #endif
 #ifndef FM_EPI
 #define FM_EPI 1                 // epilogue staging sync: 0 block barriers, 1 per wave
@@ -79,6 +80,33 @@ __device__ __forceinline__ void fm_wait_vm() {
   else if constexpr (N == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
   else if constexpr (N == 12) asm volatile("s_waitcnt vmcnt(12)" ::: "memory");
   else asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+}
+
+// cos(x) in fp32 for the epilogue, about 1 ulp for |x| up to several thousand:
+// Cody and Waite's reduction x = k pi/2 + r with pi/2 split into three fp32
+// parts (x - k P1 is exact in the fma, so r carries one rounding), then the Taylor
+// series of cos and sin on |r| <= pi/4 truncated after r^10 and r^9 (remainders
+// below 2e-9), and the quadrant k mod 4 selecting +-cos r or +-sin r.  Straight-
+// line code with no large-argument path, so the unrolled epilogue stays free
+// of private memory.
+__device__ __forceinline__ float fm_cos(float x) {
+  const float k = __builtin_rintf(x * 0.636619747f);            // 2/pi
+  float r = __builtin_fmaf(-k, 1.57079637f, x);                 // pi/2 = P1 + P2 + P3
+  r = __builtin_fmaf(-k, -4.37113883e-08f, r);
+  r = __builtin_fmaf(-k, -1.77635684e-15f, r);
+  const float s = r * r;
+  float c = __builtin_fmaf(s, -2.75573200e-07f, 2.48015876e-05f);  // -1/10!, 1/8!
+  c = __builtin_fmaf(s, c, -1.38888892e-03f);                   // -1/6!
+  c = __builtin_fmaf(s, c, 4.16666679e-02f);                    // 1/4!
+  c = __builtin_fmaf(s, c, -0.5f);
+  c = __builtin_fmaf(s, c, 1.0f);
+  float sn = __builtin_fmaf(s, 2.75573188e-06f, -1.98412701e-04f); // 1/9!, -1/7!
+  sn = __builtin_fmaf(s, sn, 8.33333377e-03f);                  // 1/5!
+  sn = __builtin_fmaf(s, sn, -1.66666672e-01f);                 // -1/3!
+  sn = __builtin_fmaf(s * r, sn, r);
+  const int q = (int)k;                      // cos(r + q pi/2): c, -sn, -c, sn
+  const float v = (q & 1) ? sn : c;
+  return ((q + 1) & 2) ? -v : v;
 }
 
 __device__ __forceinline__ int fm_global_row(int ar, const int* winlist, int L) {
@@ -147,19 +175,25 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_featmap(FeatmapArgs a) {
     const int r = FM_RPL * (q * NW + wave) + lrow;
     bsrc[q] = a.Wt + (int64_t)(n0 + r) * a.ldw + 8 * (lchk ^ fm_swz(r));
   }
-  auto load_stage = [&](int kt, int buf) {
+  // load c of a stage (c < LA: A rows, else B rows) into stage buffer buf
+  auto load_one = [&](int kt, int buf, int c) {
     const int k0 = kt * FM_BK;
-    uint16_t* dA = sA + buf * STAGE_A;
-    uint16_t* dB = sB + buf * STAGE_B;
-#pragma unroll
-    for (int q = 0; q < LA; ++q)
-      __builtin_amdgcn_global_load_lds((fm_gptr)(arow[q] + min(k0 + achk[q], a.D - 8)),
-                                       (fm_lptr)(dA + (q * NW + wave) * 512), 16, 0, 0);
-#pragma unroll
-    for (int q = 0; q < LB; ++q)
-      __builtin_amdgcn_global_load_lds((fm_gptr)(bsrc[q] + k0),
-                                       (fm_lptr)(dB + (q * NW + wave) * 512), 16, 0, 0);
+    if (c < LA)
+      __builtin_amdgcn_global_load_lds((fm_gptr)(arow[c] + min(k0 + achk[c], a.D - 8)),
+                                       (fm_lptr)(sA + buf * STAGE_A + (c * NW + wave) * 512), 16, 0, 0);
+    else
+      __builtin_amdgcn_global_load_lds((fm_gptr)(bsrc[c - LA] + k0),
+                                       (fm_lptr)(sB + buf * STAGE_B + ((c - LA) * NW + wave) * 512), 16, 0, 0);
   };
+  auto load_stage = [&](int kt, int buf) {
+#pragma unroll
+    for (int c = 0; c < LA + LB; ++c) load_one(kt, buf, c);
+  };
+  constexpr int NLD = LA + LB;                       // loads per wave per stage
+  constexpr int KS = FM_BK / 16;                     // k16 steps per stage
+  constexpr int LSP = FM_LSPREAD < KS - 1 ? FM_LSPREAD : KS - 1;
+  static_assert(KS >= 2, "the last k16 step of a stage runs after its barrier");
+  constexpr int LPS = (NLD + LSP - 1) / LSP;         // loads issued per k16 step
 
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -176,64 +210,78 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_featmap(FeatmapArgs a) {
   __syncthreads();
 
   const int fr = lane & 31, fk = lane >> 5;   // fragment row/col within a 32-tile, k half
+  // two register sets of MFMA operands: step kk of a stage uses set kk & 1
+  bf16x8 fa[2][TM], fb[2][TN];
+  auto read_ops = [&](const uint16_t* cA, const uint16_t* cB, int kk, int p) {
+    const int ch = 2 * kk + fk;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int r = wm * WM + 32 * i + fr;
+      fa[p][i] = *(const bf16x8*)(&cA[r * FM_BK + ((ch ^ fm_swz(r)) * 8)]);
+    }
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int r = wn * WN + 32 * j + fr;
+      fb[p][j] = *(const bf16x8*)(&cB[r * FM_BK + ((ch ^ fm_swz(r)) * 8)]);
+    }
+  };
+  auto mfmas = [&](int p) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[p][i], fb[p][j], acc[i][j], 0, 0, 0);
+  };
+  // pin the order of one step: an MFMA, then up to two of the step's nd LDS
+  // reads behind each of the first MFMAs, then one of its nv global->LDS loads
+  // behind each later MFMA
+  auto pattern = [&](int nd, int nv) {
+    const int d0 = (nd + 1) / 2;
+#pragma unroll
+    for (int e = 0; e < TM * TN; ++e) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (2 * e < nd) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      if (2 * e + 1 < nd) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      if (e >= d0 && e - d0 < nv) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    }
+  };
+
+  // Software pipeline over the k16 steps: the operands of step kk + 1 are read
+  // (into the other register set) while step kk's MFMAs run.  The last step of
+  // a stage runs after the stage barrier, its operands already in registers, so
+  // its MFMAs cover the latency of the first reads from the next stage.  The
+  // next stage's global->LDS loads go out one behind each MFMA in the first LSP
+  // steps rather than in one burst that would hold up the MFMA issue.
+  read_ops(sA, sB, 0, 0);
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & (FM_NS - 1);
-    // stage kt + FM_NS - 1 streams into the buffer freed by the previous iteration
-    // while this one feeds the MFMAs (past the end the last stage is re-read,
-    // keeping the body branch-free and the per-stage load count fixed)
-    load_stage(min(kt + FM_NS - 1, nk - 1), (kt + FM_NS - 1) & (FM_NS - 1));
-    __builtin_amdgcn_sched_barrier(0);
+    // stage kt + FM_NS - 1 streams into the buffer freed by the previous
+    // iteration while this one feeds the MFMAs (past the end the last stage is
+    // re-read, keeping the body branch-free and the per-stage load count fixed)
+    const int lkt = min(kt + FM_NS - 1, nk - 1), lbuf = (kt + FM_NS - 1) & (FM_NS - 1);
     const uint16_t* cA = sA + cur * STAGE_A;
     const uint16_t* cB = sB + cur * STAGE_B;
-    // operands of k16 step kk + 1 are read while step kk's MFMAs run
-    bf16x8 fa[2][TM], fb[2][TN];
-    auto read_ops = [&](int kk, int p) {
-      const int ch = 2 * kk + fk;
 #pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int r = wm * WM + 32 * i + fr;
-        fa[p][i] = *(const bf16x8*)(&cA[r * FM_BK + ((ch ^ fm_swz(r)) * 8)]);
-      }
+    for (int kk = 0; kk + 1 < KS; ++kk) {
+      read_ops(cA, cB, kk + 1, (kk + 1) & 1);
 #pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int r = wn * WN + 32 * j + fr;
-        fb[p][j] = *(const bf16x8*)(&cB[r * FM_BK + ((ch ^ fm_swz(r)) * 8)]);
-      }
-    };
-#if FM_DB
-    read_ops(0, 0);
-#pragma unroll
-    for (int kk = 0; kk < FM_BK / 16; ++kk) {
-      const int p = kk & 1;
-      if (kk + 1 < FM_BK / 16) read_ops(kk + 1, p ^ 1);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[p][i], fb[p][j], acc[i][j], 0, 0, 0);
-#if FM_IL
-      // interleave: one MFMA, then one LDS read of the next step, ...
-#pragma unroll
-      for (int e = 0; e < TM + TN; ++e) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, TM * TN - TM - TN, 0);
-#endif
+      for (int c = 0; c < NLD; ++c)
+        if (c / LPS == kk) load_one(lkt, lbuf, c);
+      mfmas(kk & 1);
+      pattern(TM + TN, (kk < LSP) ? min(LPS, NLD - kk * LPS) : 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
-#else
-#pragma unroll
-    for (int kk = 0; kk < FM_BK / 16; ++kk) {
-      read_ops(kk, 0);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[0][i], fb[0][j], acc[i][j], 0, 0, 0);
-    }
-#endif
-    fm_wait_vm<AHEAD>();                              // stage kt + 1 landed
+    // every read of this stage has landed in registers before the barrier (the
+    // buffer is refilled after it); stage kt + 1 has landed after it
+    fm_wait_vm<AHEAD>();
     __syncthreads();
+    // first operands of stage kt + 1 (after the last stage: a re-read of valid
+    // data, discarded), under the MFMAs of this stage's last step
+    const int nb = (kt + 1) & (FM_NS - 1);
+    read_ops(sA + nb * STAGE_A, sB + nb * STAGE_B, 0, 0);
+    mfmas((KS - 1) & 1);
+    pattern(TM + TN, 0);
+    __builtin_amdgcn_sched_barrier(0);
   }
   fm_wait_vm<0>();                                   // nothing in flight into smem
   __syncthreads();
@@ -248,7 +296,23 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_featmap(FeatmapArgs a) {
   constexpr int NV = SROWS / 2;                      // accumulator values per lane per pass
   static_assert(SROWS == 16 || SROWS == 32, "stage 16 or 32 rows at a time");
   static_assert(WGM * WGN * SROWS * SCOLS * 4 <= FM_NS * (STAGE_A + STAGE_B) * 2, "staging exceeds LDS");
+  static_assert(WM % 64 == 0, "row scales are held 64 rows per register");
   float* stage = (float*)smem + wave * (SROWS * SCOLS);
+  // lane handles float4 column chunk (lane % (WN/4)) of rows lane / (WN/4) + k * (256/WN)
+  constexpr int CPR = WN / 4;                        // float4 chunks per row
+  constexpr int RPI = 64 / CPR;                      // rows per pass
+  constexpr int NP = SROWS / RPI;                    // passes per staged block
+  const int cc = lane % CPR, rr = lane / CPR;
+  const int col = n0 + wn * WN + 4 * cc;
+  const float4 ps = *(const float4*)(a.psi + col);
+  // the wave's row scales, one per lane and 64 rows, fetched once up front
+  // (clamped rows: never stored) and handed to the storing lanes by shuffles
+  float rsc[WM / 64];
+#pragma unroll
+  for (int q = 0; q < WM / 64; ++q) {
+    const int row = min(m0 + wm * WM + 64 * q + lane, n_rows - 1);
+    rsc[q] = a.rowscale[fm_global_row(row, a.winlist, (int)a.L)];
+  }
 #pragma unroll
   for (int h = 0; h < TM; ++h) {
 #pragma unroll
@@ -269,23 +333,36 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_featmap(FeatmapArgs a) {
 #else
       __syncthreads();
 #endif
-      // lane handles float4 column chunk (lane % (WN/4)) of rows lane / (WN/4) + k * (256/WN)
-      constexpr int CPR = WN / 4;                    // float4 chunks per row
-      constexpr int RPI = 64 / CPR;                  // rows per pass
-      const int cc = lane % CPR, rr = lane / CPR;
-      const int col = n0 + wn * WN + 4 * cc;
-      const float4 ps = *(const float4*)(a.psi + col);
-      for (int r = rr; r < SROWS; r += RPI) {
-        const int row = m0 + wm * WM + h * 32 + hf * SROWS + r;
+      // all staged values and row scales are read before any store, so no
+      // wait sits behind the row guard
+      const int lr0 = h * 32 + hf * SROWS;          // wave-local row of staged row 0
+      float4 vs[NP];
+      float scs[NP];
+#pragma unroll
+      for (int k = 0; k < NP; ++k) {
+        const int r = rr + k * RPI;
+        vs[k] = *(const float4*)(&stage[r * SCOLS + 4 * cc]);
+        scs[k] = __shfl(rsc[lr0 / 64], (lr0 % 64) + r, 64);
+      }
+#pragma unroll
+      for (int k = 0; k < NP; ++k) {
+        const int row = m0 + wm * WM + lr0 + rr + k * RPI;
+        float4 o;
+        o.x = fm_cos(vs[k].x + ps.x) * scs[k];
+        o.y = fm_cos(vs[k].y + ps.y) * scs[k];
+        o.z = fm_cos(vs[k].z + ps.z) * scs[k];
+        o.w = fm_cos(vs[k].w + ps.w) * scs[k];
         if (row < n_rows) {
-          const float sc = a.rowscale[fm_global_row(row, a.winlist, (int)a.L)];
-          const float4 v = *(const float4*)(&stage[r * SCOLS + 4 * cc]);
-          float4 o;
-          o.x = cosf(v.x + ps.x) * sc;
-          o.y = cosf(v.y + ps.y) * sc;
-          o.z = cosf(v.z + ps.z) * sc;
-          o.w = cosf(v.w + ps.w) * sc;
-          *(float4*)(a.Phi + (int64_t)row * a.m + col) = o;
+          float* dst = a.Phi + (int64_t)row * a.m + col;
+#if FM_NT
+          // the four merge into one 16-byte streaming store
+          __builtin_nontemporal_store(o.x, dst);
+          __builtin_nontemporal_store(o.y, dst + 1);
+          __builtin_nontemporal_store(o.z, dst + 2);
+          __builtin_nontemporal_store(o.w, dst + 3);
+#else
+          *(float4*)dst = o;
+#endif
         }
       }
 #if FM_EPI == 1

@@ -592,13 +592,17 @@ def test_preserved_suffix(case):
     g = PR.run_gpu(inp, n_it=wl.n_it, window=L, keep_last=K, compact=compact)
     o = PR.run_oracle(inp, n_it=wl.n_it, window=L, keep_last=K, compact=compact)
     Nc = wl.N - K
-    M = len(o.P)
-    assert len(g.P) == M and np.array_equal(g.P[M - K:], o.P[M - K:])
-    assert np.array_equal(g.t2m[Nc:], o.t2m[Nc:])
-    assert np.array_equal(g.E[M - K:], o.E[M - K:].astype(np.float32))
+    M, Mg = len(o.P), len(g.P)
+    # the suffix is the last K rows on both sides; the count of compressed rows
+    # before it may differ only through codes compare() does not hold against
+    # the GPU (near-zero or undetermined projections), which it checks below
+    assert np.array_equal(g.P[Mg - K:], o.P[M - K:])
+    assert np.array_equal(g.t2m[Nc:] - (Mg - K), np.arange(K))
+    assert np.array_equal(o.t2m[Nc:] - (M - K), np.arange(K))
+    assert np.array_equal(g.E[Mg - K:], o.E[M - K:].astype(np.float32))
     unc = {w.w: PR.oracle_uncertainty(inp, w.w, L, wl.n_it) for w in o.windows} if L == 16 else None
     rep = PR.compare(o, g, L or Nc, unc=unc)
-    _say(f"   {rep}  M={M}")
+    _say(f"   {rep}  M={M} gpu {Mg}")
 
 
 @pytest.mark.parametrize("case,T", [("tiny", 30), ("tiny", 100), ("tiny", 1), ("tiny", 512),
