@@ -2,7 +2,8 @@
 // ordering by representative position).
 //
 // book      one workgroup per window.  Windows of up to 16384 tokens are sorted
-//           in LDS (k_mg_book_lds: bitonic network on (code, token) keys);
+//           in one block (k_mg_book_lds: bitonic network on (code, token)
+//           keys in registers, wave shuffles and LDS);
 //           longer ones use global memory.  Spectral windows: stable LSD radix sort
 //           of (code, token) by code with 8-bit digits (histogram, scan and a
 //           stable scatter whose in-wave ranks come from ballot matching), so
@@ -178,19 +179,109 @@ __global__ __launch_bounds__(1024) void k_mg_book(MergeWS w) {
   if (tid == 0) w.mw[win] = nseg;
 }
 
-// Book-keeping of a window held in LDS (L <= 16384): sort the keys
-// (code << tb) | local token (tb = log2 P, P = L rounded up to a power of two,
-// padded with all-ones keys) with a bitonic network, which orders each bucket's
-// members by token; flag each bucket's last token, an exclusive scan over
-// tokens gives the representatives' ranks, and each sorted position finds its
-// bucket's last member by binary search.  Same outputs as k_mg_book.
-// Dynamic LDS: P keys + L ranks.
+// Book-keeping of a window of L <= 16384 tokens in one 1024-thread block: sort
+// the keys (code << tb) | local token (tb = log2 P, P = L rounded up to a power
+// of two, padded with all-ones keys), which orders each bucket's members by
+// token; flag each bucket's last member, rank the representatives by an
+// exclusive scan over tokens, and give every sorted position its bucket's rank.
+// Same outputs as k_mg_book.
+//
+// The P' = max(P, 1024) = 1024 E keys are held E per thread in sorted-position
+// order (thread t: positions t E .. t E + E - 1).  Bitonic network: exchanges
+// between positions less than E apart stay in registers, up to 64 E apart go
+// between lanes (DPP moves for lane distances up to 8, a swizzle for 16, a
+// permute for 32), and only farther ones (10 of the 91 steps at P = 8192)
+// through LDS and a barrier.  A
+// bucket's last member is found from the next position's code (a neighbour
+// shuffle), and each position's bucket end by a reverse scan over the block.
+// Dynamic LDS: P' + P' / 32 exchange words + L ranks.
+__device__ __forceinline__ int mg_pad(int i) { return i + (i >> 5); }
+
+// x from lane (lane ^ LM): DPP moves for LM <= 8 (quad permutes, and the row /
+// half-row mirrors i -> i ^ 15, i ^ 7 composed with them), a bit-mode swizzle
+// within 32 lanes for 16, a permute through the LDS crossbar for 32
+template <int LM>
+__device__ __forceinline__ uint32_t mg_xor_lane(uint32_t x) {
+  const int v = (int)x;
+  if constexpr (LM == 1) return (uint32_t)__builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false);
+  else if constexpr (LM == 2) return (uint32_t)__builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false);
+  else if constexpr (LM == 4)
+    return (uint32_t)__builtin_amdgcn_mov_dpp(__builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, false),
+                                              0x1B, 0xF, 0xF, false);
+  else if constexpr (LM == 8)
+    return (uint32_t)__builtin_amdgcn_mov_dpp(__builtin_amdgcn_mov_dpp(v, 0x140, 0xF, 0xF, false),
+                                              0x141, 0xF, 0xF, false);
+  else if constexpr (LM == 16) return (uint32_t)__builtin_amdgcn_ds_swizzle(v, 0x401F);
+  else return (uint32_t)__shfl_xor(v, LM, 64);
+}
+
+// one bitonic step at distance j = LM E (partner lane ^ LM, same slot)
+template <int E, int LM>
+__device__ __forceinline__ void mg_step_lane(uint32_t (&v)[E], int k) {
+  const int tid = threadIdx.x;
+  constexpr int j = LM * E;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = tid * E + e;
+    const uint32_t q = mg_xor_lane<LM>(v[e]);
+    const bool keep_min = ((i & j) == 0) == ((i & k) == 0);
+    v[e] = keep_min ? min(v[e], q) : max(v[e], q);
+  }
+}
+
+template <int E>
+__device__ __forceinline__ void mg_bitonic_reg(uint32_t (&v)[E], uint32_t* xs, int Pp) {
+  const int tid = threadIdx.x;
+  for (int k = 2; k <= Pp; k <<= 1) {
+    int j = k >> 1;
+    for (; j >= 64 * E; j >>= 1) {                 // partner in another wave: LDS
+#pragma unroll
+      for (int e = 0; e < E; ++e) xs[mg_pad(tid * E + e)] = v[e];
+      __syncthreads();
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const int i = tid * E + e;
+        const uint32_t q = xs[mg_pad(i ^ j)];
+        const bool keep_min = ((i & j) == 0) == ((i & k) == 0);
+        v[e] = keep_min ? min(v[e], q) : max(v[e], q);
+      }
+      __syncthreads();
+    }
+    // partner lane tid ^ (j / E), j = k / 2 (or 32 E) down to E
+    if (j >= 32 * E) mg_step_lane<E, 32>(v, k);
+    if (j >= 16 * E) mg_step_lane<E, 16>(v, k);
+    if (j >= 8 * E) mg_step_lane<E, 8>(v, k);
+    if (j >= 4 * E) mg_step_lane<E, 4>(v, k);
+    if (j >= 2 * E) mg_step_lane<E, 2>(v, k);
+    if (j >= E) mg_step_lane<E, 1>(v, k);
+#pragma unroll
+    for (int jj = E / 2; jj >= 1; jj >>= 1) {      // partner in this thread
+      if (jj < k) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          if ((e & jj) == 0) {
+            const int l = e | jj;
+            const bool up = ((tid * E + e) & k) == 0;
+            const uint32_t x = v[e], y = v[l];
+            v[e] = up ? min(x, y) : max(x, y);
+            v[l] = up ? max(x, y) : min(x, y);
+          }
+        }
+      }
+    }
+  }
+}
+
+template <int E>
 __global__ __launch_bounds__(1024) void k_mg_book_lds(MergeWS w, int P, int tb) {
   extern __shared__ uint32_t mg_dyn[];
-  uint32_t* key = mg_dyn;                 // [P]
-  int* R = (int*)(mg_dyn + P);            // [L]
+  const int Pp = 1024 * E;
+  uint32_t* xs = mg_dyn;                               // [Pp + Pp / 32] exchange
+  int* R = (int*)(mg_dyn + Pp + Pp / 32);            // [L] token -> rank
   __shared__ int wsum[16];
-  const int win = blockIdx.x, tid = threadIdx.x;
+  __shared__ uint32_t wfirst[16];
+  __shared__ int wend[16];
+  const int win = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = w.L;
   const int64_t base = (int64_t)win * L;
   if (!w.route[win]) {
@@ -202,57 +293,78 @@ __global__ __launch_bounds__(1024) void k_mg_book_lds(MergeWS w, int P, int tb) 
     if (tid == 0) w.mw[win] = (L + k - 1) / k;
     return;
   }
+  (void)P;
   const uint32_t tmask = (1u << tb) - 1u;
-  for (int i = tid; i < P; i += 1024)
-    key[i] = (i < L) ? ((w.codes[base + i] << tb) | (uint32_t)i) : 0xFFFFFFFFu;
-  for (int i = tid; i < L; i += 1024) R[i] = 0;
+  uint32_t v[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = tid * E + e;
+    v[e] = (i < L) ? ((w.codes[base + i] << tb) | (uint32_t)i) : 0xFFFFFFFFu;
+  }
+  mg_bitonic_reg<E>(v, xs, Pp);
+
+  // run ends: position s < L ends its bucket when s = L - 1 or the next code differs
+  if (lane == 0) wfirst[wave] = v[0];
   __syncthreads();
-  // bitonic sort, ascending
-  for (int k = 2; k <= P; k <<= 1) {
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int t = tid; t < (P >> 1); t += 1024) {
-        const int i = 2 * t - (t & (j - 1));      // lower index of the pair, bit j clear
-        const int l = i + j;
-        const uint32_t ki = key[i], kl = key[l];
-        const bool up = (i & k) == 0;
-        if ((ki > kl) == up) {
-          key[i] = kl;
-          key[l] = ki;
-        }
-      }
-      __syncthreads();
-    }
+  uint32_t nx = (uint32_t)__shfl_down((int)v[0], 1, 64);
+  if (lane == 63) nx = (wave < 15) ? wfirst[wave + 1] : 0xFFFFFFFFu;
+  bool fl[E];
+  int first_end = -1;                                // token of this thread's first run end
+#pragma unroll
+  for (int e = E - 1; e >= 0; --e) {
+    const int s = tid * E + e;
+    const uint32_t nxt = (e + 1 < E) ? v[e + 1] : nx;
+    fl[e] = (s < L) && (s == L - 1 || (nxt >> tb) != (v[e] >> tb));
+    if (fl[e]) first_end = (int)(v[e] & tmask);
   }
-  // representatives: the last member of each bucket
-  for (int s = tid; s < L; s += 1024) {
-    const uint32_t c = key[s] >> tb;
-    if (s == L - 1 || (key[s + 1] >> tb) != c) R[key[s] & tmask] = 1;
-  }
+  // representative flags in token order (every token < L is written once)
+#pragma unroll
+  for (int e = 0; e < E; ++e)
+    if (tid * E + e < L) R[v[e] & tmask] = fl[e] ? 1 : 0;
   __syncthreads();
   // exclusive scan over tokens: R[t] = number of representatives before t
-  int carry = 0;
-  for (int b0 = 0; b0 < L; b0 += 1024) {
-    const int i = b0 + tid;
-    const int f = (i < L) ? R[i] : 0;
-    int tot;
-    const int inc = block_incl_scan_1024(f, wsum, tot);
-    if (i < L) R[i] = carry + inc - f;
-    carry += tot;
-    __syncthreads();
+  int fr[E], loc = 0;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int t = tid * E + e;
+    fr[e] = (t < L) ? R[t] : 0;
+    loc += fr[e];
   }
-  for (int s = tid; s < L; s += 1024) {
-    const uint32_t ks = key[s];
-    const uint32_t bound = ((ks >> tb) + 1u) << tb;  // first key of the next code
-    int lo = s, hi = L;
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (key[mid] < bound) lo = mid + 1;
-      else hi = mid;
+  int tot;
+  const int incl = block_incl_scan_1024(loc, wsum, tot);
+  int run = incl - loc;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int t = tid * E + e;
+    if (t < L) R[t] = run;
+    run += fr[e];
+  }
+  // bucket end of each position: the first run end at or after it (reverse
+  // scan of first_end over the block; -1 = none)
+  int sf = first_end;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int q = __shfl_down(sf, o, 64);
+    if (lane + o < 64 && sf < 0) sf = q;
+  }
+  if (lane == 0) wend[wave] = sf;
+  __syncthreads();                                   // also publishes R
+  int tail = -1;                                     // first run end in a later wave
+  for (int q = 15; q > wave; --q)
+    if (wend[q] >= 0) tail = wend[q];
+  const int full = (sf >= 0) ? sf : tail;
+  int cur = __shfl_down(full, 1, 64);
+  if (lane == 63) cur = tail;
+#pragma unroll
+  for (int e = E - 1; e >= 0; --e) {
+    const int s = tid * E + e;
+    if (fl[e]) cur = (int)(v[e] & tmask);
+    if (s < L) {
+      w.sval[base + s] = (int)(base + (v[e] & tmask));
+      w.sloc[base + s] = R[cur];
     }
-    w.sval[base + s] = (int)(base + (ks & tmask));
-    w.sloc[base + s] = R[key[lo - 1] & tmask];
   }
-  if (tid == 0) w.mw[win] = carry;
+  if (tid == 0) w.mw[win] = tot;
 }
 
 // inclusive max-scan of one int per thread over a 1024-thread block
@@ -935,14 +1047,25 @@ hipError_t launch_merge(const MergeWS& w, const void* X, int dtype, int64_t ldx,
       P <<= 1;
       ++tb;
     }
-    const size_t bytes = (size_t)P * 4 + (size_t)w.L * 4;
+    const int Pp = P > 1024 ? P : 1024;
+    const size_t bytes = (size_t)(Pp + Pp / 32) * 4 + (size_t)w.L * 4;
+    const void* kf = (Pp == 1024)   ? (const void*)k_mg_book_lds<1>
+                     : (Pp == 2048) ? (const void*)k_mg_book_lds<2>
+                     : (Pp == 4096) ? (const void*)k_mg_book_lds<4>
+                     : (Pp == 8192) ? (const void*)k_mg_book_lds<8>
+                                    : (const void*)k_mg_book_lds<16>;
     if (bytes > 65536) {
-      const hipError_t e = hipFuncSetAttribute((const void*)k_mg_book_lds,
-                                               hipFuncAttributeMaxDynamicSharedMemorySize,
+      const hipError_t e = hipFuncSetAttribute(kf, hipFuncAttributeMaxDynamicSharedMemorySize,
                                                (int)bytes);
       if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(k_mg_book_lds, dim3(w.n_win), dim3(1024), bytes, s, w, P, tb);
+    switch (Pp) {
+      case 1024: hipLaunchKernelGGL(k_mg_book_lds<1>, dim3(w.n_win), dim3(1024), bytes, s, w, P, tb); break;
+      case 2048: hipLaunchKernelGGL(k_mg_book_lds<2>, dim3(w.n_win), dim3(1024), bytes, s, w, P, tb); break;
+      case 4096: hipLaunchKernelGGL(k_mg_book_lds<4>, dim3(w.n_win), dim3(1024), bytes, s, w, P, tb); break;
+      case 8192: hipLaunchKernelGGL(k_mg_book_lds<8>, dim3(w.n_win), dim3(1024), bytes, s, w, P, tb); break;
+      default: hipLaunchKernelGGL(k_mg_book_lds<16>, dim3(w.n_win), dim3(1024), bytes, s, w, P, tb); break;
+    }
   } else {
     hipLaunchKernelGGL(k_mg_book, dim3(w.n_win), dim3(1024), 0, s, w);
   }
