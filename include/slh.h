@@ -263,6 +263,21 @@ int slh_load(slh_ctx *ctx, int32_t which, const void *src, int64_t bytes);
 int slh_stage_times(slh_ctx *ctx, double *ms_out, int32_t n);
 
 /*
+ * Duration of one pass over Phi without per-launch events (measurement aid for
+ * the matvec of Algorithm 2, A v = Phi (Phi^T v)): the two pass kernels of the
+ * final step of the last slh_lanczos call (Phi^T v, then Phi t), with that
+ * step's launch configuration and data, are captured reps times as one HIP
+ * graph, replayed once untimed and once between two events on the context
+ * stream.  us_out: host, 1 double = elapsed microseconds / (2 reps), so gaps
+ * between graph nodes are included.  The replays rewrite only the step's pass
+ * scratch (partial sums), never Q, T, alpha, beta, the Ritz pairs or codes;
+ * windows that broke down early skip their passes as in the loop itself.
+ * reps in [1, 4096].  Synchronises the stream.  SLH_ESTATE before slh_lanczos
+ * or after a short-window (single-wavefront) Lanczos run, which has no passes.
+ */
+int slh_time_passes(slh_ctx *ctx, int32_t reps, double *us_out);
+
+/*
  * Spectral-energy fraction (section 5 kill test on spectral energy; rank
  * ablation): for each spectral window, sum of its r kept Ritz values divided by
  * tr(Phi_w Phi_w^T) = ||Phi_w||_F^2, the squared Frobenius norm of the rows the

@@ -565,4 +565,16 @@ hipError_t launch_lanczos(const LanczosWS& w, const double* q1_act, hipStream_t 
   return hipGetLastError();
 }
 
+// reps x (Phi^T v, Phi t) of step j, launched exactly as in launch_lanczos
+hipError_t launch_lanczos_passes(const LanczosWS& w, int j, int reps, hipStream_t s) {
+  (void)hipGetLastError();
+  const int ns = w.m / 256;
+  const int nx = (j > 0) ? (j + 15) / 16 + 1 : 0;
+  for (int q = 0; q < reps; ++q) {
+    hipLaunchKernelGGL(k_lz_phit, dim3(nx + ns * w.GA, w.n_act), dim3(512), 0, s, w, j);
+    hipLaunchKernelGGL(k_lz_phiu, dim3((j + 8) / 8 + ns * w.GA, w.n_act), dim3(512), 0, s, w, j);
+  }
+  return hipGetLastError();
+}
+
 }  // namespace slh

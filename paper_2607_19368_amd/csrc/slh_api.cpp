@@ -120,6 +120,8 @@ struct slh_ctx {
 
   hipGraphExec_t lz_exec = nullptr;
   std::string lz_key;
+  LanczosWS lz_w{};                 // workspace of the last full-size Lanczos run
+  bool lz_w_valid = false;
 
   int short_win = 1;                // SLH_OPT_SHORT_WINDOWS
   int normalize = 0;                // SLH_OPT_NORMALIZE
@@ -662,6 +664,7 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
         HIP_TRY(c, hipEventRecord(c->ev[4], c->stream));
       }
       c->fused_timed = 0;
+      c->lz_w_valid = false;
     } else {
       LanczosWS w;
       w.n_act = na;
@@ -750,6 +753,8 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
       }
       if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[3], c->stream));
       c->fused_timed = c->timing ? 2 * n_it : 0;
+      c->lz_w = w;
+      c->lz_w_valid = true;
       HIP_TRY(c, launch_tridiag_eig(w.alpha, w.beta, w.neff, na, n_it, c->r, P<double>(c->theta),
                                     P<double>(c->Seig), c->stream));
       HIP_TRY(c, launch_ritz(w.Q, P<double>(c->Seig), w.neff, na, (int)L, w.ldq, n_it, c->r,
@@ -991,6 +996,42 @@ int slh_stage_times(slh_ctx* c, double* out, int32_t n) {
   v[7] = c->norm_timed ? el(c->ev[9], c->ev[10]) : 0.0;
   for (int i = 0; i < n && i < 8; ++i) out[i] = v[i];
   (void)hipGetLastError();   // a stage that did not run leaves unrecorded events
+  return SLH_OK;
+}
+
+int slh_time_passes(slh_ctx* c, int32_t reps, double* us_out) {
+  if (!c || !us_out) return SLH_EINVAL;
+  if (reps < 1 || reps > 4096) return fail(c, SLH_EINVAL, "reps must be in [1, 4096]");
+  if (c->stage < 2 || !c->lz_w_valid)
+    return fail(c, SLH_ESTATE, "slh_time_passes needs a preceding full-size slh_lanczos");
+  const LanczosWS& w = c->lz_w;
+  hipGraph_t g = nullptr;
+  hipGraphExec_t ge = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  HIP_TRY(c, hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal));
+  const hipError_t le = launch_lanczos_passes(w, w.n_it - 1, reps, c->cap_stream);
+  const hipError_t ce = hipStreamEndCapture(c->cap_stream, &g);
+  if (le != hipSuccess || ce != hipSuccess) {
+    if (g) (void)hipGraphDestroy(g);
+    return fail(c, SLH_EHIP, "pass graph capture: %s / %s", hipGetErrorString(le),
+                hipGetErrorString(ce));
+  }
+  hipError_t e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+  (void)hipGraphDestroy(g);
+  if (e == hipSuccess) e = hipEventCreate(&e0);
+  if (e == hipSuccess) e = hipEventCreate(&e1);
+  if (e == hipSuccess) e = hipGraphLaunch(ge, c->stream);          // warm-up replay
+  if (e == hipSuccess) e = hipEventRecord(e0, c->stream);
+  if (e == hipSuccess) e = hipGraphLaunch(ge, c->stream);
+  if (e == hipSuccess) e = hipEventRecord(e1, c->stream);
+  if (e == hipSuccess) e = hipEventSynchronize(e1);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+  if (ge) (void)hipGraphExecDestroy(ge);
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  if (e != hipSuccess) return fail(c, SLH_EHIP, "slh_time_passes: %s", hipGetErrorString(e));
+  *us_out = 1000.0 * (double)ms / (2.0 * reps);
   return SLH_OK;
 }
 

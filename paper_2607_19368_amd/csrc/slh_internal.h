@@ -59,6 +59,9 @@ struct LanczosWS {
 hipError_t launch_lanczos(const LanczosWS& w, const double* q1_act, hipStream_t s,
                           const hipEvent_t* ev_before = nullptr,
                           const hipEvent_t* ev_after = nullptr);
+// reps x the two Phi passes of step j (Phi^T v, then Phi t_j), launched as in
+// launch_lanczos; they rewrite only Spart, Upart, H1 and H2 (for timing)
+hipError_t launch_lanczos_passes(const LanczosWS& w, int j, int reps, hipStream_t s);
 
 // ---- eigensolve + Ritz + SimHash (k_eig.hip, k_hash.hip) ----
 hipError_t launch_tridiag_eig(const double* alpha, const double* beta, const int* neff,

@@ -26,7 +26,7 @@ EXPORTS = [
     "slh_gen_params", "slh_gen_start", "slh_create", "slh_destroy", "slh_last_error",
     "slh_set_option", "slh_set_stream", "slh_route", "slh_feature_map", "slh_lanczos",
     "slh_simhash", "slh_merge", "slh_merge_capacity", "slh_copy_out", "slh_num_windows",
-    "slh_num_spectral", "slh_load", "slh_stage_times", "slh_spectral_energy",
+    "slh_num_spectral", "slh_load", "slh_stage_times", "slh_time_passes", "slh_spectral_energy",
     "slh_bucket_purity",
 ]
 
@@ -67,6 +67,7 @@ def load():
         "slh_spectral_energy": (i32, [vp, vp]),
         "slh_bucket_purity": (i32, [vp, vp, i32, i64, ctypes.c_double, vp]),
         "slh_stage_times": (i32, [vp, vp, i32]),
+        "slh_time_passes": (i32, [vp, i32, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -255,6 +256,13 @@ def slh_stage_times(ctx):
     out = np.zeros(len(STAGE_NAMES), np.float64)
     _check(ctx, load().slh_stage_times(ctx.handle, _ptr(out), len(out)), "slh_stage_times")
     return dict(zip(STAGE_NAMES, out.tolist()))
+
+
+def slh_time_passes(ctx, reps=96):
+    """Microseconds per pass over Phi, from a graph replay of the last Lanczos step's passes."""
+    out = np.zeros(1, np.float64)
+    _check(ctx, load().slh_time_passes(ctx.handle, int(reps), _ptr(out)), "slh_time_passes")
+    return float(out[0])
 
 
 def slh_load(ctx, which, src):

@@ -692,3 +692,57 @@ def test_exact_target_length(case, T):
     assert np.array_equal(gP, oP) and np.array_equal(gt, ot)
     rel = np.linalg.norm(gE - oE, axis=1) / np.maximum(np.linalg.norm(oE, axis=1), 1e-30)
     assert rel.max() <= 1e-5
+
+
+@pytest.mark.parametrize("case", ["tiny", "windows256"])
+def test_time_passes(case):
+    """slh_time_passes replays the final step's two passes over Phi as a graph:
+    it returns a positive duration and leaves every result of slh_lanczos (Q,
+    alpha, beta, Ritz values and vectors) and the SimHash codes bit-identical;
+    it is refused before slh_lanczos and after a short-window run."""
+    import paper_2607_19368_amd as P
+    from paper_2607_19368_amd import slh as B
+    if case == "tiny":
+        inp, L = make_inputs("tiny"), 0
+    else:
+        inp, L = _custom("tpw", 4 * 256, 512, 256, 24, 8, 8), 256
+    wl = inp.workload
+    Xd = PR.to_device_x(inp)
+
+    def run(time_it):
+        ctx = P.slh_create(wl.N, wl.D, wl.m, wl.r, wl.bits, 0)
+        if L:
+            P.slh_set_option(ctx, B.SLH_OPT_WINDOW_LEN, L)
+        P.slh_feature_map(ctx, Xd)
+        if time_it:
+            with pytest.raises(B.SLHError):
+                P.slh_time_passes(ctx, 4)
+        P.slh_lanczos(ctx, wl.n_it)
+        outs = [P.slh_copy_out(ctx, k) for k in (B.SLH_OUT_Q, B.SLH_OUT_ALPHA, B.SLH_OUT_BETA,
+                                                  B.SLH_OUT_THETA, B.SLH_OUT_Z)]
+        us = None
+        if time_it:
+            us = P.slh_time_passes(ctx, 16)
+            after = [P.slh_copy_out(ctx, k) for k in (B.SLH_OUT_Q, B.SLH_OUT_ALPHA, B.SLH_OUT_BETA,
+                                                       B.SLH_OUT_THETA, B.SLH_OUT_Z)]
+            for a, b in zip(outs, after):
+                assert np.array_equal(a, b)
+        P.slh_simhash(ctx)
+        return us, P.slh_copy_out(ctx, B.SLH_OUT_CODES)
+
+    us, codes_t = run(True)
+    _, codes = run(False)
+    _say(f"[time passes] {case}: {us:.2f} us per pass")
+    assert np.isfinite(us) and 0.0 < us < 1e5
+    assert np.array_equal(codes_t, codes)
+    # short windows have no passes over Phi
+    inp16 = make_inputs("local16", N=524)
+    w16 = inp16.workload
+    ctx = P.slh_create(w16.N, w16.D, w16.m, w16.r, w16.bits, 0)
+    P.slh_set_option(ctx, B.SLH_OPT_KEEP_LAST, w16.keep_last)
+    P.slh_set_option(ctx, B.SLH_OPT_WINDOW_LEN, 16)
+    P.slh_feature_map(ctx, PR.to_device_x(inp16))
+    P.slh_lanczos(ctx, w16.n_it)
+    with pytest.raises(B.SLHError):
+        P.slh_time_passes(ctx, 4)
+
