@@ -674,16 +674,11 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
       w.ldq = n_it + 1;
       w.tol = c->tol;
       {
-        // about four blocks per CU over all windows in each pass over Phi (blocks of
-        // RBA rows x 256 columns)
-        const int64_t target = (int64_t)4 * c->n_cu;
-        auto rows8 = [](int64_t rows) {          // multiple of 8 in [8, 32]
-          rows = ((rows + 7) / 8) * 8;
-          return (int)std::max<int64_t>(8, std::min<int64_t>(rows, 32));
-        };
-        const int ns = (int)(c->m / 256);
-        const int64_t ga = std::max<int64_t>(1, target / ((int64_t)na * ns));
-        w.RWA = rows8((L + 8 * ga - 1) / (8 * ga));
+        // blocks of RBA rows x 256 columns in each pass over Phi, 8 rows per wave
+        // for m >= 2048 and 16 below (measured per step: 8192 x 2048 and
+        // 32768 x 2048 fastest at 8, the latter 13.5 ms against 15.9 at 32;
+        // 4096 x 1024 and 32 windows of 2048 x 1024 fastest at 16)
+        w.RWA = (c->m >= 2048) ? 8 : 16;
         w.RBA = 8 * w.RWA;
         w.GA = (int)((L + w.RBA - 1) / w.RBA);
         w.G3 = (int)((L + 31) / 32);
