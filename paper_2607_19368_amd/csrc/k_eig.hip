@@ -215,7 +215,10 @@ hipError_t launch_tridiag_eig(const double* alpha, const double* beta, const int
 // Z[a][i][c] = sum_{k < n_eff} Q[a][k][i] Seig[a][k][c]   (fp64).
 // A block owns 32 rows; thread (row rl = tid % 32, group cg = tid / 32) owns
 // CPT = r / 8 (rounded up) columns.  S and the block's Q rows are staged through
-// LDS 32 values of k at a time, every load of a chunk issued at once.
+// LDS 32 values of k at a time.  Each chunk is fetched into registers with
+// unconditional loads (indices clamped; values past n_eff or r are masked when
+// stored to LDS), the next chunk's loads in flight while the current one is
+// used, so the kernel waits on memory about once per chunk.
 template <int CPT>
 __global__ __launch_bounds__(256) void k_ritz(const double* __restrict__ Q,
                                               const double* __restrict__ Seig,
@@ -233,18 +236,40 @@ __global__ __launch_bounds__(256) void k_ritz(const double* __restrict__ Q,
   double acc[CPT];
 #pragma unroll
   for (int c = 0; c < CPT; ++c) acc[c] = 0.0;
+  // a chunk: 32 x 8 CPT values of S (CPT per thread) and 32 x 32 of Q (4 per thread)
+  double vs[CPT], vq[4];
+  auto fetch = [&](int k0) {
+    const int kl = max(min(32, n - k0) - 1, 0) + k0;   // last valid k of the chunk
+#pragma unroll
+    for (int q = 0; q < CPT; ++q) {
+      const int e = tid + 256 * q;
+      const int kr = e / (8 * CPT), c = e % (8 * CPT);
+      vs[q] = Sa[(int64_t)min(k0 + kr, kl) * r + min(c, r - 1)];
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = tid + 256 * q;
+      const int kr = e >> 5, rr = e & 31;
+      vq[q] = Qa[(int64_t)min(k0 + kr, kl) * L + min(r0 + rr, L - 1)];
+    }
+  };
+  if (n > 0) fetch(0);
   for (int k0 = 0; k0 < n; k0 += 32) {
     const int nk = min(32, n - k0);
-    // S rows k0 .. k0 + 31 (zero past n_eff or r) and Q[k][r0 .. r0 + 31]
-    for (int e = tid; e < 32 * 8 * CPT; e += 256) {
+#pragma unroll
+    for (int q = 0; q < CPT; ++q) {
+      const int e = tid + 256 * q;
       const int kr = e / (8 * CPT), c = e % (8 * CPT);
-      sS[kr][c] = (kr < nk && c < r) ? Sa[(int64_t)(k0 + kr) * r + c] : 0.0;
+      sS[kr][c] = (kr < nk && c < r) ? vs[q] : 0.0;
     }
-    for (int e = tid; e < 32 * 32; e += 256) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = tid + 256 * q;
       const int kr = e >> 5, rr = e & 31;
-      sQ[kr][rr] = (kr < nk) ? Qa[(int64_t)(k0 + kr) * L + min(r0 + rr, L - 1)] : 0.0;
+      sQ[kr][rr] = (kr < nk) ? vq[q] : 0.0;
     }
     __syncthreads();
+    if (k0 + 32 < n) fetch(k0 + 32);           // in flight during the FMAs below
 #pragma unroll 8
     for (int kk = 0; kk < 32; ++kk) {
       const double q = sQ[kk][rl];
