@@ -16,6 +16,7 @@ __global__ __launch_bounds__(256) void k_rownorm(const void* __restrict__ Xv, in
                                                  double sqrt2m, int gauss,
                                                  double* __restrict__ nrm2_fm,
                                                  double* __restrict__ nrm_x,
+                                                 double* __restrict__ inv_x,
                                                  float* __restrict__ rowscale,
                                                  uint16_t* __restrict__ Xb) {
   const int lane = threadIdx.x & 63;
@@ -62,15 +63,17 @@ __global__ __launch_bounds__(256) void k_rownorm(const void* __restrict__ Xv, in
   s_x = wave_sum_f64(s_x);
   if (lane == 0) {
     nrm2_fm[row] = s_fm;
-    nrm_x[row] = sqrt(s_x);
+    const double nx = sqrt(s_x);
+    nrm_x[row] = nx;
+    inv_x[row] = nx > 0.0 ? 1.0 / nx : 0.0;
     double sc = gauss ? 1.0 : exp(s_fm * inv2sqrtD);
     rowscale[row] = (float)(sc * sqrt2m);
   }
 }
 
 hipError_t launch_rownorm(const void* X, int dtype, int64_t ldx, int64_t N, int D, int m,
-                          int gauss, double* nrm2_fm, double* nrm_x, float* rowscale,
-                          uint16_t* Xb, hipStream_t s) {
+                          int gauss, double* nrm2_fm, double* nrm_x, double* inv_x,
+                          float* rowscale, uint16_t* Xb, hipStream_t s) {
   (void)hipGetLastError();
   if (N <= 0) return hipSuccess;
   dim3 grid((unsigned)((N + 3) / 4));
@@ -78,10 +81,10 @@ hipError_t launch_rownorm(const void* X, int dtype, int64_t ldx, int64_t N, int 
   double sqrt2m = sqrt(2.0 / (double)m);
   if (dtype == 0)
     hipLaunchKernelGGL(k_rownorm<0>, grid, dim3(256), 0, s, X, ldx, N, D, inv2sqrtD, sqrt2m,
-                       gauss, nrm2_fm, nrm_x, rowscale, Xb);
+                       gauss, nrm2_fm, nrm_x, inv_x, rowscale, Xb);
   else
     hipLaunchKernelGGL(k_rownorm<1>, grid, dim3(256), 0, s, X, ldx, N, D, inv2sqrtD, sqrt2m,
-                       gauss, nrm2_fm, nrm_x, rowscale, Xb);
+                       gauss, nrm2_fm, nrm_x, inv_x, rowscale, Xb);
   return hipGetLastError();
 }
 

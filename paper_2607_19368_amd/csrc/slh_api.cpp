@@ -111,7 +111,7 @@ struct slh_ctx {
 
   std::vector<DevBuf*> all;
   DevBuf Wt, psi, R, q1all, q1act, winlist, route;
-  DevBuf nrm2_fm, nrm_x, rowscale, Xb, Phi;
+  DevBuf nrm2_fm, nrm_x, inv_x, rowscale, Xb, Phi;
   DevBuf Q, T, U, Z1, Spart, H1, H2part, H2, alpha, beta, neff, stop, amax;
   DevBuf theta, Seig, Z, proj, codes;
   DevBuf keyA, keyB, valA, valB, tmpi, segid, segk, sval, sloc, mw, wbase, sseg, Mtot;
@@ -238,6 +238,7 @@ int check_x(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx) {
 int prep_norms(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx) {
   ENSURE(c, c->nrm2_fm, c->N * sizeof(double));
   ENSURE(c, c->nrm_x, c->N * sizeof(double));
+  ENSURE(c, c->inv_x, c->N * sizeof(double));
   ENSURE(c, c->rowscale, c->N * sizeof(float));
   uint16_t* xb = nullptr;
   if (dtype == SLH_F32) {
@@ -246,7 +247,7 @@ int prep_norms(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx) {
   }
   HIP_TRY(c, launch_rownorm(X, dtype == SLH_BF16 ? 0 : 1, ldx, c->N, (int)c->D, (int)c->m,
                             c->gauss, P<double>(c->nrm2_fm), P<double>(c->nrm_x),
-                            P<float>(c->rowscale), xb, c->stream));
+                            P<double>(c->inv_x), P<float>(c->rowscale), xb, c->stream));
   c->norms_of = X;
   return SLH_OK;
 }
@@ -422,7 +423,7 @@ void slh_destroy(slh_ctx* c) {
   if (!c) return;
   drop_graph(c);
   DevBuf* bufs[] = {&c->Wt, &c->psi, &c->R, &c->q1all, &c->q1act, &c->winlist, &c->route,
-                    &c->nrm2_fm, &c->nrm_x, &c->rowscale, &c->Xb, &c->Phi, &c->Q, &c->T,
+                    &c->nrm2_fm, &c->nrm_x, &c->inv_x, &c->rowscale, &c->Xb, &c->Phi, &c->Q, &c->T,
                     &c->U, &c->Z1, &c->Spart, &c->H1, &c->H2part, &c->H2,
                     &c->alpha, &c->beta, &c->neff, &c->stop, &c->amax, &c->theta, &c->Seig, &c->Z,
                     &c->proj, &c->codes, &c->keyA, &c->keyB, &c->valA, &c->valB, &c->tmpi,
@@ -537,9 +538,9 @@ int slh_route(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, double rho,
   if (!(rho > 0.0)) return fail(c, SLH_EINVAL, "rho must be > 0");
   const int64_t L = window_len(c);
   if ((rc = prep_norms(c, X, dtype, ldx))) return rc;
-  ENSURE(c, c->rpart, (size_t)c->n_win * ((c->D + 1023) / 1024) * 2 * sizeof(double));
+  ENSURE(c, c->rpart, (size_t)c->n_win * route_slices((int)c->D) * 2 * sizeof(double));
   ENSURE(c, c->scores, (size_t)c->n_win * sizeof(double));
-  HIP_TRY(c, launch_route_scores(X, dtype == SLH_BF16 ? 0 : 1, ldx, P<double>(c->nrm_x),
+  HIP_TRY(c, launch_route_scores(X, dtype == SLH_BF16 ? 0 : 1, ldx, P<double>(c->inv_x),
                                  (int)c->n_win, (int)L, (int)c->D, P<double>(c->rpart),
                                  P<double>(c->scores), c->stream));
   std::vector<double> sc((size_t)c->n_win);

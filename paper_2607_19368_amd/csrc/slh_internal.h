@@ -11,8 +11,8 @@ namespace slh {
 // s_i = exp(nrm2_fm[i] / (2 sqrt(D))) (or 1 for the Gaussian map).
 // For fp32 X it also writes the bf16 copy Xb (row stride D).
 hipError_t launch_rownorm(const void* X, int dtype, int64_t ldx, int64_t N, int D, int m,
-                          int gauss, double* nrm2_fm, double* nrm_x, float* rowscale,
-                          uint16_t* Xb, hipStream_t s);
+                          int gauss, double* nrm2_fm, double* nrm_x, double* inv_x,
+                          float* rowscale, uint16_t* Xb, hipStream_t s);
 
 // ---- feature map (k_featmap.hip) ----
 struct FeatmapArgs {
@@ -137,7 +137,9 @@ hipError_t launch_merge(const MergeWS& w, const void* X, int dtype, int64_t ldx,
                         float* E, int* P, int* tok2macro, hipStream_t s);
 
 // ---- adaptive routing (k_route.hip) ----
-hipError_t launch_route_scores(const void* X, int dtype, int64_t ldx, const double* nrm_x,
+// inv_x: 1 / |x_i| per row (0 for a zero row); part: n_win * route_slices(D) * 2
+int route_slices(int D);
+hipError_t launch_route_scores(const void* X, int dtype, int64_t ldx, const double* inv_x,
                                int n_win, int L, int D, double* part, double* scores,
                                hipStream_t s);
 
