@@ -235,21 +235,23 @@ __global__ __launch_bounds__(512) void k_lz_phit(LanczosWS w, int j) {
 // 16 columns x 16 partial lanes).  Every load is issued before the first
 // reduction.
 // ---------------------------------------------------------------------------
+// KT = 16-step slots of k per thread: 16 KT >= n_it (fewer registers for short runs)
+template <int KT>
 __global__ __launch_bounds__(256) void k_lz_finish(LanczosWS w, int j) {
   const int a = blockIdx.y, g = blockIdx.x, tid = threadIdx.x;
   const int m = w.m, hs = w.ldq + 1;
   const int cl = tid & 15, pl = tid >> 4;
   const int c = g * 16 + cl;                   // m is a multiple of 16
   const double* H2 = w.H2 + (int64_t)a * hs;
-  // The loads of t_k and h2_k (k = pl + 16 e < j <= 256), of the |h2|^2 terms
+  // The loads of t_k and h2_k (k = pl + 16 e < j <= 16 KT), of the |h2|^2 terms
   // (k = tid, tid + 256 < j), of |z1|^2 and of the step state are all issued
   // before the first use, with clamped indices (surplus values are masked), so
   // the kernel waits on memory once.
   const int jm = max(j - 1, 0);
   const double* Ta = w.T + (int64_t)a * w.ldq * m + c;
-  double tv[16], hv[16];
+  double tv[KT], hv[KT];
 #pragma unroll
-  for (int e = 0; e < 16; ++e) {
+  for (int e = 0; e < KT; ++e) {
     const int k = min(pl + 16 * e, jm);
     tv[e] = Ta[(int64_t)k * m];
     hv[e] = H2[k];
@@ -267,7 +269,7 @@ __global__ __launch_bounds__(256) void k_lz_finish(LanczosWS w, int j) {
   {
     double acc[4] = {0, 0, 0, 0};
 #pragma unroll
-    for (int e = 0; e < 16; ++e)
+    for (int e = 0; e < KT; ++e)
       if (pl + 16 * e < j) acc[e & 3] = fma(tv[e], hv[e], acc[e & 3]);
     corr = (acc[0] + acc[1]) + (acc[2] + acc[3]);
   }
@@ -383,8 +385,11 @@ __global__ __launch_bounds__(512) void k_lz_phiu(LanczosWS w, int j) {
 // (row, kg) loads Q[k][row] for k = kg + 8 t (k < j) once, into registers, and
 // uses them for the q_j update, for z1 = u - Q h1 and for the h2 partials.
 // ---------------------------------------------------------------------------
+// MAXT = 8-step slots of k per thread: 8 MAXT >= n_it, MAXT a multiple of 8
+// (fewer registers for short runs)
+template <int MAXT>
 __global__ __launch_bounds__(256) void k_lz_orth(LanczosWS w, int j) {
-  constexpr int MAXT = 32;                     // n_it <= 256
+  static_assert(MAXT % 8 == 0, "slots are reduced 8 at a time");
   const int a = blockIdx.y, g = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63;
   const int L = w.L, hs = w.ldq + 1;
@@ -545,6 +550,28 @@ static void launch_timed(K kernel, dim3 grid, dim3 block, hipStream_t s, hipEven
   else hipLaunchKernelGGL(kernel, grid, block, 0, s, w, j);
 }
 
+// the smallest slot counts that cover n_it (finish: 16 KT >= n_it; orth: 8 MAXT >= n_it,
+// MAXT a multiple of 8)
+static void launch_finish(const LanczosWS& w, int j, hipStream_t s) {
+  const dim3 g(w.m / 16, w.n_act), b(256);
+  const int kt = (w.n_it + 15) / 16;
+  if (kt <= 2) hipLaunchKernelGGL(k_lz_finish<2>, g, b, 0, s, w, j);
+  else if (kt <= 4) hipLaunchKernelGGL(k_lz_finish<4>, g, b, 0, s, w, j);
+  else if (kt <= 6) hipLaunchKernelGGL(k_lz_finish<6>, g, b, 0, s, w, j);
+  else if (kt <= 8) hipLaunchKernelGGL(k_lz_finish<8>, g, b, 0, s, w, j);
+  else if (kt <= 12) hipLaunchKernelGGL(k_lz_finish<12>, g, b, 0, s, w, j);
+  else hipLaunchKernelGGL(k_lz_finish<16>, g, b, 0, s, w, j);
+}
+
+static void launch_orth(const LanczosWS& w, int j, hipStream_t s) {
+  const dim3 g(w.G3, w.n_act), b(256);
+  const int mt = (w.n_it + 7) / 8;                 // MAXT: a multiple of 8 (h2 butterflies)
+  if (mt <= 8) hipLaunchKernelGGL(k_lz_orth<8>, g, b, 0, s, w, j);
+  else if (mt <= 16) hipLaunchKernelGGL(k_lz_orth<16>, g, b, 0, s, w, j);
+  else if (mt <= 24) hipLaunchKernelGGL(k_lz_orth<24>, g, b, 0, s, w, j);
+  else hipLaunchKernelGGL(k_lz_orth<32>, g, b, 0, s, w, j);
+}
+
 hipError_t launch_lanczos(const LanczosWS& w, const double* q1_act, hipStream_t s,
                           const hipEvent_t* ev_before, const hipEvent_t* ev_after) {
   (void)hipGetLastError();
@@ -554,11 +581,11 @@ hipError_t launch_lanczos(const LanczosWS& w, const double* q1_act, hipStream_t 
     const int nx = (j > 0) ? (j + 15) / 16 + 1 : 0;
     launch_timed(k_lz_phit, dim3(nx + ns * w.GA, w.n_act), dim3(512), s,
                  ev_before ? ev_before[2 * j] : nullptr, ev_after ? ev_after[2 * j] : nullptr, w, j);
-    hipLaunchKernelGGL(k_lz_finish, dim3(w.m / 16, w.n_act), dim3(256), 0, s, w, j);
+    launch_finish(w, j, s);
     launch_timed(k_lz_phiu, dim3((j + 8) / 8 + ns * w.GA, w.n_act), dim3(512), s,
                  ev_before ? ev_before[2 * j + 1] : nullptr,
                  ev_after ? ev_after[2 * j + 1] : nullptr, w, j);
-    hipLaunchKernelGGL(k_lz_orth, dim3(w.G3, w.n_act), dim3(256), 0, s, w, j);
+    launch_orth(w, j, s);
   }
   hipLaunchKernelGGL(k_lz_h2sum, dim3((w.n_it + 15) / 16 + 1, w.n_act), dim3(512), 0, s, w);
   hipLaunchKernelGGL(k_lz_last_beta, dim3(w.n_act), dim3(256), 0, s, w);
