@@ -116,7 +116,7 @@ struct slh_ctx {
   DevBuf theta, Seig, Z, proj, codes;
   DevBuf keyA, keyB, valA, valB, tmpi, segid, segk, sval, sloc, mw, wbase, sseg, Mtot;
   DevBuf part, part_seg, part_cnt, part_nsum, part_end;
-  DevBuf rpart, scores;
+  DevBuf rpart, scores, rsu;
 
   hipGraphExec_t lz_exec = nullptr;
   std::string lz_key;
@@ -429,7 +429,7 @@ void slh_destroy(slh_ctx* c) {
                     &c->proj, &c->codes, &c->keyA, &c->keyB, &c->valA, &c->valB, &c->tmpi,
                     &c->segid, &c->segk, &c->sval, &c->sloc, &c->mw, &c->wbase, &c->sseg,
                     &c->Mtot, &c->part, &c->part_seg, &c->part_cnt, &c->part_nsum,
-                    &c->part_end, &c->rpart, &c->scores};
+                    &c->part_end, &c->rpart, &c->scores, &c->rsu};
   for (DevBuf* b : bufs)
     if (b->p) (void)hipFree(b->p);
   if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
@@ -537,12 +537,33 @@ int slh_route(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, double rho,
   if (rc) return rc;
   if (!(rho > 0.0)) return fail(c, SLH_EINVAL, "rho must be > 0");
   const int64_t L = window_len(c);
-  if ((rc = prep_norms(c, X, dtype, ldx))) return rc;
   ENSURE(c, c->rpart, (size_t)c->n_win * route_slices((int)c->D) * 2 * sizeof(double));
   ENSURE(c, c->scores, (size_t)c->n_win * sizeof(double));
-  HIP_TRY(c, launch_route_scores(X, dtype == SLH_BF16 ? 0 : 1, ldx, P<double>(c->inv_x),
-                                 (int)c->n_win, (int)L, (int)c->D, P<double>(c->rpart),
-                                 P<double>(c->scores), c->stream));
+  const int G = route_norm_groups((int)L, (int)c->D);
+  if (G > 0) {
+    // one read of X for the row norms and the scores
+    ENSURE(c, c->nrm2_fm, c->N * sizeof(double));
+    ENSURE(c, c->nrm_x, c->N * sizeof(double));
+    ENSURE(c, c->inv_x, c->N * sizeof(double));
+    ENSURE(c, c->rowscale, c->N * sizeof(float));
+    uint16_t* xb = nullptr;
+    if (dtype == SLH_F32) {
+      ENSURE(c, c->Xb, (size_t)c->N * c->D * sizeof(uint16_t));
+      xb = P<uint16_t>(c->Xb);
+    }
+    ENSURE(c, c->rsu, (size_t)c->n_win * G * 2 * c->D * sizeof(double));
+    HIP_TRY(c, launch_route_norm_scores(X, dtype == SLH_BF16 ? 0 : 1, ldx, (int)c->n_win, (int)L,
+                                        (int)c->D, (int)c->m, c->gauss, P<double>(c->nrm2_fm),
+                                        P<double>(c->nrm_x), P<double>(c->inv_x),
+                                        P<float>(c->rowscale), xb, P<double>(c->rsu),
+                                        P<double>(c->rpart), P<double>(c->scores), c->stream));
+    c->norms_of = X;
+  } else {
+    if ((rc = prep_norms(c, X, dtype, ldx))) return rc;
+    HIP_TRY(c, launch_route_scores(X, dtype == SLH_BF16 ? 0 : 1, ldx, P<double>(c->inv_x),
+                                   (int)c->n_win, (int)L, (int)c->D, P<double>(c->rpart),
+                                   P<double>(c->scores), c->stream));
+  }
   std::vector<double> sc((size_t)c->n_win);
   HIP_TRY(c, hipMemcpyAsync(sc.data(), c->scores.p, sc.size() * sizeof(double),
                             hipMemcpyDeviceToHost, c->stream));

@@ -139,6 +139,14 @@ hipError_t launch_merge(const MergeWS& w, const void* X, int dtype, int64_t ldx,
 // ---- adaptive routing (k_route.hip) ----
 // inv_x: 1 / |x_i| per row (0 for a zero row); part: n_win * route_slices(D) * 2
 int route_slices(int D);
+// fused row norms + scores (one read of X) for D <= 4096: the row-norm kernel's
+// outputs for the n_win * L rows plus the scores; psu: n_win * G * 2 * D doubles
+// with G = route_norm_groups(L, D) (0: not available, use the two kernels)
+int route_norm_groups(int L, int D);
+hipError_t launch_route_norm_scores(const void* X, int dtype, int64_t ldx, int n_win, int L,
+                                    int D, int m, int gauss, double* nrm2_fm, double* nrm_x,
+                                    double* inv_x, float* rowscale, uint16_t* Xb, double* psu,
+                                    double* part, double* scores, hipStream_t s);
 hipError_t launch_route_scores(const void* X, int dtype, int64_t ldx, const double* inv_x,
                                int n_win, int L, int D, double* part, double* scores,
                                hipStream_t s);

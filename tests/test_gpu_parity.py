@@ -209,6 +209,28 @@ def test_adaptive_literal_threshold_routes_all_to_chunk():
     PR.compare(o, g, 256)
 
 
+@pytest.mark.parametrize("case", ["bf16_fused", "f32_fused", "bf16_wide"])
+def test_router_scores_both_paths(case):
+    """Eq. 8 scores and routes against the oracle on both implementations: the
+    fused row-norm + score kernel (D <= 4096, bf16 and fp32 X) and the separate
+    row-norm and score kernels (D > 4096); scores within 1e-9, routes equal, and
+    the compressed output compared as everywhere else."""
+    D = {"bf16_fused": 512, "f32_fused": 512, "bf16_wide": 4104}[case]
+    x = "f32" if case == "f32_fused" else "bf16"
+    L, nw = 128, 6
+    inp = _custom(f"rt_{case}", nw * L, D, 256, 16, 8, 6, x=x)
+    Xs = [inp.x_float(slice(w * L, (w + 1) * L)) for w in range(nw)]
+    so = np.array([O.redundancy_score(xw) for xw in Xs])
+    srt = np.sort(so)[::-1]
+    tau = 0.5 * (srt[2] + srt[3])
+    _say(f"[router] {case} D={D} scores {np.round(so, 4)} tau={tau:.5f}")
+    g = PR.run_gpu(inp, n_it=16, window=L, rho=4.0, tau=tau)
+    assert np.max(np.abs(g.scores - so)) < 1e-9
+    o = PR.run_oracle(inp, n_it=16, window=L, rho=4.0, tau=tau)
+    assert np.array_equal(g.route, o.route) and int(g.route.sum()) == 3
+    PR.compare(o, g, L)
+
+
 # ------------------------------------------------------------------ edge cases
 def test_identical_rows_break_down():
     """Identical rows: Phi Phi^T = |phi|^2 11^T has rank one, so Lanczos breaks
