@@ -93,14 +93,14 @@ __global__ __launch_bounds__(256) void k_route_part(const void* __restrict__ X, 
   }
 }
 
-// Fused row norms and router partials for D <= 2048 CPT (one read of X for
-// both): workgroup (window, group of RT_RB rows) covers every column, thread t
-// columns 8 t + 2048 c (c < CPT).  Rows go R at a time (the next R in flight):
-// each thread's share of |x|^2 is summed over the workgroup in a fixed order
-// (wave butterfly, then the 4 waves in order, through a double-buffered LDS
-// slot: one barrier per R rows); the row's outputs are those of the row-norm
-// kernel (|x|^2 of the bf16 values, |x|, 1 / |x|, the feature-map scale and,
-// for fp32 X, the bf16 copy); S and U are accumulated for the thread's columns
+// Fused row norms and router partials for D <= 512 NW CPT (one read of X for
+// both): workgroup (window, group of RT_RB rows) of NW waves covers every
+// column, thread t columns 8 t + 512 NW c (c < CPT).  Rows go R at a time (the next R in
+// flight): each thread's share of |x|^2 is summed over the workgroup in a
+// fixed order (wave butterfly, then the NW waves in order, through a
+// double-buffered LDS slot: one barrier per R rows); the row's outputs are those of the row-norm
+// kernel (|x|^2 of the bf16 values, |x|, 1 / |x|, the feature-map scale, taken
+// after the row loop from |x|^2 kept in LDS, and, for fp32 X, the bf16 copy); S and U are accumulated for the thread's columns
 // and written as the group's partial vectors, added over the groups in order
 // by k_route_su.
 constexpr int RT_RB = 256;                     // rows per workgroup
@@ -138,8 +138,8 @@ __device__ __forceinline__ void rt_unpack(const RtRaw<DT>& r, float (&x)[8]) {
   }
 }
 
-template <int DT, int CPT>
-__global__ __launch_bounds__(256) void k_route_norm(
+template <int DT, int NW, int CPT>
+__global__ __launch_bounds__(64 * NW) void k_route_norm(
     const void* __restrict__ X, int64_t ldx, int L, int D, double inv2sqrtD, double sqrt2m,
     int gauss, double* __restrict__ nrm2_fm, double* __restrict__ nrm_x,
     double* __restrict__ inv_x, float* __restrict__ rowscale, uint16_t* __restrict__ Xb,
@@ -154,7 +154,7 @@ __global__ __launch_bounds__(256) void k_route_norm(
   bool cin[CPT];
 #pragma unroll
   for (int c = 0; c < CPT; ++c) {
-    const int c8 = 8 * tid + 2048 * c;
+    const int c8 = 8 * tid + 512 * NW * c;
     cin[c] = c8 < D;
     col[c] = min(c8, D - 8);
   }
@@ -163,7 +163,8 @@ __global__ __launch_bounds__(256) void k_route_norm(
   for (int c = 0; c < CPT; ++c)
 #pragma unroll
     for (int k = 0; k < 8; ++k) S[c][k] = U[c][k] = 0.0;
-  __shared__ double red[2][4][R * NV];
+  __shared__ double red[2][NW][R * NV];
+  __shared__ double sq_l[RT_RB];
   RtRaw<DT> rc[R][CPT], rn[R][CPT];
   auto load = [&](RtRaw<DT> (&dst)[R][CPT], int b) {
 #pragma unroll
@@ -210,8 +211,12 @@ __global__ __launch_bounds__(256) void k_route_norm(
     }
     __syncthreads();
 #pragma unroll
-    for (int v = 0; v < R * NV; ++v)
-      q[v] = (red[par][0][v] + red[par][1][v]) + (red[par][2][v] + red[par][3][v]);
+    for (int v = 0; v < R * NV; ++v) {
+      double t = 0.0;
+#pragma unroll
+      for (int w8 = 0; w8 < NW; ++w8) t += red[par][w8][v];
+      q[v] = t;
+    }
     par ^= 1;
 #pragma unroll
     for (int e = 0; e < R; ++e) {
@@ -247,8 +252,7 @@ __global__ __launch_bounds__(256) void k_route_norm(
           nrm2_fm[row] = sfm;
           nrm_x[row] = nx;
           inv_x[row] = inv;
-          const double sc = gauss ? 1.0 : exp(sfm * inv2sqrtD);
-          rowscale[row] = (float)(sc * sqrt2m);
+          sq_l[b + e] = sfm;                       // feature-map scale after the loop
         }
       }
     }
@@ -256,6 +260,12 @@ __global__ __launch_bounds__(256) void k_route_norm(
     for (int e = 0; e < R; ++e)
 #pragma unroll
       for (int c = 0; c < CPT; ++c) rc[e][c] = rn[e][c];
+  }
+  // feature-map scales of the group's rows (the exp kept out of the row loop)
+  __syncthreads();
+  for (int r = tid; r < nrow; r += 64 * NW) {
+    const double sc = gauss ? 1.0 : exp(sq_l[r] * inv2sqrtD);
+    rowscale[row0 + r] = (float)(sc * sqrt2m);
   }
   // partial vectors of the group: psu[((win G + g) 2 + {0: S, 1: U}) D + col]
   double* ps = psu + ((int64_t)win * G + g) * 2 * D;
@@ -313,6 +323,19 @@ int route_slices(int D) { return (D + RT_COLS - 1) / RT_COLS; }
 
 int route_norm_groups(int L, int D) { return D <= 4096 ? (L + RT_RB - 1) / RT_RB : 0; }
 
+template <int NW, int CPT>
+static void launch_route_norm(int dtype, dim3 grid, hipStream_t s, const void* X, int64_t ldx,
+                              int L, int D, double inv2sqrtD, double sqrt2m, int gauss,
+                              double* nrm2_fm, double* nrm_x, double* inv_x, float* rowscale,
+                              uint16_t* Xb, double* psu) {
+  if (dtype == 0)
+    hipLaunchKernelGGL((k_route_norm<0, NW, CPT>), grid, dim3(64 * NW), 0, s, X, ldx, L, D, inv2sqrtD,
+                       sqrt2m, gauss, nrm2_fm, nrm_x, inv_x, rowscale, Xb, psu);
+  else
+    hipLaunchKernelGGL((k_route_norm<1, NW, CPT>), grid, dim3(64 * NW), 0, s, X, ldx, L, D, inv2sqrtD,
+                       sqrt2m, gauss, nrm2_fm, nrm_x, inv_x, rowscale, Xb, psu);
+}
+
 hipError_t launch_route_norm_scores(const void* X, int dtype, int64_t ldx, int n_win, int L,
                                     int D, int m, int gauss, double* nrm2_fm, double* nrm_x,
                                     double* inv_x, float* rowscale, uint16_t* Xb, double* psu,
@@ -323,22 +346,13 @@ hipError_t launch_route_norm_scores(const void* X, int dtype, int64_t ldx, int n
   if (G < 1 || D % 8 != 0 || D < 8) return hipErrorInvalidValue;
   const double inv2sqrtD = 1.0 / (2.0 * sqrt((double)D));
   const double sqrt2m = sqrt(2.0 / (double)m);
-  const dim3 grid(n_win, G), blk(256);
-  if (dtype == 0) {
-    if (D <= 2048)
-      hipLaunchKernelGGL((k_route_norm<0, 1>), grid, blk, 0, s, X, ldx, L, D, inv2sqrtD, sqrt2m,
-                         gauss, nrm2_fm, nrm_x, inv_x, rowscale, Xb, psu);
-    else
-      hipLaunchKernelGGL((k_route_norm<0, 2>), grid, blk, 0, s, X, ldx, L, D, inv2sqrtD, sqrt2m,
-                         gauss, nrm2_fm, nrm_x, inv_x, rowscale, Xb, psu);
-  } else {
-    if (D <= 2048)
-      hipLaunchKernelGGL((k_route_norm<1, 1>), grid, blk, 0, s, X, ldx, L, D, inv2sqrtD, sqrt2m,
-                         gauss, nrm2_fm, nrm_x, inv_x, rowscale, Xb, psu);
-    else
-      hipLaunchKernelGGL((k_route_norm<1, 2>), grid, blk, 0, s, X, ldx, L, D, inv2sqrtD, sqrt2m,
-                         gauss, nrm2_fm, nrm_x, inv_x, rowscale, Xb, psu);
-  }
+  const dim3 grid(n_win, G);
+  // up to 2048 columns one chunk per thread on D / 512 waves; wider rows two
+  // chunks on 4 waves (measured faster than one chunk on 8 waves at D = 4096)
+  if (D <= 512) launch_route_norm<1, 1>(dtype, grid, s, X, ldx, L, D, inv2sqrtD, sqrt2m, gauss, nrm2_fm, nrm_x, inv_x, rowscale, Xb, psu);
+  else if (D <= 1024) launch_route_norm<2, 1>(dtype, grid, s, X, ldx, L, D, inv2sqrtD, sqrt2m, gauss, nrm2_fm, nrm_x, inv_x, rowscale, Xb, psu);
+  else if (D <= 2048) launch_route_norm<4, 1>(dtype, grid, s, X, ldx, L, D, inv2sqrtD, sqrt2m, gauss, nrm2_fm, nrm_x, inv_x, rowscale, Xb, psu);
+  else launch_route_norm<4, 2>(dtype, grid, s, X, ldx, L, D, inv2sqrtD, sqrt2m, gauss, nrm2_fm, nrm_x, inv_x, rowscale, Xb, psu);
   const int ncs = route_slices(D);
   hipLaunchKernelGGL(k_route_su, dim3(n_win, ncs), dim3(64), 0, s, psu, G, D, part);
   hipLaunchKernelGGL(k_route_final, dim3(n_win), dim3(64), 0, s, part, ncs, L, scores);
