@@ -2,8 +2,8 @@
 // ordering by representative position).
 //
 // book      one workgroup per window.  Windows of up to 16384 tokens are sorted
-//           in one block (k_mg_book_lds: bitonic network on (code, token)
-//           keys in registers, wave shuffles and LDS);
+//           in one block (k_mg_book_lds: LSD radix sort of (code, token) keys
+//           by code in LDS, 8 bits per pass, ranks by ballot matching);
 //           longer ones use global memory.  Spectral windows: stable LSD radix sort
 //           of (code, token) by code with 8-bit digits (histogram, scan and a
 //           stable scatter whose in-wave ranks come from ballot matching), so
@@ -181,108 +181,35 @@ __global__ __launch_bounds__(1024) void k_mg_book(MergeWS w) {
 
 // Book-keeping of a window of L <= 16384 tokens in one 1024-thread block: sort
 // the keys (code << tb) | local token (tb = log2 P, P = L rounded up to a power
-// of two, padded with all-ones keys), which orders each bucket's members by
-// token; flag each bucket's last member, rank the representatives by an
-// exclusive scan over tokens, and give every sorted position its bucket's rank.
-// Same outputs as k_mg_book.
+// of two) by code, stably, so each bucket's members stay in token order; flag
+// each bucket's last member, rank the representatives by an exclusive scan
+// over tokens, and give every sorted position its bucket's rank.  Same outputs
+// as k_mg_book.
 //
-// The P' = max(P, 1024) = 1024 E keys are held E per thread in sorted-position
-// order (thread t: positions t E .. t E + E - 1).  Bitonic network: exchanges
-// between positions less than E apart stay in registers, up to 64 E apart go
-// between lanes (DPP moves for lane distances up to 8, a swizzle for 16, a
-// permute for 32), and only farther ones (10 of the 91 steps at P = 8192)
-// through LDS and a barrier.  A
-// bucket's last member is found from the next position's code (a neighbour
-// shuffle), and each position's bucket end by a reverse scan over the block.
-// Dynamic LDS: P' + P' / 32 exchange words + L ranks.
-__device__ __forceinline__ int mg_pad(int i) { return i + (i >> 5); }
-
-// x from lane (lane ^ LM): DPP moves for LM <= 8 (quad permutes, and the row /
-// half-row mirrors i -> i ^ 15, i ^ 7 composed with them), a bit-mode swizzle
-// within 32 lanes for 16, a permute through the LDS crossbar for 32
-template <int LM>
-__device__ __forceinline__ uint32_t mg_xor_lane(uint32_t x) {
-  const int v = (int)x;
-  if constexpr (LM == 1) return (uint32_t)__builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false);
-  else if constexpr (LM == 2) return (uint32_t)__builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false);
-  else if constexpr (LM == 4)
-    return (uint32_t)__builtin_amdgcn_mov_dpp(__builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, false),
-                                              0x1B, 0xF, 0xF, false);
-  else if constexpr (LM == 8)
-    return (uint32_t)__builtin_amdgcn_mov_dpp(__builtin_amdgcn_mov_dpp(v, 0x140, 0xF, 0xF, false),
-                                              0x141, 0xF, 0xF, false);
-  else if constexpr (LM == 16) return (uint32_t)__builtin_amdgcn_ds_swizzle(v, 0x401F);
-  else return (uint32_t)__shfl_xor(v, LM, 64);
-}
-
-// one bitonic step at distance j = LM E (partner lane ^ LM, same slot)
-template <int E, int LM>
-__device__ __forceinline__ void mg_step_lane(uint32_t (&v)[E], int k) {
-  const int tid = threadIdx.x;
-  constexpr int j = LM * E;
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    const int i = tid * E + e;
-    const uint32_t q = mg_xor_lane<LM>(v[e]);
-    const bool keep_min = ((i & j) == 0) == ((i & k) == 0);
-    v[e] = keep_min ? min(v[e], q) : max(v[e], q);
-  }
-}
-
-template <int E>
-__device__ __forceinline__ void mg_bitonic_reg(uint32_t (&v)[E], uint32_t* xs, int Pp) {
-  const int tid = threadIdx.x;
-  for (int k = 2; k <= Pp; k <<= 1) {
-    int j = k >> 1;
-    for (; j >= 64 * E; j >>= 1) {                 // partner in another wave: LDS
-#pragma unroll
-      for (int e = 0; e < E; ++e) xs[mg_pad(tid * E + e)] = v[e];
-      __syncthreads();
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const int i = tid * E + e;
-        const uint32_t q = xs[mg_pad(i ^ j)];
-        const bool keep_min = ((i & j) == 0) == ((i & k) == 0);
-        v[e] = keep_min ? min(v[e], q) : max(v[e], q);
-      }
-      __syncthreads();
-    }
-    // partner lane tid ^ (j / E), j = k / 2 (or 32 E) down to E
-    if (j >= 32 * E) mg_step_lane<E, 32>(v, k);
-    if (j >= 16 * E) mg_step_lane<E, 16>(v, k);
-    if (j >= 8 * E) mg_step_lane<E, 8>(v, k);
-    if (j >= 4 * E) mg_step_lane<E, 4>(v, k);
-    if (j >= 2 * E) mg_step_lane<E, 2>(v, k);
-    if (j >= E) mg_step_lane<E, 1>(v, k);
-#pragma unroll
-    for (int jj = E / 2; jj >= 1; jj >>= 1) {      // partner in this thread
-      if (jj < k) {
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-          if ((e & jj) == 0) {
-            const int l = e | jj;
-            const bool up = ((tid * E + e) & k) == 0;
-            const uint32_t x = v[e], y = v[l];
-            v[e] = up ? min(x, y) : max(x, y);
-            v[l] = up ? max(x, y) : min(x, y);
-          }
-        }
-      }
-    }
-  }
-}
-
+// Sort: LSD radix on the code, 8 bits per pass (codes have at most 16 bits, so
+// at most two passes), keys in LDS.  Each of the 16 waves owns a contiguous
+// range of positions: it counts its digits into its row of a 16 x 256 table
+// (LDS integer atomics), one scan over (digit, wave) turns the table into
+// output offsets, and a second sweep, 64 positions at a time in order, finds
+// the lanes of each digit (8 ballots); the group's lowest lane takes the
+// group's offsets with one atomic add, and every key goes to that offset plus
+// its rank among the earlier lanes of its group, which keeps the pass stable.  The
+// sorted keys are then held E = max(P, 1024) / 1024 per thread (thread t:
+// positions t E .. t E + E - 1): a bucket's last member is found from the next
+// position's code (a neighbour shuffle), and each position's bucket end by a
+// reverse scan over the block.  Dynamic LDS: two buffers of L keys (the second
+// reused for the token ranks).
 template <int E>
 __global__ __launch_bounds__(1024) void k_mg_book_lds(MergeWS w, int P, int tb) {
   extern __shared__ uint32_t mg_dyn[];
-  const int Pp = 1024 * E;
-  uint32_t* xs = mg_dyn;                               // [Pp + Pp / 32] exchange
-  int* R = (int*)(mg_dyn + Pp + Pp / 32);            // [L] token -> rank
+  const int L = w.L;
+  uint32_t* bufA = mg_dyn;                            // [L]
+  uint32_t* bufB = mg_dyn + L;                        // [L]
+  __shared__ int hw[16][256];                         // per wave: digit counts, then offsets
   __shared__ int wsum[16];
   __shared__ uint32_t wfirst[16];
   __shared__ int wend[16];
   const int win = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int L = w.L;
   const int64_t base = (int64_t)win * L;
   if (!w.route[win]) {
     const int k = w.chunk_k;
@@ -295,13 +222,76 @@ __global__ __launch_bounds__(1024) void k_mg_book_lds(MergeWS w, int P, int tb) 
   }
   (void)P;
   const uint32_t tmask = (1u << tb) - 1u;
+  for (int i = tid; i < L; i += 1024) bufA[i] = (w.codes[base + i] << tb) | (uint32_t)i;
+
+  const int npass = (w.bits + 7) / 8;
+  const int span = (L + 15) / 16;                     // positions per wave
+  const int p0 = min(wave * span, L), p1 = min(p0 + span, L);
+  const uint64_t lt = (1ull << lane) - 1ull;          // lanes below this one
+  uint32_t* src = bufA;
+  uint32_t* dst = bufB;
+  // lanes of this wave whose digit equals this lane's (valid lanes only)
+  auto match = [&](int d, bool valid) {
+    uint64_t m = __ballot(valid);
+#pragma unroll
+    for (int bit = 0; bit < 8; ++bit) {
+      const bool on = (d >> bit) & 1;
+      const uint64_t bb = __ballot(on);
+      m &= on ? bb : ~bb;
+    }
+    return m;
+  };
+  for (int pass = 0; pass < npass; ++pass) {
+    const int sh = tb + 8 * pass;
+    for (int q = lane; q < 256; q += 64) hw[wave][q] = 0;
+    __syncthreads();                                  // keys of the previous pass complete
+    // counts need no order: integer adds, every chunk's in flight at once
+    for (int i = p0 + lane; i < p1; i += 64) atomicAdd(&hw[wave][(src[i] >> sh) & 255u], 1);
+    __syncthreads();
+    // offsets: digits in order, waves in order within a digit
+    int cnt[16], tot = 0;
+    if (tid < 256) {
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        cnt[q] = hw[q][tid];
+        tot += cnt[q];
+      }
+    }
+    int total;
+    const int incl = block_incl_scan_1024(tid < 256 ? tot : 0, wsum, total);
+    if (tid < 256) {
+      int off = incl - tot;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        hw[q][tid] = off;
+        off += cnt[q];
+      }
+    }
+    __syncthreads();
+    for (int c0 = p0; c0 < p1; c0 += 64) {
+      const int i = c0 + lane;
+      const bool valid = i < p1;
+      const uint32_t k = src[min(i, L - 1)];
+      const int d = (int)((k >> sh) & 255u);
+      const uint64_t m = match(d, valid);
+      int off = 0;
+      if (valid && (m & lt) == 0)                     // the group's lowest lane
+        off = atomicAdd(&hw[wave][d], __popcll(m));
+      off = __shfl(off, (__ffsll((long long)m) - 1) & 63, 64);
+      if (valid) dst[off + __popcll(m & lt)] = k;
+    }
+    uint32_t* t = src;
+    src = dst;
+    dst = t;
+  }
+  __syncthreads();                                    // sorted keys in src
+  int* R = (int*)dst;                                 // [L] token -> rank
   uint32_t v[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) {
-    const int i = tid * E + e;
-    v[e] = (i < L) ? ((w.codes[base + i] << tb) | (uint32_t)i) : 0xFFFFFFFFu;
+    const int pos = tid * E + e;
+    v[e] = (pos < L) ? src[pos] : 0xFFFFFFFFu;
   }
-  mg_bitonic_reg<E>(v, xs, Pp);
 
   // run ends: position s < L ends its bucket when s = L - 1 or the next code differs
   if (lane == 0) wfirst[wave] = v[0];
@@ -1048,7 +1038,7 @@ hipError_t launch_merge(const MergeWS& w, const void* X, int dtype, int64_t ldx,
       ++tb;
     }
     const int Pp = P > 1024 ? P : 1024;
-    const size_t bytes = (size_t)(Pp + Pp / 32) * 4 + (size_t)w.L * 4;
+    const size_t bytes = (size_t)2 * w.L * 4;
     const void* kf = (Pp == 1024)   ? (const void*)k_mg_book_lds<1>
                      : (Pp == 2048) ? (const void*)k_mg_book_lds<2>
                      : (Pp == 4096) ? (const void*)k_mg_book_lds<4>
