@@ -6,7 +6,8 @@
 //
 // Tiling: a workgroup of WGM x WGN waves owns a BM x BN output tile (256 x 256
 // with 2 x 4 waves, two waves per SIMD so that one issues MFMAs while the other
-// waits on memory; 128 x 128 with 2 x 2 waves for small problems); each wave
+// waits on memory; 128 x 128, 64 x 128 or 64 x 64 when the large tiles would
+// leave CUs idle, see launch_featmap); each wave
 // owns (BM/WGM) x (BN/WGN) as 32x32 MFMA tiles.  K advances FM_BK at a time
 // through FM_NS LDS stages filled by direct global-to-LDS loads issued
 // FM_NS - 1 stages ahead of the MFMAs that consume them (no register staging),
@@ -378,22 +379,34 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_featmap(FeatmapArgs a) {
 
 
 
-hipError_t launch_featmap(const FeatmapArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+template <int BM, int BN, int WGM, int WGN>
+static void launch_tiles(const FeatmapArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  const int64_t t = ((a.n_rows + BM - 1) / BM) * (a.m / BN);
+  auto k = k_featmap<BM, BN, WGM, WGN>;
+  const dim3 blk(64 * WGM * WGN);
+  if (e0) hipExtLaunchKernelGGL(k, dim3((unsigned)t), blk, 0, s, e0, e1, 0, a);
+  else hipLaunchKernelGGL(k, dim3((unsigned)t), blk, 0, s, a);
+}
+
+hipError_t launch_featmap(const FeatmapArgs& a, int n_cu, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   (void)hipGetLastError();
   if (a.n_rows <= 0) return hipSuccess;
-  // 256 x 256 tiles when that still gives at least one tile per CU, else 128 x 128
-  int64_t t256 = ((a.n_rows + 255) / 256) * (a.m / FM_BIG_BN);
-  if (a.m % FM_BIG_BN == 0 && t256 >= 256) {
-    auto k = k_featmap<256, FM_BIG_BN, FM_BIG_WGM, FM_BIG_WGN>;
-    const dim3 blk(64 * FM_BIG_WGM * FM_BIG_WGN);
-    if (e0) hipExtLaunchKernelGGL(k, dim3((unsigned)t256), blk, 0, s, e0, e1, 0, a);
-    else hipLaunchKernelGGL(k, dim3((unsigned)t256), blk, 0, s, a);
-  } else {
-    int64_t t128 = ((a.n_rows + 127) / 128) * (a.m / 128);
-    auto k = k_featmap<128, 128, 2, 2>;
-    if (e0) hipExtLaunchKernelGGL(k, dim3((unsigned)t128), dim3(256), 0, s, e0, e1, 0, a);
-    else hipLaunchKernelGGL(k, dim3((unsigned)t128), dim3(256), 0, s, a);
-  }
+  // Tile shape by how the tiles fill the CUs.  256 x 256 (eight waves) when
+  // every CU gets a tile; below that, the largest of 128 x 128 (eight waves),
+  // 64 x 128 (four) and 64 x 64 (two) that still gives every CU two tiles, so
+  // that two workgroups share each CU's MFMA pipes and cover each other's
+  // memory waits (measured at 4096 x 4096 x 1024, 8192 x 3584 x 256 and
+  // 4000 x 3584 x 2048: the rule picks the fastest shape or one within 2%).
+  const int64_t rb = (a.n_rows + 63) / 64, rb2 = (a.n_rows + 127) / 128;
+  const int64_t t256 = ((a.n_rows + 255) / 256) * (a.m / FM_BIG_BN);
+  if (a.m % FM_BIG_BN == 0 && t256 >= n_cu)
+    launch_tiles<256, FM_BIG_BN, FM_BIG_WGM, FM_BIG_WGN>(a, s, e0, e1);
+  else if (rb2 * (a.m / 128) >= 2LL * n_cu)
+    launch_tiles<128, 128, 2, 4>(a, s, e0, e1);
+  else if (rb * (a.m / 128) >= 2LL * n_cu)
+    launch_tiles<64, 128, 1, 4>(a, s, e0, e1);
+  else
+    launch_tiles<64, 64, 1, 2>(a, s, e0, e1);
   return hipGetLastError();
 }
 

@@ -623,7 +623,7 @@ int slh_feature_map(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx) {
   a.D = (int)c->D;
   a.ldw = (int)(((c->D + 63) / 64) * 64);
   a.m = (int)c->m;
-  HIP_TRY(c, launch_featmap(a, c->stream, c->timing ? c->ev[0] : nullptr,
+  HIP_TRY(c, launch_featmap(a, c->n_cu, c->stream, c->timing ? c->ev[0] : nullptr,
                             c->timing ? c->ev[1] : nullptr));
   if (c->normalize && c->n_act > 0) {
     const int G = normalise_groups(c->n_act, (int)L, (int)c->m, c->n_cu);

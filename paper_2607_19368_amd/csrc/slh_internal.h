@@ -28,8 +28,9 @@ struct FeatmapArgs {
   int D, m;
   int ldw;                // D rounded up to a multiple of 64
 };
-// e0/e1 (may be NULL): receive the kernel's own start / end timestamps.
-hipError_t launch_featmap(const FeatmapArgs& a, hipStream_t s, hipEvent_t e0 = nullptr,
+// n_cu: compute units of the device (picks the tile shape).  e0/e1 (may be
+// NULL): receive the kernel's own start / end timestamps.
+hipError_t launch_featmap(const FeatmapArgs& a, int n_cu, hipStream_t s, hipEvent_t e0 = nullptr,
                           hipEvent_t e1 = nullptr);
 
 // ---- Lanczos (k_lanczos.hip) ----

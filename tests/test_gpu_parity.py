@@ -41,12 +41,22 @@ def _custom(name, N, D, m, n_it, r, bits, seed=0, x="bf16", vocab=32768):
 
 
 # ------------------------------------------------------------------ feature map
-@pytest.mark.parametrize("case", ["tiny", "ragged", "mistral7b_head"])
+# tiles used at 256 CUs: tiny, ragged, mistral7b_head -> 64 x 64; tiles64x128 ->
+# 64 x 128; tiles128 -> 128 x 128; tiles256 -> 256 x 256 (all with a ragged last
+# row block except tiny)
+@pytest.mark.parametrize("case", ["tiny", "ragged", "mistral7b_head", "tiles64x128", "tiles128",
+                                  "tiles256"])
 def test_feature_map_parity(case):
     if case == "tiny":
         inp = make_inputs("tiny")
     elif case == "ragged":
         inp = _custom("ragged", 1000, 264, 512, 16, 4, 6)
+    elif case == "tiles64x128":
+        inp = _custom("tiles64x128", 4090, 264, 1024, 16, 4, 6)
+    elif case == "tiles128":
+        inp = _custom("tiles128", 4000, 264, 2048, 16, 4, 6)
+    elif case == "tiles256":
+        inp = _custom("tiles256", 8000, 264, 2048, 16, 4, 6)
     else:
         inp = _custom("mistral7b_head", 1536, 4096, 1024, 16, 8, 10)
     wl = inp.workload
