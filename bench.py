@@ -21,12 +21,12 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 
 
-PASS_REPS = 96                   # graph replays of the last step's two passes
+PASS_REPS = 96                   # graph replays of the last step's pass over Phi
 
 
 def measured_traffic(workload):
-    """HBM bytes per pass over Phi from the committed counter summary, if it was
-    taken on the current kernel source and this workload; else None."""
+    """HBM bytes per Lanczos pass (k_lz_step) from the committed counter summary,
+    if it was taken on the current kernel source and this workload; else None."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "lanczos_passes_qwen7b_traffic.md")
     src = os.path.join(ROOT, "paper_2607_19368_amd", "csrc", "k_lanczos.hip")
@@ -208,23 +208,26 @@ def main():
         out["stages_ms"]["ms_per_step_with_events"] = ms2
         if stage_sum["phi_pass_count"] > 0:
             ev_ms = stage_sum["phi_pass_ms_sum"] / stage_sum["phi_pass_count"]
-            # the kernel duration: the last step's two passes replayed 96 times as
+            # the kernel duration: the last step's pass replayed PASS_REPS times as
             # one HIP graph between two events on the context stream (the per-launch
             # event pairs above add a dispatch overhead that varies by machine)
             pass_ms = 1e-3 * P.slh_time_passes(ctx, PASS_REPS)
-            # algorithmic bytes per pass over Phi (either half of the implicit
-            # matvec, Eq. 4): Phi once (4 B/elt) + the L-vector (q in, or u out) +
-            # the m-vector (t out, or t in), fp64, per window
-            alg = n_win * (4.0 * L * wl.m + 8.0 * (L + wl.m))
+            # algorithmic bytes of the pass of step j (both halves of the implicit
+            # matvec of Eq. 4 on one read of Phi, plus the full re-orthogonalisation),
+            # per window: Phi (4 B/elt), t_j in (fp64 m-vector), Q_{j-1} and z1 of
+            # step j-1 in, q_j and z1 out (fp64 L-vectors): 4 L m + 8 m + 8 L (j + 3);
+            # the replayed step is the last, j = n_it - 1
+            j_last = wl.n_it - 1
+            alg = n_win * (4.0 * L * wl.m + 8.0 * wl.m + 8.0 * L * (j_last + 3))
             ach = alg / (pass_ms * 1e-3) / 1e9
             out["roofline"] = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                "frac": ach / HBM_PEAK_GBS, "traffic": measured_traffic(wl.name),
                                "traffic_unit": "HBM bytes per pass (FETCH_SIZE + WRITE_SIZE, "
                                                "copy-calibrated; profiles/lanczos_passes_qwen7b_traffic.md)",
-                               "kernel": "k_lz_phit + k_lz_phiu (t = Phi^T q and u = Phi t)",
+                               "kernel": "k_lz_step (u = Phi t_j, z1, Phi^T z1 partials, h2 partials)",
                                "bytes_per_launch": alg, "avg_launch_ms": pass_ms,
-                               "timing": f"slh_time_passes: {PASS_REPS} x (Phi^T q, Phi t) of the last "
-                                         "step as one HIP graph between two events",
+                               "timing": f"slh_time_passes: {PASS_REPS} x the pass of the last step "
+                                         "as one HIP graph between two events",
                                "avg_launch_ms_events": ev_ms,
                                "frac_events": alg / (ev_ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
             out["stages_ms"]["phi_pass_avg_ms"] = ev_ms

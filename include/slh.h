@@ -255,7 +255,7 @@ int slh_load(slh_ctx *ctx, int32_t which, const void *src, int64_t bytes);
  * Stage timings of the most recent calls, from HIP events on the context
  * stream (requires SLH_OPT_TIMING = 1 before those calls).  Fills up to n of:
  *   [0] feature map ms        [1] Lanczos loop ms (all steps, all windows)
- *   [2] sum of Phi-pass ms     [3] number of Phi passes timed (2 per step)
+ *   [2] sum of Phi-pass ms     [3] number of Phi passes timed (1 per step)
  *   [4] eigensolve + Ritz ms  [5] SimHash ms   [6] merge ms
  *   [7] row normalisation ms (SLH_OPT_NORMALIZE = 1, else 0)
  * Synchronises the stream.
@@ -264,16 +264,18 @@ int slh_stage_times(slh_ctx *ctx, double *ms_out, int32_t n);
 
 /*
  * Duration of one pass over Phi without per-launch events (measurement aid for
- * the matvec of Algorithm 2, A v = Phi (Phi^T v)): the two pass kernels of the
- * final step of the last slh_lanczos call (Phi^T v, then Phi t), with that
- * step's launch configuration and data, are captured reps times as one HIP
+ * the matvec of Algorithm 2, A v = Phi (Phi^T v)): the pass kernel of the final
+ * step of the last slh_lanczos call (u = Phi t_j and the partials of Phi^T z1
+ * on one read of Phi, with the step's re-orthogonalisation work), with that
+ * step's launch configuration and data, is captured reps times as one HIP
  * graph, replayed once untimed and once between two events on the context
- * stream.  us_out: host, 1 double = elapsed microseconds / (2 reps), so gaps
- * between graph nodes are included.  The replays rewrite only the step's pass
- * scratch (partial sums), never Q, T, alpha, beta, the Ritz pairs or codes;
- * windows that broke down early skip their passes as in the loop itself.
- * reps in [1, 4096].  Synchronises the stream.  SLH_ESTATE before slh_lanczos
- * or after a short-window (single-wavefront) Lanczos run, which has no passes.
+ * stream.  us_out: host, 1 double = elapsed microseconds / reps, so gaps
+ * between graph nodes are included.  The replays write their row vectors to
+ * scratch and record no step state: they rewrite only the step's partial sums,
+ * never Q, alpha, beta, the Ritz pairs or codes; windows that broke down early
+ * skip their passes as in the loop itself.  reps in [1, 4096].  Synchronises the
+ * stream.  SLH_ESTATE before slh_lanczos or after a short-window
+ * (single-wavefront) Lanczos run, which has no passes.
  */
 int slh_time_passes(slh_ctx *ctx, int32_t reps, double *us_out);
 

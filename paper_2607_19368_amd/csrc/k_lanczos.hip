@@ -93,6 +93,32 @@ __device__ __forceinline__ double half_sum8_f64(const double (&v)[8]) {
   return y;
 }
 
+// The same over each 16-lane quarter: lane l holds the quarter sum of value
+// index ((l>>3)&1)*4 + ((l>>2)&1)*2 + ((l>>1)&1).
+__device__ __forceinline__ double quarter_sum8_f64(const double (&v)[8]) {
+  const int lane = threadIdx.x & 63;
+  double w[4];
+  const bool b8 = lane & 8;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    double keep = b8 ? v[e + 4] : v[e];
+    double send = b8 ? v[e] : v[e + 4];
+    w[e] = keep + __shfl_xor(send, 8, 64);
+  }
+  double x[2];
+  const bool b4 = lane & 4;
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    double keep = b4 ? w[e + 2] : w[e];
+    double send = b4 ? w[e] : w[e + 2];
+    x[e] = keep + __shfl_xor(send, 4, 64);
+  }
+  const bool b2 = lane & 2;
+  double y = (b2 ? x[1] : x[0]) + __shfl_xor(b2 ? x[0] : x[1], 2, 64);
+  y += __shfl_xor(y, 1, 64);
+  return y;
+}
+
 // Value of v in lane l (l uniform), through the scalar unit.
 __device__ __forceinline__ double readlane_f64(double v, int l) {
   const unsigned long long x = (unsigned long long)__double_as_longlong(v);
@@ -160,343 +186,345 @@ __device__ __forceinline__ void h2_reduce_block(const LanczosWS& w, int a, int j
 }
 
 // ---------------------------------------------------------------------------
-// phit: blocks [0, nx) reduce h2 (k < j) and |z1|^2 of step j-1 over the orth
-// blocks; the rest own (row group rg, 256-column slice sl): each of the 8
-// waves streams rows r0 + wave + 8 q (q < RWA) of the slice, lane = 4 columns
-// (one float4), 8 rows in flight plus the next 8.  Loads are unconditional
-// (row clamped into the group); rows past the group carry weight 0.
+// The pass over Phi.  A block owns RB consecutive rows and all m columns of
+// them, held in registers: 8 waves, wave = (row subset p, 256-column slice sl),
+// sl = wave % ns, p = wave / ns; the WPS = RB / RPW subsets of RPW rows each
+// cover the block's rows (waves with p >= WPS, when ns does not divide 8, take
+// no rows).  Lane = 4 columns (one float4 per row) of the wave's slice.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(512) void k_lz_phit(LanczosWS w, int j) {
-  const int a = blockIdx.y;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int L = w.L, m = w.m, hs = w.ldq + 1;
-  const int nx = (j > 0) ? (j + 15) / 16 + 1 : 0;
-  int g = blockIdx.x;
-  if (g < nx) {
-    if (w.stop[a]) return;
-    h2_reduce_block(w, a, j, g, nx);
-    return;
-  }
-  g -= nx;
-  const int ns = m >> 8;
-  const int sl = g % ns, rg = g / ns;
-  const int r0 = rg * w.RBA;
-  const int r1 = min(L, r0 + w.RBA);
-  const float* base = w.Phi + (int64_t)a * L * m + sl * 256 + 4 * lane;
-  const double* vsrc = (j == 0) ? (w.Q + (int64_t)a * w.ldq * L) : (w.Z1 + (int64_t)a * L);
-  double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-  float4 vc[8], vn[8];
-  double wc, wn;
-  // rows r0 + wave + 8 (8 b + e), e < 8, of batch b; lane e (mod 8) also loads the
-  // weight of row e (0 past the group), broadcast when the batch is consumed
-  auto load8 = [&](float4 (&dst)[8], double& wd, int b) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int i = min(r0 + wave + 8 * (8 * b + e), r1 - 1);
-      dst[e] = *(const float4*)(base + (int64_t)i * m);
-    }
-    const int iw = r0 + wave + 8 * (8 * b + (lane & 7));
-    const double v = vsrc[min(iw, r1 - 1)];
-    wd = (iw < r1) ? v : 0.0;
-  };
-  const int nb = w.RWA / 8;
-  load8(vc, wc, 0);                 // in flight while the stop flag is read
-  if (w.stop[a]) return;
-  for (int b = 0; b < nb; ++b) {
-    if (b + 1 < nb) load8(vn, wn, b + 1);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const double q = readlane_f64(wc, e);
-      s0 = fma((double)vc[e].x, q, s0);
-      s1 = fma((double)vc[e].y, q, s1);
-      s2 = fma((double)vc[e].z, q, s2);
-      s3 = fma((double)vc[e].w, q, s3);
-    }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) vc[e] = vn[e];
-    wc = wn;
-  }
-  __shared__ double cred[8][257];
-  cred[wave][4 * lane + 0] = s0;
-  cred[wave][4 * lane + 1] = s1;
-  cred[wave][4 * lane + 2] = s2;
-  cred[wave][4 * lane + 3] = s3;
-  __syncthreads();
-  if (tid < 256) {
-    double t = 0.0;
-#pragma unroll
-    for (int q = 0; q < 8; ++q) t += cred[q][tid];
-    w.Spart[((int64_t)a * w.GA + rg) * m + sl * 256 + tid] = t;
-  }
+// The float4 of one Phi row as an opaque value at its point of use, so that its
+// conversion to fp64 is not hoisted: otherwise every row of the block is held
+// converted (twice the registers) across the phases that use it.
+__device__ __forceinline__ float4 pin_row(float4 x) {
+  asm volatile("" : "+v"(x.x), "+v"(x.y), "+v"(x.z), "+v"(x.w));
+  return x;
 }
 
-// ---------------------------------------------------------------------------
-// finish: beta_{j-1}, breakdown, and t_j on 16 columns per block (256 threads:
-// 16 columns x 16 partial lanes).  Every load is issued before the first
-// reduction.
-// ---------------------------------------------------------------------------
-// KT = 16-step slots of k per thread: 16 KT >= n_it (fewer registers for short runs)
-template <int KT>
-__global__ __launch_bounds__(256) void k_lz_finish(LanczosWS w, int j) {
-  const int a = blockIdx.y, g = blockIdx.x, tid = threadIdx.x;
-  const int m = w.m, hs = w.ldq + 1;
-  const int cl = tid & 15, pl = tid >> 4;
-  const int c = g * 16 + cl;                   // m is a multiple of 16
-  const double* H2 = w.H2 + (int64_t)a * hs;
-  // The loads of t_k and h2_k (k = pl + 16 e < j <= 16 KT), of the |h2|^2 terms
-  // (k = tid, tid + 256 < j), of |z1|^2 and of the step state are all issued
-  // before the first use, with clamped indices (surplus values are masked), so
-  // the kernel waits on memory once.
-  const int jm = max(j - 1, 0);
-  const double* Ta = w.T + (int64_t)a * w.ldq * m + c;
-  double tv[KT], hv[KT];
+struct StepGeom {
+  int sl, p, rw0;
+  bool rows;
+};
+template <int RB, int RPW>
+__device__ __forceinline__ StepGeom step_geom(int m, int r0) {
+  constexpr int WPS = RB / RPW;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int ns = m >> 8;
+  StepGeom gm;
+  gm.sl = wave % ns;
+  gm.p = wave / ns;
+  gm.rows = gm.p < WPS;
+  gm.rw0 = r0 + gm.p * RPW;
+  return gm;
+}
+
+// Column partials of Phi^T z over the block's rows (z of row rl in zs[rl], 0
+// past L) into Spart[a][g][:]: each wave sums its RPW rows for its 4 columns
+// per lane; the WPS subsets of one slice are combined through cr in a fixed order.
+template <int RB, int RPW>
+__device__ __forceinline__ void step_colsums(const LanczosWS& w, int a, int g, const StepGeom& gm,
+                                             const float4 (&v)[RPW], const double* zs,
+                                             double (*cr)[256]) {
+  constexpr int WPS = RB / RPW;
+  const int lane = threadIdx.x & 63, ns = w.m >> 8;
+  double c[4] = {0.0, 0.0, 0.0, 0.0};
+  if (gm.rows) {
 #pragma unroll
-  for (int e = 0; e < KT; ++e) {
-    const int k = min(pl + 16 * e, jm);
-    tv[e] = Ta[(int64_t)k * m];
-    hv[e] = H2[k];
+    for (int i = 0; i < RPW; ++i) {
+      const double z = zs[gm.p * RPW + i];
+      const float4 x = pin_row(v[i]);
+      c[0] = fma((double)x.x, z, c[0]);
+      c[1] = fma((double)x.y, z, c[1]);
+      c[2] = fma((double)x.z, z, c[2]);
+      c[3] = fma((double)x.w, z, c[3]);
+    }
   }
-  const double hq0 = H2[min(tid, jm)], hq1 = H2[min(tid + 256, jm)];
-  const double z2 = H2[w.ldq];
-  const int stopped = w.stop[a];
-  const double amax = w.amax[a];
-  // partial of Phi^T z1 over row groups pl, pl + 16, ...
-  const double* Sp = w.Spart + (int64_t)a * w.GA * m + c;
-  const int cnt = (w.GA - pl + 15) / 16;
-  const double s = sum_strided(Sp + (int64_t)pl * m, (int64_t)16 * m, cnt > 0 ? cnt : 0);
-  // partial of sum_k h2_k t_k over k = pl, pl + 16, ... < j
-  double corr;
-  {
-    double acc[4] = {0, 0, 0, 0};
+  if (WPS > 1) {
+    if (gm.rows && gm.p > 0) {
 #pragma unroll
-    for (int e = 0; e < KT; ++e)
-      if (pl + 16 * e < j) acc[e & 3] = fma(tv[e], hv[e], acc[e & 3]);
-    corr = (acc[0] + acc[1]) + (acc[2] + acc[3]);
-  }
-  // |h2|^2 partial
-  double hh = 0.0;
-  if (tid < j) hh = fma(hq0, hq0, hh);
-  if (tid + 256 < j) hh = fma(hq1, hq1, hh);
-  if (stopped) return;
-  __shared__ double red[4];
-  __shared__ double sh;
-  __shared__ double rs[16][17], rc[16][17];
-  rs[pl][cl] = s;
-  rc[pl][cl] = corr;
-  double inv = 1.0;
-  if (j > 0) {
-    hh = block_sum_f64(hh, red);               // (its barriers also publish rs / rc)
-    if (tid == 0) {
-      const double b2 = z2 - hh;               // |z1 - Q h2|^2 for orthonormal Q
-      const double beta = b2 > 0.0 ? sqrt(b2) : 0.0;
-      const bool brk = !(beta > w.tol * amax);
-      sh = brk ? 0.0 : beta;
-      if (g == 0) {
-        w.beta[(int64_t)a * w.n_it + j - 1] = beta;
-        if (brk) w.stop[a] = 1;                // n_eff stays j
+      for (int e = 0; e < 4; ++e) cr[(gm.p - 1) * ns + gm.sl][4 * lane + e] = c[e];
+    }
+    __syncthreads();
+    if (gm.rows && gm.p == 0) {
+      for (int q = 1; q < WPS; ++q) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) c[e] += cr[(q - 1) * ns + gm.sl][4 * lane + e];
       }
     }
-    __syncthreads();
-    if (sh == 0.0) return;
-    inv = 1.0 / sh;
-  } else {
-    __syncthreads();
   }
-  if (tid < 16) {
-    double S = 0.0, C = 0.0;
-    for (int p = 0; p < 16; ++p) {
-      S += rs[p][cl];
-      C += rc[p][cl];
-    }
-    w.T[((int64_t)a * w.ldq + j) * m + c] = (j > 0) ? (S - C) * inv : S;
+  if (gm.rows && gm.p == 0) {
+    double* dst = w.Spart + ((int64_t)a * w.G3 + g) * w.m + gm.sl * 256 + 4 * lane;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) dst[e] = c[e];
   }
 }
 
-// ---------------------------------------------------------------------------
-// phiu: blocks [0, nx) form h1_k = t_k^T t_j, k <= j (one wave per k); the
-// rest own (row group, 256-column slice) exactly as in phit and write the
-// slice's partial of u = Phi t_j for each row (Upart[slice][row]): lane = 4
-// columns, the 8 rows of a batch are summed over the wave in one butterfly.
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(512) void k_lz_phiu(LanczosWS w, int j) {
-  const int a = blockIdx.y;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+// Initial pass: partials of Phi^T q_0 (t_0 before reduction).
+template <int RB, int RPW>
+__global__ __launch_bounds__(512) void k_lz_init(LanczosWS w) {
+  constexpr int WPS = RB / RPW;
+  const int a = blockIdx.y, g = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
   const int L = w.L, m = w.m;
-  const double* Ta = w.T + (int64_t)a * w.ldq * m;
-  const double* tj = Ta + (int64_t)j * m;
-  const int nx = (j + 8) / 8;
-  int g = blockIdx.x;
-  if (g < nx) {
-    if (w.stop[a]) return;
-    const int k = g * 8 + wave;
-    if (k > j) return;
-    const double* tk = Ta + (int64_t)k * m;
-    double acc[4] = {0, 0, 0, 0};
-    for (int c0 = 0; c0 < m; c0 += 256) {      // m is a multiple of 256
+  const int r0 = g * RB;
+  const StepGeom gm = step_geom<RB, RPW>(m, r0);
+  const double q0 = (tid < RB) ? w.Q[(int64_t)a * w.ldq * L + min(r0 + tid, L - 1)] : 0.0;
+  float4 v[RPW];
+  if (gm.rows) {
+    const float* base = w.Phi + (int64_t)a * L * m + gm.sl * 256 + 4 * lane;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) acc[e] = fma(tk[c0 + 64 * e + lane], tj[c0 + 64 * e + lane], acc[e]);
-    }
-    double v = (acc[0] + acc[1]) + (acc[2] + acc[3]);
-    v = wave_sum_f64(v);
-    if (lane == 0) w.H1[(int64_t)a * (w.ldq + 1) + k] = v;
-    return;
+    for (int i = 0; i < RPW; ++i) v[i] = *(const float4*)(base + (int64_t)min(gm.rw0 + i, L - 1) * m);
   }
-  g -= nx;
-  const int ns = m >> 8;
-  const int sl = g % ns, rg = g / ns;
-  const int r0 = rg * w.RBA;
-  const int r1 = min(L, r0 + w.RBA);
-  const float* base = w.Phi + (int64_t)a * L * m + sl * 256 + 4 * lane;
-  float4 vc[8], vn[8];
-  auto load8 = [&](float4 (&dst)[8], int b) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int i = min(r0 + wave + 8 * (8 * b + e), r1 - 1);
-      dst[e] = *(const float4*)(base + (int64_t)i * m);
-    }
-  };
-  const int nb = w.RWA / 8;
-  load8(vc, 0);                     // in flight while t_j and the stop flag are read
-  const double* tc = tj + sl * 256 + 4 * lane;
-  const double t0 = tc[0], t1 = tc[1], t2 = tc[2], t3 = tc[3];
-  if (w.stop[a]) return;
-  double* up = w.Upart + ((int64_t)a * ns + sl) * L;
-  const int idx = ((lane >> 5) & 1) * 4 + ((lane >> 4) & 1) * 2 + ((lane >> 3) & 1);
-  for (int b = 0; b < nb; ++b) {
-    if (b + 1 < nb) load8(vn, b + 1);
-    double p[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      double d = (double)vc[e].x * t0;
-      d = fma((double)vc[e].y, t1, d);
-      d = fma((double)vc[e].z, t2, d);
-      p[e] = fma((double)vc[e].w, t3, d);
-    }
-    const double tot = wave_sum8_f64(p);
-    const int i = r0 + wave + 8 * (8 * b + idx);
-    if ((lane & 7) == 0 && i < r1) up[i] = tot;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) vc[e] = vn[e];
-  }
+  __shared__ double zs[RB];
+  __shared__ double cr[WPS > 1 ? 7 : 1][256];
+  if (tid < RB) zs[tid] = (r0 + tid < L) ? q0 : 0.0;
+  __syncthreads();
+  step_colsums<RB, RPW>(w, a, g, gm, v, zs, cr);
 }
 
 // ---------------------------------------------------------------------------
-// orth on 32 rows per block (256 threads = 32 rows x 8 k-groups).  Thread
-// (row, kg) loads Q[k][row] for k = kg + 8 t (k < j) once, into registers, and
-// uses them for the q_j update, for z1 = u - Q h1 and for the h2 partials.
+// One Lanczos step j on the block's RB rows, with one read of their Phi rows.
+// From the previous step: z1 (row space), h2 = Q_{j-1}^T z1 and |z1|^2 (reduced),
+// and t~ = Phi^T z1 / |z1| with alpha~ = |t~|^2 (feature space).
+//   beta_{j-1} = |z1 - Q_{j-1} h2| = sqrt(|z1|^2 - |h2|^2) (Q orthonormal), and
+//     the breakdown test;
+//   q_j = (z1 - Q_{j-1} h2) / beta_{j-1}     (second Gram-Schmidt pass of step
+//     j-1, in row space; stored as Q[j]);
+//   u = A q_j from the row dots Phi t~ = A z1 / |z1| and the Lanczos relation
+//     A Q_{j-1} = Q_{j-1} T_{j-1} + beta_{j-1} q_j e^T (T_{j-1} tridiagonal of
+//     the alphas and betas so far):
+//       u = (|z1| Phi t~ - Q_{j-1} g - beta_{j-1} h2_{j-1} q_j) / beta_{j-1},
+//       g = T_{j-1} h2;
+//     alpha_j = q_j^T A q_j = (|z1|^2 alpha~ - h2^T g) / beta_{j-1}^2 - 2 h2_{j-1};
+//     (without this correction the h2 of each step would re-enter the next one
+//     amplified by |A| / beta);
+//   z1 = u - alpha_j q_j - beta_{j-1} q_{j-1}   (the three-term recurrence);
+//   partials of Phi^T z1 (column sums), of h2 = Q_j^T z1 and of |z1|^2.
+// Row-space work: thread = (row rl < RB, k-group kg < KG = 512 / RB); MAXT =
+// slots of k = kg + KG t per thread, KG MAXT >= n_it.
 // ---------------------------------------------------------------------------
-// MAXT = 8-step slots of k per thread: 8 MAXT >= n_it, MAXT a multiple of 8
-// (fewer registers for short runs)
-template <int MAXT>
-__global__ __launch_bounds__(256) void k_lz_orth(LanczosWS w, int j) {
-  static_assert(MAXT % 8 == 0, "slots are reduced 8 at a time");
+// dry = 1 (timing replays): q_j and z1 go to Zs, no bookkeeping, no breakdown exit.
+template <int RB, int RPW, int MAXT>
+__global__ __launch_bounds__(512) void k_lz_step(LanczosWS w, int j, int dry) {
+  static_assert(RB == 16 || RB == 32, "rows per block");
+  constexpr int WPS = RB / RPW, KG = 512 / RB;
   const int a = blockIdx.y, g = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63;
-  const int L = w.L, hs = w.ldq + 1;
-  const int rl = tid & 31, kg = tid >> 5;
-  const int r0 = g * 32;
-  const int i = r0 + rl;
-  const int ic = min(i, L - 1);
+  const int L = w.L, m = w.m, hs = w.ldq + 1, nbr = m >> 4;
+  const int r0 = g * RB;
+  const StepGeom gm = step_geom<RB, RPW>(m, r0);
+  const int rl = tid & (RB - 1), kg = tid / RB;   // row-space work: (row, k-group)
+  const int ir = r0 + rl, irc = min(ir, L - 1);
   const double* Qa = w.Q + (int64_t)a * w.ldq * L;
-  const int nt = (j - kg + 7) / 8;             // k = kg + 8 t < j
-  // every global load of the kernel is issued here, before the first use
-  // (indices clamped; values that are not needed are never used)
   const int jm = max(j - 1, 0);
-  double qv[MAXT];
+  // Every small load is issued before the Phi rows, so waiting for them leaves
+  // the Phi loads in flight.  Indices are clamped; surplus values are unused.
+  double qv[MAXT];                             // Q[k][row], k = kg + KG t < j
 #pragma unroll
   for (int t = 0; t < MAXT; ++t)
-    if (8 * t < j) qv[t] = Qa[(int64_t)min(kg + 8 * t, jm) * L + ic];
-  const double* H1a = w.H1 + (int64_t)a * hs;
+    if (KG * t < j) qv[t] = Qa[(int64_t)min(kg + KG * t, jm) * L + irc];
   const double* H2a = w.H2 + (int64_t)a * hs;
-  const double h1v0 = H1a[min(tid, j)], h1v1 = H1a[min(tid + 256, j)];
-  const double h2v0 = H2a[min(tid, jm)], h2v1 = H2a[min(tid + 256, jm)];
-  const int ns = w.m >> 8;                     // <= 8 column slices
-  const double* up = w.Upart + (int64_t)a * ns * L + ic;
-  double us[8];
-#pragma unroll
-  for (int sl = 0; sl < 8; ++sl) us[sl] = up[(int64_t)min(sl, ns - 1) * L];
-  const double zi = w.Z1[(int64_t)a * L + ic];
-  const double bet = w.beta[(int64_t)a * w.n_it + jm];
-  const double q0 = Qa[ic];
+  const double h2v = H2a[min(tid, jm)];        // n_it <= 512
+  const double z2 = H2a[w.ldq];
+  const double apv = w.Apart[(int64_t)a * nbr + min(tid, nbr - 1)];
+  const double zp = w.Z1[(int64_t)a * L + irc];
+  const double qp = Qa[(int64_t)jm * L + irc];  // q_{j-1}, or q_0 when j = 0
+  const double alv = w.alpha[(int64_t)a * w.n_it + min(tid, jm)];
+  const double bev = w.beta[(int64_t)a * w.n_it + min(tid, jm)];
   const int stopped = w.stop[a];
-  const double amax0 = (j > 0) ? w.amax[a] : 0.0;
-  __shared__ double h1[264], h2[264];
-  __shared__ double rq[8][33], rz[8][33];
-  __shared__ double sz[32], sq[32];
-  double ui = 0.0;
+  const double amax0 = w.amax[2 * a + (j & 1)];   // max |alpha| before step j
+  double tv[4] = {0.0, 0.0, 0.0, 0.0};
+  float4 v[RPW];
+  if (gm.rows) {
+    const double* tt = w.T + ((int64_t)a * w.ldq + (j & 1)) * m + gm.sl * 256 + 4 * lane;
 #pragma unroll
-  for (int sl = 0; sl < 8; ++sl)
-    if (sl < ns) ui += us[sl];
-  if (tid <= j) h1[tid] = h1v0;
-  if (tid + 256 <= j) h1[tid + 256] = h1v1;
-  if (tid < j) h2[tid] = h2v0;
-  if (tid + 256 < j) h2[tid + 256] = h2v1;
-  if (stopped) return;
-  __syncthreads();
-  if (g == 0 && tid == 0) {
-    w.alpha[(int64_t)a * w.n_it + j] = h1[j];
-    w.amax[a] = fmax(amax0, fabs(h1[j]));
-    w.neff[a] = j + 1;
+    for (int e = 0; e < 4; ++e) tv[e] = tt[e];
+    const float* base = w.Phi + (int64_t)a * L * m + gm.sl * 256 + 4 * lane;
+#pragma unroll
+    for (int i = 0; i < RPW; ++i) v[i] = *(const float4*)(base + (int64_t)min(gm.rw0 + i, L - 1) * m);
   }
-  // Q_{j-1} h2 (q_j update) and Q_{j-1} h1 (z1) over this thread's k
+  if (stopped) return;
+  __shared__ double red[8];
+  __shared__ double h2s[264], bes[264], gs[264];
+  __shared__ double rq[KG][RB + 1], rg[KG][RB + 1];
+  __shared__ double pr[RB][9];
+  __shared__ double sq[RB], sqp[RB], sg[RB], zs[RB];
+  __shared__ double cr[WPS > 1 ? 7 : 1][256];
+  const double alpha_t = block_sum_f64((tid < nbr) ? apv : 0.0, red);   // |t~|^2
+  double alpha = alpha_t, beta = 0.0, h2last = 0.0;
+  if (j > 0) {
+    const double hh = block_sum_f64((tid < j) ? h2v * h2v : 0.0, red);
+    const double b2 = z2 - hh;
+    beta = b2 > 0.0 ? sqrt(b2) : 0.0;
+    if (!dry && !(beta > w.tol * amax0)) {     // breakdown: n_eff stays j
+      if (g == 0 && tid == 0) {
+        w.beta[(int64_t)a * w.n_it + j - 1] = beta;
+        w.stop[a] = 1;
+      }
+      return;
+    }
+    if (tid < j) {
+      h2s[tid] = h2v;
+      bes[tid] = bev;
+    }
+    __syncthreads();
+    // g = T_{j-1} h2 (alpha_i on the diagonal, beta_i beside it; beta_{j-1} is
+    // not part of T_{j-1})
+    double gi = 0.0;
+    if (tid < j) {
+      gi = alv * h2v;
+      if (tid > 0) gi = fma(bes[tid - 1], h2s[tid - 1], gi);
+      if (tid + 1 < j) gi = fma(bev, h2s[tid + 1], gi);
+      gs[tid] = gi;
+    }
+    const double hth = block_sum_f64((tid < j) ? h2v * gi : 0.0, red);
+    h2last = h2s[j - 1];
+    alpha = (z2 * alpha_t - hth) / (beta * beta) - 2.0 * h2last;
+  }
+  if (!dry && g == 0 && tid == 0) {
+    if (j > 0) w.beta[(int64_t)a * w.n_it + j - 1] = beta;
+    w.alpha[(int64_t)a * w.n_it + j] = alpha;
+    w.amax[2 * a + ((j + 1) & 1)] = fmax(amax0, fabs(alpha));   // the other slot:
+    w.neff[a] = j + 1;                                          // read by the next step
+  }
+  __syncthreads();
+  // Q_{j-1} h2 (for q_j) and Q_{j-1} g (for u) over this thread's k, then over
+  // the KG k-groups in order
   {
-    double aq[2] = {0, 0}, az[2] = {0, 0};
+    double aq[2] = {0.0, 0.0}, ag[2] = {0.0, 0.0};
 #pragma unroll
     for (int t = 0; t < MAXT; ++t) {
-      if (t < nt) {
-        const int k = kg + 8 * t;
-        aq[t & 1] = fma(qv[t], h2[k], aq[t & 1]);
-        az[t & 1] = fma(qv[t], h1[k], az[t & 1]);
+      if (KG * t < j && kg + KG * t < j) {
+        aq[t & 1] = fma(qv[t], h2s[kg + KG * t], aq[t & 1]);
+        ag[t & 1] = fma(qv[t], gs[kg + KG * t], ag[t & 1]);
       }
     }
     rq[kg][rl] = aq[0] + aq[1];
-    rz[kg][rl] = az[0] + az[1];
+    rg[kg][rl] = ag[0] + ag[1];
   }
   __syncthreads();
-  if (tid < 32) {
-    double z = 0.0, q = 0.0;
-    if (i < L) {
-      if (j > 0) {
-        double sub = 0.0;
-        for (int p = 0; p < 8; ++p) sub += rq[p][rl];
-        q = (zi - sub) / bet;
-        w.Q[((int64_t)a * w.ldq + j) * L + i] = q;
-      } else {
-        q = q0;
+  if (tid < RB) {
+    double q = qp, qm = 0.0, sub_g = 0.0;
+    if (j > 0) {
+      double sub = 0.0;
+      for (int k = 0; k < KG; ++k) {
+        sub += rq[k][rl];
+        sub_g += rg[k][rl];
       }
-      double zs = 0.0;
-      for (int p = 0; p < 8; ++p) zs += rz[p][rl];
-      z = ui - fma(q, h1[j], zs);
-      w.Z1[(int64_t)a * L + i] = z;
+      q = (zp - sub) / beta;
+      qm = qp;
+      if (ir < L) (dry ? w.Zs + (int64_t)a * 2 * L : w.Q + ((int64_t)a * w.ldq + j) * L)[ir] = q;
     }
-    sz[rl] = z;
     sq[rl] = q;
+    sqp[rl] = qm;
+    sg[rl] = sub_g;
+  }
+  // Phi t~: per row, 4 products per lane summed over the wave (8 rows per
+  // butterfly), then over the slices
+  if (gm.rows) {
+    const int idx = ((lane >> 5) & 1) * 4 + ((lane >> 4) & 1) * 2 + ((lane >> 3) & 1);
+#pragma unroll
+    for (int i0 = 0; i0 < RPW; i0 += 8) {
+      double d[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        if (i0 + e < RPW) {
+          const float4 y = pin_row(v[i0 + e]);
+          double x = (double)y.x * tv[0];
+          x = fma((double)y.y, tv[1], x);
+          x = fma((double)y.z, tv[2], x);
+          d[e] = fma((double)y.w, tv[3], x);
+        } else {
+          d[e] = 0.0;
+        }
+      }
+      const double tot = wave_sum8_f64(d);
+      if ((lane & 7) == 0 && i0 + idx < RPW) pr[gm.p * RPW + i0 + idx][gm.sl] = tot;
+    }
   }
   __syncthreads();
-  // partials of h2_k = sum over these rows of Q[k] z1 for k < j (from the registers,
-  // summed over the 32 rows of each half wave, 8 values per butterfly) and k = j
+  if (tid < RB) {
+    double z = 0.0;
+    if (ir < L) {
+      double u = 0.0;
+      for (int q = 0; q < (m >> 8); ++q) u += pr[rl][q];
+      if (j > 0) u = (fma(sqrt(z2), u, -sg[rl]) - beta * h2last * sq[rl]) / beta;
+      z = (u - alpha * sq[rl]) - beta * sqp[rl];
+      (dry ? w.Zs + ((int64_t)a * 2 + 1) * L : w.Z1 + (int64_t)a * L)[ir] = z;
+    }
+    zs[rl] = z;
+  }
+  __syncthreads();
+  step_colsums<RB, RPW>(w, a, g, gm, v, zs, cr);
+  // partials of h2_k = sum over the rows of Q[k] z1: k < j from the registers
+  // (summed over the RB rows of each half or quarter wave, 8 slots per
+  // butterfly), then k = j and |z1|^2
   double* hp = w.H2part + ((int64_t)a * w.G3 + g) * hs;
-  const double zl = sz[rl];
-  const int idx = ((lane >> 4) & 1) * 4 + ((lane >> 3) & 1) * 2 + ((lane >> 2) & 1);
+  const double zl = zs[rl];
+  const int hidx = (RB == 32) ? ((lane >> 4) & 1) * 4 + ((lane >> 3) & 1) * 2 + ((lane >> 2) & 1)
+                              : ((lane >> 3) & 1) * 4 + ((lane >> 2) & 1) * 2 + ((lane >> 1) & 1);
 #pragma unroll
   for (int t0 = 0; t0 < MAXT; t0 += 8) {
-    if (8 * t0 < j) {                          // block-uniform
+    if (KG * t0 < j) {                         // block-uniform
       double v8[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v8[e] = (t0 + e < nt) ? qv[t0 + e] * zl : 0.0;
-      const double tot = half_sum8_f64(v8);
-      const int k = kg + 8 * (t0 + idx);
-      if ((lane & 3) == 0 && k < j) hp[k] = tot;
+      for (int e = 0; e < 8; ++e)
+        v8[e] = (t0 + e < MAXT && kg + KG * (t0 + e) < j) ? qv[min(t0 + e, MAXT - 1)] * zl : 0.0;
+      const double tot = (RB == 32) ? half_sum8_f64(v8) : quarter_sum8_f64(v8);
+      const int k = kg + KG * (t0 + hidx);
+      // lanes that agree in the index bits hold equal sums: one of them writes
+      if ((lane & (RB == 32 ? 3 : 1)) == 0 && t0 + hidx < MAXT && k < j) hp[k] = tot;
     }
   }
-  if (tid < 64) {
-    // k = j and |z1|^2 over the 32 rows: lanes 0-31 and 32-63 of wave 0
-    const double v = (tid < 32) ? sq[rl] * sz[rl] : sz[rl] * sz[rl];
-    double t = v;
+  if (tid < 2 * RB) {
+    const double x = (tid < RB) ? sq[rl] * zs[rl] : zs[rl] * zs[rl];
+    double t = x;
 #pragma unroll
-    for (int o = 16; o >= 1; o >>= 1) t += __shfl_xor(t, o, 64);
+    for (int o = RB / 2; o >= 1; o >>= 1) t += __shfl_xor(t, o, 64);
     if (tid == 0) hp[j] = t;
-    if (tid == 32) hp[w.ldq] = t;
+    if (tid == RB) hp[w.ldq] = t;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Reduction after the pass of step j (j = -1: the initial pass): blocks
+// [0, nx) reduce h2 (k <= j) and |z1|^2 over the row groups into H2; the others
+// own 16 columns (x 32 partial lanes over the row groups): t_{j+1} = (Phi^T z1)
+// / |z1| (Phi^T q_0 for the initial pass) into T[(j + 1) & 1], and the block's
+// partial of |t_{j+1}|^2.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(512) void k_lz_reduce(LanczosWS w, int j) {
+  const int a = blockIdx.y, tid = threadIdx.x;
+  const int m = w.m, hs = w.ldq + 1;
+  const int nx = (j >= 0) ? (j + 16) / 16 + 1 : 0;
+  int g = blockIdx.x;
+  if (g < nx) {
+    if (w.stop[a]) return;
+    h2_reduce_block(w, a, j + 1, g, nx);
+    return;
+  }
+  g -= nx;
+  const int cl = tid & 15, pl = tid >> 4;
+  const int c = g * 16 + cl;                   // m is a multiple of 16
+  const int cnt = (w.G3 - pl + 31) / 32;
+  const double s = sum_strided(w.Spart + ((int64_t)a * w.G3 + pl) * m + c, (int64_t)32 * m,
+                               cnt > 0 ? cnt : 0);
+  if (w.stop[a]) return;
+  __shared__ double rs[32][17];
+  __shared__ double zb;
+  rs[pl][cl] = s;
+  double z2 = 1.0;
+  if (j >= 0) z2 = block_colsum<1, 512>(w.H2part + (int64_t)a * w.G3 * hs + w.ldq, hs, w.G3, 0, 1);
+  if (tid == 0) zb = z2;
+  __syncthreads();
+  if (tid < 16) {
+    double S = 0.0;
+    for (int q = 0; q < 32; ++q) S += rs[q][cl];
+    double t = S;
+    if (j >= 0) t = zb > 0.0 ? S / sqrt(zb) : 0.0;
+    w.T[((int64_t)a * w.ldq + ((j + 1) & 1)) * m + c] = t;
+    double t2 = t * t;
+#pragma unroll
+    for (int o = 8; o >= 1; o >>= 1) t2 += __shfl_xor(t2, o, 64);
+    if (tid == 0) w.Apart[(int64_t)a * (m >> 4) + g] = t2;
   }
 }
 
@@ -537,70 +565,96 @@ __global__ void k_lz_start(LanczosWS w, const double* __restrict__ q1) {
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     w.stop[a] = 0;
     w.neff[a] = 0;
-    w.amax[a] = 0.0;
+    w.amax[2 * a] = 0.0;
+    w.amax[2 * a + 1] = 0.0;
   }
 }
 
 
-// Launch, with the kernel's own start / end timestamps in (e0, e1) when given.
-template <typename K>
-static void launch_timed(K kernel, dim3 grid, dim3 block, hipStream_t s, hipEvent_t e0,
-                         hipEvent_t e1, const LanczosWS& w, int j) {
-  if (e0) hipExtLaunchKernelGGL(kernel, grid, block, 0, s, e0, e1, 0, w, j);
-  else hipLaunchKernelGGL(kernel, grid, block, 0, s, w, j);
+// rows per wave of the pass: RB / (8 / ns) for ns = m / 256 column slices
+static int step_rpw(int m, int rb) {
+  const int wps = 8 / (m >> 8);
+  return rb / wps;
 }
 
-// the smallest slot counts that cover n_it (finish: 16 KT >= n_it; orth: 8 MAXT >= n_it,
-// MAXT a multiple of 8)
-static void launch_finish(const LanczosWS& w, int j, hipStream_t s) {
-  const dim3 g(w.m / 16, w.n_act), b(256);
-  const int kt = (w.n_it + 15) / 16;
-  if (kt <= 2) hipLaunchKernelGGL(k_lz_finish<2>, g, b, 0, s, w, j);
-  else if (kt <= 4) hipLaunchKernelGGL(k_lz_finish<4>, g, b, 0, s, w, j);
-  else if (kt <= 6) hipLaunchKernelGGL(k_lz_finish<6>, g, b, 0, s, w, j);
-  else if (kt <= 8) hipLaunchKernelGGL(k_lz_finish<8>, g, b, 0, s, w, j);
-  else if (kt <= 12) hipLaunchKernelGGL(k_lz_finish<12>, g, b, 0, s, w, j);
-  else hipLaunchKernelGGL(k_lz_finish<16>, g, b, 0, s, w, j);
+template <int RB, int RPW>
+static void launch_init_t(const LanczosWS& w, hipStream_t s) {
+  hipLaunchKernelGGL((k_lz_init<RB, RPW>), dim3(w.G3, w.n_act), dim3(512), 0, s, w);
+}
+template <int RB>
+static void launch_init_r(const LanczosWS& w, hipStream_t s) {
+  switch (step_rpw(w.m, RB)) {
+    case RB / 8: launch_init_t<RB, RB / 8>(w, s); break;
+    case RB / 4: launch_init_t<RB, RB / 4>(w, s); break;
+    case RB / 2: launch_init_t<RB, RB / 2>(w, s); break;
+    default: launch_init_t<RB, RB>(w, s); break;
+  }
+}
+static void launch_init(const LanczosWS& w, hipStream_t s) {
+  if (w.RB == 16) launch_init_r<16>(w, s);
+  else launch_init_r<32>(w, s);
 }
 
-static void launch_orth(const LanczosWS& w, int j, hipStream_t s) {
-  const dim3 g(w.G3, w.n_act), b(256);
-  const int mt = (w.n_it + 7) / 8;                 // MAXT: a multiple of 8 (h2 butterflies)
-  if (mt <= 8) hipLaunchKernelGGL(k_lz_orth<8>, g, b, 0, s, w, j);
-  else if (mt <= 16) hipLaunchKernelGGL(k_lz_orth<16>, g, b, 0, s, w, j);
-  else if (mt <= 24) hipLaunchKernelGGL(k_lz_orth<24>, g, b, 0, s, w, j);
-  else hipLaunchKernelGGL(k_lz_orth<32>, g, b, 0, s, w, j);
+template <int RB, int RPW, int MAXT>
+static void launch_step_t(const LanczosWS& w, int j, int dry, hipStream_t s, hipEvent_t e0,
+                          hipEvent_t e1) {
+  const dim3 g(w.G3, w.n_act), b(512);
+  auto k = k_lz_step<RB, RPW, MAXT>;
+  if (e0) hipExtLaunchKernelGGL(k, g, b, 0, s, e0, e1, 0, w, j, dry);
+  else hipLaunchKernelGGL(k, g, b, 0, s, w, j, dry);
+}
+// MAXT: the smallest slot count with (512 / RB) MAXT >= n_it
+template <int RB, int RPW>
+static void launch_step_m(const LanczosWS& w, int j, int dry, hipStream_t s, hipEvent_t e0,
+                          hipEvent_t e1) {
+  constexpr int KG = 512 / RB;
+  if (w.n_it <= KG * 4) launch_step_t<RB, RPW, 4>(w, j, dry, s, e0, e1);
+  else if (w.n_it <= KG * 8) launch_step_t<RB, RPW, 8>(w, j, dry, s, e0, e1);
+  else launch_step_t<RB, RPW, 16>(w, j, dry, s, e0, e1);
+}
+template <int RB>
+static void launch_step_r(const LanczosWS& w, int j, int dry, hipStream_t s, hipEvent_t e0,
+                          hipEvent_t e1) {
+  switch (step_rpw(w.m, RB)) {
+    case RB / 8: launch_step_m<RB, RB / 8>(w, j, dry, s, e0, e1); break;
+    case RB / 4: launch_step_m<RB, RB / 4>(w, j, dry, s, e0, e1); break;
+    case RB / 2: launch_step_m<RB, RB / 2>(w, j, dry, s, e0, e1); break;
+    default: launch_step_m<RB, RB>(w, j, dry, s, e0, e1); break;
+  }
+}
+static void launch_step(const LanczosWS& w, int j, int dry, hipStream_t s, hipEvent_t e0 = nullptr,
+                        hipEvent_t e1 = nullptr) {
+  if (w.RB == 16) launch_step_r<16>(w, j, dry, s, e0, e1);
+  else launch_step_r<32>(w, j, dry, s, e0, e1);
+}
+
+static void launch_reduce(const LanczosWS& w, int j, hipStream_t s) {
+  const int nx = (j >= 0) ? (j + 16) / 16 + 1 : 0;
+  hipLaunchKernelGGL(k_lz_reduce, dim3(nx + w.m / 16, w.n_act), dim3(512), 0, s, w, j);
 }
 
 hipError_t launch_lanczos(const LanczosWS& w, const double* q1_act, hipStream_t s,
                           const hipEvent_t* ev_before, const hipEvent_t* ev_after) {
   (void)hipGetLastError();
+  if (w.m % 256 != 0 || w.m > 2048 || w.n_it > 256 || w.n_it < 1 || (w.RB != 16 && w.RB != 32) ||
+      w.G3 != (w.L + w.RB - 1) / w.RB)
+    return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_lz_start, dim3((w.L + 255) / 256, w.n_act), dim3(256), 0, s, w, q1_act);
-  const int ns = w.m / 256;
+  launch_init(w, s);
+  launch_reduce(w, -1, s);
   for (int j = 0; j < w.n_it; ++j) {
-    const int nx = (j > 0) ? (j + 15) / 16 + 1 : 0;
-    launch_timed(k_lz_phit, dim3(nx + ns * w.GA, w.n_act), dim3(512), s,
-                 ev_before ? ev_before[2 * j] : nullptr, ev_after ? ev_after[2 * j] : nullptr, w, j);
-    launch_finish(w, j, s);
-    launch_timed(k_lz_phiu, dim3((j + 8) / 8 + ns * w.GA, w.n_act), dim3(512), s,
-                 ev_before ? ev_before[2 * j + 1] : nullptr,
-                 ev_after ? ev_after[2 * j + 1] : nullptr, w, j);
-    launch_orth(w, j, s);
+    launch_step(w, j, 0, s, ev_before ? ev_before[j] : nullptr, ev_after ? ev_after[j] : nullptr);
+    if (j + 1 < w.n_it) launch_reduce(w, j, s);
   }
   hipLaunchKernelGGL(k_lz_h2sum, dim3((w.n_it + 15) / 16 + 1, w.n_act), dim3(512), 0, s, w);
   hipLaunchKernelGGL(k_lz_last_beta, dim3(w.n_act), dim3(256), 0, s, w);
   return hipGetLastError();
 }
 
-// reps x (Phi^T v, Phi t) of step j, launched exactly as in launch_lanczos
+// reps x the pass of step j, launched as in launch_lanczos but dry
 hipError_t launch_lanczos_passes(const LanczosWS& w, int j, int reps, hipStream_t s) {
   (void)hipGetLastError();
-  const int ns = w.m / 256;
-  const int nx = (j > 0) ? (j + 15) / 16 + 1 : 0;
-  for (int q = 0; q < reps; ++q) {
-    hipLaunchKernelGGL(k_lz_phit, dim3(nx + ns * w.GA, w.n_act), dim3(512), 0, s, w, j);
-    hipLaunchKernelGGL(k_lz_phiu, dim3((j + 8) / 8 + ns * w.GA, w.n_act), dim3(512), 0, s, w, j);
-  }
+  for (int q = 0; q < reps; ++q) launch_step(w, j, 1, s);
   return hipGetLastError();
 }
 

@@ -112,7 +112,7 @@ struct slh_ctx {
   std::vector<DevBuf*> all;
   DevBuf Wt, psi, R, q1all, q1act, winlist, route;
   DevBuf nrm2_fm, nrm_x, inv_x, rowscale, Xb, Phi;
-  DevBuf Q, T, U, Z1, Spart, H1, H2part, H2, alpha, beta, neff, stop, amax;
+  DevBuf Q, T, Apart, Z1, Spart, Zs, H2part, H2, alpha, beta, neff, stop, amax;
   DevBuf theta, Seig, Z, proj, codes;
   DevBuf keyA, keyB, valA, valB, tmpi, segid, segk, sval, sloc, mw, wbase, sseg, Mtot;
   DevBuf part, part_seg, part_cnt, part_nsum, part_end;
@@ -424,7 +424,7 @@ void slh_destroy(slh_ctx* c) {
   drop_graph(c);
   DevBuf* bufs[] = {&c->Wt, &c->psi, &c->R, &c->q1all, &c->q1act, &c->winlist, &c->route,
                     &c->nrm2_fm, &c->nrm_x, &c->inv_x, &c->rowscale, &c->Xb, &c->Phi, &c->Q, &c->T,
-                    &c->U, &c->Z1, &c->Spart, &c->H1, &c->H2part, &c->H2,
+                    &c->Apart, &c->Z1, &c->Spart, &c->Zs, &c->H2part, &c->H2,
                     &c->alpha, &c->beta, &c->neff, &c->stop, &c->amax, &c->theta, &c->Seig, &c->Z,
                     &c->proj, &c->codes, &c->keyA, &c->keyB, &c->valA, &c->valB, &c->tmpi,
                     &c->segid, &c->segk, &c->sval, &c->sloc, &c->mw, &c->wbase, &c->sseg,
@@ -689,46 +689,42 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
       c->lz_w_valid = false;
     } else {
       LanczosWS w;
+      memset(&w, 0, sizeof w);      // the graph key compares the bytes
       w.n_act = na;
       w.L = (int)L;
       w.m = (int)c->m;
       w.n_it = n_it;
       w.ldq = n_it + 1;
       w.tol = c->tol;
-      {
-        // blocks of RBA rows x 256 columns in each pass over Phi, 8 rows per wave
-        // for m >= 2048 and 16 below (measured per step: 8192 x 2048 and
-        // 32768 x 2048 fastest at 8, the latter 13.5 ms against 15.9 at 32;
-        // 4096 x 1024 and 32 windows of 2048 x 1024 fastest at 16)
-        w.RWA = (c->m >= 2048) ? 8 : 16;
-        w.RBA = 8 * w.RWA;
-        w.GA = (int)((L + w.RBA - 1) / w.RBA);
-        w.G3 = (int)((L + 31) / 32);
-      }
+#ifndef SLH_LZ_RB
+#define SLH_LZ_RB 16
+#endif
+      w.RB = SLH_LZ_RB;
+      w.G3 = (int)((L + w.RB - 1) / w.RB);
       const size_t hs = (size_t)w.ldq + 1;
       ENSURE(c, c->Q, (size_t)na * w.ldq * L * 8);
       ENSURE(c, c->T, (size_t)na * w.ldq * c->m * 8);
-      ENSURE(c, c->U, (size_t)na * (c->m / 256) * L * 8);
+      ENSURE(c, c->Apart, (size_t)na * (c->m / 16) * 8);
       ENSURE(c, c->Z1, (size_t)na * L * 8);
-      ENSURE(c, c->Spart, (size_t)na * w.GA * c->m * 8);
-      ENSURE(c, c->H1, (size_t)na * hs * 8);
+      ENSURE(c, c->Spart, (size_t)na * w.G3 * c->m * 8);
+      ENSURE(c, c->Zs, (size_t)na * 2 * L * 8);
       ENSURE(c, c->H2part, (size_t)na * w.G3 * hs * 8);
       ENSURE(c, c->H2, (size_t)na * hs * 8);
       ENSURE(c, c->alpha, (size_t)na * n_it * 8);
       ENSURE(c, c->beta, (size_t)na * n_it * 8);
       ENSURE(c, c->neff, (size_t)na * 4);
       ENSURE(c, c->stop, (size_t)na * 4);
-      ENSURE(c, c->amax, (size_t)na * 8);
+      ENSURE(c, c->amax, (size_t)na * 2 * 8);
       ENSURE(c, c->theta, (size_t)na * c->r * 8);
       ENSURE(c, c->Seig, (size_t)na * n_it * c->r * 8);
       ENSURE(c, c->Z, (size_t)na * L * c->r * 8);
       w.Phi = P<float>(c->Phi);
       w.Q = P<double>(c->Q);
       w.T = P<double>(c->T);
-      w.Upart = P<double>(c->U);
+      w.Apart = P<double>(c->Apart);
       w.Z1 = P<double>(c->Z1);
       w.Spart = P<double>(c->Spart);
-      w.H1 = P<double>(c->H1);
+      w.Zs = P<double>(c->Zs);
       w.H2part = P<double>(c->H2part);
       w.H2 = P<double>(c->H2);
       w.alpha = P<double>(c->alpha);
@@ -739,7 +735,7 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
       if (c->timing) {
         // timing: launch the step sequence directly so that every pass over Phi
         // can be bracketed by events (events inside a captured graph cannot be timed)
-        int rc_ev = make_events(c, 2 * n_it);
+        int rc_ev = make_events(c, n_it);
         if (rc_ev) return rc_ev;
         HIP_TRY(c, hipEventRecord(c->ev[2], c->stream));
         HIP_TRY(c, launch_lanczos(w, q1act, c->stream, c->ev_fb.data(), c->ev_fa.data()));
@@ -769,7 +765,7 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
         HIP_TRY(c, hipGraphLaunch(c->lz_exec, c->stream));
       }
       if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[3], c->stream));
-      c->fused_timed = c->timing ? 2 * n_it : 0;
+      c->fused_timed = c->timing ? n_it : 0;
       c->lz_w = w;
       c->lz_w_valid = true;
       HIP_TRY(c, launch_tridiag_eig(w.alpha, w.beta, w.neff, na, n_it, c->r, P<double>(c->theta),
@@ -1048,7 +1044,7 @@ int slh_time_passes(slh_ctx* c, int32_t reps, double* us_out) {
   if (e0) (void)hipEventDestroy(e0);
   if (e1) (void)hipEventDestroy(e1);
   if (e != hipSuccess) return fail(c, SLH_EHIP, "slh_time_passes: %s", hipGetErrorString(e));
-  *us_out = 1000.0 * (double)ms / (2.0 * reps);
+  *us_out = 1000.0 * (double)ms / reps;
   return SLH_OK;
 }
 

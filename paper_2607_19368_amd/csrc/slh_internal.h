@@ -38,30 +38,32 @@ struct LanczosWS {
   int n_act, L, m, n_it, ldq;   // ldq = n_it + 1 vectors per window
   const float* Phi;             // [n_act][L][m]
   double* Q;                    // [n_act][ldq][L]  Lanczos basis, vector-major
-  double* T;                    // [n_act][ldq][m]  t_k = Phi^T q_k
-  double* Upart;                // [n_act][m/256][L] partials of u = Phi t_j per column slice
-  double* Z1;                   // [n_act][L]       after the first Gram-Schmidt pass
-  double* Spart;                // [n_act][GA][m]   partials of Phi^T z1 per row group
-  double* H1;                   // [n_act][ldq+1]   Q_j^T u
+  double* T;                    // [n_act][ldq][m]  t_j = Phi^T z1 / |z1| of step j-1 in slot j & 1
+  double* Apart;                // [n_act][m/16]    partials of |t_j|^2 (= alpha_j) per 16 columns
+  double* Z1;                   // [n_act][L]       z1 of the last step (before the second pass)
+  double* Spart;                // [n_act][G3][m]   partials of Phi^T z1 per row group
   double* H2part;               // [n_act][G3][ldq+1] (slot ldq: |z1|^2)
   double* H2;                   // [n_act][ldq+1]   Q^T z1 and |z1|^2
+  double* Zs;                   // [n_act][2][L]    row outputs of timing replays
   double* alpha;                // [n_act][n_it]
   double* beta;                 // [n_act][n_it]
   int* neff;                    // [n_act]  steps done
   int* stop;                    // [n_act]  1 after breakdown
-  double* amax;                 // [n_act]  max |alpha| so far (breakdown scale)
+  double* amax;                 // [n_act][2] max |alpha| so far (breakdown scale): step j reads
+                                //   slot j & 1 and writes the other
   double tol;
-  int GA, RBA, RWA;             // both passes: row groups of RBA = 8 * RWA rows (RWA in {8,16,24,32})
-  int G3;                       // orthogonalisation blocks of 32 rows
+  int RB;                       // rows per block of the pass (16 or 32)
+  int G3;                       // row groups of RB rows (one block of the pass each)
 };
-// ev_before/ev_after (may be NULL): 2 * n_it events each, receiving the start
-// and end timestamps of the two Phi passes of every step (index 2j: Phi^T v,
-// 2j + 1: Phi t_j).
+// One pass over Phi per step (k_lz_step) and one reduction.  ev_before/ev_after
+// (may be NULL): n_it events each, receiving the start and end timestamps of
+// the pass of every step.  Requires m % 256 == 0, m <= 2048, 1 <= n_it <= 256.
 hipError_t launch_lanczos(const LanczosWS& w, const double* q1_act, hipStream_t s,
                           const hipEvent_t* ev_before = nullptr,
                           const hipEvent_t* ev_after = nullptr);
-// reps x the two Phi passes of step j (Phi^T v, then Phi t_j), launched as in
-// launch_lanczos; they rewrite only Spart, Upart, H1 and H2 (for timing)
+// reps x the pass of step j, launched as in launch_lanczos but dry: its rows go
+// to Zs and it records no alpha, beta, n_eff or breakdown (for timing); it
+// rewrites Spart and H2part
 hipError_t launch_lanczos_passes(const LanczosWS& w, int j, int reps, hipStream_t s);
 
 // ---- eigensolve + Ritz + SimHash (k_eig.hip, k_hash.hip) ----

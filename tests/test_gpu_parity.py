@@ -728,7 +728,7 @@ def test_exact_target_length(case, T):
 
 @pytest.mark.parametrize("case", ["tiny", "windows256"])
 def test_time_passes(case):
-    """slh_time_passes replays the final step's two passes over Phi as a graph:
+    """slh_time_passes replays the final step's pass over Phi as a graph:
     it returns a positive duration and leaves every result of slh_lanczos (Q,
     alpha, beta, Ritz values and vectors) and the SimHash codes bit-identical;
     it is refused before slh_lanczos and after a short-window run."""
