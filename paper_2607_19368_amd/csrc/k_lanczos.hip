@@ -127,20 +127,28 @@ __device__ __forceinline__ double readlane_f64(double v, int l) {
   return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 
-// Sum of src[g * ld] over g < G with 8 loads in flight (fixed order).
-// Every batch issues its 8 loads unconditionally (index clamped to G - 1, the
+// Sum of src[g * ld] over g < G with 16 loads in flight (fixed order).
+// Every batch issues its 16 loads unconditionally (index clamped to G - 1, the
 // surplus values masked to zero afterwards), so a ragged tail costs one round
 // trip rather than one per element.
 __device__ __forceinline__ double sum_strided(const double* __restrict__ src, int64_t ld, int G) {
-  double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  for (int g = 0; g < G; g += 8) {
-    double v[8];
+  constexpr int NF = 16;
+  double acc[NF];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = src[(int64_t)min(g + e, G - 1) * ld];
+  for (int e = 0; e < NF; ++e) acc[e] = 0.0;
+  for (int g = 0; g < G; g += NF) {
+    double v[NF];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] += (g + e < G) ? v[e] : 0.0;
+    for (int e = 0; e < NF; ++e) v[e] = src[(int64_t)min(g + e, G - 1) * ld];
+#pragma unroll
+    for (int e = 0; e < NF; ++e) acc[e] += (g + e < G) ? v[e] : 0.0;
   }
-  return ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
+#pragma unroll
+  for (int h = NF / 2; h >= 1; h >>= 1) {
+#pragma unroll
+    for (int e = 0; e < h; ++e) acc[e] += acc[e + h];
+  }
+  return acc[0];
 }
 
 // Column reduction by one block of NT threads: returns, in the threads with
@@ -168,15 +176,33 @@ __device__ __forceinline__ double block_colsum(const double* __restrict__ src, i
   return t;
 }
 
-// Block g of nx = ceil(j / 16) + 1 (512 threads): H2[k] = sum over the orth
-// blocks of the h2 partials for k in [16 g, 16 g + 16) (k < j), or, for the
+// |z1|^2 of window a: the sum over the row groups of H2part[g][ldq], by a block
+// of 512 threads in a fixed order (every caller gets the same bits).  Four
+// clamped loads per thread and batch.
+__device__ __forceinline__ double z2_sum(const LanczosWS& w, int a, double* red) {
+  const int hs = w.ldq + 1, G = w.G3, tid = threadIdx.x;
+  const double* src = w.H2part + (int64_t)a * G * hs + w.ldq;
+  double acc = 0.0;
+  for (int g0 = 0; g0 < G; g0 += 4 * 512) {
+    double v[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = src[(int64_t)min(g0 + tid + 512 * e, G - 1) * hs];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc += (g0 + tid + 512 * e < G) ? v[e] : 0.0;
+  }
+  return block_sum_f64(acc, red);
+}
+
+// Block g of nx = ceil(j / 16) + 1 (512 threads): H2[k] = sum over the row
+// groups of the h2 partials for k in [16 g, 16 g + 16) (k < j), or, for the
 // last block, |z1|^2 (slot ldq).
 __device__ __forceinline__ void h2_reduce_block(const LanczosWS& w, int a, int j, int g, int nx) {
   const int hs = w.ldq + 1;
   const double* hp = w.H2part + (int64_t)a * w.G3 * hs;
   double* dst = w.H2 + (int64_t)a * hs;
   if (g == nx - 1) {
-    const double v = block_colsum<1, 512>(hp + w.ldq, hs, w.G3, 0, 1);
+    __shared__ double red[8];
+    const double v = z2_sum(w, a, red);
     if (threadIdx.x == 0) dst[w.ldq] = v;
   } else {
     const int c0 = g * 16;
@@ -268,10 +294,11 @@ __global__ __launch_bounds__(512) void k_lz_init(LanczosWS w) {
   const StepGeom gm = step_geom<RB, RPW>(m, r0);
   const double q0 = (tid < RB) ? w.Q[(int64_t)a * w.ldq * L + min(r0 + tid, L - 1)] : 0.0;
   float4 v[RPW];
-  if (gm.rows) {
+  {
+    const int prow = r0 + min(gm.p, WPS - 1) * RPW;
     const float* base = w.Phi + (int64_t)a * L * m + gm.sl * 256 + 4 * lane;
 #pragma unroll
-    for (int i = 0; i < RPW; ++i) v[i] = *(const float4*)(base + (int64_t)min(gm.rw0 + i, L - 1) * m);
+    for (int i = 0; i < RPW; ++i) v[i] = *(const float4*)(base + (int64_t)min(prow + i, L - 1) * m);
   }
   __shared__ double zs[RB];
   __shared__ double cr[WPS > 1 ? 7 : 1][256];
@@ -316,11 +343,13 @@ __global__ __launch_bounds__(512) void k_lz_step(LanczosWS w, int j, int dry) {
   const double* Qa = w.Q + (int64_t)a * w.ldq * L;
   const int jm = max(j - 1, 0);
   // Every small load is issued before the Phi rows, so waiting for them leaves
-  // the Phi loads in flight.  Indices are clamped; surplus values are unused.
+  // the Phi loads in flight.  Every load is unconditional, with clamped indices
+  // (surplus values are unused): a load under a branch would make the compiler
+  // wait, where the branches join, as if the other path had issued no later
+  // loads, i.e. for most of the Phi rows.
   double qv[MAXT];                             // Q[k][row], k = kg + KG t < j
 #pragma unroll
-  for (int t = 0; t < MAXT; ++t)
-    if (KG * t < j) qv[t] = Qa[(int64_t)min(kg + KG * t, jm) * L + irc];
+  for (int t = 0; t < MAXT; ++t) qv[t] = Qa[(int64_t)min(kg + KG * t, jm) * L + irc];
   const double* H2a = w.H2 + (int64_t)a * hs;
   const double h2v = H2a[min(tid, jm)];        // n_it <= 512
   const double z2 = H2a[w.ldq];
@@ -331,15 +360,17 @@ __global__ __launch_bounds__(512) void k_lz_step(LanczosWS w, int j, int dry) {
   const double bev = w.beta[(int64_t)a * w.n_it + min(tid, jm)];
   const int stopped = w.stop[a];
   const double amax0 = w.amax[2 * a + (j & 1)];   // max |alpha| before step j
-  double tv[4] = {0.0, 0.0, 0.0, 0.0};
+  // waves without rows (ns not dividing 8) load those of the last row subset
+  const int prow = r0 + min(gm.p, WPS - 1) * RPW;
+  double tv[4];
   float4 v[RPW];
-  if (gm.rows) {
+  {
     const double* tt = w.T + ((int64_t)a * w.ldq + (j & 1)) * m + gm.sl * 256 + 4 * lane;
 #pragma unroll
     for (int e = 0; e < 4; ++e) tv[e] = tt[e];
     const float* base = w.Phi + (int64_t)a * L * m + gm.sl * 256 + 4 * lane;
 #pragma unroll
-    for (int i = 0; i < RPW; ++i) v[i] = *(const float4*)(base + (int64_t)min(gm.rw0 + i, L - 1) * m);
+    for (int i = 0; i < RPW; ++i) v[i] = *(const float4*)(base + (int64_t)min(prow + i, L - 1) * m);
   }
   if (stopped) return;
   __shared__ double red[8];
@@ -504,22 +535,23 @@ __global__ __launch_bounds__(512) void k_lz_reduce(LanczosWS w, int j) {
   g -= nx;
   const int cl = tid & 15, pl = tid >> 4;
   const int c = g * 16 + cl;                   // m is a multiple of 16
+  if (w.stop[a]) return;
+  __shared__ double red[8];
+  __shared__ double rs[32][17];
+  // |z1|^2 first: its loads go out ahead of the column sums' (same routine and
+  // order as the h2 block, so t and the next pass use the same |z1|)
+  double z2 = 1.0;
+  if (j >= 0) z2 = z2_sum(w, a, red);
   const int cnt = (w.G3 - pl + 31) / 32;
   const double s = sum_strided(w.Spart + ((int64_t)a * w.G3 + pl) * m + c, (int64_t)32 * m,
                                cnt > 0 ? cnt : 0);
-  if (w.stop[a]) return;
-  __shared__ double rs[32][17];
-  __shared__ double zb;
   rs[pl][cl] = s;
-  double z2 = 1.0;
-  if (j >= 0) z2 = block_colsum<1, 512>(w.H2part + (int64_t)a * w.G3 * hs + w.ldq, hs, w.G3, 0, 1);
-  if (tid == 0) zb = z2;
   __syncthreads();
   if (tid < 16) {
     double S = 0.0;
     for (int q = 0; q < 32; ++q) S += rs[q][cl];
     double t = S;
-    if (j >= 0) t = zb > 0.0 ? S / sqrt(zb) : 0.0;
+    if (j >= 0) t = z2 > 0.0 ? S / sqrt(z2) : 0.0;
     w.T[((int64_t)a * w.ldq + ((j + 1) & 1)) * m + c] = t;
     double t2 = t * t;
 #pragma unroll
