@@ -35,6 +35,7 @@
 #include <hip/hip_ext.h>
 
 #include <algorithm>
+#include <type_traits>
 
 namespace slh {
 
@@ -212,103 +213,109 @@ __device__ __forceinline__ void h2_reduce_block(const LanczosWS& w, int a, int j
 }
 
 // ---------------------------------------------------------------------------
-// The pass over Phi.  A block owns RB consecutive rows and all m columns of
-// them, held in registers: 8 waves, wave = (row subset p, 256-column slice sl),
-// sl = wave % ns, p = wave / ns; the WPS = RB / RPW subsets of RPW rows each
-// cover the block's rows (waves with p >= WPS, when ns does not divide 8, take
-// no rows).  Lane = 4 columns (one float4 per row) of the wave's slice.
+// The pass over Phi.  A block owns NCH chunks of RC = 16 consecutive rows and
+// all m columns of them; 8 waves, wave = (row subset p, 256-column slice sl),
+// sl = wave % ns, p = wave / ns; the WPS = RC / RPW subsets of RPW rows each
+// cover a chunk (waves with p >= WPS, when ns does not divide 8, take no rows
+// and load those of the last subset).  Lane = 4 columns (one float4 per row) of
+// the wave's slice.  A chunk's rows are held in registers; when another chunk
+// follows, they are copied to LDS after the row dots so that the next chunk's
+// loads are in flight while this chunk's column sums are taken.
 // ---------------------------------------------------------------------------
-// The float4 of one Phi row as an opaque value at its point of use, so that its
-// conversion to fp64 is not hoisted: otherwise every row of the block is held
-// converted (twice the registers) across the phases that use it.
-__device__ __forceinline__ float4 pin_row(float4 x) {
-  asm volatile("" : "+v"(x.x), "+v"(x.y), "+v"(x.z), "+v"(x.w));
-  return x;
-}
+constexpr int LZ_RC = 16;
 
 struct StepGeom {
-  int sl, p, rw0;
+  int sl, p;
   bool rows;
 };
-template <int RB, int RPW>
-__device__ __forceinline__ StepGeom step_geom(int m, int r0) {
-  constexpr int WPS = RB / RPW;
+template <int RPW>
+__device__ __forceinline__ StepGeom step_geom(int m) {
+  constexpr int WPS = LZ_RC / RPW;
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int ns = m >> 8;
   StepGeom gm;
   gm.sl = wave % ns;
   gm.p = wave / ns;
   gm.rows = gm.p < WPS;
-  gm.rw0 = r0 + gm.p * RPW;
   return gm;
 }
 
-// Column partials of Phi^T z over the block's rows (z of row rl in zs[rl], 0
-// past L) into Spart[a][g][:]: each wave sums its RPW rows for its 4 columns
-// per lane; the WPS subsets of one slice are combined through cr in a fixed order.
-template <int RB, int RPW>
-__device__ __forceinline__ void step_colsums(const LanczosWS& w, int a, int g, const StepGeom& gm,
-                                             const float4 (&v)[RPW], const double* zs,
-                                             double (*cr)[256]) {
-  constexpr int WPS = RB / RPW;
+// The float4 of one Phi row as an opaque value at its point of use, so that its
+// conversion to fp64 is not hoisted: otherwise every row of the chunk is held
+// converted (twice the registers) across the phases that use it.
+__device__ __forceinline__ float4 pin_row(float4 x) {
+  asm volatile("" : "+v"(x.x), "+v"(x.y), "+v"(x.z), "+v"(x.w));
+  return x;
+}
+
+// Column partials of the block (4 per lane of each slice; the WPS row subsets of
+// a slice are combined through cr in a fixed order) into Spart[a][g][:].
+template <int WPS>
+__device__ __forceinline__ void lz_store_colsums(const LanczosWS& w, int a, int g,
+                                                 const StepGeom& gm, double (&col)[4],
+                                                 double (*cr)[256]) {
   const int lane = threadIdx.x & 63, ns = w.m >> 8;
-  double c[4] = {0.0, 0.0, 0.0, 0.0};
-  if (gm.rows) {
-#pragma unroll
-    for (int i = 0; i < RPW; ++i) {
-      const double z = zs[gm.p * RPW + i];
-      const float4 x = pin_row(v[i]);
-      c[0] = fma((double)x.x, z, c[0]);
-      c[1] = fma((double)x.y, z, c[1]);
-      c[2] = fma((double)x.z, z, c[2]);
-      c[3] = fma((double)x.w, z, c[3]);
-    }
-  }
   if (WPS > 1) {
     if (gm.rows && gm.p > 0) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) cr[(gm.p - 1) * ns + gm.sl][4 * lane + e] = c[e];
+      for (int e = 0; e < 4; ++e) cr[(gm.p - 1) * ns + gm.sl][4 * lane + e] = col[e];
     }
     __syncthreads();
     if (gm.rows && gm.p == 0) {
       for (int q = 1; q < WPS; ++q) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) c[e] += cr[(q - 1) * ns + gm.sl][4 * lane + e];
+        for (int e = 0; e < 4; ++e) col[e] += cr[(q - 1) * ns + gm.sl][4 * lane + e];
       }
     }
   }
   if (gm.rows && gm.p == 0) {
     double* dst = w.Spart + ((int64_t)a * w.G3 + g) * w.m + gm.sl * 256 + 4 * lane;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) dst[e] = c[e];
+    for (int e = 0; e < 4; ++e) dst[e] = col[e];
   }
 }
 
-// Initial pass: partials of Phi^T q_0 (t_0 before reduction).
-template <int RB, int RPW>
+// Initial pass: partials of Phi^T q_0 (t_0 before reduction), over the same row
+// groups as the step's pass.
+template <int RPW>
 __global__ __launch_bounds__(512) void k_lz_init(LanczosWS w) {
-  constexpr int WPS = RB / RPW;
+  constexpr int WPS = LZ_RC / RPW;
   const int a = blockIdx.y, g = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
-  const int L = w.L, m = w.m;
-  const int r0 = g * RB;
-  const StepGeom gm = step_geom<RB, RPW>(m, r0);
-  const double q0 = (tid < RB) ? w.Q[(int64_t)a * w.ldq * L + min(r0 + tid, L - 1)] : 0.0;
-  float4 v[RPW];
-  {
-    const int prow = r0 + min(gm.p, WPS - 1) * RPW;
-    const float* base = w.Phi + (int64_t)a * L * m + gm.sl * 256 + 4 * lane;
-#pragma unroll
-    for (int i = 0; i < RPW; ++i) v[i] = *(const float4*)(base + (int64_t)min(prow + i, L - 1) * m);
-  }
-  __shared__ double zs[RB];
+  const int L = w.L, m = w.m, nch = w.NCH;
+  const int r0 = g * LZ_RC * nch;
+  const StepGeom gm = step_geom<RPW>(m);
+  const int prow = min(gm.p, WPS - 1) * RPW;
+  const float* pbase = w.Phi + (int64_t)a * L * m + gm.sl * 256 + 4 * lane;
+  const double* q0 = w.Q + (int64_t)a * w.ldq * L;
+  __shared__ double zs[LZ_RC];
   __shared__ double cr[WPS > 1 ? 7 : 1][256];
-  if (tid < RB) zs[tid] = (r0 + tid < L) ? q0 : 0.0;
-  __syncthreads();
-  step_colsums<RB, RPW>(w, a, g, gm, v, zs, cr);
+  double col[4] = {0.0, 0.0, 0.0, 0.0};
+  for (int c = 0; c < nch; ++c) {
+    const int rc0 = r0 + LZ_RC * c;
+    const double z = q0[min(rc0 + (tid & (LZ_RC - 1)), L - 1)];
+    float4 v[RPW];
+#pragma unroll
+    for (int i = 0; i < RPW; ++i) v[i] = *(const float4*)(pbase + (int64_t)min(rc0 + prow + i, L - 1) * m);
+    if (tid < LZ_RC) zs[tid] = (rc0 + tid < L) ? z : 0.0;
+    __syncthreads();
+    if (gm.rows) {
+#pragma unroll
+      for (int i = 0; i < RPW; ++i) {
+        const double zz = zs[gm.p * RPW + i];
+        const float4 x = pin_row(v[i]);
+        col[0] = fma((double)x.x, zz, col[0]);
+        col[1] = fma((double)x.y, zz, col[1]);
+        col[2] = fma((double)x.z, zz, col[2]);
+        col[3] = fma((double)x.w, zz, col[3]);
+      }
+    }
+    __syncthreads();
+  }
+  lz_store_colsums<WPS>(w, a, g, gm, col, cr);
 }
 
 // ---------------------------------------------------------------------------
-// One Lanczos step j on the block's RB rows, with one read of their Phi rows.
+// One Lanczos step j on the block's rows, with one read of their Phi rows.
 // From the previous step: z1 (row space), h2 = Q_{j-1}^T z1 and |z1|^2 (reduced),
 // and t~ = Phi^T z1 / |z1| with alpha~ = |t~|^2 (feature space).
 //   beta_{j-1} = |z1 - Q_{j-1} h2| = sqrt(|z1|^2 - |h2|^2) (Q orthonormal), and
@@ -324,60 +331,69 @@ __global__ __launch_bounds__(512) void k_lz_init(LanczosWS w) {
 //     (without this correction the h2 of each step would re-enter the next one
 //     amplified by |A| / beta);
 //   z1 = u - alpha_j q_j - beta_{j-1} q_{j-1}   (the three-term recurrence);
-//   partials of Phi^T z1 (column sums), of h2 = Q_j^T z1 and of |z1|^2.
-// Row-space work: thread = (row rl < RB, k-group kg < KG = 512 / RB); MAXT =
-// slots of k = kg + KG t per thread, KG MAXT >= n_it.
-// ---------------------------------------------------------------------------
+//   partials of Phi^T z1 (column sums), of h2 = Q_j^T z1 and of |z1|^2 over the
+//   block's rows.
+// Row-space work of a chunk: thread = (row rl < 16, k-group kg < 32); MAXT =
+// slots of k = kg + 32 t per thread, 32 MAXT >= n_it.
 // dry = 1 (timing replays): q_j and z1 go to Zs, no bookkeeping, no breakdown exit.
-template <int RB, int RPW, int MAXT>
+// Dynamic LDS: 16 m floats (the staged chunk) when NCH > 1, else none.
+// ---------------------------------------------------------------------------
+// STAGED: blocks of NCH > 1 chunks (else NCH = 1, no LDS staging and a smaller
+// register footprint, two blocks per CU).
+template <int RPW, int MAXT, bool STAGED>
 __global__ __launch_bounds__(512) void k_lz_step(LanczosWS w, int j, int dry) {
-  static_assert(RB == 16 || RB == 32, "rows per block");
-  constexpr int WPS = RB / RPW, KG = 512 / RB;
+  constexpr int RC = LZ_RC, WPS = RC / RPW, KG = 512 / RC;
+  extern __shared__ float4 phis[];             // [RC][m / 4] staged chunk
   const int a = blockIdx.y, g = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63;
-  const int L = w.L, m = w.m, hs = w.ldq + 1, nbr = m >> 4;
-  const int r0 = g * RB;
-  const StepGeom gm = step_geom<RB, RPW>(m, r0);
-  const int rl = tid & (RB - 1), kg = tid / RB;   // row-space work: (row, k-group)
-  const int ir = r0 + rl, irc = min(ir, L - 1);
+  const int L = w.L, m = w.m, hs = w.ldq + 1, nbr = m >> 4, nch = w.NCH, m4 = m >> 2;
+  const int r0 = g * RC * nch;
+  const StepGeom gm = step_geom<RPW>(m);
+  const int rl = tid & (RC - 1), kg = tid / RC;
   const double* Qa = w.Q + (int64_t)a * w.ldq * L;
   const int jm = max(j - 1, 0);
+  const int prow = min(gm.p, WPS - 1) * RPW;   // the wave's rows within a chunk
+  const float* pbase = w.Phi + (int64_t)a * L * m + gm.sl * 256 + 4 * lane;
   // Every small load is issued before the Phi rows, so waiting for them leaves
   // the Phi loads in flight.  Every load is unconditional, with clamped indices
   // (surplus values are unused): a load under a branch would make the compiler
   // wait, where the branches join, as if the other path had issued no later
   // loads, i.e. for most of the Phi rows.
-  double qv[MAXT];                             // Q[k][row], k = kg + KG t < j
-#pragma unroll
-  for (int t = 0; t < MAXT; ++t) qv[t] = Qa[(int64_t)min(kg + KG * t, jm) * L + irc];
   const double* H2a = w.H2 + (int64_t)a * hs;
   const double h2v = H2a[min(tid, jm)];        // n_it <= 512
   const double z2 = H2a[w.ldq];
   const double apv = w.Apart[(int64_t)a * nbr + min(tid, nbr - 1)];
-  const double zp = w.Z1[(int64_t)a * L + irc];
-  const double qp = Qa[(int64_t)jm * L + irc];  // q_{j-1}, or q_0 when j = 0
   const double alv = w.alpha[(int64_t)a * w.n_it + min(tid, jm)];
   const double bev = w.beta[(int64_t)a * w.n_it + min(tid, jm)];
   const int stopped = w.stop[a];
   const double amax0 = w.amax[2 * a + (j & 1)];   // max |alpha| before step j
-  // waves without rows (ns not dividing 8) load those of the last row subset
-  const int prow = r0 + min(gm.p, WPS - 1) * RPW;
   double tv[4];
-  float4 v[RPW];
   {
     const double* tt = w.T + ((int64_t)a * w.ldq + (j & 1)) * m + gm.sl * 256 + 4 * lane;
 #pragma unroll
     for (int e = 0; e < 4; ++e) tv[e] = tt[e];
-    const float* base = w.Phi + (int64_t)a * L * m + gm.sl * 256 + 4 * lane;
-#pragma unroll
-    for (int i = 0; i < RPW; ++i) v[i] = *(const float4*)(base + (int64_t)min(prow + i, L - 1) * m);
   }
+  // a chunk's loads: Q[k][row] for k = kg + KG t < j, z1 and q_{j-1} of the
+  // thread's row, the wave's Phi rows
+  double qv[MAXT], zp, qp;
+  float4 v[RPW];
+  auto load_chunk = [&](int c) {
+    const int rc0 = r0 + RC * c;
+    const int irc = min(rc0 + rl, L - 1);
+#pragma unroll
+    for (int t = 0; t < MAXT; ++t) qv[t] = Qa[(int64_t)min(kg + KG * t, jm) * L + irc];
+    zp = w.Z1[(int64_t)a * L + irc];
+    qp = Qa[(int64_t)jm * L + irc];            // q_{j-1}, or q_0 when j = 0
+#pragma unroll
+    for (int i = 0; i < RPW; ++i) v[i] = *(const float4*)(pbase + (int64_t)min(rc0 + prow + i, L - 1) * m);
+  };
+  load_chunk(0);
   if (stopped) return;
   __shared__ double red[8];
   __shared__ double h2s[264], bes[264], gs[264];
-  __shared__ double rq[KG][RB + 1], rg[KG][RB + 1];
-  __shared__ double pr[RB][9];
-  __shared__ double sq[RB], sqp[RB], sg[RB], zs[RB];
+  __shared__ double rq[KG][RC + 1], rg[KG][RC + 1];
+  __shared__ double pr[RC][9];
+  __shared__ double zs[RC];
   __shared__ double cr[WPS > 1 ? 7 : 1][256];
   const double alpha_t = block_sum_f64((tid < nbr) ? apv : 0.0, red);   // |t~|^2
   double alpha = alpha_t, beta = 0.0, h2last = 0.0;
@@ -417,101 +433,154 @@ __global__ __launch_bounds__(512) void k_lz_step(LanczosWS w, int j, int dry) {
     w.neff[a] = j + 1;                                          // read by the next step
   }
   __syncthreads();
-  // Q_{j-1} h2 (for q_j) and Q_{j-1} g (for u) over this thread's k, then over
-  // the KG k-groups in order
-  {
-    double aq[2] = {0.0, 0.0}, ag[2] = {0.0, 0.0};
+  const double zn = sqrt(z2);
+  double* qdst = dry ? w.Zs + (int64_t)a * 2 * L : w.Q + ((int64_t)a * w.ldq + j) * L;
+  double* zdst = dry ? w.Zs + ((int64_t)a * 2 + 1) * L : w.Z1 + (int64_t)a * L;
+  double col[4] = {0.0, 0.0, 0.0, 0.0};      // Phi^T z1 over the block's rows
+  double h2acc[MAXT];                         // Q[k] z1 over this thread's rows
 #pragma unroll
-    for (int t = 0; t < MAXT; ++t) {
-      if (KG * t < j && kg + KG * t < j) {
-        aq[t & 1] = fma(qv[t], h2s[kg + KG * t], aq[t & 1]);
-        ag[t & 1] = fma(qv[t], gs[kg + KG * t], ag[t & 1]);
-      }
-    }
-    rq[kg][rl] = aq[0] + aq[1];
-    rg[kg][rl] = ag[0] + ag[1];
-  }
-  __syncthreads();
-  if (tid < RB) {
-    double q = qp, qm = 0.0, sub_g = 0.0;
-    if (j > 0) {
-      double sub = 0.0;
-      for (int k = 0; k < KG; ++k) {
-        sub += rq[k][rl];
-        sub_g += rg[k][rl];
-      }
-      q = (zp - sub) / beta;
-      qm = qp;
-      if (ir < L) (dry ? w.Zs + (int64_t)a * 2 * L : w.Q + ((int64_t)a * w.ldq + j) * L)[ir] = q;
-    }
-    sq[rl] = q;
-    sqp[rl] = qm;
-    sg[rl] = sub_g;
-  }
-  // Phi t~: per row, 4 products per lane summed over the wave (8 rows per
-  // butterfly), then over the slices
-  if (gm.rows) {
-    const int idx = ((lane >> 5) & 1) * 4 + ((lane >> 4) & 1) * 2 + ((lane >> 3) & 1);
+  for (int t = 0; t < MAXT; ++t) h2acc[t] = 0.0;
+  double qz = 0.0, zz = 0.0;                  // q_j . z1 and |z1|^2 (threads < RC)
+  const int idx = ((lane >> 5) & 1) * 4 + ((lane >> 4) & 1) * 2 + ((lane >> 3) & 1);
+  // one chunk; MORE: another chunk follows (stage this one in LDS, prefetch the next)
+  auto chunk = [&](int c, auto more_tag) {
+    constexpr bool MORE = decltype(more_tag)::value;
+    const int ir = r0 + RC * c + rl;
+    // row space: Q_{j-1} h2 (for q_j) and Q_{j-1} g (for u) over this thread's k
+    {
+      double aq[2] = {0.0, 0.0}, ag[2] = {0.0, 0.0};
 #pragma unroll
-    for (int i0 = 0; i0 < RPW; i0 += 8) {
-      double d[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        if (i0 + e < RPW) {
-          const float4 y = pin_row(v[i0 + e]);
-          double x = (double)y.x * tv[0];
-          x = fma((double)y.y, tv[1], x);
-          x = fma((double)y.z, tv[2], x);
-          d[e] = fma((double)y.w, tv[3], x);
-        } else {
-          d[e] = 0.0;
+      for (int t = 0; t < MAXT; ++t) {
+        if (KG * t < j && kg + KG * t < j) {
+          aq[t & 1] = fma(qv[t], h2s[kg + KG * t], aq[t & 1]);
+          ag[t & 1] = fma(qv[t], gs[kg + KG * t], ag[t & 1]);
         }
       }
-      const double tot = wave_sum8_f64(d);
-      if ((lane & 7) == 0 && i0 + idx < RPW) pr[gm.p * RPW + i0 + idx][gm.sl] = tot;
+      rq[kg][rl] = aq[0] + aq[1];
+      rg[kg][rl] = ag[0] + ag[1];
     }
-  }
-  __syncthreads();
-  if (tid < RB) {
-    double z = 0.0;
-    if (ir < L) {
-      double u = 0.0;
-      for (int q = 0; q < (m >> 8); ++q) u += pr[rl][q];
-      if (j > 0) u = (fma(sqrt(z2), u, -sg[rl]) - beta * h2last * sq[rl]) / beta;
-      z = (u - alpha * sq[rl]) - beta * sqp[rl];
-      (dry ? w.Zs + ((int64_t)a * 2 + 1) * L : w.Z1 + (int64_t)a * L)[ir] = z;
+    // Phi t~: per row, 4 products per lane summed over the wave (8 rows per
+    // butterfly), then over the slices
+    if (gm.rows) {
+#pragma unroll
+      for (int i0 = 0; i0 < RPW; i0 += 8) {
+        double d[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          if (i0 + e < RPW) {
+            const float4 y = pin_row(v[i0 + e]);
+            double x = (double)y.x * tv[0];
+            x = fma((double)y.y, tv[1], x);
+            x = fma((double)y.z, tv[2], x);
+            d[e] = fma((double)y.w, tv[3], x);
+          } else {
+            d[e] = 0.0;
+          }
+        }
+        const double tot = wave_sum8_f64(d);
+        if ((lane & 7) == 0 && i0 + idx < RPW) pr[gm.p * RPW + i0 + idx][gm.sl] = tot;
+      }
     }
-    zs[rl] = z;
+    // this chunk's row values, then (another chunk following) stage its Phi rows
+    // in LDS and put the next chunk's loads in flight
+    double qvc[MAXT];
+#pragma unroll
+    for (int t = 0; t < MAXT; ++t) qvc[t] = qv[t];
+    const double zpc = zp, qpc = qp;
+    if constexpr (MORE) {
+      if (gm.rows) {
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) phis[(gm.p * RPW + i) * m4 + gm.sl * 64 + lane] = pin_row(v[i]);
+      }
+      load_chunk(c + 1);
+    }
+    __syncthreads();
+    // sums over the KG k-groups: wave 0, lane = (part, row), 4 parts of KG / 4
+    // groups, combined by two butterflies (fixed order)
+    double sub = 0.0, sub_g = 0.0;
+    if (tid < 64 && j > 0) {
+      const int k0 = (tid >> 4) * (KG / 4);
+#pragma unroll
+      for (int k = 0; k < KG / 4; ++k) {
+        sub += rq[k0 + k][rl];
+        sub_g += rg[k0 + k][rl];
+      }
+      sub += __shfl_xor(sub, 16, 64);
+      sub_g += __shfl_xor(sub_g, 16, 64);
+      sub += __shfl_xor(sub, 32, 64);
+      sub_g += __shfl_xor(sub_g, 32, 64);
+    }
+    if (tid < RC) {
+      double q = qpc, qm = 0.0;
+      if (j > 0) {
+        q = (zpc - sub) / beta;
+        qm = qpc;
+        if (ir < L) qdst[ir] = q;
+      }
+      double z = 0.0;
+      if (ir < L) {
+        double u = 0.0;
+        for (int s2 = 0; s2 < (m >> 8); ++s2) u += pr[rl][s2];
+        if (j > 0) u = (fma(zn, u, -sub_g) - beta * h2last * q) / beta;
+        z = (u - alpha * q) - beta * qm;
+        zdst[ir] = z;
+      }
+      zs[rl] = z;
+      qz = fma(q, z, qz);
+      zz = fma(z, z, zz);
+    }
+    __syncthreads();
+    // column sums of the chunk (its rows from LDS, or still in registers for the
+    // last chunk) and the h2 terms of this thread's row
+    if (gm.rows) {
+#pragma unroll
+      for (int i = 0; i < RPW; ++i) {
+        const double zr = zs[gm.p * RPW + i];
+        float4 x;
+        if constexpr (MORE) x = phis[(gm.p * RPW + i) * m4 + gm.sl * 64 + lane];
+        else x = pin_row(v[i]);
+        col[0] = fma((double)x.x, zr, col[0]);
+        col[1] = fma((double)x.y, zr, col[1]);
+        col[2] = fma((double)x.z, zr, col[2]);
+        col[3] = fma((double)x.w, zr, col[3]);
+      }
+    }
+    const double zl = zs[rl];
+#pragma unroll
+    for (int t = 0; t < MAXT; ++t) h2acc[t] = fma(qvc[t], zl, h2acc[t]);
+    if constexpr (MORE) __syncthreads();       // before the staged rows are replaced
+  };
+  if constexpr (STAGED) {
+    for (int c = 0; c + 1 < nch; ++c) chunk(c, std::true_type{});
   }
-  __syncthreads();
-  step_colsums<RB, RPW>(w, a, g, gm, v, zs, cr);
-  // partials of h2_k = sum over the rows of Q[k] z1: k < j from the registers
-  // (summed over the RB rows of each half or quarter wave, 8 slots per
-  // butterfly), then k = j and |z1|^2
+  chunk(nch - 1, std::false_type{});
+  lz_store_colsums<WPS>(w, a, g, gm, col, cr);
+  // h2 partials: k < j summed over the 16 rows of each quarter wave (8 slots per
+  // butterfly), then k = j and |z1|^2 over the first 16 threads
   double* hp = w.H2part + ((int64_t)a * w.G3 + g) * hs;
-  const double zl = zs[rl];
-  const int hidx = (RB == 32) ? ((lane >> 4) & 1) * 4 + ((lane >> 3) & 1) * 2 + ((lane >> 2) & 1)
-                              : ((lane >> 3) & 1) * 4 + ((lane >> 2) & 1) * 2 + ((lane >> 1) & 1);
+  const int hidx = ((lane >> 3) & 1) * 4 + ((lane >> 2) & 1) * 2 + ((lane >> 1) & 1);
 #pragma unroll
   for (int t0 = 0; t0 < MAXT; t0 += 8) {
     if (KG * t0 < j) {                         // block-uniform
       double v8[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        v8[e] = (t0 + e < MAXT && kg + KG * (t0 + e) < j) ? qv[min(t0 + e, MAXT - 1)] * zl : 0.0;
-      const double tot = (RB == 32) ? half_sum8_f64(v8) : quarter_sum8_f64(v8);
+        v8[e] = (t0 + e < MAXT && kg + KG * (t0 + e) < j) ? h2acc[min(t0 + e, MAXT - 1)] : 0.0;
+      const double tot = quarter_sum8_f64(v8);
       const int k = kg + KG * (t0 + hidx);
       // lanes that agree in the index bits hold equal sums: one of them writes
-      if ((lane & (RB == 32 ? 3 : 1)) == 0 && t0 + hidx < MAXT && k < j) hp[k] = tot;
+      if ((lane & 1) == 0 && t0 + hidx < MAXT && k < j) hp[k] = tot;
     }
   }
-  if (tid < 2 * RB) {
-    const double x = (tid < RB) ? sq[rl] * zs[rl] : zs[rl] * zs[rl];
-    double t = x;
+  if (tid < 64) {
+    // all of wave 0 takes part in every shuffle (a lane that skips one supplies
+    // no value to it): lanes RC..2RC-1 take |z1|^2 of lanes 0..RC-1
+    const double zsh = __shfl(zz, tid & (RC - 1), 64);
+    double t = (tid < RC) ? qz : zsh;
 #pragma unroll
-    for (int o = RB / 2; o >= 1; o >>= 1) t += __shfl_xor(t, o, 64);
+    for (int o = RC / 2; o >= 1; o >>= 1) t += __shfl_xor(t, o, 64);
     if (tid == 0) hp[j] = t;
-    if (tid == RB) hp[w.ldq] = t;
+    if (tid == RC) hp[w.ldq] = t;
   }
 }
 
@@ -603,61 +672,58 @@ __global__ void k_lz_start(LanczosWS w, const double* __restrict__ q1) {
 }
 
 
-// rows per wave of the pass: RB / (8 / ns) for ns = m / 256 column slices
-static int step_rpw(int m, int rb) {
-  const int wps = 8 / (m >> 8);
-  return rb / wps;
-}
+// rows per wave of a 16-row chunk: 16 / (8 / ns) for ns = m / 256 column slices
+static int step_rpw(int m) { return LZ_RC / (8 / (m >> 8)); }
 
-template <int RB, int RPW>
+template <int RPW>
 static void launch_init_t(const LanczosWS& w, hipStream_t s) {
-  hipLaunchKernelGGL((k_lz_init<RB, RPW>), dim3(w.G3, w.n_act), dim3(512), 0, s, w);
-}
-template <int RB>
-static void launch_init_r(const LanczosWS& w, hipStream_t s) {
-  switch (step_rpw(w.m, RB)) {
-    case RB / 8: launch_init_t<RB, RB / 8>(w, s); break;
-    case RB / 4: launch_init_t<RB, RB / 4>(w, s); break;
-    case RB / 2: launch_init_t<RB, RB / 2>(w, s); break;
-    default: launch_init_t<RB, RB>(w, s); break;
-  }
+  hipLaunchKernelGGL(k_lz_init<RPW>, dim3(w.G3, w.n_act), dim3(512), 0, s, w);
 }
 static void launch_init(const LanczosWS& w, hipStream_t s) {
-  if (w.RB == 16) launch_init_r<16>(w, s);
-  else launch_init_r<32>(w, s);
-}
-
-template <int RB, int RPW, int MAXT>
-static void launch_step_t(const LanczosWS& w, int j, int dry, hipStream_t s, hipEvent_t e0,
-                          hipEvent_t e1) {
-  const dim3 g(w.G3, w.n_act), b(512);
-  auto k = k_lz_step<RB, RPW, MAXT>;
-  if (e0) hipExtLaunchKernelGGL(k, g, b, 0, s, e0, e1, 0, w, j, dry);
-  else hipLaunchKernelGGL(k, g, b, 0, s, w, j, dry);
-}
-// MAXT: the smallest slot count with (512 / RB) MAXT >= n_it
-template <int RB, int RPW>
-static void launch_step_m(const LanczosWS& w, int j, int dry, hipStream_t s, hipEvent_t e0,
-                          hipEvent_t e1) {
-  constexpr int KG = 512 / RB;
-  if (w.n_it <= KG * 4) launch_step_t<RB, RPW, 4>(w, j, dry, s, e0, e1);
-  else if (w.n_it <= KG * 8) launch_step_t<RB, RPW, 8>(w, j, dry, s, e0, e1);
-  else launch_step_t<RB, RPW, 16>(w, j, dry, s, e0, e1);
-}
-template <int RB>
-static void launch_step_r(const LanczosWS& w, int j, int dry, hipStream_t s, hipEvent_t e0,
-                          hipEvent_t e1) {
-  switch (step_rpw(w.m, RB)) {
-    case RB / 8: launch_step_m<RB, RB / 8>(w, j, dry, s, e0, e1); break;
-    case RB / 4: launch_step_m<RB, RB / 4>(w, j, dry, s, e0, e1); break;
-    case RB / 2: launch_step_m<RB, RB / 2>(w, j, dry, s, e0, e1); break;
-    default: launch_step_m<RB, RB>(w, j, dry, s, e0, e1); break;
+  switch (step_rpw(w.m)) {
+    case 2: launch_init_t<2>(w, s); break;
+    case 4: launch_init_t<4>(w, s); break;
+    case 8: launch_init_t<8>(w, s); break;
+    default: launch_init_t<16>(w, s); break;
   }
 }
-static void launch_step(const LanczosWS& w, int j, int dry, hipStream_t s, hipEvent_t e0 = nullptr,
-                        hipEvent_t e1 = nullptr) {
-  if (w.RB == 16) launch_step_r<16>(w, j, dry, s, e0, e1);
-  else launch_step_r<32>(w, j, dry, s, e0, e1);
+
+template <int RPW, int MAXT, bool STAGED>
+static hipError_t launch_step_s(const LanczosWS& w, int j, int dry, hipStream_t s, hipEvent_t e0,
+                                hipEvent_t e1) {
+  const dim3 g(w.G3, w.n_act), b(512);
+  auto k = k_lz_step<RPW, MAXT, STAGED>;
+  const size_t lds = STAGED ? (size_t)LZ_RC * w.m * sizeof(float) : 0;
+  if (lds > 65536) {
+    const hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  if (e0) hipExtLaunchKernelGGL(k, g, b, lds, s, e0, e1, 0, w, j, dry);
+  else hipLaunchKernelGGL(k, g, b, lds, s, w, j, dry);
+  return hipSuccess;
+}
+template <int RPW, int MAXT>
+static hipError_t launch_step_t(const LanczosWS& w, int j, int dry, hipStream_t s, hipEvent_t e0,
+                                hipEvent_t e1) {
+  if (w.NCH > 1) return launch_step_s<RPW, MAXT, true>(w, j, dry, s, e0, e1);
+  return launch_step_s<RPW, MAXT, false>(w, j, dry, s, e0, e1);
+}
+// MAXT: the smallest slot count with 32 MAXT >= n_it
+template <int RPW>
+static hipError_t launch_step_m(const LanczosWS& w, int j, int dry, hipStream_t s, hipEvent_t e0,
+                                hipEvent_t e1) {
+  if (w.n_it <= 128) return launch_step_t<RPW, 4>(w, j, dry, s, e0, e1);
+  return launch_step_t<RPW, 8>(w, j, dry, s, e0, e1);
+}
+static hipError_t launch_step(const LanczosWS& w, int j, int dry, hipStream_t s,
+                              hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr) {
+  switch (step_rpw(w.m)) {
+    case 2: return launch_step_m<2>(w, j, dry, s, e0, e1);
+    case 4: return launch_step_m<4>(w, j, dry, s, e0, e1);
+    case 8: return launch_step_m<8>(w, j, dry, s, e0, e1);
+    default: return launch_step_m<16>(w, j, dry, s, e0, e1);
+  }
 }
 
 static void launch_reduce(const LanczosWS& w, int j, hipStream_t s) {
@@ -668,14 +734,16 @@ static void launch_reduce(const LanczosWS& w, int j, hipStream_t s) {
 hipError_t launch_lanczos(const LanczosWS& w, const double* q1_act, hipStream_t s,
                           const hipEvent_t* ev_before, const hipEvent_t* ev_after) {
   (void)hipGetLastError();
-  if (w.m % 256 != 0 || w.m > 2048 || w.n_it > 256 || w.n_it < 1 || (w.RB != 16 && w.RB != 32) ||
-      w.G3 != (w.L + w.RB - 1) / w.RB)
+  if (w.m % 256 != 0 || w.m > 2048 || w.n_it > 256 || w.n_it < 1 || w.NCH < 1 ||
+      w.G3 != (w.L + LZ_RC * w.NCH - 1) / (LZ_RC * w.NCH))
     return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_lz_start, dim3((w.L + 255) / 256, w.n_act), dim3(256), 0, s, w, q1_act);
   launch_init(w, s);
   launch_reduce(w, -1, s);
   for (int j = 0; j < w.n_it; ++j) {
-    launch_step(w, j, 0, s, ev_before ? ev_before[j] : nullptr, ev_after ? ev_after[j] : nullptr);
+    const hipError_t e = launch_step(w, j, 0, s, ev_before ? ev_before[j] : nullptr,
+                                     ev_after ? ev_after[j] : nullptr);
+    if (e != hipSuccess) return e;
     if (j + 1 < w.n_it) launch_reduce(w, j, s);
   }
   hipLaunchKernelGGL(k_lz_h2sum, dim3((w.n_it + 15) / 16 + 1, w.n_act), dim3(512), 0, s, w);
@@ -686,7 +754,10 @@ hipError_t launch_lanczos(const LanczosWS& w, const double* q1_act, hipStream_t 
 // reps x the pass of step j, launched as in launch_lanczos but dry
 hipError_t launch_lanczos_passes(const LanczosWS& w, int j, int reps, hipStream_t s) {
   (void)hipGetLastError();
-  for (int q = 0; q < reps; ++q) launch_step(w, j, 1, s);
+  for (int q = 0; q < reps; ++q) {
+    const hipError_t e = launch_step(w, j, 1, s);
+    if (e != hipSuccess) return e;
+  }
   return hipGetLastError();
 }
 

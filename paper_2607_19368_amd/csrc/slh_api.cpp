@@ -696,11 +696,17 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
       w.n_it = n_it;
       w.ldq = n_it + 1;
       w.tol = c->tol;
-#ifndef SLH_LZ_RB
-#define SLH_LZ_RB 16
-#endif
-      w.RB = SLH_LZ_RB;
-      w.G3 = (int)((L + w.RB - 1) / w.RB);
+      // chunks of 16 rows per block of the pass: one chunk per block while the
+      // blocks fit two per CU (all resident at once); beyond that, about one
+      // block per CU, each streaming its chunks with the next in flight (the
+      // current one staged in LDS, 16 m floats, so such a block runs alone on
+      // its CU)
+      {
+        const int64_t chunks = (int64_t)na * ((L + 15) / 16);
+        const int64_t ncu = std::max(1, c->n_cu);
+        w.NCH = chunks <= 2 * ncu ? 1 : (int)((chunks + ncu - 1) / ncu);
+        w.G3 = (int)((L + 16 * w.NCH - 1) / (16 * w.NCH));
+      }
       const size_t hs = (size_t)w.ldq + 1;
       ENSURE(c, c->Q, (size_t)na * w.ldq * L * 8);
       ENSURE(c, c->T, (size_t)na * w.ldq * c->m * 8);

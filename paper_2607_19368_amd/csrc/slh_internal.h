@@ -52,8 +52,8 @@ struct LanczosWS {
   double* amax;                 // [n_act][2] max |alpha| so far (breakdown scale): step j reads
                                 //   slot j & 1 and writes the other
   double tol;
-  int RB;                       // rows per block of the pass (16 or 32)
-  int G3;                       // row groups of RB rows (one block of the pass each)
+  int NCH;                      // chunks of 16 rows per block of the pass
+  int G3;                       // row groups of 16 NCH rows (one block of the pass each)
 };
 // One pass over Phi per step (k_lz_step) and one reduction.  ev_before/ev_after
 // (may be NULL): n_it events each, receiving the start and end timestamps of
