@@ -4,31 +4,23 @@
 // Each window runs its own recurrence; all windows advance in lockstep (grid
 // dimension y = window).  Vectors and every reduction are fp64; Phi is fp32.
 //
-// Step j keeps q_j (Q[j], length L) and t_j = Phi^T q_j (T[j], length m) and
-// runs four kernels:
-//   phit    partials of Phi^T v, v = q_0 (j = 0) or z1 of step j-1 (the vector
-//           after the first Gram-Schmidt pass), over (row group, 256-column
-//           slice) blocks; the first blocks of the launch reduce the partials
-//           of h2 = Q^T z1 and |z1|^2 of step j-1.
-//   finish  beta_{j-1} = |z1 - Q h2| = sqrt(|z1|^2 - |h2|^2) (Q orthonormal),
-//           the breakdown test, and t_j = (Phi^T z1 - sum_k h2_k t_k) / beta
-//           (the second Gram-Schmidt pass applied in feature space; its
-//           coefficients h2 are at rounding level).
-//   phiu    u = Phi t_j (= A q_j): the same (row group, column slice) blocks
-//           write per-slice partial row dots; the first blocks of the launch
-//           form h1 = Q_j^T u as t_k^T t_j (k <= j), the same inner products
-//           taken in feature space, so no pass over Q is needed.
-//   orth    per 32 rows: u from its slice partials; q_j = (z1 - Q_{j-1} h2) /
-//           beta (second pass in row space, stored as Q[j]); alpha_j = h1_j;
-//           z1 = u - Q_j h1 (first classical Gram-Schmidt pass of step j);
-//           partials of h2 = Q_j^T z1 and |z1|^2.  One read of Q_j feeds both
-//           the q_j update and z1.
-// Phi is streamed twice per step: Phi^T z1 is always streamed.  (Forming
-// Phi^T q_{j+1} from Phi^T u through the whole three-term recurrence would save
-// a pass but multiplies rounding errors by alpha_j / beta_j every step.)  All
-// partial sums are combined in a fixed order, so results are bitwise
-// reproducible.  alpha_j and beta_j are those of Algorithm 2: alpha_j before any
-// subtraction, beta_j the norm after re-orthogonalization.
+// A run is k_lz_start (q_0), k_lz_init (partials of Phi^T q_0), k_lz_reduce
+// (t_0 = Phi^T q_0), then per step j one pass and (but for the last step) one
+// reduction:
+//   k_lz_step    one read of the step's Phi rows: q_j (second Gram-Schmidt pass
+//                of step j-1, in row space), u = A q_j from the row dots with
+//                t~_j, z1 = u - alpha_j q_j - beta_{j-1} q_{j-1} (the
+//                three-term recurrence, i.e. the first pass), and the partials
+//                of Phi^T z1, of h2 = Q_j^T z1 and of |z1|^2 per block of rows.
+//   k_lz_reduce  t~_{j+1} = Phi^T z1 / |z1| with the partials of |t~|^2, and h2
+//                and |z1|^2 for the next pass.
+// t~_{j+1} differs from Phi^T q_{j+1} by the rounding-level h2 term, which the
+// next pass carries into u and alpha through the Lanczos relation (see
+// k_lz_step); the basis Q stays fully re-orthogonalized in row space.
+// k_lz_h2sum and k_lz_last_beta give beta of the last step.  All partial sums are
+// combined in a fixed order, so results are bitwise reproducible.  alpha_j and
+// beta_j are those of Algorithm 2: alpha_j = q_j^T A q_j, beta_j the norm after
+// re-orthogonalization.
 #include "slh_device.h"
 #include "slh_internal.h"
 
