@@ -170,19 +170,29 @@ __device__ __forceinline__ double block_colsum(const double* __restrict__ src, i
 }
 
 // |z1|^2 of window a: the sum over the row groups of H2part[g][ldq], by a block
-// of 512 threads in a fixed order (every caller gets the same bits).  Four
-// clamped loads per thread and batch.
-__device__ __forceinline__ double z2_sum(const LanczosWS& w, int a, double* red) {
+// of 512 threads in a fixed order (every caller gets the same bits).  Split in
+// a load part (four clamped loads per thread and batch, for G3 <= 2048 one
+// batch) and the reduction, so that a caller can put other loads in flight
+// between them.
+struct Z2Part {
+  double v[4];
+};
+__device__ __forceinline__ Z2Part z2_load(const LanczosWS& w, int a, int g0) {
   const int hs = w.ldq + 1, G = w.G3, tid = threadIdx.x;
   const double* src = w.H2part + (int64_t)a * G * hs + w.ldq;
+  Z2Part p;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) p.v[e] = src[(int64_t)min(g0 + tid + 512 * e, G - 1) * hs];
+  return p;
+}
+__device__ __forceinline__ double z2_add(const Z2Part& p, int G, int g0, double acc) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) acc += (g0 + (int)threadIdx.x + 512 * e < G) ? p.v[e] : 0.0;
+  return acc;
+}
+__device__ __forceinline__ double z2_sum(const LanczosWS& w, int a, double* red) {
   double acc = 0.0;
-  for (int g0 = 0; g0 < G; g0 += 4 * 512) {
-    double v[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) v[e] = src[(int64_t)min(g0 + tid + 512 * e, G - 1) * hs];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) acc += (g0 + tid + 512 * e < G) ? v[e] : 0.0;
-  }
+  for (int g0 = 0; g0 < w.G3; g0 += 4 * 512) acc = z2_add(z2_load(w, a, g0), w.G3, g0, acc);
   return block_sum_f64(acc, red);
 }
 
@@ -332,8 +342,10 @@ __global__ __launch_bounds__(512) void k_lz_init(LanczosWS w) {
 // ---------------------------------------------------------------------------
 // STAGED: blocks of NCH > 1 chunks (else NCH = 1, no LDS staging and a smaller
 // register footprint, two blocks per CU).
+// Unstaged: at most 128 VGPRs (four waves per SIMD), so that two blocks share a
+// CU and all of the pass's blocks are resident at once.
 template <int RPW, int MAXT, bool STAGED>
-__global__ __launch_bounds__(512) void k_lz_step(LanczosWS w, int j, int dry) {
+__global__ __launch_bounds__(512, STAGED ? 2 : 4) void k_lz_step(LanczosWS w, int j, int dry) {
   constexpr int RC = LZ_RC, WPS = RC / RPW, KG = 512 / RC;
   extern __shared__ float4 phis[];             // [RC][m / 4] staged chunk
   const int a = blockIdx.y, g = blockIdx.x;
@@ -599,13 +611,20 @@ __global__ __launch_bounds__(512) void k_lz_reduce(LanczosWS w, int j) {
   if (w.stop[a]) return;
   __shared__ double red[8];
   __shared__ double rs[32][17];
-  // |z1|^2 first: its loads go out ahead of the column sums' (same routine and
-  // order as the h2 block, so t and the next pass use the same |z1|)
-  double z2 = 1.0;
-  if (j >= 0) z2 = z2_sum(w, a, red);
+  // |z1|^2 and the column sums with both sets of loads in flight together (the
+  // same |z1|^2 routine and order as the h2 block, so t and the next pass use
+  // the same |z1|); the |z1|^2 reduction's barriers come after the sums' loads
+  double z2acc = 0.0;
+  const Z2Part zp0 = z2_load(w, a, 0);          // unconditional: valid for any j
   const int cnt = (w.G3 - pl + 31) / 32;
   const double s = sum_strided(w.Spart + ((int64_t)a * w.G3 + pl) * m + c, (int64_t)32 * m,
                                cnt > 0 ? cnt : 0);
+  double z2 = 1.0;
+  if (j >= 0) {
+    z2acc = z2_add(zp0, w.G3, 0, z2acc);
+    for (int g0 = 4 * 512; g0 < w.G3; g0 += 4 * 512) z2acc = z2_add(z2_load(w, a, g0), w.G3, g0, z2acc);
+    z2 = block_sum_f64(z2acc, red);
+  }
   rs[pl][cl] = s;
   __syncthreads();
   if (tid < 16) {
