@@ -492,14 +492,18 @@ __global__ __launch_bounds__(512, STAGED ? 2 : 4) void k_lz_step(LanczosWS w, in
       sub_g += __shfl_xor(sub_g, 32, 64);
     }
   };
-  // q_j and z1 of the thread's row (threads < RC), stored, into zs
-  auto row_z = [&](int ir, double sub, double sub_g, double zpc, double qpc) {
-    double q = qpc, qm = 0.0;
+  // q_j of the thread's row (threads < RC; stored) and the remaining terms of u
+  auto row_q = [&](int ir, double sub, double zpc, double qpc, double& q, double& qm) {
+    q = qpc;
+    qm = 0.0;
     if (j > 0) {
       q = (zpc - sub) / beta;
       qm = qpc;
       if (ir < L) qdst[ir] = q;
     }
+  };
+  // z1 of the thread's row (threads < RC), stored, into zs
+  auto row_z = [&](int ir, double sub_g, double q, double qm) {
     double z = 0.0;
     if (ir < L) {
       double u = 0.0;
@@ -546,7 +550,16 @@ __global__ __launch_bounds__(512, STAGED ? 2 : 4) void k_lz_step(LanczosWS w, in
 #pragma unroll
     for (int t = 0; t < MAXT; ++t) qvc[t] = qv[t];
     const double zpc = zp, qpc = qp;
-    double sub, sub_g;
+    // Staged: q_j and the k-group sums before the row dots (they need only the
+    // prologue, so this barrier falls while the chunk's Phi rows are in flight).
+    // Unstaged they follow the dots (taken before, they cost the 128-VGPR
+    // kernel a spill: 19.0 against 18.2 us at qwen7b).
+    double sub = 0.0, sub_g = 0.0, q = 0.0, qm = 0.0;
+    if constexpr (STAGED) {
+      __syncthreads();
+      kgroup_sums(sub, sub_g);
+      if (tid < RC) row_q(ir, sub, zpc, qpc, q, qm);
+    }
     if constexpr (MORE) {
       // stage this chunk's Phi rows in LDS and put the next chunk's loads in flight
       dots(0, RPW);
@@ -556,8 +569,7 @@ __global__ __launch_bounds__(512, STAGED ? 2 : 4) void k_lz_step(LanczosWS w, in
       }
       load_chunk(c + 1);
       __syncthreads();
-      kgroup_sums(sub, sub_g);
-      if (tid < RC) row_z(ir, sub, sub_g, zpc, qpc);
+      if (tid < RC) row_z(ir, sub_g, q, qm);
       __syncthreads();
       colsums(0, RPW, true);
     } else {
@@ -565,8 +577,11 @@ __global__ __launch_bounds__(512, STAGED ? 2 : 4) void k_lz_step(LanczosWS w, in
       // the second half arrives, measured slower: 19.7 against 18.5 us at qwen7b)
       dots(0, RPW);
       __syncthreads();
-      kgroup_sums(sub, sub_g);
-      if (tid < RC) row_z(ir, sub, sub_g, zpc, qpc);
+      if constexpr (!STAGED) {
+        kgroup_sums(sub, sub_g);
+        if (tid < RC) row_q(ir, sub, zpc, qpc, q, qm);
+      }
+      if (tid < RC) row_z(ir, sub_g, q, qm);
       __syncthreads();
       colsums(0, RPW, false);
     }
