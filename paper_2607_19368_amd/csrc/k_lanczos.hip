@@ -144,26 +144,28 @@ __device__ __forceinline__ double sum_strided(const double* __restrict__ src, in
   return acc[0];
 }
 
-// Column reduction by one block of NT threads: returns, in the threads with
-// threadIdx.x < CPB, sum_{g<G} src[g*ld + c0 + threadIdx.x] (0 past ncol);
-// CPB columns x (NT / CPB) partial lanes, fixed order.  All threads must call it.
-template <int CPB, int NT>
-__device__ __forceinline__ double block_colsum(const double* __restrict__ src, int64_t ld, int G,
-                                               int c0, int ncol) {
-  constexpr int PL = NT / CPB;
-  __shared__ double red[PL][CPB + 1];
-  const int tid = threadIdx.x, cl = tid % CPB, pl = tid / CPB;
+// Column reduction by one block of 512 threads over 16 columns: returns, in
+// threads < 16, sum_{g<G} src[g*ld + c0 + threadIdx.x] (0 past ncol).  Thread
+// (cl = tid & 15, pl = tid >> 4) sums rows pl, pl + 32, ...; the four partial
+// lanes of a column within a wave are added by two butterflies and the 8 waves'
+// sums in LDS, all in a fixed order.  All threads must call it.
+__device__ __forceinline__ double colsum16(const double* __restrict__ src, int64_t ld, int G,
+                                           int c0, int ncol) {
+  __shared__ double red[8][17];
+  const int tid = threadIdx.x, cl = tid & 15, pl = tid >> 4;
   const int col = c0 + cl;
   double acc = 0.0;
   if (col < ncol) {
-    const int cnt = (G - pl + PL - 1) / PL;
-    acc = sum_strided(src + (int64_t)pl * ld + col, (int64_t)PL * ld, cnt > 0 ? cnt : 0);
+    const int cnt = (G - pl + 31) / 32;
+    acc = sum_strided(src + (int64_t)pl * ld + col, (int64_t)32 * ld, cnt > 0 ? cnt : 0);
   }
-  red[pl][cl] = acc;
+  acc += __shfl_xor(acc, 16, 64);
+  acc += __shfl_xor(acc, 32, 64);
+  if ((tid & 63) < 16) red[tid >> 6][cl] = acc;
   __syncthreads();
   double t = 0.0;
-  if (tid < CPB && col < ncol) {
-    for (int p = 0; p < PL; ++p) t += red[p][cl];
+  if (tid < 16 && col < ncol) {
+    for (int w = 0; w < 8; ++w) t += red[w][cl];
   }
   __syncthreads();
   return t;
@@ -209,7 +211,7 @@ __device__ __forceinline__ void h2_reduce_block(const LanczosWS& w, int a, int j
     if (threadIdx.x == 0) dst[w.ldq] = v;
   } else {
     const int c0 = g * 16;
-    const double v = block_colsum<16, 512>(hp, hs, w.G3, c0, j);
+    const double v = colsum16(hp, hs, w.G3, c0, j);
     if (threadIdx.x < 16 && c0 + threadIdx.x < j) dst[c0 + threadIdx.x] = v;
   }
 }
@@ -646,7 +648,7 @@ __global__ __launch_bounds__(512) void k_lz_reduce(LanczosWS w, int j) {
   const int c = g * 16 + cl;                   // m is a multiple of 16
   if (w.stop[a]) return;
   __shared__ double red[8];
-  __shared__ double rs[32][17];
+  __shared__ double rs[8][17];
   // |z1|^2 and the column sums with both sets of loads in flight together (the
   // same |z1|^2 routine and order as the h2 block, so t and the next pass use
   // the same |z1|); the |z1|^2 reduction's barriers come after the sums' loads
@@ -661,11 +663,15 @@ __global__ __launch_bounds__(512) void k_lz_reduce(LanczosWS w, int j) {
     for (int g0 = 4 * 512; g0 < w.G3; g0 += 4 * 512) z2acc = z2_add(z2_load(w, a, g0), w.G3, g0, z2acc);
     z2 = block_sum_f64(z2acc, red);
   }
-  rs[pl][cl] = s;
+  // the four partial lanes of a column within a wave by two butterflies, the 8
+  // waves' sums in LDS (fixed order)
+  double sw = s + __shfl_xor(s, 16, 64);
+  sw += __shfl_xor(sw, 32, 64);
+  if ((tid & 63) < 16) rs[tid >> 6][cl] = sw;
   __syncthreads();
   if (tid < 16) {
     double S = 0.0;
-    for (int q = 0; q < 32; ++q) S += rs[q][cl];
+    for (int q = 0; q < 8; ++q) S += rs[q][cl];
     double t = S;
     if (j >= 0) t = z2 > 0.0 ? S / sqrt(z2) : 0.0;
     w.T[((int64_t)a * w.ldq + ((j + 1) & 1)) * m + c] = t;
