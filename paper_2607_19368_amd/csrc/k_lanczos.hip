@@ -633,7 +633,12 @@ __global__ __launch_bounds__(512, STAGED ? 2 : 4) void k_lz_step(LanczosWS w, in
 // / |z1| (Phi^T q_0 for the initial pass) into T[(j + 1) & 1], and the block's
 // partial of |t_{j+1}|^2.
 // ---------------------------------------------------------------------------
+// CPB columns per column block, PL = 512 / CPB partial lanes over the row groups
+// (CPB grows as G3 shrinks, so that few lanes idle; see launch_reduce).
+template <int CPB>
 __global__ __launch_bounds__(512) void k_lz_reduce(LanczosWS w, int j) {
+  constexpr int PL = 512 / CPB;                     // partial lanes per column
+  constexpr int WL = CPB < 64 ? 64 / CPB : 1;       // ... of them within one wave
   const int a = blockIdx.y, tid = threadIdx.x;
   const int m = w.m, hs = w.ldq + 1;
   const int nx = (j >= 0) ? (j + 16) / 16 + 1 : 0;
@@ -644,18 +649,18 @@ __global__ __launch_bounds__(512) void k_lz_reduce(LanczosWS w, int j) {
     return;
   }
   g -= nx;
-  const int cl = tid & 15, pl = tid >> 4;
-  const int c = g * 16 + cl;                   // m is a multiple of 16
+  const int cl = tid % CPB, pl = tid / CPB;
+  const int c = g * CPB + cl;                       // m is a multiple of CPB
   if (w.stop[a]) return;
   __shared__ double red[8];
-  __shared__ double rs[8][17];
+  __shared__ double rs[PL / WL][CPB + 1];
   // |z1|^2 and the column sums with both sets of loads in flight together (the
   // same |z1|^2 routine and order as the h2 block, so t and the next pass use
   // the same |z1|); the |z1|^2 reduction's barriers come after the sums' loads
   double z2acc = 0.0;
-  const Z2Part zp0 = z2_load(w, a, 0);          // unconditional: valid for any j
-  const int cnt = (w.G3 - pl + 31) / 32;
-  const double s = sum_strided(w.Spart + ((int64_t)a * w.G3 + pl) * m + c, (int64_t)32 * m,
+  const Z2Part zp0 = z2_load(w, a, 0);              // unconditional: valid for any j
+  const int cnt = (w.G3 - pl + PL - 1) / PL;
+  const double s = sum_strided(w.Spart + ((int64_t)a * w.G3 + pl) * m + c, (int64_t)PL * m,
                                cnt > 0 ? cnt : 0);
   double z2 = 1.0;
   if (j >= 0) {
@@ -663,22 +668,24 @@ __global__ __launch_bounds__(512) void k_lz_reduce(LanczosWS w, int j) {
     for (int g0 = 4 * 512; g0 < w.G3; g0 += 4 * 512) z2acc = z2_add(z2_load(w, a, g0), w.G3, g0, z2acc);
     z2 = block_sum_f64(z2acc, red);
   }
-  // the four partial lanes of a column within a wave by two butterflies, the 8
+  // the WL partial lanes of a column within a wave by butterflies, then the
   // waves' sums in LDS (fixed order)
-  double sw = s + __shfl_xor(s, 16, 64);
-  sw += __shfl_xor(sw, 32, 64);
-  if ((tid & 63) < 16) rs[tid >> 6][cl] = sw;
+  double sw = s;
+#pragma unroll
+  for (int o = CPB; o < 64; o <<= 1) sw += __shfl_xor(sw, o, 64);
+  if (pl % WL == 0) rs[pl / WL][cl] = sw;
   __syncthreads();
-  if (tid < 16) {
+  if (tid < CPB) {
     double S = 0.0;
-    for (int q = 0; q < 8; ++q) S += rs[q][cl];
+    for (int q = 0; q < PL / WL; ++q) S += rs[q][cl];
     double t = S;
     if (j >= 0) t = z2 > 0.0 ? S / sqrt(z2) : 0.0;
     w.T[((int64_t)a * w.ldq + ((j + 1) & 1)) * m + c] = t;
+    // |t|^2 partials per 16 columns
     double t2 = t * t;
 #pragma unroll
     for (int o = 8; o >= 1; o >>= 1) t2 += __shfl_xor(t2, o, 64);
-    if (tid == 0) w.Apart[(int64_t)a * (m >> 4) + g] = t2;
+    if ((tid & 15) == 0) w.Apart[(int64_t)a * (m >> 4) + (c >> 4)] = t2;
   }
 }
 
@@ -779,9 +786,14 @@ static hipError_t launch_step(const LanczosWS& w, int j, int dry, hipStream_t s,
   }
 }
 
+// columns per column block: 16 (32 partial lanes) for 32 or more row groups,
+// wider blocks for fewer (e.g. 8 row groups per window: 64 columns x 8 lanes)
 static void launch_reduce(const LanczosWS& w, int j, hipStream_t s) {
   const int nx = (j >= 0) ? (j + 16) / 16 + 1 : 0;
-  hipLaunchKernelGGL(k_lz_reduce, dim3(nx + w.m / 16, w.n_act), dim3(512), 0, s, w, j);
+  if (w.G3 >= 32) hipLaunchKernelGGL(k_lz_reduce<16>, dim3(nx + w.m / 16, w.n_act), dim3(512), 0, s, w, j);
+  else if (w.G3 >= 16) hipLaunchKernelGGL(k_lz_reduce<32>, dim3(nx + w.m / 32, w.n_act), dim3(512), 0, s, w, j);
+  else if (w.G3 >= 8) hipLaunchKernelGGL(k_lz_reduce<64>, dim3(nx + w.m / 64, w.n_act), dim3(512), 0, s, w, j);
+  else hipLaunchKernelGGL(k_lz_reduce<128>, dim3(nx + w.m / 128, w.n_act), dim3(512), 0, s, w, j);
 }
 
 hipError_t launch_lanczos(const LanczosWS& w, const double* q1_act, hipStream_t s,
