@@ -8,6 +8,8 @@
 #include "slh_device.h"
 #include "slh_internal.h"
 
+#include <algorithm>
+
 namespace slh {
 
 template <int DT>  // 0 = bf16, 1 = f32
@@ -85,6 +87,25 @@ hipError_t launch_rownorm(const void* X, int dtype, int64_t ldx, int64_t N, int 
   else
     hipLaunchKernelGGL(k_rownorm<1>, grid, dim3(256), 0, s, X, ldx, N, D, inv2sqrtD, sqrt2m,
                        gauss, nrm2_fm, nrm_x, inv_x, rowscale, Xb);
+  return hipGetLastError();
+}
+
+// dst[a][0..L) = src[winlist[a]][0..L) for the active windows (one launch for
+// all of them, rather than a copy per window).
+__global__ void k_gather_windows(double* __restrict__ dst, const double* __restrict__ src,
+                                 const int* __restrict__ winlist, int64_t L) {
+  const int a = blockIdx.y;
+  const int64_t w = winlist[a];
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < L; i += (int64_t)gridDim.x * 256)
+    dst[(int64_t)a * L + i] = src[w * L + i];
+}
+
+hipError_t launch_gather_windows(double* dst, const double* src, const int* winlist, int64_t L,
+                                 int n_act, hipStream_t s) {
+  (void)hipGetLastError();
+  if (n_act <= 0 || L <= 0) return hipSuccess;
+  const unsigned gx = (unsigned)std::min<int64_t>((L + 255) / 256, 64);
+  hipLaunchKernelGGL(k_gather_windows, dim3(gx, n_act), dim3(256), 0, s, dst, src, winlist, L);
   return hipGetLastError();
 }
 

@@ -663,10 +663,8 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
     const double* q1act = P<double>(c->q1all);
     if (na != c->n_win) {
       ENSURE(c, c->q1act, (size_t)na * L * sizeof(double));
-      for (int a = 0; a < na; ++a)
-        HIP_TRY(c, hipMemcpyAsync(P<double>(c->q1act) + (int64_t)a * L,
-                                  P<double>(c->q1all) + (int64_t)c->winlist_h[(size_t)a] * L,
-                                  L * sizeof(double), hipMemcpyDeviceToDevice, c->stream));
+      HIP_TRY(c, launch_gather_windows(P<double>(c->q1act), P<double>(c->q1all), P<int>(c->winlist),
+                                       L, na, c->stream));
       q1act = P<double>(c->q1act);
     }
     if (c->short_win && local_supported((int)L, n_it, c->r)) {

@@ -14,6 +14,10 @@ hipError_t launch_rownorm(const void* X, int dtype, int64_t ldx, int64_t N, int 
                           int gauss, double* nrm2_fm, double* nrm_x, double* inv_x,
                           float* rowscale, uint16_t* Xb, hipStream_t s);
 
+// dst[a] = src[winlist[a]] (L doubles each) for a < n_act; winlist on the device.
+hipError_t launch_gather_windows(double* dst, const double* src, const int* winlist, int64_t L,
+                                 int n_act, hipStream_t s);
+
 // ---- feature map (k_featmap.hip) ----
 struct FeatmapArgs {
   const uint16_t* X;      // bf16 rows, global token index, row stride ldx
