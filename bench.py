@@ -225,6 +225,9 @@ def main():
                                "traffic_unit": "HBM bytes per pass (FETCH_SIZE + WRITE_SIZE, "
                                                "copy-calibrated; profiles/lanczos_passes_qwen7b_traffic.md)",
                                "kernel": "k_lz_step (u = Phi t_j, z1, Phi^T z1 partials, h2 partials)",
+                               "passes_per_step": 1,
+                               "form": "fused: one read of Phi per Lanczos step serves both products "
+                                       "of the implicit matvec",
                                "bytes_per_launch": alg, "avg_launch_ms": pass_ms,
                                "timing": f"slh_time_passes: {PASS_REPS} x the pass of the last step "
                                          "as one HIP graph between two events",
