@@ -81,11 +81,21 @@ def test_feature_map_gauss_option():
 
 
 # ------------------------------------------------------------------ Lanczos .. SimHash on the oracle's Phi
-@pytest.mark.parametrize("case", ["tiny", "ragged"])
+# staged_m512 / staged_m256: 1024 chunks of 16 rows, more than two per CU, so
+# each block of the pass streams several chunks through LDS (small m: 4 and 2
+# rows per wave and chunk)
+@pytest.mark.parametrize("case", ["tiny", "ragged", "staged_m512", "staged_m256"])
 def test_lanczos_stage_on_oracle_phi(case):
     """Loads fp32(Phi_oracle) so both sides run Lanczos on the same operator:
     alpha/beta, Ritz values, Ritz vectors and codes must then agree closely."""
-    inp = make_inputs("tiny") if case == "tiny" else _custom("ragged", 1000, 264, 512, 40, 12, 8)
+    if case == "tiny":
+        inp = make_inputs("tiny")
+    elif case == "ragged":
+        inp = _custom("ragged", 1000, 264, 512, 40, 12, 8)
+    elif case == "staged_m512":
+        inp = _custom("staged_m512", 16380, 264, 512, 24, 8, 8)
+    else:
+        inp = _custom("staged_m256", 16380, 264, 256, 24, 8, 8)
     wl = inp.workload
     X = inp.x_float()
     Phi32 = O.feature_map(X, OP.projection(0, wl.D, wl.m), OP.phases(0, wl.m)).astype(np.float32)
