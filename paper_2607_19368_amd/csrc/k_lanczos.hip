@@ -59,33 +59,6 @@ __device__ __forceinline__ double wave_sum8_f64(const double (&v)[8]) {
   return y;
 }
 
-// The same over each half wave (lanes 0-31 and 32-63 separately): lane l holds
-// the half-wave sum of value index ((l>>4)&1)*4 + ((l>>3)&1)*2 + ((l>>2)&1).
-__device__ __forceinline__ double half_sum8_f64(const double (&v)[8]) {
-  const int lane = threadIdx.x & 63;
-  double w[4];
-  const bool b16 = lane & 16;
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    double keep = b16 ? v[e + 4] : v[e];
-    double send = b16 ? v[e] : v[e + 4];
-    w[e] = keep + __shfl_xor(send, 16, 64);
-  }
-  double x[2];
-  const bool b8 = lane & 8;
-#pragma unroll
-  for (int e = 0; e < 2; ++e) {
-    double keep = b8 ? w[e + 2] : w[e];
-    double send = b8 ? w[e] : w[e + 2];
-    x[e] = keep + __shfl_xor(send, 8, 64);
-  }
-  const bool b4 = lane & 4;
-  double y = (b4 ? x[1] : x[0]) + __shfl_xor(b4 ? x[0] : x[1], 4, 64);
-  y += __shfl_xor(y, 2, 64);
-  y += __shfl_xor(y, 1, 64);
-  return y;
-}
-
 // The same over each 16-lane quarter: lane l holds the quarter sum of value
 // index ((l>>3)&1)*4 + ((l>>2)&1)*2 + ((l>>1)&1).
 __device__ __forceinline__ double quarter_sum8_f64(const double (&v)[8]) {
@@ -110,14 +83,6 @@ __device__ __forceinline__ double quarter_sum8_f64(const double (&v)[8]) {
   double y = (b2 ? x[1] : x[0]) + __shfl_xor(b2 ? x[0] : x[1], 2, 64);
   y += __shfl_xor(y, 1, 64);
   return y;
-}
-
-// Value of v in lane l (l uniform), through the scalar unit.
-__device__ __forceinline__ double readlane_f64(double v, int l) {
-  const unsigned long long x = (unsigned long long)__double_as_longlong(v);
-  const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)x, l);
-  const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(x >> 32), l);
-  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 
 // Sum of src[g * ld] over g < G with 16 loads in flight (fixed order).
