@@ -166,18 +166,21 @@ __device__ __forceinline__ double z2_sum(const LanczosWS& w, int a, double* red)
 // Block g of nx = ceil(j / 16) + 1 (512 threads): H2[k] = sum over the row
 // groups of the h2 partials for k in [16 g, 16 g + 16) (k < j), or, for the
 // last block, |z1|^2 (slot ldq).
-__device__ __forceinline__ void h2_reduce_block(const LanczosWS& w, int a, int j, int g, int nx) {
+// stopped: the window broke down (nothing is written; the flag is read by the
+// caller alongside the loads rather than before them).
+__device__ __forceinline__ void h2_reduce_block(const LanczosWS& w, int a, int j, int g, int nx,
+                                                int stopped) {
   const int hs = w.ldq + 1;
   const double* hp = w.H2part + (int64_t)a * w.G3 * hs;
   double* dst = w.H2 + (int64_t)a * hs;
   if (g == nx - 1) {
     __shared__ double red[8];
     const double v = z2_sum(w, a, red);
-    if (threadIdx.x == 0) dst[w.ldq] = v;
+    if (threadIdx.x == 0 && !stopped) dst[w.ldq] = v;
   } else {
     const int c0 = g * 16;
     const double v = colsum16(hp, hs, w.G3, c0, j);
-    if (threadIdx.x < 16 && c0 + threadIdx.x < j) dst[c0 + threadIdx.x] = v;
+    if (threadIdx.x < 16 && c0 + threadIdx.x < j && !stopped) dst[c0 + threadIdx.x] = v;
   }
 }
 
@@ -608,15 +611,14 @@ __global__ __launch_bounds__(512) void k_lz_reduce(LanczosWS w, int j) {
   const int m = w.m, hs = w.ldq + 1;
   const int nx = (j >= 0) ? (j + 16) / 16 + 1 : 0;
   int g = blockIdx.x;
+  const int stopped = w.stop[a];                    // checked after the loads are out
   if (g < nx) {
-    if (w.stop[a]) return;
-    h2_reduce_block(w, a, j + 1, g, nx);
+    h2_reduce_block(w, a, j + 1, g, nx, stopped);
     return;
   }
   g -= nx;
   const int cl = tid % CPB, pl = tid / CPB;
   const int c = g * CPB + cl;                       // m is a multiple of CPB
-  if (w.stop[a]) return;
   __shared__ double red[8];
   __shared__ double rs[PL / WL][CPB + 1];
   // |z1|^2 and the column sums with both sets of loads in flight together (the
@@ -627,20 +629,22 @@ __global__ __launch_bounds__(512) void k_lz_reduce(LanczosWS w, int j) {
   const int cnt = (w.G3 - pl + PL - 1) / PL;
   const double s = sum_strided(w.Spart + ((int64_t)a * w.G3 + pl) * m + c, (int64_t)PL * m,
                                cnt > 0 ? cnt : 0);
-  double z2 = 1.0;
-  if (j >= 0) {
-    z2acc = z2_add(zp0, w.G3, 0, z2acc);
-    for (int g0 = 4 * 512; g0 < w.G3; g0 += 4 * 512) z2acc = z2_add(z2_load(w, a, g0), w.G3, g0, z2acc);
-    z2 = block_sum_f64(z2acc, red);
-  }
-  // the WL partial lanes of a column within a wave by butterflies, then the
-  // waves' sums in LDS (fixed order)
+  if (stopped) return;
+  z2acc = z2_add(zp0, w.G3, 0, z2acc);
+  for (int g0 = 4 * 512; g0 < w.G3; g0 += 4 * 512) z2acc = z2_add(z2_load(w, a, g0), w.G3, g0, z2acc);
+  // |z1|^2 as block_sum_f64 forms it (wave butterflies, then the 8 waves in
+  // order: the same bits as the h2 block) and the WL partial lanes of a column
+  // within a wave by butterflies, then the waves' column sums, one barrier for both
+  const double zw = wave_sum_f64(z2acc);
   double sw = s;
 #pragma unroll
   for (int o = CPB; o < 64; o <<= 1) sw += __shfl_xor(sw, o, 64);
+  if ((tid & 63) == 0) red[tid >> 6] = zw;
   if (pl % WL == 0) rs[pl / WL][cl] = sw;
   __syncthreads();
   if (tid < CPB) {
+    double z2 = 0.0;
+    for (int q = 0; q < 8; ++q) z2 += red[q];
     double S = 0.0;
     for (int q = 0; q < PL / WL; ++q) S += rs[q][cl];
     double t = S;
@@ -659,9 +663,8 @@ __global__ __launch_bounds__(512) void k_lz_reduce(LanczosWS w, int j) {
 // beta = sqrt(|z1|^2 - |h2|^2).
 __global__ __launch_bounds__(512) void k_lz_h2sum(LanczosWS w) {
   const int a = blockIdx.y;
-  if (w.stop[a]) return;
   const int j = w.n_it, nx = (j + 15) / 16 + 1;
-  h2_reduce_block(w, a, j, blockIdx.x, nx);
+  h2_reduce_block(w, a, j, blockIdx.x, nx, w.stop[a]);
 }
 
 __global__ __launch_bounds__(256) void k_lz_last_beta(LanczosWS w) {
