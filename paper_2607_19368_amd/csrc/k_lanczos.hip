@@ -339,6 +339,11 @@ __global__ __launch_bounds__(512, STAGED ? 2 : 4) void k_lz_step(LanczosWS w, in
   const double apv = w.Apart[(int64_t)a * nbr + min(tid, nbr - 1)];
   const double alv = w.alpha[(int64_t)a * w.n_it + min(tid, jm)];
   const double bev = w.beta[(int64_t)a * w.n_it + min(tid, jm)];
+  // the neighbours of entry tid of h2 and beta, for g = T_{j-1} h2 without an
+  // LDS exchange, and h2_{j-1}
+  const double h2p = H2a[max(min(tid - 1, jm), 0)], h2n = H2a[min(tid + 1, jm)];
+  const double bep = w.beta[(int64_t)a * w.n_it + max(min(tid - 1, jm), 0)];
+  const double h2l = H2a[jm];
   const int stopped = w.stop[a];
   const double amax0 = w.amax[2 * a + (j & 1)];   // max |alpha| before step j
   double tv[4];
@@ -366,16 +371,44 @@ __global__ __launch_bounds__(512, STAGED ? 2 : 4) void k_lz_step(LanczosWS w, in
   };
   load_chunk(0);
   if (stopped) return;
-  __shared__ double red[8];
-  __shared__ double h2s[264], bes[264], gs[264];
+  __shared__ double h2s[264], gs[264];
   __shared__ double rq[KG][RC + 1], rg[KG][RC + 1];
   __shared__ double pr[RC][9];
   __shared__ double zs[RC];
   __shared__ double cr[WPS > 1 ? 7 : 1][256];
-  const double alpha_t = block_sum_f64((tid < nbr) ? apv : 0.0, red);   // |t~|^2
+  // g = T_{j-1} h2 (alpha_i on the diagonal, beta_i beside it; beta_{j-1} is
+  // not part of T_{j-1}) from the loaded neighbours; |t~|^2 (alpha~), |h2|^2 and
+  // h2^T g summed as block_sum_f64 does (wave butterflies, then the 8 waves in
+  // order), with h2 and g put in LDS, under one barrier
+  const int wv = tid >> 6;
+  __shared__ double red3[3][8];
+  {
+    double gi = 0.0;
+    if (tid < j) {
+      gi = alv * h2v;
+      if (tid > 0) gi = fma(bep, h2p, gi);
+      if (tid + 1 < j) gi = fma(bev, h2n, gi);
+      h2s[tid] = h2v;
+      gs[tid] = gi;
+    }
+    const double va = wave_sum_f64((tid < nbr) ? apv : 0.0);
+    const double vh = wave_sum_f64((tid < j) ? h2v * h2v : 0.0);
+    const double vg = wave_sum_f64((tid < j) ? h2v * gi : 0.0);
+    if (lane == 0) {
+      red3[0][wv] = va;
+      red3[1][wv] = vh;
+      red3[2][wv] = vg;
+    }
+  }
+  __syncthreads();
+  double alpha_t = 0.0, hh = 0.0, hth = 0.0;
+  for (int q = 0; q < 8; ++q) {
+    alpha_t += red3[0][q];
+    hh += red3[1][q];
+    hth += red3[2][q];
+  }
   double alpha = alpha_t, beta = 0.0, h2last = 0.0;
   if (j > 0) {
-    const double hh = block_sum_f64((tid < j) ? h2v * h2v : 0.0, red);
     const double b2 = z2 - hh;
     beta = b2 > 0.0 ? sqrt(b2) : 0.0;
     if (!dry && !(beta > w.tol * amax0)) {     // breakdown: n_eff stays j
@@ -385,22 +418,7 @@ __global__ __launch_bounds__(512, STAGED ? 2 : 4) void k_lz_step(LanczosWS w, in
       }
       return;
     }
-    if (tid < j) {
-      h2s[tid] = h2v;
-      bes[tid] = bev;
-    }
-    __syncthreads();
-    // g = T_{j-1} h2 (alpha_i on the diagonal, beta_i beside it; beta_{j-1} is
-    // not part of T_{j-1})
-    double gi = 0.0;
-    if (tid < j) {
-      gi = alv * h2v;
-      if (tid > 0) gi = fma(bes[tid - 1], h2s[tid - 1], gi);
-      if (tid + 1 < j) gi = fma(bev, h2s[tid + 1], gi);
-      gs[tid] = gi;
-    }
-    const double hth = block_sum_f64((tid < j) ? h2v * gi : 0.0, red);
-    h2last = h2s[j - 1];
+    h2last = h2l;
     alpha = (z2 * alpha_t - hth) / (beta * beta) - 2.0 * h2last;
   }
   if (!dry && g == 0 && tid == 0) {
@@ -409,7 +427,6 @@ __global__ __launch_bounds__(512, STAGED ? 2 : 4) void k_lz_step(LanczosWS w, in
     w.amax[2 * a + ((j + 1) & 1)] = fmax(amax0, fabs(alpha));   // the other slot:
     w.neff[a] = j + 1;                                          // read by the next step
   }
-  __syncthreads();
   const double zn = sqrt(z2);
   double* qdst = dry ? w.Zs + (int64_t)a * 2 * L : w.Q + ((int64_t)a * w.ldq + j) * L;
   double* zdst = dry ? w.Zs + ((int64_t)a * 2 + 1) * L : w.Z1 + (int64_t)a * L;
