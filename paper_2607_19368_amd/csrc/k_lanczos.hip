@@ -542,11 +542,9 @@ __global__ __launch_bounds__(512, STAGED ? 2 : 4) void k_lz_step(LanczosWS w, in
     // Unstaged they follow the dots (taken before, they cost the 128-VGPR
     // kernel a spill: 19.0 against 18.2 us at qwen7b).
     double sub = 0.0, sub_g = 0.0, q = 0.0, qm = 0.0;
-    if constexpr (STAGED) {
-      __syncthreads();
-      kgroup_sums(sub, sub_g);
-      if (tid < RC) row_q(ir, sub, zpc, qpc, q, qm);
-    }
+    __syncthreads();
+    kgroup_sums(sub, sub_g);
+    if (tid < RC) row_q(ir, sub, zpc, qpc, q, qm);
     if constexpr (MORE) {
       // stage this chunk's Phi rows in LDS and put the next chunk's loads in flight
       dots(0, RPW);
@@ -564,10 +562,6 @@ __global__ __launch_bounds__(512, STAGED ? 2 : 4) void k_lz_step(LanczosWS w, in
       // the second half arrives, measured slower: 19.7 against 18.5 us at qwen7b)
       dots(0, RPW);
       __syncthreads();
-      if constexpr (!STAGED) {
-        kgroup_sums(sub, sub_g);
-        if (tid < RC) row_q(ir, sub, zpc, qpc, q, qm);
-      }
       if (tid < RC) row_z(ir, sub_g, q, qm);
       __syncthreads();
       colsums(0, RPW, false);
