@@ -62,15 +62,18 @@ class Run:
 
 def run_gpu(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel=0, compact=False,
             phi_from=None, codes_from=None, want_phi=False, X=None, short_windows=None,
-            normalise=False, scheme=0, keep_last=None):
+            normalise=False, scheme=0, keep_last=None, timing=False):
     """phi_from: host float32 array (n_act*L, m) loaded instead of computing Phi;
     codes_from: host uint32 (N,) loaded instead of computing codes;
-    short_windows: value of SLH_OPT_SHORT_WINDOWS (None keeps the default)."""
+    short_windows: value of SLH_OPT_SHORT_WINDOWS (None keeps the default);
+    timing: SLH_OPT_TIMING = 1 (every Lanczos pass launched directly, timed)."""
     import torch
     import paper_2607_19368_amd as P
     from paper_2607_19368_amd import slh as B
     wl = inp.workload
     ctx = P.slh_create(wl.N, wl.D, wl.m, wl.r, wl.bits, seed)
+    if timing:
+        P.slh_set_option(ctx, B.SLH_OPT_TIMING, 1)
     K = wl.keep_last if keep_last is None else keep_last
     if K:
         P.slh_set_option(ctx, B.SLH_OPT_KEEP_LAST, K)

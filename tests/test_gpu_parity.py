@@ -302,6 +302,20 @@ def test_compact_positions_and_determinism():
         assert np.array_equal(a.alpha, b.alpha)
 
 
+
+def test_timing_mode_matches_graph_mode_qwen7b():
+    """The benchmark's timing mode (each Lanczos pass launched directly between
+    events) and the production graph give the same bits at the full qwen7b size."""
+    inp = make_inputs("qwen7b")
+    wl = inp.workload
+    _say("timing vs graph mode: qwen7b", wl.N, wl.D, wl.m, wl.n_it)
+    g1 = PR.run_gpu(inp, n_it=wl.n_it)
+    g2 = PR.run_gpu(inp, n_it=wl.n_it, timing=True)
+    assert np.array_equal(g1.E, g2.E) and np.array_equal(g1.t2m, g2.t2m)
+    for a, b in zip(g1.windows, g2.windows):
+        assert np.array_equal(a.alpha, b.alpha) and np.array_equal(a.beta, b.beta)
+        assert np.array_equal(a.Z, b.Z) and np.array_equal(a.codes, b.codes)
+
 def test_call_order_and_capacity_errors():
     import torch
     import paper_2607_19368_amd as P
