@@ -413,6 +413,39 @@ def adjust_to_target(groups, T):
     return pieces
 
 
+def target_budgets(T, spectral, L, k, keep_last=0):
+    """Per-window output budgets for an exact total length T over windows of L
+    tokens (section 3.3 adjustment to the target; the appendix's per-window
+    exact budgets for the adaptive backend; reading R20, parity unpinned).
+
+    spectral: one flag per window (True = spectral path, False = chunk
+    pooling).  A chunk window yields ceil(L / k) macro-tokens of its own and the
+    keep_last preserved tokens one each; the spectral windows share the rest,
+    B = T - (chunk macro-tokens) - keep_last, as floor(B / n) each plus one for
+    the first B mod n spectral windows in window order.  Chunk windows get 0.
+    Raises ValueError when some spectral budget would leave [1, L], or when
+    there is no spectral window and B != 0."""
+    flags = [bool(f) for f in spectral]
+    n = sum(flags)
+    chunk = sum(-(-L // k) for f in flags if not f)
+    B = T - chunk - keep_last
+    if n == 0:
+        if B != 0:
+            raise ValueError("target unreachable without spectral windows")
+        return [0] * len(flags)
+    if B < n or B > n * L:
+        raise ValueError("target unreachable with this routing")
+    q, rem = divmod(B, n)
+    out, a = [], 0
+    for f in flags:
+        if f:
+            out.append(q + (1 if a < rem else 0))
+            a += 1
+        else:
+            out.append(0)
+    return out
+
+
 def merge_groups(X, groups, positions=None, compact=False):
     """Eq. 7 and max positions for given member groups (in macro order)."""
     X = np.asarray(X)
@@ -491,40 +524,3 @@ def compress(X, W, psi, q1, R, n_it, r, kernel="softmax", positions=None, keep_p
     codes = simhash(Z, R)
     mg = merge(X, codes, positions, scheme=scheme)
     return CompressResult(Phi if keep_phi else None, lz, vals, Z, proj, codes, mg)
-
-
-@dataclass
-class WindowResult:
-    window: int
-    score: float
-    spectral: bool
-    E: np.ndarray
-    P: np.ndarray
-    tok2macro: np.ndarray      # window-local macro index per token
-    detail: CompressResult = None
-
-
-def compress_adaptive(X, L, rho, W, psi, q1_of_window, R, n_it, r, tau=None,
-                      kernel="softmax", keep_detail=False, scheme="max"):
-    """Adaptive backend over consecutive windows of L tokens (section 3.6):
-    score each window (Eq. 8), route it, run chunk pooling (section 3.5) or
-    Spectral-LSH (Algorithm 1) on it with global positions, and return the
-    macro-tokens of all windows in ascending position order."""
-    N = X.shape[0]
-    if N % L:
-        raise ValueError("N must be a multiple of the window length")
-    out = []
-    for w in range(N // L):
-        Xw = X[w * L:(w + 1) * L]
-        score = redundancy_score(Xw)
-        spectral = route_window(L, score, rho, tau)
-        if spectral:
-            res = compress(Xw, W, psi, q1_of_window(w), R, n_it, r, kernel,
-                           positions=w * L + np.arange(L), keep_phi=False, scheme=scheme)
-            out.append(WindowResult(w, score, True, res.merge.E, res.merge.P,
-                                    res.merge.tok2macro, res if keep_detail else None))
-        else:
-            k = chunk_size(rho)
-            E, P = chunk_pool(Xw, k, pos0=w * L, scheme=scheme)
-            out.append(WindowResult(w, score, False, E, P, np.arange(L) // k))
-    return out

@@ -712,17 +712,7 @@ def test_exact_target_length(case, T):
     torch.cuda.synchronize()
     gE, gP, gt = E[:M].cpu().numpy(), Pp[:M].cpu().numpy(), t2m.cpu().numpy()
     # oracle: budgets, adjusted groups per spectral window, chunk windows, tail
-    n_s = int(route.sum())
-    chunk = sum((Lw + O.chunk_size(rho) - 1) // O.chunk_size(rho) for w in range(Nc // Lw)
-                if not route[w]) if rho else 0
-    Bud = T - chunk - K
-    budgets, a = [], 0
-    for w in range(Nc // Lw):
-        if route[w]:
-            budgets.append(Bud // n_s + (1 if a < Bud % n_s else 0))
-            a += 1
-        else:
-            budgets.append(0)
+    budgets = O.target_budgets(T, route, Lw, O.chunk_size(rho) if rho else 1, K)
     X = inp.x_float()
     Es, Ps, tms = [], [], np.zeros(wl.N, np.int64)
     base = 0

@@ -326,6 +326,44 @@ def test_simhash_collision_law():
         assert O.simhash(Z, R)[0] == int(((Z[0] @ R) > 0) @ (1 << np.arange(b)))
 
 
+# ---------------------------------------------------------------- bf16 rounding
+def _bf16_cases():
+    rows = []
+    with open(os.path.join(GOLD, "bf16_round_hand.txt")) as f:
+        for line in f:
+            if line.startswith("F32 "):
+                t = line.split()
+                rows.append((int(t[1], 16), int(t[3], 16)))
+    return rows
+
+
+@pytest.mark.parametrize("fn", ["bf16_round", "projection_rounding"])
+def test_bf16_round_hand_ties_and_library_cast(fn):
+    """Reading R2: round-to-nearest-even from float32.  Pinned by hand-worked
+    ties (tests/golden/bf16_round_hand.txt) and by torch's float32 -> bfloat16
+    conversion (round to nearest even) on random bit patterns of every finite
+    magnitude; both rounding routines of the oracle are checked (the feature
+    map's input rounding and the W draw's)."""
+    import torch
+    rnd = O.bf16_round if fn == "bf16_round" else OP._f32_to_bf16_f64
+    cases = _bf16_cases()
+    assert len(cases) >= 10
+    x = np.array([c[0] for c in cases], np.uint32).view(np.float32)
+    want = (np.array([c[1] for c in cases], np.uint32) << 16).view(np.float32).astype(np.float64)
+    got = rnd(x)
+    assert np.array_equal(got, want), [hex(int(v)) for v in np.asarray(got, np.float32).view(np.uint32)]
+    rng = np.random.default_rng(17)
+    bits = rng.integers(0, 2**32, 200000, dtype=np.uint64).astype(np.uint32)
+    bits = bits[(bits & 0x7F800000) != 0x7F800000]           # finite only
+    ties = (rng.integers(0, 2**16, 5000, dtype=np.uint64).astype(np.uint32) << 16) | 0x8000
+    vals = np.concatenate([bits, ties & 0xFF7FFFFF]).view(np.float32)
+    ref = torch.from_numpy(vals.copy()).to(torch.bfloat16).to(torch.float64).numpy()
+    out = rnd(vals)
+    fin = np.isfinite(ref)
+    assert np.array_equal(out[fin], ref[fin])
+    assert np.all(np.isinf(out[~fin]) & (np.sign(out[~fin]) == np.sign(ref[~fin])))
+
+
 # ---------------------------------------------------------------- merge
 def test_merge_hand_example():
     X = _rows("merge_hand.txt", "X")
@@ -337,6 +375,70 @@ def test_merge_hand_example():
     # a bucket whose mean is zero yields the zero vector
     z = O.merge(np.array([[1.0, 0.0], [-1.0, 0.0]]), np.array([4, 4]))
     assert np.all(z.E == 0) and list(z.P) == [1]
+
+
+def test_merge_groups_hand_example_and_agreement_with_merge():
+    """merge_groups (Eq. 7 on given member groups, max positions): the hand
+    example of tests/golden/merge_hand.txt given as groups in macro order, at
+    positions offset by 10 (each position is the group's largest member
+    position, not its smallest), and on random codes the same E, P and token
+    map as merge() when handed merge()'s own groups."""
+    X = _rows("merge_hand.txt", "X")
+    groups = [np.array([0, 2]), np.array([3]), np.array([1, 4])]
+    E, P, t2m = O.merge_groups(X, groups)
+    assert list(P) == list(_rows("merge_hand.txt", "P")[0].astype(int))
+    assert list(t2m) == list(_rows("merge_hand.txt", "MAP")[0].astype(int))
+    assert np.allclose(E, _rows("merge_hand.txt", "E"), rtol=0, atol=1e-15)
+    _, P10, _ = O.merge_groups(X, groups, positions=10 + np.arange(5))
+    assert list(P10) == [12, 13, 14]
+    _, Pc, _ = O.merge_groups(X, groups, compact=True)
+    assert list(Pc) == [0, 1, 2]
+    rng = np.random.default_rng(23)
+    for trial in range(5):
+        N = int(rng.integers(30, 300))
+        Xr = rng.standard_normal((N, 6))
+        codes = rng.integers(0, int(rng.integers(2, 50)), N)
+        pos = 100 * trial + np.arange(N)
+        mg = O.merge(Xr, codes, positions=pos)
+        E2, P2, t2 = O.merge_groups(Xr, mg.members, positions=pos)
+        assert np.array_equal(E2, mg.E) and np.array_equal(P2, mg.P)
+        assert np.array_equal(t2, mg.tok2macro)
+
+
+def test_target_budgets_hand_and_invariants():
+    """Reading R20 (parity unpinned: the paper states per-window exact budgets
+    but no rule).  Hand example: 5 windows of 256, windows 1 and 4 routed to
+    chunk pooling with k = 8 (32 macro-tokens each), 12 preserved tokens,
+    T = 140: B = 140 - 64 - 12 = 64 over 3 spectral windows = 21 each and one
+    more for the first (64 mod 3 = 1).  Then the exact-fit and unreachable
+    cases, and invariants on random routings."""
+    assert O.target_budgets(140, [1, 0, 1, 1, 0], 256, 8, 12) == [22, 0, 21, 21, 0]
+    assert O.target_budgets(512, [1], 8192, 1) == [512]
+    assert O.target_budgets(3, [1, 1, 1], 16, 4) == [1, 1, 1]
+    assert O.target_budgets(64, [0, 0], 256, 8) == [0, 0]
+    # a chunk window of 10 tokens with k = 4 yields ceil(10 / 4) = 3
+    assert O.target_budgets(3 + 5, [0, 1], 10, 4) == [0, 5]
+    for T, sp in ((2, [1, 1, 1]), (49, [1, 1, 1]), (63, [0, 0])):
+        with pytest.raises(ValueError):
+            O.target_budgets(T, sp, 16, 8)
+    rng = np.random.default_rng(29)
+    for trial in range(50):
+        nw = int(rng.integers(1, 20))
+        L = int(rng.choice([16, 64, 256]))
+        k = int(rng.integers(1, 9))
+        K = int(rng.integers(0, 13))
+        sp = rng.random(nw) < 0.6
+        n = int(sp.sum())
+        chunk = int((~sp).sum()) * (-(-L // k))
+        if n == 0:
+            continue
+        T = chunk + K + int(rng.integers(n, n * L + 1))
+        b = O.target_budgets(T, sp, L, k, K)
+        assert sum(b) == T - chunk - K
+        sb = [v for v, f in zip(b, sp) if f]
+        assert all(1 <= v <= L for v in sb) and max(sb) - min(sb) <= 1
+        assert sb == sorted(sb, reverse=True)
+        assert all(v == 0 for v, f in zip(b, sp) if not f)
 
 
 def test_position_schemes_hand_example():
