@@ -1,10 +1,12 @@
 """Throughput of the Spectral-LSH hot path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload qwen7b] [--no-cpu-baseline]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload qwen7b_exact] [--no-cpu-baseline]
 
 A step is one pass of the whole path over one prompt already resident in HBM:
 feature map -> Lanczos (all steps) -> eigensolve + Ritz -> SimHash -> merge
-(plus routing for the windowed adaptive workload).  Prints one JSON line.
+(plus routing for the windowed adaptive workload).  The default workload is the
+Qwen2.5-7B-shaped prompt (N=8192, D=3584) compressed to exactly N / 16 = 512
+macro-tokens (rho = 16 with the exact-length adjustment).  Prints one JSON line.
 """
 import argparse
 import json
@@ -19,18 +21,20 @@ sys.path.insert(0, ROOT)
 METRIC = "compressed prompt tokens/sec at N=8192,D=3584,ρ=16; Lanczos matvec HBM GB/s"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+INFINITY_CACHE_BYTES = 256 * 2**20   # MI355X last-level (MALL) cache
 
 
 PASS_REPS = 96                   # graph replays of the last step's pass over Phi
 
 
-def measured_traffic(workload):
+def measured_traffic(wl):
     """HBM bytes per Lanczos pass (k_lz_step) from the committed counter summary,
-    if it was taken on the current kernel source and this workload; else None."""
+    if it was taken on the current kernel source and on this pass shape (one
+    window of N=8192, m=2048, 96 steps); else None."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "lanczos_passes_qwen7b_traffic.md")
     src = os.path.join(ROOT, "paper_2607_19368_amd", "csrc", "k_lanczos.hip")
-    if workload != "qwen7b" or not os.path.exists(path):
+    if (wl.N, wl.m, wl.n_it, wl.window) != (8192, 2048, 96, 0) or not os.path.exists(path):
         return None
     fields = {}
     for line in open(path):
@@ -48,7 +52,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="qwen7b")
+    ap.add_argument("--workload", default="qwen7b_exact")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--timing", type=int, default=1, help="record per-stage HIP events")
     return ap.parse_args()
@@ -61,9 +65,13 @@ def cpu_baseline(inp, min_seconds=10.0, max_reps=40, tau=None):
     import numpy as np
     from oracle import params as OP
     from oracle import spectral_lsh as O
+    blas = None
     try:
         from threadpoolctl import threadpool_info
-        cores = max((d.get("num_threads", 1) for d in threadpool_info()), default=1)
+        info = [d for d in threadpool_info() if d.get("user_api") == "blas"] or threadpool_info()
+        cores = max((d.get("num_threads", 1) for d in info), default=1)
+        if info:
+            blas = f"{info[0].get('internal_api')} {info[0].get('version')}"
     except Exception:
         cores = len(os.sched_getaffinity(0))
     wl = inp.workload
@@ -73,26 +81,46 @@ def cpu_baseline(inp, min_seconds=10.0, max_reps=40, tau=None):
     R = OP.hyperplanes(0, wl.r, wl.bits)
     q1 = [OP.start_vector(0, L, w) for w in range(wl.N // L)]
     times = []
+    stage = {k: 0.0 for k in ("route_chunk", "feature_map", "lanczos", "eigh_ritz", "simhash",
+                              "merge", "adjust")}
     while len(times) < 2 or (sum(times) < min_seconds and len(times) < max_reps):
         t0 = time.perf_counter()
         for w in range(wl.N // L):
+            ta = time.perf_counter()
             Xw = inp.x_float(slice(w * L, (w + 1) * L))
             if wl.adaptive and not O.route_window(L, O.redundancy_score(Xw), wl.rho, tau):
                 O.chunk_pool(Xw, O.chunk_size(wl.rho), pos0=w * L)
+                stage["route_chunk"] += time.perf_counter() - ta
                 continue
+            tb = time.perf_counter()
             Phi = O.feature_map(Xw, W, psi)
             if wl.normalise:
                 Phi, _ = O.normalised_features(Phi)
+            tc = time.perf_counter()
             lz = O.lanczos(Phi, q1[w], wl.n_it)
+            td = time.perf_counter()
             _, Z, _, _ = O.ritz(lz, wl.r)
+            te = time.perf_counter()
             codes = O.simhash(Z, R)
-            O.merge(Xw, codes, positions=w * L + np.arange(L))
+            tf = time.perf_counter()
+            mg = O.merge(Xw, codes, positions=w * L + np.arange(L))
+            tg = time.perf_counter()
+            if wl.target and not wl.adaptive:
+                O.merge_groups(Xw, O.adjust_to_target(mg.members, wl.target),
+                               positions=w * L + np.arange(L))
+            th = time.perf_counter()
+            for k, (u, v) in zip(("route_chunk", "feature_map", "lanczos", "eigh_ritz", "simhash",
+                                  "merge", "adjust"),
+                                 ((ta, tb), (tb, tc), (tc, td), (td, te), (te, tf), (tf, tg), (tg, th))):
+                stage[k] += v - u
         times.append(time.perf_counter() - t0)
     t = sum(times) / len(times)
     return {"value": wl.N / t, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"the full {wl.name} prompt ({wl.N} tokens), feature map through merge, "
-                      f"{len(times)} runs in {sum(times):.1f} s ({t:.2f} s each)",
-            "seconds": t}
+            "sample": f"the full {wl.name} prompt ({wl.N} tokens), feature map through merge"
+                      + (" and the exact-length adjustment" if wl.target and not wl.adaptive else "")
+                      + f", {len(times)} runs in {sum(times):.1f} s ({t:.2f} s each)",
+            "seconds": t, "blas": blas,
+            "stage_seconds": {k: v / len(times) for k, v in stage.items() if v > 0}}
 
 
 def main():
@@ -150,9 +178,14 @@ def main():
     for _ in range(a.warmup):
         M = step()
     torch.cuda.synchronize()
+    # every step ends in slh_merge, which returns M to the host (a stream
+    # synchronisation), so the host clock between steps times each step
+    step_ms = []
     t0 = time.perf_counter()
     for _ in range(a.steps):
+        ts = time.perf_counter()
         M = step()
+        step_ms.append(1e3 * (time.perf_counter() - ts))
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     ms_per_step = 1e3 * dt / a.steps
@@ -194,7 +227,26 @@ def main():
                          "eigensolve/Ritz/SimHash, fp32 merge sums",
             "M": int(M), "rho_achieved": wl.N / max(1, int(M)),
         },
+        "step_ms": {"median": float(np.median(step_ms)), "p10": float(np.percentile(step_ms, 10)),
+                    "p90": float(np.percentile(step_ms, 90)), "n": len(step_ms)},
     }
+    # measured ceilings, in the same job: a plain read of 1 GiB (four times the
+    # Infinity Cache: HBM), a plain read of a buffer the size of Phi read over
+    # and over (what the cache serves a buffer that fits in it), and a
+    # register-only bf16 MFMA loop
+    peaks = None
+    if a.timing:
+        phi_bytes = ctx.n_spectral * L * wl.m * 4
+        big = torch.empty(2**30, dtype=torch.uint8, device="cuda")
+        hbm = P.slh_peak_read(big, reps=10)
+        small = big[:max(4096, (phi_bytes // 16) * 16)]
+        cached = P.slh_peak_read(small, reps=50)
+        del big, small
+        mf = P.slh_peak_mfma(reps=5)
+        peaks = {"read_1GiB_gbs": hbm, "read_phi_sized_gbs": cached, "mfma_bf16_tflops": mf,
+                 "phi_bytes": phi_bytes,
+                 "phi_fits_infinity_cache": bool(phi_bytes <= INFINITY_CACHE_BYTES)}
+        out["measured_peaks"] = peaks
     if a.timing:
         K = a.steps
         n_win = ctx.n_spectral
@@ -203,7 +255,8 @@ def main():
         fm_tf = flops / (fm_ms * 1e-3) / 1e12
         out["featmap_mfma"] = {"bound": "mfma", "achieved": fm_tf, "peak": BF16_PEAK_TFLOPS,
                                "unit": "TFLOP/s", "frac": fm_tf / BF16_PEAK_TFLOPS,
-                               "avg_launch_ms": fm_ms}
+                               "avg_launch_ms": fm_ms, "peak_measured": peaks["mfma_bf16_tflops"],
+                               "frac_of_measured": fm_tf / peaks["mfma_bf16_tflops"]}
         out["stages_ms"] = {k: v / K for k, v in stage_sum.items() if k != "phi_pass_count"}
         out["stages_ms"]["ms_per_step_with_events"] = ms2
         if stage_sum["phi_pass_count"] > 0:
@@ -221,7 +274,12 @@ def main():
             alg = n_win * (4.0 * L * wl.m + 8.0 * wl.m + 8.0 * L * (j_last + 3))
             ach = alg / (pass_ms * 1e-3) / 1e9
             out["roofline"] = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                               "frac": ach / HBM_PEAK_GBS, "traffic": measured_traffic(wl.name),
+                               "frac": ach / HBM_PEAK_GBS, "traffic": measured_traffic(wl),
+                               "peak_measured_hbm_read": peaks["read_1GiB_gbs"],
+                               "frac_of_measured_hbm_read": ach / peaks["read_1GiB_gbs"],
+                               "peak_measured_phi_sized_read": peaks["read_phi_sized_gbs"],
+                               "frac_of_measured_phi_sized_read": ach / peaks["read_phi_sized_gbs"],
+                               "phi_fits_infinity_cache": peaks["phi_fits_infinity_cache"],
                                "traffic_unit": "HBM bytes per pass (FETCH_SIZE + WRITE_SIZE, "
                                                "copy-calibrated; profiles/lanczos_passes_qwen7b_traffic.md)",
                                "kernel": "k_lz_step (u = Phi t_j, z1, Phi^T z1 partials, h2 partials)",
@@ -267,7 +325,8 @@ def main():
             "energy_ms": 1e3 * (t1 - t0), "purity_ms": 1e3 * (t2 - t1)}
     if not a.no_cpu_baseline:
         cb = cpu_baseline(inp, tau=tau if wl.adaptive else None)
-        out["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
+        out["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample", "blas",
+                                                  "stage_seconds")}
     print(json.dumps(out), flush=True)
 
 

@@ -170,7 +170,10 @@ int slh_route(slh_ctx *ctx, const void *X, int32_t x_dtype, int64_t ldx,
 /*
  * Step 1 (Eq. 3, Algorithm 1 first line): Phi = s(x) sqrt(2/m) cos(bf16(X) W + psi)
  * for the tokens of every spectral window, stored fp32 in the context.
- * X as for slh_route.  Asynchronous.
+ * X as for slh_route.  The row norms behind s(x) (and the member norms slh_merge
+ * uses) are taken from X on every call, unless slh_route has just taken them
+ * from the same X (pointer, type and stride) for this pass; a new prompt may
+ * therefore be written into the same buffer between passes.  Asynchronous.
  */
 int slh_feature_map(slh_ctx *ctx, const void *X, int32_t x_dtype, int64_t ldx);
 
@@ -202,7 +205,8 @@ int slh_simhash(slh_ctx *ctx, uint32_t *codes_out);
  * E = mean of the member rows of X (as given) rescaled to the mean member norm
  * (zero if the mean is zero), position = max member token index (global, 0-based;
  * or 0..M-1 in compact mode), macro-tokens in ascending position order.
- * X: the same tokens passed to slh_feature_map.
+ * X: the same tokens passed to slh_feature_map (their row norms from that call
+ * are reused; after slh_load of codes, or for another X, they are recomputed).
  * emb_out: device, cap x D floats (row-major); pos_out: device, cap int32;
  * tok2macro_out: device, N int32 (macro index of each token), may be NULL;
  * cap >= the bound n_spectral_windows * min(L, 2^bits) + chunk groups.
@@ -246,10 +250,32 @@ int slh_copy_out(slh_ctx *ctx, int32_t which, void *dst_host, int64_t bytes);
  * Replace a stage's result with caller data so a later stage can be checked on
  * its own (step-wise parity).  src: device memory, `bytes` exactly:
  *   SLH_OUT_PHI    n_act*L*m floats  -> Phi; the next call may be slh_lanczos
+ *   SLH_OUT_ALPHA  n_act*n_it doubles -> the diagonal of T per window; sets the
+ *                  order n_it (r <= n_it <= min(L, 256)) and n_eff = n_it for
+ *                  every window, clears beta; load first
+ *   SLH_OUT_BETA   n_act*n_it doubles -> beta_1..beta_{n_it} per window (the
+ *                  first n_it - 1 are T's off-diagonal)
+ *   SLH_OUT_Q      n_act*(n_it+1)*L doubles -> the basis, vector-major
+ *                  (after alpha, beta and Q the next call may be slh_eigh_ritz)
  *   SLH_OUT_CODES  N uint32          -> codes; the next call may be slh_merge
- * Asynchronous (device-to-device copy on the context stream).
+ * Asynchronous (device-to-device copy on the context stream), except that
+ * SLH_OUT_ALPHA synchronises the stream.
  */
 int slh_load(slh_ctx *ctx, int32_t which, const void *src, int64_t bytes);
+
+/*
+ * Eigh(T) and the Ritz coordinates alone (Algorithm 1: lambda, V <- Eigh(T);
+ * Z <- Q V[:, n-r:n]) on the tridiagonal and basis the context holds: those
+ * of the last slh_lanczos, or alpha, beta and Q given by slh_load (stage-wise
+ * checks of the eigensolver on a chosen T).  slh_lanczos already includes
+ * this step.  n_it must equal the order of T.  Kept eigenvalues whose gaps are
+ * at most 1e-8 |T| (|T| = max_k |alpha_k| + |beta_k-1| + |beta_k|) are a
+ * cluster: their vectors are orthogonalised against each other within the
+ * inverse iteration.  ritz_out / iters_out as for slh_lanczos (the call
+ * synchronises when either is non-NULL).  SLH_ESTATE when neither a Lanczos
+ * run nor a loaded alpha, beta and Q is present.
+ */
+int slh_eigh_ritz(slh_ctx *ctx, int32_t n_it, double *ritz_out, int32_t *iters_out);
 
 /*
  * Stage timings of the most recent calls, from HIP events on the context
@@ -301,6 +327,24 @@ int slh_spectral_energy(slh_ctx *ctx, double *energy_out);
  */
 int slh_bucket_purity(slh_ctx *ctx, const void *X, int32_t x_dtype, int64_t ldx, double thresh,
                       int64_t *counts_out);
+
+/*
+ * Measured ceilings for the roofline figures (measurement aids, not part of the
+ * method; no context needed).  Both time `reps` launches (after one untimed
+ * launch) with HIP events on `stream` (a hipStream_t, NULL = null stream) and
+ * synchronise it.
+ * slh_peak_read: a plain streaming read of every 16-byte word of buf (device,
+ *   `bytes` long, a multiple of 16 and >= 4096, 16-byte aligned; its contents
+ *   are not changed in practice) -> *gbs_out = bytes * reps / time in GB/s.  A
+ *   buffer larger than the 256 MB Infinity Cache measures HBM; a smaller one
+ *   read again and again measures what the cache serves.
+ * slh_peak_mfma: independent chains of dense bf16 32x32x16 MFMAs with their
+ *   operands in registers, two waves per SIMD on every CU -> *tflops_out in
+ *   TFLOP/s.  sink: device, 16 bytes (written only in a case that does not occur).
+ * reps in [1, 1000]; SLH_EINVAL for bad arguments, SLH_EHIP if a launch fails.
+ */
+int slh_peak_read(void *buf, int64_t bytes, int32_t reps, void *stream, double *gbs_out);
+int slh_peak_mfma(int32_t reps, void *sink, void *stream, double *tflops_out);
 
 /* Number of windows and of spectral windows of the current routing. */
 int64_t slh_num_windows(const slh_ctx *ctx);

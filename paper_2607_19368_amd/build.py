@@ -28,6 +28,7 @@ SOURCES = [
     "k_hash.hip",
     "k_merge.hip",
     "k_route.hip",
+    "k_peak.hip",
 ]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

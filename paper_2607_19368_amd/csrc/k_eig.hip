@@ -1,13 +1,22 @@
 // Eigh(T) for the Lanczos tridiagonal and the top-r Ritz coordinates
 // (Algorithm 1: lambda, V = Eigh(T); Z = Q V[:, n-k:n]).
 //
-// One 256-thread workgroup per kept eigenpair.  The eigenvalue is isolated by
+// Eigenvalues: one 256-thread workgroup per kept eigenvalue isolates it by
 // Sturm-count multisection (256 probe points per round, one per thread; the
 // count of negative pivots of T - x I is the number of eigenvalues below x)
-// until the bracket is a few ulps wide; the eigenvector by inverse iteration with a
-// partially pivoted LU of T - theta I (two solves from a fixed pseudo-random
-// start).  The vector is normalised and its sign chosen so that its first
-// nonzero entry is positive.  Everything is fp64.
+// until the bracket is a few ulps wide.
+// Eigenvectors: one workgroup per kept eigenvalue, inverse iteration with a
+// partially pivoted LU of T - theta I from a start vector of its own.  Two
+// vectors computed this way for eigenvalues g apart are orthogonal only to
+// about 6e-18 |T| / g (measured on Wilkinson's W21+), and for (numerically)
+// repeated eigenvalues they are independent directions of the eigenspace
+// rather than an orthonormal basis of it.  So kept eigenvalues whose
+// consecutive gaps are at most EIG_CLUSTER |T| (|T| the Gershgorin bound) form
+// clusters, and one workgroup per window then orthonormalises each cluster's
+// vectors in ascending order (modified Gram-Schmidt, two passes).  Outside
+// clusters the vectors are orthogonal to about 6e-12.  Each vector is
+// normalised and its sign chosen so that its first nonzero entry is positive.
+// Everything is fp64.
 #include "slh_device.h"
 #include "slh_internal.h"
 
@@ -16,6 +25,7 @@
 namespace slh {
 
 #define EIG_NMAX 256
+#define EIG_CLUSTER 1e-6
 
 // 1/d from the hardware reciprocal refined by one Newton step (d a normal number)
 __device__ __forceinline__ double rcp_nr(double d) {
@@ -41,55 +51,64 @@ __device__ __forceinline__ int sturm_count(const double* al, const double* b2, i
 
 #define EIG_T 256                // threads per eigenpair: one multisection probe each
 
-// theta: [n_act][r]; Seig: [n_act][n_it][r] (row k, kept column c)
-__global__ __launch_bounds__(EIG_T) void k_tridiag_eig(const double* __restrict__ alpha,
-                                                       const double* __restrict__ beta,
-                                                       const int* __restrict__ neff, int n_it,
-                                                       int r, double* __restrict__ theta,
-                                                       double* __restrict__ Seig) {
+// T of window a into LDS (al: diagonal, b1: off-diagonal, b2: its squares) and
+// its Gershgorin interval [lo, hi], |T| bound tnorm and largest b^2 (every wave
+// computes the same values).
+struct TriInfo {
+  double lo, hi, tnorm, bmax;
+};
+__device__ __forceinline__ TriInfo load_tridiag(const double* __restrict__ alp,
+                                                const double* __restrict__ bet, int n, double* al,
+                                                double* b1, double* b2) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  for (int k = tid; k < n; k += EIG_T) {
+    al[k] = alp[k];
+    const double b = (k < n - 1) ? bet[k] : 0.0;
+    b1[k] = b;
+    b2[k] = b * b;
+  }
+  __syncthreads();
+  TriInfo t;
+  t.lo = DBL_MAX;
+  t.hi = -DBL_MAX;
+  t.bmax = 0.0;
+  t.tnorm = 0.0;
+  for (int k = lane; k < n; k += 64) {
+    const double off = fabs(b1[k]) + (k > 0 ? fabs(b1[k - 1]) : 0.0);
+    t.lo = fmin(t.lo, al[k] - off);
+    t.hi = fmax(t.hi, al[k] + off);
+    t.bmax = fmax(t.bmax, b2[k]);
+    t.tnorm = fmax(t.tnorm, fabs(al[k]) + off);
+  }
+  for (int o = 32; o >= 1; o >>= 1) {
+    t.lo = fmin(t.lo, __shfl_xor(t.lo, o, 64));
+    t.hi = fmax(t.hi, __shfl_xor(t.hi, o, 64));
+    t.bmax = fmax(t.bmax, __shfl_xor(t.bmax, o, 64));
+    t.tnorm = fmax(t.tnorm, __shfl_xor(t.tnorm, o, 64));
+  }
+  return t;
+}
+
+// theta: [n_act][r], ascending kept eigenvalues (zero for the r - r_eff
+// leading columns of a window that stopped after n_eff < r steps).
+__global__ __launch_bounds__(EIG_T) void k_eig_values(const double* __restrict__ alpha,
+                                                      const double* __restrict__ beta,
+                                                      const int* __restrict__ neff, int n_it,
+                                                      int r, double* __restrict__ theta) {
   const int c = blockIdx.x, a = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int n = neff[a];
   const int r_eff = min(r, n);
-  double* Sa = Seig + (int64_t)a * n_it * r;
   if (c < r - r_eff) {
-    for (int k = tid; k < n_it; k += EIG_T) Sa[(int64_t)k * r + c] = 0.0;
     if (tid == 0) theta[(int64_t)a * r + c] = 0.0;
     return;
   }
   const int kidx = n - r + c;   // ascending index of the wanted eigenvalue
   __shared__ double al[EIG_NMAX], b1[EIG_NMAX], b2[EIG_NMAX];
-  __shared__ double y[EIG_NMAX], w[EIG_NMAX];
-  __shared__ double fu1[EIG_NMAX], fu2[EIG_NMAX], fd[EIG_NMAX], fl[EIG_NMAX];
-  __shared__ int piv[EIG_NMAX];
   __shared__ unsigned long long smask[EIG_T / 64];
-  const double* alp = alpha + (int64_t)a * n_it;
-  const double* bet = beta + (int64_t)a * n_it;
-  for (int k = tid; k < n; k += EIG_T) {
-    al[k] = alp[k];
-    double b = (k < n - 1) ? bet[k] : 0.0;
-    b1[k] = b;
-    b2[k] = b * b;
-  }
-  __syncthreads();
-  // Gershgorin bounds and the pivot floor (every wave computes the same values)
-  double lo = DBL_MAX, hi = -DBL_MAX, bmax = 0.0, tnorm = 0.0;
-  for (int k = lane; k < n; k += 64) {
-    double off = fabs(b1[k]) + (k > 0 ? fabs(b1[k - 1]) : 0.0);
-    lo = fmin(lo, al[k] - off);
-    hi = fmax(hi, al[k] + off);
-    bmax = fmax(bmax, b2[k]);
-    tnorm = fmax(tnorm, fabs(al[k]) + off);
-  }
-  for (int o = 32; o >= 1; o >>= 1) {
-    lo = fmin(lo, __shfl_xor(lo, o, 64));
-    hi = fmax(hi, __shfl_xor(hi, o, 64));
-    bmax = fmax(bmax, __shfl_xor(bmax, o, 64));
-    tnorm = fmax(tnorm, __shfl_xor(tnorm, o, 64));
-  }
-  const double pivmin = DBL_MIN * fmax(1.0, bmax);
-  const double pad = 2.0 * DBL_EPSILON * fmax(tnorm, DBL_MIN) + 2.0 * pivmin;
-  lo -= pad;
-  hi += pad;
+  const TriInfo ti = load_tridiag(alpha + (int64_t)a * n_it, beta + (int64_t)a * n_it, n, al, b1, b2);
+  const double pivmin = DBL_MIN * fmax(1.0, ti.bmax);
+  const double pad = 2.0 * DBL_EPSILON * fmax(ti.tnorm, DBL_MIN) + 2.0 * pivmin;
+  double lo = ti.lo - pad, hi = ti.hi + pad;
   // multisection: count(lo) <= kidx < count(hi); EIG_T probes per round,
   // probe p at lo + (hi - lo) (p + 1) / (EIG_T + 1), evaluated by thread p
   for (int it = 0; it < 64; ++it) {
@@ -111,30 +130,69 @@ __global__ __launch_bounds__(EIG_T) void k_tridiag_eig(const double* __restrict_
     lo = nlo;
     hi = nhi;
   }
-  const double th = 0.5 * (lo + hi);
+  if (tid == 0) theta[(int64_t)a * r + c] = 0.5 * (lo + hi);
+}
 
-  // inverse iteration: LU of T - th I with partial pivoting on thread 0; the
-  // triangular solves carry the running entries in registers
+// Unit norm and the sign rule (first nonzero entry positive) for y[0..n), into
+// column k of Sa (rows n..n_it-1 zero); wave 0 only.
+__device__ __forceinline__ void store_unit_column(const double* y, int n, int n_it, int r, int k,
+                                                  double* Sa) {
+  const int lane = threadIdx.x & 63;
+  double nr = 0.0;
+  int first = n - 1;
+  for (int i = lane; i < n; i += 64) {
+    nr = fma(y[i], y[i], nr);
+    if (y[i] != 0.0 && i < first) first = i;
+  }
+  nr = wave_sum_f64(nr);
+  for (int o = 32; o >= 1; o >>= 1) first = min(first, __shfl_xor(first, o, 64));
+  double sc = 1.0 / sqrt(nr);
+  if (y[first] < 0.0) sc = -sc;
+  for (int i = lane; i < n_it; i += 64) Sa[(int64_t)i * r + k] = (i < n) ? y[i] * sc : 0.0;
+}
+
+// Seig: [n_act][n_it][r] (row k, kept column c); rows n_eff.. are zero.
+__global__ __launch_bounds__(EIG_T) void k_eig_vectors(const double* __restrict__ alpha,
+                                                       const double* __restrict__ beta,
+                                                       const int* __restrict__ neff, int n_it,
+                                                       int r, const double* __restrict__ theta,
+                                                       double* __restrict__ Seig) {
+  const int c = blockIdx.x, a = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int n = neff[a];
+  const int r_eff = min(r, n);
+  double* Sa = Seig + (int64_t)a * n_it * r;
+  if (c < r - r_eff) {
+    for (int k = tid; k < n_it; k += EIG_T) Sa[(int64_t)k * r + c] = 0.0;
+    return;
+  }
+  const double th = theta[(int64_t)a * r + c];
+  __shared__ double al[EIG_NMAX], b1[EIG_NMAX], b2[EIG_NMAX];
+  __shared__ double y[EIG_NMAX], w[EIG_NMAX];
+  __shared__ double fu1[EIG_NMAX], fu2[EIG_NMAX], fd[EIG_NMAX], fl[EIG_NMAX];
+  __shared__ int piv[EIG_NMAX];
+  const TriInfo ti = load_tridiag(alpha + (int64_t)a * n_it, beta + (int64_t)a * n_it, n, al, b1, b2);
+  // LU of T - th I with partial pivoting on thread 0; the triangular solves
+  // carry the running entries in registers
   if (tid == 0) {
-    const double eps_piv = DBL_EPSILON * fmax(tnorm, DBL_MIN);
+    const double eps_piv = DBL_EPSILON * fmax(ti.tnorm, DBL_MIN);
     // T - th I = P L U; U has diagonal fd (stored inverted), superdiagonals fu1,
-    // fu2.  Row k+1 is swapped up when its entry in column k is larger; both
+    // fu2.  Row i+1 is swapped up when its entry in column i is larger; both
     // cases are computed branch-free.
     double dcur = al[0] - th, ucur = (n > 1) ? b1[0] : 0.0;
-    for (int k = 0; k < n - 1; ++k) {
-      const double sub = b1[k];                   // entry (k+1, k)
-      const double dnext = al[k + 1] - th;
-      const double unext = (k + 1 < n - 1) ? b1[k + 1] : 0.0;
+    for (int i = 0; i < n - 1; ++i) {
+      const double sub = b1[i];                   // entry (i+1, i)
+      const double dnext = al[i + 1] - th;
+      const double unext = (i + 1 < n - 1) ? b1[i + 1] : 0.0;
       const bool swap = fabs(dcur) < fabs(sub);
       if (!swap && fabs(dcur) < eps_piv) dcur = (dcur < 0.0 ? -eps_piv : eps_piv);
       const double p = swap ? sub : dcur;         // pivot
       const double ip = rcp_nr(p);
       const double l = (swap ? dcur : sub) * ip;
-      fd[k] = ip;
-      fu1[k] = swap ? dnext : ucur;
-      fu2[k] = swap ? unext : 0.0;
-      fl[k] = l;
-      piv[k] = swap;
+      fd[i] = ip;
+      fu1[i] = swap ? dnext : ucur;
+      fu2[i] = swap ? unext : 0.0;
+      fl[i] = l;
+      piv[i] = swap;
       const double nd = swap ? fma(-l, dnext, ucur) : fma(-l, ucur, dnext);
       ucur = swap ? -l * unext : unext;
       dcur = nd;
@@ -144,62 +202,91 @@ __global__ __launch_bounds__(EIG_T) void k_tridiag_eig(const double* __restrict_
     fu1[n - 1] = 0.0;
     fu2[n - 1] = 0.0;
   }
-  // start vector: fixed pseudo-random entries in [-1, 1)
-  for (int k = tid; k < n; k += EIG_T) {
-    unsigned h = (unsigned)(k + 1) * 2654435761u;
+  // start vector: fixed pseudo-random entries in [-1, 1), a different
+  // sequence for each kept column (independent directions in a repeated
+  // eigenspace)
+  for (int i = tid; i < n; i += EIG_T) {
+    unsigned h = (unsigned)(i + 1) * 2654435761u + (unsigned)c * 0x9E3779B9u;
     h ^= h >> 15;
     h *= 2246822519u;
     h ^= h >> 13;
-    y[k] = (double)(h >> 8) * (2.0 / 16777216.0) - 1.0;
+    y[i] = (double)(h >> 8) * (2.0 / 16777216.0) - 1.0;
   }
   __syncthreads();
   for (int itr = 0; itr < 2; ++itr) {
     if (tid == 0) {
-      // forward: apply L^{-1} P to y into w (cur = running entry k); input and
+      // forward: apply L^{-1} P to y into w (cur = running entry i); input and
       // output arrays differ, so the loads run ahead of the recurrence
       double cur = y[0];
 #pragma unroll 4
-      for (int k = 0; k < n - 1; ++k) {
-        const double nxt = y[k + 1], l = fl[k];
-        const bool pk = piv[k];
-        w[k] = pk ? nxt : cur;
+      for (int i = 0; i < n - 1; ++i) {
+        const double nxt = y[i + 1], l = fl[i];
+        const bool pk = piv[i];
+        w[i] = pk ? nxt : cur;
         cur = pk ? fma(-l, nxt, cur) : fma(-l, cur, nxt);
       }
       w[n - 1] = cur;
-      // backward: U x = w into y (x1 = x[k+1], x2 = x[k+2])
+      // backward: U x = w into y (x1 = x[i+1], x2 = x[i+2])
       double x1 = 0.0, x2 = 0.0;
 #pragma unroll 4
-      for (int k = n - 1; k >= 0; --k) {
-        const double xk = ((w[k] - fu1[k] * x1) - fu2[k] * x2) * fd[k];
-        y[k] = xk;
+      for (int i = n - 1; i >= 0; --i) {
+        const double xi = ((w[i] - fu1[i] * x1) - fu2[i] * x2) * fd[i];
+        y[i] = xi;
         x2 = x1;
-        x1 = xk;
+        x1 = xi;
       }
     }
     __syncthreads();
     // rescale by the largest magnitude (every wave computes the same value)
     double mx = 0.0;
-    for (int k = lane; k < n; k += 64) mx = fmax(mx, fabs(y[k]));
+    for (int i = lane; i < n; i += 64) mx = fmax(mx, fabs(y[i]));
     for (int o = 32; o >= 1; o >>= 1) mx = fmax(mx, __shfl_xor(mx, o, 64));
     __syncthreads();
     const double inv = mx > 0.0 ? 1.0 / mx : 1.0;
-    for (int k = tid; k < n; k += EIG_T) y[k] *= inv;
+    for (int i = tid; i < n; i += EIG_T) y[i] *= inv;
     __syncthreads();
   }
-  // unit norm; sign such that the first nonzero entry is positive (wave 0)
-  if (wv == 0) {
-    double nr = 0.0;
-    int first = n - 1;
-    for (int k = lane; k < n; k += 64) {
-      nr = fma(y[k], y[k], nr);
-      if (y[k] != 0.0 && k < first) first = k;
+  if (wv == 0) store_unit_column(y, n, n_it, r, c, Sa);
+}
+
+// Per window: the kept columns of each cluster (consecutive kept eigenvalues
+// at most EIG_CLUSTER |T| apart) orthonormalised in ascending order by
+// modified Gram-Schmidt, two passes, against the cluster's earlier columns;
+// then unit norm and the sign rule again.  Windows without clusters only read
+// theta and T.
+__global__ __launch_bounds__(EIG_T) void k_eig_orth(const double* __restrict__ alpha,
+                                                    const double* __restrict__ beta,
+                                                    const int* __restrict__ neff, int n_it, int r,
+                                                    const double* __restrict__ theta,
+                                                    double* __restrict__ Seig) {
+  const int a = blockIdx.x, tid = threadIdx.x, wv = tid >> 6;
+  const int n = neff[a];
+  const int c_lo = r - min(r, n);
+  double* Sa = Seig + (int64_t)a * n_it * r;
+  const double* tha = theta + (int64_t)a * r;
+  __shared__ double al[EIG_NMAX], b1[EIG_NMAX], b2[EIG_NMAX];
+  __shared__ double y[EIG_NMAX];
+  __shared__ double red[EIG_T / 64];
+  const TriInfo ti = load_tridiag(alpha + (int64_t)a * n_it, beta + (int64_t)a * n_it, n, al, b1, b2);
+  const double ctol = EIG_CLUSTER * ti.tnorm;
+  for (int c = c_lo; c < r;) {
+    int c1 = c;
+    while (c1 + 1 < r && tha[c1 + 1] - tha[c1] <= ctol) ++c1;
+    for (int k = c + 1; k <= c1; ++k) {
+      if (tid < n) y[tid] = Sa[(int64_t)tid * r + k];
+      __syncthreads();
+      for (int pass = 0; pass < 2; ++pass) {
+        for (int p = c; p < k; ++p) {
+          const double sp = (tid < n) ? Sa[(int64_t)tid * r + p] : 0.0;
+          const double d = block_sum_f64((tid < n) ? y[tid] * sp : 0.0, red);
+          if (tid < n) y[tid] = fma(-d, sp, y[tid]);
+          __syncthreads();
+        }
+      }
+      if (wv == 0) store_unit_column(y, n, n_it, r, k, Sa);
+      __syncthreads();               // column k is read for the next members
     }
-    nr = wave_sum_f64(nr);
-    for (int o = 32; o >= 1; o >>= 1) first = min(first, __shfl_xor(first, o, 64));
-    double sc = 1.0 / sqrt(nr);
-    if (y[first] < 0.0) sc = -sc;
-    if (lane == 0) theta[(int64_t)a * r + c] = th;
-    for (int k = lane; k < n_it; k += 64) Sa[(int64_t)k * r + c] = (k < n) ? y[k] * sc : 0.0;
+    c = c1 + 1;
   }
 }
 
@@ -207,8 +294,13 @@ hipError_t launch_tridiag_eig(const double* alpha, const double* beta, const int
                               int n_act, int n_it, int r, double* theta, double* Seig,
                               hipStream_t s) {
   (void)hipGetLastError();
-  hipLaunchKernelGGL(k_tridiag_eig, dim3(r, n_act), dim3(EIG_T), 0, s, alpha, beta, neff, n_it, r,
-                     theta, Seig);
+  if (n_it > EIG_NMAX || r > n_it) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_eig_values, dim3(r, n_act), dim3(EIG_T), 0, s, alpha, beta, neff, n_it, r,
+                     theta);
+  hipLaunchKernelGGL(k_eig_vectors, dim3(r, n_act), dim3(EIG_T), 0, s, alpha, beta, neff, n_it,
+                     r, theta, Seig);
+  hipLaunchKernelGGL(k_eig_orth, dim3(n_act), dim3(EIG_T), 0, s, alpha, beta, neff, n_it, r, theta,
+                     Seig);
   return hipGetLastError();
 }
 

@@ -29,47 +29,21 @@ namespace slh {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-#ifndef FM_BK
-#define FM_BK 64                 // K per LDS stage (32 or 64)
-#endif
-#ifndef FM_NS
-#define FM_NS 2                  // LDS stages (loads run FM_NS - 1 stages ahead)
-#endif
-#ifndef FM_LSPREAD
-#define FM_LSPREAD 1             // k16 steps over which a stage's global->LDS loads are issued
-#endif
-#ifndef FM_NT
-#define FM_NT 1                  // stream Phi out with non-temporal stores
-#endif
-#ifndef FM_EPI
-#define FM_EPI 1                 // epilogue staging sync: 0 block barriers, 1 per wave
-#endif
-#ifndef FM_BIG_BN
-#define FM_BIG_BN 256            // N extent of the large tile (256 x FM_BIG_BN)
-#endif
-#ifndef FM_SROWS
-#define FM_SROWS 32              // epilogue rows staged per pass (16 or 32)
-#endif
-#ifndef FM_BIG_WGM
-#define FM_BIG_WGM 2             // waves along M in the large tile
-#endif
-#ifndef FM_BIG_WGN
-#define FM_BIG_WGN 4             // waves along N in the 256 x 256 tile (2 x FM_BIG_WGN waves)
-#endif
+constexpr int FM_BK = 64;                // K per LDS stage
+constexpr int FM_NS = 2;                 // LDS stages (loads run one stage ahead)
+constexpr int FM_LSPREAD = 1;            // k16 steps over which a stage's global->LDS loads go out
+constexpr int FM_SROWS = 32;             // epilogue rows staged per pass
 constexpr int FM_CPR = FM_BK / 8;        // 16-byte chunks per LDS row
 constexpr int FM_RPL = 64 / FM_CPR;      // rows filled by one 1 KB direct-to-LDS load
 
 // Physical 16-byte chunk of logical chunk c in LDS row r is c ^ fm_swz(r).  The
 // LDS serves 16 lanes' 16-byte reads per clock over 256 bytes, so the 16
 // consecutive rows read at one logical chunk must land in 16 distinct 16-byte
-// bank groups.  64-byte rows (4 chunks): row r sits at group 4 (r & 3) + chunk,
-// so the chunk must differ across r >> 2.  128-byte rows (8 chunks): group
-// 8 (r & 1) + chunk, so the chunk must differ across the even (odd) rows; the
-// r & 7 term also keeps any 8 consecutive rows distinct.
-__device__ __forceinline__ int fm_swz(int r) {
-  if constexpr (FM_CPR == 4) return (r >> 2) & 3;
-  else return (r & 7) ^ ((r >> 3) & 1);
-}
+// bank groups.  A 128-byte row (8 chunks) sits at group 8 (r & 1) + chunk, so
+// the chunk must differ across the even (odd) rows; the r & 7 term also keeps
+// any 8 consecutive rows distinct.
+static_assert(FM_CPR == 8, "the swizzle is laid out for 128-byte LDS rows");
+__device__ __forceinline__ int fm_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 // s_waitcnt vmcnt(N) for the counts the pipeline uses
 template <int N>
@@ -295,7 +269,6 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_featmap(FeatmapArgs a) {
   // pad 8 floats: rows 4 apart (the two half-waves of a store) start 32 banks apart
   constexpr int SROWS = FM_SROWS, SCOLS = WN + 8;    // staged rows x (cols + pad)
   constexpr int NV = SROWS / 2;                      // accumulator values per lane per pass
-  static_assert(SROWS == 16 || SROWS == 32, "stage 16 or 32 rows at a time");
   static_assert(WGM * WGN * SROWS * SCOLS * 4 <= FM_NS * (STAGE_A + STAGE_B) * 2, "staging exceeds LDS");
   static_assert(WM % 64 == 0, "row scales are held 64 rows per register");
   float* stage = (float*)smem + wave * (SROWS * SCOLS);
@@ -327,13 +300,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_featmap(FeatmapArgs a) {
           stage[r * SCOLS + 32 * j + fr] = acc[h][j][v];
         }
       }
-#if FM_EPI == 1
+      // the staging region is the wave's own: a wave barrier orders it
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#else
-      __syncthreads();
-#endif
       // all staged values and row scales are read before any store, so no
       // wait sits behind the row guard
       const int lr0 = h * 32 + hf * SROWS;          // wave-local row of staged row 0
@@ -355,24 +325,16 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_featmap(FeatmapArgs a) {
         o.w = fm_cos(vs[k].w + ps.w) * scs[k];
         if (row < n_rows) {
           float* dst = a.Phi + (int64_t)row * a.m + col;
-#if FM_NT
           // the four merge into one 16-byte streaming store
           __builtin_nontemporal_store(o.x, dst);
           __builtin_nontemporal_store(o.y, dst + 1);
           __builtin_nontemporal_store(o.z, dst + 2);
           __builtin_nontemporal_store(o.w, dst + 3);
-#else
-          *(float4*)dst = o;
-#endif
         }
       }
-#if FM_EPI == 1
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#else
-      __syncthreads();
-#endif
     }
   }
 }
@@ -398,9 +360,9 @@ hipError_t launch_featmap(const FeatmapArgs& a, int n_cu, hipStream_t s, hipEven
   // memory waits (measured at 4096 x 4096 x 1024, 8192 x 3584 x 256 and
   // 4000 x 3584 x 2048: the rule picks the fastest shape or one within 2%).
   const int64_t rb = (a.n_rows + 63) / 64, rb2 = (a.n_rows + 127) / 128;
-  const int64_t t256 = ((a.n_rows + 255) / 256) * (a.m / FM_BIG_BN);
-  if (a.m % FM_BIG_BN == 0 && t256 >= n_cu)
-    launch_tiles<256, FM_BIG_BN, FM_BIG_WGM, FM_BIG_WGN>(a, s, e0, e1);
+  const int64_t t256 = ((a.n_rows + 255) / 256) * (a.m / 256);
+  if (a.m % 256 == 0 && t256 >= n_cu)
+    launch_tiles<256, 256, 2, 4>(a, s, e0, e1);
   else if (rb2 * (a.m / 128) >= 2LL * n_cu)
     launch_tiles<128, 128, 2, 4>(a, s, e0, e1);
   else if (rb * (a.m / 128) >= 2LL * n_cu)

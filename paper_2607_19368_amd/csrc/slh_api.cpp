@@ -106,7 +106,16 @@ struct slh_ctx {
   // stage: 0 ready, 1 feature map done, 2 Lanczos done, 3 SimHash done
   int stage = 0;
   int n_it = 0;
-  const void* norms_of = nullptr;   // X for which the row norms are current
+  // Row norms (s(x) of Eq. 3, the member norms of Eq. 7) are computed from X
+  // by slh_route or slh_feature_map and reused only within the same pass over
+  // one prompt: slh_feature_map recomputes them unless slh_route has just
+  // computed them for the same X (norms_fresh), and slh_merge reuses them only
+  // if they were computed for the same X in this pass.  A new prompt written
+  // into the same buffer therefore never inherits the previous prompt's norms.
+  const void* norms_of = nullptr;   // X (pointer, type, stride) the row norms were taken from
+  int32_t norms_dtype = -1;
+  int64_t norms_ldx = -1;
+  bool norms_fresh = false;         // set by slh_route, consumed by slh_feature_map
   int64_t q1_L = -1;                // window length q1all was drawn for
 
   std::vector<DevBuf*> all;
@@ -127,6 +136,7 @@ struct slh_ctx {
   int normalize = 0;                // SLH_OPT_NORMALIZE
   int pos_scheme = 0;               // SLH_OPT_POS_SCHEME
   int merged = 0;                   // slh_merge ran on the current codes
+  int t_loaded = 0;                 // slh_load of alpha (1), beta (2), Q (4) since slh_lanczos
   int64_t Ntot = 0;                 // prompt length; N = Ntot - keep_last tokens are compressed
   int64_t keep_last = 0;            // SLH_OPT_KEEP_LAST
   int64_t target_len = 0;           // SLH_OPT_TARGET_LEN (0 = off)
@@ -249,7 +259,20 @@ int prep_norms(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx) {
                             c->gauss, P<double>(c->nrm2_fm), P<double>(c->nrm_x),
                             P<double>(c->inv_x), P<float>(c->rowscale), xb, c->stream));
   c->norms_of = X;
+  c->norms_dtype = dtype;
+  c->norms_ldx = ldx;
   return SLH_OK;
+}
+
+bool norms_match(const slh_ctx* c, const void* X, int32_t dtype, int64_t ldx) {
+  return c->norms_of == X && c->norms_dtype == dtype && c->norms_ldx == ldx;
+}
+
+void forget_norms(slh_ctx* c) {
+  c->norms_of = nullptr;
+  c->norms_dtype = -1;
+  c->norms_ldx = -1;
+  c->norms_fresh = false;
 }
 
 int upload_routing(slh_ctx* c) {
@@ -446,7 +469,7 @@ int slh_set_option(slh_ctx* c, int32_t key, double v) {
     case SLH_OPT_KERNEL:
       if (v != 0.0 && v != 1.0) return fail(c, SLH_EINVAL, "KERNEL must be 0 or 1");
       c->gauss = (int)v;
-      c->norms_of = nullptr;
+      forget_norms(c);
       break;
     case SLH_OPT_WINDOW_LEN: {
       const int64_t L = (int64_t)v;
@@ -486,7 +509,7 @@ int slh_set_option(slh_ctx* c, int32_t key, double v) {
       c->keep_last = K;
       c->N = Nc;
       c->n_win = Nc / Le;
-      c->norms_of = nullptr;
+      forget_norms(c);
       c->q1_L = -1;
       route_all_spectral(c);
       c->routed = false;
@@ -558,6 +581,8 @@ int slh_route(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, double rho,
                                         P<float>(c->rowscale), xb, P<double>(c->rsu),
                                         P<double>(c->rpart), P<double>(c->scores), c->stream));
     c->norms_of = X;
+    c->norms_dtype = dtype;
+    c->norms_ldx = ldx;
   } else {
     if ((rc = prep_norms(c, X, dtype, ldx))) return rc;
     HIP_TRY(c, launch_route_scores(X, dtype == SLH_BF16 ? 0 : 1, ldx, P<double>(c->inv_x),
@@ -589,6 +614,7 @@ int slh_route(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, double rho,
   }
   c->n_act = (int)c->winlist_h.size();
   c->chunk_k = std::max(1, (int)std::nearbyint(rho));   // round half to even
+  c->norms_fresh = true;
   c->routed = true;
   c->routing_on_device = false;
   drop_graph(c);
@@ -605,8 +631,9 @@ int slh_feature_map(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx) {
   int rc = check_x(c, X, dtype, ldx);
   if (rc) return rc;
   if ((rc = ensure_routing(c))) return rc;
-  if (c->norms_of != X || dtype == SLH_F32)
+  if (!(c->norms_fresh && norms_match(c, X, dtype, ldx)))
     if ((rc = prep_norms(c, X, dtype, ldx))) return rc;
+  c->norms_fresh = false;
   const int64_t L = window_len(c);
   const int64_t rows = (int64_t)c->n_act * L;
   ENSURE(c, c->Phi, (size_t)std::max<int64_t>(rows, 1) * c->m * sizeof(float));
@@ -790,6 +817,38 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
   }
   c->stage = 2;
   c->merged = 0;
+  c->t_loaded = 0;
+  return SLH_OK;
+}
+
+int slh_eigh_ritz(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) {
+  if (!c) return SLH_EINVAL;
+  const bool loaded = c->t_loaded == 7;
+  if (!loaded && c->stage < 2)
+    return fail(c, SLH_ESTATE, "slh_eigh_ritz needs slh_lanczos or slh_load of alpha, beta and Q");
+  if (n_it != c->n_it)
+    return fail(c, SLH_EINVAL, "n_it %d differs from the tridiagonal's order %d", n_it, c->n_it);
+  const int64_t L = window_len(c);
+  const int na = c->n_act;
+  if (na > 0) {
+    ENSURE(c, c->theta, (size_t)na * c->r * 8);
+    ENSURE(c, c->Seig, (size_t)na * n_it * c->r * 8);
+    ENSURE(c, c->Z, (size_t)na * L * c->r * 8);
+    HIP_TRY(c, launch_tridiag_eig(P<double>(c->alpha), P<double>(c->beta), P<int>(c->neff), na,
+                                  n_it, c->r, P<double>(c->theta), P<double>(c->Seig), c->stream));
+    HIP_TRY(c, launch_ritz(P<double>(c->Q), P<double>(c->Seig), P<int>(c->neff), na, (int)L,
+                           n_it + 1, n_it, c->r, P<double>(c->Z), c->stream));
+    if (ritz_out)
+      HIP_TRY(c, hipMemcpyAsync(ritz_out, c->theta.p, (size_t)na * c->r * 8, hipMemcpyDeviceToHost,
+                                c->stream));
+    if (iters_out)
+      HIP_TRY(c, hipMemcpyAsync(iters_out, c->neff.p, (size_t)na * 4, hipMemcpyDeviceToHost,
+                                c->stream));
+    if (ritz_out || iters_out) HIP_TRY(c, hipStreamSynchronize(c->stream));
+  }
+  c->lz_w_valid = false;            // the pass replay needs a Lanczos run
+  c->stage = 2;
+  c->merged = 0;
   return SLH_OK;
 }
 
@@ -825,7 +884,7 @@ int slh_merge(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, float* emb_
   if (!emb_out || !pos_out || !M_out) return fail(c, SLH_EINVAL, "NULL output");
   const int64_t need = capacity(c);
   if (cap < need) return fail(c, SLH_EINVAL, "cap %lld < required %lld", (long long)cap, (long long)need);
-  if (c->norms_of != X)
+  if (!norms_match(c, X, dtype, ldx))
     if ((rc = prep_norms(c, X, dtype, ldx))) return rc;
   const int64_t L = window_len(c);
   const int64_t N = c->N;
@@ -918,6 +977,7 @@ int slh_merge(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, float* emb_
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   *M_out = M + c->keep_last;
   c->merged = 1;
+  forget_norms(c);                  // the next prompt may reuse this buffer
   return SLH_OK;
 }
 
@@ -943,8 +1003,8 @@ int slh_bucket_purity(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, dou
   int rc = check_x(c, X, dtype, ldx);
   if (rc) return rc;
   if (!(thresh >= -1.0 && thresh <= 1.0)) return fail(c, SLH_EINVAL, "thresh must be in [-1, 1]");
-  if (c->norms_of != X)
-    if ((rc = prep_norms(c, X, dtype, ldx))) return rc;
+  if ((rc = prep_norms(c, X, dtype, ldx))) return rc;
+  forget_norms(c);
   const int64_t N = c->N, L = window_len(c);
   // tiles of 64 x 64 sorted positions that hold same-bucket pairs (spectral windows)
   std::vector<int> seg((size_t)N);
@@ -1054,6 +1114,7 @@ int slh_time_passes(slh_ctx* c, int32_t reps, double* us_out) {
 
 int slh_load(slh_ctx* c, int32_t which, const void* src, int64_t bytes) {
   if (!c || !src) return SLH_EINVAL;
+  forget_norms(c);
   const int64_t L = window_len(c);
   const int64_t na = c->n_act;
   int rc = ensure_routing(c);
@@ -1076,7 +1137,40 @@ int slh_load(slh_ctx* c, int32_t which, const void* src, int64_t bytes) {
     c->merged = 0;
     return SLH_OK;
   }
-  return fail(c, SLH_EINVAL, "slh_load supports SLH_OUT_PHI and SLH_OUT_CODES");
+  if (which == SLH_OUT_ALPHA) {
+    // alpha of every spectral window: n_act x n_it doubles; sets n_it and
+    // n_eff = n_it (and clears beta)
+    if (na < 1 || bytes <= 0 || bytes % (na * 8) != 0)
+      return fail(c, SLH_EINVAL, "bytes must be a positive multiple of n_act * 8");
+    const int64_t n_it = bytes / (na * 8);
+    if (n_it < c->r || n_it > std::min<int64_t>(L, 256))
+      return fail(c, SLH_EINVAL, "need r <= n_it <= min(L, 256) (n_it=%lld)", (long long)n_it);
+    ENSURE(c, c->alpha, (size_t)bytes);
+    ENSURE(c, c->beta, (size_t)bytes);
+    ENSURE(c, c->neff, (size_t)na * 4);
+    ENSURE(c, c->Q, (size_t)na * (n_it + 1) * L * 8);
+    HIP_TRY(c, hipMemcpyAsync(c->alpha.p, src, (size_t)bytes, hipMemcpyDeviceToDevice, c->stream));
+    HIP_TRY(c, hipMemsetAsync(c->beta.p, 0, (size_t)bytes, c->stream));
+    std::vector<int> ne((size_t)na, (int)n_it);
+    HIP_TRY(c, hipMemcpyAsync(c->neff.p, ne.data(), ne.size() * 4, hipMemcpyHostToDevice, c->stream));
+    HIP_TRY(c, hipStreamSynchronize(c->stream));     // ne leaves scope
+    c->n_it = (int)n_it;
+    c->t_loaded = 1;
+    c->lz_w_valid = false;
+    c->stage = 1;
+    c->merged = 0;
+    return SLH_OK;
+  }
+  if (which == SLH_OUT_BETA || which == SLH_OUT_Q) {
+    if (!(c->t_loaded & 1)) return fail(c, SLH_ESTATE, "load SLH_OUT_ALPHA first");
+    const int64_t want = which == SLH_OUT_BETA ? na * c->n_it * 8 : na * (c->n_it + 1) * L * 8;
+    if (bytes != want) return fail(c, SLH_EINVAL, "bytes must be %lld", (long long)want);
+    DevBuf& b = which == SLH_OUT_BETA ? c->beta : c->Q;
+    HIP_TRY(c, hipMemcpyAsync(b.p, src, (size_t)want, hipMemcpyDeviceToDevice, c->stream));
+    c->t_loaded |= which == SLH_OUT_BETA ? 2 : 4;
+    return SLH_OK;
+  }
+  return fail(c, SLH_EINVAL, "slh_load supports SLH_OUT_PHI, ALPHA, BETA, Q and CODES");
 }
 
 int slh_copy_out(slh_ctx* c, int32_t which, void* dst, int64_t bytes) {

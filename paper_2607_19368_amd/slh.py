@@ -27,7 +27,7 @@ EXPORTS = [
     "slh_set_option", "slh_set_stream", "slh_route", "slh_feature_map", "slh_lanczos",
     "slh_simhash", "slh_merge", "slh_merge_capacity", "slh_copy_out", "slh_num_windows",
     "slh_num_spectral", "slh_load", "slh_stage_times", "slh_time_passes", "slh_spectral_energy",
-    "slh_bucket_purity",
+    "slh_bucket_purity", "slh_eigh_ritz", "slh_peak_read", "slh_peak_mfma",
 ]
 
 _lib = None
@@ -57,6 +57,9 @@ def load():
         "slh_route": (i32, [vp, vp, i32, i64, ctypes.c_double, ctypes.c_double, vp, vp]),
         "slh_feature_map": (i32, [vp, vp, i32, i64]),
         "slh_lanczos": (i32, [vp, i32, vp, vp]),
+        "slh_eigh_ritz": (i32, [vp, i32, vp, vp]),
+        "slh_peak_read": (i32, [vp, i64, i32, vp, vp]),
+        "slh_peak_mfma": (i32, [i32, vp, vp, vp]),
         "slh_simhash": (i32, [vp, vp]),
         "slh_merge": (i32, [vp, vp, i32, i64, vp, vp, vp, i64, vp]),
         "slh_merge_capacity": (i64, [vp]),
@@ -202,6 +205,21 @@ def slh_lanczos(ctx, n_it, want=True):
     return None
 
 
+def slh_eigh_ritz(ctx, n_it, want=True):
+    """Eigh(T) and Z = Q S on the context's T and Q (after slh_lanczos, or after
+    slh_load of SLH_OUT_ALPHA, SLH_OUT_BETA and SLH_OUT_Q); returns (ritz, iters)
+    as slh_lanczos does, or None."""
+    ctx.n_it = n_it
+    na = ctx.n_spectral
+    if want:
+        ritz = np.zeros((na, ctx.r), np.float64)
+        iters = np.zeros(na, np.int32)
+        _check(ctx, load().slh_eigh_ritz(ctx.handle, n_it, _ptr(ritz), _ptr(iters)), "slh_eigh_ritz")
+        return ritz, iters
+    _check(ctx, load().slh_eigh_ritz(ctx.handle, n_it, None, None), "slh_eigh_ritz")
+    return None
+
+
 def slh_simhash(ctx, codes_out=None):
     p = ctypes.c_void_p(codes_out.data_ptr()) if codes_out is not None else None
     _check(ctx, load().slh_simhash(ctx.handle, p), "slh_simhash")
@@ -266,9 +284,12 @@ def slh_time_passes(ctx, reps=96):
 
 
 def slh_load(ctx, which, src):
-    """Replace the Phi (SLH_OUT_PHI) or codes (SLH_OUT_CODES) stage result with a device tensor."""
+    """Replace a stage result (SLH_OUT_PHI, SLH_OUT_ALPHA, SLH_OUT_BETA, SLH_OUT_Q or
+    SLH_OUT_CODES) with a device tensor."""
     nbytes = src.numel() * src.element_size()
     _check(ctx, load().slh_load(ctx.handle, which, ctypes.c_void_p(src.data_ptr()), nbytes), "slh_load")
+    if which == SLH_OUT_ALPHA:
+        ctx.n_it = nbytes // (8 * max(1, ctx.n_spectral))
 
 
 def slh_copy_out(ctx, which):
@@ -279,7 +300,17 @@ def slh_copy_out(ctx, which):
 
 
 def compress(ctx, X, n_it, rho=None, tau=-1.0, want_ritz=False):
-    """The whole path on one prompt: [route] -> feature map -> Lanczos -> SimHash -> merge."""
+    """The whole path on one prompt: [route] -> feature map -> Lanczos -> SimHash -> merge.
+
+    rho <= 1 is the identity path (the paper's appendix on backends: at a
+    compression ratio of at most one the prompt is returned as it is): X itself,
+    positions 0..N-1 and the identity token map, with M = N and no library call
+    (ctx may then be None)."""
+    if rho is not None and rho <= 1.0:
+        import torch
+        N = X.shape[0]
+        pos = torch.arange(N, dtype=torch.int32, device=X.device)
+        return X, pos, pos.clone(), N, None
     if rho is not None:
         slh_route(ctx, X, rho, tau)
     slh_feature_map(ctx, X)
@@ -304,3 +335,28 @@ def slh_bucket_purity(ctx, X, thresh=0.7):
     _check(ctx, load().slh_bucket_purity(ctx.handle, p, dt, ld, float(thresh), _ptr(out)),
            "slh_bucket_purity")
     return int(out[0]), int(out[1])
+
+
+def slh_peak_read(buf, reps=20, stream=None):
+    """GB/s of a plain streaming read of the device tensor `buf` (measurement aid)."""
+    import torch
+    st = torch.cuda.current_stream() if stream is None else stream
+    out = np.zeros(1, np.float64)
+    rc = load().slh_peak_read(ctypes.c_void_p(buf.data_ptr()), buf.numel() * buf.element_size(),
+                              int(reps), ctypes.c_void_p(st.cuda_stream), _ptr(out))
+    if rc != SLH_OK:
+        raise SLHError(f"slh_peak_read failed ({rc})")
+    return float(out[0])
+
+
+def slh_peak_mfma(reps=10, stream=None):
+    """TFLOP/s of independent dense bf16 MFMA chains (measurement aid)."""
+    import torch
+    st = torch.cuda.current_stream() if stream is None else stream
+    sink = torch.empty(4, dtype=torch.float32, device="cuda")
+    out = np.zeros(1, np.float64)
+    rc = load().slh_peak_mfma(int(reps), ctypes.c_void_p(sink.data_ptr()),
+                              ctypes.c_void_p(st.cuda_stream), _ptr(out))
+    if rc != SLH_OK:
+        raise SLHError(f"slh_peak_mfma failed ({rc})")
+    return float(out[0])

@@ -58,6 +58,8 @@ class Run:
     route: np.ndarray = None
     R: np.ndarray = None             # SimHash hyperplanes (oracle runs)
     rowsum: np.ndarray = None        # estimated row sums of the normalised operator
+    xrows: object = None             # oracle runs: rows -> X as given (float64), for checks
+    compact: bool = False            # positions are 0..M-1
 
 
 def run_gpu(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel=0, compact=False,
@@ -137,6 +139,8 @@ def run_oracle(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel="softmax"
     psi = OP.phases(seed, wl.m)
     R = OP.hyperplanes(seed, wl.r, wl.bits)
     run = Run()
+    run.xrows = inp.x_float
+    run.compact = compact
     Es, Ps = [], []
     t2m = np.zeros(N, np.int64)
     base = 0
@@ -192,6 +196,17 @@ def run_oracle(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel="softmax"
     return run
 
 
+_PARAMS = {}
+
+
+def _params(seed, D, m, r, bits):
+    """The oracle's W, psi, R for these sizes, drawn once per process."""
+    key = (seed, D, m, r, bits)
+    if key not in _PARAMS:
+        _PARAMS[key] = (OP.projection(seed, D, m), OP.phases(seed, m), OP.hyperplanes(seed, r, bits))
+    return _PARAMS[key]
+
+
 def oracle_uncertainty(inp, w, L, n_it, seed=0, normalise=False):
     """How far two valid fp64 evaluations of the method disagree on window w.
 
@@ -201,9 +216,7 @@ def oracle_uncertainty(inp, w, L, n_it, seed=0, normalise=False):
     max |proj - proj_reversed| over the window: SimHash bits whose oracle
     projection is smaller than this are not determined in fp64 arithmetic."""
     wl = inp.workload
-    W = OP.projection(seed, wl.D, wl.m)
-    psi = OP.phases(seed, wl.m)
-    R = OP.hyperplanes(seed, wl.r, wl.bits)
+    W, psi, R = _params(seed, wl.D, wl.m, wl.r, wl.bits)
     Xw = inp.x_float(slice(w * L, (w + 1) * L))
     q1 = OP.start_vector(seed, L, w)
     rv = np.arange(L)[::-1]
@@ -238,6 +251,8 @@ class Report:
     buckets_excluded: int = 0
     undetermined_rows: int = 0
     undecided_windows: int = 0
+    literal_rule_mismatch_rows: int = 0   # code mismatches outside the bare 1e-5 band
+    gpu_macros_validated: int = 0         # GPU macros checked on their own members
 
 
 def compare(o, g, L, check_spectral=True, ritz_rel=RITZ_REL, angle=ANGLE, emb_rel=EMB_REL,
@@ -303,17 +318,25 @@ def compare(o, g, L, check_spectral=True, ritz_rel=RITZ_REL, angle=ANGLE, emb_re
         if undecided:
             rep.undetermined_rows += L
             rep.excluded_rows += L
+            rep.literal_rule_mismatch_rows += int(np.count_nonzero(
+                (a.codes != b.codes) & ~np.any(np.abs(a.proj) < EXCL, axis=1)))
             excluded_tok[w * L:(w + 1) * L] = True
             continue
         ex = np.any(np.abs(a.proj) < EXCL, axis=1)
+        rep.literal_rule_mismatch_rows += int(np.count_nonzero((a.codes != b.codes) & ~ex))
         tiny = (a.ritz != 0) & (np.abs(a.ritz) <= floor_a)
         if np.count_nonzero(tiny) >= 2 and o.R is not None:
             # a null space of dimension >= 2 inside the Krylov space: any basis of
             # it is a valid set of Ritz vectors, so a bit is determined only where
-            # no rotation of that basis can flip it (Cauchy-Schwarz bound)
+            # no rotation of that basis can flip it.  The null space adds
+            # Z[i, null] U R[null, l] to the projection for some orthogonal U,
+            # at most |Z[i, null]| |R[null, l]| in magnitude (Cauchy-Schwarz),
+            # so the part of the projection outside the null space must exceed
+            # that bound
             zt = np.linalg.norm(a.Z[:, tiny], axis=1)[:, None]
             rt = np.linalg.norm(o.R[tiny], axis=0)[None, :]
-            und = np.any(np.abs(a.proj) <= zt * rt, axis=1) & ~ex
+            p_out = a.Z[:, ~tiny] @ o.R[~tiny]
+            und = np.any(np.abs(p_out) <= zt * rt, axis=1) & ~ex
             rep.undetermined_rows += int(und.sum())
             ex |= und
         if unc is not None and w in unc:
@@ -353,15 +376,18 @@ def compare(o, g, L, check_spectral=True, ritz_rel=RITZ_REL, angle=ANGLE, emb_re
         assert np.all(np.diff(g.P) >= 0)
     else:
         assert np.all(np.diff(g.P) > 0)
+    compact = bool(o.compact)
     for k, mm in enumerate(members_g):
-        if g.P[k] == k:
-            continue                                   # compact positions (or coincidence)
+        if compact:
+            assert g.P[k] == k
+            continue
         if scheme == "max":
             assert g.P[k] == max(mm)
         elif scheme == "median":
             assert g.P[k] in mm
         else:
             assert min(mm) <= g.P[k] <= max(mm)
+    matched = np.zeros(Mg, bool)
     for k, mm in enumerate(members_o):
         if excluded_tok[mm].any():
             rep.buckets_excluded += 1
@@ -374,4 +400,25 @@ def compare(o, g, L, check_spectral=True, ritz_rel=RITZ_REL, angle=ANGLE, emb_re
         rep.max_emb_rel = max(rep.max_emb_rel, float(err))
         assert err <= emb_rel, (k, err)
         rep.buckets_checked += 1
+        matched[kg] = True
+    # every GPU macro-token no checked oracle bucket vouches for (it holds a row
+    # the rules exclude) must still be a valid macro-token of its own members:
+    # one window, one GPU code (spectral windows), the scheme's position of
+    # its members, and the Eq. 7 renormalised mean of their rows
+    if o.xrows is not None:
+        gcodes = {w.w: w.codes for w in g.windows}
+        for kg in np.flatnonzero(~matched):
+            mm = np.asarray(members_g[kg])
+            w0 = int(mm[0]) // L
+            assert np.all(mm // L == w0), (kg, mm[:5])          # one window
+            if w0 in gcodes:                                     # one code
+                cw = gcodes[w0][mm - w0 * L]
+                assert np.all(cw == cw[0]), (kg, np.unique(cw))
+            if not compact and scheme == "max":
+                assert g.P[kg] == mm.max()
+            ref = O.renormalised_mean(o.xrows(mm))
+            den = np.linalg.norm(ref)
+            err = np.linalg.norm(g.E[kg] - ref) / (den if den > 0 else 1.0)
+            assert err <= emb_rel, (kg, err)
+            rep.gpu_macros_validated += 1
     return rep

@@ -92,3 +92,14 @@ def test_header_constants_match_binding():
     assert len(defs) >= 20
     for name, val in defs.items():
         assert getattr(B, name) == int(val), name
+
+
+@pytest.mark.parametrize("rho", [1.0, 0.5])
+def test_identity_path_returns_prompt_unchanged(rho):
+    """rho <= 1: the wrapper returns X itself with positions 0..N-1 and the
+    identity token map, without calling the library (no GPU involved)."""
+    import torch
+    X = torch.randn(37, 16, dtype=torch.float32)
+    E, P, t2m, M, lz = B.compress(None, X, 8, rho=rho)
+    assert E is X and M == 37 and lz is None
+    assert torch.equal(P, torch.arange(37, dtype=torch.int32)) and torch.equal(t2m, P)

@@ -123,6 +123,141 @@ def test_lanczos_stage_on_oracle_phi(case):
     assert np.max(np.abs(gw.proj - proj)) < 1e-7
 
 
+# ------------------------------------------------------------------ Eigh(T) on given tridiagonals
+def _tridiag_case(case):
+    """(list of (alpha, beta) per window, r): beta has n entries, the last unused."""
+    rng = np.random.default_rng(31)
+    if case == "wilkinson21":
+        n = 21
+        al = np.abs(10.0 - np.arange(n))
+        return [(al, np.ones(n))], 21
+    if case == "toeplitz96":
+        n = 96
+        return [(np.full(n, 2.0), np.full(n, -1.0))], 64
+    if case == "repeated_blocks":
+        bd = rng.uniform(0.0, 4.0, 8)
+        bo = rng.uniform(0.5, 1.5, 8)
+        al = np.tile(bd, 3)
+        be = np.tile(bo, 3)
+        be[7] = be[15] = 0.0
+        return [(al, be)], 24
+    if case == "null_space":
+        al = np.concatenate([np.zeros(4), rng.uniform(1.0, 3.0, 12)])
+        be = np.concatenate([np.zeros(4), rng.uniform(0.2, 0.8, 12)])
+        return [(al, be)], 16
+    # three windows of order 21: W21+, W21- and a random T
+    n = 21
+    k = np.arange(n)
+    return [(np.abs(10.0 - k), np.ones(n)), (10.0 - k, np.ones(n)),
+            (rng.uniform(-2, 2, n), rng.uniform(0.1, 1.0, n))], 12
+
+
+@pytest.mark.parametrize("case", ["wilkinson21", "toeplitz96", "repeated_blocks", "null_space",
+                                  "windows"])
+def test_eigensolve_stage(case):
+    """Eigh(T) and the Ritz coordinates alone (slh_eigh_ritz, Algorithm 1) on
+    tridiagonals loaded with slh_load, with Q = [I; 0] so that Z holds the kept
+    eigenvectors S.  Wilkinson's W21+ has a top pair 1e-13 apart; the repeated
+    blocks give every eigenvalue multiplicity 3; the null-space case has a
+    4-fold zero eigenvalue; the Toeplitz T has the closed-form spectrum
+    a + 2 b cos(k pi / (n + 1)).  Eigenvalues within 1e-12 relative of LAPACK
+    (absolute 1e-13 |T| for zero ones), kept vectors orthonormal to 1e-10,
+    residuals |T s - theta s| <= 1e-12 |T|, the first nonzero entry of each
+    vector positive, vectors outside clusters equal to LAPACK's within their
+    conditioning (1e-10 + 4 eps |T| / gap, the gap to the nearest other
+    eigenvalue of T), and cluster columns spanning LAPACK's subspace.  Where
+    the first nonzero entry is at rounding level (an exact zero in LAPACK's
+    vector of a decoupled block) its sign is not determined, and the vector is
+    compared up to sign."""
+    import torch
+    import paper_2607_19368_amd as P
+    from paper_2607_19368_amd import slh as B
+    wins, r = _tridiag_case(case)
+    nw, n = len(wins), len(wins[0][0])
+    L = 64 if nw > 1 else max(64, n)
+    ctx = P.slh_create(L * nw, 8, 256, r, 1, 0)
+    if nw > 1:
+        P.slh_set_option(ctx, B.SLH_OPT_WINDOW_LEN, L)
+    al = np.stack([w[0] for w in wins]).astype(np.float64)
+    be = np.stack([w[1] for w in wins]).astype(np.float64)
+    Q = np.zeros((nw, n + 1, L))
+    Q[:, np.arange(n), np.arange(n)] = 1.0
+    for which, arr in ((B.SLH_OUT_ALPHA, al), (B.SLH_OUT_BETA, be), (B.SLH_OUT_Q, Q)):
+        P.slh_load(ctx, which, torch.from_numpy(np.ascontiguousarray(arr)).cuda())
+    ritz, iters = P.slh_eigh_ritz(ctx, n)
+    Z = P.slh_copy_out(ctx, B.SLH_OUT_Z)
+    assert list(iters) == [n] * nw
+    for a in range(nw):
+        T = O.tridiagonal(al[a], be[a][:n - 1])
+        tn = np.max(np.sum(np.abs(T), axis=1))
+        th_all, S_all = O.eigh_tridiagonal(al[a], be[a][:n - 1])
+        th_o, S_o = th_all[n - r:], S_all[:, n - r:]
+        S = Z[a][:n]
+        assert np.all(Z[a][n:] == 0)
+        big = np.abs(th_o) > 1e-3 * tn
+        err = np.abs(ritz[a] - th_o)
+        assert np.all(err[big] <= 1e-12 * np.abs(th_o[big])), (case, a, err[big].max())
+        assert np.all(err[~big] <= 1e-13 * tn), (case, a, err[~big].max(initial=0))
+        orth = np.abs(S.T @ S - np.eye(r)).max()
+        res = np.abs(T @ S - S * ritz[a][None, :]).max()
+        _say(f"[eigh] {case} window {a}: max theta err {err.max():.2e}  |S^T S - I| {orth:.2e}  "
+             f"residual {res:.2e} (|T| {tn:.2f})")
+        assert orth <= 1e-10 and res <= 1e-12 * tn
+        for c in range(r):
+            nz = np.flatnonzero(S[:, c] != 0.0)
+            assert S[nz[0], c] > 0
+        # clusters by the same rule as the library: gaps <= 1e-6 |T|
+        gaps = np.diff(th_o) <= 1e-6 * tn
+        c = 0
+        while c < r:
+            c1 = c
+            while c1 + 1 < r and gaps[c1]:
+                c1 += 1
+            if c1 == c:
+                kk = n - r + c
+                gap = min([abs(th_all[kk] - th_all[q]) for q in (kk - 1, kk + 1) if 0 <= q < n],
+                          default=tn)
+                tol = 1e-10 + 4 * 2.2e-16 * tn / max(gap, 1e-300)
+                first = S[np.flatnonzero(S[:, c] != 0.0)[0], c]
+                d_same = np.abs(S[:, c] - S_o[:, c]).max()
+                d = d_same if abs(first) > 1e-12 else min(d_same, np.abs(S[:, c] + S_o[:, c]).max())
+                assert d <= tol, (case, a, c, d, tol)
+            else:
+                sv = np.linalg.svd(S_o[:, c:c1 + 1].T @ S[:, c:c1 + 1], compute_uv=False)
+                assert sv.min() >= 1.0 - 1e-10, (case, a, c, c1, sv)
+            c = c1 + 1
+
+
+@pytest.mark.parametrize("n_it", [96, 160, 256])
+def test_lanczos_basis_orthonormal(n_it):
+    """The GPU Lanczos basis (Algorithm 2 with full re-orthogonalization: the
+    three-term recurrence, then one classical Gram-Schmidt pass against the
+    whole basis, beta from |z1|^2 - |h2|^2) on the oracle's Phi stays
+    orthonormal: |Q^T Q - I| <= 1e-12 over the n_it vectors, and its alpha and
+    beta match the oracle's (two Gram-Schmidt passes) to 1e-9."""
+    import torch
+    import paper_2607_19368_amd as P
+    from paper_2607_19368_amd import slh as B
+    inp = _custom("qorth", 4000, 264, 512, n_it, 8, 8)
+    wl = inp.workload
+    Phi32 = O.feature_map(inp.x_float(), OP.projection(0, wl.D, wl.m),
+                          OP.phases(0, wl.m)).astype(np.float32)
+    ctx = P.slh_create(wl.N, wl.D, wl.m, wl.r, wl.bits, 0)
+    P.slh_load(ctx, B.SLH_OUT_PHI, torch.from_numpy(Phi32).cuda())
+    _, iters = P.slh_lanczos(ctx, n_it)
+    assert iters[0] == n_it
+    Q = P.slh_copy_out(ctx, B.SLH_OUT_Q)[0][:n_it]
+    orth = np.abs(Q @ Q.T - np.eye(n_it)).max()
+    lz = O.lanczos(Phi32.astype(np.float64), OP.start_vector(0, wl.N, 0), n_it)
+    al = P.slh_copy_out(ctx, B.SLH_OUT_ALPHA)[0]
+    be = P.slh_copy_out(ctx, B.SLH_OUT_BETA)[0]
+    ra = np.max(np.abs(al - lz.alpha) / np.abs(lz.alpha))
+    rb = np.max(np.abs(be - lz.beta) / np.abs(lz.beta))
+    _say(f"[basis] n_it={n_it}: |Q^T Q - I| = {orth:.2e}  alpha rel {ra:.2e}  beta rel {rb:.2e}")
+    assert orth <= 1e-12
+    assert ra <= 1e-9 and rb <= 1e-9
+
+
 # ------------------------------------------------------------------ merge on the oracle's codes
 @pytest.mark.parametrize("case", ["tiny", "mistral7b", "windows"])
 def test_merge_stage_on_oracle_codes(case):
@@ -316,6 +451,57 @@ def test_timing_mode_matches_graph_mode_qwen7b():
         assert np.array_equal(a.alpha, b.alpha) and np.array_equal(a.beta, b.beta)
         assert np.array_equal(a.Z, b.Z) and np.array_equal(a.codes, b.codes)
 
+@pytest.mark.parametrize("routed", [False, True])
+def test_two_prompts_one_context_same_buffer(routed):
+    """A second prompt written into the device buffer of the first and run
+    through the same context gives, bit for bit, what a fresh context and a
+    fresh buffer give it: the row norms behind s(x) (Eq. 3) and the member
+    norms of Eq. 7 are taken from the new prompt, not reused by address.
+    Prompt B's rows are twice those of another Zipf prompt (exact in bf16), so
+    every norm differs.  routed: 4 windows of 256 through slh_route first
+    (whose row norms feed the feature map of the same pass)."""
+    import torch
+    import paper_2607_19368_amd as P
+    from paper_2607_19368_amd import slh as B
+    from workloads import f32_to_bf16_bits
+    L = 256
+    ia = _custom("pa", 4 * L, 512, 256, 16, 8, 8, seed=0)
+    ib = _custom("pb", 4 * L, 512, 256, 16, 8, 8, seed=1)
+    xb = Inputs(ib.workload, f32_to_bf16_bits(2.0 * ib.x_float()), ib.ids)
+    wl = ia.workload
+
+    def run(ctx, Xd):
+        if routed:
+            P.slh_route(ctx, Xd, 8.0, 0.25)
+        P.slh_feature_map(ctx, Xd)
+        P.slh_lanczos(ctx, wl.n_it, want=False)
+        P.slh_simhash(ctx)
+        E, Pp, t2m, M = P.slh_merge(ctx, Xd)
+        torch.cuda.synchronize()
+        return (E.cpu().numpy().copy(), Pp.cpu().numpy().copy(), t2m.cpu().numpy().copy(),
+                P.slh_copy_out(ctx, B.SLH_OUT_CODES), P.slh_copy_out(ctx, B.SLH_OUT_Z))
+
+    def fresh(inp):
+        ctx = P.slh_create(wl.N, wl.D, wl.m, wl.r, wl.bits, 0)
+        if routed:
+            P.slh_set_option(ctx, B.SLH_OPT_WINDOW_LEN, L)
+        return ctx
+
+    ctx = fresh(ia)
+    buf = PR.to_device_x(ia)
+    out_a = run(ctx, buf)
+    buf.copy_(PR.to_device_x(xb))
+    out_b = run(ctx, buf)
+    ref_b = run(fresh(xb), PR.to_device_x(xb))
+    ref_a = run(fresh(ia), PR.to_device_x(ia))
+    _say(f"[two prompts] routed={routed} M_a={len(out_a[1])} M_b={len(out_b[1])}")
+    for u, v in zip(out_b, ref_b):
+        assert u.shape == v.shape and np.array_equal(u, v)
+    for u, v in zip(out_a, ref_a):
+        assert u.shape == v.shape and np.array_equal(u, v)
+    assert not np.array_equal(out_a[0][:4], out_b[0][:4])
+
+
 def test_call_order_and_capacity_errors():
     import torch
     import paper_2607_19368_amd as P
@@ -388,15 +574,17 @@ def test_windows_with_and_without_breakdown():
     PR.compare(o, g, L, check_spectral=False)
 
 
+@pytest.mark.timeout(900)
 def test_end_to_end_local16():
     """Local backend at the paper's defaults: windows of 16 tokens, m = 256, a
-    full 16-step Krylov space per window (reduced to 64 windows here).  A window
+    full 16-step Krylov space per window, on all 512 windows (and the 12 kept
+    tokens) of the benchmark's prompt.  A window
     holding repeated tokens has a rank-deficient operator; with r = 16 all of its
     Ritz vectors are kept, including a basis of the null space inside the Krylov
     space, which the method leaves arbitrary when it is 2-dimensional or more.
     Such windows' SimHash bits are not determined, and the oracle's own
     reversed-order evaluation (parity.oracle_uncertainty) marks them."""
-    inp = make_inputs("local16", N=1036)
+    inp = make_inputs("local16")
     wl = inp.workload
     _say(f"[e2e] local16 N={wl.N} window={wl.window} n_it={wl.n_it} r={wl.r} bits={wl.bits}")
     g = PR.run_gpu(inp, n_it=wl.n_it, window=wl.window)
