@@ -346,6 +346,33 @@ int slh_bucket_purity(slh_ctx *ctx, const void *X, int32_t x_dtype, int64_t ldx,
 int slh_peak_read(void *buf, int64_t bytes, int32_t reps, void *stream, double *gbs_out);
 int slh_peak_mfma(int32_t reps, void *sink, void *stream, double *tflops_out);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the merge of
+ * slh_merge for one window of N tokens from codes the caller supplies (what
+ * slh_load(SLH_OUT_CODES) followed by slh_merge computes on a one-window
+ * context: max positions, representative mode, no preserved suffix or target
+ * length), with no context and no allocation.  Every workspace lives in one
+ * fixed array of SLH_NOALLOC_BYTES device bytes per GPU, which the library
+ * holds from its first call on that GPU until the process ends.
+ * Limits: 2 <= N <= 8192; 8 <= D <= 4096, D % 8 == 0; 1 <= bits <= 16 and
+ * every code < 2^bits; cap >= min(N, 2^bits).  Larger sizes are rejected with
+ * SLH_EINVAL before any GPU work.
+ * X: device, N x D of x_dtype, row stride ldx (ldx >= D, ldx % 8 == 0, 16-byte
+ * aligned); codes: device, N uint32; emb_out: device, cap x D floats; pos_out:
+ * device, cap int32; tok2macro_out: device, N int32, may be NULL; *M_out
+ * (host) receives M.  stream: a hipStream_t (NULL = null stream); the call
+ * synchronises it (M goes to the host).
+ * Every call on one GPU uses that GPU's array and overwrites what the last call
+ * left there: calls that overlap in time on one GPU (other threads, other
+ * streams) race, and the caller must serialise them.  SLH_EHIP if the array's
+ * device address cannot be obtained or a launch fails.
+ */
+#define SLH_NOALLOC_BYTES 17355008
+int slh_merge_noalloc(const void *X, int32_t x_dtype, int64_t ldx, int64_t N, int64_t D,
+                      const uint32_t *codes, int32_t bits, float *emb_out, int32_t *pos_out,
+                      int32_t *tok2macro_out, int64_t cap, int64_t *M_out, void *stream);
+
 /* Number of windows and of spectral windows of the current routing. */
 int64_t slh_num_windows(const slh_ctx *ctx);
 int64_t slh_num_spectral(const slh_ctx *ctx);

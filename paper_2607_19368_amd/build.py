@@ -29,6 +29,7 @@ SOURCES = [
     "k_merge.hip",
     "k_route.hip",
     "k_peak.hip",
+    "slh_noalloc.hip",
 ]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

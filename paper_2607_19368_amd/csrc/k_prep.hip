@@ -42,7 +42,7 @@ __global__ __launch_bounds__(256) void k_rownorm(const void* __restrict__ Xv, in
     s_x = s_fm;
   } else {
     const float* x = (const float*)Xv + row * ldx;
-    uint16_t* xb = Xb + row * (int64_t)D;
+    uint16_t* xb = Xb ? Xb + row * (int64_t)D : nullptr;
     for (int c = lane * 4; c < D; c += 256) {
       float4 v = *(const float4*)(x + c);
       float f[4] = {v.x, v.y, v.z, v.w};
@@ -55,10 +55,12 @@ __global__ __launch_bounds__(256) void k_rownorm(const void* __restrict__ Xv, in
         s_fm = fma(a, a, s_fm);
         s_x = fma(g, g, s_x);
       }
-      uint2 packed;
-      packed.x = (uint32_t)hb[0] | ((uint32_t)hb[1] << 16);
-      packed.y = (uint32_t)hb[2] | ((uint32_t)hb[3] << 16);
-      *(uint2*)(xb + c) = packed;
+      if (Xb) {
+        uint2 packed;
+        packed.x = (uint32_t)hb[0] | ((uint32_t)hb[1] << 16);
+        packed.y = (uint32_t)hb[2] | ((uint32_t)hb[3] << 16);
+        *(uint2*)(xb + c) = packed;
+      }
     }
   }
   s_fm = wave_sum_f64(s_fm);

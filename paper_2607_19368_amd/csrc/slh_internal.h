@@ -9,7 +9,7 @@ namespace slh {
 // Row norms of X: nrm2_fm[i] = |bf16(x_i)|^2 and nrm_x[i] = |x_i| (X as given),
 // both accumulated in fp64, and rowscale[i] = fp32(s_i * sqrt(2/m)) with
 // s_i = exp(nrm2_fm[i] / (2 sqrt(D))) (or 1 for the Gaussian map).
-// For fp32 X it also writes the bf16 copy Xb (row stride D).
+// For fp32 X it also writes the bf16 copy Xb (row stride D) unless Xb is NULL.
 hipError_t launch_rownorm(const void* X, int dtype, int64_t ldx, int64_t N, int D, int m,
                           int gauss, double* nrm2_fm, double* nrm_x, double* inv_x,
                           float* rowscale, uint16_t* Xb, hipStream_t s);

@@ -21,13 +21,14 @@ SLH_OPT_TARGET_LEN = 10
 SLH_OUT_PHI, SLH_OUT_ALPHA, SLH_OUT_BETA, SLH_OUT_Z = 1, 2, 3, 4
 SLH_OUT_PROJ, SLH_OUT_CODES, SLH_OUT_THETA, SLH_OUT_Q, SLH_OUT_WINDOWS = 5, 6, 7, 8, 9
 SLH_OUT_ROWSUM = 10
+SLH_NOALLOC_BYTES = 17355008
 
 EXPORTS = [
     "slh_gen_params", "slh_gen_start", "slh_create", "slh_destroy", "slh_last_error",
     "slh_set_option", "slh_set_stream", "slh_route", "slh_feature_map", "slh_lanczos",
     "slh_simhash", "slh_merge", "slh_merge_capacity", "slh_copy_out", "slh_num_windows",
     "slh_num_spectral", "slh_load", "slh_stage_times", "slh_time_passes", "slh_spectral_energy",
-    "slh_bucket_purity", "slh_eigh_ritz", "slh_peak_read", "slh_peak_mfma",
+    "slh_bucket_purity", "slh_eigh_ritz", "slh_peak_read", "slh_peak_mfma", "slh_merge_noalloc",
 ]
 
 _lib = None
@@ -60,6 +61,7 @@ def load():
         "slh_eigh_ritz": (i32, [vp, i32, vp, vp]),
         "slh_peak_read": (i32, [vp, i64, i32, vp, vp]),
         "slh_peak_mfma": (i32, [i32, vp, vp, vp]),
+        "slh_merge_noalloc": (i32, [vp, i32, i64, i64, i64, vp, i32, vp, vp, vp, i64, vp, vp]),
         "slh_simhash": (i32, [vp, vp]),
         "slh_merge": (i32, [vp, vp, i32, i64, vp, vp, vp, i64, vp]),
         "slh_merge_capacity": (i64, [vp]),
@@ -360,3 +362,23 @@ def slh_peak_mfma(reps=10, stream=None):
     if rc != SLH_OK:
         raise SLHError(f"slh_peak_mfma failed ({rc})")
     return float(out[0])
+
+
+def slh_merge_noalloc(X, codes, bits, emb_out, pos_out, tok2macro_out=None, stream=None):
+    """The allocation-free merge of one window from given codes (device tensors
+    throughout; outputs allocated by the caller).  Returns (E [M, D], P [M],
+    tok2macro, M) as views of the given outputs."""
+    import torch
+    p, dt, ld = _xinfo(X)
+    st = torch.cuda.current_stream() if stream is None else stream
+    M = ctypes.c_int64(0)
+    rc = load().slh_merge_noalloc(p, dt, ld, X.shape[0], X.shape[1], ctypes.c_void_p(codes.data_ptr()),
+                                  int(bits), ctypes.c_void_p(emb_out.data_ptr()),
+                                  ctypes.c_void_p(pos_out.data_ptr()),
+                                  ctypes.c_void_p(tok2macro_out.data_ptr()) if tok2macro_out is not None
+                                  else None, emb_out.shape[0], ctypes.byref(M),
+                                  ctypes.c_void_p(st.cuda_stream))
+    if rc != SLH_OK:
+        raise SLHError(f"slh_merge_noalloc failed ({rc})")
+    m = int(M.value)
+    return emb_out[:m], pos_out[:m], tok2macro_out, m
