@@ -110,10 +110,14 @@ __global__ __launch_bounds__(EIG_T) void k_eig_values(const double* __restrict__
   const double pad = 2.0 * DBL_EPSILON * fmax(ti.tnorm, DBL_MIN) + 2.0 * pivmin;
   double lo = ti.lo - pad, hi = ti.hi + pad;
   // multisection: count(lo) <= kidx < count(hi); EIG_T probes per round,
-  // probe p at lo + (hi - lo) (p + 1) / (EIG_T + 1), evaluated by thread p
+  // probe p at lo + (hi - lo) (p + 1) / (EIG_T + 1), evaluated by thread p.
+  // The bracket is narrowed to 2 eps max(|theta|, |T|): the Sturm count is
+  // exact only for a matrix within about eps |T| of T, so narrower brackets of
+  // small eigenvalues would not make them more accurate.
+  const double wstop = 2.0 * DBL_EPSILON * ti.tnorm + pivmin;
   for (int it = 0; it < 64; ++it) {
     const double wdt = hi - lo;
-    if (wdt <= 2.0 * DBL_EPSILON * fmax(fabs(lo), fabs(hi)) + pivmin) break;
+    if (wdt <= fmax(2.0 * DBL_EPSILON * fmax(fabs(lo), fabs(hi)) + pivmin, wstop)) break;
     const double step = wdt / (double)(EIG_T + 1);
     const double x = lo + step * (double)(tid + 1);
     const unsigned long long m = __ballot(sturm_count(al, b2, n, x, pivmin) > kidx);
@@ -263,10 +267,11 @@ __global__ __launch_bounds__(EIG_T) void k_eig_orth(const double* __restrict__ a
   const int n = neff[a];
   const int c_lo = r - min(r, n);
   double* Sa = Seig + (int64_t)a * n_it * r;
-  const double* tha = theta + (int64_t)a * r;
   __shared__ double al[EIG_NMAX], b1[EIG_NMAX], b2[EIG_NMAX];
-  __shared__ double y[EIG_NMAX];
+  __shared__ double y[EIG_NMAX], tha[EIG_NMAX];
   __shared__ double red[EIG_T / 64];
+  // the kept eigenvalues in LDS (the cluster scan below is sequential)
+  for (int c = threadIdx.x; c < r; c += EIG_T) tha[c] = theta[(int64_t)a * r + c];
   const TriInfo ti = load_tridiag(alpha + (int64_t)a * n_it, beta + (int64_t)a * n_it, n, al, b1, b2);
   const double ctol = EIG_CLUSTER * ti.tnorm;
   for (int c = c_lo; c < r;) {

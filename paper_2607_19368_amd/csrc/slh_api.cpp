@@ -334,6 +334,23 @@ int64_t capacity(const slh_ctx* c) {
   return cap + c->keep_last;
 }
 
+// The captured body of slh_lanczos (graph mode): the step sequence, Eigh(T)
+// and the Ritz coordinates, in one stream (a forked branch for the last beta,
+// which T does not use, made the replay about 0.1 ms slower: the branches are
+// synchronised across queues).  Returns the first launch error (the capture
+// is ended by the caller in every case).
+hipError_t launch_lanczos_graph_body(slh_ctx* c, const LanczosWS& w, const double* q1act, int na,
+                                 int n_it, int L) {
+  hipError_t e = launch_lanczos(w, q1act, c->cap_stream);
+  if (e == hipSuccess)
+    e = launch_tridiag_eig(w.alpha, w.beta, w.neff, na, n_it, c->r, P<double>(c->theta),
+                           P<double>(c->Seig), c->cap_stream);
+  if (e == hipSuccess)
+    e = launch_ritz(w.Q, P<double>(c->Seig), w.neff, na, L, w.ldq, n_it, c->r, P<double>(c->Z),
+                    c->cap_stream);
+  return e;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -456,6 +473,7 @@ void slh_destroy(slh_ctx* c) {
   for (DevBuf* b : bufs)
     if (b->p) (void)hipFree(b->p);
   if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
+
   if (c->ev_made)
     for (auto& e : c->ev) (void)hipEventDestroy(e);
   for (auto& e : c->ev_fb) (void)hipEventDestroy(e);
@@ -770,15 +788,24 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
         if (rc_ev) return rc_ev;
         HIP_TRY(c, hipEventRecord(c->ev[2], c->stream));
         HIP_TRY(c, launch_lanczos(w, q1act, c->stream, c->ev_fb.data(), c->ev_fa.data()));
+        HIP_TRY(c, hipEventRecord(c->ev[3], c->stream));
+        HIP_TRY(c, launch_tridiag_eig(w.alpha, w.beta, w.neff, na, n_it, c->r, P<double>(c->theta),
+                                      P<double>(c->Seig), c->stream));
+        HIP_TRY(c, launch_ritz(w.Q, P<double>(c->Seig), w.neff, na, (int)L, w.ldq, n_it, c->r,
+                               P<double>(c->Z), c->stream));
+        HIP_TRY(c, hipEventRecord(c->ev[4], c->stream));
       } else {
-        // the step sequence is captured once per configuration and replayed as a graph
+        // The step sequence, Eigh(T) and the Ritz coordinates are captured once
+        // per configuration and replayed as one graph.
         std::string key((const char*)&w, sizeof w);
         key.append((const char*)&q1act, sizeof q1act);
+        const void* outs[3] = {c->theta.p, c->Seig.p, c->Z.p};   // the eigensolve's outputs
+        key.append((const char*)outs, sizeof outs);
         if (!c->lz_exec || c->lz_key != key) {
           drop_graph(c);
           hipGraph_t g = nullptr;
           HIP_TRY(c, hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal));
-          hipError_t le = launch_lanczos(w, q1act, c->cap_stream);
+          hipError_t le = launch_lanczos_graph_body(c, w, q1act, na, n_it, (int)L);
           hipError_t ee = hipStreamEndCapture(c->cap_stream, &g);
           if (le != hipSuccess || ee != hipSuccess) {
             if (g) (void)hipGraphDestroy(g);
@@ -795,15 +822,9 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
         }
         HIP_TRY(c, hipGraphLaunch(c->lz_exec, c->stream));
       }
-      if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[3], c->stream));
       c->fused_timed = c->timing ? n_it : 0;
       c->lz_w = w;
       c->lz_w_valid = true;
-      HIP_TRY(c, launch_tridiag_eig(w.alpha, w.beta, w.neff, na, n_it, c->r, P<double>(c->theta),
-                                    P<double>(c->Seig), c->stream));
-      HIP_TRY(c, launch_ritz(w.Q, P<double>(c->Seig), w.neff, na, (int)L, w.ldq, n_it, c->r,
-                             P<double>(c->Z), c->stream));
-      if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[4], c->stream));
     }
   }
   if ((ritz_out || iters_out) && na > 0) {
