@@ -18,7 +18,11 @@
 //           renormalises runs that are whole buckets; runs cut by a chunk edge
 //           leave a partial sum.
 // combine   sums the partials of each cut bucket in chunk order and renormalises.
-// All orders are fixed, so results are bitwise reproducible.
+// All orders are fixed, so results are bitwise reproducible.  Every kernel
+// that passes data between its own passes through global memory is one
+// workgroup per window, so a workgroup-scope fence and a barrier order those
+// passes (a device-scope fence writes back and invalidates the L2 each time);
+// only the re-ranking kernel, whose histogram uses global atomics, keeps one.
 #include "slh_device.h"
 #include "slh_internal.h"
 
@@ -126,7 +130,7 @@ __global__ __launch_bounds__(1024) void k_mg_book(MergeWS w) {
       __threadfence_block();
       __syncthreads();
     }
-    __threadfence();
+    __threadfence_block();
     __syncthreads();
   }
   const uint32_t* K = kb[(npass - 1) & 1];
@@ -135,7 +139,7 @@ __global__ __launch_bounds__(1024) void k_mg_book(MergeWS w) {
   int* segid = w.segid + base;    // sorted order: bucket ordinal (by code)
   int* segk = w.segk + base;      // bucket ordinal -> macro rank
   for (int s = tid; s < L; s += 1024) flag[s] = 0;
-  __threadfence();
+  __threadfence_block();
   __syncthreads();
   // bucket ordinals and representatives
   int carry = 0;
@@ -153,7 +157,7 @@ __global__ __launch_bounds__(1024) void k_mg_book(MergeWS w) {
     __syncthreads();
   }
   const int nseg = carry;
-  __threadfence();
+  __threadfence_block();
   __syncthreads();
   // macro rank of each representative = number of representatives before it
   carry = 0;
@@ -166,11 +170,11 @@ __global__ __launch_bounds__(1024) void k_mg_book(MergeWS w) {
     carry += tot;
     __syncthreads();
   }
-  __threadfence();
+  __threadfence_block();
   __syncthreads();
   for (int s = tid; s < L; s += 1024)
     if (s == L - 1 || K[s + 1] != K[s]) segk[segid[s]] = flag[V[s] - base];
-  __threadfence();
+  __threadfence_block();
   __syncthreads();
   for (int s = tid; s < L; s += 1024) {
     w.sval[base + s] = V[s];
@@ -471,7 +475,7 @@ __global__ __launch_bounds__(1024) void k_mg_rerank(MergeWS w, int scheme, int* 
     tp[base + t] = -1;
     cnt[base + t] = 0;
   }
-  __threadfence();
+  __threadfence_block();
   __syncthreads();
   // representative positions at run ends; histogram of them
   for (int e = tid; e < L; e += 1024) {
@@ -499,7 +503,7 @@ __global__ __launch_bounds__(1024) void k_mg_rerank(MergeWS w, int scheme, int* 
     c2 += tot;
     __syncthreads();
   }
-  __threadfence();
+  __threadfence_block();
   __syncthreads();
   // rank = buckets with a smaller position + tied buckets with a smaller max
   for (int e = tid; e < L; e += 1024) {
@@ -512,7 +516,7 @@ __global__ __launch_bounds__(1024) void k_mg_rerank(MergeWS w, int scheme, int* 
       rk[base + st[base + e]] = r;
     }
   }
-  __threadfence();
+  __threadfence_block();
   __syncthreads();
   for (int s = tid; s < L; s += 1024) w.sloc[base + s] = rk[base + st[base + s]];
 }
@@ -559,7 +563,7 @@ __global__ __launch_bounds__(1024) void k_mg_target(MergeWS w, int* __restrict__
     carry = max(carry, tot);
     __syncthreads();
   }
-  __threadfence();
+  __threadfence_block();
   __syncthreads();
   for (int e = tid; e < L; e += 1024)
     if (e == L - 1 || w.sloc[base + e + 1] != w.sloc[base + e]) {
@@ -567,7 +571,7 @@ __global__ __launch_bounds__(1024) void k_mg_target(MergeWS w, int* __restrict__
       rsz[base + k] = e - st[base + e] + 1;
       rof[base + k] = st[base + e];
     }
-  __threadfence();
+  __threadfence_block();
   __syncthreads();
   if (M > T) {
     // exclusive prefix of the run sizes over ranks: new sorted position of each
@@ -582,7 +586,7 @@ __global__ __launch_bounds__(1024) void k_mg_target(MergeWS w, int* __restrict__
       c2 += tot;
       __syncthreads();
     }
-    __threadfence();
+    __threadfence_block();
     __syncthreads();
     for (int s = tid; s < L; s += 1024) {
       const int k = w.sloc[base + s];
@@ -590,7 +594,7 @@ __global__ __launch_bounds__(1024) void k_mg_target(MergeWS w, int* __restrict__
       t1[base + dest] = w.sval[base + s];
       fl[base + dest] = (int)((long long)k * T / M);
     }
-    __threadfence();
+    __threadfence_block();
     __syncthreads();
     for (int s = tid; s < L; s += 1024) {
       w.sval[base + s] = t1[base + s];
@@ -609,7 +613,7 @@ __global__ __launch_bounds__(1024) void k_mg_target(MergeWS w, int* __restrict__
     int tot;
     (void)block_incl_scan_1024(part, wsum, tot);
     if (tid == 0) sR = E - tot;
-    __threadfence();
+    __threadfence_block();
     __syncthreads();
     const int R = sR;
     // pieces per bucket: one more for the R largest remainders (ties: smaller k)
@@ -625,7 +629,7 @@ __global__ __launch_bounds__(1024) void k_mg_target(MergeWS w, int* __restrict__
       t1[base + k] = min(rsz[base + k], 1 + t0[base + k] + ((R > 0 && ahead < R) ? 1 : 0));
     }
     for (int t = tid; t < L; t += 1024) fl[base + t] = 0;
-    __threadfence();
+    __threadfence_block();
     __syncthreads();
     // flag each piece's last member (by token)
     for (int s = tid; s < L; s += 1024) {
@@ -636,7 +640,7 @@ __global__ __launch_bounds__(1024) void k_mg_target(MergeWS w, int* __restrict__
       const int last = (j < rr) ? (j + 1) * (q + 1) - 1 : rr * (q + 1) + (j - rr + 1) * q - 1;
       if (o == last) fl[w.sval[base + s]] = 1;
     }
-    __threadfence();
+    __threadfence_block();
     __syncthreads();
     // rank of each piece = pieces whose last member precedes its own
     int c3 = 0;
@@ -649,7 +653,7 @@ __global__ __launch_bounds__(1024) void k_mg_target(MergeWS w, int* __restrict__
       c3 += tt;
       __syncthreads();
     }
-    __threadfence();
+    __threadfence_block();
     __syncthreads();
     for (int s = tid; s < L; s += 1024) {
       const int k = w.sloc[base + s];
@@ -660,7 +664,7 @@ __global__ __launch_bounds__(1024) void k_mg_target(MergeWS w, int* __restrict__
       const int ltok = w.sval[base + rof[base + k] + last];
       fl[base + s] = t0[ltok];
     }
-    __threadfence();
+    __threadfence_block();
     __syncthreads();
     for (int s = tid; s < L; s += 1024) w.sloc[base + s] = fl[base + s];
   }
