@@ -93,6 +93,11 @@ struct slh_ctx {
   double tol = 1e-10;
   hipStream_t stream = nullptr;
   hipStream_t cap_stream = nullptr;
+  // results the host waits for (M, routing scores) arrive in pinned memory and
+  // the host spins on an event rather than sleeping in a stream synchronisation
+  void* pin = nullptr;
+  size_t pin_bytes = 0;
+  hipEvent_t ev_host = nullptr;
   int device = 0, n_cu = 256;
   std::string err;
 
@@ -191,6 +196,33 @@ int ensure(slh_ctx* c, DevBuf& b, size_t bytes) {
     return fail(c, SLH_ENOMEM, "hipMalloc(%zu): %s", bytes, hipGetErrorString(e));
   }
   b.bytes = bytes;
+  return SLH_OK;
+}
+
+// pinned host buffer of at least `bytes`
+int ensure_pinned(slh_ctx* c, size_t bytes) {
+  if (c->pin_bytes >= bytes) return SLH_OK;
+  if (c->pin) (void)hipHostFree(c->pin);
+  c->pin = nullptr;
+  c->pin_bytes = 0;
+  const size_t b = std::max<size_t>(bytes, 256);
+  const hipError_t e = hipHostMalloc(&c->pin, b, hipHostMallocDefault);
+  if (e != hipSuccess) {
+    c->pin = nullptr;
+    return fail(c, SLH_ENOMEM, "hipHostMalloc(%zu): %s", b, hipGetErrorString(e));
+  }
+  c->pin_bytes = b;
+  return SLH_OK;
+}
+
+// Wait for the work enqueued so far on the context stream by spinning on an
+// event (a woken-up stream synchronisation costs tens of microseconds).
+int wait_stream(slh_ctx* c) {
+  hipError_t e = hipEventRecord(c->ev_host, c->stream);
+  if (e != hipSuccess) return fail(c, SLH_EHIP, "hipEventRecord: %s", hipGetErrorString(e));
+  while ((e = hipEventQuery(c->ev_host)) == hipErrorNotReady) {
+  }
+  if (e != hipSuccess) return fail(c, SLH_EHIP, "hipEventQuery: %s", hipGetErrorString(e));
   return SLH_OK;
 }
 
@@ -451,7 +483,8 @@ int slh_create(slh_ctx** out, int64_t N, int64_t D, int64_t m, int32_t r, int32_
     slh_destroy(c);
     return SLH_EHIP;
   }
-  if (hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking) != hipSuccess) {
+  if (hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking) != hipSuccess ||
+      hipEventCreateWithFlags(&c->ev_host, hipEventDisableTiming) != hipSuccess) {
     slh_destroy(c);
     return SLH_EHIP;
   }
@@ -473,6 +506,8 @@ void slh_destroy(slh_ctx* c) {
   for (DevBuf* b : bufs)
     if (b->p) (void)hipFree(b->p);
   if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
+  if (c->ev_host) (void)hipEventDestroy(c->ev_host);
+  if (c->pin) (void)hipHostFree(c->pin);
 
   if (c->ev_made)
     for (auto& e : c->ev) (void)hipEventDestroy(e);
@@ -608,9 +643,11 @@ int slh_route(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, double rho,
                                    P<double>(c->scores), c->stream));
   }
   std::vector<double> sc((size_t)c->n_win);
-  HIP_TRY(c, hipMemcpyAsync(sc.data(), c->scores.p, sc.size() * sizeof(double),
+  if ((rc = ensure_pinned(c, sc.size() * sizeof(double)))) return rc;
+  HIP_TRY(c, hipMemcpyAsync(c->pin, c->scores.p, sc.size() * sizeof(double),
                             hipMemcpyDeviceToHost, c->stream));
-  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  if ((rc = wait_stream(c))) return rc;
+  std::memcpy(sc.data(), c->pin, sc.size() * sizeof(double));
   // tau(rho): 0.70 at rho <= 2, linear in log2(rho) through 0.60 at 8 and 0.55 at 16
   double t = tau;
   if (!(tau >= 0.0)) {
@@ -993,9 +1030,10 @@ int slh_merge(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, float* emb_
                                P<int>(c->Mtot), c->compact, emb_out, pos_out, tok2macro_out,
                                c->stream));
   if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[8], c->stream));
-  int M = 0;
-  HIP_TRY(c, hipMemcpyAsync(&M, c->Mtot.p, 4, hipMemcpyDeviceToHost, c->stream));
-  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  if ((rc = ensure_pinned(c, 4))) return rc;
+  HIP_TRY(c, hipMemcpyAsync(c->pin, c->Mtot.p, 4, hipMemcpyDeviceToHost, c->stream));
+  if ((rc = wait_stream(c))) return rc;
+  const int M = *(const int*)c->pin;
   *M_out = M + c->keep_last;
   c->merged = 1;
   forget_norms(c);                  // the next prompt may reuse this buffer
