@@ -364,15 +364,21 @@ def test_adaptive_literal_threshold_routes_all_to_chunk():
     PR.compare(o, g, 256)
 
 
-@pytest.mark.parametrize("case", ["bf16_fused", "f32_fused", "bf16_wide"])
+@pytest.mark.parametrize("case", ["bf16_fused", "f32_fused", "bf16_wide", "bf16_partial", "bf16_odd"])
 def test_router_scores_both_paths(case):
     """Eq. 8 scores and routes against the oracle on both implementations: the
-    fused row-norm + score kernel (D <= 4096, bf16 and fp32 X) and the separate
-    row-norm and score kernels (D > 4096); scores within 1e-9, routes equal, and
-    the compressed output compared as everywhere else."""
-    D = {"bf16_fused": 512, "f32_fused": 512, "bf16_wide": 4104}[case]
+    fused row-norm + score kernels (D <= 4096; bf16 X streamed through LDS, fp32
+    X through registers) and the separate row-norm and score kernels (D > 4096);
+    scores within 1e-9, routes equal, and the compressed output compared as
+    everywhere else.  bf16_partial: rows narrower than the workgroup's columns
+    (D = 3584 of 4096) and windows of 300 rows (a 256-row group and a 44-row
+    one); bf16_odd: D = 1032 of 2048 and windows of 131 rows (a last batch of
+    one row)."""
+    D = {"bf16_fused": 512, "f32_fused": 512, "bf16_wide": 4104, "bf16_partial": 3584,
+         "bf16_odd": 1032}[case]
     x = "f32" if case == "f32_fused" else "bf16"
-    L, nw = 128, 6
+    L = {"bf16_partial": 300, "bf16_odd": 131}.get(case, 128)
+    nw = 6
     inp = _custom(f"rt_{case}", nw * L, D, 256, 16, 8, 6, x=x)
     Xs = [inp.x_float(slice(w * L, (w + 1) * L)) for w in range(nw)]
     so = np.array([O.redundancy_score(xw) for xw in Xs])
