@@ -31,57 +31,49 @@
 
 namespace slh {
 
-// Sum 8 values over the 64 lanes of a wave with 10 shuffles.  On return lane l
-// holds the full sum of value index ((l>>5)&1)*4 + ((l>>4)&1)*2 + ((l>>3)&1).
+// Sum 8 values over the 64 lanes of a wave without LDS round trips: four
+// 32-lane trades (v_permlane32_swap), two 16-lane trades (v_permlane16_swap),
+// an 8-lane exchange (DPP row_ror:8), then a sum over each 8-lane group.  On
+// return lane l holds the full sum of value index ((l>>5)&1)*4 + ((l>>4)&1)*2 +
+// ((l>>3)&1).  Every lane of the wave must be active.
 __device__ __forceinline__ double wave_sum8_f64(const double (&v)[8]) {
   const int lane = threadIdx.x & 63;
   double w[4];
-  const bool b32 = lane & 32;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    double keep = b32 ? v[e + 4] : v[e];
-    double send = b32 ? v[e] : v[e + 4];
-    w[e] = keep + __shfl_xor(send, 32, 64);
-  }
+  for (int e = 0; e < 4; ++e) w[e] = swap32_add(v[e], v[e + 4]);
   double x[2];
-  const bool b16 = lane & 16;
 #pragma unroll
-  for (int e = 0; e < 2; ++e) {
-    double keep = b16 ? w[e + 2] : w[e];
-    double send = b16 ? w[e] : w[e + 2];
-    x[e] = keep + __shfl_xor(send, 16, 64);
-  }
+  for (int e = 0; e < 2; ++e) x[e] = swap16_add(w[e], w[e + 2]);
   const bool b8 = lane & 8;
-  double y = (b8 ? x[1] : x[0]) + __shfl_xor(b8 ? x[0] : x[1], 8, 64);
-  y += __shfl_xor(y, 4, 64);
-  y += __shfl_xor(y, 2, 64);
-  y += __shfl_xor(y, 1, 64);
-  return y;
+  const double y = (b8 ? x[1] : x[0]) + dpp_f64<DPP_ROR8>(b8 ? x[0] : x[1]);
+  return oct_sum_f64(y);
 }
 
-// The same over each 16-lane quarter: lane l holds the quarter sum of value
-// index ((l>>3)&1)*4 + ((l>>2)&1)*2 + ((l>>1)&1).
+// The same over each 16-lane quarter (DPP only): lane l holds the quarter sum
+// of value index ((l>>3)&1)*4 + ((l>>2)&1)*2 + ((l>>1)&1).  The 4-lane step
+// pairs lane i with 7 - i of its 8-lane group (row_half_mirror), which, like
+// i ^ 4, joins the two halves of the group.
 __device__ __forceinline__ double quarter_sum8_f64(const double (&v)[8]) {
   const int lane = threadIdx.x & 63;
   double w[4];
   const bool b8 = lane & 8;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    double keep = b8 ? v[e + 4] : v[e];
-    double send = b8 ? v[e] : v[e + 4];
-    w[e] = keep + __shfl_xor(send, 8, 64);
+    const double keep = b8 ? v[e + 4] : v[e];
+    const double send = b8 ? v[e] : v[e + 4];
+    w[e] = keep + dpp_f64<DPP_ROR8>(send);
   }
   double x[2];
   const bool b4 = lane & 4;
 #pragma unroll
   for (int e = 0; e < 2; ++e) {
-    double keep = b4 ? w[e + 2] : w[e];
-    double send = b4 ? w[e] : w[e + 2];
-    x[e] = keep + __shfl_xor(send, 4, 64);
+    const double keep = b4 ? w[e + 2] : w[e];
+    const double send = b4 ? w[e] : w[e + 2];
+    x[e] = keep + dpp_f64<DPP_HALF_MIRROR>(send);
   }
   const bool b2 = lane & 2;
-  double y = (b2 ? x[1] : x[0]) + __shfl_xor(b2 ? x[0] : x[1], 2, 64);
-  y += __shfl_xor(y, 1, 64);
+  double y = (b2 ? x[1] : x[0]) + dpp_f64<DPP_XOR2>(b2 ? x[0] : x[1]);
+  y += dpp_f64<DPP_XOR1>(y);
   return y;
 }
 

@@ -313,68 +313,33 @@ __device__ __forceinline__ void rs_read(const uint16_t* p, rs_u32x4 (&w)[LPB]) {
                  : "v"(a), "i"(STRIDE), "i"(2 * STRIDE), "i"(3 * STRIDE) : "memory");
 }
 
-__device__ __forceinline__ uint32_t rs_lo(double v) {
-  return (uint32_t)(uint64_t)__double_as_longlong(v);
-}
-__device__ __forceinline__ uint32_t rs_hi(double v) {
-  return (uint32_t)((uint64_t)__double_as_longlong(v) >> 32);
-}
-__device__ __forceinline__ double rs_dbl(uint32_t lo, uint32_t hi) {
-  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
-}
-
-template <int CTRL>
-__device__ __forceinline__ double rs_dpp(double v) {
-  const int lo = __builtin_amdgcn_update_dpp(0, (int)rs_lo(v), CTRL, 0xF, 0xF, false);
-  const int hi = __builtin_amdgcn_update_dpp(0, (int)rs_hi(v), CTRL, 0xF, 0xF, false);
-  return rs_dbl((uint32_t)lo, (uint32_t)hi);
+// Wave sums of a and b in a fixed order, both returned in every lane: one
+// 32-lane trade leaves a's pair sums in lanes 0-31 and b's in 32-63; sums over
+// each row of 16 lanes (lane i with i ^ 1, i ^ 2, 7 - i, 15 - i: every lane of
+// the row ends with the same bits), read out of lanes 0 and 16 (a) and 32 and
+// 48 (b).
+__device__ __forceinline__ double rs_row_sum(double v) {
+  v += dpp_f64<DPP_XOR1>(v);
+  v += dpp_f64<DPP_XOR2>(v);
+  v += dpp_f64<DPP_HALF_MIRROR>(v);
+  v += dpp_f64<DPP_MIRROR>(v);
+  return v;
 }
 
-__device__ __forceinline__ double rs_lane(double v, int l) {
-  return rs_dbl((uint32_t)__builtin_amdgcn_readlane((int)rs_lo(v), l),
-                (uint32_t)__builtin_amdgcn_readlane((int)rs_hi(v), l));
-}
-
-// Wave sums of a and b in a fixed order, both returned in every lane.  Lanes
-// 32-63 of a trade places with lanes 0-31 of b, so that one addition leaves
-// a_l + a_(l+32) in lanes l < 32 and b_(l-32) + b_l in the others; four DPP
-// exchanges within each row of 16 lanes (i ^ 1, i ^ 2, 7 - i, 15 - i; every
-// lane of a row ends with the same bits, as each step adds the same two
-// values) give the row sums, read out of lanes 0 and 16 (a) and 32 and 48 (b).
 __device__ __forceinline__ void rs_pair_sum(double a, double b, double& sa, double& sb) {
-  const auto lo = __builtin_amdgcn_permlane32_swap(rs_lo(a), rs_lo(b), false, false);
-  const auto hi = __builtin_amdgcn_permlane32_swap(rs_hi(a), rs_hi(b), false, false);
-  double v = rs_dbl(lo[0], hi[0]) + rs_dbl(lo[1], hi[1]);
-  v += rs_dpp<0xB1>(v);                          // quad_perm [1, 0, 3, 2]
-  v += rs_dpp<0x4E>(v);                          // quad_perm [2, 3, 0, 1]
-  v += rs_dpp<0x141>(v);                         // row_half_mirror
-  v += rs_dpp<0x140>(v);                         // row_mirror
-  sa = rs_lane(v, 0) + rs_lane(v, 16);
-  sb = rs_lane(v, 32) + rs_lane(v, 48);
+  const double v = rs_row_sum(swap32_add(a, b));
+  sa = readlane_f64(v, 0) + readlane_f64(v, 16);
+  sb = readlane_f64(v, 32) + readlane_f64(v, 48);
 }
 
 // The same for four values, returned in a, b, c, d: after the 32-lane trades of
-// (a, b) and (c, d), lanes 16-31 and 48-63 of the first sum trade places with
-// lanes 0-15 and 32-47 of the second (v_permlane16_swap), so that one more
-// addition leaves a, c, b, d in rows 0, 1, 2, 3 of the wave.
+// (a, b) and (c, d), a 16-lane trade leaves a, c, b, d in rows 0, 1, 2, 3.
 __device__ __forceinline__ void rs_quad_sum(double& a, double& b, double& c, double& d) {
-  const auto l1 = __builtin_amdgcn_permlane32_swap(rs_lo(a), rs_lo(b), false, false);
-  const auto h1 = __builtin_amdgcn_permlane32_swap(rs_hi(a), rs_hi(b), false, false);
-  const auto l2 = __builtin_amdgcn_permlane32_swap(rs_lo(c), rs_lo(d), false, false);
-  const auto h2 = __builtin_amdgcn_permlane32_swap(rs_hi(c), rs_hi(d), false, false);
-  const double ab = rs_dbl(l1[0], h1[0]) + rs_dbl(l1[1], h1[1]);
-  const double cd = rs_dbl(l2[0], h2[0]) + rs_dbl(l2[1], h2[1]);
-  const auto l3 = __builtin_amdgcn_permlane16_swap(rs_lo(ab), rs_lo(cd), false, false);
-  const auto h3 = __builtin_amdgcn_permlane16_swap(rs_hi(ab), rs_hi(cd), false, false);
-  double v = rs_dbl(l3[0], h3[0]) + rs_dbl(l3[1], h3[1]);
-  v += rs_dpp<0xB1>(v);
-  v += rs_dpp<0x4E>(v);
-  v += rs_dpp<0x141>(v);
-  v += rs_dpp<0x140>(v);
-  a = rs_lane(v, 0);
-  c = rs_lane(v, 16);
-  b = rs_lane(v, 32);
-  d = rs_lane(v, 48);
+  const double v = rs_row_sum(swap16_add(swap32_add(a, b), swap32_add(c, d)));
+  a = readlane_f64(v, 0);
+  c = readlane_f64(v, 16);
+  b = readlane_f64(v, 32);
+  d = readlane_f64(v, 48);
 }
 
 template <int NW, int CPT, int R, int NS, bool FULL>
@@ -484,7 +449,7 @@ __global__ __launch_bounds__(64 * NW) void k_route_norm_stream(
 #pragma unroll
     for (int e = 0; e < R; ++e) {
       if (R * j + e < nrow) {
-        const double inv = rs_lane(ih, 64 * e / R);
+        const double inv = readlane_f64(ih, 64 * e / R);
 #pragma unroll
         for (int c = 0; c < CPT; ++c)
 #pragma unroll

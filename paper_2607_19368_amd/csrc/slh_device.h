@@ -46,3 +46,63 @@ __device__ __forceinline__ double block_sum_f64(double v, double* red) {
   for (int w = 0; w < nw; ++w) s += red[w];
   return s;
 }
+
+// Lane exchanges of doubles without an LDS round trip (gfx950): DPP moves
+// within rows of 16 lanes, the 32- and 16-lane trades of v_permlane32_swap and
+// v_permlane16_swap, and lane reads into scalar registers.
+__device__ __forceinline__ uint32_t f64_lo(double v) {
+  return (uint32_t)(uint64_t)__double_as_longlong(v);
+}
+__device__ __forceinline__ uint32_t f64_hi(double v) {
+  return (uint32_t)((uint64_t)__double_as_longlong(v) >> 32);
+}
+__device__ __forceinline__ double f64_of(uint32_t lo, uint32_t hi) {
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// DPP controls used here: quad_perm [1, 0, 3, 2] (lane ^ 1), quad_perm
+// [2, 3, 0, 1] (lane ^ 2), row_half_mirror (7 - i within 8 lanes), row_mirror
+// (15 - i within 16), row_ror:8 (lane ^ 8 within 16).
+constexpr int DPP_XOR1 = 0xB1, DPP_XOR2 = 0x4E, DPP_HALF_MIRROR = 0x141, DPP_MIRROR = 0x140,
+              DPP_ROR8 = 0x128;
+
+// The value of lane dpp(l) in lane l (every lane active).
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)f64_lo(v), CTRL, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)f64_hi(v), CTRL, 0xF, 0xF, false);
+  return f64_of((uint32_t)lo, (uint32_t)hi);
+}
+
+// The value of lane l (wave-uniform).
+__device__ __forceinline__ double readlane_f64(double v, int l) {
+  return f64_of((uint32_t)__builtin_amdgcn_readlane((int)f64_lo(v), l),
+                (uint32_t)__builtin_amdgcn_readlane((int)f64_hi(v), l));
+}
+
+// a + b after lanes 32-63 of a trade places with lanes 0-31 of b: lane l < 32
+// gets a_l + a_(l+32), lane l >= 32 gets b_(l-32) + b_l.
+__device__ __forceinline__ double swap32_add(double a, double b) {
+  const auto lo = __builtin_amdgcn_permlane32_swap(f64_lo(a), f64_lo(b), false, false);
+  const auto hi = __builtin_amdgcn_permlane32_swap(f64_hi(a), f64_hi(b), false, false);
+  return f64_of(lo[0], hi[0]) + f64_of(lo[1], hi[1]);
+}
+
+// The same one level down: lanes 16-31 and 48-63 of a trade places with lanes
+// 0-15 and 32-47 of b; lane l gets a_l + a_(l+16) where bit 4 of l is 0 and
+// b_(l-16) + b_l where it is 1.
+__device__ __forceinline__ double swap16_add(double a, double b) {
+  const auto lo = __builtin_amdgcn_permlane16_swap(f64_lo(a), f64_lo(b), false, false);
+  const auto hi = __builtin_amdgcn_permlane16_swap(f64_hi(a), f64_hi(b), false, false);
+  return f64_of(lo[0], hi[0]) + f64_of(lo[1], hi[1]);
+}
+
+// Sum over each group of 8 lanes (lanes 8 k ... 8 k + 7), the same bits in all
+// 8: lane i with 7 - i, then i ^ 2, then i ^ 1 (each step adds the same two
+// values in both lanes of a pair).
+__device__ __forceinline__ double oct_sum_f64(double v) {
+  v += dpp_f64<DPP_HALF_MIRROR>(v);
+  v += dpp_f64<DPP_XOR2>(v);
+  v += dpp_f64<DPP_XOR1>(v);
+  return v;
+}

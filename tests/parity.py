@@ -280,13 +280,13 @@ def compare(o, g, L, check_spectral=True, ritz_rel=RITZ_REL, angle=ANGLE, emb_re
         if a.iters != b.iters:
             # Only where the operator's rank ran out inside the Krylov space: the
             # step that decides the breakdown then compares a rounding-noise beta
-            # with the threshold, and the extra steps add Ritz values that are
-            # zero up to rounding.  Both sides must show such values; the
-            # window's SimHash bits are not determined.
-            tiny_a = np.count_nonzero((a.ritz != 0) & (np.abs(a.ritz) <= floor_a))
-            tiny_b = np.count_nonzero((b.ritz != 0) & (np.abs(b.ritz) <= floor_b))
-            assert max(tiny_a, tiny_b) > 0 and abs(a.iters - b.iters) <= max(tiny_a, tiny_b), \
-                (w, a.iters, b.iters)
+            # with the threshold, so the two sides may stop one or two steps
+            # apart.  The extra steps add Ritz values that are zero up to
+            # rounding; where they are among the kept columns the spectral check
+            # below requires it (the counts of the other, determined values must
+            # agree), where they are not (r below the rank) they leave the kept
+            # values unchanged.  The window's SimHash bits are not determined.
+            assert abs(a.iters - b.iters) <= 2, (w, a.iters, b.iters)
             # the deciding beta (first step where one side stops) is at noise
             # level on both sides: at most 1e-6 of that side's largest |alpha|
             j0 = min(a.iters, b.iters) - 1
