@@ -16,21 +16,33 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   return (uint16_t)(u >> 16);
 }
 
-__device__ __forceinline__ double wave_sum_f64(double v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
+// Wave sums (every lane active; the same bits in every lane): the 32- and
+// 16-lane trades of v_permlane32_swap / v_permlane16_swap, then DPP within each
+// row of 16 lanes (lane ^ 8, 7 - i, lane ^ 2, lane ^ 1); each step adds the same
+// two values in both lanes of a pair.  No LDS round trips.
+__device__ __forceinline__ double wave_sum_f64(double v);
 
 __device__ __forceinline__ float wave_sum_f32(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  auto t32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(t32[0]) + __uint_as_float(t32[1]);
+  auto t16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(t16[0]) + __uint_as_float(t16[1]);
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xF, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
   return v;
 }
 
 __device__ __forceinline__ int wave_sum_i32(int v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  auto t32 = __builtin_amdgcn_permlane32_swap((uint32_t)v, (uint32_t)v, false, false);
+  v = (int)t32[0] + (int)t32[1];
+  auto t16 = __builtin_amdgcn_permlane16_swap((uint32_t)v, (uint32_t)v, false, false);
+  v = (int)t16[0] + (int)t16[1];
+  v += __builtin_amdgcn_update_dpp(0, v, 0x128, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
   return v;
 }
 
@@ -105,4 +117,11 @@ __device__ __forceinline__ double oct_sum_f64(double v) {
   v += dpp_f64<DPP_XOR2>(v);
   v += dpp_f64<DPP_XOR1>(v);
   return v;
+}
+
+__device__ __forceinline__ double wave_sum_f64(double v) {
+  v = swap32_add(v, v);
+  v = swap16_add(v, v);
+  v += dpp_f64<DPP_ROR8>(v);
+  return oct_sum_f64(v);
 }
