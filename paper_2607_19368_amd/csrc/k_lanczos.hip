@@ -116,8 +116,8 @@ __device__ __forceinline__ double colsum16(const double* __restrict__ src, int64
     const int cnt = (G - pl + 31) / 32;
     acc = sum_strided(src + (int64_t)pl * ld + col, (int64_t)32 * ld, cnt > 0 ? cnt : 0);
   }
-  acc += __shfl_xor(acc, 16, 64);
-  acc += __shfl_xor(acc, 32, 64);
+  acc = swap16_add(acc, acc);                   // + lane ^ 16
+  acc = swap32_add(acc, acc);                   // + lane ^ 32
   if ((tid & 63) < 16) red[tid >> 6][cl] = acc;
   __syncthreads();
   double t = 0.0;
@@ -465,10 +465,10 @@ __global__ __launch_bounds__(512, STAGED ? 2 : 4) void k_lz_step(LanczosWS w, in
         sub += rq[k0 + k][rl];
         sub_g += rg[k0 + k][rl];
       }
-      sub += __shfl_xor(sub, 16, 64);
-      sub_g += __shfl_xor(sub_g, 16, 64);
-      sub += __shfl_xor(sub, 32, 64);
-      sub_g += __shfl_xor(sub_g, 32, 64);
+      sub = swap16_add(sub, sub);
+      sub_g = swap16_add(sub_g, sub_g);
+      sub = swap32_add(sub, sub);
+      sub_g = swap32_add(sub_g, sub_g);
     }
   };
   // q_j of the thread's row (threads < RC; stored) and the remaining terms of u
@@ -588,10 +588,13 @@ __global__ __launch_bounds__(512, STAGED ? 2 : 4) void k_lz_step(LanczosWS w, in
   if (tid < 64) {
     // all of wave 0 takes part in every shuffle (a lane that skips one supplies
     // no value to it): lanes RC..2RC-1 take |z1|^2 of lanes 0..RC-1
-    const double zsh = __shfl(zz, tid & (RC - 1), 64);
-    double t = (tid < RC) ? qz : zsh;
-#pragma unroll
-    for (int o = RC / 2; o >= 1; o >>= 1) t += __shfl_xor(t, o, 64);
+    static_assert(RC == 16, "one row of 16 lanes");
+    // lanes 16-31 take zz of lanes 0-15 (a 16-lane trade of zz with itself)
+    const auto zl = __builtin_amdgcn_permlane16_swap(f64_lo(zz), f64_lo(zz), false, false);
+    const auto zh = __builtin_amdgcn_permlane16_swap(f64_hi(zz), f64_hi(zz), false, false);
+    double t = (tid < RC) ? qz : f64_of(zl[0], zh[0]);
+    t += dpp_f64<DPP_ROR8>(t);
+    t = oct_sum_f64(t);
     if (tid == 0) hp[j] = t;
     if (tid == RC) hp[w.ldq] = t;
   }
@@ -640,8 +643,9 @@ __global__ __launch_bounds__(512) void k_lz_reduce(LanczosWS w, int j) {
   // within a wave by butterflies, then the waves' column sums, one barrier for both
   const double zw = wave_sum_f64(z2acc);
   double sw = s;
-#pragma unroll
-  for (int o = CPB; o < 64; o <<= 1) sw += __shfl_xor(sw, o, 64);
+  static_assert(CPB >= 16, "partial lanes at distances 16 and 32 only");
+  if constexpr (CPB <= 16) sw = swap16_add(sw, sw);   // + lane ^ 16
+  if constexpr (CPB <= 32) sw = swap32_add(sw, sw);   // + lane ^ 32
   if ((tid & 63) == 0) red[tid >> 6] = zw;
   if (pl % WL == 0) rs[pl / WL][cl] = sw;
   __syncthreads();
@@ -655,8 +659,8 @@ __global__ __launch_bounds__(512) void k_lz_reduce(LanczosWS w, int j) {
     w.T[((int64_t)a * w.ldq + ((j + 1) & 1)) * m + c] = t;
     // |t|^2 partials per 16 columns
     double t2 = t * t;
-#pragma unroll
-    for (int o = 8; o >= 1; o >>= 1) t2 += __shfl_xor(t2, o, 64);
+    t2 += dpp_f64<DPP_ROR8>(t2);                    // within rows of 16 lanes, all active
+    t2 = oct_sum_f64(t2);
     if ((tid & 15) == 0) w.Apart[(int64_t)a * (m >> 4) + (c >> 4)] = t2;
   }
 }
