@@ -5,8 +5,11 @@
 // Sturm-count multisection (256 probe points per round, one per thread; the
 // count of negative pivots of T - x I is the number of eigenvalues below x)
 // until the bracket is a few ulps wide.
-// Eigenvectors: one workgroup per kept eigenvalue, inverse iteration with a
-// partially pivoted LU of T - theta I from a start vector of its own.  Two
+// Eigenvectors: one workgroup per kept eigenvalue.  Eigenvalues more than
+// EIG_TWIST_GAP |T| from their kept neighbours take the twisted factorisation
+// (twisted_vector: two pivot recurrences and two product recurrences, no
+// iteration); the others inverse iteration with a partially pivoted LU of
+// T - theta I from a start vector of its own.  Two
 // vectors computed this way for eigenvalues g apart are orthogonal only to
 // about 6e-18 |T| / g (measured on Wilkinson's W21+), and for (numerically)
 // repeated eigenvalues they are independent directions of the eigenspace
@@ -26,6 +29,7 @@ namespace slh {
 
 #define EIG_NMAX 256
 #define EIG_CLUSTER 1e-6
+#define EIG_TWIST_GAP 1e-9
 
 // 1/d from the hardware reciprocal refined by one Newton step (d a normal number)
 __device__ __forceinline__ double rcp_nr(double d) {
@@ -155,6 +159,121 @@ __device__ __forceinline__ void store_unit_column(const double* y, int n, int n_
   for (int i = lane; i < n_it; i += 64) Sa[(int64_t)i * r + k] = (i < n) ? y[i] * sc : 0.0;
 }
 
+// Eigenvector of an isolated eigenvalue th of the unreduced tridiagonal T by
+// the twisted factorisation (Parlett and Dhillon): the top-down pivots dp of
+// T - th I = L D L^T and the bottom-up pivots dm of U D U^T (the Sturm
+// recurrence run from either end; lanes 0 and 1 of wave 0 side by side, each
+// pivot below pivmin in magnitude replaced by -pivmin), the twist
+// gamma_k = dp_k + dm_k - (alpha_k - th), k the index of the smallest
+// |gamma_k| (the first of equals), and z with z_k = 1 solving N_k^T z = e_k:
+// z_i = -(beta_i / dp_i) z_(i+1) below k, z_i = -(beta_(i-1) / dm_i) z_(i-1)
+// above (lanes 0 and 1 again).  Then (T - th I) z = gamma_k e_k in exact
+// arithmetic.  Accepted (true, z in y) when every entry is finite and
+// |(T - th I) z|_inf <= 64 eps |T| |z|_inf, the level inverse iteration
+// reaches; every thread of the block must call it (it contains barriers).
+// dp, dm, ratios and the scan scratch use the caller's LDS arrays.
+__device__ __forceinline__ bool twisted_vector(const double* al, const double* b1, const double* b2,
+                                            int n, double th, double tnorm, double pivmin,
+                                            double* dp, double* dm, double* rat, double* sc,
+                                            double* y) {
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  __shared__ int kst;
+  __shared__ double mred[2][EIG_T / 64];
+  if (tid < 2) {
+    const bool fw = tid == 0;
+    double* out = fw ? dp : dm;
+    int i = fw ? 0 : n - 1;
+    double d = al[i] - th;
+    if (fabs(d) < pivmin) d = -pivmin;
+    out[i] = d;
+    for (int s2 = 1; s2 < n; ++s2) {
+      i = fw ? s2 : n - 1 - s2;
+      d = (al[i] - th) - b2[fw ? i - 1 : i] * rcp_nr(d);
+      if (fabs(d) < pivmin) d = -pivmin;
+      out[i] = d;
+    }
+  }
+  __syncthreads();
+  // |gamma_k| into sc; the ratios: rat[i] = beta_i / dp_i (i < n - 1) and
+  // sc2 = beta_(i-1) / dm_i (i > 0) kept in y for now
+  for (int i = tid; i < n; i += EIG_T) {
+    sc[i] = fabs(dp[i] + dm[i] - (al[i] - th));
+    rat[i] = (i < n - 1) ? b1[i] / dp[i] : 0.0;
+    y[i] = (i > 0) ? b1[i - 1] / dm[i] : 0.0;
+  }
+  __syncthreads();
+  if (wv == 0) {
+    // smallest |gamma| and its first index: lane scan, then lanes by pairs
+    double gm = DBL_MAX;
+    int gk = n;
+    for (int i = lane; i < n; i += 64)
+      if (sc[i] < gm) {
+        gm = sc[i];
+        gk = i;
+      }
+    for (int o = 32; o >= 1; o >>= 1) {
+      const double og = __shfl_xor(gm, o, 64);
+      const int ok = __shfl_xor(gk, o, 64);
+      if (og < gm || (og == gm && ok < gk)) {
+        gm = og;
+        gk = ok;
+      }
+    }
+    if (lane == 0) kst = gk;
+  }
+  __syncthreads();
+  const int k = kst;
+  // z into sc: lane 0 goes down from k, lane 1 up (the ratios up are in y)
+  if (tid < 2) {
+    const bool dn = tid == 0;
+    const int cnt = dn ? k : n - 1 - k, mx = max(k, n - 1 - k);
+    if (dn) sc[k] = 1.0;
+    double zc = 1.0;
+    for (int s2 = 1; s2 <= mx; ++s2) {
+      if (s2 <= cnt) {
+        const int i = dn ? k - s2 : k + s2;
+        zc = -(dn ? rat[i] : y[i]) * zc;
+        sc[i] = zc;
+      }
+    }
+  }
+  __syncthreads();
+  // residual and size (block maxima), finiteness
+  double rmax = 0.0, zmax = 0.0;
+  bool fin = true;
+  for (int i = tid; i < n; i += EIG_T) {
+    const double zi = sc[i];
+    double ri = (al[i] - th) * zi;
+    if (i > 0) ri = fma(b1[i - 1], sc[i - 1], ri);
+    if (i < n - 1) ri = fma(b1[i], sc[i + 1], ri);
+    fin = fin && isfinite(zi) && isfinite(ri);
+    rmax = fmax(rmax, fabs(ri));
+    zmax = fmax(zmax, fabs(zi));
+  }
+  for (int o = 32; o >= 1; o >>= 1) {
+    rmax = fmax(rmax, __shfl_xor(rmax, o, 64));
+    zmax = fmax(zmax, __shfl_xor(zmax, o, 64));
+  }
+  const bool allfin = __syncthreads_and(fin);
+  if (lane == 0) {
+    mred[0][wv] = rmax;
+    mred[1][wv] = zmax;
+  }
+  __syncthreads();
+  rmax = 0.0;
+  zmax = 0.0;
+  for (int q = 0; q < EIG_T / 64; ++q) {
+    rmax = fmax(rmax, mred[0][q]);
+    zmax = fmax(zmax, mred[1][q]);
+  }
+  const bool ok = allfin && zmax > 0.0 && rmax <= 64.0 * DBL_EPSILON * tnorm * zmax;
+  if (ok) {
+    for (int i = tid; i < n; i += EIG_T) y[i] = sc[i] / zmax;
+  }
+  __syncthreads();
+  return ok;
+}
+
 // Seig: [n_act][n_it][r] (row k, kept column c); rows n_eff.. are zero.
 __global__ __launch_bounds__(EIG_T) void k_eig_vectors(const double* __restrict__ alpha,
                                                        const double* __restrict__ beta,
@@ -175,6 +294,21 @@ __global__ __launch_bounds__(EIG_T) void k_eig_vectors(const double* __restrict_
   __shared__ double fu1[EIG_NMAX], fu2[EIG_NMAX], fd[EIG_NMAX], fl[EIG_NMAX];
   __shared__ int piv[EIG_NMAX];
   const TriInfo ti = load_tridiag(alpha + (int64_t)a * n_it, beta + (int64_t)a * n_it, n, al, b1, b2);
+  // An eigenvalue with no kept neighbour within EIG_TWIST_GAP |T| takes the
+  // twisted factorisation (its vector is then accurate to about eps |T| / gap,
+  // and k_eig_orth orthonormalises the clusters); if that fails its residual
+  // test, and for (numerically) repeated eigenvalues, inverse iteration below.
+  {
+    const double ctol = EIG_TWIST_GAP * ti.tnorm;
+    const bool lgap = c == r - r_eff || th - theta[(int64_t)a * r + c - 1] > ctol;
+    const bool rgap = c + 1 == r || theta[(int64_t)a * r + c + 1] - th > ctol;
+    if (lgap && rgap &&
+        twisted_vector(al, b1, b2, n, th, ti.tnorm, DBL_MIN * fmax(1.0, ti.bmax), fd, fl, fu1,
+                       fu2, y)) {
+      if (wv == 0) store_unit_column(y, n, n_it, r, c, Sa);
+      return;
+    }
+  }
   // LU of T - th I with partial pivoting on thread 0; the triangular solves
   // carry the running entries in registers
   if (tid == 0) {
@@ -256,57 +390,111 @@ __global__ __launch_bounds__(EIG_T) void k_eig_vectors(const double* __restrict_
 // Per window: the kept columns of each cluster (consecutive kept eigenvalues
 // at most EIG_CLUSTER |T| apart) orthonormalised in ascending order by
 // modified Gram-Schmidt, two passes, against the cluster's earlier columns;
-// then unit norm and the sign rule again.  Windows without clusters only read
-// theta and T.
+// then unit norm and the sign rule again.  The clusters are independent: wave
+// w of the workgroup takes clusters w, w + 4, ..., staging a cluster's columns
+// in its own LDS slice when they fit (else reading them from Seig), with wave
+// sums for the dot products and no workgroup barriers.  Windows without
+// clusters only read theta and T.
+constexpr int EIG_ORTH_LDS = 3072;             // doubles of LDS per wave
 __global__ __launch_bounds__(EIG_T) void k_eig_orth(const double* __restrict__ alpha,
                                                     const double* __restrict__ beta,
                                                     const int* __restrict__ neff, int n_it, int r,
                                                     const double* __restrict__ theta,
                                                     double* __restrict__ Seig) {
-  const int a = blockIdx.x, tid = threadIdx.x, wv = tid >> 6;
+  const int a = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int n = neff[a];
   const int c_lo = r - min(r, n);
   double* Sa = Seig + (int64_t)a * n_it * r;
   __shared__ double al[EIG_NMAX], b1[EIG_NMAX], b2[EIG_NMAX];
-  __shared__ double y[EIG_NMAX], tha[EIG_NMAX];
-  __shared__ double red[EIG_T / 64];
-  // the kept eigenvalues in LDS (the cluster scan below is sequential)
-  for (int c = threadIdx.x; c < r; c += EIG_T) tha[c] = theta[(int64_t)a * r + c];
+  __shared__ double tha[EIG_NMAX];
+  __shared__ int cstart[EIG_NMAX], ncl;
+  __shared__ double cb[EIG_T / 64][EIG_ORTH_LDS];
+  for (int c = tid; c < r; c += EIG_T) tha[c] = theta[(int64_t)a * r + c];
   const TriInfo ti = load_tridiag(alpha + (int64_t)a * n_it, beta + (int64_t)a * n_it, n, al, b1, b2);
   const double ctol = EIG_CLUSTER * ti.tnorm;
-  for (int c = c_lo; c < r;) {
-    int c1 = c;
-    while (c1 + 1 < r && tha[c1 + 1] - tha[c1] <= ctol) ++c1;
-    for (int k = c + 1; k <= c1; ++k) {
-      if (tid < n) y[tid] = Sa[(int64_t)tid * r + k];
-      __syncthreads();
+  // clusters of two or more kept columns, as start indices (cstart[q], end
+  // before the next start), found by one thread
+  if (tid == 0) {
+    int q = 0;
+    for (int c = c_lo; c < r;) {
+      int c1 = c;
+      while (c1 + 1 < r && tha[c1 + 1] - tha[c1] <= ctol) ++c1;
+      if (c1 > c) {
+        cstart[2 * q] = c;
+        cstart[2 * q + 1] = c1;
+        ++q;
+      }
+      c = c1 + 1;
+    }
+    ncl = q;
+  }
+  __syncthreads();
+  double* wb = cb[wv];
+  for (int q = wv; q < ncl; q += EIG_T / 64) {
+    const int c = cstart[2 * q], c1 = cstart[2 * q + 1], s = c1 - c + 1;
+    const bool staged = s * n <= EIG_ORTH_LDS;
+    // column p of the cluster (p < s): LDS slice or Seig
+    auto colp = [&](int p, int i) -> double {
+      return staged ? wb[p * n + i] : Sa[(int64_t)i * r + c + p];
+    };
+    if (staged) {
+      for (int p = 0; p < s; ++p)
+        for (int i = lane; i < n; i += 64) wb[p * n + i] = Sa[(int64_t)i * r + c + p];
+    }
+    for (int k = 1; k < s; ++k) {
+      double y[EIG_NMAX / 64];
+#pragma unroll
+      for (int t = 0; t < EIG_NMAX / 64; ++t) {
+        const int i = lane + 64 * t;
+        y[t] = (i < n) ? colp(k, i) : 0.0;
+      }
       for (int pass = 0; pass < 2; ++pass) {
-        for (int p = c; p < k; ++p) {
-          const double sp = (tid < n) ? Sa[(int64_t)tid * r + p] : 0.0;
-          const double d = block_sum_f64((tid < n) ? y[tid] * sp : 0.0, red);
-          if (tid < n) y[tid] = fma(-d, sp, y[tid]);
-          __syncthreads();
+        for (int p = 0; p < k; ++p) {
+          double d = 0.0;
+#pragma unroll
+          for (int t = 0; t < EIG_NMAX / 64; ++t) {
+            const int i = lane + 64 * t;
+            if (i < n) d = fma(y[t], colp(p, i), d);
+          }
+          d = wave_sum_f64(d);
+#pragma unroll
+          for (int t = 0; t < EIG_NMAX / 64; ++t) {
+            const int i = lane + 64 * t;
+            if (i < n) y[t] = fma(-d, colp(p, i), y[t]);
+          }
         }
       }
-      if (wv == 0) store_unit_column(y, n, n_it, r, k, Sa);
-      __syncthreads();               // column k is read for the next members
+      // unit norm and the sign rule (first nonzero entry positive), into the
+      // slice (for the later members) and Seig
+      double nr = 0.0;
+      int first = n - 1;
+#pragma unroll
+      for (int t = 0; t < EIG_NMAX / 64; ++t) {
+        const int i = lane + 64 * t;
+        if (i < n) {
+          nr = fma(y[t], y[t], nr);
+          if (y[t] != 0.0 && i < first) first = i;
+        }
+      }
+      nr = wave_sum_f64(nr);
+      for (int o = 32; o >= 1; o >>= 1) first = min(first, __shfl_xor(first, o, 64));
+      double yo = 0.0;                           // this lane's entry of slot first >> 6
+#pragma unroll
+      for (int t = 0; t < EIG_NMAX / 64; ++t) yo = (t == (first >> 6)) ? y[t] : yo;
+      const double yf = __shfl(yo, first & 63, 64);
+      double sc = 1.0 / sqrt(nr);
+      if (yf < 0.0) sc = -sc;
+#pragma unroll
+      for (int t = 0; t < EIG_NMAX / 64; ++t) {
+        const int i = lane + 64 * t;
+        if (i < n) {
+          const double v = y[t] * sc;
+          if (staged) wb[k * n + i] = v;
+          Sa[(int64_t)i * r + c + k] = v;
+        }
+      }
     }
-    c = c1 + 1;
   }
-}
-
-hipError_t launch_tridiag_eig(const double* alpha, const double* beta, const int* neff,
-                              int n_act, int n_it, int r, double* theta, double* Seig,
-                              hipStream_t s) {
-  (void)hipGetLastError();
-  if (n_it > EIG_NMAX || r > n_it) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_eig_values, dim3(r, n_act), dim3(EIG_T), 0, s, alpha, beta, neff, n_it, r,
-                     theta);
-  hipLaunchKernelGGL(k_eig_vectors, dim3(r, n_act), dim3(EIG_T), 0, s, alpha, beta, neff, n_it,
-                     r, theta, Seig);
-  hipLaunchKernelGGL(k_eig_orth, dim3(n_act), dim3(EIG_T), 0, s, alpha, beta, neff, n_it, r, theta,
-                     Seig);
-  return hipGetLastError();
 }
 
 // Z[a][i][c] = sum_{k < n_eff} Q[a][k][i] Seig[a][k][c]   (fp64).
@@ -383,7 +571,7 @@ __global__ __launch_bounds__(256) void k_ritz(const double* __restrict__ Q,
   }
 }
 
-hipError_t launch_ritz(const double* Q, const double* Seig, const int* neff, int n_act, int L,
+static hipError_t launch_ritz(const double* Q, const double* Seig, const int* neff, int n_act, int L,
                        int ldq, int n_it, int r, double* Z, hipStream_t s) {
   (void)hipGetLastError();
   const dim3 grid((unsigned)((L + 31) / 32), n_act);
@@ -394,6 +582,201 @@ hipError_t launch_ritz(const double* Q, const double* Seig, const int* neff, int
   else if (cpt <= 8) hipLaunchKernelGGL(k_ritz<8>, grid, dim3(256), 0, s, Q, Seig, neff, L, ldq, n_it, r, Z);
   else hipLaunchKernelGGL(k_ritz<16>, grid, dim3(256), 0, s, Q, Seig, neff, L, ldq, n_it, r, Z);
   return hipGetLastError();
+}
+
+// The cluster orthonormalisation of k_eig_orth and the Ritz coordinates of
+// k_ritz in one kernel, when S (n_it x r) and a block's Q rows (n_it x 32) fit
+// in LDS together: every block stages all of S and its 32 rows of Q with one
+// round of loads, repeats the (small, deterministic) orthonormalisation of the
+// clustered columns on its copy of S -- the same arithmetic as k_eig_orth, so
+// every block holds the same S -- and forms its rows of Z.  The clusters of a
+// window are found in parallel (a cluster of two or more kept columns starts
+// where the gap below is above EIG_CLUSTER |T| and the gap above is not) and
+// shared out to the waves, which need no barriers between them.
+constexpr int RZ_LDS = 12288;                  // doubles of dynamic LDS (96 KiB)
+template <int CQ>
+__global__ __launch_bounds__(256) void k_ritz_orth(const double* __restrict__ Q,
+                                                   const double* __restrict__ Seig,
+                                                   const int* __restrict__ neff,
+                                                   const double* __restrict__ alpha,
+                                                   const double* __restrict__ beta,
+                                                   const double* __restrict__ theta, int L,
+                                                   int ldq, int n_it, int r,
+                                                   double* __restrict__ Z) {
+  extern __shared__ double rzs[];
+  double* sS = rzs;                              // [k][c], k < n, row stride r
+  double* sQ = rzs + n_it * r;                   // [k][32]
+  __shared__ double tha[EIG_NMAX], mred[4];
+  __shared__ int cst[EIG_NMAX], ncl;
+  const int a = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int n = neff[a];
+  const int r0 = blockIdx.x * 32;
+  const int c_lo = r - min(r, n);
+  const double* Sa = Seig + (int64_t)a * n_it * r;
+  const double* Qa = Q + (int64_t)a * ldq * L;
+  const double* al = alpha + (int64_t)a * n_it;
+  const double* be = beta + (int64_t)a * n_it;
+  if (tid == 0) ncl = 0;
+  // one round of loads: S, the block's Q rows, theta and the Gershgorin terms
+  {
+    const int ns = n * r, nq = n * 32;
+    for (int e0 = tid; e0 < ns + nq; e0 += 256 * 24) {
+      double v[24];
+#pragma unroll
+      for (int u = 0; u < 24; ++u) {
+        const int e = min(e0 + 256 * u, ns + nq - 1);
+        v[u] = (e < ns) ? Sa[e] : Qa[(int64_t)((e - ns) >> 5) * L + min(r0 + ((e - ns) & 31), L - 1)];
+      }
+#pragma unroll
+      for (int u = 0; u < 24; ++u) {
+        const int e = e0 + 256 * u;
+        if (e < ns) sS[e] = v[u];
+        else if (e < ns + nq) sQ[e - ns] = v[u];
+      }
+    }
+  }
+  for (int c = tid; c < r; c += 256) tha[c] = theta[(int64_t)a * r + c];
+  double tn = 0.0;
+  for (int k = tid; k < n; k += 256) {
+    const double off = ((k < n - 1) ? fabs(be[k]) : 0.0) + ((k > 0) ? fabs(be[k - 1]) : 0.0);
+    tn = fmax(tn, fabs(al[k]) + off);
+  }
+  for (int o = 32; o >= 1; o >>= 1) tn = fmax(tn, __shfl_xor(tn, o, 64));
+  if (lane == 0) mred[wv] = tn;
+  __syncthreads();
+  const double ctol = EIG_CLUSTER * fmax(fmax(mred[0], mred[1]), fmax(mred[2], mred[3]));
+  for (int c = c_lo + tid; c < r; c += 256) {
+    const bool start = c == c_lo || tha[c] - tha[c - 1] > ctol;
+    if (start && c + 1 < r && tha[c + 1] - tha[c] <= ctol) {
+      int c1 = c + 1;
+      while (c1 + 1 < r && tha[c1 + 1] - tha[c1] <= ctol) ++c1;
+      const int q = atomicAdd(&ncl, 1);
+      cst[2 * q] = c;
+      cst[2 * q + 1] = c1;
+    }
+  }
+  __syncthreads();
+  for (int q = wv; q < ncl; q += 4) {
+    const int c = cst[2 * q], c1 = cst[2 * q + 1];
+    for (int k = c + 1; k <= c1; ++k) {
+      double y[EIG_NMAX / 64];
+#pragma unroll
+      for (int t = 0; t < EIG_NMAX / 64; ++t) {
+        const int i = lane + 64 * t;
+        y[t] = (i < n) ? sS[i * r + k] : 0.0;
+      }
+      for (int pass = 0; pass < 2; ++pass) {
+        for (int p = c; p < k; ++p) {
+          double d = 0.0;
+#pragma unroll
+          for (int t = 0; t < EIG_NMAX / 64; ++t) {
+            const int i = lane + 64 * t;
+            if (i < n) d = fma(y[t], sS[i * r + p], d);
+          }
+          d = wave_sum_f64(d);
+#pragma unroll
+          for (int t = 0; t < EIG_NMAX / 64; ++t) {
+            const int i = lane + 64 * t;
+            if (i < n) y[t] = fma(-d, sS[i * r + p], y[t]);
+          }
+        }
+      }
+      double nr = 0.0;
+      int first = n - 1;
+#pragma unroll
+      for (int t = 0; t < EIG_NMAX / 64; ++t) {
+        const int i = lane + 64 * t;
+        if (i < n) {
+          nr = fma(y[t], y[t], nr);
+          if (y[t] != 0.0 && i < first) first = i;
+        }
+      }
+      nr = wave_sum_f64(nr);
+      for (int o = 32; o >= 1; o >>= 1) first = min(first, __shfl_xor(first, o, 64));
+      double yo = 0.0;
+#pragma unroll
+      for (int t = 0; t < EIG_NMAX / 64; ++t) yo = (t == (first >> 6)) ? y[t] : yo;
+      const double yf = __shfl(yo, first & 63, 64);
+      double sc = 1.0 / sqrt(nr);
+      if (yf < 0.0) sc = -sc;
+#pragma unroll
+      for (int t = 0; t < EIG_NMAX / 64; ++t) {
+        const int i = lane + 64 * t;
+        if (i < n) sS[i * r + k] = y[t] * sc;
+      }
+    }
+  }
+  __syncthreads();
+  // Z rows of the block: thread (row pair rp, column group cq) owns rows
+  // 2 rp, 2 rp + 1 and columns cq CQ ... cq CQ + CQ - 1 (clamped; the surplus
+  // not stored): per k two values of Q and CQ of S for 2 CQ products
+  const int rp = tid & 15, cq = tid >> 4;
+  double acc[2][CQ];
+#pragma unroll
+  for (int c = 0; c < CQ; ++c) acc[0][c] = acc[1][c] = 0.0;
+  int col[CQ];
+#pragma unroll
+  for (int c = 0; c < CQ; ++c) col[c] = min(cq * CQ + c, r - 1);
+  for (int k = 0; k < n; ++k) {
+    const double q0 = sQ[k * 32 + 2 * rp], q1 = sQ[k * 32 + 2 * rp + 1];
+#pragma unroll
+    for (int c = 0; c < CQ; ++c) {
+      const double sv = sS[k * r + col[c]];
+      acc[0][c] = fma(q0, sv, acc[0][c]);
+      acc[1][c] = fma(q1, sv, acc[1][c]);
+    }
+  }
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int i = r0 + 2 * rp + h;
+    if (i < L) {
+      double* zr = Z + ((int64_t)a * L + i) * r;
+#pragma unroll
+      for (int c = 0; c < CQ; ++c)
+        if (cq * CQ + c < r) zr[cq * CQ + c] = acc[h][c];
+    }
+  }
+}
+
+template <int CQ>
+static hipError_t launch_ritz_orth_t(const double* Q, const double* Seig, const int* neff,
+                                     const double* alpha, const double* beta,
+                                     const double* theta, int n_act, int L, int ldq, int n_it,
+                                     int r, double* Z, hipStream_t s) {
+  const size_t lds = (size_t)n_it * (r + 32) * sizeof(double);
+  auto k = k_ritz_orth<CQ>;
+  if (lds > 65536) {
+    const hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k, dim3((unsigned)((L + 31) / 32), n_act), dim3(256), lds, s, Q, Seig, neff,
+                     alpha, beta, theta, L, ldq, n_it, r, Z);
+  return hipSuccess;
+}
+
+hipError_t launch_eigh_ritz(const double* alpha, const double* beta, const int* neff, int n_act,
+                            int n_it, int r, double* theta, double* Seig, const double* Q, int L,
+                            int ldq, double* Z, hipStream_t s) {
+  (void)hipGetLastError();
+  if (n_it > EIG_NMAX || r > n_it || r > 128 || r < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_eig_values, dim3(r, n_act), dim3(EIG_T), 0, s, alpha, beta, neff, n_it, r,
+                     theta);
+  hipLaunchKernelGGL(k_eig_vectors, dim3(r, n_act), dim3(EIG_T), 0, s, alpha, beta, neff, n_it,
+                     r, theta, Seig);
+  const int cq = (r + 15) / 16;                   // columns per thread of k_ritz_orth
+  if ((int64_t)n_it * (r + 32) <= RZ_LDS) {
+    hipError_t e;
+    if (cq <= 1) e = launch_ritz_orth_t<1>(Q, Seig, neff, alpha, beta, theta, n_act, L, ldq, n_it, r, Z, s);
+    else if (cq <= 2) e = launch_ritz_orth_t<2>(Q, Seig, neff, alpha, beta, theta, n_act, L, ldq, n_it, r, Z, s);
+    else if (cq <= 4) e = launch_ritz_orth_t<4>(Q, Seig, neff, alpha, beta, theta, n_act, L, ldq, n_it, r, Z, s);
+    else e = launch_ritz_orth_t<8>(Q, Seig, neff, alpha, beta, theta, n_act, L, ldq, n_it, r, Z, s);
+    if (e != hipSuccess) return e;
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL(k_eig_orth, dim3(n_act), dim3(EIG_T), 0, s, alpha, beta, neff, n_it, r, theta,
+                     Seig);
+  return launch_ritz(Q, Seig, neff, n_act, L, ldq, n_it, r, Z, s);
 }
 
 }  // namespace slh

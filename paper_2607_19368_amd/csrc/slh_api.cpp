@@ -375,11 +375,8 @@ hipError_t launch_lanczos_graph_body(slh_ctx* c, const LanczosWS& w, const doubl
                                  int n_it, int L) {
   hipError_t e = launch_lanczos(w, q1act, c->cap_stream);
   if (e == hipSuccess)
-    e = launch_tridiag_eig(w.alpha, w.beta, w.neff, na, n_it, c->r, P<double>(c->theta),
-                           P<double>(c->Seig), c->cap_stream);
-  if (e == hipSuccess)
-    e = launch_ritz(w.Q, P<double>(c->Seig), w.neff, na, L, w.ldq, n_it, c->r, P<double>(c->Z),
-                    c->cap_stream);
+    e = launch_eigh_ritz(w.alpha, w.beta, w.neff, na, n_it, c->r, P<double>(c->theta),
+                         P<double>(c->Seig), w.Q, L, w.ldq, P<double>(c->Z), c->cap_stream);
   return e;
 }
 
@@ -826,10 +823,9 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
         HIP_TRY(c, hipEventRecord(c->ev[2], c->stream));
         HIP_TRY(c, launch_lanczos(w, q1act, c->stream, c->ev_fb.data(), c->ev_fa.data()));
         HIP_TRY(c, hipEventRecord(c->ev[3], c->stream));
-        HIP_TRY(c, launch_tridiag_eig(w.alpha, w.beta, w.neff, na, n_it, c->r, P<double>(c->theta),
-                                      P<double>(c->Seig), c->stream));
-        HIP_TRY(c, launch_ritz(w.Q, P<double>(c->Seig), w.neff, na, (int)L, w.ldq, n_it, c->r,
-                               P<double>(c->Z), c->stream));
+        HIP_TRY(c, launch_eigh_ritz(w.alpha, w.beta, w.neff, na, n_it, c->r, P<double>(c->theta),
+                                    P<double>(c->Seig), w.Q, (int)L, w.ldq, P<double>(c->Z),
+                                    c->stream));
         HIP_TRY(c, hipEventRecord(c->ev[4], c->stream));
       } else {
         // The step sequence, Eigh(T) and the Ritz coordinates are captured once
@@ -892,10 +888,9 @@ int slh_eigh_ritz(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out
     ENSURE(c, c->theta, (size_t)na * c->r * 8);
     ENSURE(c, c->Seig, (size_t)na * n_it * c->r * 8);
     ENSURE(c, c->Z, (size_t)na * L * c->r * 8);
-    HIP_TRY(c, launch_tridiag_eig(P<double>(c->alpha), P<double>(c->beta), P<int>(c->neff), na,
-                                  n_it, c->r, P<double>(c->theta), P<double>(c->Seig), c->stream));
-    HIP_TRY(c, launch_ritz(P<double>(c->Q), P<double>(c->Seig), P<int>(c->neff), na, (int)L,
-                           n_it + 1, n_it, c->r, P<double>(c->Z), c->stream));
+    HIP_TRY(c, launch_eigh_ritz(P<double>(c->alpha), P<double>(c->beta), P<int>(c->neff), na,
+                                n_it, c->r, P<double>(c->theta), P<double>(c->Seig),
+                                P<double>(c->Q), (int)L, n_it + 1, P<double>(c->Z), c->stream));
     if (ritz_out)
       HIP_TRY(c, hipMemcpyAsync(ritz_out, c->theta.p, (size_t)na * c->r * 8, hipMemcpyDeviceToHost,
                                 c->stream));

@@ -71,11 +71,11 @@ hipError_t launch_lanczos(const LanczosWS& w, const double* q1_act, hipStream_t 
 hipError_t launch_lanczos_passes(const LanczosWS& w, int j, int reps, hipStream_t s);
 
 // ---- eigensolve + Ritz + SimHash (k_eig.hip, k_hash.hip) ----
-hipError_t launch_tridiag_eig(const double* alpha, const double* beta, const int* neff,
-                              int n_act, int n_it, int r, double* theta, double* Seig,
-                              hipStream_t s);
-hipError_t launch_ritz(const double* Q, const double* Seig, const int* neff, int n_act,
-                       int L, int ldq, int n_it, int r, double* Z, hipStream_t s);
+// Eigh(T) of every active window (theta: kept eigenvalues ascending, Seig their
+// vectors) and Z = Q S[:, kept] (Algorithm 1), all on stream s.
+hipError_t launch_eigh_ritz(const double* alpha, const double* beta, const int* neff, int n_act,
+                            int n_it, int r, double* theta, double* Seig, const double* Q, int L,
+                            int ldq, double* Z, hipStream_t s);
 hipError_t launch_simhash(const double* Z, const double* R, const int* winlist, int n_act,
                           int L, int r, int bits, uint32_t* codes, double* proj,
                           hipStream_t s);
