@@ -25,6 +25,8 @@
 
 #include <float.h>
 
+#include <algorithm>
+
 namespace slh {
 
 #define EIG_NMAX 256
@@ -593,8 +595,8 @@ static hipError_t launch_ritz(const double* Q, const double* Seig, const int* ne
 // window are found in parallel (a cluster of two or more kept columns starts
 // where the gap below is above EIG_CLUSTER |T| and the gap above is not) and
 // shared out to the waves, which need no barriers between them.
-constexpr int RZ_LDS = 12288;                  // doubles of dynamic LDS (96 KiB)
-template <int CQ>
+constexpr int RZ_LDS = 16384;                  // doubles of dynamic LDS (128 KiB)
+constexpr int RZ_NMAX = 128;                   // largest n_it of the fused path
 __global__ __launch_bounds__(256) void k_ritz_orth(const double* __restrict__ Q,
                                                    const double* __restrict__ Seig,
                                                    const int* __restrict__ neff,
@@ -604,13 +606,18 @@ __global__ __launch_bounds__(256) void k_ritz_orth(const double* __restrict__ Q,
                                                    int ldq, int n_it, int r,
                                                    double* __restrict__ Z) {
   extern __shared__ double rzs[];
-  double* sS = rzs;                              // [k][c], k < n, row stride r
-  double* sQ = rzs + n_it * r;                   // [k][32]
+  // S row-major with a padded row stride rs = r + 1, so that a column (the
+  // Gram-Schmidt reads) spreads over the LDS banks
+  const int rs = r + 1;
+  const int n4r = (n_it + 3) & ~3;               // rows allocated (k steps of 4)
+  double* sS = rzs;                              // [k][c], k < n (rows n .. n4 - 1 zero)
+  double* sQ = rzs + n4r * rs;                   // [k][32]
   __shared__ double tha[EIG_NMAX], mred[4];
   __shared__ int cst[EIG_NMAX], ncl;
   const int a = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int n = neff[a];
-  const int r0 = blockIdx.x * 32;
+  const int ntile = (L + 31) / 32;
+  const int r0 = blockIdx.x * 32;                // first tile; then every gridDim.x-th
   const int c_lo = r - min(r, n);
   const double* Sa = Seig + (int64_t)a * n_it * r;
   const double* Qa = Q + (int64_t)a * ldq * L;
@@ -630,10 +637,14 @@ __global__ __launch_bounds__(256) void k_ritz_orth(const double* __restrict__ Q,
 #pragma unroll
       for (int u = 0; u < 24; ++u) {
         const int e = e0 + 256 * u;
-        if (e < ns) sS[e] = v[u];
+        if (e < ns) sS[(e / r) * rs + e % r] = v[u];
         else if (e < ns + nq) sQ[e - ns] = v[u];
       }
     }
+    // rows n .. n4 - 1 of S and Q zero (the last step of 4 of the products)
+    const int n4 = (n + 3) & ~3;
+    for (int e = tid; e < (n4 - n) * rs; e += 256) sS[n * rs + e] = 0.0;
+    for (int e = tid; e < (n4 - n) * 32; e += 256) sQ[n * 32 + e] = 0.0;
   }
   for (int c = tid; c < r; c += 256) tha[c] = theta[(int64_t)a * r + c];
   double tn = 0.0;
@@ -663,7 +674,7 @@ __global__ __launch_bounds__(256) void k_ritz_orth(const double* __restrict__ Q,
 #pragma unroll
       for (int t = 0; t < EIG_NMAX / 64; ++t) {
         const int i = lane + 64 * t;
-        y[t] = (i < n) ? sS[i * r + k] : 0.0;
+        y[t] = (i < n) ? sS[i * rs + k] : 0.0;
       }
       for (int pass = 0; pass < 2; ++pass) {
         for (int p = c; p < k; ++p) {
@@ -671,13 +682,13 @@ __global__ __launch_bounds__(256) void k_ritz_orth(const double* __restrict__ Q,
 #pragma unroll
           for (int t = 0; t < EIG_NMAX / 64; ++t) {
             const int i = lane + 64 * t;
-            if (i < n) d = fma(y[t], sS[i * r + p], d);
+            if (i < n) d = fma(y[t], sS[i * rs + p], d);
           }
           d = wave_sum_f64(d);
 #pragma unroll
           for (int t = 0; t < EIG_NMAX / 64; ++t) {
             const int i = lane + 64 * t;
-            if (i < n) y[t] = fma(-d, sS[i * r + p], y[t]);
+            if (i < n) y[t] = fma(-d, sS[i * rs + p], y[t]);
           }
         }
       }
@@ -702,75 +713,100 @@ __global__ __launch_bounds__(256) void k_ritz_orth(const double* __restrict__ Q,
 #pragma unroll
       for (int t = 0; t < EIG_NMAX / 64; ++t) {
         const int i = lane + 64 * t;
-        if (i < n) sS[i * r + k] = y[t] * sc;
+        if (i < n) sS[i * rs + k] = y[t] * sc;
       }
     }
   }
   __syncthreads();
-  // Z rows of the block: thread (row pair rp, column group cq) owns rows
-  // 2 rp, 2 rp + 1 and columns cq CQ ... cq CQ + CQ - 1 (clamped; the surplus
-  // not stored): per k two values of Q and CQ of S for 2 CQ products
-  const int rp = tid & 15, cq = tid >> 4;
-  double acc[2][CQ];
+  // Z rows, 32 per tile, on the fp64 matrix cores: Z_tile = Q_tile^T S as
+  // 16 x 16 blocks (v_mfma_f64_16x16x4f64: lane l holds A[l % 16][l / 16] and
+  // B[l / 16][l % 16] of a 16 x 4 by 4 x 16 step, and D[l / 16 + 4 v][l % 16],
+  // v < 4); wave w takes the column blocks w, w + 4, ... of both row halves.
+  // The block's later tiles (every gridDim.x-th) have their Q rows fetched
+  // into registers while the current tile is multiplied.
+  typedef double f64x4 __attribute__((ext_vector_type(4)));
+  const int n4 = (n + 3) & ~3, nct = (r + 15) / 16;
+  const int li = lane & 15, lk = lane >> 4;
+  constexpr int QPT = RZ_NMAX * 32 / 256;         // Q values per thread and tile, at most
+  double qn[QPT];
+  auto fetch_q = [&](int t0) {
 #pragma unroll
-  for (int c = 0; c < CQ; ++c) acc[0][c] = acc[1][c] = 0.0;
-  int col[CQ];
-#pragma unroll
-  for (int c = 0; c < CQ; ++c) col[c] = min(cq * CQ + c, r - 1);
-  for (int k = 0; k < n; ++k) {
-    const double q0 = sQ[k * 32 + 2 * rp], q1 = sQ[k * 32 + 2 * rp + 1];
-#pragma unroll
-    for (int c = 0; c < CQ; ++c) {
-      const double sv = sS[k * r + col[c]];
-      acc[0][c] = fma(q0, sv, acc[0][c]);
-      acc[1][c] = fma(q1, sv, acc[1][c]);
+    for (int u = 0; u < QPT; ++u) {
+      const int e = tid + 256 * u;
+      if (e < n * 32) qn[u] = Qa[(int64_t)(e >> 5) * L + min(t0 * 32 + (e & 31), L - 1)];
     }
-  }
+  };
+  int tile = blockIdx.x;
+  if (tile + (int)gridDim.x < ntile) fetch_q(tile + gridDim.x);
+  for (;;) {
+    for (int ct = wv; ct < nct; ct += 4) {
+      const int jb = ct * 16 + li, jc = min(jb, r - 1);
+      f64x4 acc0 = {0.0, 0.0, 0.0, 0.0}, acc1 = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll 2
+      for (int k0 = 0; k0 < n4; k0 += 4) {
+        const int kk = k0 + lk;
+        const double b = sS[kk * rs + jc];
+        const double a0 = sQ[kk * 32 + li], a1 = sQ[kk * 32 + 16 + li];
+        acc0 = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b, acc1, 0, 0, 0);
+      }
+      if (jb < r) {
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int i = r0 + 2 * rp + h;
-    if (i < L) {
-      double* zr = Z + ((int64_t)a * L + i) * r;
-#pragma unroll
-      for (int c = 0; c < CQ; ++c)
-        if (cq * CQ + c < r) zr[cq * CQ + c] = acc[h][c];
+        for (int v = 0; v < 4; ++v) {
+          const int i0 = tile * 32 + lk + 4 * v, i1 = i0 + 16;
+          if (i0 < L) Z[((int64_t)a * L + i0) * r + jb] = acc0[v];
+          if (i1 < L) Z[((int64_t)a * L + i1) * r + jb] = acc1[v];
+        }
+      }
     }
+    tile += gridDim.x;
+    if (tile >= ntile) break;
+    __syncthreads();                              // sQ of the last tile read by all
+#pragma unroll
+    for (int u = 0; u < QPT; ++u) {
+      const int e = tid + 256 * u;
+      if (e < n * 32) sQ[e] = qn[u];
+    }
+    __syncthreads();
+    if (tile + (int)gridDim.x < ntile) fetch_q(tile + gridDim.x);
   }
 }
 
-template <int CQ>
-static hipError_t launch_ritz_orth_t(const double* Q, const double* Seig, const int* neff,
+static hipError_t launch_ritz_orth(const double* Q, const double* Seig, const int* neff,
                                      const double* alpha, const double* beta,
                                      const double* theta, int n_act, int L, int ldq, int n_it,
-                                     int r, double* Z, hipStream_t s) {
-  const size_t lds = (size_t)n_it * (r + 32) * sizeof(double);
-  auto k = k_ritz_orth<CQ>;
+                                     int r, double* Z, int n_cu, hipStream_t s) {
+  const size_t lds = (size_t)((n_it + 3) & ~3) * (r + 33) * sizeof(double);
+  auto k = k_ritz_orth;
   if (lds > 65536) {
     const hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize,
                                              (int)lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(k, dim3((unsigned)((L + 31) / 32), n_act), dim3(256), lds, s, Q, Seig, neff,
-                     alpha, beta, theta, L, ldq, n_it, r, Z);
+  // one round of resident blocks (as many per CU as their LDS allows, 160 KiB
+  // per CU): one tile per block while the tiles fit, else each block loops
+  // over tiles (S staged and orthonormalised once per block)
+  const int64_t ntile = (L + 31) / 32;
+  const int64_t bpc = std::max<int64_t>(1, 163840 / (int64_t)(lds + 4096));
+  const int64_t per_win = std::max<int64_t>(1, bpc * std::max(1, n_cu) / std::max(1, n_act));
+  const unsigned bx = (unsigned)std::min<int64_t>(ntile, per_win);
+  hipLaunchKernelGGL(k, dim3(bx, n_act), dim3(256), lds, s, Q, Seig, neff, alpha, beta, theta, L,
+                     ldq, n_it, r, Z);
   return hipSuccess;
 }
 
 hipError_t launch_eigh_ritz(const double* alpha, const double* beta, const int* neff, int n_act,
                             int n_it, int r, double* theta, double* Seig, const double* Q, int L,
-                            int ldq, double* Z, hipStream_t s) {
+                            int ldq, double* Z, int n_cu, hipStream_t s) {
   (void)hipGetLastError();
   if (n_it > EIG_NMAX || r > n_it || r > 128 || r < 1) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_eig_values, dim3(r, n_act), dim3(EIG_T), 0, s, alpha, beta, neff, n_it, r,
                      theta);
   hipLaunchKernelGGL(k_eig_vectors, dim3(r, n_act), dim3(EIG_T), 0, s, alpha, beta, neff, n_it,
                      r, theta, Seig);
-  const int cq = (r + 15) / 16;                   // columns per thread of k_ritz_orth
-  if ((int64_t)n_it * (r + 32) <= RZ_LDS) {
-    hipError_t e;
-    if (cq <= 1) e = launch_ritz_orth_t<1>(Q, Seig, neff, alpha, beta, theta, n_act, L, ldq, n_it, r, Z, s);
-    else if (cq <= 2) e = launch_ritz_orth_t<2>(Q, Seig, neff, alpha, beta, theta, n_act, L, ldq, n_it, r, Z, s);
-    else if (cq <= 4) e = launch_ritz_orth_t<4>(Q, Seig, neff, alpha, beta, theta, n_act, L, ldq, n_it, r, Z, s);
-    else e = launch_ritz_orth_t<8>(Q, Seig, neff, alpha, beta, theta, n_act, L, ldq, n_it, r, Z, s);
+  if ((int64_t)((n_it + 3) & ~3) * (r + 33) <= RZ_LDS && n_it <= RZ_NMAX) {
+    const hipError_t e = launch_ritz_orth(Q, Seig, neff, alpha, beta, theta, n_act, L, ldq, n_it, r,
+                                          Z, n_cu, s);
     if (e != hipSuccess) return e;
     return hipGetLastError();
   }

@@ -376,7 +376,7 @@ hipError_t launch_lanczos_graph_body(slh_ctx* c, const LanczosWS& w, const doubl
   hipError_t e = launch_lanczos(w, q1act, c->cap_stream);
   if (e == hipSuccess)
     e = launch_eigh_ritz(w.alpha, w.beta, w.neff, na, n_it, c->r, P<double>(c->theta),
-                         P<double>(c->Seig), w.Q, L, w.ldq, P<double>(c->Z), c->cap_stream);
+                         P<double>(c->Seig), w.Q, L, w.ldq, P<double>(c->Z), c->n_cu, c->cap_stream);
   return e;
 }
 
@@ -825,7 +825,7 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
         HIP_TRY(c, hipEventRecord(c->ev[3], c->stream));
         HIP_TRY(c, launch_eigh_ritz(w.alpha, w.beta, w.neff, na, n_it, c->r, P<double>(c->theta),
                                     P<double>(c->Seig), w.Q, (int)L, w.ldq, P<double>(c->Z),
-                                    c->stream));
+                                    c->n_cu, c->stream));
         HIP_TRY(c, hipEventRecord(c->ev[4], c->stream));
       } else {
         // The step sequence, Eigh(T) and the Ritz coordinates are captured once
@@ -890,7 +890,8 @@ int slh_eigh_ritz(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out
     ENSURE(c, c->Z, (size_t)na * L * c->r * 8);
     HIP_TRY(c, launch_eigh_ritz(P<double>(c->alpha), P<double>(c->beta), P<int>(c->neff), na,
                                 n_it, c->r, P<double>(c->theta), P<double>(c->Seig),
-                                P<double>(c->Q), (int)L, n_it + 1, P<double>(c->Z), c->stream));
+                                P<double>(c->Q), (int)L, n_it + 1, P<double>(c->Z), c->n_cu,
+                                c->stream));
     if (ritz_out)
       HIP_TRY(c, hipMemcpyAsync(ritz_out, c->theta.p, (size_t)na * c->r * 8, hipMemcpyDeviceToHost,
                                 c->stream));

@@ -75,7 +75,7 @@ hipError_t launch_lanczos_passes(const LanczosWS& w, int j, int reps, hipStream_
 // vectors) and Z = Q S[:, kept] (Algorithm 1), all on stream s.
 hipError_t launch_eigh_ritz(const double* alpha, const double* beta, const int* neff, int n_act,
                             int n_it, int r, double* theta, double* Seig, const double* Q, int L,
-                            int ldq, double* Z, hipStream_t s);
+                            int ldq, double* Z, int n_cu, hipStream_t s);
 hipError_t launch_simhash(const double* Z, const double* R, const int* winlist, int n_act,
                           int L, int r, int bits, uint32_t* codes, double* proj,
                           hipStream_t s);
