@@ -55,7 +55,8 @@ __device__ __forceinline__ int sturm_count(const double* al, const double* b2, i
   return cnt;
 }
 
-#define EIG_T 256                // threads per eigenpair: one multisection probe each
+#define EIG_T 256                // threads per eigenpair (vectors, orthonormalisation)
+#define EIG_VT 256               // threads per eigenvalue: one multisection probe each (512 measured slower: 43 against 36 us at n = 96)
 
 // T of window a into LDS (al: diagonal, b1: off-diagonal, b2: its squares) and
 // its Gershgorin interval [lo, hi], |T| bound tnorm and largest b^2 (every wave
@@ -97,7 +98,7 @@ __device__ __forceinline__ TriInfo load_tridiag(const double* __restrict__ alp,
 
 // theta: [n_act][r], ascending kept eigenvalues (zero for the r - r_eff
 // leading columns of a window that stopped after n_eff < r steps).
-__global__ __launch_bounds__(EIG_T) void k_eig_values(const double* __restrict__ alpha,
+__global__ __launch_bounds__(EIG_VT) void k_eig_values(const double* __restrict__ alpha,
                                                       const double* __restrict__ beta,
                                                       const int* __restrict__ neff, int n_it,
                                                       int r, double* __restrict__ theta) {
@@ -110,13 +111,13 @@ __global__ __launch_bounds__(EIG_T) void k_eig_values(const double* __restrict__
   }
   const int kidx = n - r + c;   // ascending index of the wanted eigenvalue
   __shared__ double al[EIG_NMAX], b1[EIG_NMAX], b2[EIG_NMAX];
-  __shared__ unsigned long long smask[EIG_T / 64];
+  __shared__ unsigned long long smask[EIG_VT / 64];
   const TriInfo ti = load_tridiag(alpha + (int64_t)a * n_it, beta + (int64_t)a * n_it, n, al, b1, b2);
   const double pivmin = DBL_MIN * fmax(1.0, ti.bmax);
   const double pad = 2.0 * DBL_EPSILON * fmax(ti.tnorm, DBL_MIN) + 2.0 * pivmin;
   double lo = ti.lo - pad, hi = ti.hi + pad;
-  // multisection: count(lo) <= kidx < count(hi); EIG_T probes per round,
-  // probe p at lo + (hi - lo) (p + 1) / (EIG_T + 1), evaluated by thread p.
+  // multisection: count(lo) <= kidx < count(hi); EIG_VT probes per round,
+  // probe p at lo + (hi - lo) (p + 1) / (EIG_VT + 1), evaluated by thread p.
   // The bracket is narrowed to 2 eps max(|theta|, |T|): the Sturm count is
   // exact only for a matrix within about eps |T| of T, so narrower brackets of
   // small eigenvalues would not make them more accurate.
@@ -124,18 +125,18 @@ __global__ __launch_bounds__(EIG_T) void k_eig_values(const double* __restrict__
   for (int it = 0; it < 64; ++it) {
     const double wdt = hi - lo;
     if (wdt <= fmax(2.0 * DBL_EPSILON * fmax(fabs(lo), fabs(hi)) + pivmin, wstop)) break;
-    const double step = wdt / (double)(EIG_T + 1);
+    const double step = wdt / (double)(EIG_VT + 1);
     const double x = lo + step * (double)(tid + 1);
     const unsigned long long m = __ballot(sturm_count(al, b2, n, x, pivmin) > kidx);
     if (lane == 0) smask[wv] = m;
     __syncthreads();
-    int f = EIG_T;                                 // first probe with count > kidx
+    int f = EIG_VT;                                 // first probe with count > kidx
 #pragma unroll
-    for (int q = EIG_T / 64 - 1; q >= 0; --q)
+    for (int q = EIG_VT / 64 - 1; q >= 0; --q)
       if (smask[q]) f = 64 * q + __ffsll((long long)smask[q]) - 1;
     __syncthreads();
     const double nlo = (f > 0) ? lo + step * (double)f : lo;
-    const double nhi = (f < EIG_T) ? lo + step * (double)(f + 1) : hi;
+    const double nhi = (f < EIG_VT) ? lo + step * (double)(f + 1) : hi;
     if (!(nhi - nlo < wdt)) break;   // no progress (bracket at rounding level)
     lo = nlo;
     hi = nhi;
@@ -164,40 +165,114 @@ __device__ __forceinline__ void store_unit_column(const double* y, int n, int n_
 // Eigenvector of an isolated eigenvalue th of the unreduced tridiagonal T by
 // the twisted factorisation (Parlett and Dhillon): the top-down pivots dp of
 // T - th I = L D L^T and the bottom-up pivots dm of U D U^T (the Sturm
-// recurrence run from either end; lanes 0 and 1 of wave 0 side by side, each
+// recurrence run from either end by lane 0 of waves 0 and 1 side by side, each
 // pivot below pivmin in magnitude replaced by -pivmin), the twist
 // gamma_k = dp_k + dm_k - (alpha_k - th), k the index of the smallest
 // |gamma_k| (the first of equals), and z with z_k = 1 solving N_k^T z = e_k:
 // z_i = -(beta_i / dp_i) z_(i+1) below k, z_i = -(beta_(i-1) / dm_i) z_(i-1)
-// above (lanes 0 and 1 again).  Then (T - th I) z = gamma_k e_k in exact
-// arithmetic.  Accepted (true, z in y) when every entry is finite and
-// |(T - th I) z|_inf <= 64 eps |T| |z|_inf, the level inverse iteration
+// above (the two lanes again).  Then (T - th I) z = gamma_k e_k in exact
+// arithmetic, and one inverse-iteration step with the same factors,
+// x = (T - th I)^-1 z, squares the error the first solve leaves (a vector
+// from one solve is orthogonal to a neighbour's only to about eps |T| / gap).
+// Accepted (true, x / |x|_inf in y) when every entry is finite and
+// |(T - th I) x|_inf <= 64 eps |T| |x|_inf, the level inverse iteration
 // reaches; every thread of the block must call it (it contains barriers).
-// dp, dm, ratios and the scan scratch use the caller's LDS arrays.
+// dp, dm, ratios and scratch use the caller's LDS arrays.  The serial
+// recurrences take their operands from LDS TV_U steps ahead; each runs on a
+// wave of its own, so that its indices stay wave-uniform (with both on lanes
+// of one wave, the per-lane index arithmetic and masking doubled each step).
+constexpr int TV_U = 8;
+
+// one lane: s = 0 .. cnt - 1 along index idx(s), operands
+// fetched TV_U steps at a time by ld(i, ...) (the index clamped to [0, n), so
+// the surplus fetches past cnt stay in bounds), then the dependent update
+// st(i, ...) in order; mx >= cnt is the trip count
+template <class IDX, class LD, class ST>
+__device__ __forceinline__ void tv_chain(int n, int cnt, int mx, IDX idx, LD ld, ST st) {
+  n = __builtin_amdgcn_readfirstlane(n);
+  cnt = __builtin_amdgcn_readfirstlane(cnt);
+  mx = __builtin_amdgcn_readfirstlane(mx);
+  for (int s0 = 0; s0 < mx; s0 += TV_U) {
+    double o0[TV_U], o1[TV_U];
+#pragma unroll
+    for (int u = 0; u < TV_U; ++u) ld(min(max(idx(min(s0 + u, cnt - 1)), 0), n - 1), o0[u], o1[u]);
+#pragma unroll
+    for (int u = 0; u < TV_U; ++u)
+      if (s0 + u < cnt) st(idx(s0 + u), o0[u], o1[u]);
+  }
+}
+
+// One wave: x_s = A_s x_(s-1) + B_s for s = 0 .. cnt - 1 (cnt <= 256), from
+// x_(-1) = x0, as a scan of affine maps instead of cnt dependent steps: lane
+// l composes the maps of its four steps 4 l .. 4 l + 3, the lanes' maps are
+// combined in lane order by a Hillis-Steele scan (shuffles), and each lane then
+// runs its four steps from the value its predecessors leave.  ld(s, A, B)
+// gives step s's coefficients (only called for s < cnt); st(s, x) receives
+// x_s.  Every lane of the wave must call it.
+template <class LD, class ST>
+__device__ __forceinline__ void wave_affine_scan(int cnt, double x0, LD ld, ST st) {
+  const int lane = threadIdx.x & 63;
+  double A[4], B[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int s2 = 4 * lane + e;
+    A[e] = 1.0;
+    B[e] = 0.0;
+    if (s2 < cnt) ld(s2, A[e], B[e]);
+  }
+  double a = 1.0, b = 0.0;                       // the lane's map: x -> a x + b
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    b = fma(A[e], b, B[e]);
+    a = A[e] * a;
+  }
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const double pa = __shfl_up(a, off, 64), pb = __shfl_up(b, off, 64);
+    if (lane >= off) {                            // this map after the earlier lanes'
+      b = fma(a, pb, b);
+      a = a * pa;
+    }
+  }
+  // value entering the lane: the inclusive map of the lanes before, applied to x0
+  const double qa = __shfl_up(a, 1, 64), qb = __shfl_up(b, 1, 64);
+  double x = (lane == 0) ? x0 : fma(qa, x0, qb);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int s2 = 4 * lane + e;
+    if (s2 < cnt) {
+      x = fma(A[e], x, B[e]);
+      st(s2, x);
+    }
+  }
+}
+
 __device__ __forceinline__ bool twisted_vector(const double* al, const double* b1, const double* b2,
                                             int n, double th, double tnorm, double pivmin,
                                             double* dp, double* dm, double* rat, double* sc,
-                                            double* y) {
+                                            double* tw, double* y) {
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   __shared__ int kst;
   __shared__ double mred[2][EIG_T / 64];
-  if (tid < 2) {
-    const bool fw = tid == 0;
+  if (tid == 0 || tid == 64) {
+    // wave-uniform in the one active lane, so indices and branches stay scalar
+    const bool fw = __builtin_amdgcn_readfirstlane(tid) == 0;
     double* out = fw ? dp : dm;
-    int i = fw ? 0 : n - 1;
-    double d = al[i] - th;
-    if (fabs(d) < pivmin) d = -pivmin;
-    out[i] = d;
-    for (int s2 = 1; s2 < n; ++s2) {
-      i = fw ? s2 : n - 1 - s2;
-      d = (al[i] - th) - b2[fw ? i - 1 : i] * rcp_nr(d);
-      if (fabs(d) < pivmin) d = -pivmin;
-      out[i] = d;
-    }
+    double d = 0.0;
+    tv_chain(n, n, n, [&](int s2) { return fw ? s2 : n - 1 - s2; },
+             [&](int i, double& am, double& bb) {
+               am = al[i] - th;
+               bb = fw ? b2[max(i - 1, 0)] : b2[i];
+             },
+             [&](int i, double am, double bb) {
+               d = (i == (fw ? 0 : n - 1)) ? am : am - bb * rcp_nr(d);
+               if (fabs(d) < pivmin) d = -pivmin;
+               out[i] = d;
+             });
   }
   __syncthreads();
-  // |gamma_k| into sc; the ratios: rat[i] = beta_i / dp_i (i < n - 1) and
-  // sc2 = beta_(i-1) / dm_i (i > 0) kept in y for now
+  // |gamma_k| into sc; the ratios rat[i] = beta_i / dp_i (i < n - 1) and
+  // y[i] = beta_(i-1) / dm_i (i > 0)
   for (int i = tid; i < n; i += EIG_T) {
     sc[i] = fabs(dp[i] + dm[i] - (al[i] - th));
     rat[i] = (i < n - 1) ? b1[i] / dp[i] : 0.0;
@@ -224,20 +299,65 @@ __device__ __forceinline__ bool twisted_vector(const double* al, const double* b
     if (lane == 0) kst = gk;
   }
   __syncthreads();
-  const int k = kst;
-  // z into sc: lane 0 goes down from k, lane 1 up (the ratios up are in y)
-  if (tid < 2) {
-    const bool dn = tid == 0;
-    const int cnt = dn ? k : n - 1 - k, mx = max(k, n - 1 - k);
-    if (dn) sc[k] = 1.0;
-    double zc = 1.0;
-    for (int s2 = 1; s2 <= mx; ++s2) {
-      if (s2 <= cnt) {
-        const int i = dn ? k - s2 : k + s2;
-        zc = -(dn ? rat[i] : y[i]) * zc;
-        sc[i] = zc;
-      }
+  const int k = __builtin_amdgcn_readfirstlane(kst);
+  // z into sc: wave 0 goes down from k, wave 1 up (z_i = -rat_i z_(i+1) and
+  // z_i = -y_i z_(i-1), products as affine scans)
+  if (wv < 2) {
+    const bool dn = wv == 0;
+    if (dn && lane == 0) sc[k] = 1.0;
+    wave_affine_scan(dn ? k : n - 1 - k, 1.0,
+                     [&](int s2, double& A, double& Bc) {
+                       A = dn ? -rat[k - 1 - s2] : -y[k + 1 + s2];
+                       Bc = 0.0;
+                     },
+                     [&](int s2, double x) { sc[dn ? k - 1 - s2 : k + 1 + s2] = x; });
+  }
+  __syncthreads();
+  // One inverse-iteration step with the same factors, x = (T - th I)^-1 z,
+  // T - th I = N_k D_k N_k^T (N_k unit, l_i = rat[i] below the diagonal above
+  // row k, u_i = y[i + 1] above it below row k; D_k = dp above k, gamma_k at
+  // k, dm below): N_k t = z from either end towards k (the two lanes), then
+  // t_k and t / D_k, then N_k^T x = t outwards from k.  Skipped when gamma_k
+  // is below pivmin (z is then exact to working precision).
+  const double gk = dp[k] + dm[k] - (al[k] - th);
+  const bool refine = fabs(gk) >= pivmin;         // the same in every thread
+  if (refine && wv < 2) {
+    const bool dn = wv == 0;                      // wave 0: rows 0 .. k - 1, wave 1: n - 1 .. k + 1
+    wave_affine_scan(dn ? k : n - 1 - k, 0.0,
+                     [&](int s2, double& A, double& Bc) {
+                       const int i = dn ? s2 : n - 1 - s2;
+                       A = dn ? (i > 0 ? -rat[i - 1] : 0.0) : (i < n - 1 ? -y[i + 1] : 0.0);
+                       Bc = sc[i];
+                     },
+                     [&](int s2, double x) { tw[dn ? s2 : n - 1 - s2] = x; });
+  }
+  __syncthreads();
+  for (int i = tid; i < n && refine; i += EIG_T) {
+    double t = tw[i], d;
+    if (i < k) {
+      d = dp[i];
+    } else if (i > k) {
+      d = dm[i];
+    } else {
+      t = sc[k];
+      if (k > 0) t = fma(-rat[k - 1], tw[k - 1], t);
+      if (k < n - 1) t = fma(-y[k + 1], tw[k + 1], t);
+      d = gk;
     }
+    dp[i] = t / d;                              // each thread rewrites only its own dp[i]
+  }
+  __syncthreads();
+  if (refine && wv < 2) {
+    const bool dn = wv == 0;
+    const double xk = dp[k];
+    if (dn && lane == 0) sc[k] = xk;
+    wave_affine_scan(dn ? k : n - 1 - k, xk,
+                     [&](int s2, double& A, double& Bc) {
+                       const int i = dn ? k - 1 - s2 : k + 1 + s2;
+                       A = dn ? -rat[i] : -y[i];
+                       Bc = dp[i];
+                     },
+                     [&](int s2, double x) { sc[dn ? k - 1 - s2 : k + 1 + s2] = x; });
   }
   __syncthreads();
   // residual and size (block maxima), finiteness
@@ -306,7 +426,7 @@ __global__ __launch_bounds__(EIG_T) void k_eig_vectors(const double* __restrict_
     const bool rgap = c + 1 == r || theta[(int64_t)a * r + c + 1] - th > ctol;
     if (lgap && rgap &&
         twisted_vector(al, b1, b2, n, th, ti.tnorm, DBL_MIN * fmax(1.0, ti.bmax), fd, fl, fu1,
-                       fu2, y)) {
+                       fu2, w, y)) {
       if (wv == 0) store_unit_column(y, n, n_it, r, c, Sa);
       return;
     }
@@ -800,7 +920,7 @@ hipError_t launch_eigh_ritz(const double* alpha, const double* beta, const int* 
                             int ldq, double* Z, int n_cu, hipStream_t s) {
   (void)hipGetLastError();
   if (n_it > EIG_NMAX || r > n_it || r > 128 || r < 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_eig_values, dim3(r, n_act), dim3(EIG_T), 0, s, alpha, beta, neff, n_it, r,
+  hipLaunchKernelGGL(k_eig_values, dim3(r, n_act), dim3(EIG_VT), 0, s, alpha, beta, neff, n_it, r,
                      theta);
   hipLaunchKernelGGL(k_eig_vectors, dim3(r, n_act), dim3(EIG_T), 0, s, alpha, beta, neff, n_it,
                      r, theta, Seig);
