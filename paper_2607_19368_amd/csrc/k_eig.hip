@@ -3,8 +3,8 @@
 //
 // Eigenvalues: one 256-thread workgroup per kept eigenvalue isolates it by
 // Sturm-count multisection (256 probe points per round, one per thread; the
-// count of negative pivots of T - x I is the number of eigenvalues below x)
-// until the bracket is a few ulps wide.
+// sign changes along the leading principal minors of T - x I count the
+// eigenvalues below x) until the bracket is a few ulps wide.
 // Eigenvectors: one workgroup per kept eigenvalue.  Eigenvalues more than
 // EIG_TWIST_GAP |T| from their kept neighbours take the twisted factorisation
 // (twisted_vector: two pivot recurrences and two product recurrences, no
@@ -39,18 +39,80 @@ __device__ __forceinline__ double rcp_nr(double d) {
   return fma(r, fma(-d, r, 1.0), r);
 }
 
-// Number of eigenvalues of T below x: negative pivots of the LDL^T factorisation
-// of T - x I (Sturm count), pivots below pivmin in magnitude replaced by -pivmin.
-__device__ __forceinline__ int sturm_count(const double* al, const double* b2, int n, double x,
-                                           double pivmin) {
-  double d = al[0] - x;
-  if (fabs(d) < pivmin) d = -pivmin;
-  int cnt = d < 0.0;
-#pragma unroll 4
-  for (int i = 1; i < n; ++i) {
-    d = (al[i] - x) - b2[i - 1] * rcp_nr(d);
-    if (fabs(d) < pivmin) d = -pivmin;
-    cnt += d < 0.0;
+// Number of eigenvalues of T below x: the sign changes along the leading
+// principal minors q_k = det(T_k - x I) (Sturm sequence), from q_(-1) = 0,
+// q_0 = 1 and q_(k+1) = (alpha_k - x) q_k - beta_(k-1)^2 q_(k-1); a change at
+// k is a negative pivot q_k / q_(k-1) of the LDL^T factorisation of T - x I.
+// Each step's rounding errors are those of the pivot recurrence (a relative
+// error on alpha_k - x and on the beta^2 term), but no division is needed.
+// The caller scales T and x by a power of two so that |T| <= 1 (an exact
+// scaling), stores an[k] = alpha_k and b2s[k] = beta_(k-1)^2 raised to at
+// least EIG_B2MIN (b2s[0] unused), so that two consecutive minors never both
+// vanish, and gives both arrays 8 entries beyond n rounded down to a multiple
+// of 8.  The pair (q_k, q_(k-1)) is rescaled by a power of two every 8 steps:
+// in 8 steps it grows at most 3^8 times and shrinks at most (EIG_B2MIN / 3)^8,
+// far from overflow and underflow (raising beta^2 to EIG_B2MIN moves no
+// eigenvalue by more than 2^-53 |T|).  A change is a difference of sign bits:
+// each step shifts the sign of q_k into a mask, and every 8 steps the
+// differences of neighbouring bits are counted.  An exact zero q_k needs no
+// rule of its own: its neighbours q_(k-1) and q_(k+1) = -beta_(k-1)^2 q_(k-1)
+// have opposite signs, so the pair of steps counts one change whatever the
+// zero's sign bit (the pivot form counts a zero pivot as negative and the
+// next one, of the same pair, as positive).
+#define EIG_B2MIN 0x1p-110
+__device__ __forceinline__ void minors_step(double a, double b2, double xn, double& pm, double& pc,
+                                            uint32_t& sg) {
+  const double pn = fma(a - xn, pc, -(b2 * pm));
+  sg = __builtin_amdgcn_alignbit(sg, f64_hi(pn), 31);   // (sg << 1) | sign bit of q
+  pm = pc;
+  pc = pn;
+}
+// cnt8 <= 8 steps from operands A (alpha) and B (beta^2), 2 per double2
+__device__ __forceinline__ void minors_8(const double2 (&A)[4], const double2 (&B)[4], int cnt8,
+                                         double xn, double& pm, double& pc, uint32_t& sg,
+                                         int& cnt) {
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    if (2 * u < cnt8) minors_step(A[u].x, B[u].x, xn, pm, pc, sg);
+    if (2 * u + 1 < cnt8) minors_step(A[u].y, B[u].y, xn, pm, pc, sg);
+  }
+  cnt += __builtin_popcount((sg ^ (sg >> 1)) & ((1u << cnt8) - 1u));
+  const int e = __builtin_amdgcn_frexp_exp(fmax(fabs(pc), fabs(pm)));
+  pc = __builtin_amdgcn_ldexp(pc, -e);
+  pm = __builtin_amdgcn_ldexp(pm, -e);
+}
+__device__ __forceinline__ void minors_load(const double2* a2, const double2* c2, int q,
+                                            double2 (&A)[4], double2 (&B)[4]) {
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    A[u] = a2[4 * q + u];
+    B[u] = c2[4 * q + u];
+  }
+}
+__device__ __forceinline__ int sturm_count(const double* an, const double* b2s, int n, double xn) {
+  double pm = 0.0, pc = 1.0;
+  uint32_t sg = 0;   // sign bits, newest lowest; q_0 = 1 > 0
+  int cnt = 0;
+  const int n8 = __builtin_amdgcn_readfirstlane(n >> 3), rem = __builtin_amdgcn_readfirstlane(n & 7);
+  const double2* a2 = reinterpret_cast<const double2*>(an);
+  const double2* c2 = reinterpret_cast<const double2*>(b2s);
+  // two operand buffers in turn: the next 8 steps' operands are read while
+  // these 8 run
+  double2 A0[4], B0[4], A1[4], B1[4];
+  minors_load(a2, c2, 0, A0, B0);
+  int q = 0;
+  for (; q + 2 <= n8; q += 2) {
+    minors_load(a2, c2, q + 1, A1, B1);
+    minors_8(A0, B0, 8, xn, pm, pc, sg, cnt);
+    minors_load(a2, c2, q + 2, A0, B0);
+    minors_8(A1, B1, 8, xn, pm, pc, sg, cnt);
+  }
+  if (q < n8) {   // one full group left, then the remainder from the next
+    minors_load(a2, c2, q + 1, A1, B1);
+    minors_8(A0, B0, 8, xn, pm, pc, sg, cnt);
+    minors_8(A1, B1, rem, xn, pm, pc, sg, cnt);
+  } else {
+    minors_8(A0, B0, rem, xn, pm, pc, sg, cnt);
   }
   return cnt;
 }
@@ -111,9 +173,18 @@ __global__ __launch_bounds__(EIG_VT) void k_eig_values(const double* __restrict_
   }
   const int kidx = n - r + c;   // ascending index of the wanted eigenvalue
   __shared__ double al[EIG_NMAX], b1[EIG_NMAX], b2[EIG_NMAX];
+  __shared__ __align__(16) double an[EIG_NMAX + 8], b2s[EIG_NMAX + 8];
   __shared__ unsigned long long smask[EIG_VT / 64];
   const TriInfo ti = load_tridiag(alpha + (int64_t)a * n_it, beta + (int64_t)a * n_it, n, al, b1, b2);
   const double pivmin = DBL_MIN * fmax(1.0, ti.bmax);
+  // T / 2^esc with |T| / 2^esc < 1, the operands of the minors recurrence
+  const int esc = (ti.tnorm > 0.0) ? __builtin_amdgcn_frexp_exp(ti.tnorm) : 0;
+  for (int k = tid; k < n; k += EIG_VT) {
+    an[k] = __builtin_amdgcn_ldexp(al[k], -esc);
+    const double bs = (k > 0) ? __builtin_amdgcn_ldexp(b1[k - 1], -esc) : 0.0;
+    b2s[k] = fmax(bs * bs, EIG_B2MIN);
+  }
+  __syncthreads();
   const double pad = 2.0 * DBL_EPSILON * fmax(ti.tnorm, DBL_MIN) + 2.0 * pivmin;
   double lo = ti.lo - pad, hi = ti.hi + pad;
   // multisection: count(lo) <= kidx < count(hi); EIG_VT probes per round,
@@ -127,7 +198,8 @@ __global__ __launch_bounds__(EIG_VT) void k_eig_values(const double* __restrict_
     if (wdt <= fmax(2.0 * DBL_EPSILON * fmax(fabs(lo), fabs(hi)) + pivmin, wstop)) break;
     const double step = wdt / (double)(EIG_VT + 1);
     const double x = lo + step * (double)(tid + 1);
-    const unsigned long long m = __ballot(sturm_count(al, b2, n, x, pivmin) > kidx);
+    const unsigned long long m =
+        __ballot(sturm_count(an, b2s, n, __builtin_amdgcn_ldexp(x, -esc)) > kidx);
     if (lane == 0) smask[wv] = m;
     __syncthreads();
     int f = EIG_VT;                                 // first probe with count > kidx
