@@ -112,6 +112,14 @@ typedef struct slh_ctx slh_ctx;
                                     explicit L x L operator Phi_w Phi_w^T (the same
                                     operator and recurrence; section 3.5 local
                                     backend); 0: the general path for every L          */
+#define SLH_OPT_RESIDENT      11 /* 1 (default): a single window whose Phi fits in the
+                                    register files (m of 1024 or 2048, at most 32
+                                    rows per compute unit, n_it <= 256) runs the
+                                    whole Lanczos loop of Algorithm 2 as one
+                                    persistent kernel that holds its rows of Phi in
+                                    registers (the same recurrence; partial sums in
+                                    a different grouping); 0: one pass over Phi per
+                                    step for every shape                             */
 
 /*
  * Random parameters of the method, drawn from `seed` with Philox4x32-10
@@ -281,9 +289,12 @@ int slh_eigh_ritz(slh_ctx *ctx, int32_t n_it, double *ritz_out, int32_t *iters_o
  * Stage timings of the most recent calls, from HIP events on the context
  * stream (requires SLH_OPT_TIMING = 1 before those calls).  Fills up to n of:
  *   [0] feature map ms        [1] Lanczos loop ms (all steps, all windows)
- *   [2] sum of Phi-pass ms     [3] number of Phi passes timed (1 per step)
+ *   [2] sum of Phi-pass ms     [3] number of Lanczos steps those passes cover
+ *   (the resident kernel of SLH_OPT_RESIDENT is timed as one pass covering all
+ *   n_it steps)
  *   [4] eigensolve + Ritz ms  [5] SimHash ms   [6] merge ms
  *   [7] row normalisation ms (SLH_OPT_NORMALIZE = 1, else 0)
+ *   [8] 1 when the last slh_lanczos ran the resident kernel (SLH_OPT_RESIDENT)
  * Synchronises the stream.
  */
 int slh_stage_times(slh_ctx *ctx, double *ms_out, int32_t n);
@@ -299,8 +310,13 @@ int slh_stage_times(slh_ctx *ctx, double *ms_out, int32_t n);
  * between graph nodes are included.  The replays write their row vectors to
  * scratch and record no step state: they rewrite only the step's partial sums,
  * never Q, alpha, beta, the Ritz pairs or codes; windows that broke down early
- * skip their passes as in the loop itself.  reps in [1, 4096].  Synchronises the
- * stream.  SLH_ESTATE before slh_lanczos or after a short-window
+ * skip their passes as in the loop itself.  After a run of the resident kernel
+ * (SLH_OPT_RESIDENT) the call instead launches that run reps times, each
+ * kernel between two events (its start kernel and buffer clears outside
+ * them), and us_out is the kernel's mean duration over the runs after the
+ * first, divided by n_it (per Lanczos step); those runs recompute the whole
+ * Lanczos loop and rewrite Q, alpha and beta with the same values.  reps in
+ * [1, 4096].  Synchronises the stream.  SLH_ESTATE before slh_lanczos or after a short-window
  * (single-wavefront) Lanczos run, which has no passes.
  */
 int slh_time_passes(slh_ctx *ctx, int32_t reps, double *us_out);

@@ -21,6 +21,7 @@ SOURCES = [
     "k_prep.hip",
     "k_featmap.hip",
     "k_lanczos.hip",
+    "k_lzres.hip",
     "k_eig.hip",
     "k_local.hip",
     "k_norm.hip",

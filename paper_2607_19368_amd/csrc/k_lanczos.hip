@@ -31,24 +31,6 @@
 
 namespace slh {
 
-// Sum 8 values over the 64 lanes of a wave without LDS round trips: four
-// 32-lane trades (v_permlane32_swap), two 16-lane trades (v_permlane16_swap),
-// an 8-lane exchange (DPP row_ror:8), then a sum over each 8-lane group.  On
-// return lane l holds the full sum of value index ((l>>5)&1)*4 + ((l>>4)&1)*2 +
-// ((l>>3)&1).  Every lane of the wave must be active.
-__device__ __forceinline__ double wave_sum8_f64(const double (&v)[8]) {
-  const int lane = threadIdx.x & 63;
-  double w[4];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) w[e] = swap32_add(v[e], v[e + 4]);
-  double x[2];
-#pragma unroll
-  for (int e = 0; e < 2; ++e) x[e] = swap16_add(w[e], w[e + 2]);
-  const bool b8 = lane & 8;
-  const double y = (b8 ? x[1] : x[0]) + dpp_f64<DPP_ROR8>(b8 ? x[0] : x[1]);
-  return oct_sum_f64(y);
-}
-
 // The same over each 16-lane quarter (DPP only): lane l holds the quarter sum
 // of value index ((l>>3)&1)*4 + ((l>>2)&1)*2 + ((l>>1)&1).  The 4-lane step
 // pairs lane i with 7 - i of its 8-lane group (row_half_mirror), which, like
@@ -769,6 +751,11 @@ static void launch_reduce(const LanczosWS& w, int j, hipStream_t s) {
   else if (w.G3 >= 16) hipLaunchKernelGGL(k_lz_reduce<32>, dim3(nx + w.m / 32, w.n_act), dim3(512), 0, s, w, j);
   else if (w.G3 >= 8) hipLaunchKernelGGL(k_lz_reduce<64>, dim3(nx + w.m / 64, w.n_act), dim3(512), 0, s, w, j);
   else hipLaunchKernelGGL(k_lz_reduce<128>, dim3(nx + w.m / 128, w.n_act), dim3(512), 0, s, w, j);
+}
+
+hipError_t launch_lanczos_start(const LanczosWS& w, const double* q1_act, hipStream_t s) {
+  hipLaunchKernelGGL(k_lz_start, dim3((w.L + 255) / 256, w.n_act), dim3(256), 0, s, w, q1_act);
+  return hipGetLastError();
 }
 
 hipError_t launch_lanczos(const LanczosWS& w, const double* q1_act, hipStream_t s,

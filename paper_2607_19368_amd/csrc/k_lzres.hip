@@ -1,0 +1,523 @@
+// Implicit Lanczos with full re-orthogonalization (Algorithm 2; operator of
+// Eq. 4, A v = Phi (Phi^T v)) for one window whose Phi fits in the register
+// files of the device, as one persistent kernel for the whole run.
+//
+// Block b of nb (one per compute unit) holds rows [RB b, RB b + RB) of Phi in
+// registers for the whole run, loaded once, and its rows of the basis Q in
+// LDS.  Each step is the same computation as the pass and the reduction of
+// the streaming path (k_lz_step, k_lz_reduce: q_j by the second Gram-Schmidt
+// pass of step j-1 in row space, u = A q_j from the row dots with t~ and the
+// Lanczos relation, z1 by the three-term recurrence, then t~ = Phi^T z1 / |z1|
+// and h2 = Q_j^T z1), in two phases:
+//   rows     every block: its rows of q_j and z1, and its partials of Phi^T z1,
+//            of h2 and of |z1|^2;
+//   columns  block b: t~ over its m / nb columns and the partial of |t~|^2;
+//            h2 entries b, b + nb, ...; |z1|^2 (every block).
+// The scalars of a step (alpha, beta, the breakdown test) are computed by
+// every block from the same reduced values in the same order, so all blocks
+// agree and leave the loop together.  Results are bitwise reproducible.
+//
+// The blocks synchronise only through the data they exchange, with no
+// barrier: every value passed between blocks is written with an agent-scope
+// atomic store (coherent across the device's L2 caches) carrying its step in
+// its two lowest mantissa bits (1 + (step & 1); a perturbation of at most
+// 3 ulp, the same for every reader), and a reader polls each value it needs
+// until the tag is that of the step it waits for.  The buffers are zeroed
+// (tag 0, never valid) before the launch; every slot in use is rewritten at
+// every step, and no block can rewrite a slot of step e + 1 before every
+// reader has consumed step e's value (it first needs values that those
+// readers produce after reading), so the two tags suffice.  Every wait is
+// bounded: after LR_SPIN polls a block sets an error word and leaves, and the
+// others, seeing it, leave too.  The host launches the kernel only when all
+// nb blocks are resident at once (one per compute unit; checked with the
+// occupancy calculator).
+#include "slh_device.h"
+#include "slh_internal.h"
+
+namespace slh {
+
+namespace {
+
+constexpr int LR_T = 256;          // threads per block: 4 waves, one per SIMD
+constexpr int LR_SPIN = 1 << 20;   // polls before a barrier gives up
+
+__device__ __forceinline__ void st_flag(unsigned* p, unsigned v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned ld_flag(unsigned* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// bar: [LR_ERR] error word
+constexpr int LR_ERR = LZ_BAR_ERR;
+
+// v tagged with step e into *p
+__device__ __forceinline__ void st_tag(double* p, double v, int e) {
+  const long long x = (__double_as_longlong(v) & ~3LL) | (long long)(1 + (e & 1));
+  __hip_atomic_store((long long*)p, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// two tagged values into p[0..1] (16-byte aligned) with one coherent 16-byte
+// store; each half carries its own tag, so the store need not be atomic as a whole
+__device__ __forceinline__ void st_tag2(double* p, double v0, double v1, int e) {
+  typedef long long ll2 __attribute__((ext_vector_type(2)));
+  ll2 x;
+  x.x = (__double_as_longlong(v0) & ~3LL) | (long long)(1 + (e & 1));
+  x.y = (__double_as_longlong(v1) & ~3LL) | (long long)(1 + (e & 1));
+  // s_nop: a VALU write to the data registers of a store wider than 8 bytes
+  // must not follow it directly (the compiler adds this wait state only to
+  // stores of its own)
+  asm volatile("global_store_dwordx4 %0, %1, off sc1\n\ts_nop 1" : : "v"(p), "v"(x) : "memory");
+}
+__device__ __forceinline__ long long ld_raw(double* p) {
+  return __hip_atomic_load((long long*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ bool tag_is(long long x, int e) { return (int)(x & 3) == 1 + (e & 1); }
+
+// v[u] = *addr(u) of step e for the u with bit u of act set (0 for the others),
+// polling until every tag matches; false after LR_SPIN polls or when the error
+// word is set (the error word is then set)
+template <int N, class ADDR>
+__device__ __forceinline__ bool ld_wait(ADDR addr, unsigned act, int e, unsigned* bar,
+                                        double (&v)[N]) {
+  long long x[N];
+#pragma unroll
+  for (int u = 0; u < N; ++u) x[u] = ((act >> u) & 1) ? ld_raw(addr(u)) : 0;
+  bool ok = true;
+  for (int s = 0;; ++s) {
+    bool all = true;
+#pragma unroll
+    for (int u = 0; u < N; ++u) all = all && (((act >> u) & 1) == 0 || tag_is(x[u], e));
+    if (all) break;
+    if (s > LR_SPIN || ((s & 63) == 63 && ld_flag(bar + LR_ERR) != 0)) {
+      st_flag(bar + LR_ERR, 1u);
+      ok = false;
+      break;
+    }
+#pragma unroll
+    for (int u = 0; u < N; ++u)
+      if (((act >> u) & 1) && !tag_is(x[u], e)) x[u] = ld_raw(addr(u));
+  }
+#pragma unroll
+  for (int u = 0; u < N; ++u) v[u] = ((act >> u) & 1) ? __longlong_as_double(x[u]) : 0.0;
+  return ok;
+}
+
+// true in every thread when no thread of the block saw a failure (a barrier)
+__device__ __forceinline__ bool block_ok(bool ok) {
+  __shared__ int bad;
+  if (threadIdx.x == 0) bad = 0;
+  __syncthreads();
+  if (!ok) bad = 1;
+  __syncthreads();
+  return bad == 0;
+}
+
+// The float4 of one Phi row as an opaque value at its point of use, so that its
+// conversion to fp64 is not hoisted (the converted rows would need twice the
+// registers).
+__device__ __forceinline__ float4 pin4(float4 x) {
+  asm volatile("" : "+v"(x.x), "+v"(x.y), "+v"(x.z), "+v"(x.w));
+  return x;
+}
+
+// three block sums at once (fixed order: wave sums, then the 4 waves in order)
+__device__ __forceinline__ void block_sum3(double& a, double& b, double& c, double (*red)[4]) {
+  a = wave_sum_f64(a);
+  b = wave_sum_f64(b);
+  c = wave_sum_f64(c);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) {
+    red[0][threadIdx.x >> 6] = a;
+    red[1][threadIdx.x >> 6] = b;
+    red[2][threadIdx.x >> 6] = c;
+  }
+  __syncthreads();
+  a = ((red[0][0] + red[0][1]) + red[0][2]) + red[0][3];
+  b = ((red[1][0] + red[1][1]) + red[1][2]) + red[1][3];
+  c = ((red[2][0] + red[2][1]) + red[2][2]) + red[2][3];
+}
+
+}  // namespace
+
+// RB rows per block; CPL = m / 256 columns per lane (the lane's columns are
+// 64 CPL w + 256 h + 4 lane + e for wave w, h < CPL / 4, e < 4).
+// Workspace use: Spart [m / CB][nb][CB] (CB = m / nb), H2part [nb][ldq + 1], H2 [ldq + 1], T [m],
+// Apart [nb]; outputs alpha, beta, neff, stop and Q[1..] as the streaming path.
+// Dynamic LDS: the block's rows of Q, (n_it + 1) (RB + 1) doubles.
+template <int RB, int CPL>
+__global__ __launch_bounds__(LR_T, 1) void k_lz_resident(LanczosWS w, unsigned* bar,
+                                                         const double* __restrict__ q1) {
+  constexpr int NH = CPL / 4, KG = LR_T / RB, QS = RB + 1;   // QS: row stride of Qs (bank spread)
+  static_assert(CPL % 4 == 0 && RB % 8 == 0 && LR_T % RB == 0, "shape");
+  const int b = blockIdx.x, nb = gridDim.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int L = w.L, m = w.m, n_it = w.n_it, ldq = w.ldq, hs = ldq + 1;
+  const int r0 = b * RB;
+  const int cb = wv * 64 * CPL + 4 * lane;
+  extern __shared__ double Qs[];                 // [n_it + 1][QS]
+  __shared__ double h2s[256], gs[256], als[256], bes[256];
+  __shared__ double prw[4][RB];
+  __shared__ double zs[RB], qr[RB], qmr[RB], sgr[RB];
+  __shared__ double rq[KG][RB + 1], rg[KG][RB + 1];
+  __shared__ double red[3][4];
+  __shared__ double cpart[LR_T];
+  double* Spart = w.Spart;
+  double* Hpart = w.H2part;
+  double* H2 = w.H2;
+  double* Tv = w.T;
+  double* Ap = w.Apart;
+
+  // the block's rows of Phi (rows past L are zero) and of q_0
+  float4 ph[RB][NH];
+#pragma unroll
+  for (int r = 0; r < RB; ++r) {
+    const int row = min(r0 + r, L - 1);
+#pragma unroll
+    for (int h = 0; h < NH; ++h) ph[r][h] = *(const float4*)(w.Phi + (int64_t)row * m + cb + 256 * h);
+  }
+  if (r0 + RB > L) {
+#pragma unroll
+    for (int r = 0; r < RB; ++r)
+      if (r0 + r >= L) {
+#pragma unroll
+        for (int h = 0; h < NH; ++h) ph[r][h] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+  }
+  if (tid < RB) {
+    const double q = (r0 + tid < L) ? q1[r0 + tid] : 0.0;
+    Qs[tid] = q;
+    zs[tid] = q;
+  }
+  __syncthreads();
+
+  // partials of Phi^T zs over the block's rows, tagged with step e
+  auto col_partials = [&](int e) {
+    double col[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) col[c] = 0.0;
+#pragma unroll
+    for (int r = 0; r < RB; ++r) {
+      const double z = zs[r];
+#pragma unroll
+      for (int h = 0; h < NH; ++h) {
+        const float4 x = pin4(ph[r][h]);
+        col[4 * h + 0] = fma((double)x.x, z, col[4 * h + 0]);
+        col[4 * h + 1] = fma((double)x.y, z, col[4 * h + 1]);
+        col[4 * h + 2] = fma((double)x.z, z, col[4 * h + 2]);
+        col[4 * h + 3] = fma((double)x.w, z, col[4 * h + 3]);
+      }
+    }
+    // column c of block b at ((c / CB) nb + b) CB + c % CB: the partials a block
+    // reduces are contiguous (CB = m / nb, a multiple of 4)
+    const int CB = m / nb;
+#pragma unroll
+    for (int h = 0; h < NH; ++h) {
+      const int c = cb + 256 * h;
+      double* dst = Spart + ((int64_t)(c / CB) * nb + b) * CB + c % CB;
+#pragma unroll
+      for (int q = 0; q < 4; q += 2) st_tag2(dst + q, col[4 * h + q], col[4 * h + q + 1], e);
+    }
+  };
+  // t over the block's columns from the partials of step e (scaled by 1 / |z1|
+  // when norm, |z1|^2 summed here from its partials first), and the block's
+  // partial of |t|^2, tagged with step e.  Thread = (column cl < CB, partial
+  // lane pl < PL); the nb / PL = CPL partials of a lane and the |z1|^2 partial
+  // are polled together.  false when a wait failed.
+  auto col_reduce = [&](bool norm, double& z2v, int e) -> bool {
+    const int CB = m / nb, PL = LR_T / CB;
+    const int c = b * CB + tid % CB;
+    const int64_t base = (int64_t)b * nb * CB + tid;
+    double v[CPL], zv[1];
+    bool ok = ld_wait<CPL>([&](int u) { return Spart + base + u * LR_T; }, (1u << CPL) - 1u, e, bar, v);
+    if (norm)
+      ok = ld_wait<1>([&](int) { return Hpart + (int64_t)tid * hs + ldq; }, tid < nb ? 1u : 0u, e,
+                      bar, zv) && ok;
+    if (!block_ok(ok)) return false;
+    if (norm) {
+      double d1 = 0.0, d2 = 0.0;
+      block_sum3(zv[0], d1, d2, red);
+      z2v = zv[0];
+    }
+    double sm = 0.0;
+#pragma unroll
+    for (int u = 0; u < CPL; ++u) sm += v[u];
+    cpart[tid] = sm;
+    __syncthreads();
+    if (tid < CB) {
+      double S = 0.0;
+#pragma unroll 8
+      for (int p = 0; p < PL; ++p) S += cpart[p * CB + tid];
+      const double t = norm ? (z2v > 0.0 ? S / sqrt(z2v) : 0.0) : S;
+      st_tag(Tv + c, t, e);
+      cpart[tid] = t * t;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      double a2 = 0.0;
+      for (int q = 0; q < CB; ++q) a2 += cpart[q];
+      st_tag(Ap + b, a2, e);
+    }
+    return true;
+  };
+  // sum over the blocks of the h2 partial k (or |z1|^2 for k = ldq) of step e
+  auto hpart_sum = [&](int k, int e, double& out) -> bool {
+    double hv[1];
+    const bool ok = ld_wait<1>([&](int) { return Hpart + (int64_t)tid * hs + k; }, tid < nb ? 1u : 0u,
+                               e, bar, hv);
+    if (!block_ok(ok)) return false;
+    double d1 = 0.0, d2 = 0.0;
+    block_sum3(hv[0], d1, d2, red);
+    out = hv[0];
+    return true;
+  };
+
+  // t_0 = Phi^T q_0 and its |t_0|^2 partials: step 0 of the tags
+  col_partials(0);
+  double z2 = 0.0;
+  if (!col_reduce(false, z2, 0)) return;
+
+  double amax = 0.0;
+  const int idx = ((lane >> 5) & 1) * 4 + ((lane >> 4) & 1) * 2 + ((lane >> 3) & 1);
+  for (int j = 0; j < n_it; ++j) {
+    // ---- rows: the reduced values of the previous step (tags of step j),
+    // those of this step tagged j + 1
+    double tv[CPL], a1[1], h1[1];
+    bool ok = ld_wait<CPL>([&](int u) { return Tv + cb + 256 * (u >> 2) + (u & 3); }, (1u << CPL) - 1u,
+                           j, bar, tv);
+    ok = ld_wait<1>([&](int) { return Ap + tid; }, tid < nb ? 1u : 0u, j, bar, a1) && ok;
+    ok = ld_wait<1>([&](int) { return H2 + tid; }, tid < j ? 1u : 0u, j, bar, h1) && ok;
+    if (!block_ok(ok)) return;
+    const double apv = a1[0], h2v = h1[0];
+    if (tid < j) h2s[tid] = h2v;
+    __syncthreads();
+    // g = T_{j-1} h2 (alpha_k on the diagonal, beta_k beside it; beta_{j-1} is
+    // not part of T_{j-1}); alpha~ = |t~|^2, |h2|^2 and h2^T g
+    double gi = 0.0;
+    if (tid < j) {
+      gi = als[tid] * h2v;
+      if (tid > 0) gi = fma(bes[tid - 1], h2s[tid - 1], gi);
+      if (tid + 1 < j) gi = fma(bes[tid], h2s[tid + 1], gi);
+      gs[tid] = gi;
+    }
+    double alpha_t = apv, hh = h2v * h2v, hth = h2v * gi;
+    block_sum3(alpha_t, hh, hth, red);
+    double alpha = alpha_t, beta = 0.0, h2last = 0.0;
+    if (j > 0) {
+      const double b2 = z2 - hh;
+      beta = b2 > 0.0 ? sqrt(b2) : 0.0;
+      if (!(beta > w.tol * amax)) {             // breakdown: n_eff stays j
+        if (b == 0 && tid == 0) {
+          w.beta[j - 1] = beta;
+          w.stop[0] = 1;
+        }
+        return;
+      }
+      h2last = h2s[j - 1];
+      alpha = (z2 * alpha_t - hth) / (beta * beta) - 2.0 * h2last;
+    }
+    amax = fmax(amax, fabs(alpha));
+    if (tid == 0) {
+      als[j] = alpha;
+      if (j > 0) bes[j - 1] = beta;
+      if (b == 0) {
+        if (j > 0) w.beta[j - 1] = beta;
+        w.alpha[j] = alpha;
+        w.neff[0] = j + 1;
+      }
+    }
+    // Q_{j-1} h2 and Q_{j-1} g of each row: thread = (row i, k-group kg)
+    {
+      const int i = tid % RB, kg = tid / RB;
+      double aq = 0.0, ag = 0.0;
+      for (int k = kg; k < j; k += KG) {
+        const double qk = Qs[k * QS + i];
+        aq = fma(qk, h2s[k], aq);
+        ag = fma(qk, gs[k], ag);
+      }
+      rq[kg][i] = aq;
+      rg[kg][i] = ag;
+    }
+    __syncthreads();
+    if (tid < RB) {
+      const int i = tid, row = r0 + i;
+      double sub = 0.0, sg = 0.0;
+      for (int q = 0; q < KG; ++q) {
+        sub += rq[q][i];
+        sg += rg[q][i];
+      }
+      double q = Qs[i], qm = 0.0;                 // j = 0: q_0
+      if (j > 0) {
+        q = (row < L) ? (zs[i] - sub) / beta : 0.0;
+        qm = Qs[(j - 1) * QS + i];
+        Qs[j * QS + i] = q;
+        if (row < L) w.Q[(int64_t)j * L + row] = q;
+      }
+      qr[i] = q;
+      qmr[i] = qm;
+      sgr[i] = sg;
+    }
+    // Phi t~ of the block's rows: 4 CPL products per lane and row, summed over
+    // the wave 8 rows at a time, then over the 4 waves
+#pragma unroll
+    for (int r8 = 0; r8 < RB; r8 += 8) {
+      double d[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        double x = 0.0;
+#pragma unroll
+        for (int h = 0; h < NH; ++h) {
+          const float4 y = pin4(ph[r8 + e][h]);
+          x = fma((double)y.x, tv[4 * h + 0], x);
+          x = fma((double)y.y, tv[4 * h + 1], x);
+          x = fma((double)y.z, tv[4 * h + 2], x);
+          x = fma((double)y.w, tv[4 * h + 3], x);
+        }
+        d[e] = x;
+      }
+      const double tot = wave_sum8_f64(d);
+      if ((lane & 7) == 0) prw[wv][r8 + idx] = tot;
+    }
+    __syncthreads();
+    if (tid < RB) {
+      const int i = tid;
+      double u = ((prw[0][i] + prw[1][i]) + prw[2][i]) + prw[3][i];
+      const double q = qr[i];
+      if (j > 0) u = (fma(sqrt(z2), u, -sgr[i]) - beta * h2last * q) / beta;
+      const double z = (u - alpha * q) - beta * qmr[i];
+      zs[i] = (r0 + i < L) ? z : 0.0;
+    }
+    __syncthreads();
+    // partials of Phi^T z1, of h2 = Q_j^T z1 (k <= j) and of |z1|^2
+    col_partials(j + 1);
+    for (int k = tid; k <= j + 1; k += LR_T) {
+      double v = 0.0;
+      double a4[4] = {0.0, 0.0, 0.0, 0.0};
+      const double* qk = (k <= j) ? Qs + k * QS : zs;
+#pragma unroll
+      for (int i = 0; i < RB; ++i) a4[i & 3] = fma(qk[i], zs[i], a4[i & 3]);
+      v = (a4[0] + a4[1]) + (a4[2] + a4[3]);
+      st_tag(Hpart + (int64_t)b * hs + (k <= j ? k : ldq), v, j + 1);
+    }
+    // ---- columns: |z1|^2 (every block), t~_{j+1}, h2
+    if (j + 1 < n_it) {
+      if (!col_reduce(true, z2, j + 1)) return;
+    } else {
+      if (!hpart_sum(ldq, j + 1, z2)) return;
+    }
+    for (int k = b; k <= j; k += nb) {
+      double v = 0.0;
+      if (!hpart_sum(k, j + 1, v)) return;
+      if (tid == 0) st_tag(H2 + k, v, j + 1);
+    }
+  }
+  // beta of the last step (reported; T does not use it)
+  if (b == 0) {
+    double hv[1];
+    const bool ok = ld_wait<1>([&](int) { return H2 + tid; }, tid < n_it ? 1u : 0u, n_it, bar, hv);
+    if (!block_ok(ok)) return;
+    double hh2 = hv[0] * hv[0], d1 = 0.0, d2 = 0.0;
+    block_sum3(hh2, d1, d2, red);
+    if (tid == 0) {
+      const double b2 = z2 - hh2;
+      w.beta[n_it - 1] = b2 > 0.0 ? sqrt(b2) : 0.0;
+    }
+  }
+}
+
+namespace {
+struct ResShape {
+  int rb, nb;
+};
+// rows per block for the resident kernel, or rb = 0 when the shape does not
+// qualify: one window, m of 1024 or 2048, nb = ceil(L / rb) rounded up to a
+// power of two, dividing m, at most one block per compute unit and per row group of the
+// workspace, n_it <= 256
+ResShape res_shape(const LanczosWS& w, int n_cu) {
+  ResShape s{0, 0};
+  if (w.n_act != 1 || (w.m != 1024 && w.m != 2048) || w.n_it > 256 || w.n_it < 1) return s;
+  const int cpl = w.m / 256;
+  for (int rb : {32, 16}) {
+    if (rb * cpl > 256) continue;              // registers: rb * cpl floats per lane
+    int nb = 1;                                // ceil(L / rb) rounded up to a power of two
+    while (nb * rb < w.L) nb *= 2;             // (blocks past the last row hold zeros)
+    if (nb > n_cu || nb > w.G3 || (nb & (nb - 1)) != 0 || w.m % nb != 0 || w.m / nb > LR_T ||
+        w.m / nb < 4)
+      continue;   // (G3 row groups: the rows of Spart and H2part)
+    s.rb = rb;
+    s.nb = nb;
+    return s;
+  }
+  return s;
+}
+template <int RB, int CPL>
+hipError_t launch_res_t(const LanczosWS& w, const ResShape& sh, unsigned* bar, const double* q1,
+                        bool check, hipStream_t s) {
+  auto k = k_lz_resident<RB, CPL>;
+  const size_t lds = (size_t)(w.n_it + 1) * (RB + 1) * sizeof(double);
+  if (lds > 65536) {
+    const hipError_t e =
+        hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  if (check) {
+    int per_cu = 0;
+    const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)k, LR_T, lds);
+    if (e != hipSuccess) return e;
+    return per_cu >= 1 ? hipSuccess : hipErrorInvalidConfiguration;
+  }
+  hipLaunchKernelGGL(k, dim3(sh.nb), dim3(LR_T), lds, s, w, bar, q1);
+  return hipGetLastError();
+}
+hipError_t launch_res(const LanczosWS& w, const ResShape& sh, unsigned* bar, const double* q1,
+                      bool check, hipStream_t s) {
+  if (w.m == 2048) return sh.rb == 32 ? launch_res_t<32, 8>(w, sh, bar, q1, check, s)
+                                      : launch_res_t<16, 8>(w, sh, bar, q1, check, s);
+  return sh.rb == 32 ? launch_res_t<32, 4>(w, sh, bar, q1, check, s)
+                     : launch_res_t<16, 4>(w, sh, bar, q1, check, s);
+}
+}  // namespace
+
+bool lanczos_resident_ok(const LanczosWS& w, int n_cu) {
+  const ResShape sh = res_shape(w, n_cu);
+  if (sh.rb == 0) return false;
+  (void)hipGetLastError();
+  return launch_res(w, sh, nullptr, nullptr, true, nullptr) == hipSuccess;
+}
+
+size_t lanczos_resident_bar_words(int n_cu) {
+  (void)n_cu;
+  return (size_t)LR_ERR + 32;   // the error word on a line of its own
+}
+
+hipError_t launch_lanczos_resident(const LanczosWS& w, const double* q1_act, unsigned* bar,
+                                   int n_cu, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  (void)hipGetLastError();
+  const ResShape sh = res_shape(w, n_cu);
+  if (sh.rb == 0) return hipErrorInvalidValue;
+  hipError_t e = launch_lanczos_start(w, q1_act, s);
+  if (e != hipSuccess) return e;
+  // the error word, and every buffer of tagged values zeroed (tag 0: not yet written)
+  const int64_t hs = w.ldq + 1;
+  const struct {
+    void* p;
+    int64_t words;
+  } clr[] = {{bar, (int64_t)lanczos_resident_bar_words(n_cu)},
+             {w.Spart, 2 * (int64_t)sh.nb * w.m},
+             {w.H2part, 2 * (int64_t)sh.nb * hs},
+             {w.T, 2 * (int64_t)w.m},
+             {w.Apart, 2 * (int64_t)sh.nb},
+             {w.H2, 2 * hs}};
+  for (const auto& z : clr) {
+    e = launch_fill_u32((uint32_t*)z.p, z.words, 0u, s);
+    if (e != hipSuccess) return e;
+  }
+  if (e0) {
+    e = hipEventRecord(e0, s);
+    if (e != hipSuccess) return e;
+  }
+  e = launch_res(w, sh, bar, q1_act, false, s);
+  if (e != hipSuccess) return e;
+  if (e1) e = hipEventRecord(e1, s);
+  return e;
+}
+
+}  // namespace slh

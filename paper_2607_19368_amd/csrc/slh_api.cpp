@@ -136,6 +136,9 @@ struct slh_ctx {
   std::string lz_key;
   LanczosWS lz_w{};                 // workspace of the last full-size Lanczos run
   bool lz_w_valid = false;
+  bool lz_res = false;              // that run used the resident kernel
+  int resident = 1;                 // SLH_OPT_RESIDENT
+  DevBuf lz_bar;                    // its grid-barrier words (generation, error, arrivals)
 
   int short_win = 1;                // SLH_OPT_SHORT_WINDOWS
   int normalize = 0;                // SLH_OPT_NORMALIZE
@@ -157,7 +160,8 @@ struct slh_ctx {
   std::vector<hipEvent_t> ev_fb, ev_fa;    // around each fused pass
   hipEvent_t ev[12] = {};                   // stage brackets: fm, lz, eig, sh, mg
   bool ev_made = false;
-  int fused_timed = 0;
+  int fused_timed = 0;              // event pairs in ev_fb / ev_fa
+  int passes_timed = 0;             // Lanczos steps they cover
   int norm_timed = 0;
 };
 
@@ -372,8 +376,10 @@ int64_t capacity(const slh_ctx* c) {
 // synchronised across queues).  Returns the first launch error (the capture
 // is ended by the caller in every case).
 hipError_t launch_lanczos_graph_body(slh_ctx* c, const LanczosWS& w, const double* q1act, int na,
-                                 int n_it, int L) {
-  hipError_t e = launch_lanczos(w, q1act, c->cap_stream);
+                                 int n_it, int L, bool res) {
+  hipError_t e = res ? launch_lanczos_resident(w, q1act, P<unsigned>(c->lz_bar), c->n_cu,
+                                               c->cap_stream)
+                     : launch_lanczos(w, q1act, c->cap_stream);
   if (e == hipSuccess)
     e = launch_eigh_ritz(w.alpha, w.beta, w.neff, na, n_it, c->r, P<double>(c->theta),
                          P<double>(c->Seig), w.Q, L, w.ldq, P<double>(c->Z), c->n_cu, c->cap_stream);
@@ -499,7 +505,7 @@ void slh_destroy(slh_ctx* c) {
                     &c->proj, &c->codes, &c->keyA, &c->keyB, &c->valA, &c->valB, &c->tmpi,
                     &c->segid, &c->segk, &c->sval, &c->sloc, &c->mw, &c->wbase, &c->sseg,
                     &c->Mtot, &c->part, &c->part_seg, &c->part_cnt, &c->part_nsum,
-                    &c->part_end, &c->rpart, &c->scores, &c->rsu};
+                    &c->part_end, &c->rpart, &c->scores, &c->rsu, &c->lz_bar};
   for (DevBuf* b : bufs)
     if (b->p) (void)hipFree(b->p);
   if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
@@ -584,6 +590,10 @@ int slh_set_option(slh_ctx* c, int32_t key, double v) {
     case SLH_OPT_SHORT_WINDOWS:
       if (v != 0.0 && v != 1.0) return fail(c, SLH_EINVAL, "SHORT_WINDOWS must be 0 or 1");
       c->short_win = (int)v;
+      break;
+    case SLH_OPT_RESIDENT:
+      if (v != 0.0 && v != 1.0) return fail(c, SLH_EINVAL, "RESIDENT must be 0 or 1");
+      c->resident = (int)v;
       break;
     default:
       return fail(c, SLH_EINVAL, "unknown option %d", key);
@@ -763,7 +773,9 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
         HIP_TRY(c, hipEventRecord(c->ev[4], c->stream));
       }
       c->fused_timed = 0;
+      c->passes_timed = 0;
       c->lz_w_valid = false;
+      c->lz_res = false;
     } else {
       LanczosWS w;
       memset(&w, 0, sizeof w);      // the graph key compares the bytes
@@ -787,7 +799,8 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
       const size_t hs = (size_t)w.ldq + 1;
       ENSURE(c, c->Q, (size_t)na * w.ldq * L * 8);
       ENSURE(c, c->T, (size_t)na * w.ldq * c->m * 8);
-      ENSURE(c, c->Apart, (size_t)na * (c->m / 16) * 8);
+      // |t|^2 partials: m / 16 per window, or one per block of the resident kernel
+      ENSURE(c, c->Apart, (size_t)na * std::max<int64_t>(c->m / 16, c->n_cu) * 8);
       ENSURE(c, c->Z1, (size_t)na * L * 8);
       ENSURE(c, c->Spart, (size_t)na * w.G3 * c->m * 8);
       ENSURE(c, c->Zs, (size_t)na * 2 * L * 8);
@@ -815,13 +828,21 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
       w.neff = P<int>(c->neff);
       w.stop = P<int>(c->stop);
       w.amax = P<double>(c->amax);
+      // one window whose Phi fits in the register files: the resident kernel
+      const bool res = c->resident && lanczos_resident_ok(w, c->n_cu);
+      (void)hipGetLastError();
+      if (res) ENSURE(c, c->lz_bar, lanczos_resident_bar_words(c->n_cu) * sizeof(unsigned));
       if (c->timing) {
         // timing: launch the step sequence directly so that every pass over Phi
         // can be bracketed by events (events inside a captured graph cannot be timed)
         int rc_ev = make_events(c, n_it);
         if (rc_ev) return rc_ev;
         HIP_TRY(c, hipEventRecord(c->ev[2], c->stream));
-        HIP_TRY(c, launch_lanczos(w, q1act, c->stream, c->ev_fb.data(), c->ev_fa.data()));
+        if (res)
+          HIP_TRY(c, launch_lanczos_resident(w, q1act, P<unsigned>(c->lz_bar), c->n_cu, c->stream,
+                                             c->ev_fb[0], c->ev_fa[0]));
+        else
+          HIP_TRY(c, launch_lanczos(w, q1act, c->stream, c->ev_fb.data(), c->ev_fa.data()));
         HIP_TRY(c, hipEventRecord(c->ev[3], c->stream));
         HIP_TRY(c, launch_eigh_ritz(w.alpha, w.beta, w.neff, na, n_it, c->r, P<double>(c->theta),
                                     P<double>(c->Seig), w.Q, (int)L, w.ldq, P<double>(c->Z),
@@ -832,13 +853,14 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
         // per configuration and replayed as one graph.
         std::string key((const char*)&w, sizeof w);
         key.append((const char*)&q1act, sizeof q1act);
+        key.append(res ? "r" : "s");
         const void* outs[3] = {c->theta.p, c->Seig.p, c->Z.p};   // the eigensolve's outputs
         key.append((const char*)outs, sizeof outs);
         if (!c->lz_exec || c->lz_key != key) {
           drop_graph(c);
           hipGraph_t g = nullptr;
           HIP_TRY(c, hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal));
-          hipError_t le = launch_lanczos_graph_body(c, w, q1act, na, n_it, (int)L);
+          hipError_t le = launch_lanczos_graph_body(c, w, q1act, na, n_it, (int)L, res);
           hipError_t ee = hipStreamEndCapture(c->cap_stream, &g);
           if (le != hipSuccess || ee != hipSuccess) {
             if (g) (void)hipGraphDestroy(g);
@@ -855,9 +877,11 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
         }
         HIP_TRY(c, hipGraphLaunch(c->lz_exec, c->stream));
       }
-      c->fused_timed = c->timing ? n_it : 0;
+      c->fused_timed = c->timing ? (res ? 1 : n_it) : 0;
+      c->passes_timed = c->timing ? n_it : 0;
       c->lz_w = w;
       c->lz_w_valid = true;
+      c->lz_res = res;
     }
   }
   if ((ritz_out || iters_out) && na > 0) {
@@ -868,6 +892,11 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
       HIP_TRY(c, hipMemcpyAsync(iters_out, c->neff.p, (size_t)na * 4, hipMemcpyDeviceToHost,
                                 c->stream));
     HIP_TRY(c, hipStreamSynchronize(c->stream));
+    if (c->lz_res) {
+      unsigned ew = 0;
+      HIP_TRY(c, hipMemcpy(&ew, P<unsigned>(c->lz_bar) + LZ_BAR_ERR, 4, hipMemcpyDeviceToHost));
+      if (ew) return fail(c, SLH_EHIP, "Lanczos: a wait between blocks of the resident kernel timed out");
+    }
   }
   c->stage = 2;
   c->merged = 0;
@@ -1026,9 +1055,14 @@ int slh_merge(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, float* emb_
                                P<int>(c->Mtot), c->compact, emb_out, pos_out, tok2macro_out,
                                c->stream));
   if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[8], c->stream));
-  if ((rc = ensure_pinned(c, 4))) return rc;
+  if ((rc = ensure_pinned(c, 8))) return rc;
   HIP_TRY(c, hipMemcpyAsync(c->pin, c->Mtot.p, 4, hipMemcpyDeviceToHost, c->stream));
+  if (c->lz_res)
+    HIP_TRY(c, hipMemcpyAsync((char*)c->pin + 4, P<unsigned>(c->lz_bar) + LZ_BAR_ERR, 4,
+                              hipMemcpyDeviceToHost, c->stream));
   if ((rc = wait_stream(c))) return rc;
+  if (c->lz_res && ((const unsigned*)c->pin)[1] != 0)
+    return fail(c, SLH_EHIP, "Lanczos: a wait between blocks of the resident kernel timed out");
   const int M = *(const int*)c->pin;
   *M_out = M + c->keep_last;
   c->merged = 1;
@@ -1109,7 +1143,7 @@ int slh_stage_times(slh_ctx* c, double* out, int32_t n) {
   if (!c || !out || n < 0) return SLH_EINVAL;
   if (!c->timing || !c->ev_made) return fail(c, SLH_ESTATE, "SLH_OPT_TIMING is off");
   HIP_TRY(c, hipStreamSynchronize(c->stream));
-  double v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  double v[9] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
   float ms = 0.f;
   auto el = [&](hipEvent_t a, hipEvent_t b) -> double {
     float t = 0.f;
@@ -1121,12 +1155,13 @@ int slh_stage_times(slh_ctx* c, double* out, int32_t n) {
     ms = (float)el(c->ev_fb[(size_t)j], c->ev_fa[(size_t)j]);
     v[2] += ms;
   }
-  v[3] = c->fused_timed;
+  v[3] = c->passes_timed;
   v[4] = el(c->ev[3], c->ev[4]);
   v[5] = el(c->ev[5], c->ev[6]);
   v[6] = el(c->ev[7], c->ev[8]);
   v[7] = c->norm_timed ? el(c->ev[9], c->ev[10]) : 0.0;
-  for (int i = 0; i < n && i < 8; ++i) out[i] = v[i];
+  v[8] = c->lz_res ? 1.0 : 0.0;
+  for (int i = 0; i < n && i < 9; ++i) out[i] = v[i];
   (void)hipGetLastError();   // a stage that did not run leaves unrecorded events
   return SLH_OK;
 }
@@ -1140,6 +1175,30 @@ int slh_time_passes(slh_ctx* c, int32_t reps, double* us_out) {
   hipGraph_t g = nullptr;
   hipGraphExec_t ge = nullptr;
   hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (c->lz_res) {
+    // the resident kernel: reps whole runs, each kernel between two events
+    // (its start kernel and buffer clears outside them); us per Lanczos step
+    const double* q1act = (c->n_act != c->n_win) ? P<double>(c->q1act) : P<double>(c->q1all);
+    hipEvent_t r0 = nullptr, r1 = nullptr;
+    hipError_t e = hipEventCreate(&r0);
+    if (e == hipSuccess) e = hipEventCreate(&r1);
+    double tot = 0.0;
+    for (int q = 0; q < reps && e == hipSuccess; ++q) {
+      e = launch_lanczos_resident(w, q1act, P<unsigned>(c->lz_bar), c->n_cu, c->stream, r0, r1);
+      if (e == hipSuccess) e = hipEventSynchronize(r1);
+      float ms = 0.f;
+      if (e == hipSuccess) e = hipEventElapsedTime(&ms, r0, r1);
+      if (q > 0 || reps == 1) tot += ms;   // the first run warms up
+    }
+    if (r0) (void)hipEventDestroy(r0);
+    if (r1) (void)hipEventDestroy(r1);
+    if (e != hipSuccess) return fail(c, SLH_EHIP, "slh_time_passes: %s", hipGetErrorString(e));
+    unsigned ew = 0;
+    HIP_TRY(c, hipMemcpy(&ew, P<unsigned>(c->lz_bar) + LZ_BAR_ERR, 4, hipMemcpyDeviceToHost));
+    if (ew) return fail(c, SLH_EHIP, "Lanczos: a wait between blocks of the resident kernel timed out");
+    *us_out = 1000.0 * tot / (reps > 1 ? reps - 1 : 1) / w.n_it;
+    return SLH_OK;
+  }
   HIP_TRY(c, hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal));
   const hipError_t le = launch_lanczos_passes(w, w.n_it - 1, reps, c->cap_stream);
   const hipError_t ce = hipStreamEndCapture(c->cap_stream, &g);
@@ -1212,6 +1271,7 @@ int slh_load(slh_ctx* c, int32_t which, const void* src, int64_t bytes) {
     c->n_it = (int)n_it;
     c->t_loaded = 1;
     c->lz_w_valid = false;
+    c->lz_res = false;
     c->stage = 1;
     c->merged = 0;
     return SLH_OK;

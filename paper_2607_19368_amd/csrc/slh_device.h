@@ -125,3 +125,21 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
   v += dpp_f64<DPP_ROR8>(v);
   return oct_sum_f64(v);
 }
+
+// Sum 8 values over the 64 lanes of a wave without LDS round trips: four
+// 32-lane trades (v_permlane32_swap), two 16-lane trades (v_permlane16_swap),
+// an 8-lane exchange (DPP row_ror:8), then a sum over each 8-lane group.  On
+// return lane l holds the full sum of value index ((l>>5)&1)*4 + ((l>>4)&1)*2 +
+// ((l>>3)&1).  Every lane of the wave must be active.
+__device__ __forceinline__ double wave_sum8_f64(const double (&v)[8]) {
+  const int lane = threadIdx.x & 63;
+  double w[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) w[e] = swap32_add(v[e], v[e + 4]);
+  double x[2];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) x[e] = swap16_add(w[e], w[e + 2]);
+  const bool b8 = lane & 8;
+  const double y = (b8 ? x[1] : x[0]) + dpp_f64<DPP_ROR8>(b8 ? x[0] : x[1]);
+  return oct_sum_f64(y);
+}

@@ -69,6 +69,26 @@ hipError_t launch_lanczos(const LanczosWS& w, const double* q1_act, hipStream_t 
 // to Zs and it records no alpha, beta, n_eff or breakdown (for timing); it
 // rewrites Spart and H2part
 hipError_t launch_lanczos_passes(const LanczosWS& w, int j, int reps, hipStream_t s);
+// q_0 of every active window into Q[a][0], alpha and beta zeroed, the
+// per-window state (n_eff, stop) cleared (k_lz_start)
+hipError_t launch_lanczos_start(const LanczosWS& w, const double* q1_act, hipStream_t s);
+
+// ---- resident Lanczos (k_lzres.hip): one window whose Phi fits in the register
+// files, the whole run as one persistent kernel (rows of Phi held in registers;
+// the blocks exchange step-tagged values instead of meeting at barriers) ----
+// true when the shape qualifies (n_act 1, m 1024 or 2048, at most 32 rows per
+// compute unit, n_it <= 256) and every block of the kernel can be resident
+bool lanczos_resident_ok(const LanczosWS& w, int n_cu);
+// 32-bit words of the kernel's status buffer; its error word, at index
+// LZ_BAR_ERR, is nonzero after a wait between blocks timed out (the run's
+// results are then invalid)
+size_t lanczos_resident_bar_words(int n_cu);
+constexpr int LZ_BAR_ERR = 32;
+// k_lz_start, the status and exchange buffers cleared, the persistent kernel (bracketed by
+// e0 / e1 when given); the same outputs as launch_lanczos
+hipError_t launch_lanczos_resident(const LanczosWS& w, const double* q1_act, unsigned* bar,
+                                   int n_cu, hipStream_t s, hipEvent_t e0 = nullptr,
+                                   hipEvent_t e1 = nullptr);
 
 // ---- eigensolve + Ritz + SimHash (k_eig.hip, k_hash.hip) ----
 // Eigh(T) of every active window (theta: kept eigenvalues ascending, Seig their

@@ -64,11 +64,12 @@ class Run:
 
 def run_gpu(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel=0, compact=False,
             phi_from=None, codes_from=None, want_phi=False, X=None, short_windows=None,
-            normalise=False, scheme=0, keep_last=None, timing=False):
+            normalise=False, scheme=0, keep_last=None, timing=False, resident=None):
     """phi_from: host float32 array (n_act*L, m) loaded instead of computing Phi;
     codes_from: host uint32 (N,) loaded instead of computing codes;
     short_windows: value of SLH_OPT_SHORT_WINDOWS (None keeps the default);
-    timing: SLH_OPT_TIMING = 1 (every Lanczos pass launched directly, timed)."""
+    timing: SLH_OPT_TIMING = 1 (every Lanczos pass launched directly, timed);
+    resident: value of SLH_OPT_RESIDENT (None keeps the default)."""
     import torch
     import paper_2607_19368_amd as P
     from paper_2607_19368_amd import slh as B
@@ -87,6 +88,8 @@ def run_gpu(inp, n_it, seed=0, window=0, rho=None, tau=-1.0, kernel=0, compact=F
         P.slh_set_option(ctx, B.SLH_OPT_POS_MODE, 1)
     if short_windows is not None:
         P.slh_set_option(ctx, B.SLH_OPT_SHORT_WINDOWS, short_windows)
+    if resident is not None:
+        P.slh_set_option(ctx, B.SLH_OPT_RESIDENT, resident)
     if normalise:
         P.slh_set_option(ctx, B.SLH_OPT_NORMALIZE, 1)
     if scheme:

@@ -303,18 +303,79 @@ E2E = {
     "tiny": dict(),
     "mistral7b": dict(),
     "qwen7b": dict(),
+    # the same prompt with one pass over Phi per Lanczos step instead of the
+    # resident kernel that the default takes at this size
+    "qwen7b_streaming": dict(resident=0),
 }
 
 
 @pytest.mark.parametrize("name", list(E2E))
 def test_end_to_end(name):
-    inp = make_inputs(name)
+    inp = make_inputs(name.replace("_streaming", ""))
     wl = inp.workload
     _say(f"[e2e] {name} N={wl.N} D={wl.D} m={wl.m} n_it={wl.n_it} r={wl.r} bits={wl.bits}")
-    g = PR.run_gpu(inp, n_it=wl.n_it)
+    g = PR.run_gpu(inp, n_it=wl.n_it, **E2E[name])
     o = PR.run_oracle(inp, n_it=wl.n_it)
     rep = PR.compare(o, g, wl.N)
     _say(f"   {rep}  M={len(g.P)}  rho_achieved={wl.N / len(g.P):.2f}")
+
+
+# ------------------------------------------------------------------ resident Lanczos kernel
+def _lanczos_on_phi(Phi32, wl, n_it, resident):
+    """Lanczos + Eigh + Ritz on a loaded Phi with SLH_OPT_RESIDENT = resident
+    (timing mode, so that the stage record says which path ran)."""
+    import torch
+    import paper_2607_19368_amd as P
+    from paper_2607_19368_amd import slh as B
+    ctx = P.slh_create(wl.N, wl.D, wl.m, wl.r, wl.bits, 0)
+    P.slh_set_option(ctx, B.SLH_OPT_TIMING, 1)
+    P.slh_set_option(ctx, B.SLH_OPT_RESIDENT, resident)
+    P.slh_load(ctx, B.SLH_OUT_PHI, torch.from_numpy(Phi32).cuda())
+    ritz, iters = P.slh_lanczos(ctx, n_it)
+    out = dict(ritz=ritz[0], iters=iters[0],
+               Q=P.slh_copy_out(ctx, B.SLH_OUT_Q)[0][:iters[0]],
+               alpha=P.slh_copy_out(ctx, B.SLH_OUT_ALPHA)[0],
+               beta=P.slh_copy_out(ctx, B.SLH_OUT_BETA)[0],
+               Z=P.slh_copy_out(ctx, B.SLH_OUT_Z)[0],
+               used=P.slh_stage_times(ctx)["lanczos_resident"])
+    return out
+
+
+@pytest.mark.parametrize("case", ["m1024_ragged", "m2048"])
+def test_resident_lanczos_on_oracle_phi(case):
+    """The resident kernel (the whole Lanczos loop of Algorithm 2 as one
+    persistent kernel, rows of Phi held in registers, blocks exchanging
+    step-tagged values) on the oracle's Phi: it runs where SLH_OPT_RESIDENT
+    allows it and not otherwise; its basis is orthonormal to 1e-12; alpha and
+    beta match the oracle's to 1e-9; against the streaming path on the same Phi
+    (the same recurrence, partial sums grouped differently) alpha, beta and the
+    Ritz values agree to 1e-10 relative and the kept Ritz subspace to 1e-8 rad.
+    A row count that is not a multiple of the block's 32 rows (2000) pads the
+    last blocks with zero rows."""
+    N, m = (2000, 1024) if case == "m1024_ragged" else (4096, 2048)
+    n_it = 64
+    inp = _custom("res_" + case, N, 264, m, n_it, 16, 8)
+    wl = inp.workload
+    Phi32 = O.feature_map(inp.x_float(), OP.projection(0, wl.D, wl.m),
+                          OP.phases(0, wl.m)).astype(np.float32)
+    res = _lanczos_on_phi(Phi32, wl, n_it, 1)
+    stm = _lanczos_on_phi(Phi32, wl, n_it, 0)
+    assert res["used"] == 1.0 and stm["used"] == 0.0
+    assert res["iters"] == stm["iters"] == n_it
+    Q = res["Q"]
+    orth = np.abs(Q @ Q.T - np.eye(n_it)).max()
+    lz = O.lanczos(Phi32.astype(np.float64), OP.start_vector(0, wl.N, 0), n_it)
+    ra = np.max(np.abs(res["alpha"] - lz.alpha) / np.abs(lz.alpha))
+    rb = np.max(np.abs(res["beta"] - lz.beta) / np.abs(lz.beta))
+    da = np.max(np.abs(res["alpha"] - stm["alpha"]) / np.abs(stm["alpha"]))
+    db = np.max(np.abs(res["beta"] - stm["beta"]) / np.abs(stm["beta"]))
+    dr = np.max(np.abs(res["ritz"] - stm["ritz"]) / np.abs(stm["ritz"]))
+    ang = PR.subspace_angle(stm["Z"], res["Z"])
+    _say(f"[resident] {case}: |Q^T Q - I| {orth:.2e}  alpha/beta vs oracle {ra:.2e}/{rb:.2e}  "
+         f"vs streaming alpha {da:.2e} beta {db:.2e} ritz {dr:.2e} angle {ang:.2e}")
+    assert orth <= 1e-12
+    assert ra <= 1e-9 and rb <= 1e-9
+    assert da <= 1e-10 and db <= 1e-10 and dr <= 1e-10 and ang <= 1e-8
 
 
 @pytest.mark.timeout(900)
@@ -393,12 +454,15 @@ def test_router_scores_both_paths(case):
 
 
 # ------------------------------------------------------------------ edge cases
-def test_identical_rows_break_down():
+@pytest.mark.parametrize("m", [256, 1024])
+def test_identical_rows_break_down(m):
     """Identical rows: Phi Phi^T = |phi|^2 11^T has rank one, so Lanczos breaks
-    down after two steps on both sides; the leading Ritz columns are zero."""
+    down after two steps on both sides; the leading Ritz columns are zero.  At
+    m = 1024 the run takes the resident kernel, whose blocks all leave the loop
+    at the same step."""
     base = make_inputs("tiny")
     X = np.tile(base.X[:1], (256, 1))
-    wl = Workload("ident", 256, 256, 256, 16, 8, 6, 4.0, 0, 0, "f32")
+    wl = Workload("ident", 256, 256, m, 16, 8, 6, 4.0, 0, 0, "f32")
     inp = Inputs(wl, X, np.zeros(256))
     g = PR.run_gpu(inp, n_it=16)
     o = PR.run_oracle(inp, n_it=16)
@@ -934,7 +998,7 @@ def test_exact_target_length(case, T):
     assert rel.max() <= 1e-5
 
 
-@pytest.mark.parametrize("case", ["tiny", "windows256"])
+@pytest.mark.parametrize("case", ["tiny", "windows256", "resident"])
 def test_time_passes(case):
     """slh_time_passes replays the final step's pass over Phi as a graph:
     it returns a positive duration and leaves every result of slh_lanczos (Q,
@@ -944,6 +1008,8 @@ def test_time_passes(case):
     from paper_2607_19368_amd import slh as B
     if case == "tiny":
         inp, L = make_inputs("tiny"), 0
+    elif case == "resident":                  # the resident kernel: its runs are timed
+        inp, L = _custom("tpr", 2048, 264, 1024, 32, 8, 8), 0
     else:
         inp, L = _custom("tpw", 4 * 256, 512, 256, 24, 8, 8), 256
     wl = inp.workload
