@@ -312,8 +312,7 @@ int slh_stage_times(slh_ctx *ctx, double *ms_out, int32_t n);
  * never Q, alpha, beta, the Ritz pairs or codes; windows that broke down early
  * skip their passes as in the loop itself.  After a run of the resident kernel
  * (SLH_OPT_RESIDENT) the call instead launches that run reps times, each
- * kernel between two events (its start kernel and buffer clears outside
- * them), and us_out is the kernel's mean duration over the runs after the
+ * kernel between two events (its preparation kernel outside them), and us_out is the kernel's mean duration over the runs after the
  * first, divided by n_it (per Lanczos step); those runs recompute the whole
  * Lanczos loop and rewrite Q, alpha and beta with the same values.  reps in
  * [1, 4096].  Synchronises the stream.  SLH_ESTATE before slh_lanczos or after a short-window

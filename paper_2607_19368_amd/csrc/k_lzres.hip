@@ -219,23 +219,28 @@ __global__ __launch_bounds__(LR_T, 1) void k_lz_resident(LanczosWS w, unsigned* 
   };
   // t over the block's columns from the partials of step e (scaled by 1 / |z1|
   // when norm, |z1|^2 summed here from its partials first), and the block's
-  // partial of |t|^2, tagged with step e.  Thread = (column cl < CB, partial
-  // lane pl < PL); the nb / PL = CPL partials of a lane and the |z1|^2 partial
-  // are polled together.  false when a wait failed.
-  auto col_reduce = [&](bool norm, double& z2v, int e) -> bool {
+  // partial of |t|^2, tagged with step e; with kh >= 0 also the h2 entry kh.
+  // Thread = (column cl < CB, partial lane pl < PL); the nb / PL = CPL
+  // partials of a lane, the |z1|^2 partial and the h2 partial are polled
+  // together.  false when a wait failed.
+  auto col_reduce = [&](bool norm, double& z2v, int e, int kh) -> bool {
     const int CB = m / nb, PL = LR_T / CB;
     const int c = b * CB + tid % CB;
     const int64_t base = (int64_t)b * nb * CB + tid;
-    double v[CPL], zv[1];
+    double v[CPL], zv[1], hv[1];
     bool ok = ld_wait<CPL>([&](int u) { return Spart + base + u * LR_T; }, (1u << CPL) - 1u, e, bar, v);
     if (norm)
       ok = ld_wait<1>([&](int) { return Hpart + (int64_t)tid * hs + ldq; }, tid < nb ? 1u : 0u, e,
                       bar, zv) && ok;
+    ok = ld_wait<1>([&](int) { return Hpart + (int64_t)tid * hs + kh; }, (kh >= 0 && tid < nb) ? 1u : 0u,
+                    e, bar, hv) && ok;
     if (!block_ok(ok)) return false;
-    if (norm) {
-      double d1 = 0.0, d2 = 0.0;
-      block_sum3(zv[0], d1, d2, red);
-      z2v = zv[0];
+    if (norm || kh >= 0) {
+      double d2 = 0.0;
+      if (!norm) zv[0] = 0.0;
+      block_sum3(zv[0], hv[0], d2, red);
+      if (norm) z2v = zv[0];
+      if (kh >= 0 && tid == 0) st_tag(H2 + kh, hv[0], e);
     }
     double sm = 0.0;
 #pragma unroll
@@ -273,16 +278,39 @@ __global__ __launch_bounds__(LR_T, 1) void k_lz_resident(LanczosWS w, unsigned* 
   // t_0 = Phi^T q_0 and its |t_0|^2 partials: step 0 of the tags
   col_partials(0);
   double z2 = 0.0;
-  if (!col_reduce(false, z2, 0)) return;
+  if (!col_reduce(false, z2, 0, -1)) return;
 
   double amax = 0.0;
   const int idx = ((lane >> 5) & 1) * 4 + ((lane >> 4) & 1) * 2 + ((lane >> 3) & 1);
   for (int j = 0; j < n_it; ++j) {
     // ---- rows: the reduced values of the previous step (tags of step j),
-    // those of this step tagged j + 1
+    // those of this step tagged j + 1.  A wave takes its row dots as soon as its
+    // own entries of t~ have arrived (the scalars of the step wait for values
+    // of every block).
     double tv[CPL], a1[1], h1[1];
     bool ok = ld_wait<CPL>([&](int u) { return Tv + cb + 256 * (u >> 2) + (u & 3); }, (1u << CPL) - 1u,
                            j, bar, tv);
+    // Phi t~ of the block's rows: 4 CPL products per lane and row, summed over
+    // the wave 8 rows at a time (into prw), then over the 4 waves
+#pragma unroll
+    for (int r8 = 0; r8 < RB; r8 += 8) {
+      double d[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        double x = 0.0;
+#pragma unroll
+        for (int h = 0; h < NH; ++h) {
+          const float4 y = pin4(ph[r8 + e][h]);
+          x = fma((double)y.x, tv[4 * h + 0], x);
+          x = fma((double)y.y, tv[4 * h + 1], x);
+          x = fma((double)y.z, tv[4 * h + 2], x);
+          x = fma((double)y.w, tv[4 * h + 3], x);
+        }
+        d[e] = x;
+      }
+      const double tot = wave_sum8_f64(d);
+      if ((lane & 7) == 0) prw[wv][r8 + idx] = tot;
+    }
     ok = ld_wait<1>([&](int) { return Ap + tid; }, tid < nb ? 1u : 0u, j, bar, a1) && ok;
     ok = ld_wait<1>([&](int) { return H2 + tid; }, tid < j ? 1u : 0u, j, bar, h1) && ok;
     if (!block_ok(ok)) return;
@@ -355,27 +383,6 @@ __global__ __launch_bounds__(LR_T, 1) void k_lz_resident(LanczosWS w, unsigned* 
       qmr[i] = qm;
       sgr[i] = sg;
     }
-    // Phi t~ of the block's rows: 4 CPL products per lane and row, summed over
-    // the wave 8 rows at a time, then over the 4 waves
-#pragma unroll
-    for (int r8 = 0; r8 < RB; r8 += 8) {
-      double d[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        double x = 0.0;
-#pragma unroll
-        for (int h = 0; h < NH; ++h) {
-          const float4 y = pin4(ph[r8 + e][h]);
-          x = fma((double)y.x, tv[4 * h + 0], x);
-          x = fma((double)y.y, tv[4 * h + 1], x);
-          x = fma((double)y.z, tv[4 * h + 2], x);
-          x = fma((double)y.w, tv[4 * h + 3], x);
-        }
-        d[e] = x;
-      }
-      const double tot = wave_sum8_f64(d);
-      if ((lane & 7) == 0) prw[wv][r8 + idx] = tot;
-    }
     __syncthreads();
     if (tid < RB) {
       const int i = tid;
@@ -386,8 +393,8 @@ __global__ __launch_bounds__(LR_T, 1) void k_lz_resident(LanczosWS w, unsigned* 
       zs[i] = (r0 + i < L) ? z : 0.0;
     }
     __syncthreads();
-    // partials of Phi^T z1, of h2 = Q_j^T z1 (k <= j) and of |z1|^2
-    col_partials(j + 1);
+    // partials of h2 = Q_j^T z1 (k <= j) and of |z1|^2, then of Phi^T z1 (the
+    // small stores ahead of the 16 KB of column partials)
     for (int k = tid; k <= j + 1; k += LR_T) {
       double v = 0.0;
       double a4[4] = {0.0, 0.0, 0.0, 0.0};
@@ -397,13 +404,16 @@ __global__ __launch_bounds__(LR_T, 1) void k_lz_resident(LanczosWS w, unsigned* 
       v = (a4[0] + a4[1]) + (a4[2] + a4[3]);
       st_tag(Hpart + (int64_t)b * hs + (k <= j ? k : ldq), v, j + 1);
     }
+    col_partials(j + 1);
     // ---- columns: |z1|^2 (every block), t~_{j+1}, h2
+    int k0 = b;                                   // h2 entries of this block: b, b + nb, ...
     if (j + 1 < n_it) {
-      if (!col_reduce(true, z2, j + 1)) return;
+      if (!col_reduce(true, z2, j + 1, b <= j ? b : -1)) return;
+      k0 = b + nb;
     } else {
       if (!hpart_sum(ldq, j + 1, z2)) return;
     }
-    for (int k = b; k <= j; k += nb) {
+    for (int k = k0; k <= j; k += nb) {
       double v = 0.0;
       if (!hpart_sum(k, j + 1, v)) return;
       if (tid == 0) st_tag(H2 + k, v, j + 1);
@@ -421,6 +431,33 @@ __global__ __launch_bounds__(LR_T, 1) void k_lz_resident(LanczosWS w, unsigned* 
       w.beta[n_it - 1] = b2 > 0.0 ? sqrt(b2) : 0.0;
     }
   }
+}
+
+// Everything the kernel expects before it starts, in one launch: q_0 into
+// Q[0], alpha, beta, n_eff, the breakdown flag and max |alpha| cleared (the
+// streaming path's k_lz_start), and the status word and every buffer of tagged
+// values zeroed (tag 0: not yet written).
+struct ResClear {
+  double* p[6];
+  int64_t n[6];   // doubles
+};
+__global__ void k_lz_res_prep(LanczosWS w, const double* __restrict__ q1, ResClear z) {
+  const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t st = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = t0; i < w.L; i += st) w.Q[i] = q1[i];
+  for (int64_t i = t0; i < w.n_it; i += st) {
+    w.alpha[i] = 0.0;
+    w.beta[i] = 0.0;
+  }
+  if (t0 == 0) {
+    w.stop[0] = 0;
+    w.neff[0] = 0;
+    w.amax[0] = 0.0;
+    w.amax[1] = 0.0;
+  }
+#pragma unroll
+  for (int q = 0; q < 6; ++q)
+    for (int64_t i = t0; i < z.n[q]; i += st) z.p[q][i] = 0.0;
 }
 
 namespace {
@@ -493,23 +530,18 @@ hipError_t launch_lanczos_resident(const LanczosWS& w, const double* q1_act, uns
   (void)hipGetLastError();
   const ResShape sh = res_shape(w, n_cu);
   if (sh.rb == 0) return hipErrorInvalidValue;
-  hipError_t e = launch_lanczos_start(w, q1_act, s);
-  if (e != hipSuccess) return e;
-  // the error word, and every buffer of tagged values zeroed (tag 0: not yet written)
   const int64_t hs = w.ldq + 1;
-  const struct {
-    void* p;
-    int64_t words;
-  } clr[] = {{bar, (int64_t)lanczos_resident_bar_words(n_cu)},
-             {w.Spart, 2 * (int64_t)sh.nb * w.m},
-             {w.H2part, 2 * (int64_t)sh.nb * hs},
-             {w.T, 2 * (int64_t)w.m},
-             {w.Apart, 2 * (int64_t)sh.nb},
-             {w.H2, 2 * hs}};
-  for (const auto& z : clr) {
-    e = launch_fill_u32((uint32_t*)z.p, z.words, 0u, s);
-    if (e != hipSuccess) return e;
+  ResClear z;
+  const double* const bufs[6] = {(const double*)bar, w.Spart, w.H2part, w.T, w.Apart, w.H2};
+  const int64_t lens[6] = {(int64_t)lanczos_resident_bar_words(n_cu) / 2, (int64_t)sh.nb * w.m,
+                           (int64_t)sh.nb * hs, (int64_t)w.m, (int64_t)sh.nb, hs};
+  for (int q = 0; q < 6; ++q) {
+    z.p[q] = const_cast<double*>(bufs[q]);
+    z.n[q] = lens[q];
   }
+  hipLaunchKernelGGL(k_lz_res_prep, dim3(256), dim3(256), 0, s, w, q1_act, z);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   if (e0) {
     e = hipEventRecord(e0, s);
     if (e != hipSuccess) return e;

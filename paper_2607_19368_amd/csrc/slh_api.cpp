@@ -1177,7 +1177,7 @@ int slh_time_passes(slh_ctx* c, int32_t reps, double* us_out) {
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (c->lz_res) {
     // the resident kernel: reps whole runs, each kernel between two events
-    // (its start kernel and buffer clears outside them); us per Lanczos step
+    // (its preparation kernel outside them); us per Lanczos step
     const double* q1act = (c->n_act != c->n_win) ? P<double>(c->q1act) : P<double>(c->q1all);
     hipEvent_t r0 = nullptr, r1 = nullptr;
     hipError_t e = hipEventCreate(&r0);

@@ -84,8 +84,9 @@ bool lanczos_resident_ok(const LanczosWS& w, int n_cu);
 // results are then invalid)
 size_t lanczos_resident_bar_words(int n_cu);
 constexpr int LZ_BAR_ERR = 32;
-// k_lz_start, the status and exchange buffers cleared, the persistent kernel (bracketed by
-// e0 / e1 when given); the same outputs as launch_lanczos
+// one preparation kernel (q_0 into Q[0] and the state cleared as k_lz_start
+// does; the status and exchange buffers zeroed), then the persistent kernel
+// (bracketed by e0 / e1 when given); the same outputs as launch_lanczos
 hipError_t launch_lanczos_resident(const LanczosWS& w, const double* q1_act, unsigned* bar,
                                    int n_cu, hipStream_t s, hipEvent_t e0 = nullptr,
                                    hipEvent_t e1 = nullptr);
