@@ -1,12 +1,12 @@
 // Eigh(T) for the Lanczos tridiagonal and the top-r Ritz coordinates
 // (Algorithm 1: lambda, V = Eigh(T); Z = Q V[:, n-k:n]).
 //
-// Eigenvalues: one 256-thread workgroup per kept eigenvalue isolates it by
-// Sturm-count multisection (256 probe points per round, one per thread; the
+// One 256-thread workgroup per kept eigenpair (k_eig_pairs).  Its eigenvalue
+// by Sturm-count multisection (256 probe points per round, one per thread; the
 // sign changes along the leading principal minors of T - x I count the
-// eigenvalues below x) until the bracket is a few ulps wide.
-// Eigenvectors: one workgroup per kept eigenvalue.  Eigenvalues more than
-// EIG_TWIST_GAP |T| from their kept neighbours take the twisted factorisation
+// eigenvalues below x) until the bracket is a few ulps wide; then its vector.
+// Eigenvalues more than EIG_TWIST_GAP |T| from every other eigenvalue of T
+// (two more Sturm counts) take the twisted factorisation
 // (twisted_vector: two pivot recurrences and two product recurrences, no
 // iteration); the others inverse iteration with a partially pivoted LU of
 // T - theta I from a start vector of its own.  Two
@@ -158,27 +158,16 @@ __device__ __forceinline__ TriInfo load_tridiag(const double* __restrict__ alp,
   return t;
 }
 
-// theta: [n_act][r], ascending kept eigenvalues (zero for the r - r_eff
-// leading columns of a window that stopped after n_eff < r steps).
-__global__ __launch_bounds__(EIG_VT) void k_eig_values(const double* __restrict__ alpha,
-                                                      const double* __restrict__ beta,
-                                                      const int* __restrict__ neff, int n_it,
-                                                      int r, double* __restrict__ theta) {
-  const int c = blockIdx.x, a = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int n = neff[a];
-  const int r_eff = min(r, n);
-  if (c < r - r_eff) {
-    if (tid == 0) theta[(int64_t)a * r + c] = 0.0;
-    return;
-  }
-  const int kidx = n - r + c;   // ascending index of the wanted eigenvalue
-  __shared__ double al[EIG_NMAX], b1[EIG_NMAX], b2[EIG_NMAX];
-  __shared__ __align__(16) double an[EIG_NMAX + 8], b2s[EIG_NMAX + 8];
-  __shared__ unsigned long long smask[EIG_VT / 64];
-  const TriInfo ti = load_tridiag(alpha + (int64_t)a * n_it, beta + (int64_t)a * n_it, n, al, b1, b2);
+// The eigenvalue of ascending index kidx of the tridiagonal in LDS (al, b1;
+// Gershgorin information ti) by Sturm-count multisection; every thread of the
+// block calls it and gets the value.  On return an, b2s hold T / 2^esc (the
+// operands of the minors recurrence, |T| / 2^esc < 1).  smask: EIG_VT / 64
+// words of LDS.
+__device__ double multisect(const double* al, const double* b1, int n, const TriInfo& ti, int kidx,
+                            double* an, double* b2s, unsigned long long* smask, int& esc) {
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const double pivmin = DBL_MIN * fmax(1.0, ti.bmax);
-  // T / 2^esc with |T| / 2^esc < 1, the operands of the minors recurrence
-  const int esc = (ti.tnorm > 0.0) ? __builtin_amdgcn_frexp_exp(ti.tnorm) : 0;
+  esc = (ti.tnorm > 0.0) ? __builtin_amdgcn_frexp_exp(ti.tnorm) : 0;
   for (int k = tid; k < n; k += EIG_VT) {
     an[k] = __builtin_amdgcn_ldexp(al[k], -esc);
     const double bs = (k > 0) ? __builtin_amdgcn_ldexp(b1[k - 1], -esc) : 0.0;
@@ -213,7 +202,7 @@ __global__ __launch_bounds__(EIG_VT) void k_eig_values(const double* __restrict_
     lo = nlo;
     hi = nhi;
   }
-  if (tid == 0) theta[(int64_t)a * r + c] = 0.5 * (lo + hi);
+  return 0.5 * (lo + hi);
 }
 
 // Unit norm and the sign rule (first nonzero entry positive) for y[0..n), into
@@ -469,34 +458,46 @@ __device__ __forceinline__ bool twisted_vector(const double* al, const double* b
 }
 
 // Seig: [n_act][n_it][r] (row k, kept column c); rows n_eff.. are zero.
-__global__ __launch_bounds__(EIG_T) void k_eig_vectors(const double* __restrict__ alpha,
-                                                       const double* __restrict__ beta,
-                                                       const int* __restrict__ neff, int n_it,
-                                                       int r, const double* __restrict__ theta,
-                                                       double* __restrict__ Seig) {
+// theta: [n_act][r], ascending kept eigenvalues (zero for the r - r_eff
+// leading columns of a window that stopped after n_eff < r steps); Seig
+// [n_act][n_it][r] their vectors.  Block (c, a): kept eigenpair c of window a,
+// its eigenvalue by multisection, then its vector.
+__global__ __launch_bounds__(EIG_T) void k_eig_pairs(const double* __restrict__ alpha,
+                                                     const double* __restrict__ beta,
+                                                     const int* __restrict__ neff, int n_it,
+                                                     int r, double* __restrict__ theta,
+                                                     double* __restrict__ Seig) {
   const int c = blockIdx.x, a = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int n = neff[a];
   const int r_eff = min(r, n);
   double* Sa = Seig + (int64_t)a * n_it * r;
   if (c < r - r_eff) {
+    if (tid == 0) theta[(int64_t)a * r + c] = 0.0;
     for (int k = tid; k < n_it; k += EIG_T) Sa[(int64_t)k * r + c] = 0.0;
     return;
   }
-  const double th = theta[(int64_t)a * r + c];
   __shared__ double al[EIG_NMAX], b1[EIG_NMAX], b2[EIG_NMAX];
   __shared__ double y[EIG_NMAX], w[EIG_NMAX];
   __shared__ double fu1[EIG_NMAX], fu2[EIG_NMAX], fd[EIG_NMAX], fl[EIG_NMAX];
   __shared__ int piv[EIG_NMAX];
+  __shared__ __align__(16) double an[EIG_NMAX + 8], b2s[EIG_NMAX + 8];
+  __shared__ unsigned long long smask[EIG_VT / 64];
+  __shared__ int cnt2[2];
   const TriInfo ti = load_tridiag(alpha + (int64_t)a * n_it, beta + (int64_t)a * n_it, n, al, b1, b2);
-  // An eigenvalue with no kept neighbour within EIG_TWIST_GAP |T| takes the
-  // twisted factorisation (its vector is then accurate to about eps |T| / gap,
-  // and k_eig_orth orthonormalises the clusters); if that fails its residual
-  // test, and for (numerically) repeated eigenvalues, inverse iteration below.
+  int esc = 0;
+  const double th = multisect(al, b1, n, ti, n - r + c, an, b2s, smask, esc);
+  if (tid == 0) theta[(int64_t)a * r + c] = th;
+  // An eigenvalue alone in [th - EIG_TWIST_GAP |T|, th + EIG_TWIST_GAP |T|)
+  // (two Sturm counts) takes the twisted factorisation (its vector is then
+  // accurate to about eps |T| / gap, and the clusters of kept eigenvalues are
+  // orthonormalised later); if that fails its residual test, and for
+  // (numerically) repeated eigenvalues, inverse iteration below.
   {
     const double ctol = EIG_TWIST_GAP * ti.tnorm;
-    const bool lgap = c == r - r_eff || th - theta[(int64_t)a * r + c - 1] > ctol;
-    const bool rgap = c + 1 == r || theta[(int64_t)a * r + c + 1] - th > ctol;
-    if (lgap && rgap &&
+    if (tid < 2)
+      cnt2[tid] = sturm_count(an, b2s, n, __builtin_amdgcn_ldexp(tid ? th + ctol : th - ctol, -esc));
+    __syncthreads();
+    if (cnt2[1] - cnt2[0] == 1 &&
         twisted_vector(al, b1, b2, n, th, ti.tnorm, DBL_MIN * fmax(1.0, ti.bmax), fd, fl, fu1,
                        fu2, w, y)) {
       if (wv == 0) store_unit_column(y, n, n_it, r, c, Sa);
@@ -992,10 +993,9 @@ hipError_t launch_eigh_ritz(const double* alpha, const double* beta, const int* 
                             int ldq, double* Z, int n_cu, hipStream_t s) {
   (void)hipGetLastError();
   if (n_it > EIG_NMAX || r > n_it || r > 128 || r < 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_eig_values, dim3(r, n_act), dim3(EIG_VT), 0, s, alpha, beta, neff, n_it, r,
-                     theta);
-  hipLaunchKernelGGL(k_eig_vectors, dim3(r, n_act), dim3(EIG_T), 0, s, alpha, beta, neff, n_it,
-                     r, theta, Seig);
+  static_assert(EIG_VT == EIG_T, "one block size for the pairs");
+  hipLaunchKernelGGL(k_eig_pairs, dim3(r, n_act), dim3(EIG_T), 0, s, alpha, beta, neff, n_it, r,
+                     theta, Seig);
   if ((int64_t)((n_it + 3) & ~3) * (r + 33) <= RZ_LDS && n_it <= RZ_NMAX) {
     const hipError_t e = launch_ritz_orth(Q, Seig, neff, alpha, beta, theta, n_act, L, ldq, n_it, r,
                                           Z, n_cu, s);
