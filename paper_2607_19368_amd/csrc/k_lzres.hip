@@ -38,7 +38,7 @@ namespace slh {
 
 namespace {
 
-constexpr int LR_T = 256;          // threads per block: 4 waves, one per SIMD
+constexpr int LR_T = 256;          // threads per block at m = 1024 (one wave per SIMD); 512 at m = 2048
 constexpr int LR_SPIN = 1 << 20;   // polls before a barrier gives up
 
 __device__ __forceinline__ void st_flag(unsigned* p, unsigned v) {
@@ -120,8 +120,9 @@ __device__ __forceinline__ float4 pin4(float4 x) {
   return x;
 }
 
-// three block sums at once (fixed order: wave sums, then the 4 waves in order)
-__device__ __forceinline__ void block_sum3(double& a, double& b, double& c, double (*red)[4]) {
+// three block sums at once (fixed order: wave sums, then the NW waves in order)
+template <int NW>
+__device__ __forceinline__ void block_sum3(double& a, double& b, double& c, double (*red)[NW]) {
   a = wave_sum_f64(a);
   b = wave_sum_f64(b);
   c = wave_sum_f64(c);
@@ -132,34 +133,59 @@ __device__ __forceinline__ void block_sum3(double& a, double& b, double& c, doub
     red[2][threadIdx.x >> 6] = c;
   }
   __syncthreads();
-  a = ((red[0][0] + red[0][1]) + red[0][2]) + red[0][3];
-  b = ((red[1][0] + red[1][1]) + red[1][2]) + red[1][3];
-  c = ((red[2][0] + red[2][1]) + red[2][2]) + red[2][3];
+  a = red[0][0];
+  b = red[1][0];
+  c = red[2][0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) {
+    a += red[0][w];
+    b += red[1][w];
+    c += red[2][w];
+  }
+}
+
+// The held rows of Phi marked as rewritten (an empty statement, in place), so
+// that their fp64 conversions are neither hoisted out of the step loop nor
+// shared between a step's two uses (converted once they would need twice the
+// registers).  In place: the registers must all be VGPRs, or each one held in
+// an accumulation register is moved out and back.
+template <int RB, int NH>
+__device__ __forceinline__ void launder_rows(float4 (&ph)[RB][NH]) {
+#pragma unroll
+  for (int r = 0; r < RB; ++r)
+#pragma unroll
+    for (int h = 0; h < NH; ++h)
+      asm volatile("" : "+v"(ph[r][h].x), "+v"(ph[r][h].y), "+v"(ph[r][h].z), "+v"(ph[r][h].w));
 }
 
 }  // namespace
 
-// RB rows per block; CPL = m / 256 columns per lane (the lane's columns are
+// RB rows per block; CPL = m / NT columns per lane (the lane's columns are
 // 64 CPL w + 256 h + 4 lane + e for wave w, h < CPL / 4, e < 4).
 // Workspace use: Spart [m / CB][nb][CB] (CB = m / nb), H2part [nb][ldq + 1], H2 [ldq + 1], T [m],
 // Apart [nb]; outputs alpha, beta, neff, stop and Q[1..] as the streaming path.
 // Dynamic LDS: the block's rows of Q, (n_it + 1) (RB + 1) doubles.
-template <int RB, int CPL>
-__global__ __launch_bounds__(LR_T, 1) void k_lz_resident(LanczosWS w, unsigned* bar,
-                                                         const double* __restrict__ q1) {
-  constexpr int NH = CPL / 4, KG = LR_T / RB, QS = RB + 1;   // QS: row stride of Qs (bank spread)
-  static_assert(CPL % 4 == 0 && RB % 8 == 0 && LR_T % RB == 0, "shape");
+// NT threads per block (NW = NT / 64 waves); INPLACE: the held rows fit in
+// VGPRs (two waves per SIMD: 128 floats a lane) and are laundered in place once
+// per use, else (one wave per SIMD, 256 floats a lane, part of them in
+// accumulation registers) each use goes through pin4.
+template <int RB, int CPL, int NT>
+__global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* bar,
+                                                       const double* __restrict__ q1) {
+  constexpr int NW = NT / 64, NH = CPL / 4, KG = NT / RB, QS = RB + 1;   // QS: row stride of Qs (bank spread)
+  constexpr bool INPLACE = RB * CPL <= 128;
+  static_assert(CPL % 4 == 0 && RB % 8 == 0 && NT % RB == 0, "shape");
   const int b = blockIdx.x, nb = gridDim.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int L = w.L, m = w.m, n_it = w.n_it, ldq = w.ldq, hs = ldq + 1;
   const int r0 = b * RB;
   const int cb = wv * 64 * CPL + 4 * lane;
   extern __shared__ double Qs[];                 // [n_it + 1][QS]
   __shared__ double h2s[256], gs[256], als[256], bes[256];
-  __shared__ double prw[4][RB];
+  __shared__ double prw[NW][RB];
   __shared__ double zs[RB], qr[RB], qmr[RB], sgr[RB];
   __shared__ double rq[KG][RB + 1], rg[KG][RB + 1];
-  __shared__ double red[3][4];
-  __shared__ double cpart[LR_T];
+  __shared__ double red[3][NW];
+  __shared__ double cpart[NT];
   double* Spart = w.Spart;
   double* Hpart = w.H2part;
   double* H2 = w.H2;
@@ -194,12 +220,13 @@ __global__ __launch_bounds__(LR_T, 1) void k_lz_resident(LanczosWS w, unsigned* 
     double col[CPL];
 #pragma unroll
     for (int c = 0; c < CPL; ++c) col[c] = 0.0;
+    if constexpr (INPLACE) launder_rows(ph);
 #pragma unroll
     for (int r = 0; r < RB; ++r) {
       const double z = zs[r];
 #pragma unroll
       for (int h = 0; h < NH; ++h) {
-        const float4 x = pin4(ph[r][h]);
+        const float4 x = INPLACE ? ph[r][h] : pin4(ph[r][h]);
         col[4 * h + 0] = fma((double)x.x, z, col[4 * h + 0]);
         col[4 * h + 1] = fma((double)x.y, z, col[4 * h + 1]);
         col[4 * h + 2] = fma((double)x.z, z, col[4 * h + 2]);
@@ -224,11 +251,11 @@ __global__ __launch_bounds__(LR_T, 1) void k_lz_resident(LanczosWS w, unsigned* 
   // partials of a lane, the |z1|^2 partial and the h2 partial are polled
   // together.  false when a wait failed.
   auto col_reduce = [&](bool norm, double& z2v, int e, int kh) -> bool {
-    const int CB = m / nb, PL = LR_T / CB;
+    const int CB = m / nb, PL = NT / CB;
     const int c = b * CB + tid % CB;
     const int64_t base = (int64_t)b * nb * CB + tid;
     double v[CPL], zv[1], hv[1];
-    bool ok = ld_wait<CPL>([&](int u) { return Spart + base + u * LR_T; }, (1u << CPL) - 1u, e, bar, v);
+    bool ok = ld_wait<CPL>([&](int u) { return Spart + base + u * NT; }, (1u << CPL) - 1u, e, bar, v);
     if (norm)
       ok = ld_wait<1>([&](int) { return Hpart + (int64_t)tid * hs + ldq; }, tid < nb ? 1u : 0u, e,
                       bar, zv) && ok;
@@ -291,7 +318,8 @@ __global__ __launch_bounds__(LR_T, 1) void k_lz_resident(LanczosWS w, unsigned* 
     bool ok = ld_wait<CPL>([&](int u) { return Tv + cb + 256 * (u >> 2) + (u & 3); }, (1u << CPL) - 1u,
                            j, bar, tv);
     // Phi t~ of the block's rows: 4 CPL products per lane and row, summed over
-    // the wave 8 rows at a time (into prw), then over the 4 waves
+    // the wave 8 rows at a time (into prw), then over the NW waves
+    if constexpr (INPLACE) launder_rows(ph);
 #pragma unroll
     for (int r8 = 0; r8 < RB; r8 += 8) {
       double d[8];
@@ -300,7 +328,7 @@ __global__ __launch_bounds__(LR_T, 1) void k_lz_resident(LanczosWS w, unsigned* 
         double x = 0.0;
 #pragma unroll
         for (int h = 0; h < NH; ++h) {
-          const float4 y = pin4(ph[r8 + e][h]);
+          const float4 y = INPLACE ? ph[r8 + e][h] : pin4(ph[r8 + e][h]);
           x = fma((double)y.x, tv[4 * h + 0], x);
           x = fma((double)y.y, tv[4 * h + 1], x);
           x = fma((double)y.z, tv[4 * h + 2], x);
@@ -386,7 +414,9 @@ __global__ __launch_bounds__(LR_T, 1) void k_lz_resident(LanczosWS w, unsigned* 
     __syncthreads();
     if (tid < RB) {
       const int i = tid;
-      double u = ((prw[0][i] + prw[1][i]) + prw[2][i]) + prw[3][i];
+      double u = prw[0][i];
+#pragma unroll
+      for (int q = 1; q < NW; ++q) u += prw[q][i];
       const double q = qr[i];
       if (j > 0) u = (fma(sqrt(z2), u, -sgr[i]) - beta * h2last * q) / beta;
       const double z = (u - alpha * q) - beta * qmr[i];
@@ -395,7 +425,7 @@ __global__ __launch_bounds__(LR_T, 1) void k_lz_resident(LanczosWS w, unsigned* 
     __syncthreads();
     // partials of h2 = Q_j^T z1 (k <= j) and of |z1|^2, then of Phi^T z1 (the
     // small stores ahead of the 16 KB of column partials)
-    for (int k = tid; k <= j + 1; k += LR_T) {
+    for (int k = tid; k <= j + 1; k += NT) {
       double v = 0.0;
       double a4[4] = {0.0, 0.0, 0.0, 0.0};
       const double* qk = (k <= j) ? Qs + k * QS : zs;
@@ -462,33 +492,34 @@ __global__ void k_lz_res_prep(LanczosWS w, const double* __restrict__ q1, ResCle
 
 namespace {
 struct ResShape {
-  int rb, nb;
+  int rb, nb, nt;   // rows per block, blocks, threads per block
 };
-// rows per block for the resident kernel, or rb = 0 when the shape does not
-// qualify: one window, m of 1024 or 2048, nb = ceil(L / rb) rounded up to a
-// power of two, dividing m, at most one block per compute unit and per row group of the
+// The resident kernel's shape, or rb = 0 when it does not qualify: one window,
+// m of 1024 (256 threads, 4 columns a lane) or 2048 (512 threads, 4 columns a
+// lane), rb of 32 or 16 rows a block, nb = ceil(L / rb) rounded up to a power of
+// two, dividing m, at most one block per compute unit and per row group of the
 // workspace, n_it <= 256
 ResShape res_shape(const LanczosWS& w, int n_cu) {
-  ResShape s{0, 0};
+  ResShape s{0, 0, 0};
   if (w.n_act != 1 || (w.m != 1024 && w.m != 2048) || w.n_it > 256 || w.n_it < 1) return s;
-  const int cpl = w.m / 256;
+  const int nt = w.m == 2048 ? 512 : LR_T;
   for (int rb : {32, 16}) {
-    if (rb * cpl > 256) continue;              // registers: rb * cpl floats per lane
     int nb = 1;                                // ceil(L / rb) rounded up to a power of two
     while (nb * rb < w.L) nb *= 2;             // (blocks past the last row hold zeros)
-    if (nb > n_cu || nb > w.G3 || (nb & (nb - 1)) != 0 || w.m % nb != 0 || w.m / nb > LR_T ||
+    if (nb > n_cu || nb > w.G3 || (nb & (nb - 1)) != 0 || w.m % nb != 0 || w.m / nb > nt ||
         w.m / nb < 4)
       continue;   // (G3 row groups: the rows of Spart and H2part)
     s.rb = rb;
     s.nb = nb;
+    s.nt = nt;
     return s;
   }
   return s;
 }
-template <int RB, int CPL>
+template <int RB, int CPL, int NT>
 hipError_t launch_res_t(const LanczosWS& w, const ResShape& sh, unsigned* bar, const double* q1,
                         bool check, hipStream_t s) {
-  auto k = k_lz_resident<RB, CPL>;
+  auto k = k_lz_resident<RB, CPL, NT>;
   const size_t lds = (size_t)(w.n_it + 1) * (RB + 1) * sizeof(double);
   if (lds > 65536) {
     const hipError_t e =
@@ -497,19 +528,19 @@ hipError_t launch_res_t(const LanczosWS& w, const ResShape& sh, unsigned* bar, c
   }
   if (check) {
     int per_cu = 0;
-    const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)k, LR_T, lds);
+    const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)k, NT, lds);
     if (e != hipSuccess) return e;
     return per_cu >= 1 ? hipSuccess : hipErrorInvalidConfiguration;
   }
-  hipLaunchKernelGGL(k, dim3(sh.nb), dim3(LR_T), lds, s, w, bar, q1);
+  hipLaunchKernelGGL(k, dim3(sh.nb), dim3(NT), lds, s, w, bar, q1);
   return hipGetLastError();
 }
 hipError_t launch_res(const LanczosWS& w, const ResShape& sh, unsigned* bar, const double* q1,
                       bool check, hipStream_t s) {
-  if (w.m == 2048) return sh.rb == 32 ? launch_res_t<32, 8>(w, sh, bar, q1, check, s)
-                                      : launch_res_t<16, 8>(w, sh, bar, q1, check, s);
-  return sh.rb == 32 ? launch_res_t<32, 4>(w, sh, bar, q1, check, s)
-                     : launch_res_t<16, 4>(w, sh, bar, q1, check, s);
+  if (w.m == 2048) return sh.rb == 32 ? launch_res_t<32, 4, 512>(w, sh, bar, q1, check, s)
+                                      : launch_res_t<16, 4, 512>(w, sh, bar, q1, check, s);
+  return sh.rb == 32 ? launch_res_t<32, 4, LR_T>(w, sh, bar, q1, check, s)
+                     : launch_res_t<16, 4, LR_T>(w, sh, bar, q1, check, s);
 }
 }  // namespace
 
