@@ -247,11 +247,11 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
   // t over the block's columns from the partials of step e (scaled by 1 / |z1|
   // when norm, |z1|^2 summed here from its partials first), and the block's
   // partial of |t|^2, tagged with step e; with kh >= 0 also the h2 entry kh.
-  // Thread = (column cl < CB, partial lane pl < PL); the nb / PL = CPL
+  // Thread = (column cl < CB, partial lane pl < NT / CB); the CPL
   // partials of a lane, the |z1|^2 partial and the h2 partial are polled
   // together.  false when a wait failed.
   auto col_reduce = [&](bool norm, double& z2v, int e, int kh) -> bool {
-    const int CB = m / nb, PL = NT / CB;
+    const int CB = m / nb;
     const int c = b * CB + tid % CB;
     const int64_t base = (int64_t)b * nb * CB + tid;
     double v[CPL], zv[1], hv[1];
@@ -272,12 +272,16 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
     double sm = 0.0;
 #pragma unroll
     for (int u = 0; u < CPL; ++u) sm += v[u];
-    cpart[tid] = sm;
+    // a column's partial lanes within a wave lie CB lanes apart: an xor
+    // butterfly over them (both lanes of a pair get the same sum), then the
+    // waves' sums (for CB >= 64, the column's lanes) in order
+    for (int o = CB; o < 64; o <<= 1) sm += __shfl_xor(sm, o);
+    const int SD = CB < 64 ? 64 : CB;
+    if (lane < CB) cpart[tid] = sm;
     __syncthreads();
     if (tid < CB) {
       double S = 0.0;
-#pragma unroll 8
-      for (int p = 0; p < PL; ++p) S += cpart[p * CB + tid];
+      for (int p = 0; p < NT / SD; ++p) S += cpart[p * SD + tid];
       const double t = norm ? (z2v > 0.0 ? S / sqrt(z2v) : 0.0) : S;
       st_tag(Tv + c, t, e);
       cpart[tid] = t * t;
