@@ -50,6 +50,8 @@ __device__ __forceinline__ unsigned ld_flag(unsigned* p) {
 
 // bar: [LR_ERR] error word
 constexpr int LR_ERR = LZ_BAR_ERR;
+// copies of t~ (T holds [ldq][m] doubles)
+__host__ __device__ constexpr int res_copies(int ldq) { return ldq < 8 ? ldq : 8; }
 
 // v tagged with step e into *p
 __device__ __forceinline__ void st_tag(double* p, double v, int e) {
@@ -162,8 +164,10 @@ __device__ __forceinline__ void launder_rows(float4 (&ph)[RB][NH]) {
 
 // RB rows per block; CPL = m / NT columns per lane (the lane's columns are
 // 64 CPL w + 256 h + 4 lane + e for wave w, h < CPL / 4, e < 4).
-// Workspace use: Spart [m / CB][nb][CB] (CB = m / nb), H2part [nb][ldq + 1], H2 [ldq + 1], T [m],
-// Apart [nb]; outputs alpha, beta, neff, stop and Q[1..] as the streaming path.
+// Workspace use: Spart [m / CB][nb][CB] (CB = m / nb), H2part [nb][ldq + 1], H2 [ldq + 1],
+// T [C][m] with C = res_copies(ldq) (t~ written to every copy, block b reading
+// copy b mod C, so that the blocks' polls of t~ spread over C times as many
+// lines), Apart [nb]; outputs alpha, beta, neff, stop and Q[1..] as the streaming path.
 // Dynamic LDS: the block's rows of Q, (n_it + 1) (RB + 1) doubles.
 // NT threads per block (NW = NT / 64 waves); INPLACE: the held rows fit in
 // VGPRs (two waves per SIMD: 128 floats a lane) and are laundered in place once
@@ -185,11 +189,13 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
   __shared__ double zs[RB], qr[RB], qmr[RB], sgr[RB];
   __shared__ double rq[KG][RB + 1], rg[KG][RB + 1];
   __shared__ double red[3][NW];
-  __shared__ double cpart[NT];
+  __shared__ double cpart[NT], tsq[NT];
+  const int ntc = res_copies(ldq);
   double* Spart = w.Spart;
   double* Hpart = w.H2part;
   double* H2 = w.H2;
   double* Tv = w.T;
+  double* const Tr = w.T + (int64_t)(b % ntc) * m;   // the copy of t~ this block reads
   double* Ap = w.Apart;
 
   // the block's rows of Phi (rows past L are zero) and of q_0
@@ -252,7 +258,6 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
   // together.  false when a wait failed.
   auto col_reduce = [&](bool norm, double& z2v, int e, int kh) -> bool {
     const int CB = m / nb;
-    const int c = b * CB + tid % CB;
     const int64_t base = (int64_t)b * nb * CB + tid;
     double v[CPL], zv[1], hv[1];
     bool ok = ld_wait<CPL>([&](int u) { return Spart + base + u * NT; }, (1u << CPL) - 1u, e, bar, v);
@@ -279,17 +284,19 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
     const int SD = CB < 64 ? 64 : CB;
     if (lane < CB) cpart[tid] = sm;
     __syncthreads();
-    if (tid < CB) {
+    // thread (copy r, column cl) sums the column (the same sum in every copy)
+    for (int q = tid; q < CB * ntc; q += NT) {
+      const int cl = q % CB, r = q / CB;
       double S = 0.0;
-      for (int p = 0; p < NT / SD; ++p) S += cpart[p * SD + tid];
+      for (int p = 0; p < NT / SD; ++p) S += cpart[p * SD + cl];
       const double t = norm ? (z2v > 0.0 ? S / sqrt(z2v) : 0.0) : S;
-      st_tag(Tv + c, t, e);
-      cpart[tid] = t * t;
+      st_tag(Tv + (int64_t)r * m + b * CB + cl, t, e);
+      if (r == 0) tsq[cl] = t * t;
     }
     __syncthreads();
     if (tid == 0) {
       double a2 = 0.0;
-      for (int q = 0; q < CB; ++q) a2 += cpart[q];
+      for (int q = 0; q < CB; ++q) a2 += tsq[q];
       st_tag(Ap + b, a2, e);
     }
     return true;
@@ -319,7 +326,7 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
     // own entries of t~ have arrived (the scalars of the step wait for values
     // of every block).
     double tv[CPL], a1[1], h1[1];
-    bool ok = ld_wait<CPL>([&](int u) { return Tv + cb + 256 * (u >> 2) + (u & 3); }, (1u << CPL) - 1u,
+    bool ok = ld_wait<CPL>([&](int u) { return Tr + cb + 256 * (u >> 2) + (u & 3); }, (1u << CPL) - 1u,
                            j, bar, tv);
     // Phi t~ of the block's rows: 4 CPL products per lane and row, summed over
     // the wave 8 rows at a time (into prw), then over the NW waves
@@ -569,7 +576,7 @@ hipError_t launch_lanczos_resident(const LanczosWS& w, const double* q1_act, uns
   ResClear z;
   const double* const bufs[6] = {(const double*)bar, w.Spart, w.H2part, w.T, w.Apart, w.H2};
   const int64_t lens[6] = {(int64_t)lanczos_resident_bar_words(n_cu) / 2, (int64_t)sh.nb * w.m,
-                           (int64_t)sh.nb * hs, (int64_t)w.m, (int64_t)sh.nb, hs};
+                           (int64_t)sh.nb * hs, (int64_t)res_copies(w.ldq) * w.m, (int64_t)sh.nb, hs};
   for (int q = 0; q < 6; ++q) {
     z.p[q] = const_cast<double*>(bufs[q]);
     z.n[q] = lens[q];
