@@ -223,43 +223,79 @@ __device__ __forceinline__ void store_unit_column(const double* y, int n, int n_
   for (int i = lane; i < n_it; i += 64) Sa[(int64_t)i * r + k] = (i < n) ? y[i] * sc : 0.0;
 }
 
-// Eigenvector of an isolated eigenvalue th of the unreduced tridiagonal T by
-// the twisted factorisation (Parlett and Dhillon): the top-down pivots dp of
-// T - th I = L D L^T and the bottom-up pivots dm of U D U^T (the Sturm
-// recurrence run from either end by lane 0 of waves 0 and 1 side by side, each
-// pivot below pivmin in magnitude replaced by -pivmin), the twist
-// gamma_k = dp_k + dm_k - (alpha_k - th), k the index of the smallest
-// |gamma_k| (the first of equals), and z with z_k = 1 solving N_k^T z = e_k:
-// z_i = -(beta_i / dp_i) z_(i+1) below k, z_i = -(beta_(i-1) / dm_i) z_(i-1)
-// above (the two lanes again).  Then (T - th I) z = gamma_k e_k in exact
-// arithmetic, and one inverse-iteration step with the same factors,
-// x = (T - th I)^-1 z, squares the error the first solve leaves (a vector
-// from one solve is orthogonal to a neighbour's only to about eps |T| / gap).
-// Accepted (true, x / |x|_inf in y) when every entry is finite and
-// |(T - th I) x|_inf <= 64 eps |T| |x|_inf, the level inverse iteration
-// reaches; every thread of the block must call it (it contains barriers).
-// dp, dm, ratios and scratch use the caller's LDS arrays.  The serial
-// recurrences take their operands from LDS TV_U steps ahead; each runs on a
-// wave of its own, so that its indices stay wave-uniform (with both on lanes
-// of one wave, the per-lane index arithmetic and masking doubled each step).
-constexpr int TV_U = 8;
-
-// one lane: s = 0 .. cnt - 1 along index idx(s), operands
-// fetched TV_U steps at a time by ld(i, ...) (the index clamped to [0, n), so
-// the surplus fetches past cnt stay in bounds), then the dependent update
-// st(i, ...) in order; mx >= cnt is the trip count
-template <class IDX, class LD, class ST>
-__device__ __forceinline__ void tv_chain(int n, int cnt, int mx, IDX idx, LD ld, ST st) {
+// The leading (fw) or trailing principal minors q_s of T - th I, s = 0 .. n - 1
+// along rows i = s (fw) or i = n - 1 - s, q_(-1) = 1: q_s = A_s q_(s-1) - B_s
+// q_(s-2), with the operands of the scaled matrix of multisect in step order
+// (A_s = (alpha_i - th) / 2^esc; B_s = beta_(i-1)^2 / 4^esc going down, beta_i^2
+// / 4^esc going up), zero past n up to a multiple of 8 and 16-byte aligned.
+// One FMA per step on the dependent chain; the pair (q_s, q_(s-1)) is rescaled
+// by a power of two after every 8 steps as in sturm_count.  minors_chain runs
+// the chain on one lane and keeps only the pair entering each group of 8 steps
+// (ck[2 g], ck[2 g + 1]); minors_group then replays group g from its pair --
+// the same operations in the same order, so the same values -- into qn[i] =
+// q_s and qd[i] = q_(s-1), one scale for both, so that the pivot of row i is
+// qn[i] / qd[i] (times 2^esc).  The groups replay side by side, a thread each.
+__device__ __forceinline__ void minors_load8(const double* A, const double* B, int s0,
+                                             double2 (&a)[4], double2 (&b)[4]) {
+  const double2* a2 = reinterpret_cast<const double2*>(A + s0);
+  const double2* b2 = reinterpret_cast<const double2*>(B + s0);
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    a[u] = a2[u];
+    b[u] = b2[u];
+  }
+}
+__device__ __forceinline__ double minors_step(double a, double b, double& pm, double& pc) {
+  const double pn = fma(a, pc, -(b * pm));
+  pm = pc;
+  pc = pn;
+  return pn;
+}
+__device__ __forceinline__ void minors_chain(const double* A, const double* B, int n, double* ck) {
   n = __builtin_amdgcn_readfirstlane(n);
-  cnt = __builtin_amdgcn_readfirstlane(cnt);
-  mx = __builtin_amdgcn_readfirstlane(mx);
-  for (int s0 = 0; s0 < mx; s0 += TV_U) {
-    double o0[TV_U], o1[TV_U];
+  double pm = 0.0, pc = 1.0;
+  auto run8 = [&](int s0, const double2 (&a)[4], const double2 (&b)[4]) {
+    ck[s0 / 4] = pm;
+    ck[s0 / 4 + 1] = pc;
 #pragma unroll
-    for (int u = 0; u < TV_U; ++u) ld(min(max(idx(min(s0 + u, cnt - 1)), 0), n - 1), o0[u], o1[u]);
+    for (int u = 0; u < 4; ++u) {        // steps past n change nothing that is kept
+      minors_step(a[u].x, b[u].x, pm, pc);
+      minors_step(a[u].y, b[u].y, pm, pc);
+    }
+    const int e = __builtin_amdgcn_frexp_exp(fmax(fabs(pc), fabs(pm)));
+    pc = __builtin_amdgcn_ldexp(pc, -e);
+    pm = __builtin_amdgcn_ldexp(pm, -e);
+  };
+  // the operands of the next 8 steps are read while these run
+  double2 a0[4], b0[4], a1[4], b1[4];
+  minors_load8(A, B, 0, a0, b0);
+  int s0 = 0;
+  for (; s0 + 8 < n; s0 += 16) {
+    minors_load8(A, B, s0 + 8, a1, b1);
+    run8(s0, a0, b0);
+    if (s0 + 16 < n) minors_load8(A, B, s0 + 16, a0, b0);
+    run8(s0 + 8, a1, b1);
+  }
+  if (s0 < n) run8(s0, a0, b0);
+}
+__device__ __forceinline__ void minors_group(const double* A, const double* B, int n, bool fw,
+                                             const double* ck, int g, double* qn, double* qd) {
+  double2 a[4], b[4];
+  minors_load8(A, B, 8 * g, a, b);
+  double pm = ck[2 * g], pc = ck[2 * g + 1];
+  auto put = [&](int s, double pq, double pn) {
+    if (s < n) {
+      const int i = fw ? s : n - 1 - s;
+      qn[i] = pn;
+      qd[i] = pq;
+    }
+  };
 #pragma unroll
-    for (int u = 0; u < TV_U; ++u)
-      if (s0 + u < cnt) st(idx(s0 + u), o0[u], o1[u]);
+  for (int u = 0; u < 4; ++u) {
+    double pq = pc;
+    put(8 * g + 2 * u, pq, minors_step(a[u].x, b[u].x, pm, pc));
+    pq = pc;
+    put(8 * g + 2 * u + 1, pq, minors_step(a[u].y, b[u].y, pm, pc));
   }
 }
 
@@ -308,36 +344,78 @@ __device__ __forceinline__ void wave_affine_scan(int cnt, double x0, LD ld, ST s
   }
 }
 
+// Eigenvector of an isolated eigenvalue th of the unreduced tridiagonal T by
+// the twisted factorisation (Parlett and Dhillon): the top-down pivots dp of
+// T - th I = L D L^T and the bottom-up pivots dm of U D U^T (ratios of
+// consecutive leading and trailing principal minors: the two minors
+// recurrences run by lane 0 of waves 0 and 1 side by side, their groups of 8
+// steps replayed and the divisions made by every thread; each pivot below pivmin in magnitude replaced by
+// -pivmin), the twist gamma_k = dp_k + dm_k - (alpha_k - th), k the index of
+// the smallest |gamma_k| (the first of equals), and z with z_k = 1 solving
+// N_k^T z = e_k:
+// z_i = -(beta_i / dp_i) z_(i+1) below k, z_i = -(beta_(i-1) / dm_i) z_(i-1)
+// above (the two lanes again).  Then (T - th I) z = gamma_k e_k in exact
+// arithmetic, and one inverse-iteration step with the same factors,
+// x = (T - th I)^-1 z, squares the error the first solve leaves (a vector
+// from one solve is orthogonal to a neighbour's only to about eps |T| / gap).
+// Accepted (true, x / |x|_inf in y) when every entry is finite and
+// |(T - th I) x|_inf <= 64 eps |T| |x|_inf, the level inverse iteration
+// reaches; every thread of the block must call it (it contains barriers).
+// dp, dm, ratios and scratch use the caller's LDS arrays; an, b2s and esc are
+// the scaled operands multisect leaves.
 __device__ __forceinline__ bool twisted_vector(const double* al, const double* b1, const double* b2,
+                                            const double* an, const double* b2s, int esc,
                                             int n, double th, double tnorm, double pivmin,
                                             double* dp, double* dm, double* rat, double* sc,
                                             double* tw, double* y) {
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   __shared__ int kst;
   __shared__ double mred[2][EIG_T / 64];
-  if (tid == 0 || tid == 64) {
-    // wave-uniform in the one active lane, so indices and branches stay scalar
-    const bool fw = __builtin_amdgcn_readfirstlane(tid) == 0;
-    double* out = fw ? dp : dm;
-    double d = 0.0;
-    tv_chain(n, n, n, [&](int s2) { return fw ? s2 : n - 1 - s2; },
-             [&](int i, double& am, double& bb) {
-               am = al[i] - th;
-               bb = fw ? b2[max(i - 1, 0)] : b2[i];
-             },
-             [&](int i, double am, double bb) {
-               d = (i == (fw ? 0 : n - 1)) ? am : am - bb * rcp_nr(d);
-               if (fabs(d) < pivmin) d = -pivmin;
-               out[i] = d;
-             });
+  __shared__ double qm[4][EIG_NMAX];              // leading minors (qn, qd), then trailing
+  __shared__ __align__(16) double mop[4][EIG_NMAX + 8];   // A, B going down, then going up
+  __shared__ double ck[2][EIG_NMAX / 4];          // the pairs entering each group of 8 steps
+  const double thn = __builtin_amdgcn_ldexp(th, -esc);
+  const int ng = (n + 7) >> 3;                    // groups of 8 steps per direction
+  for (int s = tid; s < 8 * ng; s += EIG_T) {
+    const bool in = s < n;
+    mop[0][s] = in ? an[s] - thn : 0.0;
+    mop[1][s] = in ? b2s[s] : 0.0;
+    mop[2][s] = in ? an[n - 1 - s] - thn : 0.0;
+    mop[3][s] = in ? b2s[min(n - s, n - 1)] : 0.0;
   }
   __syncthreads();
-  // |gamma_k| into sc; the ratios rat[i] = beta_i / dp_i (i < n - 1) and
-  // y[i] = beta_(i-1) / dm_i (i > 0)
+  if (tid == 0 || tid == 64) {
+    // wave-uniform in the one active lane, so indices and branches stay scalar
+    const int h = __builtin_amdgcn_readfirstlane(tid) == 0 ? 0 : 2;
+    minors_chain(mop[h], mop[h + 1], n, ck[h / 2]);
+  }
+  __syncthreads();
+  if (tid < 2 * ng) {
+    const bool fw = tid < ng;
+    const int h = fw ? 0 : 2;
+    minors_group(mop[h], mop[h + 1], n, fw, ck[h / 2], fw ? tid : tid - ng, qm[h], qm[h + 1]);
+  }
+  __syncthreads();
+  // The pivots, dp_i = q_i / q_(i-1) of the leading minors and dm_i of the
+  // trailing ones; a pivot below pivmin in magnitude (or no number: a zero
+  // minor before it) becomes -pivmin, and the pivot after a replaced one is
+  // formed from the replacement, (alpha - th) - beta^2 / (-pivmin), as the
+  // pivot recurrence d_i = (alpha_i - th) - beta^2 / d_(i-1) does.  Then
+  // |gamma_k| into sc and the ratios rat[i] = beta_i / dp_i (i < n - 1) and
+  // y[i] = beta_(i-1) / dm_i (i > 0).
+  auto small = [&](double d) { return !(fabs(d) >= pivmin); };
+  auto ratio = [&](int h, int k) { return __builtin_amdgcn_ldexp(qm[h][k] / qm[h + 1][k], esc); };
   for (int i = tid; i < n; i += EIG_T) {
-    sc[i] = fabs(dp[i] + dm[i] - (al[i] - th));
-    rat[i] = (i < n - 1) ? b1[i] / dp[i] : 0.0;
-    y[i] = (i > 0) ? b1[i - 1] / dm[i] : 0.0;
+    const double am = al[i] - th;
+    double p = (i > 0 && small(ratio(0, i - 1))) ? am + b2[i - 1] / pivmin : ratio(0, i);
+    double q = (i < n - 1 && small(ratio(2, i + 1))) ? am + b2[i] / pivmin : ratio(2, i);
+    if (small(p)) p = -pivmin;
+    if (small(q)) q = -pivmin;
+    dp[i] = p;
+    dm[i] = q;
+    sc[i] = fabs(p + q - am);
+    rat[i] = (i < n - 1) ? b1[i] / p : 0.0;
+    y[i] = (i > 0) ? b1[i - 1] / q : 0.0;
   }
   __syncthreads();
   if (wv == 0) {
@@ -498,7 +576,7 @@ __global__ __launch_bounds__(EIG_T) void k_eig_pairs(const double* __restrict__ 
       cnt2[tid] = sturm_count(an, b2s, n, __builtin_amdgcn_ldexp(tid ? th + ctol : th - ctol, -esc));
     __syncthreads();
     if (cnt2[1] - cnt2[0] == 1 &&
-        twisted_vector(al, b1, b2, n, th, ti.tnorm, DBL_MIN * fmax(1.0, ti.bmax), fd, fl, fu1,
+        twisted_vector(al, b1, b2, an, b2s, esc, n, th, ti.tnorm, DBL_MIN * fmax(1.0, ti.bmax), fd, fl, fu1,
                        fu2, w, y)) {
       if (wv == 0) store_unit_column(y, n, n_it, r, c, Sa);
       return;
