@@ -423,29 +423,35 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
       sgr[i] = sg;
     }
     __syncthreads();
-    if (tid < RB) {
-      const int i = tid;
-      double u = prw[0][i];
+    // z1 of the block's rows, and their partial of |z1|^2 (wave 0 holds the RB rows)
+    if (tid < 64) {
+      double z = 0.0;
+      if (tid < RB) {
+        const int i = tid;
+        double u = prw[0][i];
 #pragma unroll
-      for (int q = 1; q < NW; ++q) u += prw[q][i];
-      const double q = qr[i];
-      if (j > 0) u = (fma(sqrt(z2), u, -sgr[i]) - beta * h2last * q) / beta;
-      const double z = (u - alpha * q) - beta * qmr[i];
-      zs[i] = (r0 + i < L) ? z : 0.0;
+        for (int q = 1; q < NW; ++q) u += prw[q][i];
+        const double q = qr[i];
+        if (j > 0) u = (fma(sqrt(z2), u, -sgr[i]) - beta * h2last * q) / beta;
+        z = (u - alpha * q) - beta * qmr[i];
+        z = (r0 + i < L) ? z : 0.0;
+        zs[i] = z;
+      }
+      const double zz = wave_sum_f64(z * z);
+      if (tid == 0) st_tag(Hpart + (int64_t)b * hs + ldq, zz, j + 1);
     }
     __syncthreads();
-    // partials of h2 = Q_j^T z1 (k <= j) and of |z1|^2, then of Phi^T z1 (the
-    // small stores ahead of the 16 KB of column partials)
-    for (int k = tid; k <= j + 1; k += NT) {
-      double v = 0.0;
+    // partials of Phi^T z1, then of h2 = Q_j^T z1 (k <= j): the h2 partials are
+    // read only after the column partials have been reduced, so they are formed
+    // while those travel
+    col_partials(j + 1);
+    for (int k = tid; k <= j; k += NT) {
       double a4[4] = {0.0, 0.0, 0.0, 0.0};
-      const double* qk = (k <= j) ? Qs + k * QS : zs;
+      const double* qk = Qs + k * QS;
 #pragma unroll
       for (int i = 0; i < RB; ++i) a4[i & 3] = fma(qk[i], zs[i], a4[i & 3]);
-      v = (a4[0] + a4[1]) + (a4[2] + a4[3]);
-      st_tag(Hpart + (int64_t)b * hs + (k <= j ? k : ldq), v, j + 1);
+      st_tag(Hpart + (int64_t)b * hs + k, (a4[0] + a4[1]) + (a4[2] + a4[3]), j + 1);
     }
-    col_partials(j + 1);
     // ---- columns: |z1|^2 (every block), t~_{j+1}, h2
     int k0 = b;                                   // h2 entries of this block: b, b + nb, ...
     if (j + 1 < n_it) {
