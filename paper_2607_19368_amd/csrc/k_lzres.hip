@@ -104,6 +104,15 @@ __device__ __forceinline__ bool ld_wait(ADDR addr, unsigned act, int e, unsigned
   return ok;
 }
 
+// Every store this thread issued acknowledged (vmcnt counts stores as well as
+// loads here), then a block barrier: the block's polls that follow do not
+// compete in the CU's memory path with its own stores, which other blocks are
+// waiting for.
+__device__ __forceinline__ void stores_done_barrier() {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+}
+
 // true in every thread when no thread of the block saw a failure (a barrier)
 __device__ __forceinline__ bool block_ok(bool ok) {
   __shared__ int bad;
@@ -167,7 +176,8 @@ __device__ __forceinline__ void launder_rows(float4 (&ph)[RB][NH]) {
 // Workspace use: Spart [m / CB][nb][CB] (CB = m / nb), H2part [nb][ldq + 1], H2 [ldq + 1],
 // T [C][m] with C = res_copies(ldq) (t~ written to every copy, block b reading
 // copy b mod C, so that the blocks' polls of t~ spread over C times as many
-// lines), Apart [nb]; outputs alpha, beta, neff, stop and Q[1..] as the streaming path.
+// lines); outputs alpha, beta, neff, stop and Q[1..] as the streaming path.
+// A block waits for its own stores before it starts polling (stores_done_barrier).
 // Dynamic LDS: the block's rows of Q, (n_it + 1) (RB + 1) doubles.
 // NT threads per block (NW = NT / 64 waves); INPLACE: the held rows fit in
 // VGPRs (two waves per SIMD: 128 floats a lane) and are laundered in place once
@@ -189,14 +199,13 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
   __shared__ double zs[RB], qr[RB], qmr[RB], sgr[RB];
   __shared__ double rq[KG][RB + 1], rg[KG][RB + 1];
   __shared__ double red[3][NW];
-  __shared__ double cpart[NT], tsq[NT];
+  __shared__ double cpart[NT];
   const int ntc = res_copies(ldq);
   double* Spart = w.Spart;
   double* Hpart = w.H2part;
   double* H2 = w.H2;
   double* Tv = w.T;
   double* const Tr = w.T + (int64_t)(b % ntc) * m;   // the copy of t~ this block reads
-  double* Ap = w.Apart;
 
   // the block's rows of Phi (rows past L are zero) and of q_0
   float4 ph[RB][NH];
@@ -251,14 +260,13 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
     }
   };
   // t over the block's columns from the partials of step e (scaled by 1 / |z1|
-  // when norm, |z1|^2 summed here from its partials first), and the block's
-  // partial of |t|^2, tagged with step e; with kh >= 0 also the h2 entry kh.
-  // Thread = (column cl < CB, partial lane pl < NT / CB); the CPL
-  // partials of a lane, the |z1|^2 partial and the h2 partial are polled
-  // together.  false when a wait failed.
+  // when norm, |z1|^2 summed here from its partials first) into every copy,
+  // tagged with step e; with kh >= 0 first the h2 entry kh.  Thread = (column
+  // cl < CB, partial lane pl < NT / CB).  false when a wait failed.
   auto col_reduce = [&](bool norm, double& z2v, int e, int kh) -> bool {
     const int CB = m / nb;
     const int64_t base = (int64_t)b * nb * CB + tid;
+    stores_done_barrier();
     double v[CPL], zv[1], hv[1];
     bool ok = ld_wait<CPL>([&](int u) { return Spart + base + u * NT; }, (1u << CPL) - 1u, e, bar, v);
     if (norm)
@@ -291,18 +299,13 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
       for (int p = 0; p < NT / SD; ++p) S += cpart[p * SD + cl];
       const double t = norm ? (z2v > 0.0 ? S / sqrt(z2v) : 0.0) : S;
       st_tag(Tv + (int64_t)r * m + b * CB + cl, t, e);
-      if (r == 0) tsq[cl] = t * t;
     }
-    __syncthreads();
-    if (tid == 0) {
-      double a2 = 0.0;
-      for (int q = 0; q < CB; ++q) a2 += tsq[q];
-      st_tag(Ap + b, a2, e);
-    }
+    stores_done_barrier();
     return true;
   };
   // sum over the blocks of the h2 partial k (or |z1|^2 for k = ldq) of step e
   auto hpart_sum = [&](int k, int e, double& out) -> bool {
+    stores_done_barrier();
     double hv[1];
     const bool ok = ld_wait<1>([&](int) { return Hpart + (int64_t)tid * hs + k; }, tid < nb ? 1u : 0u,
                                e, bar, hv);
@@ -325,7 +328,7 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
     // those of this step tagged j + 1.  A wave takes its row dots as soon as its
     // own entries of t~ have arrived (the scalars of the step wait for values
     // of every block).
-    double tv[CPL], a1[1], h1[1];
+    double tv[CPL], h1[1];
     bool ok = ld_wait<CPL>([&](int u) { return Tr + cb + 256 * (u >> 2) + (u & 3); }, (1u << CPL) - 1u,
                            j, bar, tv);
     // Phi t~ of the block's rows: 4 CPL products per lane and row, summed over
@@ -350,10 +353,14 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
       const double tot = wave_sum8_f64(d);
       if ((lane & 7) == 0) prw[wv][r8 + idx] = tot;
     }
-    ok = ld_wait<1>([&](int) { return Ap + tid; }, tid < nb ? 1u : 0u, j, bar, a1) && ok;
     ok = ld_wait<1>([&](int) { return H2 + tid; }, tid < j ? 1u : 0u, j, bar, h1) && ok;
     if (!block_ok(ok)) return;
-    const double apv = a1[0], h2v = h1[0];
+    const double h2v = h1[0];
+    // this thread's share of alpha~ = |t~|^2: every block holds all of t~ and
+    // sums it in the same order, so every block gets the same value
+    double apv = 0.0;
+#pragma unroll
+    for (int u = 0; u < CPL; ++u) apv = fma(tv[u], tv[u], apv);
     if (tid < j) h2s[tid] = h2v;
     __syncthreads();
     // g = T_{j-1} h2 (alpha_k on the diagonal, beta_k beside it; beta_{j-1} is
@@ -582,7 +589,7 @@ hipError_t launch_lanczos_resident(const LanczosWS& w, const double* q1_act, uns
   ResClear z;
   const double* const bufs[6] = {(const double*)bar, w.Spart, w.H2part, w.T, w.Apart, w.H2};
   const int64_t lens[6] = {(int64_t)lanczos_resident_bar_words(n_cu) / 2, (int64_t)sh.nb * w.m,
-                           (int64_t)sh.nb * hs, (int64_t)res_copies(w.ldq) * w.m, (int64_t)sh.nb, hs};
+                           (int64_t)sh.nb * hs, (int64_t)res_copies(w.ldq) * w.m, 0, hs};
   for (int q = 0; q < 6; ++q) {
     z.p[q] = const_cast<double*>(bufs[q]);
     z.n[q] = lens[q];
