@@ -31,6 +31,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int FM_BK = 64;                // K per LDS stage
 constexpr int FM_NS = 2;                 // LDS stages (loads run one stage ahead)
+static_assert(FM_NS == 2, "the stage waits allow no load in flight");
 constexpr int FM_LSPREAD = 1;            // k16 steps over which a stage's global->LDS loads go out
 constexpr int FM_SROWS = 32;             // epilogue rows staged per pass
 constexpr int FM_CPR = FM_BK / 8;        // 16-byte chunks per LDS row
@@ -45,17 +46,9 @@ constexpr int FM_RPL = 64 / FM_CPR;      // rows filled by one 1 KB direct-to-LD
 static_assert(FM_CPR == 8, "the swizzle is laid out for 128-byte LDS rows");
 __device__ __forceinline__ int fm_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
-// s_waitcnt vmcnt(N) for the counts the pipeline uses
-template <int N>
-__device__ __forceinline__ void fm_wait_vm() {
-  static_assert(N == 0 || N == 4 || N == 6 || N == 8 || N == 12 || N == 16, "unsupported count");
-  if constexpr (N == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  else if constexpr (N == 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
-  else if constexpr (N == 6) asm volatile("s_waitcnt vmcnt(6)" ::: "memory");
-  else if constexpr (N == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-  else if constexpr (N == 12) asm volatile("s_waitcnt vmcnt(12)" ::: "memory");
-  else asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
-}
+// every global->LDS load of this wave landed (with two stages the next stage's
+// loads are issued during the current one, so a stage wait allows none in flight)
+__device__ __forceinline__ void fm_wait_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // cos(x) in fp32 for the epilogue, about 1 ulp for |x| up to several thousand:
 // Cody and Waite's reduction x = k pi/2 + r with pi/2 split into three fp32
@@ -112,7 +105,6 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_featmap(FeatmapArgs a) {
   // a stage is loaded in groups of FM_RPL rows (1 KB, one direct-to-LDS load per wave)
   constexpr int LA = BM / FM_RPL / NW, LB = BN / FM_RPL / NW;  // loads per wave per stage
   static_assert(LA * FM_RPL * NW == BM && LB * FM_RPL * NW == BN, "row groups must split over the waves");
-  constexpr int AHEAD = (FM_NS - 2) * (LA + LB);     // loads allowed in flight at a stage wait
   // FM_NS K stages of A and B; reused after the main loop to stage the output
   __shared__ __attribute__((aligned(16))) uint16_t smem[FM_NS * (STAGE_A + STAGE_B)];
   uint16_t* sA = smem;                        // [FM_NS][BM * FM_BK]
@@ -181,7 +173,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_featmap(FeatmapArgs a) {
   const int nk = a.ldw / FM_BK;
 #pragma unroll
   for (int p = 0; p < FM_NS - 1; ++p) load_stage(min(p, nk - 1), p);
-  fm_wait_vm<AHEAD>();                               // stage 0 landed (this wave's part)
+  fm_wait_loads();                                   // stage 0 landed (this wave's part)
   __syncthreads();
 
   const int fr = lane & 31, fk = lane >> 5;   // fragment row/col within a 32-tile, k half
@@ -248,7 +240,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_featmap(FeatmapArgs a) {
     }
     // every read of this stage has landed in registers before the barrier (the
     // buffer is refilled after it); stage kt + 1 has landed after it
-    fm_wait_vm<AHEAD>();
+    fm_wait_loads();
     __syncthreads();
     // first operands of stage kt + 1 (after the last stage: a re-read of valid
     // data, discarded), under the MFMAs of this stage's last step
@@ -258,7 +250,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_featmap(FeatmapArgs a) {
     pattern(TM + TN, 0);
     __builtin_amdgcn_sched_barrier(0);
   }
-  fm_wait_vm<0>();                                   // nothing in flight into smem
+  fm_wait_loads();                                   // nothing in flight into smem
   __syncthreads();
 
   // epilogue, 32 rows of each wave at a time: stage the accumulators in the
