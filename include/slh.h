@@ -218,11 +218,35 @@ int slh_simhash(slh_ctx *ctx, uint32_t *codes_out);
  * emb_out: device, cap x D floats (row-major); pos_out: device, cap int32;
  * tok2macro_out: device, N int32 (macro index of each token), may be NULL;
  * cap >= the bound n_spectral_windows * min(L, 2^bits) + chunk groups.
- * *M_out (host) receives M.  Synchronises the stream.
+ * *M_out (host) receives M.  Synchronises the stream.  SLH_ESTATE while a
+ * merge from slh_merge_async has not been waited for.
  */
 int slh_merge(slh_ctx *ctx, const void *X, int32_t x_dtype, int64_t ldx,
               float *emb_out, int32_t *pos_out, int32_t *tok2macro_out,
               int64_t cap, int64_t *M_out);
+
+/*
+ * Step 5 (Eq. 7; section 3.4 max positions; section 3.6 ordering) as
+ * slh_merge, without waiting: the merge is enqueued on the context's
+ * stream and the call returns, so that the host can enqueue the next prompt's
+ * steps (slh_feature_map ...) before this one's M is known.  The outputs hold
+ * the result, and M is returned, once slh_merge_wait returns for this merge.
+ * At most two merges may be outstanding (SLH_ESTATE otherwise); each is waited
+ * for, in order.  A later merge writes its own outputs, so the caller gives
+ * consecutive merges different output buffers if it reads them after the next
+ * merge was enqueued.  Same arguments and errors as slh_merge, without M_out.
+ */
+int slh_merge_async(slh_ctx *ctx, const void *X, int32_t x_dtype, int64_t ldx,
+                    float *emb_out, int32_t *pos_out, int32_t *tok2macro_out,
+                    int64_t cap);
+
+/*
+ * Waits for the oldest merge enqueued by slh_merge_async and not yet waited for
+ * (spinning on an event: the stream up to that merge has finished) and stores
+ * its M in *M_out (host).  SLH_ESTATE when none is outstanding; SLH_EHIP when a
+ * wait between blocks of the resident Lanczos kernel of that prompt timed out.
+ */
+int slh_merge_wait(slh_ctx *ctx, int64_t *M_out);
 
 /* Capacity slh_merge needs for the current routing. */
 int64_t slh_merge_capacity(const slh_ctx *ctx);

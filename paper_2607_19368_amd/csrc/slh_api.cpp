@@ -98,6 +98,13 @@ struct slh_ctx {
   void* pin = nullptr;
   size_t pin_bytes = 0;
   hipEvent_t ev_host = nullptr;
+  // merges in flight (slh_merge_async): slot s = count & 1 of a pinned ring
+  // holds (M, the resident Lanczos kernel's error word) of that merge, written
+  // by the stream and marked by mq_ev[s]; mq_head merges enqueued, mq_tail waited for
+  unsigned* mq_pin = nullptr;
+  hipEvent_t mq_ev[2] = {nullptr, nullptr};
+  int64_t mq_head = 0, mq_tail = 0;
+  int mq_res[2] = {0, 0}, mq_keep[2] = {0, 0};
   int device = 0, n_cu = 256;
   std::string err;
 
@@ -487,7 +494,10 @@ int slh_create(slh_ctx** out, int64_t N, int64_t D, int64_t m, int32_t r, int32_
     return SLH_EHIP;
   }
   if (hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking) != hipSuccess ||
-      hipEventCreateWithFlags(&c->ev_host, hipEventDisableTiming) != hipSuccess) {
+      hipEventCreateWithFlags(&c->ev_host, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c->mq_ev[0], hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c->mq_ev[1], hipEventDisableTiming) != hipSuccess ||
+      hipHostMalloc((void**)&c->mq_pin, 4 * sizeof(unsigned), hipHostMallocDefault) != hipSuccess) {
     slh_destroy(c);
     return SLH_EHIP;
   }
@@ -497,6 +507,7 @@ int slh_create(slh_ctx** out, int64_t N, int64_t D, int64_t m, int32_t r, int32_
 
 void slh_destroy(slh_ctx* c) {
   if (!c) return;
+  if (c->mq_head != c->mq_tail) (void)hipStreamSynchronize(c->stream);   // merges still in flight
   drop_graph(c);
   DevBuf* bufs[] = {&c->Wt, &c->psi, &c->R, &c->q1all, &c->q1act, &c->winlist, &c->route,
                     &c->nrm2_fm, &c->nrm_x, &c->inv_x, &c->rowscale, &c->Xb, &c->Phi, &c->Q, &c->T,
@@ -511,6 +522,9 @@ void slh_destroy(slh_ctx* c) {
   if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
   if (c->ev_host) (void)hipEventDestroy(c->ev_host);
   if (c->pin) (void)hipHostFree(c->pin);
+  for (auto& e : c->mq_ev)
+    if (e) (void)hipEventDestroy(e);
+  if (c->mq_pin) (void)hipHostFree(c->mq_pin);
 
   if (c->ev_made)
     for (auto& e : c->ev) (void)hipEventDestroy(e);
@@ -958,13 +972,15 @@ int slh_simhash(slh_ctx* c, uint32_t* codes_out) {
   return SLH_OK;
 }
 
-int slh_merge(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, float* emb_out,
-              int32_t* pos_out, int32_t* tok2macro_out, int64_t cap, int64_t* M_out) {
+int slh_merge_async(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, float* emb_out,
+                    int32_t* pos_out, int32_t* tok2macro_out, int64_t cap) {
   if (!c) return SLH_EINVAL;
   if (c->stage < 3) return fail(c, SLH_ESTATE, "slh_merge before slh_simhash");
+  if (c->mq_head - c->mq_tail >= 2)
+    return fail(c, SLH_ESTATE, "two merges outstanding: slh_merge_wait first");
   int rc = check_x(c, X, dtype, ldx);
   if (rc) return rc;
-  if (!emb_out || !pos_out || !M_out) return fail(c, SLH_EINVAL, "NULL output");
+  if (!emb_out || !pos_out) return fail(c, SLH_EINVAL, "NULL output");
   const int64_t need = capacity(c);
   if (cap < need) return fail(c, SLH_EINVAL, "cap %lld < required %lld", (long long)cap, (long long)need);
   if (!norms_match(c, X, dtype, ldx))
@@ -1055,19 +1071,44 @@ int slh_merge(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, float* emb_
                                P<int>(c->Mtot), c->compact, emb_out, pos_out, tok2macro_out,
                                c->stream));
   if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[8], c->stream));
-  if ((rc = ensure_pinned(c, 8))) return rc;
-  HIP_TRY(c, hipMemcpyAsync(c->pin, c->Mtot.p, 4, hipMemcpyDeviceToHost, c->stream));
+  const int sl = (int)(c->mq_head & 1);
+  HIP_TRY(c, hipMemcpyAsync(c->mq_pin + 2 * sl, c->Mtot.p, 4, hipMemcpyDeviceToHost, c->stream));
   if (c->lz_res)
-    HIP_TRY(c, hipMemcpyAsync((char*)c->pin + 4, P<unsigned>(c->lz_bar) + LZ_BAR_ERR, 4,
+    HIP_TRY(c, hipMemcpyAsync(c->mq_pin + 2 * sl + 1, P<unsigned>(c->lz_bar) + LZ_BAR_ERR, 4,
                               hipMemcpyDeviceToHost, c->stream));
-  if ((rc = wait_stream(c))) return rc;
-  if (c->lz_res && ((const unsigned*)c->pin)[1] != 0)
-    return fail(c, SLH_EHIP, "Lanczos: a wait between blocks of the resident kernel timed out");
-  const int M = *(const int*)c->pin;
-  *M_out = M + c->keep_last;
+  HIP_TRY(c, hipEventRecord(c->mq_ev[sl], c->stream));
+  c->mq_res[sl] = c->lz_res;
+  c->mq_keep[sl] = (int)c->keep_last;
+  ++c->mq_head;
   c->merged = 1;
   forget_norms(c);                  // the next prompt may reuse this buffer
   return SLH_OK;
+}
+
+int slh_merge_wait(slh_ctx* c, int64_t* M_out) {
+  if (!c || !M_out) return SLH_EINVAL;
+  if (c->mq_tail == c->mq_head) return fail(c, SLH_ESTATE, "slh_merge_wait with no merge outstanding");
+  const int sl = (int)(c->mq_tail & 1);
+  hipError_t e;
+  while ((e = hipEventQuery(c->mq_ev[sl])) == hipErrorNotReady) {
+  }
+  ++c->mq_tail;
+  if (e != hipSuccess) return fail(c, SLH_EHIP, "hipEventQuery: %s", hipGetErrorString(e));
+  if (c->mq_res[sl] && c->mq_pin[2 * sl + 1] != 0)
+    return fail(c, SLH_EHIP, "Lanczos: a wait between blocks of the resident kernel timed out");
+  *M_out = (int64_t)(int)c->mq_pin[2 * sl] + c->mq_keep[sl];
+  return SLH_OK;
+}
+
+int slh_merge(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, float* emb_out,
+              int32_t* pos_out, int32_t* tok2macro_out, int64_t cap, int64_t* M_out) {
+  if (!c) return SLH_EINVAL;
+  if (!M_out) return fail(c, SLH_EINVAL, "NULL output");
+  if (c->mq_head != c->mq_tail)
+    return fail(c, SLH_ESTATE, "slh_merge while a merge from slh_merge_async is outstanding");
+  const int rc = slh_merge_async(c, X, dtype, ldx, emb_out, pos_out, tok2macro_out, cap);
+  if (rc) return rc;
+  return slh_merge_wait(c, M_out);
 }
 
 int slh_spectral_energy(slh_ctx* c, double* out) {

@@ -29,6 +29,7 @@ EXPORTS = [
     "slh_simhash", "slh_merge", "slh_merge_capacity", "slh_copy_out", "slh_num_windows",
     "slh_num_spectral", "slh_load", "slh_stage_times", "slh_time_passes", "slh_spectral_energy",
     "slh_bucket_purity", "slh_eigh_ritz", "slh_peak_read", "slh_peak_mfma", "slh_merge_noalloc",
+    "slh_merge_async", "slh_merge_wait",
 ]
 
 _lib = None
@@ -64,6 +65,8 @@ def load():
         "slh_merge_noalloc": (i32, [vp, i32, i64, i64, i64, vp, i32, vp, vp, vp, i64, vp, vp]),
         "slh_simhash": (i32, [vp, vp]),
         "slh_merge": (i32, [vp, vp, i32, i64, vp, vp, vp, i64, vp]),
+        "slh_merge_async": (i32, [vp, vp, i32, i64, vp, vp, vp, i64]),
+        "slh_merge_wait": (i32, [vp, vp]),
         "slh_merge_capacity": (i64, [vp]),
         "slh_copy_out": (i32, [vp, i32, vp, i64]),
         "slh_num_windows": (i64, [vp]),
@@ -251,6 +254,24 @@ def slh_merge(ctx, X, emb_out=None, pos_out=None, tok2macro_out=None):
                                  ctypes.byref(M)), "slh_merge")
     m = int(M.value)
     return emb_out[:m], pos_out[:m], tok2macro_out, m
+
+
+def slh_merge_async(ctx, X, emb_out, pos_out, tok2macro_out=None):
+    """Enqueues the merge into the given device outputs and returns at once; the
+    outputs hold the result once slh_merge_wait has returned its M."""
+    p, dt, ld = _xinfo(X)
+    _check(ctx, load().slh_merge_async(ctx.handle, p, dt, ld, ctypes.c_void_p(emb_out.data_ptr()),
+                                       ctypes.c_void_p(pos_out.data_ptr()),
+                                       ctypes.c_void_p(tok2macro_out.data_ptr())
+                                       if tok2macro_out is not None else None,
+                                       emb_out.shape[0]), "slh_merge_async")
+
+
+def slh_merge_wait(ctx):
+    """M of the oldest merge from slh_merge_async not yet waited for."""
+    M = ctypes.c_int64(0)
+    _check(ctx, load().slh_merge_wait(ctx.handle, ctypes.byref(M)), "slh_merge_wait")
+    return int(M.value)
 
 
 _OUT = {

@@ -572,6 +572,62 @@ def test_two_prompts_one_context_same_buffer(routed):
     assert not np.array_equal(out_a[0][:4], out_b[0][:4])
 
 
+@pytest.mark.parametrize("m", [256, 1024])
+def test_merge_async_pipelined(m):
+    """slh_merge_async / slh_merge_wait: two prompts through one context with the
+    second prompt's steps enqueued before the first one's M is read give, bit for
+    bit, the outputs and M of slh_merge on each in a context of its own.  A third
+    merge (or a slh_merge) is refused while two are outstanding, and a wait needs
+    an outstanding merge.  m = 1024: the resident Lanczos kernel, whose error word
+    each wait checks; m = 256: the streaming path."""
+    import torch
+    import paper_2607_19368_amd as P
+    from paper_2607_19368_amd import slh as B
+    ia = _custom("qa", 2048, 512, m, 16, 8, 8, seed=0)
+    ib = _custom("qb", 2048, 512, m, 16, 8, 8, seed=1)
+    wl = ia.workload
+
+    def steps(ctx, X):
+        P.slh_feature_map(ctx, X)
+        P.slh_lanczos(ctx, wl.n_it, want=False)
+        P.slh_simhash(ctx)
+
+    def sync_run(inp):
+        ctx = P.slh_create(wl.N, wl.D, wl.m, wl.r, wl.bits, 0)
+        X = PR.to_device_x(inp)
+        steps(ctx, X)
+        E, Pp, t2m, M = P.slh_merge(ctx, X)
+        torch.cuda.synchronize()
+        return E.cpu().numpy().copy(), Pp.cpu().numpy().copy(), t2m.cpu().numpy().copy(), M
+
+    ref = [sync_run(ia), sync_run(ib)]
+    ctx = P.slh_create(wl.N, wl.D, wl.m, wl.r, wl.bits, 0)
+    xs = [PR.to_device_x(ia), PR.to_device_x(ib)]
+    cap = P.slh_merge_capacity(ctx)
+    outs = [(torch.empty((cap, wl.D), dtype=torch.float32, device="cuda"),
+             torch.empty(cap, dtype=torch.int32, device="cuda"),
+             torch.empty(wl.N, dtype=torch.int32, device="cuda")) for _ in range(2)]
+    _say(f"[merge async] m={m} cap={cap}")
+    for X, o in zip(xs, outs):
+        steps(ctx, X)
+        P.slh_merge_async(ctx, X, *o)
+    steps(ctx, xs[0])
+    with pytest.raises(B.SLHError):
+        P.slh_merge_async(ctx, xs[0], *outs[0])
+    with pytest.raises(B.SLHError):
+        P.slh_merge(ctx, xs[0])
+    Ms = [P.slh_merge_wait(ctx), P.slh_merge_wait(ctx)]
+    with pytest.raises(B.SLHError):
+        P.slh_merge_wait(ctx)
+    torch.cuda.synchronize()
+    for (E, Pp, t2m), M, (rE, rP, rt, rM) in zip(outs, Ms, ref):
+        assert M == rM
+        assert np.array_equal(E[:M].cpu().numpy(), rE)
+        assert np.array_equal(Pp[:M].cpu().numpy(), rP)
+        assert np.array_equal(t2m.cpu().numpy(), rt)
+    assert Ms[0] != Ms[1] or not np.array_equal(ref[0][0], ref[1][0])
+
+
 def test_call_order_and_capacity_errors():
     import torch
     import paper_2607_19368_amd as P
