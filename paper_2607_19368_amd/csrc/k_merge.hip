@@ -1016,6 +1016,21 @@ __global__ __launch_bounds__(256) void k_mg_tail(const void* __restrict__ X, int
   }
 }
 
+// M and the resident Lanczos kernel's error word (0 without it) into host-pinned
+// memory, in place of two copies; the event the host waits on is recorded after
+// this kernel, and its system-scope release makes the two words visible
+__global__ void k_mg_report(const int* __restrict__ Mtot, const unsigned* __restrict__ err,
+                            unsigned* __restrict__ out) {
+  out[0] = (unsigned)*Mtot;
+  out[1] = err ? *err : 0u;
+}
+
+hipError_t launch_merge_report(const int* Mtot, const unsigned* err, unsigned* out, hipStream_t s) {
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(k_mg_report, dim3(1), dim3(1), 0, s, Mtot, err, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_merge_tail(const void* X, int dtype, int64_t ldx, int D, int64_t N, int K,
                              const int* Mtot, int compact, float* E, int* P, int* tok2macro,
                              hipStream_t s) {

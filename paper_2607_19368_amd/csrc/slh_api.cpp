@@ -156,6 +156,8 @@ struct slh_ctx {
   int64_t keep_last = 0;            // SLH_OPT_KEEP_LAST
   int64_t target_len = 0;           // SLH_OPT_TARGET_LEN (0 = off)
   std::vector<int> tw_h;            // per-window budgets of the last merge
+  std::vector<int> tw_dev_h;        // the budgets in tg_tw (uploaded to tw_dev_p)
+  void* tw_dev_p = nullptr;
   DevBuf tg_tw, tg_scr;
   DevBuf dg_tiles, dg_counts;
   DevBuf posv, mg_pre;
@@ -1052,8 +1054,12 @@ int slh_merge_async(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, float
     ENSURE(c, c->tg_tw, (size_t)c->n_win * 4);
     ENSURE(c, c->tg_scr, (size_t)N * 4);
     ENSURE(c, c->mg_pre, (size_t)N * 8);
-    HIP_TRY(c, hipMemcpyAsync(c->tg_tw.p, c->tw_h.data(), (size_t)c->n_win * 4,
-                              hipMemcpyHostToDevice, c->stream));
+    if (c->tg_tw.p != c->tw_dev_p || c->tw_h != c->tw_dev_h) {   // budgets changed
+      HIP_TRY(c, hipMemcpyAsync(c->tg_tw.p, c->tw_h.data(), (size_t)c->n_win * 4,
+                                hipMemcpyHostToDevice, c->stream));
+      c->tw_dev_h = c->tw_h;
+      c->tw_dev_p = c->tg_tw.p;
+    }
     w.tw = P<int>(c->tg_tw);
     w.tg = P<int>(c->tg_scr);
     w.pre = P<long long>(c->mg_pre);
@@ -1072,10 +1078,8 @@ int slh_merge_async(slh_ctx* c, const void* X, int32_t dtype, int64_t ldx, float
                                c->stream));
   if (c->timing) HIP_TRY(c, hipEventRecord(c->ev[8], c->stream));
   const int sl = (int)(c->mq_head & 1);
-  HIP_TRY(c, hipMemcpyAsync(c->mq_pin + 2 * sl, c->Mtot.p, 4, hipMemcpyDeviceToHost, c->stream));
-  if (c->lz_res)
-    HIP_TRY(c, hipMemcpyAsync(c->mq_pin + 2 * sl + 1, P<unsigned>(c->lz_bar) + LZ_BAR_ERR, 4,
-                              hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, launch_merge_report(P<int>(c->Mtot), c->lz_res ? P<unsigned>(c->lz_bar) + LZ_BAR_ERR : nullptr,
+                                 c->mq_pin + 2 * sl, c->stream));
   HIP_TRY(c, hipEventRecord(c->mq_ev[sl], c->stream));
   c->mq_res[sl] = c->lz_res;
   c->mq_keep[sl] = (int)c->keep_last;

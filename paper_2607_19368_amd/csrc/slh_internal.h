@@ -158,6 +158,7 @@ struct MergeWS {
 };
 int merge_nchunks(int64_t N, int CH);
 // preserved suffix: tail tokens N .. N + K - 1 become macro-tokens *Mtot .. *Mtot + K - 1
+hipError_t launch_merge_report(const int* Mtot, const unsigned* err, unsigned* out, hipStream_t s);
 hipError_t launch_merge_tail(const void* X, int dtype, int64_t ldx, int D, int64_t N, int K,
                              const int* Mtot, int compact, float* E, int* P, int* tok2macro,
                              hipStream_t s);
