@@ -864,6 +864,14 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
                                     P<double>(c->Seig), w.Q, (int)L, w.ldq, P<double>(c->Z),
                                     c->n_cu, c->stream));
         HIP_TRY(c, hipEventRecord(c->ev[4], c->stream));
+      } else if (res) {
+        // the resident path is four kernels, launched directly: the end of a
+        // graph costs a gap before the stream's next kernel
+        HIP_TRY(c, launch_lanczos_resident(w, q1act, P<unsigned>(c->lz_bar), c->n_cu, c->stream,
+                                           nullptr, nullptr));
+        HIP_TRY(c, launch_eigh_ritz(w.alpha, w.beta, w.neff, na, n_it, c->r, P<double>(c->theta),
+                                    P<double>(c->Seig), w.Q, (int)L, w.ldq, P<double>(c->Z),
+                                    c->n_cu, c->stream));
       } else {
         // The step sequence, Eigh(T) and the Ritz coordinates are captured once
         // per configuration and replayed as one graph.
