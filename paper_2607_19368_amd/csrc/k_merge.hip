@@ -382,6 +382,79 @@ __device__ __forceinline__ int block_incl_max_1024(int v, int* wsum, int& total)
   return max(v, pre);
 }
 
+// Scans of n values over a 1024-thread block, one block scan per 16384
+// positions: thread t takes the contiguous positions c0 + t E .. c0 + t E + E - 1
+// of each such chunk (E = ceil(chunk / 1024) <= 16), holding their values in
+// registers.  val(i) gives position i's value, put(i, x) receives the exclusive
+// prefix sum at i; returns the total.
+template <class VAL, class PUT>
+__device__ __forceinline__ int blocked_excl_sum(int n, VAL val, PUT put, int* wsum) {
+  int carry = 0;
+  for (int c0 = 0; c0 < n; c0 += 16384) {
+    const int nc = min(16384, n - c0), E = (nc + 1023) >> 10, i0 = c0 + threadIdx.x * E;
+    int v[16], loc = 0;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      v[e] = (e < E && i0 + e < c0 + nc) ? val(i0 + e) : 0;
+      loc += v[e];
+    }
+    int tot;
+    int run = carry + block_incl_scan_1024(loc, wsum, tot) - loc;
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      if (e < E && i0 + e < c0 + nc) {
+        put(i0 + e, run);
+        run += v[e];
+      }
+    carry += tot;
+    __syncthreads();                                // wsum is reused
+  }
+  return carry;
+}
+// The same blocking for the most recent start at or before each position:
+// put(i, s) receives the largest s <= i with is_start(s) (INT_MIN if none).
+template <class START, class PUT>
+__device__ __forceinline__ void blocked_last_start(int n, START is_start, PUT put, int* wsum) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int carry = INT_MIN;
+  for (int c0 = 0; c0 < n; c0 += 16384) {
+    const int nc = min(16384, n - c0), E = (nc + 1023) >> 10, i0 = c0 + threadIdx.x * E;
+    bool f[16];
+    int lm = INT_MIN;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      f[e] = e < E && i0 + e < c0 + nc && is_start(i0 + e);
+      if (f[e]) lm = i0 + e;                       // starts increase with the position
+    }
+    // exclusive max over the threads before this one (and the earlier chunks)
+    int v = lm;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_up(v, o, 64);
+      if (lane >= o) v = max(v, t);
+    }
+    int ex = __shfl_up(v, 1, 64);
+    if (lane == 0) ex = INT_MIN;
+    __syncthreads();
+    if (lane == 63) wsum[wave] = v;
+    __syncthreads();
+    int tot = INT_MIN;
+    for (int k = 0; k < 16; ++k) {
+      if (k < wave) ex = max(ex, wsum[k]);
+      tot = max(tot, wsum[k]);
+    }
+    int run = max(ex, carry);
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      if (e < E && i0 + e < c0 + nc) {
+        if (f[e]) run = i0 + e;
+        put(i0 + e, run);
+      }
+    carry = max(carry, tot);
+    __syncthreads();                                // wsum is reused
+  }
+}
+
 // inclusive scan (sum) of one int64 per thread over a 1024-thread block
 __device__ __forceinline__ long long block_incl_scan_i64(long long v, long long* wsum,
                                                          long long& total) {
@@ -551,18 +624,9 @@ __global__ __launch_bounds__(1024) void k_mg_target(MergeWS w, int* __restrict__
   if (T <= 0 || T == M) return;
   __shared__ int wsum[16];
   __shared__ int sR;
-  // run starts: max-scan of the start indices in sorted order
-  int carry = INT_MIN;
-  for (int b0 = 0; b0 < L; b0 += 1024) {
-    const int s = b0 + tid;
-    int v = INT_MIN;
-    if (s < L) v = (s == 0 || w.sloc[base + s] != w.sloc[base + s - 1]) ? s : INT_MIN;
-    int tot;
-    const int inc = block_incl_max_1024(v, wsum, tot);
-    if (s < L) st[base + s] = max(inc, carry);
-    carry = max(carry, tot);
-    __syncthreads();
-  }
+  // run starts: the most recent start of a run at or before each sorted position
+  blocked_last_start(L, [&](int s) { return s == 0 || w.sloc[base + s] != w.sloc[base + s - 1]; },
+                     [&](int s, int x) { st[base + s] = x; }, wsum);
   __threadfence_block();
   __syncthreads();
   for (int e = tid; e < L; e += 1024)
@@ -576,16 +640,8 @@ __global__ __launch_bounds__(1024) void k_mg_target(MergeWS w, int* __restrict__
   if (M > T) {
     // exclusive prefix of the run sizes over ranks: new sorted position of each
     // bucket's first member
-    int c2 = 0;
-    for (int b0 = 0; b0 < M; b0 += 1024) {
-      const int k = b0 + tid;
-      const int v = (k < M) ? rsz[base + k] : 0;
-      int tot;
-      const int inc = block_incl_scan_1024(v, wsum, tot);
-      if (k < M) t0[base + k] = c2 + inc - v;
-      c2 += tot;
-      __syncthreads();
-    }
+    (void)blocked_excl_sum(M, [&](int k) { return rsz[base + k]; },
+                           [&](int k, int x) { t0[base + k] = x; }, wsum);
     __threadfence_block();
     __syncthreads();
     for (int s = tid; s < L; s += 1024) {
@@ -643,16 +699,8 @@ __global__ __launch_bounds__(1024) void k_mg_target(MergeWS w, int* __restrict__
     __threadfence_block();
     __syncthreads();
     // rank of each piece = pieces whose last member precedes its own
-    int c3 = 0;
-    for (int b0 = 0; b0 < L; b0 += 1024) {
-      const int t = b0 + tid;
-      const int v = (t < L) ? fl[base + t] : 0;
-      int tt;
-      const int inc = block_incl_scan_1024(v, wsum, tt);
-      if (t < L) t0[base + t] = c3 + inc - v;
-      c3 += tt;
-      __syncthreads();
-    }
+    (void)blocked_excl_sum(L, [&](int t) { return fl[base + t]; },
+                           [&](int t, int x) { t0[base + t] = x; }, wsum);
     __threadfence_block();
     __syncthreads();
     for (int s = tid; s < L; s += 1024) {

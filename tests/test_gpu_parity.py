@@ -976,7 +976,7 @@ def test_preserved_suffix(case):
 
 
 @pytest.mark.parametrize("case,T", [("tiny", 30), ("tiny", 100), ("tiny", 1), ("tiny", 512),
-                                    ("windows", 200), ("windows", 700), ("long", 300),
+                                    ("windows", 200), ("windows", 700), ("long", 300), ("long", 6000),
                                     ("keep", 90)])
 def test_exact_target_length(case, T):
     """SLH_OPT_TARGET_LEN (reading R20; the paper gives no algorithm, so the
@@ -984,8 +984,9 @@ def test_exact_target_length(case, T):
     codes loaded, the GPU merge must produce exactly the oracle's adjusted
     groups (positions and token maps bit-exact, embeddings 1e-5).  tiny: one
     window of 512 (merge to 30 / 1, split to 100 / 512); windows: 8 windows of
-    256, half routed to chunk pooling; long: one window of 20000 tokens;
-    keep: 512 + 12 preserved tokens."""
+    256, half routed to chunk pooling; long: one window of 20000 tokens (more
+    than one 16384-position chunk of the block scans; merged to 300, split to
+    6000); keep: 512 + 12 preserved tokens."""
     import torch
     import paper_2607_19368_amd as P
     from paper_2607_19368_amd import slh as B
