@@ -10,8 +10,8 @@
 // Lanczos relation, z1 by the three-term recurrence, then t~ = Phi^T z1 / |z1|
 // and h2 = Q_j^T z1), in two phases:
 //   rows     every block: its rows of q_j and z1, and its partials of Phi^T z1,
-//            of h2 and of |z1|^2;
-//   columns  block b: t~ over its m / nb columns and the partial of |t~|^2;
+//            of h2 and of |z1|^2 (alpha~ = |t~|^2 it sums from the t~ it holds);
+//   columns  block b: t~ over its m / nb columns (written to every copy of t~);
 //            h2 entries b, b + nb, ...; |z1|^2 (every block).
 // The scalars of a step (alpha, beta, the breakdown test) are computed by
 // every block from the same reduced values in the same order, so all blocks
@@ -28,9 +28,11 @@
 // reader has consumed step e's value (it first needs values that those
 // readers produce after reading), so the two tags suffice.  Every wait is
 // bounded: after LR_SPIN polls a block sets an error word and leaves, and the
-// others, seeing it, leave too.  The host launches the kernel only when all
-// nb blocks are resident at once (one per compute unit; checked with the
-// occupancy calculator).
+// others, seeing it, leave too.  A block's own stores are acknowledged
+// before its waves start polling: its polls and its stores share the CU's path
+// to memory, and its stores are what the other blocks are waiting for.  The
+// host launches the kernel only when all nb blocks are resident at once (one
+// per compute unit; checked with the occupancy calculator).
 #include "slh_device.h"
 #include "slh_internal.h"
 
