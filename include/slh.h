@@ -120,6 +120,13 @@ typedef struct slh_ctx slh_ctx;
                                     registers (the same recurrence; partial sums in
                                     a different grouping); 0: one pass over Phi per
                                     step for every shape                             */
+#define SLH_OPT_WAIT_POLLS    12 /* polls after which a wait of the resident Lanczos
+                                    kernel for a value of another block gives up
+                                    (the blocks then leave and the call that reads
+                                    the run's results reports SLH_EHIP); 0
+                                    (default): 2^20, far beyond any wait of a
+                                    healthy run (about a second).  Small values
+                                    exercise that error path                       */
 
 /*
  * Random parameters of the method, drawn from `seed` with Philox4x32-10

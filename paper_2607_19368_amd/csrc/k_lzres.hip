@@ -27,7 +27,7 @@
 // every step, and no block can rewrite a slot of step e + 1 before every
 // reader has consumed step e's value (it first needs values that those
 // readers produce after reading), so the two tags suffice.  Every wait is
-// bounded: after LR_SPIN polls a block sets an error word and leaves, and the
+// bounded: after LR_SPIN polls (or w.spin) a block sets an error word and leaves, and the
 // others, seeing it, leave too.  A block's own stores are acknowledged
 // before its waves start polling: its polls and its stores share the CU's path
 // to memory, and its stores are what the other blocks are waiting for.  The
@@ -78,10 +78,10 @@ __device__ __forceinline__ long long ld_raw(double* p) {
 __device__ __forceinline__ bool tag_is(long long x, int e) { return (int)(x & 3) == 1 + (e & 1); }
 
 // v[u] = *addr(u) of step e for the u with bit u of act set (0 for the others),
-// polling until every tag matches; false after LR_SPIN polls or when the error
+// polling until every tag matches; false after spin polls or when the error
 // word is set (the error word is then set)
 template <int N, class ADDR>
-__device__ __forceinline__ bool ld_wait(ADDR addr, unsigned act, int e, unsigned* bar,
+__device__ __forceinline__ bool ld_wait(ADDR addr, unsigned act, int e, unsigned* bar, int spin,
                                         double (&v)[N]) {
   long long x[N];
 #pragma unroll
@@ -92,7 +92,7 @@ __device__ __forceinline__ bool ld_wait(ADDR addr, unsigned act, int e, unsigned
 #pragma unroll
     for (int u = 0; u < N; ++u) all = all && (((act >> u) & 1) == 0 || tag_is(x[u], e));
     if (all) break;
-    if (s > LR_SPIN || ((s & 63) == 63 && ld_flag(bar + LR_ERR) != 0)) {
+    if (s > spin || ((s & 63) == 63 && ld_flag(bar + LR_ERR) != 0)) {
       st_flag(bar + LR_ERR, 1u);
       ok = false;
       break;
@@ -185,7 +185,7 @@ __device__ __forceinline__ void launder_rows(float4 (&ph)[RB][NH]) {
 // VGPRs (two waves per SIMD: 128 floats a lane) and are laundered in place once
 // per use, else (one wave per SIMD, 256 floats a lane, part of them in
 // accumulation registers) each use goes through pin4.
-template <int RB, int CPL, int NT>
+template <int RB, int CPL, int NT, bool SPIN>
 __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* bar,
                                                        const double* __restrict__ q1) {
   constexpr int NW = NT / 64, NH = CPL / 4, KG = NT / RB, QS = RB + 1;   // QS: row stride of Qs (bank spread)
@@ -193,6 +193,8 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
   static_assert(CPL % 4 == 0 && RB % 8 == 0 && NT % RB == 0, "shape");
   const int b = blockIdx.x, nb = gridDim.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int L = w.L, m = w.m, n_it = w.n_it, ldq = w.ldq, hs = ldq + 1;
+  // SPIN: the wait limit from w.spin (SLH_OPT_WAIT_POLLS), else the constant
+  const int spin = SPIN ? (w.spin > 0 ? w.spin : LR_SPIN) : LR_SPIN;
   const int r0 = b * RB;
   const int cb = wv * 64 * CPL + 4 * lane;
   extern __shared__ double Qs[];                 // [n_it + 1][QS]
@@ -270,12 +272,12 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
     const int64_t base = (int64_t)b * nb * CB + tid;
     stores_done_barrier();
     double v[CPL], zv[1], hv[1];
-    bool ok = ld_wait<CPL>([&](int u) { return Spart + base + u * NT; }, (1u << CPL) - 1u, e, bar, v);
+    bool ok = ld_wait<CPL>([&](int u) { return Spart + base + u * NT; }, (1u << CPL) - 1u, e, bar, spin, v);
     if (norm)
       ok = ld_wait<1>([&](int) { return Hpart + (int64_t)tid * hs + ldq; }, tid < nb ? 1u : 0u, e,
-                      bar, zv) && ok;
+                      bar, spin, zv) && ok;
     ok = ld_wait<1>([&](int) { return Hpart + (int64_t)tid * hs + kh; }, (kh >= 0 && tid < nb) ? 1u : 0u,
-                    e, bar, hv) && ok;
+                    e, bar, spin, hv) && ok;
     if (!block_ok(ok)) return false;
     if (norm || kh >= 0) {
       double d2 = 0.0;
@@ -310,7 +312,7 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
     stores_done_barrier();
     double hv[1];
     const bool ok = ld_wait<1>([&](int) { return Hpart + (int64_t)tid * hs + k; }, tid < nb ? 1u : 0u,
-                               e, bar, hv);
+                               e, bar, spin, hv);
     if (!block_ok(ok)) return false;
     double d1 = 0.0, d2 = 0.0;
     block_sum3(hv[0], d1, d2, red);
@@ -332,7 +334,7 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
     // of every block).
     double tv[CPL], h1[1];
     bool ok = ld_wait<CPL>([&](int u) { return Tr + cb + 256 * (u >> 2) + (u & 3); }, (1u << CPL) - 1u,
-                           j, bar, tv);
+                           j, bar, spin, tv);
     // Phi t~ of the block's rows: 4 CPL products per lane and row, summed over
     // the wave 8 rows at a time (into prw), then over the NW waves
     if constexpr (INPLACE) launder_rows(ph);
@@ -355,7 +357,7 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
       const double tot = wave_sum8_f64(d);
       if ((lane & 7) == 0) prw[wv][r8 + idx] = tot;
     }
-    ok = ld_wait<1>([&](int) { return H2 + tid; }, tid < j ? 1u : 0u, j, bar, h1) && ok;
+    ok = ld_wait<1>([&](int) { return H2 + tid; }, tid < j ? 1u : 0u, j, bar, spin, h1) && ok;
     if (!block_ok(ok)) return;
     const double h2v = h1[0];
     // this thread's share of alpha~ = |t~|^2: every block holds all of t~ and
@@ -478,7 +480,7 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
   // beta of the last step (reported; T does not use it)
   if (b == 0) {
     double hv[1];
-    const bool ok = ld_wait<1>([&](int) { return H2 + tid; }, tid < n_it ? 1u : 0u, n_it, bar, hv);
+    const bool ok = ld_wait<1>([&](int) { return H2 + tid; }, tid < n_it ? 1u : 0u, n_it, bar, spin, hv);
     if (!block_ok(ok)) return;
     double hh2 = hv[0] * hv[0], d1 = 0.0, d2 = 0.0;
     block_sum3(hh2, d1, d2, red);
@@ -542,10 +544,10 @@ ResShape res_shape(const LanczosWS& w, int n_cu) {
   }
   return s;
 }
-template <int RB, int CPL, int NT>
+template <int RB, int CPL, int NT, bool SPIN>
 hipError_t launch_res_t(const LanczosWS& w, const ResShape& sh, unsigned* bar, const double* q1,
                         bool check, hipStream_t s) {
-  auto k = k_lz_resident<RB, CPL, NT>;
+  auto k = k_lz_resident<RB, CPL, NT, SPIN>;
   const size_t lds = (size_t)(w.n_it + 1) * (RB + 1) * sizeof(double);
   if (lds > 65536) {
     const hipError_t e =
@@ -561,12 +563,20 @@ hipError_t launch_res_t(const LanczosWS& w, const ResShape& sh, unsigned* bar, c
   hipLaunchKernelGGL(k, dim3(sh.nb), dim3(NT), lds, s, w, bar, q1);
   return hipGetLastError();
 }
+template <bool SPIN>
+hipError_t launch_res_s(const LanczosWS& w, const ResShape& sh, unsigned* bar, const double* q1,
+                        bool check, hipStream_t s) {
+  if (w.m == 2048) return sh.rb == 32 ? launch_res_t<32, 4, 512, SPIN>(w, sh, bar, q1, check, s)
+                                      : launch_res_t<16, 4, 512, SPIN>(w, sh, bar, q1, check, s);
+  return sh.rb == 32 ? launch_res_t<32, 4, LR_T, SPIN>(w, sh, bar, q1, check, s)
+                     : launch_res_t<16, 4, LR_T, SPIN>(w, sh, bar, q1, check, s);
+}
+// a wait limit other than the built-in one (SLH_OPT_WAIT_POLLS) takes an
+// instantiation of its own, so that the limit stays a constant in the other
 hipError_t launch_res(const LanczosWS& w, const ResShape& sh, unsigned* bar, const double* q1,
                       bool check, hipStream_t s) {
-  if (w.m == 2048) return sh.rb == 32 ? launch_res_t<32, 4, 512>(w, sh, bar, q1, check, s)
-                                      : launch_res_t<16, 4, 512>(w, sh, bar, q1, check, s);
-  return sh.rb == 32 ? launch_res_t<32, 4, LR_T>(w, sh, bar, q1, check, s)
-                     : launch_res_t<16, 4, LR_T>(w, sh, bar, q1, check, s);
+  return w.spin > 0 ? launch_res_s<true>(w, sh, bar, q1, check, s)
+                    : launch_res_s<false>(w, sh, bar, q1, check, s);
 }
 }  // namespace
 

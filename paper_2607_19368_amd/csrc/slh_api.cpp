@@ -145,6 +145,7 @@ struct slh_ctx {
   bool lz_w_valid = false;
   bool lz_res = false;              // that run used the resident kernel
   int resident = 1;                 // SLH_OPT_RESIDENT
+  int wait_polls = 0;               // SLH_OPT_WAIT_POLLS (0: the built-in limit)
   DevBuf lz_bar;                    // its grid-barrier words (generation, error, arrivals)
 
   int short_win = 1;                // SLH_OPT_SHORT_WINDOWS
@@ -611,6 +612,11 @@ int slh_set_option(slh_ctx* c, int32_t key, double v) {
       if (v != 0.0 && v != 1.0) return fail(c, SLH_EINVAL, "RESIDENT must be 0 or 1");
       c->resident = (int)v;
       break;
+    case SLH_OPT_WAIT_POLLS:
+      if (!(v >= 0.0 && v <= 2147483647.0) || v != (double)(int)v)
+        return fail(c, SLH_EINVAL, "WAIT_POLLS must be an integer in [0, 2^31)");
+      c->wait_polls = (int)v;
+      break;
     default:
       return fail(c, SLH_EINVAL, "unknown option %d", key);
   }
@@ -801,6 +807,7 @@ int slh_lanczos(slh_ctx* c, int32_t n_it, double* ritz_out, int32_t* iters_out) 
       w.n_it = n_it;
       w.ldq = n_it + 1;
       w.tol = c->tol;
+      w.spin = c->wait_polls;
       // chunks of 16 rows per block of the pass: one chunk per block while the
       // blocks fit two per CU (all resident at once); beyond that, about one
       // block per CU, each streaming its chunks with the next in flight (the

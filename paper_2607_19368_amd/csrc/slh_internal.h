@@ -58,6 +58,8 @@ struct LanczosWS {
   double tol;
   int NCH;                      // chunks of 16 rows per block of the pass
   int G3;                       // row groups of 16 NCH rows (one block of the pass each)
+  int spin;                     // resident kernel: polls before a wait between blocks
+                                //   gives up (0: the built-in 2^20)
 };
 // One pass over Phi per step (k_lz_step) and one reduction.  ev_before/ev_after
 // (may be NULL): n_it events each, receiving the start and end timestamps of

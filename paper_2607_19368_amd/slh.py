@@ -17,7 +17,7 @@ SLH_OK, SLH_EINVAL, SLH_ENOMEM, SLH_EHIP, SLH_ESTATE = 0, -1, -2, -3, -4
 SLH_BF16, SLH_F32 = 0, 1
 SLH_OPT_KERNEL, SLH_OPT_WINDOW_LEN, SLH_OPT_POS_MODE, SLH_OPT_BREAKDOWN_TOL, SLH_OPT_TIMING = 1, 2, 3, 4, 5
 SLH_OPT_SHORT_WINDOWS, SLH_OPT_NORMALIZE, SLH_OPT_POS_SCHEME, SLH_OPT_KEEP_LAST = 6, 7, 8, 9
-SLH_OPT_TARGET_LEN, SLH_OPT_RESIDENT = 10, 11
+SLH_OPT_TARGET_LEN, SLH_OPT_RESIDENT, SLH_OPT_WAIT_POLLS = 10, 11, 12
 SLH_OUT_PHI, SLH_OUT_ALPHA, SLH_OUT_BETA, SLH_OUT_Z = 1, 2, 3, 4
 SLH_OUT_PROJ, SLH_OUT_CODES, SLH_OUT_THETA, SLH_OUT_Q, SLH_OUT_WINDOWS = 5, 6, 7, 8, 9
 SLH_OUT_ROWSUM = 10

@@ -628,6 +628,42 @@ def test_merge_async_pipelined(m):
     assert Ms[0] != Ms[1] or not np.array_equal(ref[0][0], ref[1][0])
 
 
+def test_resident_wait_timeout_reported():
+    """A wait of the resident Lanczos kernel that gives up is reported, not hung:
+    with SLH_OPT_WAIT_POLLS = 1 (a wait for another block's value gives up after
+    a couple of polls, far sooner than the blocks' first exchange) every block
+    leaves through the error path and slh_merge raises SLH_EHIP (timed out);
+    back at the default the same context runs the prompt again and matches a
+    fresh context bit for bit."""
+    import torch
+    import paper_2607_19368_amd as P
+    from paper_2607_19368_amd import slh as B
+    inp = _custom("wt", 2048, 512, 1024, 16, 8, 8, seed=5)
+    wl = inp.workload
+    X = PR.to_device_x(inp)
+
+    def run(ctx):
+        P.slh_feature_map(ctx, X)
+        P.slh_lanczos(ctx, wl.n_it, want=False)
+        P.slh_simhash(ctx)
+        E, Pp, t2m, M = P.slh_merge(ctx, X)
+        torch.cuda.synchronize()
+        return E.cpu().numpy().copy(), Pp.cpu().numpy().copy(), t2m.cpu().numpy().copy()
+
+    ctx = P.slh_create(wl.N, wl.D, wl.m, wl.r, wl.bits, 0)
+    P.slh_set_option(ctx, B.SLH_OPT_WAIT_POLLS, 1)
+    _say("[wait timeout] resident run with one poll per wait")
+    with pytest.raises(B.SLHError, match="timed out"):
+        run(ctx)
+    P.slh_set_option(ctx, B.SLH_OPT_WAIT_POLLS, 0)
+    again = run(ctx)
+    ref = run(P.slh_create(wl.N, wl.D, wl.m, wl.r, wl.bits, 0))
+    for u, v in zip(again, ref):
+        assert u.shape == v.shape and np.array_equal(u, v)
+    with pytest.raises(B.SLHError):
+        P.slh_set_option(ctx, B.SLH_OPT_WAIT_POLLS, -1)
+
+
 def test_call_order_and_capacity_errors():
     import torch
     import paper_2607_19368_amd as P
