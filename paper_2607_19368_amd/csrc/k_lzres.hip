@@ -378,7 +378,7 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
     }
     double alpha_t = apv, hh = h2v * h2v, hth = h2v * gi;
     block_sum3(alpha_t, hh, hth, red);
-    double alpha = alpha_t, beta = 0.0, h2last = 0.0;
+    double alpha = alpha_t, beta = 0.0, h2last = 0.0, ibeta = 0.0;
     if (j > 0) {
       const double b2 = z2 - hh;
       beta = b2 > 0.0 ? sqrt(b2) : 0.0;
@@ -391,6 +391,10 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
       }
       h2last = h2s[j - 1];
       alpha = (z2 * alpha_t - hth) / (beta * beta) - 2.0 * h2last;
+      // (the 256-thread kernel multiplies by 1 / beta below: one division per
+      // step rather than two per row on the block's dependent path; at 512
+      // threads the extra value held costs more than the divisions)
+      if constexpr (NT <= 256) ibeta = 1.0 / beta;
     }
     amax = fmax(amax, fabs(alpha));
     if (tid == 0) {
@@ -424,7 +428,8 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
       }
       double q = Qs[i], qm = 0.0;                 // j = 0: q_0
       if (j > 0) {
-        q = (row < L) ? (zs[i] - sub) / beta : 0.0;
+        if constexpr (NT <= 256) q = (row < L) ? (zs[i] - sub) * ibeta : 0.0;
+        else q = (row < L) ? (zs[i] - sub) / beta : 0.0;
         qm = Qs[(j - 1) * QS + i];
         Qs[j * QS + i] = q;
         if (row < L) w.Q[(int64_t)j * L + row] = q;
@@ -443,7 +448,11 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
 #pragma unroll
         for (int q = 1; q < NW; ++q) u += prw[q][i];
         const double q = qr[i];
-        if (j > 0) u = (fma(sqrt(z2), u, -sgr[i]) - beta * h2last * q) / beta;
+        if constexpr (NT <= 256) {
+          if (j > 0) u = (fma(sqrt(z2), u, -sgr[i]) - beta * h2last * q) * ibeta;
+        } else {
+          if (j > 0) u = (fma(sqrt(z2), u, -sgr[i]) - beta * h2last * q) / beta;
+        }
         z = (u - alpha * q) - beta * qmr[i];
         z = (r0 + i < L) ? z : 0.0;
         zs[i] = z;
@@ -456,12 +465,28 @@ __global__ __launch_bounds__(NT, 1) void k_lz_resident(LanczosWS w, unsigned* ba
     // read only after the column partials have been reduced, so they are formed
     // while those travel
     col_partials(j + 1);
-    for (int k = tid; k <= j; k += NT) {
-      double a4[4] = {0.0, 0.0, 0.0, 0.0};
-      const double* qk = Qs + k * QS;
+    if constexpr (NT <= 256) {
+      // four threads per entry k (four lanes of a wave), RB / 4 rows each
+      for (int t = tid; t < 4 * (j + 1); t += NT) {
+        const int k = t >> 2, p4 = t & 3;
+        const double* qk = Qs + k * QS + p4 * (RB / 4);
+        const double* zq = zs + p4 * (RB / 4);
+        double a2[2] = {0.0, 0.0};
 #pragma unroll
-      for (int i = 0; i < RB; ++i) a4[i & 3] = fma(qk[i], zs[i], a4[i & 3]);
-      st_tag(Hpart + (int64_t)b * hs + k, (a4[0] + a4[1]) + (a4[2] + a4[3]), j + 1);
+        for (int i = 0; i < RB / 4; ++i) a2[i & 1] = fma(qk[i], zq[i], a2[i & 1]);
+        double v = a2[0] + a2[1];
+        v += __shfl_xor(v, 1);
+        v += __shfl_xor(v, 2);
+        if (p4 == 0) st_tag(Hpart + (int64_t)b * hs + k, v, j + 1);
+      }
+    } else {
+      for (int k = tid; k <= j; k += NT) {
+        double a4[4] = {0.0, 0.0, 0.0, 0.0};
+        const double* qk = Qs + k * QS;
+#pragma unroll
+        for (int i = 0; i < RB; ++i) a4[i & 3] = fma(qk[i], zs[i], a4[i & 3]);
+        st_tag(Hpart + (int64_t)b * hs + k, (a4[0] + a4[1]) + (a4[2] + a4[3]), j + 1);
+      }
     }
     // ---- columns: |z1|^2 (every block), t~_{j+1}, h2
     int k0 = b;                                   // h2 entries of this block: b, b + nb, ...
