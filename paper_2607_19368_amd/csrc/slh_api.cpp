@@ -519,7 +519,9 @@ void slh_destroy(slh_ctx* c) {
                     &c->proj, &c->codes, &c->keyA, &c->keyB, &c->valA, &c->valB, &c->tmpi,
                     &c->segid, &c->segk, &c->sval, &c->sloc, &c->mw, &c->wbase, &c->sseg,
                     &c->Mtot, &c->part, &c->part_seg, &c->part_cnt, &c->part_nsum,
-                    &c->part_end, &c->rpart, &c->scores, &c->rsu, &c->lz_bar};
+                    &c->part_end, &c->rpart, &c->scores, &c->rsu, &c->lz_bar, &c->nm_part, &c->nm_csum, &c->rowsum, &c->dg_counts,
+                    &c->dg_energy, &c->dg_rowsq, &c->dg_tiles, &c->mg_pre, &c->posv, &c->tg_scr,
+                    &c->tg_tw};
   for (DevBuf* b : bufs)
     if (b->p) (void)hipFree(b->p);
   if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);

@@ -103,3 +103,17 @@ def test_identity_path_returns_prompt_unchanged(rho):
     E, P, t2m, M, lz = B.compress(None, X, 8, rho=rho)
     assert E is X and M == 37 and lz is None
     assert torch.equal(P, torch.arange(37, dtype=torch.int32)) and torch.equal(t2m, P)
+
+
+def test_destroy_frees_every_context_buffer():
+    """Every grow-only device buffer that the context declares is on the list
+    slh_destroy frees (a buffer missing from it leaks once per context)."""
+    src = open(os.path.join(ROOT, "paper_2607_19368_amd", "csrc", "slh_api.cpp")).read()
+    declared = set()
+    for m in re.finditer(r"^\s*DevBuf ([^;]+);", src, re.M):
+        declared.update(n.strip() for n in m.group(1).split(","))
+    i = src.index("DevBuf* bufs[] = {")
+    freed = set(re.findall(r"&c->(\w+)", src[i:src.index("};", i)]))
+    assert declared, "no DevBuf members found"
+    assert declared - freed == set(), "not freed by slh_destroy"
+    assert freed - declared == set()

@@ -45,7 +45,7 @@ def _custom(name, N, D, m, n_it, r, bits, seed=0, x="bf16", vocab=32768):
 # 64 x 128; tiles128 -> 128 x 128; tiles256 -> 256 x 256 (all with a ragged last
 # row block except tiny)
 @pytest.mark.parametrize("case", ["tiny", "ragged", "mistral7b_head", "tiles64x128", "tiles128",
-                                  "tiles256"])
+                                  "tiles256", "mistral7b_full", "ragged_m256"])
 def test_feature_map_parity(case):
     if case == "tiny":
         inp = make_inputs("tiny")
@@ -57,6 +57,13 @@ def test_feature_map_parity(case):
         inp = _custom("tiles128", 4000, 264, 2048, 16, 4, 6)
     elif case == "tiles256":
         inp = _custom("tiles256", 8000, 264, 2048, 16, 4, 6)
+    elif case == "mistral7b_full":
+        # the whole 4096 x 4096 x 1024 product (64 x 128 tiles, two per CU)
+        inp = _custom("mistral7b_full", 4096, 4096, 1024, 16, 4, 6)
+    elif case == "ragged_m256":
+        # 8204 rows (the last 64-row tile partial), D = 3000 (47 K stages, the last
+        # one zero-filled past D), m = 256 (64 x 64 tiles)
+        inp = _custom("ragged_m256", 8204, 3000, 256, 16, 4, 6)
     else:
         inp = _custom("mistral7b_head", 1536, 4096, 1024, 16, 8, 10)
     wl = inp.workload
