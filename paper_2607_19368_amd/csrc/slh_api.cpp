@@ -257,14 +257,19 @@ T* P(DevBuf& b) {
 int make_events(slh_ctx* c, int n_fused) {
   const unsigned fl = hipEventDisableSystemFence;
   if (!c->ev_made) {
+    // events made before a failed creation are kept (and destroyed with the context)
     for (auto& e : c->ev)
-      HIP_TRY(c, hipEventCreateWithFlags(&e, fl));
+      if (!e) HIP_TRY(c, hipEventCreateWithFlags(&e, fl));
     c->ev_made = true;
   }
   while ((int)c->ev_fb.size() < n_fused) {
-    hipEvent_t a, b;
-    HIP_TRY(c, hipEventCreateWithFlags(&a, fl));
-    HIP_TRY(c, hipEventCreateWithFlags(&b, fl));
+    hipEvent_t a = nullptr, b = nullptr;
+    hipError_t e = hipEventCreateWithFlags(&a, fl);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&b, fl);
+    if (e != hipSuccess) {
+      if (a) (void)hipEventDestroy(a);
+      return fail(c, SLH_EHIP, "hipEventCreateWithFlags: %s", hipGetErrorString(e));
+    }
     c->ev_fb.push_back(a);
     c->ev_fa.push_back(b);
   }
@@ -531,8 +536,8 @@ void slh_destroy(slh_ctx* c) {
     if (e) (void)hipEventDestroy(e);
   if (c->mq_pin) (void)hipHostFree(c->mq_pin);
 
-  if (c->ev_made)
-    for (auto& e : c->ev) (void)hipEventDestroy(e);
+  for (auto& e : c->ev)
+    if (e) (void)hipEventDestroy(e);
   for (auto& e : c->ev_fb) (void)hipEventDestroy(e);
   for (auto& e : c->ev_fa) (void)hipEventDestroy(e);
   delete c;
