@@ -5,6 +5,7 @@ Every function keeps the C name and takes torch tensors for device buffers
 library's HIP kernels.  There is no fallback: if the library is not built or
 cannot be loaded, every call raises.
 """
+import collections
 import ctypes
 import os
 
@@ -118,6 +119,7 @@ class Ctx:
         self.N, self.D, self.m, self.r, self.bits = N, D, m, r, bits
         self.n_it = 0
         self.keep_last = 0          # preserved suffix (tokens N - keep_last .. N - 1)
+        self.in_flight = collections.deque()   # tensors of merges not yet waited for
 
     def __del__(self):
         if getattr(self, "handle", None) and _lib is not None:
@@ -235,6 +237,26 @@ def slh_merge_capacity(ctx):
     return int(load().slh_merge_capacity(ctx.handle))
 
 
+def _check_merge_outputs(ctx, X, emb_out, pos_out, tok2macro_out):
+    """The library writes the outputs through raw device pointers: they must be
+    contiguous tensors of the right type and shape on X's device."""
+    import torch
+    specs = (("emb_out", emb_out, torch.float32, (None, ctx.D)),
+             ("pos_out", pos_out, torch.int32, (None,)),
+             ("tok2macro_out", tok2macro_out, torch.int32, (ctx.N,)))
+    for name, t, dt, shape in specs:
+        if t is None:
+            continue
+        if not isinstance(t, torch.Tensor) or not t.is_cuda or t.device != X.device:
+            raise SLHError(f"{name} must be a device tensor on {X.device}")
+        if (t.dtype != dt or not t.is_contiguous() or t.dim() != len(shape)
+                or any(w is not None and w != d for w, d in zip(shape, t.shape))):
+            want = ", ".join("cap" if w is None else str(w) for w in shape)
+            raise SLHError(f"{name} must be a contiguous {dt} tensor of shape ({want},)")
+    if pos_out.shape[0] < emb_out.shape[0]:
+        raise SLHError("pos_out must hold at least as many entries as emb_out")
+
+
 def slh_merge(ctx, X, emb_out=None, pos_out=None, tok2macro_out=None):
     """Returns (E [M, D] float32, P [M] int32, tok2macro [N] int32, M) as device tensors
     (views of the given or newly allocated outputs)."""
@@ -247,6 +269,7 @@ def slh_merge(ctx, X, emb_out=None, pos_out=None, tok2macro_out=None):
         pos_out = torch.empty(cap, dtype=torch.int32, device=X.device)
     if tok2macro_out is None:
         tok2macro_out = torch.empty(ctx.N, dtype=torch.int32, device=X.device)
+    _check_merge_outputs(ctx, X, emb_out, pos_out, tok2macro_out)
     M = ctypes.c_int64(0)
     _check(ctx, load().slh_merge(ctx.handle, p, dt, ld, ctypes.c_void_p(emb_out.data_ptr()),
                                  ctypes.c_void_p(pos_out.data_ptr()),
@@ -258,19 +281,26 @@ def slh_merge(ctx, X, emb_out=None, pos_out=None, tok2macro_out=None):
 
 def slh_merge_async(ctx, X, emb_out, pos_out, tok2macro_out=None):
     """Enqueues the merge into the given device outputs and returns at once; the
-    outputs hold the result once slh_merge_wait has returned its M."""
+    outputs hold the result once slh_merge_wait has returned its M.  X and the
+    outputs are kept referenced until that wait, since the GPU still reads and
+    writes them."""
     p, dt, ld = _xinfo(X)
+    _check_merge_outputs(ctx, X, emb_out, pos_out, tok2macro_out)
     _check(ctx, load().slh_merge_async(ctx.handle, p, dt, ld, ctypes.c_void_p(emb_out.data_ptr()),
                                        ctypes.c_void_p(pos_out.data_ptr()),
                                        ctypes.c_void_p(tok2macro_out.data_ptr())
                                        if tok2macro_out is not None else None,
                                        emb_out.shape[0]), "slh_merge_async")
+    ctx.in_flight.append((X, emb_out, pos_out, tok2macro_out))
 
 
 def slh_merge_wait(ctx):
     """M of the oldest merge from slh_merge_async not yet waited for."""
     M = ctypes.c_int64(0)
-    _check(ctx, load().slh_merge_wait(ctx.handle, ctypes.byref(M)), "slh_merge_wait")
+    rc = load().slh_merge_wait(ctx.handle, ctypes.byref(M))
+    if rc != SLH_ESTATE and ctx.in_flight:
+        ctx.in_flight.popleft()          # that merge has left the GPU
+    _check(ctx, rc, "slh_merge_wait")
     return int(M.value)
 
 

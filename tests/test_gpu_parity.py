@@ -584,8 +584,9 @@ def test_merge_async_pipelined(m):
     """slh_merge_async / slh_merge_wait: two prompts through one context with the
     second prompt's steps enqueued before the first one's M is read give, bit for
     bit, the outputs and M of slh_merge on each in a context of its own.  A third
-    merge (or a slh_merge) is refused while two are outstanding, and a wait needs
-    an outstanding merge.  m = 1024: the resident Lanczos kernel, whose error word
+    merge (or a slh_merge) is refused while two are outstanding, a wait needs
+    an outstanding merge, and outputs of the wrong place, type or shape are
+    refused by the binding.  m = 1024: the resident Lanczos kernel, whose error word
     each wait checks; m = 256: the streaming path."""
     import torch
     import paper_2607_19368_amd as P
@@ -615,15 +616,24 @@ def test_merge_async_pipelined(m):
              torch.empty(cap, dtype=torch.int32, device="cuda"),
              torch.empty(wl.N, dtype=torch.int32, device="cuda")) for _ in range(2)]
     _say(f"[merge async] m={m} cap={cap}")
-    for X, o in zip(xs, outs):
+    for i, (X, o) in enumerate(zip(xs, outs)):
         steps(ctx, X)
+        if i == 0:
+            # outputs the library could not write through are refused before any call:
+            # a host tensor, a wrong dtype, a wrong width, pos_out shorter than emb_out
+            for bad in ((o[0].cpu(), o[1], o[2]), (o[0], o[1].to(torch.int64), o[2]),
+                        (o[0][:, :-1], o[1], o[2]), (o[0], o[1][:-1], o[2])):
+                with pytest.raises(B.SLHError):
+                    P.slh_merge_async(ctx, X, *bad)
         P.slh_merge_async(ctx, X, *o)
+    assert len(ctx.in_flight) == 2            # X and the outputs stay referenced
     steps(ctx, xs[0])
     with pytest.raises(B.SLHError):
         P.slh_merge_async(ctx, xs[0], *outs[0])
     with pytest.raises(B.SLHError):
         P.slh_merge(ctx, xs[0])
     Ms = [P.slh_merge_wait(ctx), P.slh_merge_wait(ctx)]
+    assert len(ctx.in_flight) == 0
     with pytest.raises(B.SLHError):
         P.slh_merge_wait(ctx)
     torch.cuda.synchronize()
