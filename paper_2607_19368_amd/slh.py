@@ -228,6 +228,9 @@ def slh_eigh_ritz(ctx, n_it, want=True):
 
 
 def slh_simhash(ctx, codes_out=None):
+    if codes_out is not None:
+        import torch
+        _device_tensor("codes_out", codes_out, (torch.int32, torch.uint32), (ctx.N,))
     p = ctypes.c_void_p(codes_out.data_ptr()) if codes_out is not None else None
     _check(ctx, load().slh_simhash(ctx.handle, p), "slh_simhash")
     return codes_out
@@ -237,22 +240,29 @@ def slh_merge_capacity(ctx):
     return int(load().slh_merge_capacity(ctx.handle))
 
 
-def _check_merge_outputs(ctx, X, emb_out, pos_out, tok2macro_out):
-    """The library writes the outputs through raw device pointers: they must be
-    contiguous tensors of the right type and shape on X's device."""
+def _device_tensor(name, t, dtypes=None, shape=None, device=None):
+    """The library reads or writes t through a raw device pointer: it must be a
+    contiguous device tensor (of one of `dtypes`, of `shape` where an entry
+    None is free, on `device`)."""
     import torch
-    specs = (("emb_out", emb_out, torch.float32, (None, ctx.D)),
-             ("pos_out", pos_out, torch.int32, (None,)),
-             ("tok2macro_out", tok2macro_out, torch.int32, (ctx.N,)))
-    for name, t, dt, shape in specs:
-        if t is None:
-            continue
-        if not isinstance(t, torch.Tensor) or not t.is_cuda or t.device != X.device:
-            raise SLHError(f"{name} must be a device tensor on {X.device}")
-        if (t.dtype != dt or not t.is_contiguous() or t.dim() != len(shape)
-                or any(w is not None and w != d for w, d in zip(shape, t.shape))):
-            want = ", ".join("cap" if w is None else str(w) for w in shape)
-            raise SLHError(f"{name} must be a contiguous {dt} tensor of shape ({want},)")
+    if not isinstance(t, torch.Tensor) or not t.is_cuda or (device is not None and t.device != device):
+        raise SLHError(f"{name} must be a device tensor" + (f" on {device}" if device is not None else ""))
+    if (dtypes is not None and t.dtype not in dtypes) or not t.is_contiguous():
+        kinds = " or ".join(str(d) for d in dtypes) if dtypes is not None else "any type"
+        raise SLHError(f"{name} must be a contiguous tensor of {kinds}")
+    if shape is not None and (t.dim() != len(shape)
+                              or any(w is not None and w != d for w, d in zip(shape, t.shape))):
+        want = ", ".join("*" if w is None else str(w) for w in shape)
+        raise SLHError(f"{name} must have shape ({want})")
+
+
+def _check_merge_outputs(D, N, device, emb_out, pos_out, tok2macro_out):
+    """Merge outputs: E [cap, D] float32, P [>= cap] int32, tok2macro [N] int32."""
+    import torch
+    _device_tensor("emb_out", emb_out, (torch.float32,), (None, D), device)
+    _device_tensor("pos_out", pos_out, (torch.int32,), (None,), device)
+    if tok2macro_out is not None:
+        _device_tensor("tok2macro_out", tok2macro_out, (torch.int32,), (N,), device)
     if pos_out.shape[0] < emb_out.shape[0]:
         raise SLHError("pos_out must hold at least as many entries as emb_out")
 
@@ -269,7 +279,7 @@ def slh_merge(ctx, X, emb_out=None, pos_out=None, tok2macro_out=None):
         pos_out = torch.empty(cap, dtype=torch.int32, device=X.device)
     if tok2macro_out is None:
         tok2macro_out = torch.empty(ctx.N, dtype=torch.int32, device=X.device)
-    _check_merge_outputs(ctx, X, emb_out, pos_out, tok2macro_out)
+    _check_merge_outputs(ctx.D, ctx.N, X.device, emb_out, pos_out, tok2macro_out)
     M = ctypes.c_int64(0)
     _check(ctx, load().slh_merge(ctx.handle, p, dt, ld, ctypes.c_void_p(emb_out.data_ptr()),
                                  ctypes.c_void_p(pos_out.data_ptr()),
@@ -285,7 +295,7 @@ def slh_merge_async(ctx, X, emb_out, pos_out, tok2macro_out=None):
     outputs are kept referenced until that wait, since the GPU still reads and
     writes them."""
     p, dt, ld = _xinfo(X)
-    _check_merge_outputs(ctx, X, emb_out, pos_out, tok2macro_out)
+    _check_merge_outputs(ctx.D, ctx.N, X.device, emb_out, pos_out, tok2macro_out)
     _check(ctx, load().slh_merge_async(ctx.handle, p, dt, ld, ctypes.c_void_p(emb_out.data_ptr()),
                                        ctypes.c_void_p(pos_out.data_ptr()),
                                        ctypes.c_void_p(tok2macro_out.data_ptr())
@@ -339,6 +349,11 @@ def slh_time_passes(ctx, reps=96):
 def slh_load(ctx, which, src):
     """Replace a stage result (SLH_OUT_PHI, SLH_OUT_ALPHA, SLH_OUT_BETA, SLH_OUT_Q or
     SLH_OUT_CODES) with a device tensor."""
+    import torch
+    kinds = {SLH_OUT_PHI: (torch.float32,), SLH_OUT_ALPHA: (torch.float64,),
+             SLH_OUT_BETA: (torch.float64,), SLH_OUT_Q: (torch.float64,),
+             SLH_OUT_CODES: (torch.int32, torch.uint32)}
+    _device_tensor("src", src, kinds.get(which))
     nbytes = src.numel() * src.element_size()
     _check(ctx, load().slh_load(ctx.handle, which, ctypes.c_void_p(src.data_ptr()), nbytes), "slh_load")
     if which == SLH_OUT_ALPHA:
@@ -393,6 +408,7 @@ def slh_bucket_purity(ctx, X, thresh=0.7):
 def slh_peak_read(buf, reps=20, stream=None):
     """GB/s of a plain streaming read of the device tensor `buf` (measurement aid)."""
     import torch
+    _device_tensor("buf", buf)
     st = torch.cuda.current_stream() if stream is None else stream
     out = np.zeros(1, np.float64)
     rc = load().slh_peak_read(ctypes.c_void_p(buf.data_ptr()), buf.numel() * buf.element_size(),
@@ -421,6 +437,8 @@ def slh_merge_noalloc(X, codes, bits, emb_out, pos_out, tok2macro_out=None, stre
     tok2macro, M) as views of the given outputs."""
     import torch
     p, dt, ld = _xinfo(X)
+    _device_tensor("codes", codes, (torch.int32, torch.uint32), (X.shape[0],), X.device)
+    _check_merge_outputs(X.shape[1], X.shape[0], X.device, emb_out, pos_out, tok2macro_out)
     st = torch.cuda.current_stream() if stream is None else stream
     M = ctypes.c_int64(0)
     rc = load().slh_merge_noalloc(p, dt, ld, X.shape[0], X.shape[1], ctypes.c_void_p(codes.data_ptr()),
